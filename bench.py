@@ -1,0 +1,177 @@
+#!/usr/bin/env python3
+"""Throughput of batched pipeline-schedule simulation on one GPU.
+
+One step = one pass of the hot path over one batch: simulate every candidate
+of the batch (makespan, per-rank bubble, per-rank peak activation memory,
+flags) and reduce the batch to its best (makespan, index).  Inputs are seeded
+synthetic candidates already resident in device memory when timing starts.
+
+Default workload: the 8-rank vision-language instance (ViT on ranks 0-1, LLM
+on ranks 2-7, 32 samples), 65,536 candidates per batch.
+
+Prints one JSON line.  Besides the throughput it carries
+  roofline      the simulation kernel's algorithmic HBM bytes per launch
+                (2 bytes per order entry read + the outputs written) over its
+                average launch time from HIP events on the launch stream,
+                against the 8 TB/s HBM peak;
+  cpu_baseline  the CPU oracle timed on this host on a bounded sample of the
+                same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--config", type=int, default=2, help="workload id 1-5")
+    ap.add_argument("--n-cand", type=int, default=0, help="override candidates per batch")
+    ap.add_argument("--variant", type=int, default=0)
+    ap.add_argument("--wpb", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=1.5,
+                    help="wall-time bound of the CPU oracle baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU; "
+                          f"--gpus {args.gpus} (WORLD_SIZE {world}) is not supported. "
+                          "Candidates are independent, so several GPUs would each take a "
+                          "contiguous candidate range and min-reduce one 64-bit key."}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2504_14145_amd as dip
+    import workloads as W
+
+    cfg = W.get(args.config)
+    n_cand = args.n_cand or (cfg.chunk or cfg.n_cand)
+    t0 = time.time()
+    prob = W.make_problem(cfg)
+    gen = W.generator_for(prob, cfg)
+    rows = gen.generate(0, n_cand)
+    log(f"[bench] workload {cfg.name}: {n_cand} candidates x {prob.n_total} ops, "
+        f"stride {prob.stride}, generated in {time.time() - t0:.1f}s")
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    orders = torch.from_numpy(rows).to(dev)
+    sim = dip.Sim(prob)
+    if args.variant or args.wpb:
+        rc = sim.configure(args.variant, args.wpb)
+        if rc != dip.OK:
+            raise SystemExit(f"variant {args.variant}/{args.wpb} unsupported: {dip.strerror(rc)}")
+    info = sim.info
+    log(f"[bench] kernel config {info}")
+    out = sim.outputs(n_cand)
+    key = torch.empty(1, dtype=torch.int64, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step(ev_pair=None):
+        key.fill_(-1)
+        if ev_pair is not None:
+            ev_pair[0].record(stream)
+        dip.evaluate(sim.h, None, orders, n_cand, *out, stream=stream)
+        if ev_pair is not None:
+            ev_pair[1].record(stream)
+        dip.argmin(sim.h, out[0], out[3], n_cand, 0, key, stream=stream)
+
+    # first call uploads the costs
+    dip.evaluate(sim.h, sim.costs, orders, n_cand, *out, stream=stream)
+    torch.cuda.synchronize()
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        step(events[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    kern_ms = [a.elapsed_time(b) for a, b in events]
+    kern_avg_s = sum(kern_ms) / len(kern_ms) / 1e3
+    best = dip.decode_key(int(key.item()))
+    flags = out[3].cpu().numpy()
+    log(f"[bench] {args.steps} steps in {wall * 1e3:.2f} ms; sim kernel avg "
+        f"{kern_avg_s * 1e6:.1f} us (min {min(kern_ms) * 1e3:.1f} us); best {best}; "
+        f"deadlock {np.mean(flags & 1 > 0):.3f} cap {np.mean(flags & 2 > 0):.3f}")
+
+    ms_per_step = wall / args.steps * 1e3
+    cand_per_s = n_cand * args.steps / wall
+    ops_per_s = cand_per_s * prob.n_total
+    P = prob.n_ranks
+    bytes_per_cand = 2 * prob.n_total + 4 + 4 * P + 4 * P + 1
+    achieved_gbs = n_cand * bytes_per_cand / kern_avg_s / 1e9
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle
+        cores = max(1, min(16, len(os.sched_getaffinity(0))))
+        sample = min(n_cand, 8192)
+        done = 0
+        tc = time.perf_counter()
+        while True:
+            oracle.evaluate(prob, rows[:sample], threads=cores)
+            done += sample
+            if time.perf_counter() - tc >= args.cpu_seconds:
+                break
+        dt = time.perf_counter() - tc
+        cpu = {"value": done / dt, "unit": "candidates/s", "cores": cores, "kind": "oracle",
+               "ops_per_s": done * prob.n_total / dt,
+               "sample": f"first {sample} candidates of the batch, repeated "
+                         f"{done // sample}x ({dt:.2f} s wall on {cores} threads)"}
+        log(f"[bench] cpu oracle {done / dt:.0f} candidates/s on {cores} threads")
+
+    rec = {
+        "metric": "candidate schedules simulated/sec",
+        "value": cand_per_s,
+        "unit": "candidates/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "n_cand": n_cand, "ranks": P, "lanes": cfg.L,
+                   "ops_per_candidate": prob.n_total, "microbatches": cfg.samples,
+                   "parallelism": "single GPU"},
+        "ops_per_s": ops_per_s,
+        "sim_kernel_us": kern_avg_s * 1e6,
+        "kernel_variant": info["variant"],
+        "best": {"index": best[0], "makespan_us": best[1]},
+        "roofline": {"bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": None},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+    sim.close()
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,181 @@
+/*
+ * dip_sim.h -- batched simulation of candidate pipeline schedules on one GPU.
+ *
+ * The problem (DIP, arXiv 2504.14145): a training iteration's pipeline is a
+ * DAG of pipeline stages -- the forward or backward pass of one
+ * sub-microbatch on one model chunk (Sec. 5.2) -- placed on physical
+ * pipeline ranks, each of which runs one stage at a time (the per-rank t_last
+ * of Sec. 5.2).  A stage may start once its rank is free and the outputs of
+ * its predecessor stages have arrived; a transfer between different ranks is
+ * asynchronous and adds a latency to the edge (Sec. 6.3).  A candidate
+ * schedule is one action order per rank (Sec. 6.3's per-worker action list).
+ * Each candidate is scored by its iteration time, under a per-rank activation
+ * memory limit whose liveness is that of a stage pair, forward start to
+ * backward end (Sec. 5.3's memory constraint), and the searcher keeps the
+ * best candidate (Sec. 5.1's best rollout score).
+ *
+ * This library evaluates millions of candidates of ONE instance per call:
+ *   dip_sim_create   -- validate and upload the instance's topology;
+ *   dip_sim_evaluate -- simulate a batch: makespan, per-rank idle time
+ *                       ("bubble"), per-rank peak activation memory, flags;
+ *   dip_sim_argmin   -- fold the best (makespan, index) of a batch into a
+ *                       running 64-bit key, so chunked batches reduce exactly;
+ *   dip_sim_destroy.
+ *
+ * Semantics per candidate (all integers; results are exact):
+ *   start(o)  = max(free(rank(o)), max over predecessors p of end(p)+comm(p,o))
+ *   end(o)    = start(o) + cost(o), ops taken in each rank's order
+ *   makespan  = max end(o);  bubble[r] = makespan - sum of rank r's costs
+ *   peak[r]   = max over prefixes of rank r's order of the running sum of
+ *               +act(slot) at each forward and -act(slot) at each backward,
+ *               starting from 0 (so it is a function of the order alone)
+ *   flags     = DIP_FLAG_DEADLOCK if the orders and the data edges form a
+ *               cycle (the simulation stalls with ops left); makespan and
+ *               bubble are then -1 while peak keeps the order-scan value;
+ *             | DIP_FLAG_CAP if some rank has mem_cap[r] >= 0 and
+ *               peak[r] > mem_cap[r];
+ *             | DIP_FLAG_INVALID alone, if some rank's section is not a
+ *               permutation of its op ids; every output is then -1.
+ *
+ * Threading and streams: a handle is not thread-safe; distinct handles are
+ * independent.  evaluate and argmin enqueue work on the given HIP stream
+ * (a hipStream_t passed as void*, NULL = the default stream) and return
+ * without waiting; outputs are valid once that stream has reached the work.
+ * Every call returns DIP_OK (0) or a negative DIP_E_* code; nothing throws
+ * across this boundary.
+ */
+#ifndef DIP_SIM_H
+#define DIP_SIM_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define DIP_SIM_ABI_VERSION 1
+
+enum {
+  DIP_OK = 0,
+  DIP_E_INVAL = -1,       /* null pointer, negative count, misaligned buffer   */
+  DIP_E_TOPO = -2,        /* malformed topology (ids, CSR, slots, kinds)       */
+  DIP_E_RANGE = -3,       /* negative cost, or totals that could overflow int32 */
+  DIP_E_UNSUPPORTED = -4, /* shape no kernel variant handles (> 64 ranks, ...) */
+  DIP_E_NOMEM = -5,       /* host or device allocation failed                   */
+  DIP_E_HIP = -6,         /* HIP runtime error; see dip_sim_strerror            */
+  DIP_E_STATE = -7        /* evaluate before any costs were supplied            */
+};
+
+#define DIP_FLAG_DEADLOCK 1u
+#define DIP_FLAG_CAP 2u
+#define DIP_FLAG_INVALID 4u
+
+/* Opaque handle; owns only its device-side copies of the instance tables and
+ * any scratch memory, released by dip_sim_destroy. */
+typedef struct dip_sim dip_sim;
+
+/* Instance topology.  Host pointers, read during dip_sim_create only.
+ *
+ * Ops are numbered per rank ("rank-local id" 0 .. n_ops[r]-1) and globally
+ * (g = off[r] + id, off[r] = n_ops[0] + ... + n_ops[r-1]).  The workload
+ * generators of this repository enumerate a rank's ops by model chunk
+ * ascending, then sub-microbatch ascending, forward before backward, so
+ * id = 2 * slot_local + kind; the library itself relies on no such rule. */
+typedef struct {
+  int32_t n_ranks;           /* P, 1 .. 64                                      */
+  const int32_t *n_ops;      /* [P] ops per rank, each 0 .. 32768 (int16 ids)   */
+  const int32_t *pred_ptr;   /* [N+1] CSR row pointers over global op index,
+                                pred_ptr[0] = 0, non-decreasing                 */
+  const int32_t *pred_op;    /* [E] global index of each predecessor, != own g  */
+  const uint8_t *op_kind;    /* [N] 0 = forward (+act at start),
+                                    1 = backward (-act at end)                  */
+  const int32_t *op_slot;    /* [N] activation slot 0 .. n_slots-1; a forward
+                                and its backward share one slot                 */
+  int32_t n_slots;
+  const int32_t *mem_cap;    /* [P] per-rank cap in memory units, < 0 = none    */
+  int64_t cand_stride;       /* int16 elements per candidate row: >= N and a
+                                multiple of 8 (16-byte rows)                    */
+} dip_topology;
+
+/* Per-batch costs.  Host pointers, read during the call that receives them. */
+typedef struct {
+  const int32_t *op_cost;    /* [N] microseconds, >= 0                          */
+  const int32_t *edge_comm;  /* [E] microseconds, >= 0, aligned with pred_op;
+                                charge only edges between different ranks       */
+  const int32_t *slot_act;   /* [n_slots] memory units, >= 0                    */
+} dip_costs;
+
+/* Reported shape of a handle (what dip_sim_create chose). */
+typedef struct {
+  int32_t n_ranks;
+  int32_t n_ops_total;       /* N */
+  int32_t n_edges;           /* E */
+  int32_t variant;           /* kernel variant in use, see dip_sim_configure     */
+  int64_t cand_stride;
+  int32_t lanes_per_group;   /* power of two >= n_ranks: lanes per candidate     */
+  int32_t groups_per_wave;   /* candidates simulated side by side by one wave    */
+  int32_t waves_per_block;
+  int32_t lds_bytes;         /* dynamic LDS per block                            */
+  int32_t max_blocks;        /* resident blocks the grid is capped at            */
+  int64_t scratch_bytes;     /* device scratch owned by the handle               */
+} dip_sim_info;
+
+/* Host-only checks, no device access: the same checks create / evaluate run
+ * first.  Useful where no GPU is present. */
+int dip_sim_check_topology(const dip_topology *topo);
+int dip_sim_check_costs(const dip_topology *topo, const dip_costs *costs);
+
+/* Validate the topology, copy it to the current HIP device and choose a
+ * kernel variant for this device.  On success *out owns device memory. */
+int dip_sim_create(const dip_topology *topo, dip_sim **out);
+
+/* Force a kernel variant (0 = automatic choice) and waves per block
+ * (0 = automatic).  DIP_E_UNSUPPORTED if the variant does not fit the device.
+ * Variants: 1 tables, orders and end times in LDS; 2 tables in global memory,
+ * orders and end times in LDS; 3 end times in LDS only; 4 nothing in LDS
+ * (end times in device scratch). */
+int dip_sim_configure(dip_sim *h, int32_t variant, int32_t waves_per_block);
+
+int dip_sim_get_info(const dip_sim *h, dip_sim_info *info);
+
+/* Simulate candidates orders[0 .. n_cand-1].
+ *   costs      host pointers, or NULL to reuse the costs of the previous call
+ *              (DIP_E_STATE if there is none).  Costs are validated (sum of
+ *              all op costs and edge latencies <= INT32_MAX; per rank, the
+ *              activations of its slots sum to <= INT32_MAX) and copied
+ *              stream-ordered before the launch.
+ *   orders     device, int16 [n_cand][cand_stride], 16-byte aligned; row c
+ *              holds rank 0's order, then rank 1's, ... with no gaps; entries
+ *              past N are ignored.
+ *   out_*      device: makespan int32 [n_cand], bubble int32 [n_cand][P],
+ *              peakmem int32 [n_cand][P], flags uint8 [n_cand].
+ *   stream     hipStream_t as void*.
+ * n_cand == 0 is a no-op. */
+int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders,
+                     int64_t n_cand, int32_t *out_makespan, int32_t *out_bubble,
+                     int32_t *out_peakmem, uint8_t *out_flags, void *stream);
+
+/* Fold the lexicographic minimum of (makespan[i], index_base + i) over the
+ * candidates with flags[i] == 0 into *inout_best_key (device, uint64):
+ * key = (uint64)makespan << 32 | index, and the caller initialises it to
+ * UINT64_MAX, which also means "no valid candidate".  Ties go to the lowest
+ * index.  Requires index_base >= 0 and index_base + n_cand <= 2^32 - 1.
+ * makespan and flags are device pointers (typically evaluate's outputs). */
+int dip_sim_argmin(dip_sim *h, const int32_t *makespan, const uint8_t *flags,
+                   int64_t n_cand, int64_t index_base, uint64_t *inout_best_key,
+                   void *stream);
+
+/* Release the handle's device memory.  Waits for the device first. */
+void dip_sim_destroy(dip_sim *h);
+
+/* Static description of a return code; for DIP_E_HIP, the last HIP error
+ * seen by this thread. */
+const char *dip_sim_strerror(int code);
+
+int dip_sim_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DIP_SIM_H */

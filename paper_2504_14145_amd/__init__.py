@@ -1,0 +1,257 @@
+"""Python binding of the dip_sim C ABI (include/dip_sim.h).
+
+Argument marshalling only: every step of the simulation and of the argmin
+runs in the HIP kernels of ``libdip_sim.so``.  The functions keep the ABI's
+names (create, evaluate, argmin, destroy, ...) and take host numpy arrays for
+the instance and torch device tensors for candidates and outputs; PyTorch
+provides device memory and the stream, nothing else.  Importing works without
+a GPU; loading the library fails loudly if it has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from . import _build
+
+LIB_PATH = _build.LIB
+
+OK = 0
+E_INVAL, E_TOPO, E_RANGE, E_UNSUPPORTED, E_NOMEM, E_HIP, E_STATE = -1, -2, -3, -4, -5, -6, -7
+FLAG_DEADLOCK, FLAG_CAP, FLAG_INVALID = 1, 2, 4
+NO_KEY = (1 << 64) - 1
+
+EXPORTS = ("dip_sim_abi_version", "dip_sim_check_topology", "dip_sim_check_costs",
+           "dip_sim_create", "dip_sim_configure", "dip_sim_get_info", "dip_sim_evaluate",
+           "dip_sim_argmin", "dip_sim_destroy", "dip_sim_strerror")
+
+
+class DipSimError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {strerror(code)} ({code})")
+
+
+class Topology(ctypes.Structure):
+    _fields_ = [("n_ranks", ctypes.c_int32), ("n_ops", ctypes.c_void_p),
+                ("pred_ptr", ctypes.c_void_p), ("pred_op", ctypes.c_void_p),
+                ("op_kind", ctypes.c_void_p), ("op_slot", ctypes.c_void_p),
+                ("n_slots", ctypes.c_int32), ("mem_cap", ctypes.c_void_p),
+                ("cand_stride", ctypes.c_int64)]
+
+
+class Costs(ctypes.Structure):
+    _fields_ = [("op_cost", ctypes.c_void_p), ("edge_comm", ctypes.c_void_p),
+                ("slot_act", ctypes.c_void_p)]
+
+
+class Info(ctypes.Structure):
+    _fields_ = [("n_ranks", ctypes.c_int32), ("n_ops_total", ctypes.c_int32),
+                ("n_edges", ctypes.c_int32), ("variant", ctypes.c_int32),
+                ("cand_stride", ctypes.c_int64), ("lanes_per_group", ctypes.c_int32),
+                ("groups_per_wave", ctypes.c_int32), ("waves_per_block", ctypes.c_int32),
+                ("lds_bytes", ctypes.c_int32), ("max_blocks", ctypes.c_int32),
+                ("scratch_bytes", ctypes.c_int64)]
+
+    def as_dict(self):
+        return {k: getattr(self, k) for k, _ in self._fields_}
+
+
+_lib = None
+
+
+def load():
+    """The built library; raises if it is missing (no silent fallback)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build()")
+        lib = ctypes.CDLL(LIB_PATH)
+        vp, i32, i64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+        lib.dip_sim_abi_version.restype = ctypes.c_int
+        lib.dip_sim_check_topology.argtypes = [ctypes.POINTER(Topology)]
+        lib.dip_sim_check_costs.argtypes = [ctypes.POINTER(Topology), ctypes.POINTER(Costs)]
+        lib.dip_sim_create.argtypes = [ctypes.POINTER(Topology), ctypes.POINTER(vp)]
+        lib.dip_sim_configure.argtypes = [vp, i32, i32]
+        lib.dip_sim_get_info.argtypes = [vp, ctypes.POINTER(Info)]
+        lib.dip_sim_evaluate.argtypes = [vp, ctypes.POINTER(Costs), vp, i64, vp, vp, vp, vp, vp]
+        lib.dip_sim_argmin.argtypes = [vp, vp, vp, i64, i64, vp, vp]
+        lib.dip_sim_destroy.argtypes = [vp]
+        lib.dip_sim_destroy.restype = None
+        lib.dip_sim_strerror.argtypes = [ctypes.c_int]
+        lib.dip_sim_strerror.restype = ctypes.c_char_p
+        for name in ("dip_sim_check_topology", "dip_sim_check_costs", "dip_sim_create",
+                     "dip_sim_configure", "dip_sim_get_info", "dip_sim_evaluate",
+                     "dip_sim_argmin"):
+            getattr(lib, name).restype = ctypes.c_int
+        _lib = lib
+    return _lib
+
+
+def strerror(code: int) -> str:
+    return load().dip_sim_strerror(int(code)).decode()
+
+
+def _check(code: int, where: str):
+    if code != OK:
+        raise DipSimError(code, where)
+
+
+# ------------------------------------------------------------ host marshalling
+
+class HostTopology:
+    """Contiguous host copies of an instance's topology plus the ctypes view."""
+
+    def __init__(self, n_ranks, n_ops, pred_ptr, pred_op, op_kind, op_slot, n_slots,
+                 mem_cap, cand_stride):
+        self.keep = dict(
+            n_ops=np.ascontiguousarray(n_ops, np.int32),
+            pred_ptr=np.ascontiguousarray(pred_ptr, np.int32),
+            pred_op=np.ascontiguousarray(pred_op, np.int32) if len(pred_op) else np.zeros(1, np.int32),
+            op_kind=np.ascontiguousarray(op_kind, np.uint8),
+            op_slot=np.ascontiguousarray(op_slot, np.int32),
+            mem_cap=np.ascontiguousarray(mem_cap, np.int32))
+        k = self.keep
+        self.c = Topology(int(n_ranks), k["n_ops"].ctypes.data, k["pred_ptr"].ctypes.data,
+                          k["pred_op"].ctypes.data, k["op_kind"].ctypes.data,
+                          k["op_slot"].ctypes.data, int(n_slots), k["mem_cap"].ctypes.data,
+                          int(cand_stride))
+
+    @classmethod
+    def of(cls, prob):
+        return cls(prob.n_ranks, prob.n_ops, prob.pred_ptr, prob.pred_op, prob.op_kind,
+                   prob.op_slot, prob.n_slots, prob.mem_cap, prob.stride)
+
+
+class HostCosts:
+    def __init__(self, op_cost, edge_comm, slot_act):
+        self.keep = [np.ascontiguousarray(op_cost, np.int32),
+                     np.ascontiguousarray(edge_comm, np.int32) if len(edge_comm) else np.zeros(1, np.int32),
+                     np.ascontiguousarray(slot_act, np.int32) if len(slot_act) else np.zeros(1, np.int32)]
+        self.c = Costs(*(a.ctypes.data for a in self.keep))
+
+    @classmethod
+    def of(cls, prob):
+        return cls(prob.op_cost, prob.edge_comm, prob.slot_act)
+
+
+# ------------------------------------------------------------ ABI, same names
+
+def check_topology(topo: HostTopology) -> int:
+    return load().dip_sim_check_topology(ctypes.byref(topo.c))
+
+
+def check_costs(topo: HostTopology, costs: HostCosts) -> int:
+    return load().dip_sim_check_costs(ctypes.byref(topo.c), ctypes.byref(costs.c))
+
+
+def create(topo: HostTopology) -> ctypes.c_void_p:
+    h = ctypes.c_void_p()
+    _check(load().dip_sim_create(ctypes.byref(topo.c), ctypes.byref(h)), "dip_sim_create")
+    return h
+
+
+def configure(h, variant: int = 0, waves_per_block: int = 0) -> int:
+    return load().dip_sim_configure(h, int(variant), int(waves_per_block))
+
+
+def get_info(h) -> dict:
+    info = Info()
+    _check(load().dip_sim_get_info(h, ctypes.byref(info)), "dip_sim_get_info")
+    return info.as_dict()
+
+
+def _stream_ptr(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    return getattr(stream, "cuda_stream", stream)
+
+
+def evaluate(h, costs, orders, n_cand, out_makespan, out_bubble, out_peakmem, out_flags,
+             stream=None) -> None:
+    """Device tensors in, device tensors out; enqueued on ``stream`` (torch's
+    current stream by default)."""
+    rc = load().dip_sim_evaluate(
+        h, ctypes.byref(costs.c) if costs is not None else None, orders.data_ptr(),
+        int(n_cand), out_makespan.data_ptr(), out_bubble.data_ptr(),
+        out_peakmem.data_ptr(), out_flags.data_ptr(), _stream_ptr(stream))
+    _check(rc, "dip_sim_evaluate")
+
+
+def argmin(h, makespan, flags, n_cand, index_base, inout_best_key, stream=None) -> None:
+    rc = load().dip_sim_argmin(h, makespan.data_ptr(), flags.data_ptr(), int(n_cand),
+                               int(index_base), inout_best_key.data_ptr(),
+                               _stream_ptr(stream))
+    _check(rc, "dip_sim_argmin")
+
+
+def destroy(h) -> None:
+    if h:
+        load().dip_sim_destroy(h)
+
+
+def decode_key(key: int):
+    """(best global index, best makespan), or (-1, -1) when nothing was valid."""
+    key = int(key) & NO_KEY
+    if key == NO_KEY:
+        return -1, -1
+    return key & 0xFFFFFFFF, key >> 32
+
+
+# ------------------------------------------------------------ convenience
+
+class Sim:
+    """Owns one handle; tensors are torch CUDA tensors."""
+
+    def __init__(self, prob, costs=True):
+        self.topo = HostTopology.of(prob)
+        self.P = int(prob.n_ranks)
+        self.stride = int(prob.stride)
+        self.h = create(self.topo)
+        self.costs = HostCosts.of(prob) if costs is True else costs
+        self._costs_sent = False
+
+    def close(self):
+        if self.h:
+            destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def configure(self, variant=0, waves_per_block=0) -> int:
+        return configure(self.h, variant, waves_per_block)
+
+    @property
+    def info(self) -> dict:
+        return get_info(self.h)
+
+    def outputs(self, n, device="cuda"):
+        import torch
+        return (torch.empty(n, dtype=torch.int32, device=device),
+                torch.empty((n, self.P), dtype=torch.int32, device=device),
+                torch.empty((n, self.P), dtype=torch.int32, device=device),
+                torch.empty(n, dtype=torch.uint8, device=device))
+
+    def evaluate(self, orders, out=None, stream=None, resend_costs=False):
+        n = int(orders.shape[0])
+        assert orders.dtype.itemsize == 2 and orders.is_contiguous()
+        assert orders.shape[1] == self.stride
+        out = self.outputs(n, orders.device) if out is None else out
+        send = self.costs if (resend_costs or not self._costs_sent) else None
+        evaluate(self.h, send, orders, n, *out, stream=stream)
+        self._costs_sent = True
+        return out
+
+    def argmin(self, makespan, flags, index_base=0, key=None, stream=None):
+        import torch
+        if key is None:
+            key = torch.full((1,), -1, dtype=torch.int64, device=makespan.device)
+        argmin(self.h, makespan, flags, int(makespan.shape[0]), index_base, key, stream=stream)
+        return key

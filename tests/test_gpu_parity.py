@@ -1,0 +1,184 @@
+"""GPU parity: the HIP path through the C ABI against the CPU oracle,
+element by element and bit-exact (all quantities are integers)."""
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2504_14145_amd as dip
+
+DEV = "cuda:0"
+
+
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def run_gpu(sim, rows_np):
+    orders = torch.from_numpy(np.ascontiguousarray(rows_np)).to(DEV)
+    ms, bub, pk, fl = sim.evaluate(orders)
+    torch.cuda.synchronize()
+    return ms.cpu().numpy(), bub.cpu().numpy(), pk.cpu().numpy(), fl.cpu().numpy()
+
+
+def assert_same(got, want, idx=None):
+    ms, bub, pk, fl = got
+    if idx is not None:
+        ms, bub, pk, fl = ms[idx], bub[idx], pk[idx], fl[idx]
+    np.testing.assert_array_equal(fl, want.flags)
+    np.testing.assert_array_equal(ms, want.makespan)
+    np.testing.assert_array_equal(bub, want.bubble)
+    np.testing.assert_array_equal(pk, want.peak)
+
+
+SMALL = {1: 1024, 2: 4099, 3: 515, 4: 259, 5: 67}
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
+def test_parity_small_all_variants(cid):
+    """Every config at an oracle-friendly size with a ragged tail, under every
+    kernel variant that fits the device."""
+    need_gpu()
+    prob = W.make_problem(cid)
+    rows = W.generator_for(prob, cid).generate(0, SMALL[cid])
+    want = O.evaluate(prob, rows, threads=16)
+    sim = dip.Sim(prob)
+    print(f"config {cid} auto variant: {sim.info}", flush=True)
+    tried = 0
+    for variant in (0, 1, 2, 3, 4):
+        for wpb in (0, 1, 4):
+            if sim.configure(variant, wpb) != dip.OK:
+                continue
+            tried += 1
+            print(f"  variant {variant} wpb {wpb}: {sim.info['variant']}", flush=True)
+            assert_same(run_gpu(sim, rows), want)
+    assert tried >= 2
+    sim.close()
+
+
+def test_parity_full_bench_workload():
+    """The 8-stage VLM workload at its full 65,536 candidates, in the launch
+    configuration the benchmark times, compared on every candidate, plus the
+    argmin."""
+    need_gpu()
+    prob = W.make_problem(2)
+    cfg = W.get(2)
+    rows = W.generator_for(prob, 2).generate(0, cfg.n_cand)
+    want = O.evaluate(prob, rows, threads=16)
+    sim = dip.Sim(prob)
+    got = run_gpu(sim, rows)
+    assert_same(got, want)
+    key = sim.argmin(torch.from_numpy(got[0]).to(DEV), torch.from_numpy(got[3]).to(DEV))
+    torch.cuda.synchronize()
+    assert dip.decode_key(int(key.item())) == O.argmin(want.makespan, want.flags)
+    sim.close()
+
+
+@pytest.mark.parametrize("cid,n", [(3, 65536), (4, 32768), (5, 16384)])
+def test_parity_large_sampled(cid, n):
+    """Larger batches: every GPU output of a sample of candidates (first,
+    last, a random spread) against the oracle run on just those rows."""
+    need_gpu()
+    prob = W.make_problem(cid)
+    rows = W.generator_for(prob, cid).generate(0, n)
+    sim = dip.Sim(prob)
+    got = run_gpu(sim, rows)
+    rng = np.random.default_rng(cid)
+    idx = np.unique(np.concatenate([[0, n - 1], rng.choice(n, size=min(n, 384), replace=False)]))
+    want = O.evaluate(prob, rows[idx], threads=16)
+    assert_same(got, want, idx)
+    sim.close()
+
+
+def test_edge_cases_invalid_deadlock_single():
+    need_gpu()
+    prob = W.make_problem(1)
+    base = W.generator_for(prob, 1).generate(0, 8)
+    rows = [base[i].copy() for i in range(8)]
+    rows[1][3] = 99                     # id out of range on rank 0
+    rows[2][16 + 2] = rows[2][16 + 5]   # duplicate on rank 1
+    i0, i1 = int(np.nonzero(rows[3][:16] == 0)[0][0]), int(np.nonzero(rows[3][:16] == 1)[0][0])
+    rows[3][i0], rows[3][i1] = 1, 0     # B0 before F0 on rank 0: deadlock
+    rows[4][-1] = -7                    # negative id on the last rank
+    rows = np.stack(rows)
+    want = O.evaluate(prob, rows)
+    assert want.flags[1] == O.FLAG_INVALID and want.flags[3] & O.FLAG_DEADLOCK
+    sim = dip.Sim(prob)
+    for n in (1, 2, 5, 8):
+        got = run_gpu(sim, rows[:n])
+        assert_same(got, O.evaluate(prob, rows[:n]))
+    sim.close()
+
+
+def test_zero_candidates_is_noop():
+    need_gpu()
+    prob = W.make_problem(1)
+    sim = dip.Sim(prob)
+    out = sim.outputs(1)
+    dip.evaluate(sim.h, sim.costs, torch.empty((0, prob.stride), dtype=torch.int16, device=DEV),
+                 0, *out)
+    torch.cuda.synchronize()
+    sim.close()
+
+
+def test_errors_through_abi():
+    need_gpu()
+    prob = W.make_problem(1)
+    sim = dip.Sim(prob)
+    rows = torch.zeros((4, prob.stride), dtype=torch.int16, device=DEV)
+    out = sim.outputs(4)
+    with pytest.raises(dip.DipSimError) as e:
+        dip.evaluate(sim.h, None, rows, 4, *out)        # no costs yet
+    assert e.value.code == dip.E_STATE
+    dip.evaluate(sim.h, sim.costs, rows, 4, *out)
+    flat = torch.zeros(4 * prob.stride + 8, dtype=torch.int16, device=DEV)
+    with pytest.raises(dip.DipSimError) as e:
+        dip.evaluate(sim.h, None, flat[1:], 4, *out)     # misaligned rows
+    assert e.value.code == dip.E_INVAL
+    key = torch.full((1,), -1, dtype=torch.int64, device=DEV)
+    with pytest.raises(dip.DipSimError) as e:
+        dip.argmin(sim.h, out[0], out[3], 4, 2**32 - 2, key)
+    assert e.value.code == dip.E_RANGE
+    torch.cuda.synchronize()
+    sim.close()
+
+
+def test_argmin_ties_chunks_and_empty():
+    need_gpu()
+    prob = W.make_problem(2)
+    rows = W.generator_for(prob, 2).generate(0, 3000)
+    rows = np.concatenate([rows, rows[:1000]])          # planted duplicates: ties
+    want = O.evaluate(prob, rows, threads=16)
+    sim = dip.Sim(prob)
+    ms, bub, pk, fl = sim.evaluate(torch.from_numpy(rows).to(DEV))
+    key = torch.full((1,), -1, dtype=torch.int64, device=DEV)
+    # fold in uneven chunks; index_base keeps global indices
+    cuts = [0, 1, 700, 2999, 3001, 4000]
+    for a, b in zip(cuts, cuts[1:]):
+        dip.argmin(sim.h, ms[a:b], fl[a:b], b - a, a, key)
+    torch.cuda.synchronize()
+    assert dip.decode_key(int(key.item())) == O.argmin(want.makespan, want.flags)
+    # all candidates flagged: the key stays "none"
+    bad = torch.ones_like(fl)
+    key2 = sim.argmin(ms, bad)
+    torch.cuda.synchronize()
+    assert dip.decode_key(int(key2.item())) == (-1, -1)
+    sim.close()
+
+
+def test_deterministic_repeat_and_reused_costs():
+    need_gpu()
+    prob = W.make_problem(3)
+    rows = W.generator_for(prob, 3).generate(0, 300)
+    sim = dip.Sim(prob)
+    a = run_gpu(sim, rows)
+    b = run_gpu(sim, rows)           # costs not resent: reused
+    for x, y in zip(a, b):
+        np.testing.assert_array_equal(x, y)
+    sim.close()
