@@ -41,6 +41,9 @@
  * independent.  evaluate and argmin enqueue work on the given HIP stream
  * (a hipStream_t passed as void*, NULL = the default stream) and return
  * without waiting; outputs are valid once that stream has reached the work.
+ * A handle owns one device scratch area and one device copy of the costs:
+ * two evaluate calls on one handle whose kernels may overlap (different
+ * streams without an ordering between them) race; use one handle per stream.
  * Every call returns DIP_OK (0) or a negative DIP_E_* code; nothing throws
  * across this boundary.
  */
@@ -130,10 +133,18 @@ int dip_sim_check_costs(const dip_topology *topo, const dip_costs *costs);
 int dip_sim_create(const dip_topology *topo, dip_sim **out);
 
 /* Force a kernel variant (0 = automatic choice) and waves per block
- * (0 = automatic).  DIP_E_UNSUPPORTED if the variant does not fit the device.
- * Variants: 1 tables, orders and end times in LDS; 2 tables in global memory,
- * orders and end times in LDS; 3 end times in LDS only; 4 nothing in LDS
- * (end times in device scratch). */
+ * (0 = automatic).  DIP_E_UNSUPPORTED if the variant does not fit the device
+ * or the topology.  General kernels (any dependence DAG): 1 tables, orders
+ * and end times in LDS; 2 tables in global memory, orders and end times in
+ * LDS; 3 end times in LDS only; 4 nothing in LDS (end times in device
+ * scratch).  Pipeline kernels (every op with several predecessors has them
+ * all on one rank, and every op feeds at most one such op): 5 end times and
+ * orders in LDS, op records read through the caches; 6 end times in device
+ * scratch; 7 end times, orders and op records in LDS.  Variants 5 and 7 also
+ * need every edge latency below 2^16, and all pipeline kernels need the sum
+ * of all costs below 2^30, at evaluate time; when the costs do not allow the
+ * configured pipeline kernel, evaluate runs the automatically chosen general
+ * kernel instead (dip_sim_get_info reports the one that runs). */
 int dip_sim_configure(dip_sim *h, int32_t variant, int32_t waves_per_block);
 
 int dip_sim_get_info(const dip_sim *h, dip_sim_info *info);

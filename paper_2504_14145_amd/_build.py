@@ -6,7 +6,10 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRC = os.path.join(HERE, "csrc", "dip_sim.hip")
+CSRC = os.path.join(HERE, "csrc")
+SOURCES = [os.path.join(CSRC, f) for f in
+           ("host.hip", "kern_general.hip", "kern_pipe.hip", "kern_pipe_lds.hip",
+            "kern_argmin.hip")]
 LIB = os.path.join(HERE, "libdip_sim.so")
 INCLUDE = os.path.join(ROOT, "include")
 
@@ -26,7 +29,7 @@ def hipcc() -> str:
 
 def build() -> str:
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", INCLUDE, "-o", tmp, SRC]
+    cmd = [hipcc(), *HIPCC_FLAGS, "-I", INCLUDE, "-I", CSRC, "-o", tmp, *SOURCES]
     subprocess.check_call(cmd)
     os.replace(tmp, LIB)
     return LIB

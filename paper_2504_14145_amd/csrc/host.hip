@@ -1,0 +1,716 @@
+// host.hip -- the C ABI of include/dip_sim.h: validation, device tables,
+// kernel-variant choice and stream-ordered launches.
+//
+// Kernel families (see kern_general.hip, kern_pipe.hip, kern_pipe_lds.hip):
+//   variants 1-4  general kernel, any predecessor count, tables placed per
+//                 variant (all in LDS ... end times in device scratch);
+//   variant 5     pipeline kernel with end-time tables and order rows in LDS,
+//                 op records read through the caches;
+//   variant 6     pipeline kernel with end-time tables in device scratch;
+//   variant 7     as 5, with the op records in LDS too.
+// The pipeline kernel needs every op with several predecessors to have them
+// all on one rank, every op to feed at most one such op, and every time
+// below 2^30 (the sum of all costs and latencies bounds every time), so the
+// time bound is re-checked whenever costs change.
+#include <algorithm>
+#include <cstdint>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "dip_sim.h"
+#include "internal.h"
+
+using namespace dipsim;
+
+namespace {
+
+thread_local hipError_t g_last_hip = hipSuccess;
+
+constexpr int kMaxRanks = 64;
+constexpr int32_t kMaxOpsPerRank = 32768;
+constexpr int64_t kScratchCap = int64_t(2) << 30;  // device scratch ceiling
+
+#define DIP_HIP(expr)          \
+  do {                         \
+    hipError_t e_ = (expr);    \
+    if (e_ != hipSuccess) {    \
+      g_last_hip = e_;         \
+      return DIP_E_HIP;        \
+    }                          \
+  } while (0)
+
+int ceil_pow2_log2(int p) {
+  int l = 0;
+  while ((1 << l) < p) ++l;
+  return l;
+}
+
+}  // namespace
+
+struct dip_sim {
+  int device = 0;
+  int32_t P = 0, N = 0, E = 0, n_slots = 0;
+  int64_t stride = 0;
+  std::vector<int32_t> n_ops, rank_off, pred_ptr, pred_op, op_slot, cap;
+  std::vector<uint8_t> kind;
+  int32_t pwl = 0, G = 0;
+  bool pipe_ok = false;                // topology fits the pipeline kernel
+  bool pipe_costs_ok = false;          // last costs keep every time below 2^30
+  int32_t tab_stride = 0;              // pipeline kernel: words per end-time table
+  int32_t n_joins = 0;                 // ops with several predecessors
+  uint32_t join_base = 0;              // byte offset of the join blocks in a table
+  std::vector<int32_t> join_of;        // [N] join index of an op, -1 if none
+  std::vector<int32_t> feeds_join;     // [N] the join op this op feeds, -1 if none
+  std::vector<int32_t> feed_edge;      // [N] edge index of that feed
+  // device tables
+  int4 *d_rec = nullptr;               // general records [N]
+  int2 *d_edge = nullptr;              // general edges [E]
+  int4 *d_prec = nullptr;              // pipeline records [N][2]
+  int4 *d_rec16 = nullptr;             // compact pipeline records [N]
+  int32_t *d_jk = nullptr;             // [n_joins] predecessors of each join
+  bool lds16_costs_ok = false;         // compact records hold the last costs
+  int32_t *d_md = nullptr;             // pipeline memory deltas [N]
+  int32_t *d_rank_off = nullptr, *d_busy = nullptr, *d_cap = nullptr;
+  void *d_scratch_gen = nullptr;       // variant 4: end tables per resident wave
+  int64_t scratch_gen_bytes = 0;
+  void *d_scratch_pipe = nullptr;      // variant 6: epoch-stamped tables + epoch bytes
+  int64_t scratch_pipe_bytes = 0;
+  // pinned staging for cost uploads
+  unsigned char *h_stage = nullptr;
+  int64_t stage_bytes = 0;
+  hipEvent_t stage_done = nullptr;
+  bool stage_pending = false;
+  bool costs_set = false;
+  // launch configuration of the chosen variant
+  int variant = 0, wpb = 1;
+  int64_t lds_bytes = 0;
+  int max_blocks = 1;
+  int n_cu = 1;
+  int64_t lds_block_max = 65536;
+  int forced_variant = 0, forced_wpb = 0;
+  // fallback general configuration (when the pipeline kernel is chosen but
+  // the costs of a call exceed its time bound)
+  int gen_variant = 0, gen_wpb = 1, gen_max_blocks = 1;
+  int64_t gen_lds = 0;
+};
+
+namespace {
+
+struct GenBytes {
+  int64_t tab, ord, end;
+};
+
+GenBytes general_bytes(const dip_sim *h, int v) {
+  GenBytes b{0, 0, 0};
+  const int64_t G = h->G;
+  if (v == 1) b.tab = align16(int64_t(h->N) * 16) + align16(int64_t(h->E) * 8);
+  if (v <= 2) b.ord = align16(G * h->stride * 2);
+  if (v <= 3) b.end = align16(G * int64_t(h->N) * 4);
+  return b;
+}
+
+int64_t lds_for(const dip_sim *h, int v, int wpb) {
+  if (v <= 4) {
+    GenBytes b = general_bytes(h, v);
+    return b.tab + int64_t(wpb) * (b.ord + b.end);
+  }
+  if (v == 5 || v == 7) {
+    const int64_t per_wave = int64_t(h->G) * (int64_t(h->tab_stride) * 4 + h->stride * 2);
+    return int64_t(wpb) * per_wave + (v == 7 ? align16(int64_t(h->N) * 16) : 0);
+  }
+  return 0;
+}
+
+const void *kernel_ptr(const dip_sim *h, int v) {
+  if (v <= 4) return general_kernel_ptr(v);
+  if (v == 6) return pipe_kernel_ptr(h->pwl, true);
+  return pipe_lds_kernel_ptr(h->pwl, v == 7);
+}
+
+// LDS-resident pipeline kernel: compact records address a table by 16-bit
+// byte offsets.
+bool lds16_shape_ok(const dip_sim *h) { return h->pipe_ok && int64_t(h->tab_stride) * 4 <= 0xffff; }
+
+// Resident blocks per CU for (variant, waves per block); 0 if it does not fit.
+int blocks_per_cu(dip_sim *h, int v, int wpb) {
+  if (v >= 5 && !h->pipe_ok) return 0;
+  if ((v == 5 || v == 7) && !lds16_shape_ok(h)) return 0;
+  const int64_t lds = lds_for(h, v, wpb);
+  if (lds > h->lds_block_max) return 0;
+  const void *k = kernel_ptr(h, v);
+  if (lds > 65536) {
+    if (hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess) {
+      (void)hipGetLastError();
+      return 0;
+    }
+  }
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k, wpb * kWave, size_t(lds)) != hipSuccess) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  return nb;
+}
+
+int64_t scratch_need(const dip_sim *h, int v, int wpb, int blocks) {
+  if (v == 4) return int64_t(blocks) * wpb * h->G * int64_t(h->N) * 4;
+  if (v == 6) {
+    const int64_t slots = int64_t(blocks) * wpb * h->G;
+    return slots * int64_t(h->tab_stride) * 4 + align16(slots);
+  }
+  return 0;
+}
+
+// Device scratch for variant 4 (general) or 6 (pipeline).  The pipeline
+// scratch is zeroed whenever a configuration is applied: zero is "every table
+// stamped with epoch 0 and every epoch byte 0", the state its kernel expects.
+int ensure_scratch(dip_sim *h, int v, int64_t need) {
+  void **buf = v == 6 ? &h->d_scratch_pipe : &h->d_scratch_gen;
+  int64_t *have = v == 6 ? &h->scratch_pipe_bytes : &h->scratch_gen_bytes;
+  if (need > *have) {
+    if (*buf) {
+      DIP_HIP(hipDeviceSynchronize());
+      DIP_HIP(hipFree(*buf));
+      *buf = nullptr;
+    }
+    *have = 0;
+    if (hipMalloc(buf, size_t(need)) != hipSuccess) {
+      (void)hipGetLastError();
+      return DIP_E_NOMEM;
+    }
+    *have = need;
+  }
+  if (v == 6) {
+    DIP_HIP(hipDeviceSynchronize());
+    DIP_HIP(hipMemset(*buf, 0, size_t(*have)));
+    DIP_HIP(hipDeviceSynchronize());
+  }
+  return DIP_OK;
+}
+
+struct Pick {
+  int v = 0, wpb = 0, nb = 0, waves = 0;
+};
+
+Pick best_of(dip_sim *h, int v_lo, int v_hi, int forced_wpb) {
+  Pick best;
+  for (int v = v_lo; v <= v_hi; ++v) {
+    for (int w : {4, 2, 1}) {
+      if (forced_wpb && w != forced_wpb) continue;
+      const int nb = blocks_per_cu(h, v, w);
+      if (nb <= 0) continue;
+      const int waves = nb * w;
+      // prefer the lower variant (less global traffic) unless a higher one
+      // at least doubles the resident waves and the lower has fewer than 8
+      if (best.v == 0 ||
+          (waves > best.waves && (v == best.v || (best.waves < 8 && waves >= 2 * best.waves)))) {
+        best = Pick{v, w, nb, waves};
+      }
+    }
+  }
+  return best;
+}
+
+int apply_pick(dip_sim *h, const Pick &p, int *variant, int *wpb, int *max_blocks,
+               int64_t *lds) {
+  *variant = p.v;
+  *wpb = p.wpb;
+  *lds = lds_for(h, p.v, p.wpb);
+  int mb = p.nb * h->n_cu;
+  if (p.v == 4 || p.v == 6) {
+    const int64_t per_block = scratch_need(h, p.v, p.wpb, 1);
+    mb = int(std::min<int64_t>(mb, std::max<int64_t>(1, kScratchCap / per_block)));
+    int rc = ensure_scratch(h, p.v, scratch_need(h, p.v, p.wpb, mb));
+    if (rc != DIP_OK) return rc;
+  }
+  *max_blocks = mb;
+  return DIP_OK;
+}
+
+int choose_config(dip_sim *h) {
+  // general fallback first (always available)
+  const bool force_gen = h->forced_variant >= 1 && h->forced_variant <= 4;
+  Pick g = best_of(h, force_gen ? h->forced_variant : 1, force_gen ? h->forced_variant : 4,
+                   force_gen ? h->forced_wpb : 0);
+  if (g.v == 0) return DIP_E_UNSUPPORTED;
+  int rc = apply_pick(h, g, &h->gen_variant, &h->gen_wpb, &h->gen_max_blocks, &h->gen_lds);
+  if (rc != DIP_OK) return rc;
+  if (force_gen || !h->pipe_ok) {
+    if (h->forced_variant >= 5) return DIP_E_UNSUPPORTED;
+    h->variant = h->gen_variant;
+    h->wpb = h->gen_wpb;
+    h->max_blocks = h->gen_max_blocks;
+    h->lds_bytes = h->gen_lds;
+    return DIP_OK;
+  }
+  Pick p;
+  if (h->forced_variant >= 5) {
+    p = best_of(h, h->forced_variant, h->forced_variant, h->forced_wpb);
+  } else {
+    // LDS-resident if at least 4 waves stay resident (records in LDS when that
+    // keeps as many waves), else tables in device scratch
+    Pick rl = best_of(h, 7, 7, h->forced_wpb);
+    Pick gl = best_of(h, 5, 5, h->forced_wpb);
+    Pick lds = (rl.v && rl.waves >= gl.waves) ? rl : gl;
+    Pick glob = best_of(h, 6, 6, h->forced_wpb);
+    p = (lds.v && lds.waves >= 4) ? lds : (glob.v ? glob : lds);
+  }
+  if (p.v == 0) return DIP_E_UNSUPPORTED;
+  return apply_pick(h, p, &h->variant, &h->wpb, &h->max_blocks, &h->lds_bytes);
+}
+
+int check_costs_against(int32_t P, const int32_t *n_ops, const int32_t *pred_ptr,
+                        const int32_t *op_slot, const uint8_t *kind, int32_t n_slots,
+                        const dip_costs *c, int64_t *total_out) {
+  if (!c || !c->op_cost || !c->slot_act) return DIP_E_INVAL;
+  int64_t N = 0;
+  for (int r = 0; r < P; ++r) N += n_ops[r];
+  const int64_t E = pred_ptr[N];
+  if (E > 0 && !c->edge_comm) return DIP_E_INVAL;
+  int64_t total = 0;
+  for (int64_t g = 0; g < N; ++g) {
+    if (c->op_cost[g] < 0) return DIP_E_RANGE;
+    total += c->op_cost[g];
+  }
+  for (int64_t e = 0; e < E; ++e) {
+    if (c->edge_comm[e] < 0) return DIP_E_RANGE;
+    total += c->edge_comm[e];
+  }
+  if (total > INT32_MAX) return DIP_E_RANGE;
+  for (int32_t s = 0; s < n_slots; ++s)
+    if (c->slot_act[s] < 0) return DIP_E_RANGE;
+  // per rank: the running activation sum stays within int32 either way
+  int64_t off = 0;
+  for (int r = 0; r < P; ++r) {
+    int64_t up = 0, down = 0;
+    for (int64_t g = off; g < off + n_ops[r]; ++g) {
+      const int64_t act = c->slot_act[op_slot[g]];
+      if (kind[g] == 0) up += act;
+      else down += act;
+    }
+    if (up > INT32_MAX || down > INT32_MAX) return DIP_E_RANGE;
+    off += n_ops[r];
+  }
+  if (total_out) *total_out = total;
+  return DIP_OK;
+}
+
+struct StageLayout {
+  int64_t rec, edge, busy, prec, md, rec16, jk, total;
+};
+
+StageLayout stage_layout(const dip_sim *h) {
+  StageLayout L{};
+  int64_t off = 0;
+  L.rec = off; off += align16(int64_t(h->N) * 16);
+  L.edge = off; off += align16(int64_t(std::max(h->E, 1)) * 8);
+  L.busy = off; off += align16(int64_t(h->P) * 4);
+  L.prec = off; off += h->pipe_ok ? align16(int64_t(h->N) * 32) : 0;
+  L.md = off; off += h->pipe_ok ? align16(int64_t(h->N) * 4) : 0;
+  L.rec16 = off; off += h->pipe_ok ? align16(int64_t(h->N) * 16) : 0;
+  L.jk = off; off += h->pipe_ok ? align16(int64_t(std::max(h->n_joins, 1)) * 4) : 0;
+  L.total = off;
+  return L;
+}
+
+int upload_costs(dip_sim *h, const dip_costs *c, hipStream_t stream) {
+  int64_t total = 0;
+  int rc = check_costs_against(h->P, h->n_ops.data(), h->pred_ptr.data(), h->op_slot.data(),
+                               h->kind.data(), h->n_slots, c, &total);
+  if (rc != DIP_OK) return rc;
+  if (h->stage_pending) {
+    DIP_HIP(hipEventSynchronize(h->stage_done));
+    h->stage_pending = false;
+  }
+  const StageLayout L = stage_layout(h);
+  int4 *rec = reinterpret_cast<int4 *>(h->h_stage + L.rec);
+  int2 *edge = reinterpret_cast<int2 *>(h->h_stage + L.edge);
+  int32_t *busy = reinterpret_cast<int32_t *>(h->h_stage + L.busy);
+  for (int32_t g = 0; g < h->N; ++g) {
+    const int32_t act = c->slot_act[h->op_slot[g]];
+    rec[g] = make_int4(c->op_cost[g], h->kind[g] == 0 ? act : -act, h->pred_ptr[g],
+                       h->pred_ptr[g + 1]);
+  }
+  for (int32_t e = 0; e < h->E; ++e) edge[e] = make_int2(h->pred_op[e], c->edge_comm[e]);
+  for (int r = 0; r < h->P; ++r) {
+    int64_t s = 0;
+    for (int32_t g = h->rank_off[r]; g < h->rank_off[r + 1]; ++g) s += c->op_cost[g];
+    busy[r] = int32_t(s);
+  }
+  DIP_HIP(hipMemcpyAsync(h->d_rec, rec, size_t(h->N) * 16, hipMemcpyHostToDevice, stream));
+  if (h->E > 0)
+    DIP_HIP(hipMemcpyAsync(h->d_edge, edge, size_t(h->E) * 8, hipMemcpyHostToDevice, stream));
+  DIP_HIP(hipMemcpyAsync(h->d_busy, busy, size_t(h->P) * 4, hipMemcpyHostToDevice, stream));
+  h->pipe_costs_ok = false;
+  if (h->pipe_ok) {
+    // pipeline records: {cost, memdelta, polled entry (byte offset), comm}
+    // and {join block fed (byte offset, 0 = none), its k, comm into it}
+    int32_t *pr = reinterpret_cast<int32_t *>(h->h_stage + L.prec);
+    int32_t *md = reinterpret_cast<int32_t *>(h->h_stage + L.md);
+    for (int32_t g = 0; g < h->N; ++g) {
+      int32_t *q = pr + int64_t(g) * 8;
+      const int32_t np = h->pred_ptr[g + 1] - h->pred_ptr[g];
+      q[0] = rec[g].x;
+      q[1] = rec[g].y;
+      if (np == 0) {
+        q[2] = h->N * 4;
+        q[3] = 0;
+      } else if (np == 1) {
+        q[2] = h->pred_op[h->pred_ptr[g]] * 4;
+        q[3] = c->edge_comm[h->pred_ptr[g]];
+      } else {
+        q[2] = int32_t(h->join_base) + h->join_of[g] * 16;
+        q[3] = 0;
+      }
+      const int32_t o = h->feeds_join[g];
+      q[4] = o < 0 ? 0 : int32_t(h->join_base) + h->join_of[o] * 16;
+      q[5] = o < 0 ? 0 : h->pred_ptr[o + 1] - h->pred_ptr[o];
+      q[6] = o < 0 ? 0 : c->edge_comm[h->feed_edge[g]];
+      q[7] = 0;
+      md[g] = rec[g].y;
+    }
+    DIP_HIP(hipMemcpyAsync(h->d_prec, pr, size_t(h->N) * 32, hipMemcpyHostToDevice, stream));
+    DIP_HIP(hipMemcpyAsync(h->d_md, md, size_t(h->N) * 4, hipMemcpyHostToDevice, stream));
+    h->pipe_costs_ok = total < int64_t(kValueLimit);
+    // compact records: offsets and latencies in 16 bits
+    int4 *r16 = reinterpret_cast<int4 *>(h->h_stage + L.rec16);
+    int32_t *jk = reinterpret_cast<int32_t *>(h->h_stage + L.jk);
+    bool fits = lds16_shape_ok(h);
+    for (int32_t g = 0; g < h->N; ++g) {
+      const int32_t *q = pr + int64_t(g) * 8;
+      fits = fits && q[3] <= 0xffff && q[6] <= 0xffff;
+      r16[g] = make_int4(q[0], q[1], int32_t(uint32_t(q[2]) | (uint32_t(q[3]) << 16)),
+                         int32_t(uint32_t(q[4]) | (uint32_t(q[6]) << 16)));
+    }
+    for (int32_t g = 0; g < h->N; ++g)
+      if (h->join_of[g] >= 0) jk[h->join_of[g]] = h->pred_ptr[g + 1] - h->pred_ptr[g];
+    DIP_HIP(hipMemcpyAsync(h->d_rec16, r16, size_t(h->N) * 16, hipMemcpyHostToDevice, stream));
+    if (h->n_joins > 0)
+      DIP_HIP(hipMemcpyAsync(h->d_jk, jk, size_t(h->n_joins) * 4, hipMemcpyHostToDevice, stream));
+    h->lds16_costs_ok = h->pipe_costs_ok && fits;
+  }
+  DIP_HIP(hipEventRecord(h->stage_done, stream));
+  h->stage_pending = true;
+  h->costs_set = true;
+  return DIP_OK;
+}
+
+void release(dip_sim *h) {
+  if (!h) return;
+  (void)hipDeviceSynchronize();
+  if (h->d_rec) (void)hipFree(h->d_rec);
+  if (h->d_edge) (void)hipFree(h->d_edge);
+  if (h->d_prec) (void)hipFree(h->d_prec);
+  if (h->d_md) (void)hipFree(h->d_md);
+  if (h->d_rec16) (void)hipFree(h->d_rec16);
+  if (h->d_jk) (void)hipFree(h->d_jk);
+  if (h->d_rank_off) (void)hipFree(h->d_rank_off);
+  if (h->d_busy) (void)hipFree(h->d_busy);
+  if (h->d_cap) (void)hipFree(h->d_cap);
+  if (h->d_scratch_gen) (void)hipFree(h->d_scratch_gen);
+  if (h->d_scratch_pipe) (void)hipFree(h->d_scratch_pipe);
+  if (h->h_stage) (void)hipHostFree(h->h_stage);
+  if (h->stage_done) (void)hipEventDestroy(h->stage_done);
+  delete h;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dip_sim_abi_version(void) { return DIP_SIM_ABI_VERSION; }
+
+int dip_sim_check_topology(const dip_topology *t) {
+  if (!t || !t->n_ops || !t->pred_ptr || !t->op_kind || !t->op_slot || !t->mem_cap)
+    return DIP_E_INVAL;
+  if (t->n_ranks <= 0) return DIP_E_INVAL;
+  if (t->n_ranks > kMaxRanks) return DIP_E_UNSUPPORTED;
+  int64_t N = 0;
+  for (int r = 0; r < t->n_ranks; ++r) {
+    if (t->n_ops[r] < 0 || t->n_ops[r] > kMaxOpsPerRank) return DIP_E_TOPO;
+    N += t->n_ops[r];
+  }
+  if (N == 0 || N > INT32_MAX / 64) return DIP_E_TOPO;
+  if (t->cand_stride < N || t->cand_stride % 8 != 0) return DIP_E_INVAL;
+  if (t->n_slots < 0) return DIP_E_TOPO;
+  if (t->pred_ptr[0] != 0) return DIP_E_TOPO;
+  for (int64_t g = 0; g < N; ++g)
+    if (t->pred_ptr[g + 1] < t->pred_ptr[g]) return DIP_E_TOPO;
+  const int64_t E = t->pred_ptr[N];
+  if (E > 0 && !t->pred_op) return DIP_E_INVAL;
+  for (int64_t g = 0; g < N; ++g) {
+    for (int32_t e = t->pred_ptr[g]; e < t->pred_ptr[g + 1]; ++e)
+      if (t->pred_op[e] < 0 || t->pred_op[e] >= N || t->pred_op[e] == g) return DIP_E_TOPO;
+    if (t->op_kind[g] > 1) return DIP_E_TOPO;
+    if (t->op_slot[g] < 0 || t->op_slot[g] >= t->n_slots) return DIP_E_TOPO;
+  }
+  return DIP_OK;
+}
+
+int dip_sim_check_costs(const dip_topology *t, const dip_costs *c) {
+  int rc = dip_sim_check_topology(t);
+  if (rc != DIP_OK) return rc;
+  return check_costs_against(t->n_ranks, t->n_ops, t->pred_ptr, t->op_slot, t->op_kind,
+                             t->n_slots, c, nullptr);
+}
+
+int dip_sim_create(const dip_topology *t, dip_sim **out) {
+  if (!out) return DIP_E_INVAL;
+  *out = nullptr;
+  int rc = dip_sim_check_topology(t);
+  if (rc != DIP_OK) return rc;
+  dip_sim *h = new (std::nothrow) dip_sim();
+  if (!h) return DIP_E_NOMEM;
+  h->P = t->n_ranks;
+  h->n_ops.assign(t->n_ops, t->n_ops + h->P);
+  h->rank_off.assign(h->P + 1, 0);
+  for (int r = 0; r < h->P; ++r) h->rank_off[r + 1] = h->rank_off[r] + t->n_ops[r];
+  h->N = h->rank_off[h->P];
+  h->E = t->pred_ptr[h->N];
+  h->n_slots = t->n_slots;
+  h->stride = t->cand_stride;
+  h->pred_ptr.assign(t->pred_ptr, t->pred_ptr + h->N + 1);
+  if (h->E > 0) h->pred_op.assign(t->pred_op, t->pred_op + h->E);
+  h->kind.assign(t->op_kind, t->op_kind + h->N);
+  h->op_slot.assign(t->op_slot, t->op_slot + h->N);
+  h->cap.assign(t->mem_cap, t->mem_cap + h->P);
+  h->pwl = ceil_pow2_log2(h->P);
+  h->G = kWave >> h->pwl;
+  // pipeline kernel eligibility: the predecessors of a multi-predecessor op
+  // run on one rank, and no op feeds two such ops
+  {
+    std::vector<int32_t> rank_of(h->N);
+    for (int r = 0; r < h->P; ++r)
+      for (int32_t g = h->rank_off[r]; g < h->rank_off[r + 1]; ++g) rank_of[g] = r;
+    h->join_of.assign(h->N, -1);
+    h->feeds_join.assign(h->N, -1);
+    h->feed_edge.assign(h->N, -1);
+    bool ok = true;
+    for (int32_t g = 0; g < h->N && ok; ++g) {
+      const int32_t b = h->pred_ptr[g], e = h->pred_ptr[g + 1];
+      if (e - b < 2) continue;
+      h->join_of[g] = h->n_joins++;
+      for (int32_t k = b; k < e && ok; ++k) {
+        const int32_t p = h->pred_op[k];
+        if (rank_of[p] != rank_of[h->pred_op[b]] || h->feeds_join[p] >= 0) ok = false;
+        h->feeds_join[p] = g;
+        h->feed_edge[p] = k;
+      }
+    }
+    // op entries, the zero cell (index N), the never-ready cell (index N + 1)
+    const int64_t base_words = (int64_t(h->N) + 2 + 3) & ~int64_t(3);
+    const int64_t stride = base_words + 4 * int64_t(h->n_joins);
+    h->pipe_ok = ok && stride * 4 < int64_t(INT32_MAX);
+    h->join_base = uint32_t(base_words * 4);
+    h->tab_stride = int32_t(stride);
+  }
+
+  auto hip_fail = [&](hipError_t e) { g_last_hip = e; release(h); return int(DIP_E_HIP); };
+  hipError_t e;
+  if ((e = hipGetDevice(&h->device)) != hipSuccess) return hip_fail(e);
+  int v = 0;
+  if ((e = hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, h->device)) != hipSuccess)
+    return hip_fail(e);
+  h->n_cu = std::max(1, v);
+  if ((e = hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, h->device)) != hipSuccess)
+    return hip_fail(e);
+  h->lds_block_max = v;
+  if (hipDeviceGetAttribute(&v, hipDeviceAttributeSharedMemPerBlockOptin, h->device) == hipSuccess && v > 0)
+    h->lds_block_max = std::max<int64_t>(h->lds_block_max, v);
+  (void)hipGetLastError();
+  if ((e = hipMalloc(&h->d_rec, size_t(h->N) * 16)) != hipSuccess) return hip_fail(e);
+  if ((e = hipMalloc(&h->d_edge, size_t(std::max(h->E, 1)) * 8)) != hipSuccess) return hip_fail(e);
+  if (h->pipe_ok) {
+    if ((e = hipMalloc(&h->d_prec, size_t(h->N) * 32)) != hipSuccess) return hip_fail(e);
+    if ((e = hipMalloc(&h->d_md, size_t(h->N) * 4)) != hipSuccess) return hip_fail(e);
+    if ((e = hipMalloc(&h->d_rec16, size_t(h->N) * 16)) != hipSuccess) return hip_fail(e);
+    if ((e = hipMalloc(&h->d_jk, size_t(std::max(h->n_joins, 1)) * 4)) != hipSuccess)
+      return hip_fail(e);
+  }
+  if ((e = hipMalloc(&h->d_rank_off, size_t(h->P + 1) * 4)) != hipSuccess) return hip_fail(e);
+  if ((e = hipMalloc(&h->d_busy, size_t(h->P) * 4)) != hipSuccess) return hip_fail(e);
+  if ((e = hipMalloc(&h->d_cap, size_t(h->P) * 4)) != hipSuccess) return hip_fail(e);
+  if ((e = hipMemcpy(h->d_rank_off, h->rank_off.data(), size_t(h->P + 1) * 4,
+                     hipMemcpyHostToDevice)) != hipSuccess)
+    return hip_fail(e);
+  if ((e = hipMemcpy(h->d_cap, h->cap.data(), size_t(h->P) * 4, hipMemcpyHostToDevice)) != hipSuccess)
+    return hip_fail(e);
+  h->stage_bytes = stage_layout(h).total;
+  if ((e = hipHostMalloc(reinterpret_cast<void **>(&h->h_stage), size_t(h->stage_bytes),
+                         hipHostMallocDefault)) != hipSuccess)
+    return hip_fail(e);
+  if ((e = hipEventCreateWithFlags(&h->stage_done, hipEventDisableTiming)) != hipSuccess)
+    return hip_fail(e);
+  rc = choose_config(h);
+  if (rc != DIP_OK) {
+    release(h);
+    return rc;
+  }
+  *out = h;
+  return DIP_OK;
+}
+
+int dip_sim_configure(dip_sim *h, int32_t variant, int32_t waves_per_block) {
+  if (!h || variant < 0 || variant > 7) return DIP_E_INVAL;
+  if (!(waves_per_block == 0 || waves_per_block == 1 || waves_per_block == 2 ||
+        waves_per_block == 4))
+    return DIP_E_INVAL;
+  const int old_v = h->forced_variant, old_w = h->forced_wpb;
+  h->forced_variant = variant;
+  h->forced_wpb = waves_per_block;
+  int rc = choose_config(h);
+  if (rc != DIP_OK) {
+    h->forced_variant = old_v;
+    h->forced_wpb = old_w;
+    (void)choose_config(h);
+  }
+  return rc;
+}
+
+int dip_sim_get_info(const dip_sim *h, dip_sim_info *info) {
+  if (!h || !info) return DIP_E_INVAL;
+  const bool pipe_off = h->costs_set &&
+                        ((h->variant == 6 && !h->pipe_costs_ok) ||
+                         ((h->variant == 5 || h->variant == 7) && !h->lds16_costs_ok));
+  info->n_ranks = h->P;
+  info->n_ops_total = h->N;
+  info->n_edges = h->E;
+  info->variant = pipe_off ? h->gen_variant : h->variant;
+  info->cand_stride = h->stride;
+  info->lanes_per_group = 1 << h->pwl;
+  info->groups_per_wave = h->G;
+  info->waves_per_block = pipe_off ? h->gen_wpb : h->wpb;
+  info->lds_bytes = int32_t(pipe_off ? h->gen_lds : h->lds_bytes);
+  info->max_blocks = pipe_off ? h->gen_max_blocks : h->max_blocks;
+  info->scratch_bytes = h->scratch_gen_bytes + h->scratch_pipe_bytes;
+  return DIP_OK;
+}
+
+int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, int64_t n_cand,
+                     int32_t *out_makespan, int32_t *out_bubble, int32_t *out_peakmem,
+                     uint8_t *out_flags, void *stream_) {
+  if (!h || n_cand < 0) return DIP_E_INVAL;
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  if (costs) {
+    int rc = upload_costs(h, costs, stream);
+    if (rc != DIP_OK) return rc;
+  }
+  if (!h->costs_set) return DIP_E_STATE;
+  if (n_cand == 0) return DIP_OK;
+  if (!orders || !out_makespan || !out_bubble || !out_peakmem || !out_flags) return DIP_E_INVAL;
+  if ((reinterpret_cast<uintptr_t>(orders) & 15) != 0) return DIP_E_INVAL;
+  if ((reinterpret_cast<uintptr_t>(out_makespan) | reinterpret_cast<uintptr_t>(out_bubble) |
+       reinterpret_cast<uintptr_t>(out_peakmem)) & 3)
+    return DIP_E_INVAL;
+
+  const bool lds_pipe = (h->variant == 5 || h->variant == 7) && h->lds16_costs_ok;
+  const bool pipe = lds_pipe || (h->variant == 6 && h->pipe_costs_ok);
+  if (pipe) {
+    PipeArgs a{};
+    a.orders = orders;
+    a.n_cand = n_cand;
+    a.stride = h->stride;
+    a.out_ms = out_makespan;
+    a.out_bub = out_bubble;
+    a.out_peak = out_peakmem;
+    a.out_flags = out_flags;
+    a.rec = h->d_prec;
+    a.md = h->d_md;
+    a.rank_off = h->d_rank_off;
+    a.busy = h->d_busy;
+    a.cap = h->d_cap;
+    const bool gs = h->variant == 6;
+    if (gs) {
+      const int64_t slots = int64_t(h->max_blocks) * h->wpb * h->G;
+      a.gtab = static_cast<int32_t *>(h->d_scratch_pipe);
+      a.gepoch = static_cast<uint8_t *>(h->d_scratch_pipe) + slots * int64_t(h->tab_stride) * 4;
+    }
+    a.P = h->P;
+    a.N = h->N;
+    a.wpb = h->wpb;
+    a.tab_stride = h->tab_stride;
+    a.n_joins = h->n_joins;
+    a.join_base = h->join_base;
+    a.rec16 = h->d_rec16;
+    a.jk = h->d_jk;
+    const int64_t per_block = int64_t(h->wpb) * h->G;
+    const int64_t want = (n_cand + per_block - 1) / per_block;
+    const int blocks = int(std::min<int64_t>(want, h->max_blocks));
+    if (lds_pipe)
+      DIP_HIP(launch_pipe_lds(h->pwl, h->variant == 7, blocks, h->wpb, size_t(h->lds_bytes),
+                              stream, a));
+    else
+      DIP_HIP(launch_pipe(h->pwl, true, blocks, h->wpb, size_t(h->lds_bytes), stream, a));
+    return DIP_OK;
+  }
+
+  const int v = h->variant <= 4 ? h->variant : h->gen_variant;
+  const int wpb = h->variant <= 4 ? h->wpb : h->gen_wpb;
+  const int maxb = h->variant <= 4 ? h->max_blocks : h->gen_max_blocks;
+  const int64_t lds = h->variant <= 4 ? h->lds_bytes : h->gen_lds;
+  GeneralArgs a{};
+  a.orders = orders;
+  a.n_cand = n_cand;
+  a.stride = h->stride;
+  a.n_groups = (n_cand + h->G - 1) / h->G;
+  a.out_ms = out_makespan;
+  a.out_bub = out_bubble;
+  a.out_peak = out_peakmem;
+  a.out_flags = out_flags;
+  a.rec = h->d_rec;
+  a.edge = h->d_edge;
+  a.rank_off = h->d_rank_off;
+  a.busy = h->d_busy;
+  a.cap = h->d_cap;
+  a.gends = static_cast<int32_t *>(h->d_scratch_gen);
+  a.P = h->P;
+  a.pwl = h->pwl;
+  a.G = h->G;
+  a.N = h->N;
+  a.E = h->E;
+  a.wpb = wpb;
+  const GenBytes b = general_bytes(h, v);
+  a.tab_bytes = uint32_t(b.tab);
+  a.ord_bytes = uint32_t(b.ord);
+  a.end_bytes = uint32_t(b.end);
+  const int64_t want = (a.n_groups + wpb - 1) / wpb;
+  const int blocks = int(std::min<int64_t>(want, maxb));
+  DIP_HIP(launch_general(v, blocks, wpb, size_t(lds), stream, a));
+  return DIP_OK;
+}
+
+int dip_sim_argmin(dip_sim *h, const int32_t *makespan, const uint8_t *flags, int64_t n_cand,
+                   int64_t index_base, uint64_t *inout_best_key, void *stream_) {
+  if (!h || n_cand < 0 || index_base < 0) return DIP_E_INVAL;
+  if (index_base + n_cand > int64_t(UINT32_MAX)) return DIP_E_RANGE;
+  if (n_cand == 0) return DIP_OK;
+  if (!makespan || !flags || !inout_best_key) return DIP_E_INVAL;
+  if ((reinterpret_cast<uintptr_t>(inout_best_key) & 7) || (reinterpret_cast<uintptr_t>(makespan) & 3))
+    return DIP_E_INVAL;
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  const int64_t want = (n_cand + 255) / 256;
+  const int blocks = int(std::min<int64_t>(want, int64_t(h->n_cu) * 8));
+  DIP_HIP(launch_argmin(blocks, stream, makespan, flags, n_cand, uint64_t(index_base),
+                        reinterpret_cast<unsigned long long *>(inout_best_key)));
+  return DIP_OK;
+}
+
+void dip_sim_destroy(dip_sim *h) { release(h); }
+
+const char *dip_sim_strerror(int code) {
+  switch (code) {
+    case DIP_OK: return "ok";
+    case DIP_E_INVAL: return "invalid argument (null pointer, negative count or misaligned buffer)";
+    case DIP_E_TOPO: return "malformed topology";
+    case DIP_E_RANGE: return "negative cost or totals that could overflow int32";
+    case DIP_E_UNSUPPORTED: return "shape not supported by any kernel variant on this device";
+    case DIP_E_NOMEM: return "out of memory";
+    case DIP_E_HIP: return hipGetErrorString(g_last_hip);
+    case DIP_E_STATE: return "no costs supplied yet";
+    default: return "unknown error";
+  }
+}
+
+}  // extern "C"

@@ -1,0 +1,92 @@
+// internal.h -- shared between the host library and the kernel translation
+// units of libdip_sim.  Not part of the public C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace dipsim {
+
+constexpr int kWave = 64;
+
+__host__ __device__ inline int64_t align16(int64_t x) { return (x + 15) & ~int64_t(15); }
+
+// ---------------------------------------------------------------- general
+// General kernel: any DAG (predecessors walked through the CSR), tables
+// placed per variant (1: all in LDS, 2: records in global, rows and end
+// times in LDS, 3: only end times in LDS, 4: end times in device scratch).
+struct GeneralArgs {
+  const int16_t *orders;
+  int64_t n_cand;
+  int64_t stride;          // int16 elements per candidate row
+  int64_t n_groups;        // ceil(n_cand / G)
+  int32_t *out_ms;
+  int32_t *out_bub;
+  int32_t *out_peak;
+  uint8_t *out_flags;
+  const int4 *rec;         // [N] {cost, memdelta, pred_begin, pred_end}
+  const int2 *edge;        // [E] {pred global index, comm}
+  const int32_t *rank_off; // [P+1]
+  const int32_t *busy;     // [P]
+  const int32_t *cap;      // [P]
+  int32_t *gends;          // variant 4: [resident waves][G][N]
+  int32_t P, pwl, G, N, E, wpb;
+  uint32_t tab_bytes;      // LDS bytes holding rec + edge (variant 1)
+  uint32_t ord_bytes;      // LDS bytes of order rows per wave (variants 1, 2)
+  uint32_t end_bytes;      // LDS bytes of end tables per wave (variants 1-3)
+};
+
+const void *general_kernel_ptr(int variant);
+hipError_t launch_general(int variant, int blocks, int wpb, size_t lds, hipStream_t s,
+                          const GeneralArgs &a);
+
+// ---------------------------------------------------------------- pipe
+// Pipeline kernel: every op has one predecessor, none, or several that all
+// run on one rank (folded through a join block), and every time stays below
+// 2^30 so bit 30 of an end-time entry can carry the candidate epoch.
+constexpr int32_t kEpochShift = 30;
+constexpr uint32_t kValueLimit = 1u << kEpochShift;
+
+struct PipeArgs {
+  const int16_t *orders;
+  int64_t n_cand;
+  int64_t stride;           // int16 elements per candidate row
+  int32_t *out_ms;
+  int32_t *out_bub;
+  int32_t *out_peak;
+  uint8_t *out_flags;
+  const int4 *rec;          // [N][2] {cost, memdelta, poll byte offset, comm},
+                            //        {join block byte offset or 0, join k, join comm, 0}
+  const int32_t *md;        // [N] memory delta (+act at F, -act at B)
+  const int32_t *rank_off;  // [P+1]
+  const int32_t *busy;      // [P]
+  const int32_t *cap;       // [P]
+  int32_t *gtab;            // device-scratch tables [slots][tab_stride] (global store)
+  uint8_t *gepoch;          // [slots] epoch bit of each scratch table
+  int32_t P, N, wpb;
+  int32_t tab_stride;       // int32 words per candidate table
+  int32_t n_joins;          // join blocks (4 words each) ...
+  uint32_t join_base;       // ... starting at this byte offset of a table
+  // compact form for the LDS-resident kernel (tables under 64 KiB, latencies
+  // under 2^16): {cost, memdelta, poll offset | comm << 16,
+  //               join block offset | join comm << 16}
+  const int4 *rec16;        // [N]
+  const int32_t *jk;        // [n_joins] predecessors of each join
+};
+
+const void *pipe_kernel_ptr(int pwl, bool global_store);
+hipError_t launch_pipe(int pwl, bool global_store, int blocks, int wpb, size_t lds,
+                       hipStream_t s, const PipeArgs &a);
+
+// LDS-resident pipeline kernel: end-time tables and order rows in LDS,
+// records in LDS (rec_lds) or read through the caches.
+const void *pipe_lds_kernel_ptr(int pwl, bool rec_lds);
+hipError_t launch_pipe_lds(int pwl, bool rec_lds, int blocks, int wpb, size_t lds,
+                           hipStream_t s, const PipeArgs &a);
+
+// ---------------------------------------------------------------- argmin
+hipError_t launch_argmin(int blocks, hipStream_t s, const int32_t *ms, const uint8_t *flags,
+                         int64_t n, uint64_t base, unsigned long long *key);
+
+}  // namespace dipsim

@@ -51,7 +51,7 @@ def test_parity_small_all_variants(cid):
     sim = dip.Sim(prob)
     print(f"config {cid} auto variant: {sim.info}", flush=True)
     tried = 0
-    for variant in (0, 1, 2, 3, 4):
+    for variant in (0, 1, 2, 3, 4, 5, 6, 7):
         for wpb in (0, 1, 4):
             if sim.configure(variant, wpb) != dip.OK:
                 continue
