@@ -48,6 +48,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=1.5,
                     help="wall-time bound of the CPU oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="after timing, run plain device copies of this many MiB (a known-size "
+                         "kernel for scaling HBM byte counters)")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -118,6 +121,15 @@ def main():
     log(f"[bench] {args.steps} steps in {wall * 1e3:.2f} ms; sim kernel avg "
         f"{kern_avg_s * 1e6:.1f} us (min {min(kern_ms) * 1e3:.1f} us); best {best}; "
         f"deadlock {np.mean(flags & 1 > 0):.3f} cap {np.mean(flags & 2 > 0):.3f}")
+
+    if args.calib_copy_mib:
+        nb = args.calib_copy_mib << 20
+        src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copies: 3 x {nb} bytes")
 
     ms_per_step = wall / args.steps * 1e3
     cand_per_s = n_cand * args.steps / wall
