@@ -45,6 +45,7 @@ def main():
     ap.add_argument("--n-cand", type=int, default=0, help="override candidates per batch")
     ap.add_argument("--variant", type=int, default=0)
     ap.add_argument("--wpb", type=int, default=0)
+    ap.add_argument("--slots", type=int, default=0, help="pool slots per rank (pool kernel)")
     ap.add_argument("--cpu-seconds", type=float, default=1.5,
                     help="wall-time bound of the CPU oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -80,6 +81,10 @@ def main():
     torch.cuda.set_device(dev)
     orders = torch.from_numpy(rows).to(dev)
     sim = dip.Sim(prob)
+    if args.slots:
+        rc = sim.configure_pool(args.slots)
+        if rc != dip.OK:
+            raise SystemExit(f"pool slots {args.slots} unsupported: {dip.strerror(rc)}")
     if args.variant or args.wpb:
         rc = sim.configure(args.variant, args.wpb)
         if rc != dip.OK:

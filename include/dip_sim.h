@@ -56,7 +56,7 @@
 extern "C" {
 #endif
 
-#define DIP_SIM_ABI_VERSION 1
+#define DIP_SIM_ABI_VERSION 2
 
 enum {
   DIP_OK = 0,
@@ -121,6 +121,7 @@ typedef struct {
   int32_t lds_bytes;         /* dynamic LDS per block                            */
   int32_t max_blocks;        /* resident blocks the grid is capped at            */
   int64_t scratch_bytes;     /* device scratch owned by the handle               */
+  int32_t pool_slots;        /* variant 8: end-time slots per rank pool, else 0  */
 } dip_sim_info;
 
 /* Host-only checks, no device access: the same checks create / evaluate run
@@ -144,8 +145,20 @@ int dip_sim_create(const dip_topology *topo, dip_sim **out);
  * need every edge latency below 2^16, and all pipeline kernels need the sum
  * of all costs below 2^30, at evaluate time; when the costs do not allow the
  * configured pipeline kernel, evaluate runs the automatically chosen general
- * kernel instead (dip_sim_get_info reports the one that runs). */
+ * kernel instead (dip_sim_get_info reports the one that runs).
+ * Variant 8 (the automatic choice when the topology allows it: every op's
+ * consumers run on one rank, at most 1023 of them, and N < 2^22 - 2): a check
+ * kernel (permutation, peak memory, cap) followed by the pool kernel, which
+ * hands end times between ranks through per-rank pools of a few slots, and by
+ * the variant-4 kernel for the candidates whose pools filled up (results are
+ * the same either way). */
 int dip_sim_configure(dip_sim *h, int32_t variant, int32_t waves_per_block);
+
+/* Variant 8: end-time slots per rank pool, 2, 4, 8 or 16 (0 = automatic, 8).
+ * Fewer slots keep more candidates resident; a candidate whose pools fill up
+ * is re-simulated by the general kernel, so results never depend on it.
+ * DIP_E_UNSUPPORTED if the topology does not fit variant 8. */
+int dip_sim_configure_pool(dip_sim *h, int32_t slots_per_rank);
 
 int dip_sim_get_info(const dip_sim *h, dip_sim_info *info);
 

@@ -24,7 +24,8 @@ FLAG_DEADLOCK, FLAG_CAP, FLAG_INVALID = 1, 2, 4
 NO_KEY = (1 << 64) - 1
 
 EXPORTS = ("dip_sim_abi_version", "dip_sim_check_topology", "dip_sim_check_costs",
-           "dip_sim_create", "dip_sim_configure", "dip_sim_get_info", "dip_sim_evaluate",
+           "dip_sim_create", "dip_sim_configure", "dip_sim_configure_pool", "dip_sim_get_info",
+           "dip_sim_evaluate",
            "dip_sim_argmin", "dip_sim_destroy", "dip_sim_strerror")
 
 
@@ -53,7 +54,7 @@ class Info(ctypes.Structure):
                 ("cand_stride", ctypes.c_int64), ("lanes_per_group", ctypes.c_int32),
                 ("groups_per_wave", ctypes.c_int32), ("waves_per_block", ctypes.c_int32),
                 ("lds_bytes", ctypes.c_int32), ("max_blocks", ctypes.c_int32),
-                ("scratch_bytes", ctypes.c_int64)]
+                ("scratch_bytes", ctypes.c_int64), ("pool_slots", ctypes.c_int32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -75,6 +76,7 @@ def load():
         lib.dip_sim_check_costs.argtypes = [ctypes.POINTER(Topology), ctypes.POINTER(Costs)]
         lib.dip_sim_create.argtypes = [ctypes.POINTER(Topology), ctypes.POINTER(vp)]
         lib.dip_sim_configure.argtypes = [vp, i32, i32]
+        lib.dip_sim_configure_pool.argtypes = [vp, i32]
         lib.dip_sim_get_info.argtypes = [vp, ctypes.POINTER(Info)]
         lib.dip_sim_evaluate.argtypes = [vp, ctypes.POINTER(Costs), vp, i64, vp, vp, vp, vp, vp]
         lib.dip_sim_argmin.argtypes = [vp, vp, vp, i64, i64, vp, vp]
@@ -83,7 +85,8 @@ def load():
         lib.dip_sim_strerror.argtypes = [ctypes.c_int]
         lib.dip_sim_strerror.restype = ctypes.c_char_p
         for name in ("dip_sim_check_topology", "dip_sim_check_costs", "dip_sim_create",
-                     "dip_sim_configure", "dip_sim_get_info", "dip_sim_evaluate",
+                     "dip_sim_configure", "dip_sim_configure_pool", "dip_sim_get_info",
+                     "dip_sim_evaluate",
                      "dip_sim_argmin"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
@@ -157,6 +160,10 @@ def configure(h, variant: int = 0, waves_per_block: int = 0) -> int:
     return load().dip_sim_configure(h, int(variant), int(waves_per_block))
 
 
+def configure_pool(h, slots_per_rank: int = 0) -> int:
+    return load().dip_sim_configure_pool(h, int(slots_per_rank))
+
+
 def get_info(h) -> dict:
     info = Info()
     _check(load().dip_sim_get_info(h, ctypes.byref(info)), "dip_sim_get_info")
@@ -227,6 +234,9 @@ class Sim:
 
     def configure(self, variant=0, waves_per_block=0) -> int:
         return configure(self.h, variant, waves_per_block)
+
+    def configure_pool(self, slots_per_rank=0) -> int:
+        return configure_pool(self.h, slots_per_rank)
 
     @property
     def info(self) -> dict:

@@ -7,7 +7,11 @@
 //   variant 5     pipeline kernel with end-time tables and order rows in LDS,
 //                 op records read through the caches;
 //   variant 6     pipeline kernel with end-time tables in device scratch;
-//   variant 7     as 5, with the op records in LDS too.
+//   variant 7     as 5, with the op records in LDS too;
+//   variant 8     check kernel (permutation, memory) + pool kernel (end times
+//                 handed between ranks through small per-rank slot pools) +
+//                 the general kernel in list mode for candidates whose pools
+//                 filled up.
 // The pipeline kernel needs every op with several predecessors to have them
 // all on one rank, every op to feed at most one such op, and every time
 // below 2^30 (the sum of all costs and latencies bounds every time), so the
@@ -64,6 +68,19 @@ struct dip_sim {
   std::vector<int32_t> join_of;        // [N] join index of an op, -1 if none
   std::vector<int32_t> feeds_join;     // [N] the join op this op feeds, -1 if none
   std::vector<int32_t> feed_edge;      // [N] edge index of that feed
+  std::vector<int32_t> rank_of;        // [N] rank running each op
+  std::vector<int32_t> n_cons;         // [N] consumers of each op
+  bool pool_ok = false;                // topology fits the pool kernel
+  int pool_slots = 8, forced_pool_slots = 0;
+  int4 *d_pool_rec = nullptr;          // pool records [N][2]
+  int4 *d_pool_edge = nullptr;         // pool edges [E]
+  int64_t *d_retry = nullptr;          // candidates re-run by the general kernel
+  uint32_t *d_retry_count = nullptr;
+  int64_t retry_cap = 0;
+  int check_blocks_per_cu = 1;
+  void *d_scratch_fb = nullptr;        // general kernel (list mode) end tables
+  int64_t scratch_fb_bytes = 0;
+  int fb_blocks = 1;
   // device tables
   int4 *d_rec = nullptr;               // general records [N]
   int2 *d_edge = nullptr;              // general edges [E]
@@ -120,12 +137,14 @@ int64_t lds_for(const dip_sim *h, int v, int wpb) {
     const int64_t per_wave = int64_t(h->G) * (int64_t(h->tab_stride) * 4 + h->stride * 2);
     return int64_t(wpb) * per_wave + (v == 7 ? align16(int64_t(h->N) * 16) : 0);
   }
+  if (v == 8) return int64_t(wpb) * h->G * h->P * pool_bytes(h->pool_slots);
   return 0;
 }
 
 const void *kernel_ptr(const dip_sim *h, int v) {
   if (v <= 4) return general_kernel_ptr(v);
   if (v == 6) return pipe_kernel_ptr(h->pwl, true);
+  if (v == 8) return pool_kernel_ptr(h->pwl, h->pool_slots);
   return pipe_lds_kernel_ptr(h->pwl, v == 7);
 }
 
@@ -135,7 +154,8 @@ bool lds16_shape_ok(const dip_sim *h) { return h->pipe_ok && int64_t(h->tab_stri
 
 // Resident blocks per CU for (variant, waves per block); 0 if it does not fit.
 int blocks_per_cu(dip_sim *h, int v, int wpb) {
-  if (v >= 5 && !h->pipe_ok) return 0;
+  if (v >= 5 && v <= 7 && !h->pipe_ok) return 0;
+  if (v == 8 && !h->pool_ok) return 0;
   if ((v == 5 || v == 7) && !lds16_shape_ok(h)) return 0;
   const int64_t lds = lds_for(h, v, wpb);
   if (lds > h->lds_block_max) return 0;
@@ -190,6 +210,57 @@ int ensure_scratch(dip_sim *h, int v, int64_t need) {
   return DIP_OK;
 }
 
+// The pool kernel's fallback: the general kernel with end tables in device
+// scratch (variant 4), one wave per block, in list mode.
+int ensure_fallback(dip_sim *h) {
+  h->fb_blocks = h->n_cu;
+  const int64_t need = int64_t(h->fb_blocks) * h->G * int64_t(h->N) * 4;
+  if (need > h->scratch_fb_bytes) {
+    if (h->d_scratch_fb) {
+      DIP_HIP(hipDeviceSynchronize());
+      DIP_HIP(hipFree(h->d_scratch_fb));
+      h->d_scratch_fb = nullptr;
+    }
+    h->scratch_fb_bytes = 0;
+    if (hipMalloc(&h->d_scratch_fb, size_t(need)) != hipSuccess) {
+      (void)hipGetLastError();
+      return DIP_E_NOMEM;
+    }
+    h->scratch_fb_bytes = need;
+  }
+  int nb = 0;
+  const int64_t lds = 4 * check_lds_per_wave(h->N);
+  if (lds > 65536 && hipFuncSetAttribute(check_kernel_ptr(), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                         int(lds)) != hipSuccess) {
+    (void)hipGetLastError();
+    return DIP_E_UNSUPPORTED;
+  }
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, check_kernel_ptr(), 4 * kWave, size_t(lds)) !=
+          hipSuccess || nb <= 0) {
+    (void)hipGetLastError();
+    return DIP_E_UNSUPPORTED;
+  }
+  h->check_blocks_per_cu = nb;
+  return DIP_OK;
+}
+
+int ensure_retry(dip_sim *h, int64_t n) {
+  if (!h->d_retry_count) DIP_HIP(hipMalloc(&h->d_retry_count, 16));
+  if (n <= h->retry_cap) return DIP_OK;
+  if (h->d_retry) {
+    DIP_HIP(hipDeviceSynchronize());
+    DIP_HIP(hipFree(h->d_retry));
+    h->d_retry = nullptr;
+  }
+  h->retry_cap = 0;
+  if (hipMalloc(&h->d_retry, size_t(n) * 8) != hipSuccess) {
+    (void)hipGetLastError();
+    return DIP_E_NOMEM;
+  }
+  h->retry_cap = n;
+  return DIP_OK;
+}
+
 struct Pick {
   int v = 0, wpb = 0, nb = 0, waves = 0;
 };
@@ -237,7 +308,7 @@ int choose_config(dip_sim *h) {
   if (g.v == 0) return DIP_E_UNSUPPORTED;
   int rc = apply_pick(h, g, &h->gen_variant, &h->gen_wpb, &h->gen_max_blocks, &h->gen_lds);
   if (rc != DIP_OK) return rc;
-  if (force_gen || !h->pipe_ok) {
+  if (force_gen || (!h->pipe_ok && !h->pool_ok)) {
     if (h->forced_variant >= 5) return DIP_E_UNSUPPORTED;
     h->variant = h->gen_variant;
     h->wpb = h->gen_wpb;
@@ -248,6 +319,8 @@ int choose_config(dip_sim *h) {
   Pick p;
   if (h->forced_variant >= 5) {
     p = best_of(h, h->forced_variant, h->forced_variant, h->forced_wpb);
+  } else if (h->pool_ok && best_of(h, 8, 8, h->forced_wpb).v == 8) {
+    p = best_of(h, 8, 8, h->forced_wpb);
   } else {
     // LDS-resident if at least 4 waves stay resident (records in LDS when that
     // keeps as many waves), else tables in device scratch
@@ -258,6 +331,10 @@ int choose_config(dip_sim *h) {
     p = (lds.v && lds.waves >= 4) ? lds : (glob.v ? glob : lds);
   }
   if (p.v == 0) return DIP_E_UNSUPPORTED;
+  if (p.v == 8) {
+    rc = ensure_fallback(h);
+    if (rc != DIP_OK) return rc;
+  }
   return apply_pick(h, p, &h->variant, &h->wpb, &h->max_blocks, &h->lds_bytes);
 }
 
@@ -298,7 +375,7 @@ int check_costs_against(int32_t P, const int32_t *n_ops, const int32_t *pred_ptr
 }
 
 struct StageLayout {
-  int64_t rec, edge, busy, prec, md, rec16, jk, total;
+  int64_t rec, edge, busy, prec, md, rec16, jk, prec8, pedge, total;
 };
 
 StageLayout stage_layout(const dip_sim *h) {
@@ -308,9 +385,11 @@ StageLayout stage_layout(const dip_sim *h) {
   L.edge = off; off += align16(int64_t(std::max(h->E, 1)) * 8);
   L.busy = off; off += align16(int64_t(h->P) * 4);
   L.prec = off; off += h->pipe_ok ? align16(int64_t(h->N) * 32) : 0;
-  L.md = off; off += h->pipe_ok ? align16(int64_t(h->N) * 4) : 0;
+  L.md = off; off += align16(int64_t(h->N) * 4);
   L.rec16 = off; off += h->pipe_ok ? align16(int64_t(h->N) * 16) : 0;
   L.jk = off; off += h->pipe_ok ? align16(int64_t(std::max(h->n_joins, 1)) * 4) : 0;
+  L.prec8 = off; off += h->pool_ok ? align16(int64_t(h->N) * 32) : 0;
+  L.pedge = off; off += h->pool_ok ? align16(int64_t(std::max(h->E, 1)) * 16) : 0;
   L.total = off;
   return L;
 }
@@ -343,12 +422,35 @@ int upload_costs(dip_sim *h, const dip_costs *c, hipStream_t stream) {
   if (h->E > 0)
     DIP_HIP(hipMemcpyAsync(h->d_edge, edge, size_t(h->E) * 8, hipMemcpyHostToDevice, stream));
   DIP_HIP(hipMemcpyAsync(h->d_busy, busy, size_t(h->P) * 4, hipMemcpyHostToDevice, stream));
+  {
+    int32_t *md = reinterpret_cast<int32_t *>(h->h_stage + L.md);
+    for (int32_t g = 0; g < h->N; ++g) md[g] = rec[g].y;
+    DIP_HIP(hipMemcpyAsync(h->d_md, md, size_t(h->N) * 4, hipMemcpyHostToDevice, stream));
+  }
+  if (h->pool_ok) {
+    // pool records {cost, item word, preds, first edge}, {first edge as below};
+    // edges {pred rank, pred tag, comm, 0}; tags are global index + 1
+    int4 *pr = reinterpret_cast<int4 *>(h->h_stage + L.prec8);
+    int4 *pe = reinterpret_cast<int4 *>(h->h_stage + L.pedge);
+    for (int32_t e = 0; e < h->E; ++e) {
+      const int32_t p = h->pred_op[e];
+      pe[e] = make_int4(h->rank_of[p], p + 1, c->edge_comm[e], 0);
+    }
+    for (int32_t g = 0; g < h->N; ++g) {
+      const int32_t b = h->pred_ptr[g], np = h->pred_ptr[g + 1] - b;
+      const uint32_t item = h->n_cons[g] > 0 ? uint32_t(g + 1) | (uint32_t(h->n_cons[g]) << 22) : 0u;
+      pr[2 * g] = make_int4(c->op_cost[g], int32_t(item), np, b);
+      pr[2 * g + 1] = np > 0 ? pe[b] : make_int4(0, 0, 0, 0);
+    }
+    DIP_HIP(hipMemcpyAsync(h->d_pool_rec, pr, size_t(h->N) * 32, hipMemcpyHostToDevice, stream));
+    if (h->E > 0)
+      DIP_HIP(hipMemcpyAsync(h->d_pool_edge, pe, size_t(h->E) * 16, hipMemcpyHostToDevice, stream));
+  }
   h->pipe_costs_ok = false;
   if (h->pipe_ok) {
     // pipeline records: {cost, memdelta, polled entry (byte offset), comm}
     // and {join block fed (byte offset, 0 = none), its k, comm into it}
     int32_t *pr = reinterpret_cast<int32_t *>(h->h_stage + L.prec);
-    int32_t *md = reinterpret_cast<int32_t *>(h->h_stage + L.md);
     for (int32_t g = 0; g < h->N; ++g) {
       int32_t *q = pr + int64_t(g) * 8;
       const int32_t np = h->pred_ptr[g + 1] - h->pred_ptr[g];
@@ -369,10 +471,8 @@ int upload_costs(dip_sim *h, const dip_costs *c, hipStream_t stream) {
       q[5] = o < 0 ? 0 : h->pred_ptr[o + 1] - h->pred_ptr[o];
       q[6] = o < 0 ? 0 : c->edge_comm[h->feed_edge[g]];
       q[7] = 0;
-      md[g] = rec[g].y;
     }
     DIP_HIP(hipMemcpyAsync(h->d_prec, pr, size_t(h->N) * 32, hipMemcpyHostToDevice, stream));
-    DIP_HIP(hipMemcpyAsync(h->d_md, md, size_t(h->N) * 4, hipMemcpyHostToDevice, stream));
     h->pipe_costs_ok = total < int64_t(kValueLimit);
     // compact records: offsets and latencies in 16 bits
     int4 *r16 = reinterpret_cast<int4 *>(h->h_stage + L.rec16);
@@ -410,6 +510,11 @@ void release(dip_sim *h) {
   if (h->d_busy) (void)hipFree(h->d_busy);
   if (h->d_cap) (void)hipFree(h->d_cap);
   if (h->d_scratch_gen) (void)hipFree(h->d_scratch_gen);
+  if (h->d_scratch_fb) (void)hipFree(h->d_scratch_fb);
+  if (h->d_pool_rec) (void)hipFree(h->d_pool_rec);
+  if (h->d_pool_edge) (void)hipFree(h->d_pool_edge);
+  if (h->d_retry) (void)hipFree(h->d_retry);
+  if (h->d_retry_count) (void)hipFree(h->d_retry_count);
   if (h->d_scratch_pipe) (void)hipFree(h->d_scratch_pipe);
   if (h->h_stage) (void)hipHostFree(h->h_stage);
   if (h->stage_done) (void)hipEventDestroy(h->stage_done);
@@ -481,9 +586,23 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
   // pipeline kernel eligibility: the predecessors of a multi-predecessor op
   // run on one rank, and no op feeds two such ops
   {
-    std::vector<int32_t> rank_of(h->N);
+    std::vector<int32_t> &rank_of = h->rank_of;
+    rank_of.assign(h->N, 0);
     for (int r = 0; r < h->P; ++r)
       for (int32_t g = h->rank_off[r]; g < h->rank_off[r + 1]; ++g) rank_of[g] = r;
+    // pool kernel eligibility: the consumers of an op all run on one rank,
+    // at most 1023 of them, and tags (global index + 1) stay below 2^22 - 1
+    h->n_cons.assign(h->N, 0);
+    std::vector<int32_t> cons_rank(h->N, -1);
+    bool pool = int64_t(h->N) + 1 < (int64_t(1) << 22) - 1;
+    for (int32_t g = 0; g < h->N && pool; ++g)
+      for (int32_t k = h->pred_ptr[g]; k < h->pred_ptr[g + 1]; ++k) {
+        const int32_t p = h->pred_op[k];
+        if (cons_rank[p] >= 0 && cons_rank[p] != rank_of[g]) pool = false;
+        cons_rank[p] = rank_of[g];
+        if (++h->n_cons[p] > 1023) pool = false;
+      }
+    h->pool_ok = pool;
     h->join_of.assign(h->N, -1);
     h->feeds_join.assign(h->N, -1);
     h->feed_edge.assign(h->N, -1);
@@ -522,9 +641,14 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
   (void)hipGetLastError();
   if ((e = hipMalloc(&h->d_rec, size_t(h->N) * 16)) != hipSuccess) return hip_fail(e);
   if ((e = hipMalloc(&h->d_edge, size_t(std::max(h->E, 1)) * 8)) != hipSuccess) return hip_fail(e);
+  if ((e = hipMalloc(&h->d_md, size_t(h->N) * 4)) != hipSuccess) return hip_fail(e);
+  if (h->pool_ok) {
+    if ((e = hipMalloc(&h->d_pool_rec, size_t(h->N) * 32)) != hipSuccess) return hip_fail(e);
+    if ((e = hipMalloc(&h->d_pool_edge, size_t(std::max(h->E, 1)) * 16)) != hipSuccess)
+      return hip_fail(e);
+  }
   if (h->pipe_ok) {
     if ((e = hipMalloc(&h->d_prec, size_t(h->N) * 32)) != hipSuccess) return hip_fail(e);
-    if ((e = hipMalloc(&h->d_md, size_t(h->N) * 4)) != hipSuccess) return hip_fail(e);
     if ((e = hipMalloc(&h->d_rec16, size_t(h->N) * 16)) != hipSuccess) return hip_fail(e);
     if ((e = hipMalloc(&h->d_jk, size_t(std::max(h->n_joins, 1)) * 4)) != hipSuccess)
       return hip_fail(e);
@@ -553,7 +677,7 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
 }
 
 int dip_sim_configure(dip_sim *h, int32_t variant, int32_t waves_per_block) {
-  if (!h || variant < 0 || variant > 7) return DIP_E_INVAL;
+  if (!h || variant < 0 || variant > 8) return DIP_E_INVAL;
   if (!(waves_per_block == 0 || waves_per_block == 1 || waves_per_block == 2 ||
         waves_per_block == 4))
     return DIP_E_INVAL;
@@ -564,6 +688,21 @@ int dip_sim_configure(dip_sim *h, int32_t variant, int32_t waves_per_block) {
   if (rc != DIP_OK) {
     h->forced_variant = old_v;
     h->forced_wpb = old_w;
+    (void)choose_config(h);
+  }
+  return rc;
+}
+
+int dip_sim_configure_pool(dip_sim *h, int32_t slots_per_rank) {
+  if (!h || !(slots_per_rank == 0 || pool_slots_ok(slots_per_rank))) return DIP_E_INVAL;
+  if (!h->pool_ok) return DIP_E_UNSUPPORTED;
+  const int old_s = h->pool_slots, old_f = h->forced_pool_slots;
+  h->forced_pool_slots = slots_per_rank;
+  h->pool_slots = slots_per_rank ? slots_per_rank : 8;
+  int rc = choose_config(h);
+  if (rc != DIP_OK) {
+    h->pool_slots = old_s;
+    h->forced_pool_slots = old_f;
     (void)choose_config(h);
   }
   return rc;
@@ -584,7 +723,9 @@ int dip_sim_get_info(const dip_sim *h, dip_sim_info *info) {
   info->waves_per_block = pipe_off ? h->gen_wpb : h->wpb;
   info->lds_bytes = int32_t(pipe_off ? h->gen_lds : h->lds_bytes);
   info->max_blocks = pipe_off ? h->gen_max_blocks : h->max_blocks;
-  info->scratch_bytes = h->scratch_gen_bytes + h->scratch_pipe_bytes;
+  info->scratch_bytes = h->scratch_gen_bytes + h->scratch_pipe_bytes + h->scratch_fb_bytes +
+                        h->retry_cap * 8;
+  info->pool_slots = h->variant == 8 ? h->pool_slots : 0;
   return DIP_OK;
 }
 
@@ -604,6 +745,74 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
   if ((reinterpret_cast<uintptr_t>(out_makespan) | reinterpret_cast<uintptr_t>(out_bubble) |
        reinterpret_cast<uintptr_t>(out_peakmem)) & 3)
     return DIP_E_INVAL;
+
+  if (h->variant == 8) {
+    int rc = ensure_retry(h, n_cand);
+    if (rc != DIP_OK) return rc;
+    CheckArgs c{};
+    c.orders = orders;
+    c.n_cand = n_cand;
+    c.stride = h->stride;
+    c.out_ms = out_makespan;
+    c.out_bub = out_bubble;
+    c.out_peak = out_peakmem;
+    c.out_flags = out_flags;
+    c.md = h->d_md;
+    c.rank_off = h->d_rank_off;
+    c.cap = h->d_cap;
+    c.P = h->P;
+    c.N = h->N;
+    c.wpb = 4;
+    c.retry_count = h->d_retry_count;
+    const int64_t c_lds = 4 * check_lds_per_wave(h->N);
+    const int c_blocks = int(std::min<int64_t>((n_cand + 3) / 4,
+                                               int64_t(h->check_blocks_per_cu) * h->n_cu));
+    DIP_HIP(launch_check(std::max(c_blocks, 1), 4, size_t(c_lds), stream, c));
+
+    PoolArgs a{};
+    a.orders = orders;
+    a.n_cand = n_cand;
+    a.stride = h->stride;
+    a.out_ms = out_makespan;
+    a.out_bub = out_bubble;
+    a.out_flags = out_flags;
+    a.rec = h->d_pool_rec;
+    a.edge = h->d_pool_edge;
+    a.rank_off = h->d_rank_off;
+    a.busy = h->d_busy;
+    a.P = h->P;
+    a.wpb = h->wpb;
+    a.retry = h->d_retry;
+    a.retry_count = h->d_retry_count;
+    const int64_t per_block = int64_t(h->wpb) * h->G;
+    const int blocks = int(std::min<int64_t>((n_cand + per_block - 1) / per_block, h->max_blocks));
+    DIP_HIP(launch_pool(h->pwl, h->pool_slots, blocks, h->wpb, size_t(h->lds_bytes), stream, a));
+
+    GeneralArgs f{};
+    f.orders = orders;
+    f.n_cand = n_cand;
+    f.stride = h->stride;
+    f.out_ms = out_makespan;
+    f.out_bub = out_bubble;
+    f.out_peak = out_peakmem;
+    f.out_flags = out_flags;
+    f.rec = h->d_rec;
+    f.edge = h->d_edge;
+    f.rank_off = h->d_rank_off;
+    f.busy = h->d_busy;
+    f.cap = h->d_cap;
+    f.gends = static_cast<int32_t *>(h->d_scratch_fb);
+    f.P = h->P;
+    f.pwl = h->pwl;
+    f.G = h->G;
+    f.N = h->N;
+    f.E = h->E;
+    f.wpb = 1;
+    f.list = h->d_retry;
+    f.list_count = h->d_retry_count;
+    DIP_HIP(launch_general(4, h->fb_blocks, 1, 0, stream, f));
+    return DIP_OK;
+  }
 
   const bool lds_pipe = (h->variant == 5 || h->variant == 7) && h->lds16_costs_ok;
   const bool pipe = lds_pipe || (h->variant == 6 && h->pipe_costs_ok);

@@ -32,6 +32,9 @@ struct GeneralArgs {
   const int32_t *cap;      // [P]
   int32_t *gends;          // variant 4: [resident waves][G][N]
   int32_t P, pwl, G, N, E, wpb;
+  // list mode (variants 3, 4 only): simulate candidates list[0 .. *list_count-1]
+  const int64_t *list;
+  const uint32_t *list_count;
   uint32_t tab_bytes;      // LDS bytes holding rec + edge (variant 1)
   uint32_t ord_bytes;      // LDS bytes of order rows per wave (variants 1, 2)
   uint32_t end_bytes;      // LDS bytes of end tables per wave (variants 1-3)
@@ -84,6 +87,54 @@ hipError_t launch_pipe(int pwl, bool global_store, int blocks, int wpb, size_t l
 const void *pipe_lds_kernel_ptr(int pwl, bool rec_lds);
 hipError_t launch_pipe_lds(int pwl, bool rec_lds, int blocks, int wpb, size_t lds,
                            hipStream_t s, const PipeArgs &a);
+
+// ---------------------------------------------------------------- check
+// Order-only verdict of each candidate: permutation check, per-rank peak
+// memory, cap flag (one wavefront per candidate, an op-id bitmap in LDS).
+struct CheckArgs {
+  const int16_t *orders;
+  int64_t n_cand;
+  int64_t stride;
+  int32_t *out_ms;
+  int32_t *out_bub;
+  int32_t *out_peak;
+  uint8_t *out_flags;
+  const int32_t *md;        // [N] +act at a forward, -act at a backward
+  const int32_t *rank_off;  // [P+1]
+  const int32_t *cap;       // [P]
+  int32_t P, N, wpb;
+  uint32_t *retry_count;    // zeroed by the kernel when not null
+};
+
+inline int64_t check_lds_per_wave(int32_t N) { return int64_t(((N + 31) / 32 + 3) & ~3) * 4; }
+const void *check_kernel_ptr();
+hipError_t launch_check(int blocks, int wpb, size_t lds, hipStream_t s, const CheckArgs &a);
+
+// ---------------------------------------------------------------- pool
+// Timing simulation with per-rank slot pools holding the end times still to
+// be read (see kern_pool.hip).
+struct PoolArgs {
+  const int16_t *orders;
+  int64_t n_cand;
+  int64_t stride;
+  int32_t *out_ms;
+  int32_t *out_bub;
+  uint8_t *out_flags;       // the check kernel's verdicts, extended here
+  const int4 *rec;          // [N][2] {cost, item word, preds, first edge},
+                            //        {pred rank, pred tag, comm, 0} of the first edge
+  const int4 *edge;         // [E] {pred rank, pred tag, comm, 0}
+  const int32_t *rank_off;  // [P+1]
+  const int32_t *busy;      // [P]
+  int32_t P, wpb;
+  int64_t *retry;           // [n_cand] candidates the pools could not hold
+  uint32_t *retry_count;
+};
+
+inline int64_t pool_bytes(int slots) { return 16 + 8 * int64_t(slots); }
+bool pool_slots_ok(int slots);
+const void *pool_kernel_ptr(int pwl, int slots);
+hipError_t launch_pool(int pwl, int slots, int blocks, int wpb, size_t lds, hipStream_t s,
+                       const PoolArgs &a);
 
 // ---------------------------------------------------------------- argmin
 hipError_t launch_argmin(int blocks, hipStream_t s, const int32_t *ms, const uint8_t *flags,

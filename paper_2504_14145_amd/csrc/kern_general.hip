@@ -122,11 +122,22 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
   }
 
   const int64_t total_waves = int64_t(gridDim.x) * a.wpb;
-  for (int64_t cg = wslot; cg < a.n_groups; cg += total_waves) {
+  int64_t n_items = a.n_cand, n_groups = a.n_groups;
+  if constexpr (V >= 3) {
+    if (a.list) {
+      n_items = int64_t(*a.list_count);
+      n_groups = (n_items + a.G - 1) / a.G;
+    }
+  }
+  for (int64_t cg = wslot; cg < n_groups; cg += total_waves) {
     const int64_t c0 = cg * a.G;
-    const int64_t cand = c0 + grp;
-    const bool live = lane_on && cand < a.n_cand;
-    const int64_t n_here = min<int64_t>(a.G, a.n_cand - c0);
+    const int64_t item = c0 + grp;
+    const bool live = lane_on && item < n_items;
+    int64_t cand = item;
+    if constexpr (V >= 3) {
+      if (a.list) cand = live ? a.list[item] : 0;
+    }
+    const int64_t n_here = min<int64_t>(a.G, n_items - c0);
 
     // ---- stage this wave's order rows (coalesced 16-byte loads) and reset
     //      the end-time tables to "not fired" (-1)

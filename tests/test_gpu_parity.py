@@ -62,6 +62,57 @@ def test_parity_small_all_variants(cid):
     sim.close()
 
 
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
+def test_parity_pool_kernel_slots(cid):
+    """The pool kernel (check + pools + list-mode fallback) at every pool
+    size and block shape; the smallest pools send many candidates through the
+    fallback, the results must not change."""
+    need_gpu()
+    prob = W.make_problem(cid)
+    rows = W.generator_for(prob, cid).generate(0, SMALL[cid])
+    want = O.evaluate(prob, rows, threads=16)
+    sim = dip.Sim(prob)
+    for slots in (2, 4, 8, 16):
+        assert sim.configure_pool(slots) == dip.OK
+        for wpb in (0, 1, 4):
+            assert sim.configure(8, wpb) == dip.OK
+            info = sim.info
+            assert info["variant"] == 8 and info["pool_slots"] == slots
+            print(f"  slots {slots} wpb {wpb}: {info}", flush=True)
+            assert_same(run_gpu(sim, rows), want)
+    sim.close()
+
+
+def test_pool_fallback_when_pools_fill():
+    """Two ranks, three microbatches: rank 0 runs F0 F1 F2 B0 B1 B2 and the
+    last rank runs F2 B2 F1 B1 F0 B0, so rank 0 must hold three end times
+    before rank 1 reads any.  With two slots per pool the pool kernel stalls
+    on it without a deadlock; the candidate goes to the general kernel and the
+    outputs (pre-filled with a sentinel) must still be the oracle's."""
+    need_gpu()
+    prob = W.compile_instance(W.pipeline_instance(2, 3, [[5, 7, 11], [13, 17, 19]], comm=3))
+    row = np.zeros(prob.stride, np.int16)
+    row[:6] = [0, 2, 4, 1, 3, 5]
+    row[6:12] = [4, 5, 2, 3, 0, 1]
+    gpipe = row.copy()
+    gpipe[6:12] = [0, 2, 4, 1, 3, 5]
+    rows = np.stack([row, gpipe, row])
+    want = O.evaluate(prob, rows)
+    assert (want.flags == 0).all()
+    sim = dip.Sim(prob)
+    for slots in (2, 4):
+        assert sim.configure_pool(slots) == dip.OK
+        assert sim.configure(8, 0) == dip.OK
+        orders = torch.from_numpy(rows).to(DEV)
+        out = sim.outputs(len(rows))
+        for t in out:
+            t.fill_(-5 if t.dtype != torch.uint8 else 0x55)
+        dip.evaluate(sim.h, sim.costs, orders, len(rows), *out)
+        torch.cuda.synchronize()
+        assert_same(tuple(t.cpu().numpy() for t in out), want)
+    sim.close()
+
+
 def test_parity_full_bench_workload():
     """The 8-stage VLM workload at its full 65,536 candidates, in the launch
     configuration the benchmark times, compared on every candidate, plus the
