@@ -146,15 +146,15 @@ int dip_sim_create(const dip_topology *topo, dip_sim **out);
  * of all costs below 2^30, at evaluate time; when the costs do not allow the
  * configured pipeline kernel, evaluate runs the automatically chosen general
  * kernel instead (dip_sim_get_info reports the one that runs).
- * Variant 8 (the automatic choice when the topology allows it: every op's
- * consumers run on one rank, at most 1023 of them, and N < 2^22 - 2): a check
+ * Variant 8 (the automatic choice when the topology allows it: at most 255
+ * consumers per op, N < 2^25 - 1 and E < 2^24): a check
  * kernel (permutation, peak memory, cap) followed by the pool kernel, which
  * hands end times between ranks through per-rank pools of a few slots, and by
  * the variant-4 kernel for the candidates whose pools filled up (results are
  * the same either way). */
 int dip_sim_configure(dip_sim *h, int32_t variant, int32_t waves_per_block);
 
-/* Variant 8: end-time slots per rank pool, 2, 4, 8 or 16 (0 = automatic, 8).
+/* Variant 8: end-time slots per rank pool, 4, 8 or 16 (0 = automatic, 8).
  * Fewer slots keep more candidates resident; a candidate whose pools fill up
  * is re-simulated by the general kernel, so results never depend on it.
  * DIP_E_UNSUPPORTED if the topology does not fit variant 8. */

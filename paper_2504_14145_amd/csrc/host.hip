@@ -73,7 +73,7 @@ struct dip_sim {
   bool pool_ok = false;                // topology fits the pool kernel
   int pool_slots = 8, forced_pool_slots = 0;
   int4 *d_pool_rec = nullptr;          // pool records [N][2]
-  int4 *d_pool_edge = nullptr;         // pool edges [E]
+  int2 *d_pool_edge = nullptr;         // pool edges [E]
   int64_t *d_retry = nullptr;          // candidates re-run by the general kernel
   uint32_t *d_retry_count = nullptr;
   int64_t retry_cap = 0;
@@ -229,14 +229,17 @@ int ensure_fallback(dip_sim *h) {
     h->scratch_fb_bytes = need;
   }
   int nb = 0;
-  const int64_t lds = 4 * check_lds_per_wave(h->N);
-  if (lds > 65536 && hipFuncSetAttribute(check_kernel_ptr(), hipFuncAttributeMaxDynamicSharedMemorySize,
+  const int64_t lds = 4 * h->G * check_lds_per_group(h->N);
+  if (lds > h->lds_block_max) return DIP_E_UNSUPPORTED;
+  if (lds > 65536 && hipFuncSetAttribute(check_kernel_ptr(h->pwl),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize,
                                          int(lds)) != hipSuccess) {
     (void)hipGetLastError();
     return DIP_E_UNSUPPORTED;
   }
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, check_kernel_ptr(), 4 * kWave, size_t(lds)) !=
-          hipSuccess || nb <= 0) {
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, check_kernel_ptr(h->pwl), 4 * kWave,
+                                                   size_t(lds)) != hipSuccess ||
+      nb <= 0) {
     (void)hipGetLastError();
     return DIP_E_UNSUPPORTED;
   }
@@ -389,7 +392,7 @@ StageLayout stage_layout(const dip_sim *h) {
   L.rec16 = off; off += h->pipe_ok ? align16(int64_t(h->N) * 16) : 0;
   L.jk = off; off += h->pipe_ok ? align16(int64_t(std::max(h->n_joins, 1)) * 4) : 0;
   L.prec8 = off; off += h->pool_ok ? align16(int64_t(h->N) * 32) : 0;
-  L.pedge = off; off += h->pool_ok ? align16(int64_t(std::max(h->E, 1)) * 16) : 0;
+  L.pedge = off; off += h->pool_ok ? align16(int64_t(std::max(h->E, 1)) * 8) : 0;
   L.total = off;
   return L;
 }
@@ -428,23 +431,26 @@ int upload_costs(dip_sim *h, const dip_costs *c, hipStream_t stream) {
     DIP_HIP(hipMemcpyAsync(h->d_md, md, size_t(h->N) * 4, hipMemcpyHostToDevice, stream));
   }
   if (h->pool_ok) {
-    // pool records {cost, item word, preds, first edge}, {first edge as below};
-    // edges {pred rank, pred tag, comm, 0}; tags are global index + 1
+    // pool records {cost, item tag or 0, preds, first edge | readers << 24},
+    // {first edge word, comm}; edges {pred tag | pred rank << 25 | fan-out
+    // bit, comm}; tags are global index + 1
     int4 *pr = reinterpret_cast<int4 *>(h->h_stage + L.prec8);
-    int4 *pe = reinterpret_cast<int4 *>(h->h_stage + L.pedge);
+    int2 *pe = reinterpret_cast<int2 *>(h->h_stage + L.pedge);
     for (int32_t e = 0; e < h->E; ++e) {
       const int32_t p = h->pred_op[e];
-      pe[e] = make_int4(h->rank_of[p], p + 1, c->edge_comm[e], 0);
+      const uint32_t w = uint32_t(p + 1) | (uint32_t(h->rank_of[p]) << kEdgeRankShift) |
+                         (h->n_cons[p] > 1 ? kEdgeFanOut : 0u);
+      pe[e] = make_int2(int32_t(w), c->edge_comm[e]);
     }
     for (int32_t g = 0; g < h->N; ++g) {
       const int32_t b = h->pred_ptr[g], np = h->pred_ptr[g + 1] - b;
-      const uint32_t item = h->n_cons[g] > 0 ? uint32_t(g + 1) | (uint32_t(h->n_cons[g]) << 22) : 0u;
-      pr[2 * g] = make_int4(c->op_cost[g], int32_t(item), np, b);
-      pr[2 * g + 1] = np > 0 ? pe[b] : make_int4(0, 0, 0, 0);
+      const int32_t tag = h->n_cons[g] > 0 ? g + 1 : 0;
+      pr[2 * g] = make_int4(c->op_cost[g], tag, np, int32_t(uint32_t(b) | (uint32_t(h->n_cons[g]) << 24)));
+      pr[2 * g + 1] = np > 0 ? make_int4(pe[b].x, pe[b].y, 0, 0) : make_int4(0, 0, 0, 0);
     }
     DIP_HIP(hipMemcpyAsync(h->d_pool_rec, pr, size_t(h->N) * 32, hipMemcpyHostToDevice, stream));
     if (h->E > 0)
-      DIP_HIP(hipMemcpyAsync(h->d_pool_edge, pe, size_t(h->E) * 16, hipMemcpyHostToDevice, stream));
+      DIP_HIP(hipMemcpyAsync(h->d_pool_edge, pe, size_t(h->E) * 8, hipMemcpyHostToDevice, stream));
   }
   h->pipe_costs_ok = false;
   if (h->pipe_ok) {
@@ -590,18 +596,14 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
     rank_of.assign(h->N, 0);
     for (int r = 0; r < h->P; ++r)
       for (int32_t g = h->rank_off[r]; g < h->rank_off[r + 1]; ++g) rank_of[g] = r;
-    // pool kernel eligibility: the consumers of an op all run on one rank,
-    // at most 1023 of them, and tags (global index + 1) stay below 2^22 - 1
+    // pool kernel eligibility: tags (global index + 1) below 2^25, at most
+    // 255 consumers per op, edge indices below 2^24
     h->n_cons.assign(h->N, 0);
-    std::vector<int32_t> cons_rank(h->N, -1);
-    bool pool = int64_t(h->N) + 1 < (int64_t(1) << 22) - 1;
+    bool pool = int64_t(h->N) + 1 < (int64_t(1) << 25) && h->E < (1 << 24) &&
+                int64_t(h->N) * 32 < INT32_MAX;
     for (int32_t g = 0; g < h->N && pool; ++g)
-      for (int32_t k = h->pred_ptr[g]; k < h->pred_ptr[g + 1]; ++k) {
-        const int32_t p = h->pred_op[k];
-        if (cons_rank[p] >= 0 && cons_rank[p] != rank_of[g]) pool = false;
-        cons_rank[p] = rank_of[g];
-        if (++h->n_cons[p] > 1023) pool = false;
-      }
+      for (int32_t k = h->pred_ptr[g]; k < h->pred_ptr[g + 1]; ++k)
+        if (++h->n_cons[h->pred_op[k]] > 255) pool = false;
     h->pool_ok = pool;
     h->join_of.assign(h->N, -1);
     h->feeds_join.assign(h->N, -1);
@@ -644,7 +646,7 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
   if ((e = hipMalloc(&h->d_md, size_t(h->N) * 4)) != hipSuccess) return hip_fail(e);
   if (h->pool_ok) {
     if ((e = hipMalloc(&h->d_pool_rec, size_t(h->N) * 32)) != hipSuccess) return hip_fail(e);
-    if ((e = hipMalloc(&h->d_pool_edge, size_t(std::max(h->E, 1)) * 16)) != hipSuccess)
+    if ((e = hipMalloc(&h->d_pool_edge, size_t(std::max(h->E, 1)) * 8)) != hipSuccess)
       return hip_fail(e);
   }
   if (h->pipe_ok) {
@@ -764,10 +766,11 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     c.N = h->N;
     c.wpb = 4;
     c.retry_count = h->d_retry_count;
-    const int64_t c_lds = 4 * check_lds_per_wave(h->N);
-    const int c_blocks = int(std::min<int64_t>((n_cand + 3) / 4,
+    const int64_t c_lds = 4 * h->G * check_lds_per_group(h->N);
+    const int64_t c_per_block = 4 * int64_t(h->G);
+    const int c_blocks = int(std::min<int64_t>((n_cand + c_per_block - 1) / c_per_block,
                                                int64_t(h->check_blocks_per_cu) * h->n_cu));
-    DIP_HIP(launch_check(std::max(c_blocks, 1), 4, size_t(c_lds), stream, c));
+    DIP_HIP(launch_check(h->pwl, std::max(c_blocks, 1), 4, size_t(c_lds), stream, c));
 
     PoolArgs a{};
     a.orders = orders;
@@ -784,6 +787,9 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     a.wpb = h->wpb;
     a.retry = h->d_retry;
     a.retry_count = h->d_retry_count;
+    a.rec_bytes = h->N * 32;
+    a.edge_bytes = std::max(h->E, 1) * 8;
+    a.round_limit = uint32_t(h->N) + uint32_t(h->E) + 16u;
     const int64_t per_block = int64_t(h->wpb) * h->G;
     const int blocks = int(std::min<int64_t>((n_cand + per_block - 1) / per_block, h->max_blocks));
     DIP_HIP(launch_pool(h->pwl, h->pool_slots, blocks, h->wpb, size_t(h->lds_bytes), stream, a));

@@ -90,7 +90,8 @@ hipError_t launch_pipe_lds(int pwl, bool rec_lds, int blocks, int wpb, size_t ld
 
 // ---------------------------------------------------------------- check
 // Order-only verdict of each candidate: permutation check, per-rank peak
-// memory, cap flag (one wavefront per candidate, an op-id bitmap in LDS).
+// memory, cap flag (lane r of a group walks rank r's section; an op-id bitmap
+// per candidate in LDS).
 struct CheckArgs {
   const int16_t *orders;
   int64_t n_cand;
@@ -106,9 +107,11 @@ struct CheckArgs {
   uint32_t *retry_count;    // zeroed by the kernel when not null
 };
 
-inline int64_t check_lds_per_wave(int32_t N) { return int64_t(((N + 31) / 32 + 3) & ~3) * 4; }
-const void *check_kernel_ptr();
-hipError_t launch_check(int blocks, int wpb, size_t lds, hipStream_t s, const CheckArgs &a);
+// bytes of one candidate's op-id bitmap
+__host__ __device__ inline int64_t check_lds_per_group(int32_t N) { return int64_t(((N + 31) / 32 + 3) & ~3) * 4; }
+const void *check_kernel_ptr(int pwl);
+hipError_t launch_check(int pwl, int blocks, int wpb, size_t lds, hipStream_t s,
+                        const CheckArgs &a);
 
 // ---------------------------------------------------------------- pool
 // Timing simulation with per-rank slot pools holding the end times still to
@@ -120,17 +123,32 @@ struct PoolArgs {
   int32_t *out_ms;
   int32_t *out_bub;
   uint8_t *out_flags;       // the check kernel's verdicts, extended here
-  const int4 *rec;          // [N][2] {cost, item word, preds, first edge},
-                            //        {pred rank, pred tag, comm, 0} of the first edge
-  const int4 *edge;         // [E] {pred rank, pred tag, comm, 0}
+  const int4 *rec;          // [N][2] {cost, item tag or 0, preds, first edge | readers << 24},
+                            //        {first edge word, its comm, 0, 0}
+  const int2 *edge;         // [E] {edge word, comm}
   const int32_t *rank_off;  // [P+1]
   const int32_t *busy;      // [P]
   int32_t P, wpb;
   int64_t *retry;           // [n_cand] candidates the pools could not hold
   uint32_t *retry_count;
+  int32_t rec_bytes, edge_bytes;  // sizes of rec and edge (buffer descriptors)
+  uint32_t round_limit;           // rounds a candidate may take (N + E + 16)
 };
 
-inline int64_t pool_bytes(int slots) { return 16 + 8 * int64_t(slots); }
+// dword 3 of a raw buffer descriptor on CDNA
+constexpr int kBufferWord3 = 0x00020000;
+
+// edge word: predecessor tag (global index + 1) | its rank << 25 | bit 31 if
+// the predecessor has several consumers
+constexpr uint32_t kEdgeTagMask = (1u << 25) - 1u;
+constexpr uint32_t kEdgeRankShift = 25;
+constexpr uint32_t kEdgeFanOut = 1u << 31;
+
+// pool of S slots: head (freed mask, one reader-count byte per slot), S tags, S ends
+__host__ __device__ constexpr int64_t pool_head_bytes(int slots) { return slots <= 12 ? 16 : 32; }
+__host__ __device__ constexpr int64_t pool_bytes(int slots) {
+  return pool_head_bytes(slots) + 8 * int64_t(slots);
+}
 bool pool_slots_ok(int slots);
 const void *pool_kernel_ptr(int pwl, int slots);
 hipError_t launch_pool(int pwl, int slots, int blocks, int wpb, size_t lds, hipStream_t s,

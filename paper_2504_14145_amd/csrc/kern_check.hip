@@ -10,10 +10,11 @@
 //     forward to its backward (Sec. 5.3), which depends on the order only;
 //   * the cap flag: some rank's peak exceeds its cap.
 //
-// One wavefront per candidate.  A rank section is read 64 ids at a time
-// (coalesced 128-byte loads); duplicates are caught with an atomic OR into a
-// bitmap of all op ids in the wave's LDS, and the running sum is a wave
-// prefix scan carried from chunk to chunk.
+// Same layout as the simulation: G = 64 / PW candidates per wavefront, lane r
+// of a group walks rank r's section, eight ids per step (their loads, the
+// duplicate checks and the memory-delta loads each issued together).
+// Duplicates are caught by an atomic OR into the group's bitmap of all op
+// ids in LDS.
 #include "dip_sim.h"
 #include "dev_util.h"
 #include "internal.h"
@@ -23,77 +24,101 @@ namespace {
 
 extern __shared__ __align__(16) unsigned char c_lds[];
 
+template <int PWL>
 __global__ __launch_bounds__(256) void check_kernel(CheckArgs a) {
+  constexpr int PW = 1 << PWL;
+  constexpr int G = kWave / PW;
+  constexpr int U = 8;
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
-  const int bm_words = (a.N + 31) / 32;
-  uint32_t *bm = reinterpret_cast<uint32_t *>(c_lds) + wave * ((bm_words + 3) & ~3);
+  const int grp = lane >> PWL;
+  const int r = lane & (PW - 1);
+  const bool on = r < a.P;
+  const int gbit = grp << PWL;
+  const int wpg = int(check_lds_per_group(a.N) / 4);
+  uint32_t *bm = reinterpret_cast<uint32_t *>(c_lds) + (wave * G + grp) * wpg;
   if (a.retry_count && blockIdx.x == 0 && threadIdx.x == 0) *a.retry_count = 0u;
 
-  int cap_l = -1, rb_l = 0;
-  if (lane < a.P) {
-    cap_l = a.cap[lane];
-    rb_l = a.rank_off[lane];
+  int rb = 0, nr = 0, cap_r = -1;
+  if (on) {
+    rb = a.rank_off[r];
+    nr = a.rank_off[r + 1] - rb;
+    cap_r = a.cap[r];
   }
-  const int64_t n_waves = int64_t(gridDim.x) * a.wpb;
-  for (int64_t cand = int64_t(blockIdx.x) * a.wpb + wave; cand < a.n_cand; cand += n_waves) {
-    for (int i = lane; i < bm_words; i += kWave) bm[i] = 0u;
+  const int64_t n_slots = int64_t(gridDim.x) * a.wpb * G;
+  for (int64_t base = (int64_t(blockIdx.x) * a.wpb + wave) * G; base < a.n_cand; base += n_slots) {
+    const int64_t cand = base + grp;
+    const bool live = cand < a.n_cand;
+    for (int i = r; i < wpg; i += PW) bm[i] = 0u;
     bool bad = false;
-    int my_peak = 0;
-    const int16_t *row = a.orders + cand * a.stride;
-    for (int r = 0; r < a.P; ++r) {
-      const int rb = __shfl(rb_l, r, kWave);
-      const int n = a.rank_off[r + 1] - rb;
-      int carry = 0, run_max = 0;
-      for (int i0 = 0; i0 < n; i0 += kWave) {
-        const int i = i0 + lane;
-        const bool live = i < n;
-        const int id = live ? int(row[rb + i]) : 0;
-        const bool ok = live && unsigned(id) < unsigned(n);
-        const int g = rb + (ok ? id : 0);
-        int d = 0;
-        if (ok) {
-          const uint32_t bit = 1u << (g & 31);
-          const uint32_t old = atomicOr(bm + (g >> 5), bit);
-          bad = bad || (old & bit) != 0u;
-          d = a.md[g];
-        }
-        bad = bad || (live && !ok);
-        // inclusive prefix sum of the memory deltas over the 64 lanes
-        int x = d;
+    int mem = 0, peak = 0;
+    if (live && on) {
+      const int16_t *row = a.orders + cand * a.stride + rb;
+      for (int i0 = 0; i0 < nr; i0 += U) {
+        int id[U];
 #pragma unroll
-        for (int off = 1; off < kWave; off <<= 1) {
-          const int y = __shfl_up(x, off, kWave);
-          if (lane >= off) x += y;
+        for (int k = 0; k < U; ++k) id[k] = i0 + k < nr ? int(row[i0 + k]) : 0;
+        int d[U];
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+          const bool ok = unsigned(id[k]) < unsigned(nr);
+          bad = bad || !ok;
+          const int g = rb + (ok ? id[k] : 0);
+          d[k] = 0;
+          if (ok && i0 + k < nr) {
+            const uint32_t bit = 1u << (g & 31);
+            const uint32_t old = atomicOr(bm + (g >> 5), bit);
+            bad = bad || (old & bit) != 0u;
+            d[k] = a.md[g];
+          }
         }
-        x += carry;
-        if (live) run_max = max(run_max, x);
-        carry = __shfl(x, kWave - 1, kWave);
+#pragma unroll
+        for (int k = 0; k < U; ++k) {
+          mem += d[k];
+          peak = max(peak, mem);
+        }
       }
-#pragma unroll
-      for (int off = 1; off < kWave; off <<= 1) run_max = max(run_max, __shfl_xor(run_max, off, kWave));
-      if (lane == r) my_peak = run_max;
     }
-    const bool invalid = __builtin_amdgcn_ballot_w64(bad) != 0ull;
-    const bool over = lane < a.P && cap_l >= 0 && my_peak > cap_l;
-    const bool capped = __builtin_amdgcn_ballot_w64(over) != 0ull;
-    if (lane < a.P) {
-      a.out_peak[cand * a.P + lane] = invalid ? -1 : my_peak;
-      if (invalid) a.out_bub[cand * a.P + lane] = -1;
-    }
-    if (lane == 0) {
-      a.out_flags[cand] = invalid ? uint8_t(DIP_FLAG_INVALID) : uint8_t(capped ? DIP_FLAG_CAP : 0u);
-      if (invalid) a.out_ms[cand] = -1;
+    const bool g_bad = (any_in_group<PWL>(__builtin_amdgcn_ballot_w64(bad)) >> gbit) & 1;
+    const bool over = live && on && cap_r >= 0 && peak > cap_r;
+    const bool g_cap = (any_in_group<PWL>(__builtin_amdgcn_ballot_w64(over)) >> gbit) & 1;
+    if (live && on) {
+      a.out_peak[cand * a.P + r] = g_bad ? -1 : peak;
+      if (g_bad) a.out_bub[cand * a.P + r] = -1;
+      if (r == 0) {
+        a.out_flags[cand] = g_bad ? uint8_t(DIP_FLAG_INVALID) : uint8_t(g_cap ? DIP_FLAG_CAP : 0u);
+        if (g_bad) a.out_ms[cand] = -1;
+      }
     }
   }
 }
 
 }  // namespace
 
-const void *check_kernel_ptr() { return reinterpret_cast<const void *>(check_kernel); }
+const void *check_kernel_ptr(int pwl) {
+  switch (pwl) {
+    case 0: return reinterpret_cast<const void *>(check_kernel<0>);
+    case 1: return reinterpret_cast<const void *>(check_kernel<1>);
+    case 2: return reinterpret_cast<const void *>(check_kernel<2>);
+    case 3: return reinterpret_cast<const void *>(check_kernel<3>);
+    case 4: return reinterpret_cast<const void *>(check_kernel<4>);
+    case 5: return reinterpret_cast<const void *>(check_kernel<5>);
+    default: return reinterpret_cast<const void *>(check_kernel<6>);
+  }
+}
 
-hipError_t launch_check(int blocks, int wpb, size_t lds, hipStream_t s, const CheckArgs &a) {
-  check_kernel<<<dim3(blocks), dim3(wpb * kWave), lds, s>>>(a);
+hipError_t launch_check(int pwl, int blocks, int wpb, size_t lds, hipStream_t s,
+                        const CheckArgs &a) {
+  const dim3 grid(blocks), block(wpb * kWave);
+  switch (pwl) {
+    case 0: check_kernel<0><<<grid, block, lds, s>>>(a); break;
+    case 1: check_kernel<1><<<grid, block, lds, s>>>(a); break;
+    case 2: check_kernel<2><<<grid, block, lds, s>>>(a); break;
+    case 3: check_kernel<3><<<grid, block, lds, s>>>(a); break;
+    case 4: check_kernel<4><<<grid, block, lds, s>>>(a); break;
+    case 5: check_kernel<5><<<grid, block, lds, s>>>(a); break;
+    default: check_kernel<6><<<grid, block, lds, s>>>(a); break;
+  }
   return hipGetLastError();
 }
 

@@ -10,25 +10,27 @@
 // next power of two >= P); lane r of a group plays rank r.  Each round every
 // lane looks at the next op of its order.  Ranks hand end times to each other
 // through "items": the end time of an op that has consumers, tagged with the
-// op's global index + 1 and with the number of consumers that still have to
-// read it.  An op's item lives in a small pool of S slots owned by the rank
-// that ran the op:
+// op's global index + 1.  An op's item lives in a small pool of S slots owned
+// by the rank that ran the op:
 //
-//     pool (16 + 8 S bytes):  freed mask | 12 bytes pad | S x {tag word, end}
-//     tag word: bits 0-21 item tag, bits 22-31 readers left
+//     head (16 bytes, 32 for S = 16): freed mask, then one byte per slot
+//                                     counting the readers still to come
+//     tags (4 S bytes), ends (4 S bytes)
 //
-// A consumer scans the S slots of its predecessor's pool for the tag (one
-// predecessor per round), folds end + comm into a running maximum, and then
-// either decrements the readers left or, as the last reader, releases the slot
-// by setting its bit in the owner's freed mask (an LDS atomic OR).  The owner
-// reads its freed mask every round, forgets released slots (clearing the bits
-// it saw with an atomic AND) and writes each new item into a free slot.  A
-// rank whose op has consumers but whose pool is full waits: back-pressure.
+// A consumer compares its predecessor's tag with the S tags of that rank's
+// pool (one predecessor per round), reads the matching end, folds end + comm
+// into a running maximum, and releases the slot by setting its bit in the
+// owner's freed mask (an LDS atomic OR) -- for an item with several readers,
+// only the reader that takes its count to zero (an LDS atomic subtract) does.
+// The owner reads its freed mask every round, forgets released slots (clearing
+// the bits it saw with an atomic AND) and writes each new item into a free
+// slot.  A rank whose op has consumers but whose pool is full waits:
+// back-pressure.
 //
 // Only a few items are live at a time (an item dies once its consumers ran),
-// so a candidate needs P pools of a few hundred bytes, where a table of end
-// times by op would need 4 bytes per op: many more candidates stay resident
-// per CU, which is what hides the LDS and cache latencies of the round loop.
+// so a candidate needs P pools of under 150 bytes, where a table of end times
+// by op would need 4 bytes per op: many more candidates stay resident per CU,
+// which is what hides the LDS and cache latencies of the round loop.
 //
 // Verdicts: a group is done when all of its lanes ran their whole order.  A
 // round in which no lane of a group fired an op or read an item leaves its
@@ -47,11 +49,6 @@ namespace {
 
 extern __shared__ __align__(16) unsigned char p_lds[];
 
-constexpr uint32_t kTagBits = 22;
-constexpr uint32_t kTagMask = (1u << kTagBits) - 1u;
-constexpr uint32_t kOneReader = 1u << kTagBits;
-constexpr uint32_t kNoTag = kTagMask;  // never an item's tag: matches nothing
-
 __device__ __forceinline__ uint32_t ld32(uint32_t addr) {
   return *reinterpret_cast<const uint32_t *>(p_lds + addr);
 }
@@ -61,9 +58,7 @@ __device__ __forceinline__ uint4 ld128(uint32_t addr) {
 __device__ __forceinline__ void st32(uint32_t addr, uint32_t v) {
   *reinterpret_cast<uint32_t *>(p_lds + addr) = v;
 }
-__device__ __forceinline__ void st64(uint32_t addr, uint32_t lo, uint32_t hi) {
-  *reinterpret_cast<uint2 *>(p_lds + addr) = make_uint2(lo, hi);
-}
+__device__ __forceinline__ void st8(uint32_t addr, uint32_t v) { p_lds[addr] = uint8_t(v); }
 __device__ __forceinline__ uint32_t *lds_word(uint32_t addr) {
   return reinterpret_cast<uint32_t *>(__builtin_assume_aligned(p_lds + addr, 4));
 }
@@ -73,13 +68,19 @@ __device__ __forceinline__ void lds_or(uint32_t addr, uint32_t v) {
 __device__ __forceinline__ void lds_and(uint32_t addr, uint32_t v) {
   (void)__hip_atomic_fetch_and(lds_word(addr), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
 }
+__device__ __forceinline__ uint32_t lds_sub_rtn(uint32_t addr, uint32_t v) {
+  return __hip_atomic_fetch_sub(lds_word(addr), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+}
 
 template <int PWL, int S>
 __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   constexpr int PW = 1 << PWL;
   constexpr int G = kWave / PW;
-  constexpr uint32_t kPool = 16u + 8u * S;
-  constexpr uint32_t kFull = S == 32 ? 0xffffffffu : ((1u << S) - 1u);
+  constexpr uint32_t kTags = uint32_t(pool_head_bytes(S));
+  constexpr uint32_t kEnds = kTags + 4u * S;
+  constexpr uint32_t kPool = uint32_t(pool_bytes(S));
+  constexpr uint32_t kFull = (1u << S) - 1u;
+  static_assert(S >= 4 && S <= 16 && (S & (S - 1)) == 0, "pool size");
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int grp = lane >> PWL;
@@ -99,32 +100,65 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   const int last = max(nr - 1, 0);
 
   int64_t cand = (int64_t(blockIdx.x) * a.wpb + wave) * G + grp;
+  uint32_t rnd = 0;          // rounds so far
+  uint32_t cand_round = 0;   // round at which the group took its candidate
   bool has = false;   // the group holds a candidate
   bool act = false;   // this lane has an op to run
   uint8_t fl = 0;     // the check kernel's flags for the candidate
   int ptr = 0;
   uint32_t tfree = 0, acc = 0, mine = 0;
   int j = 0;
-  int4 cur = make_int4(0, 0, 0, 0);               // {cost, item word, preds, first edge}
-  int4 ce = make_int4(0, int(kNoTag), 0, 0);      // current edge {pred rank, tag, comm, 0}
-  int4 n0 = cur, n1 = ce;                         // record of the op at ptr + 1
-  int nid2 = 0;                                   // id at ptr + 2
-  const int16_t *row = a.orders;
-
-  auto load_rec = [&](int id, int4 &r0, int4 &r1) {
-    const int4 *p = a.rec + 2 * int64_t(rb + id);
-    r0 = p[0];
-    r1 = p[1];
+  // no predecessor to wait for: a tag no item carries (items are tagged
+  // global index + 1 <= N < kEdgeTagMask; free slots hold 0 or a dead tag)
+  const int2 no_edge = make_int2(int(kEdgeTagMask), 0);
+  // record {cost, item tag (0: no consumers), preds, first edge | readers << 24}
+  int4 cur = make_int4(0, 0, 0, 0);
+  int2 ce = no_edge;                      // current edge {pred edge word, comm}
+  int4 n0 = cur;                          // record of the op at ptr + 1 ...
+  int2 n1 = no_edge;                      // ... and its first edge
+  int id2 = 0;                            // id at ptr + 2
+  const int16_t *row0 = a.orders;         // this candidate's row
+  auto clamp_id = [&](int id) { return min(max(id, 0), last); };
+  // records and edges through buffer descriptors: 32-bit byte offsets, and a
+  // read past the end returns zeros instead of faulting
+  const __amdgpu_buffer_rsrc_t rec_rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<int4 *>(a.rec), 0, a.rec_bytes, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t edge_rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<int2 *>(a.edge), 0, a.edge_bytes, kBufferWord3);
+  auto rec_lo = [&](int g) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(rec_rs, uint32_t(g) * 32u, 0, 0);
+    return make_int4(int(v[0]), int(v[1]), int(v[2]), int(v[3]));
   };
+  auto rec_hi = [&](int g) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(rec_rs, uint32_t(g) * 32u + 16u, 0, 0);
+    return make_int2(int(v[0]), int(v[1]));
+  };
+  auto edge_at = [&](uint32_t e) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(edge_rs, e * 8u, 0, 0);
+    return make_int2(int(v[0]), int(v[1]));
+  };
+
+  // Global loads are staged: every round every lane issues the same loads
+  // into the staging registers below (lanes with nothing to fetch read one
+  // shared line), and only the next round moves what was fetched into place,
+  // so no round waits for a load it issued itself.
+  int4 s0 = n0;
+  int2 s1 = n1, se = no_edge;
+  uint32_t s2 = 0;   // the aligned 32-bit word holding the next id ...
+  int s2_hi = 0;     // ... in its upper half
+  bool take_rec = false, take_edge = false;
 
   // All lanes of the group call this together.
   auto start_candidate = [&]() {
     while (cand < a.n_cand && (a.out_flags[cand] & DIP_FLAG_INVALID)) cand += n_slots;
     has = cand < a.n_cand;
     act = false;
-    ce.y = int(kNoTag);
+    ce = no_edge;
+    take_rec = false;
+    take_edge = false;
     if (!has) return;
     fl = a.out_flags[cand];
+    cand_round = rnd;
     if (on) {
       uint4 *p = reinterpret_cast<uint4 *>(p_lds + my_pool);
 #pragma unroll
@@ -136,47 +170,65 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     mine = 0;
     j = 0;
     if (on && nr > 0) {
-      row = a.orders + cand * a.stride + rb;
-      const int id0 = min(max(int(row[0]), 0), last);
-      const int id1 = min(max(int(row[min(1, last)]), 0), last);
-      nid2 = min(max(int(row[min(2, last)]), 0), last);
-      int4 c1;
-      load_rec(id0, cur, c1);
-      load_rec(id1, n0, n1);
-      ce = cur.z > 0 ? c1 : make_int4(0, int(kNoTag), 0, 0);
+      row0 = a.orders + cand * a.stride;
+      const int16_t *row = row0 + rb;
+      const int id0 = clamp_id(row[0]);
+      const int id1 = clamp_id(row[min(1, last)]);
+      id2 = row[min(2, last)];
+      cur = rec_lo(rb + id0);
+      const int2 c1 = rec_hi(rb + id0);
+      n0 = rec_lo(rb + id1);
+      n1 = rec_hi(rb + id1);
+      ce = cur.z > 0 ? c1 : no_edge;
       act = true;
     }
   };
 
   start_candidate();
   uint64_t g_has = any_in_group<PWL>(__builtin_amdgcn_ballot_w64(has));
-  uint32_t round = 0;
 
   while (g_has) {
-    // ---- reads: the predecessor's pool, my freed mask
-    const uint32_t pa = gbase + uint32_t(ce.x) * kPool;
-    uint4 q[S / 2];
-#pragma unroll
-    for (int i = 0; i < S / 2; ++i) q[i] = ld128(pa + 16u + 16u * i);
-    const uint32_t fw = ld32(my_pool);
-    lds_wait();
+    // ---- what the previous round fetched
+    if (take_rec) {
+      n0 = s0;
+      n1 = s1;
+      id2 = int(int16_t(s2_hi ? (s2 >> 16) : (s2 & 0xffffu)));
+    }
+    if (take_edge) ce = se;
+    asm volatile("" : "+v"(n0.x), "+v"(n0.y), "+v"(n0.z), "+v"(n0.w), "+v"(n1.x), "+v"(n1.y),
+                 "+v"(id2), "+v"(ce.x), "+v"(ce.y)::"memory");
 
-    const uint32_t want = uint32_t(ce.y);
-    bool found = false;
-    uint32_t hit_t = 0, hit_v = 0, hit = 0;
+    // ---- reads: the tags of the predecessor's pool, my freed mask
+    const uint32_t want = uint32_t(ce.x) & kEdgeTagMask;
+    const uint32_t pa = gbase + ((uint32_t(ce.x) >> kEdgeRankShift) & 63u) * kPool;
+    uint4 q[S / 4];
+#pragma unroll
+    for (int i = 0; i < S / 4; ++i) q[i] = ld128(pa + kTags + 16u * i);
+    const uint32_t fw = ld32(my_pool);
+    // prefetch the op's next edge (taken if this round finds the current one)
+    {
+      const bool more = act && j + 1 < cur.z;
+      se = edge_at(more ? uint32_t(cur.w & 0xffffff) + j + 1 : 0u);
+    }
+
+    // the matching slot, as index bits
+    bool found = false, b0 = false, b1 = false, b2 = false, b3 = false;
 #pragma unroll
     for (int i = 0; i < S; ++i) {
-      const uint32_t t = (i & 1) ? q[i / 2].z : q[i / 2].x;
-      const uint32_t v = (i & 1) ? q[i / 2].w : q[i / 2].y;
-      const bool m = (t & kTagMask) == want;
+      const uint4 w = q[i / 4];
+      const uint32_t t = (i & 3) == 0 ? w.x : (i & 3) == 1 ? w.y : (i & 3) == 2 ? w.z : w.w;
+      const bool m = t == want;
       found = found || m;
-      hit_t = m ? t : hit_t;
-      hit_v = m ? v : hit_v;
-      hit = m ? uint32_t(i) : hit;
+      if (i & 1) b0 = b0 || m;
+      if (i & 2) b1 = b1 || m;
+      if (i & 4) b2 = b2 || m;
+      if (i & 8) b3 = b3 || m;
     }
+    const uint32_t hit = (b0 ? 1u : 0u) | (b1 ? 2u : 0u) | (b2 ? 4u : 0u) | (b3 ? 8u : 0u);
+    const uint32_t hit_v = ld32(pa + kEnds + 4u * hit);
     mine &= ~fw;
     const uint32_t free_m = ~mine & kFull;
-    const uint32_t acc_n = found ? max(acc, hit_v + uint32_t(ce.z)) : acc;
+    const uint32_t acc_n = found ? max(acc, hit_v + uint32_t(ce.y)) : acc;
     const int j_n = j + (found ? 1 : 0);
     const bool ready = act && j_n >= cur.z;
     const bool need_out = cur.y != 0;
@@ -186,49 +238,74 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
 
     // ---- writes
     if (found) {
-      if ((hit_t >> kTagBits) == 1u) lds_or(pa, 1u << hit);   // last reader frees
-      else st32(pa + 16u + 8u * hit, hit_t - kOneReader);
+      bool last_reader = true;
+      if (uint32_t(ce.x) & kEdgeFanOut) {
+        const uint32_t byte = 4u + hit;
+        const uint32_t sh = 8u * (byte & 3u);
+        const uint32_t old = lds_sub_rtn(pa + (byte & ~3u), 1u << sh);
+        last_reader = ((old >> sh) & 0xffu) == 1u;
+      }
+      if (last_reader) lds_or(pa, 1u << hit);
     }
     if (on && fw != 0u) lds_and(my_pool, ~fw);
     if (fire && need_out) {
       const uint32_t s = uint32_t(__builtin_ctz(free_m));
-      st64(my_pool + 16u + 8u * s, uint32_t(cur.y), en);
+      const uint32_t readers = uint32_t(cur.w) >> 24;
+      if (readers > 1u) st8(my_pool + 4u + s, readers);
+      st32(my_pool + kEnds + 4u * s, en);
+      st32(my_pool + kTags + 4u * s, uint32_t(cur.y));
       mine |= 1u << s;
     }
 
     // ---- register state
     bool fin = false;
+    bool adv = false;
+    take_edge = false;
     if (fire) {
       tfree = en;
       acc = 0;
       j = 0;
       ++ptr;
       fin = ptr == nr;
-      if (fin) {
-        act = false;
-        ce = make_int4(0, int(kNoTag), 0, 0);
-      } else {
-        cur = n0;
-        ce = cur.z > 0 ? n1 : make_int4(0, int(kNoTag), 0, 0);
-        load_rec(nid2, n0, n1);
-        nid2 = min(max(int(row[min(ptr + 2, last)]), 0), last);
-      }
+      act = !fin;
+      adv = !fin;
+      ce = (adv && n0.z > 0) ? n1 : no_edge;
+      if (adv) cur = n0;
     } else if (found) {
       acc = acc_n;
       j = j_n;
-      ce = j_n < cur.z ? a.edge[cur.w + j_n] : make_int4(0, int(kNoTag), 0, 0);
+      take_edge = j_n < cur.z;
+      if (!take_edge) ce = no_edge;
+    }
+    // fetch, for an advance, the record of the op after the new current one
+    // and the id after that
+    take_rec = adv;
+    {
+      const int g = adv ? rb + clamp_id(id2) : 0;
+      s0 = rec_lo(g);
+      s1 = rec_hi(g);
+      // ids are read as aligned 32-bit words (rows are 16-byte aligned)
+      const int pos = rb + min(ptr + 2, last);
+      s2_hi = adv ? (pos & 1) : 0;
+      s2 = *reinterpret_cast<const uint32_t *>(adv ? row0 + (pos & ~1) : a.orders);
     }
 
-    ++round;
+    ++rnd;
     const uint64_t b_fin = __builtin_amdgcn_ballot_w64(fin);
-    const bool stall_check = (round & 7u) == 0u;
+    const bool stall_check = (rnd & 7u) == 0u;
     if (!b_fin && !stall_check) continue;
     const uint64_t g_run = any_in_group<PWL>(__builtin_amdgcn_ballot_w64(act));
     const uint64_t ev_done = g_has & ~g_run;
-    uint64_t ev_stall = 0;
-    if (stall_check)
+    uint64_t ev_stall = 0, ev_over = 0;
+    if (stall_check) {
       ev_stall = g_run & ~any_in_group<PWL>(__builtin_amdgcn_ballot_w64(fire || found));
-    const uint64_t ev = ev_done | ev_stall;
+      // every round of a running group fires an op or reads an item, at most
+      // N + E of them per candidate; a group past that bound is handed to the
+      // general kernel rather than left running
+      ev_over = g_run & ~ev_stall &
+                any_in_group<PWL>(__builtin_amdgcn_ballot_w64(has && rnd - cand_round > a.round_limit));
+    }
+    const uint64_t ev = ev_done | ev_stall | ev_over;
     if (ev == 0) continue;
 
     // ---- some groups finished their candidate
@@ -236,7 +313,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     const bool mine_ev = (ev >> gbit) & 1;
     if (mine_ev) {
       const bool stalled = (ev_stall >> gbit) & 1;
-      const bool retry = stalled && ((g_held >> gbit) & 1);
+      const bool retry = (stalled && ((g_held >> gbit) & 1)) || ((ev_over >> gbit) & 1);
       uint32_t T = on ? tfree : 0u;
 #pragma unroll
       for (int off = 1; off < PW; off <<= 1) T = max(T, uint32_t(__shfl_xor(int(T), off, kWave)));
@@ -287,11 +364,10 @@ void launch_s(int pwl, dim3 grid, dim3 block, size_t lds, hipStream_t s, const P
 
 }  // namespace
 
-bool pool_slots_ok(int slots) { return slots == 2 || slots == 4 || slots == 8 || slots == 16; }
+bool pool_slots_ok(int slots) { return slots == 4 || slots == 8 || slots == 16; }
 
 const void *pool_kernel_ptr(int pwl, int slots) {
   switch (slots) {
-    case 2: return ptr_s<2>(pwl);
     case 4: return ptr_s<4>(pwl);
     case 16: return ptr_s<16>(pwl);
     default: return ptr_s<8>(pwl);
@@ -302,7 +378,6 @@ hipError_t launch_pool(int pwl, int slots, int blocks, int wpb, size_t lds, hipS
                        const PoolArgs &a) {
   const dim3 grid(blocks), block(wpb * kWave);
   switch (slots) {
-    case 2: launch_s<2>(pwl, grid, block, lds, s, a); break;
     case 4: launch_s<4>(pwl, grid, block, lds, s, a); break;
     case 16: launch_s<16>(pwl, grid, block, lds, s, a); break;
     default: launch_s<8>(pwl, grid, block, lds, s, a); break;

@@ -72,7 +72,7 @@ def test_parity_pool_kernel_slots(cid):
     rows = W.generator_for(prob, cid).generate(0, SMALL[cid])
     want = O.evaluate(prob, rows, threads=16)
     sim = dip.Sim(prob)
-    for slots in (2, 4, 8, 16):
+    for slots in (4, 8, 16):
         assert sim.configure_pool(slots) == dip.OK
         for wpb in (0, 1, 4):
             assert sim.configure(8, wpb) == dip.OK
@@ -84,23 +84,25 @@ def test_parity_pool_kernel_slots(cid):
 
 
 def test_pool_fallback_when_pools_fill():
-    """Two ranks, three microbatches: rank 0 runs F0 F1 F2 B0 B1 B2 and the
-    last rank runs F2 B2 F1 B1 F0 B0, so rank 0 must hold three end times
-    before rank 1 reads any.  With two slots per pool the pool kernel stalls
+    """Two ranks, five microbatches: rank 0 runs F0..F4 then B0..B4 and the
+    last rank runs F4 B4 F3 B3 ... F0 B0, so rank 0 must hold five end times
+    before rank 1 reads any.  With four slots per pool the pool kernel stalls
     on it without a deadlock; the candidate goes to the general kernel and the
     outputs (pre-filled with a sentinel) must still be the oracle's."""
     need_gpu()
-    prob = W.compile_instance(W.pipeline_instance(2, 3, [[5, 7, 11], [13, 17, 19]], comm=3))
+    M = 5
+    prob = W.compile_instance(W.pipeline_instance(2, M, [[5, 7, 11, 13, 2], [13, 17, 19, 3, 4]],
+                                                  comm=3))
     row = np.zeros(prob.stride, np.int16)
-    row[:6] = [0, 2, 4, 1, 3, 5]
-    row[6:12] = [4, 5, 2, 3, 0, 1]
+    row[:2 * M] = [2 * u for u in range(M)] + [2 * u + 1 for u in range(M)]
+    row[2 * M:4 * M] = [x for u in reversed(range(M)) for x in (2 * u, 2 * u + 1)]
     gpipe = row.copy()
-    gpipe[6:12] = [0, 2, 4, 1, 3, 5]
+    gpipe[2 * M:4 * M] = row[:2 * M]
     rows = np.stack([row, gpipe, row])
     want = O.evaluate(prob, rows)
     assert (want.flags == 0).all()
     sim = dip.Sim(prob)
-    for slots in (2, 4):
+    for slots in (4, 8):
         assert sim.configure_pool(slots) == dip.OK
         assert sim.configure(8, 0) == dip.OK
         orders = torch.from_numpy(rows).to(DEV)
