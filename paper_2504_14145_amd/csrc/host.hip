@@ -432,14 +432,13 @@ int upload_costs(dip_sim *h, const dip_costs *c, hipStream_t stream) {
   }
   if (h->pool_ok) {
     // pool records {cost, item tag or 0, preds, first edge | readers << 24},
-    // {first edge word, comm}; edges {pred tag | pred rank << 25 | fan-out
-    // bit, comm}; tags are global index + 1
+    // {first edge word, comm}; edges {pred tag | pred rank << 25, comm}; tags
+    // are global index + 1
     int4 *pr = reinterpret_cast<int4 *>(h->h_stage + L.prec8);
     int2 *pe = reinterpret_cast<int2 *>(h->h_stage + L.pedge);
     for (int32_t e = 0; e < h->E; ++e) {
       const int32_t p = h->pred_op[e];
-      const uint32_t w = uint32_t(p + 1) | (uint32_t(h->rank_of[p]) << kEdgeRankShift) |
-                         (h->n_cons[p] > 1 ? kEdgeFanOut : 0u);
+      const uint32_t w = uint32_t(p + 1) | (uint32_t(h->rank_of[p]) << kEdgeRankShift);
       pe[e] = make_int2(int32_t(w), c->edge_comm[e]);
     }
     for (int32_t g = 0; g < h->N; ++g) {

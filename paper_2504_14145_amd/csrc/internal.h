@@ -138,14 +138,12 @@ struct PoolArgs {
 // dword 3 of a raw buffer descriptor on CDNA
 constexpr int kBufferWord3 = 0x00020000;
 
-// edge word: predecessor tag (global index + 1) | its rank << 25 | bit 31 if
-// the predecessor has several consumers
+// edge word: predecessor tag (global index + 1) | its rank << 25
 constexpr uint32_t kEdgeTagMask = (1u << 25) - 1u;
 constexpr uint32_t kEdgeRankShift = 25;
-constexpr uint32_t kEdgeFanOut = 1u << 31;
 
-// pool of S slots: head (freed mask, one reader-count byte per slot), S tags, S ends
-__host__ __device__ constexpr int64_t pool_head_bytes(int slots) { return slots <= 12 ? 16 : 32; }
+// pool of S <= 16 slots: 16 bytes of reader counts (one byte per slot), S tags, S ends
+__host__ __device__ constexpr int64_t pool_head_bytes(int) { return 16; }
 __host__ __device__ constexpr int64_t pool_bytes(int slots) {
   return pool_head_bytes(slots) + 8 * int64_t(slots);
 }

@@ -11,7 +11,7 @@
 //   * the cap flag: some rank's peak exceeds its cap.
 //
 // Same layout as the simulation: G = 64 / PW candidates per wavefront, lane r
-// of a group walks rank r's section, eight ids per step (their loads, the
+// of a group walks rank r's section, sixteen ids per step (their loads, the
 // duplicate checks and the memory-delta loads each issued together).
 // Duplicates are caught by an atomic OR into the group's bitmap of all op
 // ids in LDS.
@@ -28,7 +28,7 @@ template <int PWL>
 __global__ __launch_bounds__(256) void check_kernel(CheckArgs a) {
   constexpr int PW = 1 << PWL;
   constexpr int G = kWave / PW;
-  constexpr int U = 8;
+  constexpr int U = 16;
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
   const int grp = lane >> PWL;
@@ -52,28 +52,30 @@ __global__ __launch_bounds__(256) void check_kernel(CheckArgs a) {
     for (int i = r; i < wpg; i += PW) bm[i] = 0u;
     bool bad = false;
     int mem = 0, peak = 0;
-    if (live && on) {
+    if (live && on && nr > 0) {
+      // branch-free steps: every id load, bitmap OR and delta load of a step
+      // is issued before any result is used
       const int16_t *row = a.orders + cand * a.stride + rb;
       for (int i0 = 0; i0 < nr; i0 += U) {
         int id[U];
 #pragma unroll
-        for (int k = 0; k < U; ++k) id[k] = i0 + k < nr ? int(row[i0 + k]) : 0;
+        for (int k = 0; k < U; ++k) id[k] = row[min(i0 + k, nr - 1)];
+        uint32_t old[U], bit[U];
         int d[U];
 #pragma unroll
         for (int k = 0; k < U; ++k) {
+          const bool in = i0 + k < nr;
           const bool ok = unsigned(id[k]) < unsigned(nr);
-          bad = bad || !ok;
+          bad = bad || (in && !ok);
           const int g = rb + (ok ? id[k] : 0);
-          d[k] = 0;
-          if (ok && i0 + k < nr) {
-            const uint32_t bit = 1u << (g & 31);
-            const uint32_t old = atomicOr(bm + (g >> 5), bit);
-            bad = bad || (old & bit) != 0u;
-            d[k] = a.md[g];
-          }
+          bit[k] = (in && ok) ? 1u << (g & 31) : 0u;
+          old[k] = atomicOr(bm + (g >> 5), bit[k]);
+          d[k] = a.md[g];
+          d[k] = (in && ok) ? d[k] : 0;
         }
 #pragma unroll
         for (int k = 0; k < U; ++k) {
+          bad = bad || (old[k] & bit[k]) != 0u;
           mem += d[k];
           peak = max(peak, mem);
         }

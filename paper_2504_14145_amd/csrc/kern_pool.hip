@@ -13,18 +13,15 @@
 // op's global index + 1.  An op's item lives in a small pool of S slots owned
 // by the rank that ran the op:
 //
-//     head (16 bytes, 32 for S = 16): freed mask, then one byte per slot
-//                                     counting the readers still to come
+//     counts (16 bytes): per slot, the readers still to come (0 = free)
 //     tags (4 S bytes), ends (4 S bytes)
 //
 // A consumer compares its predecessor's tag with the S tags of that rank's
 // pool (one predecessor per round), reads the matching end, folds end + comm
-// into a running maximum, and releases the slot by setting its bit in the
-// owner's freed mask (an LDS atomic OR) -- for an item with several readers,
-// only the reader that takes its count to zero (an LDS atomic subtract) does.
-// The owner reads its freed mask every round, forgets released slots (clearing
-// the bits it saw with an atomic AND) and writes each new item into a free
-// slot.  A rank whose op has consumers but whose pool is full waits:
+// into a running maximum, and decrements the slot's reader count (an LDS
+// atomic subtract on its byte).  The owner reads its counts every round and
+// writes each new item, with its number of readers, into a slot whose count
+// is zero.  A rank whose op has consumers but whose pool is full waits:
 // back-pressure.
 //
 // Only a few items are live at a time (an item dies once its consumers ran),
@@ -62,14 +59,8 @@ __device__ __forceinline__ void st8(uint32_t addr, uint32_t v) { p_lds[addr] = u
 __device__ __forceinline__ uint32_t *lds_word(uint32_t addr) {
   return reinterpret_cast<uint32_t *>(__builtin_assume_aligned(p_lds + addr, 4));
 }
-__device__ __forceinline__ void lds_or(uint32_t addr, uint32_t v) {
-  (void)__hip_atomic_fetch_or(lds_word(addr), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
-}
-__device__ __forceinline__ void lds_and(uint32_t addr, uint32_t v) {
-  (void)__hip_atomic_fetch_and(lds_word(addr), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
-}
-__device__ __forceinline__ uint32_t lds_sub_rtn(uint32_t addr, uint32_t v) {
-  return __hip_atomic_fetch_sub(lds_word(addr), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+__device__ __forceinline__ void lds_sub(uint32_t addr, uint32_t v) {
+  (void)__hip_atomic_fetch_sub(lds_word(addr), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
 }
 
 template <int PWL, int S>
@@ -79,7 +70,6 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   constexpr uint32_t kTags = uint32_t(pool_head_bytes(S));
   constexpr uint32_t kEnds = kTags + 4u * S;
   constexpr uint32_t kPool = uint32_t(pool_bytes(S));
-  constexpr uint32_t kFull = (1u << S) - 1u;
   static_assert(S >= 4 && S <= 16 && (S & (S - 1)) == 0, "pool size");
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
@@ -106,7 +96,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   bool act = false;   // this lane has an op to run
   uint8_t fl = 0;     // the check kernel's flags for the candidate
   int ptr = 0;
-  uint32_t tfree = 0, acc = 0, mine = 0;
+  uint32_t tfree = 0, acc = 0;
   int j = 0;
   // no predecessor to wait for: a tag no item carries (items are tagged
   // global index + 1 <= N < kEdgeTagMask; free slots hold 0 or a dead tag)
@@ -167,7 +157,6 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     ptr = 0;
     tfree = 0;
     acc = 0;
-    mine = 0;
     j = 0;
     if (on && nr > 0) {
       row0 = a.orders + cand * a.stride;
@@ -198,13 +187,15 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     asm volatile("" : "+v"(n0.x), "+v"(n0.y), "+v"(n0.z), "+v"(n0.w), "+v"(n1.x), "+v"(n1.y),
                  "+v"(id2), "+v"(ce.x), "+v"(ce.y)::"memory");
 
-    // ---- reads: the tags of the predecessor's pool, my freed mask
+    // ---- reads: the tags of the predecessor's pool, my reader counts
     const uint32_t want = uint32_t(ce.x) & kEdgeTagMask;
     const uint32_t pa = gbase + ((uint32_t(ce.x) >> kEdgeRankShift) & 63u) * kPool;
     uint4 q[S / 4];
 #pragma unroll
     for (int i = 0; i < S / 4; ++i) q[i] = ld128(pa + kTags + 16u * i);
-    const uint32_t fw = ld32(my_pool);
+    uint32_t cnt[S / 4];
+#pragma unroll
+    for (int i = 0; i < S / 4; ++i) cnt[i] = ld32(my_pool + 4u * i);
     // prefetch the op's next edge (taken if this round finds the current one)
     {
       const bool more = act && j + 1 < cur.z;
@@ -226,35 +217,29 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     }
     const uint32_t hit = (b0 ? 1u : 0u) | (b1 ? 2u : 0u) | (b2 ? 4u : 0u) | (b3 ? 8u : 0u);
     const uint32_t hit_v = ld32(pa + kEnds + 4u * hit);
-    mine &= ~fw;
-    const uint32_t free_m = ~mine & kFull;
+    // a slot is free when its reader count is zero: the first such slot
+    int free_s = -1;
+#pragma unroll
+    for (int i = S / 4 - 1; i >= 0; --i) {
+      const uint32_t w = cnt[i];
+      const uint32_t z = ~(((w & 0x7f7f7f7fu) + 0x7f7f7f7fu) | w | 0x7f7f7f7fu);   // 0x80 in zero bytes
+      free_s = z ? int(4 * i) + int(__builtin_ctz(z) >> 3) : free_s;
+    }
     const uint32_t acc_n = found ? max(acc, hit_v + uint32_t(ce.y)) : acc;
     const int j_n = j + (found ? 1 : 0);
     const bool ready = act && j_n >= cur.z;
     const bool need_out = cur.y != 0;
-    const bool fire = ready && (!need_out || free_m != 0u);
+    const bool fire = ready && (!need_out || free_s >= 0);
     const bool held = ready && !fire;
     const uint32_t en = max(tfree, acc_n) + uint32_t(cur.x);
 
-    // ---- writes
-    if (found) {
-      bool last_reader = true;
-      if (uint32_t(ce.x) & kEdgeFanOut) {
-        const uint32_t byte = 4u + hit;
-        const uint32_t sh = 8u * (byte & 3u);
-        const uint32_t old = lds_sub_rtn(pa + (byte & ~3u), 1u << sh);
-        last_reader = ((old >> sh) & 0xffu) == 1u;
-      }
-      if (last_reader) lds_or(pa, 1u << hit);
-    }
-    if (on && fw != 0u) lds_and(my_pool, ~fw);
+    // ---- writes: release what was read, publish what was produced
+    if (found) lds_sub(pa + (hit & ~3u), 1u << (8u * (hit & 3u)));
     if (fire && need_out) {
-      const uint32_t s = uint32_t(__builtin_ctz(free_m));
-      const uint32_t readers = uint32_t(cur.w) >> 24;
-      if (readers > 1u) st8(my_pool + 4u + s, readers);
-      st32(my_pool + kEnds + 4u * s, en);
-      st32(my_pool + kTags + 4u * s, uint32_t(cur.y));
-      mine |= 1u << s;
+      const uint32_t sl = uint32_t(free_s);
+      st8(my_pool + sl, uint32_t(cur.w) >> 24);
+      st32(my_pool + kEnds + 4u * sl, en);
+      st32(my_pool + kTags + 4u * sl, uint32_t(cur.y));
     }
 
     // ---- register state
