@@ -10,18 +10,24 @@ Default workload: the 8-rank vision-language instance (ViT on ranks 0-1, LLM
 on ranks 2-7, 32 samples), 65,536 candidates per batch.
 
 Prints one JSON line.  Besides the throughput it carries
-  roofline      the simulation kernel's algorithmic HBM bytes per launch
-                (2 bytes per order entry read + the outputs written) over its
-                average launch time from HIP events on the launch stream,
-                against the 8 TB/s HBM peak;
+  roofline      the dominant kernel's (the timing simulation's) algorithmic
+                HBM bytes per launch -- 2 bytes per order entry read + the
+                outputs written -- over its average launch time, from HIP
+                events the library records on the launch stream around each
+                kernel, against the 8 TB/s HBM peak; "traffic" is the HBM
+                bytes per launch measured with rocprofv3 counters for the same
+                kernel source (a summary under profiles/ keyed by the source
+                hash), null when the source changed since;
   cpu_baseline  the CPU oracle timed on this host on a bounded sample of the
                 same workload.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -30,6 +36,30 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pool_kernel_traffic.md")
+POOL_SOURCES = [os.path.join(ROOT, "paper_2504_14145_amd", "csrc", f)
+                for f in ("kern_pool.hip", "internal.h", "dev_util.h")]
+
+
+def pool_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in POOL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str, n_cand: int, slots: int):
+    """HBM bytes per pool-kernel launch from the committed counter summary,
+    if it was taken on this kernel source, workload, batch and pool size."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    want = f"{pool_source_hash()} {workload} {n_cand} {slots}"
+    for line in open(TRAFFIC_FILE):
+        m = re.match(r"\s*traffic:\s*(\S+ \S+ \d+ \d+)\s+fetch_bytes=(\d+)\s+write_bytes=(\d+)", line)
+        if m and m.group(1) == want:
+            return int(m.group(2)) + int(m.group(3))
+    return None
 
 
 def log(msg):
@@ -49,6 +79,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=1.5,
                     help="wall-time bound of the CPU oracle baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-steps", type=int, default=10,
+                    help="steps re-run after the timed region with per-kernel events")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, run plain device copies of this many MiB (a known-size "
                          "kernel for scaling HBM byte counters)")
@@ -127,6 +159,21 @@ def main():
         f"{kern_avg_s * 1e6:.1f} us (min {min(kern_ms) * 1e3:.1f} us); best {best}; "
         f"deadlock {np.mean(flags & 1 > 0):.3f} cap {np.mean(flags & 2 > 0):.3f}")
 
+    # per-kernel times: the library records HIP events around each kernel on
+    # the launch stream
+    dip.profile(sim.h, True)
+    per_kernel = []
+    for _ in range(max(1, args.profile_steps)):
+        step()
+        per_kernel.append(dip.last_profile(sim.h))
+    dip.profile(sim.h, False)
+    nk = min(len(p) for p in per_kernel)
+    kern_avg_ms = [sum(p[i] for p in per_kernel) / len(per_kernel) for i in range(nk)]
+    names = (["check", "simulate", "retry"] if info["variant"] == 8 else ["simulate"])[:nk]
+    dom = names.index("simulate")
+    dom_s = kern_avg_ms[dom] / 1e3
+    log(f"[bench] per-kernel avg ms: " + ", ".join(f"{n} {t:.4f}" for n, t in zip(names, kern_avg_ms)))
+
     if args.calib_copy_mib:
         nb = args.calib_copy_mib << 20
         src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
@@ -141,7 +188,10 @@ def main():
     ops_per_s = cand_per_s * prob.n_total
     P = prob.n_ranks
     bytes_per_cand = 2 * prob.n_total + 4 + 4 * P + 4 * P + 1
-    achieved_gbs = n_cand * bytes_per_cand / kern_avg_s / 1e9
+    algo_bytes = n_cand * bytes_per_cand
+    achieved_gbs = algo_bytes / dom_s / 1e9
+    slots = info.get("pool_slots", 0)
+    traffic = measured_traffic(cfg.name, n_cand, slots) if info["variant"] == 8 else None
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -179,11 +229,14 @@ def main():
                    "ops_per_candidate": prob.n_total, "microbatches": cfg.samples,
                    "parallelism": "single GPU"},
         "ops_per_s": ops_per_s,
-        "sim_kernel_us": kern_avg_s * 1e6,
+        "evaluate_us": kern_avg_s * 1e6,
+        "kernel_us": {n: t * 1e3 for n, t in zip(names, kern_avg_ms)},
         "kernel_variant": info["variant"],
+        "pool_slots": slots,
         "best": {"index": best[0], "makespan_us": best[1]},
-        "roofline": {"bound": "hbm", "achieved": achieved_gbs, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved_gbs / HBM_PEAK_GBS, "traffic": None},
+        "roofline": {"bound": "hbm", "kernel": "simulate", "achieved": achieved_gbs,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved_gbs / HBM_PEAK_GBS,
+                     "traffic": traffic, "algorithmic_bytes": algo_bytes},
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)

@@ -189,6 +189,15 @@ int dip_sim_argmin(dip_sim *h, const int32_t *makespan, const uint8_t *flags,
                    int64_t n_cand, int64_t index_base, uint64_t *inout_best_key,
                    void *stream);
 
+/* Per-kernel timing of evaluate (for measurement).  With enable != 0, each
+ * later evaluate records HIP events on its stream around each kernel it
+ * launches; dip_sim_last_profile then waits for the last of them and writes
+ * the kernel times in milliseconds, in launch order, to out_ms[0 .. *n_out-1]
+ * (n_out <= 3: variant 8 launches the check, pool and retry kernels, the
+ * others one kernel).  *n_out = 0 if the last evaluate recorded nothing. */
+int dip_sim_profile(dip_sim *h, int32_t enable);
+int dip_sim_last_profile(dip_sim *h, float *out_ms, int32_t *n_out);
+
 /* Release the handle's device memory.  Waits for the device first. */
 void dip_sim_destroy(dip_sim *h);
 

@@ -25,7 +25,7 @@ NO_KEY = (1 << 64) - 1
 
 EXPORTS = ("dip_sim_abi_version", "dip_sim_check_topology", "dip_sim_check_costs",
            "dip_sim_create", "dip_sim_configure", "dip_sim_configure_pool", "dip_sim_get_info",
-           "dip_sim_evaluate",
+           "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
            "dip_sim_argmin", "dip_sim_destroy", "dip_sim_strerror")
 
 
@@ -77,6 +77,8 @@ def load():
         lib.dip_sim_create.argtypes = [ctypes.POINTER(Topology), ctypes.POINTER(vp)]
         lib.dip_sim_configure.argtypes = [vp, i32, i32]
         lib.dip_sim_configure_pool.argtypes = [vp, i32]
+        lib.dip_sim_profile.argtypes = [vp, i32]
+        lib.dip_sim_last_profile.argtypes = [vp, vp, vp]
         lib.dip_sim_get_info.argtypes = [vp, ctypes.POINTER(Info)]
         lib.dip_sim_evaluate.argtypes = [vp, ctypes.POINTER(Costs), vp, i64, vp, vp, vp, vp, vp]
         lib.dip_sim_argmin.argtypes = [vp, vp, vp, i64, i64, vp, vp]
@@ -86,7 +88,7 @@ def load():
         lib.dip_sim_strerror.restype = ctypes.c_char_p
         for name in ("dip_sim_check_topology", "dip_sim_check_costs", "dip_sim_create",
                      "dip_sim_configure", "dip_sim_configure_pool", "dip_sim_get_info",
-                     "dip_sim_evaluate",
+                     "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
                      "dip_sim_argmin"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
@@ -162,6 +164,18 @@ def configure(h, variant: int = 0, waves_per_block: int = 0) -> int:
 
 def configure_pool(h, slots_per_rank: int = 0) -> int:
     return load().dip_sim_configure_pool(h, int(slots_per_rank))
+
+
+def profile(h, enable: bool = True) -> int:
+    return load().dip_sim_profile(h, int(bool(enable)))
+
+
+def last_profile(h) -> list:
+    """Kernel times (ms) of the last evaluate, in launch order."""
+    buf = (ctypes.c_float * 4)()
+    n = ctypes.c_int32(0)
+    _check(load().dip_sim_last_profile(h, buf, ctypes.byref(n)), "dip_sim_last_profile")
+    return [float(buf[i]) for i in range(n.value)]
 
 
 def get_info(h) -> dict:

@@ -98,6 +98,10 @@ struct dip_sim {
   unsigned char *h_stage = nullptr;
   int64_t stage_bytes = 0;
   hipEvent_t stage_done = nullptr;
+  // optional per-kernel timing of evaluate: events before each kernel and after the last
+  bool profile = false;
+  hipEvent_t prof_ev[4] = {nullptr, nullptr, nullptr, nullptr};
+  int prof_n = 0;                      // events recorded by the last evaluate
   bool stage_pending = false;
   bool costs_set = false;
   // launch configuration of the chosen variant
@@ -523,6 +527,8 @@ void release(dip_sim *h) {
   if (h->d_scratch_pipe) (void)hipFree(h->d_scratch_pipe);
   if (h->h_stage) (void)hipHostFree(h->h_stage);
   if (h->stage_done) (void)hipEventDestroy(h->stage_done);
+  for (hipEvent_t &ev : h->prof_ev)
+    if (ev) (void)hipEventDestroy(ev);
   delete h;
 }
 
@@ -747,9 +753,16 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
        reinterpret_cast<uintptr_t>(out_peakmem)) & 3)
     return DIP_E_INVAL;
 
+  h->prof_n = 0;
+  auto mark = [&](int i) -> hipError_t {
+    if (!h->profile) return hipSuccess;
+    h->prof_n = i + 1;
+    return hipEventRecord(h->prof_ev[i], stream);
+  };
   if (h->variant == 8) {
     int rc = ensure_retry(h, n_cand);
     if (rc != DIP_OK) return rc;
+    DIP_HIP(mark(0));
     CheckArgs c{};
     c.orders = orders;
     c.n_cand = n_cand;
@@ -770,6 +783,7 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     const int c_blocks = int(std::min<int64_t>((n_cand + c_per_block - 1) / c_per_block,
                                                int64_t(h->check_blocks_per_cu) * h->n_cu));
     DIP_HIP(launch_check(h->pwl, std::max(c_blocks, 1), 4, size_t(c_lds), stream, c));
+    DIP_HIP(mark(1));
 
     PoolArgs a{};
     a.orders = orders;
@@ -792,6 +806,7 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     const int64_t per_block = int64_t(h->wpb) * h->G;
     const int blocks = int(std::min<int64_t>((n_cand + per_block - 1) / per_block, h->max_blocks));
     DIP_HIP(launch_pool(h->pwl, h->pool_slots, blocks, h->wpb, size_t(h->lds_bytes), stream, a));
+    DIP_HIP(mark(2));
 
     GeneralArgs f{};
     f.orders = orders;
@@ -816,6 +831,7 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     f.list = h->d_retry;
     f.list_count = h->d_retry_count;
     DIP_HIP(launch_general(4, h->fb_blocks, 1, 0, stream, f));
+    DIP_HIP(mark(3));
     return DIP_OK;
   }
 
@@ -852,11 +868,13 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     const int64_t per_block = int64_t(h->wpb) * h->G;
     const int64_t want = (n_cand + per_block - 1) / per_block;
     const int blocks = int(std::min<int64_t>(want, h->max_blocks));
+    DIP_HIP(mark(0));
     if (lds_pipe)
       DIP_HIP(launch_pipe_lds(h->pwl, h->variant == 7, blocks, h->wpb, size_t(h->lds_bytes),
                               stream, a));
     else
       DIP_HIP(launch_pipe(h->pwl, true, blocks, h->wpb, size_t(h->lds_bytes), stream, a));
+    DIP_HIP(mark(1));
     return DIP_OK;
   }
 
@@ -891,7 +909,9 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
   a.end_bytes = uint32_t(b.end);
   const int64_t want = (a.n_groups + wpb - 1) / wpb;
   const int blocks = int(std::min<int64_t>(want, maxb));
+  DIP_HIP(mark(0));
   DIP_HIP(launch_general(v, blocks, wpb, size_t(lds), stream, a));
+  DIP_HIP(mark(1));
   return DIP_OK;
 }
 
@@ -908,6 +928,26 @@ int dip_sim_argmin(dip_sim *h, const int32_t *makespan, const uint8_t *flags, in
   const int blocks = int(std::min<int64_t>(want, int64_t(h->n_cu) * 8));
   DIP_HIP(launch_argmin(blocks, stream, makespan, flags, n_cand, uint64_t(index_base),
                         reinterpret_cast<unsigned long long *>(inout_best_key)));
+  return DIP_OK;
+}
+
+int dip_sim_profile(dip_sim *h, int32_t enable) {
+  if (!h) return DIP_E_INVAL;
+  if (enable && !h->prof_ev[0])
+    for (hipEvent_t &ev : h->prof_ev) DIP_HIP(hipEventCreate(&ev));
+  h->profile = enable != 0;
+  h->prof_n = 0;
+  return DIP_OK;
+}
+
+int dip_sim_last_profile(dip_sim *h, float *out_ms, int32_t *n_out) {
+  if (!h || !out_ms || !n_out) return DIP_E_INVAL;
+  *n_out = 0;
+  if (h->prof_n < 2) return DIP_OK;
+  DIP_HIP(hipEventSynchronize(h->prof_ev[h->prof_n - 1]));
+  for (int i = 0; i + 1 < h->prof_n; ++i)
+    DIP_HIP(hipEventElapsedTime(out_ms + i, h->prof_ev[i], h->prof_ev[i + 1]));
+  *n_out = h->prof_n - 1;
   return DIP_OK;
 }
 
