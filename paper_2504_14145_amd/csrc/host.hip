@@ -233,7 +233,7 @@ int ensure_fallback(dip_sim *h) {
     h->scratch_fb_bytes = need;
   }
   int nb = 0;
-  const int64_t lds = 4 * h->G * check_lds_per_group(h->N);
+  const int64_t lds = 4 * check_lds_per_group(h->N);
   if (lds > h->lds_block_max) return DIP_E_UNSUPPORTED;
   if (lds > 65536 && hipFuncSetAttribute(check_kernel_ptr(h->pwl),
                                          hipFuncAttributeMaxDynamicSharedMemorySize,
@@ -778,8 +778,8 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     c.N = h->N;
     c.wpb = 4;
     c.retry_count = h->d_retry_count;
-    const int64_t c_lds = 4 * h->G * check_lds_per_group(h->N);
-    const int64_t c_per_block = 4 * int64_t(h->G);
+    const int64_t c_lds = 4 * check_lds_per_group(h->N);
+    const int64_t c_per_block = 4;
     const int c_blocks = int(std::min<int64_t>((n_cand + c_per_block - 1) / c_per_block,
                                                int64_t(h->check_blocks_per_cu) * h->n_cu));
     DIP_HIP(launch_check(h->pwl, std::max(c_blocks, 1), 4, size_t(c_lds), stream, c));

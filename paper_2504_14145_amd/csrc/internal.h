@@ -90,8 +90,7 @@ hipError_t launch_pipe_lds(int pwl, bool rec_lds, int blocks, int wpb, size_t ld
 
 // ---------------------------------------------------------------- check
 // Order-only verdict of each candidate: permutation check, per-rank peak
-// memory, cap flag (lane r of a group walks rank r's section; an op-id bitmap
-// per candidate in LDS).
+// memory, cap flag (one wavefront per candidate; an op-id bitmap in LDS).
 struct CheckArgs {
   const int16_t *orders;
   int64_t n_cand;
