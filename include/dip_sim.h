@@ -154,9 +154,11 @@ int dip_sim_create(const dip_topology *topo, dip_sim **out);
  * the same either way). */
 int dip_sim_configure(dip_sim *h, int32_t variant, int32_t waves_per_block);
 
-/* Variant 8: end-time slots per rank pool, 4, 8 or 16 (0 = automatic, 8).
- * Fewer slots keep more candidates resident; a candidate whose pools fill up
- * is re-simulated by the general kernel, so results never depend on it.
+/* Variant 8: end-time slots per rank pool, 4, 8 or 16 (0 = automatic: 8,
+ * doubled for later calls when a call sent more than 1/256 of its candidates
+ * to the retry kernel).  Fewer slots keep more candidates resident; a
+ * candidate whose pools fill up is re-simulated by the general kernel, so
+ * results never depend on it.
  * DIP_E_UNSUPPORTED if the topology does not fit variant 8. */
 int dip_sim_configure_pool(dip_sim *h, int32_t slots_per_rank);
 

@@ -76,6 +76,13 @@ struct dip_sim {
   int2 *d_pool_edge = nullptr;         // pool edges [E]
   int64_t *d_retry = nullptr;          // candidates re-run by the general kernel
   uint32_t *d_retry_count = nullptr;
+  // adaptive pool size: the retry count of a call is copied back
+  // asynchronously and read by a later call, which doubles the pool when more
+  // than 1/256 of the candidates needed the retry kernel
+  uint32_t *h_retry_seen = nullptr;    // pinned
+  hipEvent_t retry_seen_ev = nullptr;
+  bool retry_seen_pending = false;
+  int64_t retry_seen_n = 0;
   int64_t retry_cap = 0;
   int check_blocks_per_cu = 1;
   void *d_scratch_fb = nullptr;        // general kernel (list mode) end tables
@@ -524,6 +531,8 @@ void release(dip_sim *h) {
   if (h->d_pool_edge) (void)hipFree(h->d_pool_edge);
   if (h->d_retry) (void)hipFree(h->d_retry);
   if (h->d_retry_count) (void)hipFree(h->d_retry_count);
+  if (h->h_retry_seen) (void)hipHostFree(h->h_retry_seen);
+  if (h->retry_seen_ev) (void)hipEventDestroy(h->retry_seen_ev);
   if (h->d_scratch_pipe) (void)hipFree(h->d_scratch_pipe);
   if (h->h_stage) (void)hipHostFree(h->h_stage);
   if (h->stage_done) (void)hipEventDestroy(h->stage_done);
@@ -759,6 +768,20 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     h->prof_n = i + 1;
     return hipEventRecord(h->prof_ev[i], stream);
   };
+  if (h->variant == 8 && h->retry_seen_pending && hipEventQuery(h->retry_seen_ev) == hipSuccess) {
+    h->retry_seen_pending = false;
+    const int64_t retried = int64_t(*h->h_retry_seen);
+    if (!h->forced_pool_slots && h->pool_slots < 16 && retried * 256 > h->retry_seen_n) {
+      const int old_s = h->pool_slots;
+      h->pool_slots *= 2;
+      if (choose_config(h) != DIP_OK || h->variant != 8) {
+        h->pool_slots = old_s;
+        int rc = choose_config(h);
+        if (rc != DIP_OK) return rc;
+      }
+    }
+  }
+  (void)hipGetLastError();
   if (h->variant == 8) {
     int rc = ensure_retry(h, n_cand);
     if (rc != DIP_OK) return rc;
@@ -832,6 +855,16 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     f.list_count = h->d_retry_count;
     DIP_HIP(launch_general(4, h->fb_blocks, 1, 0, stream, f));
     DIP_HIP(mark(3));
+    if (!h->forced_pool_slots && h->pool_slots < 16 && !h->retry_seen_pending) {
+      if (!h->h_retry_seen) {
+        DIP_HIP(hipHostMalloc(reinterpret_cast<void **>(&h->h_retry_seen), 16, hipHostMallocDefault));
+        DIP_HIP(hipEventCreateWithFlags(&h->retry_seen_ev, hipEventDisableTiming));
+      }
+      DIP_HIP(hipMemcpyAsync(h->h_retry_seen, h->d_retry_count, 4, hipMemcpyDeviceToHost, stream));
+      DIP_HIP(hipEventRecord(h->retry_seen_ev, stream));
+      h->retry_seen_pending = true;
+      h->retry_seen_n = n_cand;
+    }
     return DIP_OK;
   }
 

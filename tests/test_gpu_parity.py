@@ -235,3 +235,31 @@ def test_deterministic_repeat_and_reused_costs():
     for x, y in zip(a, b):
         np.testing.assert_array_equal(x, y)
     sim.close()
+
+
+def test_streamed_chunks_two_streams():
+    """The 16 x 4 large configuration streamed in chunks through the
+    double-buffered copy/compute streams: every chunk's outputs against the
+    oracle, and the argmin folded over all chunks against the oracle's."""
+    need_gpu()
+    from paper_2504_14145_amd.stream import ChunkStream
+    prob = W.make_problem(5)
+    chunk, n_chunks = 96, 5
+    rows = W.generator_for(prob, 5).generate(0, chunk * n_chunks - 17)   # ragged last chunk
+    want = O.evaluate(prob, rows, threads=16)
+    sim = dip.Sim(prob)
+    cs = ChunkStream(sim, chunk, keep_outputs=True)
+    for k in range(n_chunks):
+        lo, hi = k * chunk, min((k + 1) * chunk, len(rows))
+        host = torch.from_numpy(np.ascontiguousarray(rows[lo:hi])).pin_memory()
+        cs.submit(host, lo)
+    key = cs.finish()
+    for base, outs in cs.host_outs:
+        idx = np.arange(base, base + outs[0].shape[0])
+        ms, bub, pk, fl = (t.numpy() for t in outs)
+        np.testing.assert_array_equal(fl, want.flags[idx])
+        np.testing.assert_array_equal(ms, want.makespan[idx])
+        np.testing.assert_array_equal(bub, want.bubble[idx])
+        np.testing.assert_array_equal(pk, want.peak[idx])
+    assert dip.decode_key(int(key.item())) == O.argmin(want.makespan, want.flags)
+    sim.close()
