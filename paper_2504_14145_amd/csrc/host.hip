@@ -443,18 +443,19 @@ int upload_costs(dip_sim *h, const dip_costs *c, hipStream_t stream) {
   }
   if (h->pool_ok) {
     // pool records {cost, item tag or 0, preds, first edge | readers << 24},
-    // {first edge word, comm}; edges {pred tag | pred rank << 25, comm}; tags
-    // are global index + 1
+    // {first edge word, comm}; edges {pred tag | pred rank << 16, comm}; tags
+    // are rank-local ids + 1
     int4 *pr = reinterpret_cast<int4 *>(h->h_stage + L.prec8);
     int2 *pe = reinterpret_cast<int2 *>(h->h_stage + L.pedge);
     for (int32_t e = 0; e < h->E; ++e) {
       const int32_t p = h->pred_op[e];
-      const uint32_t w = uint32_t(p + 1) | (uint32_t(h->rank_of[p]) << kEdgeRankShift);
+      const int32_t rp = h->rank_of[p];
+      const uint32_t w = uint32_t(p - h->rank_off[rp] + 1) | (uint32_t(rp) << kEdgeRankShift);
       pe[e] = make_int2(int32_t(w), c->edge_comm[e]);
     }
     for (int32_t g = 0; g < h->N; ++g) {
       const int32_t b = h->pred_ptr[g], np = h->pred_ptr[g + 1] - b;
-      const int32_t tag = h->n_cons[g] > 0 ? g + 1 : 0;
+      const int32_t tag = h->n_cons[g] > 0 ? g - h->rank_off[h->rank_of[g]] + 1 : 0;
       pr[2 * g] = make_int4(c->op_cost[g], tag, np, int32_t(uint32_t(b) | (uint32_t(h->n_cons[g]) << 24)));
       pr[2 * g + 1] = np > 0 ? make_int4(pe[b].x, pe[b].y, 0, 0) : make_int4(0, 0, 0, 0);
     }
@@ -610,11 +611,10 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
     rank_of.assign(h->N, 0);
     for (int r = 0; r < h->P; ++r)
       for (int32_t g = h->rank_off[r]; g < h->rank_off[r + 1]; ++g) rank_of[g] = r;
-    // pool kernel eligibility: tags (global index + 1) below 2^25, at most
-    // 255 consumers per op, edge indices below 2^24
+    // pool kernel eligibility: at most 255 consumers per op, edge indices
+    // below 2^24 (tags are rank-local ids + 1 <= 32768 by construction)
     h->n_cons.assign(h->N, 0);
-    bool pool = int64_t(h->N) + 1 < (int64_t(1) << 25) && h->E < (1 << 24) &&
-                int64_t(h->N) * 32 < INT32_MAX;
+    bool pool = h->E < (1 << 24) && int64_t(h->N) * 32 < INT32_MAX;
     for (int32_t g = 0; g < h->N && pool; ++g)
       for (int32_t k = h->pred_ptr[g]; k < h->pred_ptr[g + 1]; ++k)
         if (++h->n_cons[h->pred_op[k]] > 255) pool = false;

@@ -122,7 +122,8 @@ struct PoolArgs {
   int32_t *out_ms;
   int32_t *out_bub;
   uint8_t *out_flags;       // the check kernel's verdicts, extended here
-  const int4 *rec;          // [N][2] {cost, item tag or 0, preds, first edge | readers << 24},
+  const int4 *rec;          // [N][2] {cost, item tag (rank-local id + 1) or 0, preds,
+                            //         first edge | readers << 24},
                             //        {first edge word, its comm, 0, 0}
   const int2 *edge;         // [E] {edge word, comm}
   const int32_t *rank_off;  // [P+1]
@@ -137,14 +138,18 @@ struct PoolArgs {
 // dword 3 of a raw buffer descriptor on CDNA
 constexpr int kBufferWord3 = 0x00020000;
 
-// edge word: predecessor tag (global index + 1) | its rank << 25
-constexpr uint32_t kEdgeTagMask = (1u << 25) - 1u;
-constexpr uint32_t kEdgeRankShift = 25;
+// edge word: predecessor tag (its rank-local id + 1) | its rank << 16
+constexpr uint32_t kEdgeTagMask = 0xffffu;
+constexpr uint32_t kEdgeRankShift = 16;
 
-// pool of S <= 16 slots: 16 bytes of reader counts (one byte per slot), S tags, S ends
+// pool of S <= 16 slots: 16 bytes of reader counts (one byte per slot),
+// S 16-bit tags (padded to 16 bytes), S 32-bit end times
 __host__ __device__ constexpr int64_t pool_head_bytes(int) { return 16; }
+__host__ __device__ constexpr int64_t pool_ends_offset(int slots) {
+  return pool_head_bytes(slots) + ((2 * int64_t(slots) + 15) / 16) * 16;
+}
 __host__ __device__ constexpr int64_t pool_bytes(int slots) {
-  return pool_head_bytes(slots) + 8 * int64_t(slots);
+  return pool_ends_offset(slots) + 4 * int64_t(slots);
 }
 bool pool_slots_ok(int slots);
 const void *pool_kernel_ptr(int pwl, int slots);

@@ -10,11 +10,12 @@
 // next power of two >= P); lane r of a group plays rank r.  Each round every
 // lane looks at the next op of its order.  Ranks hand end times to each other
 // through "items": the end time of an op that has consumers, tagged with the
-// op's global index + 1.  An op's item lives in a small pool of S slots owned
-// by the rank that ran the op:
+// op's rank-local id + 1 (16 bits: the tag only has to be unique within its
+// owner's pool).  An op's item lives in a small pool of S slots owned by the
+// rank that ran the op:
 //
 //     counts (16 bytes): per slot, the readers still to come (0 = free)
-//     tags (4 S bytes), ends (4 S bytes)
+//     tags (2 S bytes, padded to 16), ends (4 S bytes)
 //
 // A consumer compares its predecessor's tag with the S tags of that rank's
 // pool (one predecessor per round), reads the matching end, folds end + comm
@@ -56,6 +57,9 @@ __device__ __forceinline__ void st32(uint32_t addr, uint32_t v) {
   *reinterpret_cast<uint32_t *>(p_lds + addr) = v;
 }
 __device__ __forceinline__ void st8(uint32_t addr, uint32_t v) { p_lds[addr] = uint8_t(v); }
+__device__ __forceinline__ void st16(uint32_t addr, uint32_t v) {
+  *reinterpret_cast<uint16_t *>(p_lds + addr) = uint16_t(v);
+}
 __device__ __forceinline__ uint32_t *lds_word(uint32_t addr) {
   return reinterpret_cast<uint32_t *>(__builtin_assume_aligned(p_lds + addr, 4));
 }
@@ -68,7 +72,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   constexpr int PW = 1 << PWL;
   constexpr int G = kWave / PW;
   constexpr uint32_t kTags = uint32_t(pool_head_bytes(S));
-  constexpr uint32_t kEnds = kTags + 4u * S;
+  constexpr uint32_t kEnds = uint32_t(pool_ends_offset(S));
   constexpr uint32_t kPool = uint32_t(pool_bytes(S));
   static_assert(S >= 4 && S <= 16 && (S & (S - 1)) == 0, "pool size");
   const int lane = threadIdx.x & (kWave - 1);
@@ -99,9 +103,10 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   uint32_t tfree = 0, acc = 0;
   int j = 0;
   // no predecessor to wait for: a tag no item carries (items are tagged
-  // global index + 1 <= N < kEdgeTagMask; free slots hold 0 or a dead tag)
+  // rank-local id + 1 <= 32768 < kEdgeTagMask; free slots hold 0 or a dead tag)
   const int2 no_edge = make_int2(int(kEdgeTagMask), 0);
-  // record {cost, item tag (0: no consumers), preds, first edge | readers << 24}
+  // record {cost, item tag (rank-local id + 1; 0: no consumers), preds,
+  //         first edge | readers << 24}
   int4 cur = make_int4(0, 0, 0, 0);
   int2 ce = no_edge;                      // current edge {pred edge word, comm}
   int4 n0 = cur;                          // record of the op at ptr + 1 ...
@@ -190,9 +195,10 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     // ---- reads: the tags of the predecessor's pool, my reader counts
     const uint32_t want = uint32_t(ce.x) & kEdgeTagMask;
     const uint32_t pa = gbase + ((uint32_t(ce.x) >> kEdgeRankShift) & 63u) * kPool;
-    uint4 q[S / 4];
+    constexpr int kQ = (S + 7) / 8;   // 16-byte loads of tags
+    uint4 q[kQ];
 #pragma unroll
-    for (int i = 0; i < S / 4; ++i) q[i] = ld128(pa + kTags + 16u * i);
+    for (int i = 0; i < kQ; ++i) q[i] = ld128(pa + kTags + 16u * i);
     uint32_t cnt[S / 4];
 #pragma unroll
     for (int i = 0; i < S / 4; ++i) cnt[i] = ld32(my_pool + 4u * i);
@@ -206,8 +212,10 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     bool found = false, b0 = false, b1 = false, b2 = false, b3 = false;
 #pragma unroll
     for (int i = 0; i < S; ++i) {
-      const uint4 w = q[i / 4];
-      const uint32_t t = (i & 3) == 0 ? w.x : (i & 3) == 1 ? w.y : (i & 3) == 2 ? w.z : w.w;
+      const uint4 w = q[i / 8];
+      const int k = (i / 2) & 3;
+      const uint32_t pair = k == 0 ? w.x : k == 1 ? w.y : k == 2 ? w.z : w.w;
+      const uint32_t t = (i & 1) ? (pair >> 16) : (pair & 0xffffu);
       const bool m = t == want;
       found = found || m;
       if (i & 1) b0 = b0 || m;
@@ -239,7 +247,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
       const uint32_t sl = uint32_t(free_s);
       st8(my_pool + sl, uint32_t(cur.w) >> 24);
       st32(my_pool + kEnds + 4u * sl, en);
-      st32(my_pool + kTags + 4u * sl, uint32_t(cur.y));
+      st16(my_pool + kTags + 2u * sl, uint32_t(cur.y));
     }
 
     // ---- register state
