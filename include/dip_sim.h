@@ -146,7 +146,7 @@ int dip_sim_create(const dip_topology *topo, dip_sim **out);
  * of all costs below 2^30, at evaluate time; when the costs do not allow the
  * configured pipeline kernel, evaluate runs the automatically chosen general
  * kernel instead (dip_sim_get_info reports the one that runs).
- * Variant 8 (the automatic choice when the topology allows it: at most 255
+ * Variant 8 (the automatic choice when the topology allows it: at most 15
  * consumers per op and E < 2^24): a check
  * kernel (permutation, peak memory, cap) followed by the pool kernel, which
  * hands end times between ranks through per-rank pools of a few slots, and by

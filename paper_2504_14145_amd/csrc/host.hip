@@ -611,13 +611,14 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
     rank_of.assign(h->N, 0);
     for (int r = 0; r < h->P; ++r)
       for (int32_t g = h->rank_off[r]; g < h->rank_off[r + 1]; ++g) rank_of[g] = r;
-    // pool kernel eligibility: at most 255 consumers per op, edge indices
-    // below 2^24 (tags are rank-local ids + 1 <= 32768 by construction)
+    // pool kernel eligibility: at most 15 consumers per op (4-bit reader
+    // counts), edge indices below 2^24 (tags are rank-local ids + 1 <= 32768
+    // by construction)
     h->n_cons.assign(h->N, 0);
     bool pool = h->E < (1 << 24) && int64_t(h->N) * 32 < INT32_MAX;
     for (int32_t g = 0; g < h->N && pool; ++g)
       for (int32_t k = h->pred_ptr[g]; k < h->pred_ptr[g + 1]; ++k)
-        if (++h->n_cons[h->pred_op[k]] > 255) pool = false;
+        if (++h->n_cons[h->pred_op[k]] > 15) pool = false;
     h->pool_ok = pool;
     h->join_of.assign(h->N, -1);
     h->feeds_join.assign(h->N, -1);

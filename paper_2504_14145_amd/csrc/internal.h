@@ -142,7 +142,7 @@ constexpr int kBufferWord3 = 0x00020000;
 constexpr uint32_t kEdgeTagMask = 0xffffu;
 constexpr uint32_t kEdgeRankShift = 16;
 
-// pool of S <= 16 slots: 16 bytes of reader counts (one byte per slot),
+// pool of S <= 16 slots: 16 bytes of reader counts (one nibble per slot),
 // S 16-bit tags (padded to 16 bytes), S 32-bit end times
 __host__ __device__ constexpr int64_t pool_head_bytes(int) { return 16; }
 __host__ __device__ constexpr int64_t pool_ends_offset(int slots) {

@@ -14,13 +14,14 @@
 // owner's pool).  An op's item lives in a small pool of S slots owned by the
 // rank that ran the op:
 //
-//     counts (16 bytes): per slot, the readers still to come (0 = free)
+//     counts (16 bytes): per slot, a 4-bit count of the readers still to
+//                        come (0 = free)
 //     tags (2 S bytes, padded to 16), ends (4 S bytes)
 //
 // A consumer compares its predecessor's tag with the S tags of that rank's
 // pool (one predecessor per round), reads the matching end, folds end + comm
 // into a running maximum, and decrements the slot's reader count (an LDS
-// atomic subtract on its byte).  The owner reads its counts every round and
+// atomic subtract on its nibble).  The owner reads its counts every round and
 // writes each new item, with its number of readers, into a slot whose count
 // is zero.  A rank whose op has consumers but whose pool is full waits:
 // back-pressure.
@@ -56,12 +57,14 @@ __device__ __forceinline__ uint4 ld128(uint32_t addr) {
 __device__ __forceinline__ void st32(uint32_t addr, uint32_t v) {
   *reinterpret_cast<uint32_t *>(p_lds + addr) = v;
 }
-__device__ __forceinline__ void st8(uint32_t addr, uint32_t v) { p_lds[addr] = uint8_t(v); }
 __device__ __forceinline__ void st16(uint32_t addr, uint32_t v) {
   *reinterpret_cast<uint16_t *>(p_lds + addr) = uint16_t(v);
 }
 __device__ __forceinline__ uint32_t *lds_word(uint32_t addr) {
   return reinterpret_cast<uint32_t *>(__builtin_assume_aligned(p_lds + addr, 4));
+}
+__device__ __forceinline__ void lds_add(uint32_t addr, uint32_t v) {
+  (void)__hip_atomic_fetch_add(lds_word(addr), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
 }
 __device__ __forceinline__ void lds_sub(uint32_t addr, uint32_t v) {
   (void)__hip_atomic_fetch_sub(lds_word(addr), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
@@ -199,9 +202,10 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     uint4 q[kQ];
 #pragma unroll
     for (int i = 0; i < kQ; ++i) q[i] = ld128(pa + kTags + 16u * i);
-    uint32_t cnt[S / 4];
+    constexpr int kC = (S + 7) / 8;   // count words (8 nibbles each)
+    uint32_t cnt[kC];
 #pragma unroll
-    for (int i = 0; i < S / 4; ++i) cnt[i] = ld32(my_pool + 4u * i);
+    for (int i = 0; i < kC; ++i) cnt[i] = ld32(my_pool + 4u * i);
     // prefetch the op's next edge (taken if this round finds the current one)
     {
       const bool more = act && j + 1 < cur.z;
@@ -228,10 +232,10 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     // a slot is free when its reader count is zero: the first such slot
     int free_s = -1;
 #pragma unroll
-    for (int i = S / 4 - 1; i >= 0; --i) {
-      const uint32_t w = cnt[i];
-      const uint32_t z = ~(((w & 0x7f7f7f7fu) + 0x7f7f7f7fu) | w | 0x7f7f7f7fu);   // 0x80 in zero bytes
-      free_s = z ? int(4 * i) + int(__builtin_ctz(z) >> 3) : free_s;
+    for (int i = kC - 1; i >= 0; --i) {
+      const uint32_t w = i * 8 + 8 <= S ? cnt[i] : (cnt[i] | (0xffffffffu << (4 * (S - i * 8))));
+      const uint32_t z = ~(((w & 0x77777777u) + 0x77777777u) | w | 0x77777777u);   // 0x8 in zero nibbles
+      free_s = z ? int(8 * i) + int(__builtin_ctz(z) >> 2) : free_s;
     }
     const uint32_t acc_n = found ? max(acc, hit_v + uint32_t(ce.y)) : acc;
     const int j_n = j + (found ? 1 : 0);
@@ -242,10 +246,10 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     const uint32_t en = max(tfree, acc_n) + uint32_t(cur.x);
 
     // ---- writes: release what was read, publish what was produced
-    if (found) lds_sub(pa + (hit & ~3u), 1u << (8u * (hit & 3u)));
+    if (found) lds_sub(pa + 4u * (hit >> 3), 1u << (4u * (hit & 7u)));
     if (fire && need_out) {
       const uint32_t sl = uint32_t(free_s);
-      st8(my_pool + sl, uint32_t(cur.w) >> 24);
+      lds_add(my_pool + 4u * (sl >> 3), (uint32_t(cur.w) >> 24) << (4u * (sl & 7u)));
       st32(my_pool + kEnds + 4u * sl, en);
       st16(my_pool + kTags + 2u * sl, uint32_t(cur.y));
     }
