@@ -24,8 +24,8 @@ FLAG_DEADLOCK, FLAG_CAP, FLAG_INVALID = 1, 2, 4
 NO_KEY = (1 << 64) - 1
 
 EXPORTS = ("dip_sim_abi_version", "dip_sim_check_topology", "dip_sim_check_costs",
-           "dip_sim_create", "dip_sim_configure", "dip_sim_configure_pool", "dip_sim_get_info",
-           "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
+           "dip_sim_create", "dip_sim_configure", "dip_sim_configure_pool",
+           "dip_sim_configure_check", "dip_sim_get_info", "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
            "dip_sim_argmin", "dip_sim_destroy", "dip_sim_strerror")
 
 
@@ -54,7 +54,8 @@ class Info(ctypes.Structure):
                 ("cand_stride", ctypes.c_int64), ("lanes_per_group", ctypes.c_int32),
                 ("groups_per_wave", ctypes.c_int32), ("waves_per_block", ctypes.c_int32),
                 ("lds_bytes", ctypes.c_int32), ("max_blocks", ctypes.c_int32),
-                ("scratch_bytes", ctypes.c_int64), ("pool_slots", ctypes.c_int32)]
+                ("scratch_bytes", ctypes.c_int64), ("pool_slots", ctypes.c_int32),
+                ("check_kernel", ctypes.c_int32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -77,6 +78,7 @@ def load():
         lib.dip_sim_create.argtypes = [ctypes.POINTER(Topology), ctypes.POINTER(vp)]
         lib.dip_sim_configure.argtypes = [vp, i32, i32]
         lib.dip_sim_configure_pool.argtypes = [vp, i32]
+        lib.dip_sim_configure_check.argtypes = [vp, i32]
         lib.dip_sim_profile.argtypes = [vp, i32]
         lib.dip_sim_last_profile.argtypes = [vp, vp, vp]
         lib.dip_sim_get_info.argtypes = [vp, ctypes.POINTER(Info)]
@@ -87,7 +89,8 @@ def load():
         lib.dip_sim_strerror.argtypes = [ctypes.c_int]
         lib.dip_sim_strerror.restype = ctypes.c_char_p
         for name in ("dip_sim_check_topology", "dip_sim_check_costs", "dip_sim_create",
-                     "dip_sim_configure", "dip_sim_configure_pool", "dip_sim_get_info",
+                     "dip_sim_configure", "dip_sim_configure_pool", "dip_sim_configure_check",
+                     "dip_sim_get_info",
                      "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
                      "dip_sim_argmin"):
             getattr(lib, name).restype = ctypes.c_int
@@ -164,6 +167,10 @@ def configure(h, variant: int = 0, waves_per_block: int = 0) -> int:
 
 def configure_pool(h, slots_per_rank: int = 0) -> int:
     return load().dip_sim_configure_pool(h, int(slots_per_rank))
+
+
+def configure_check(h, mode: int = 0) -> int:
+    return load().dip_sim_configure_check(h, int(mode))
 
 
 def profile(h, enable: bool = True) -> int:
@@ -251,6 +258,9 @@ class Sim:
 
     def configure_pool(self, slots_per_rank=0) -> int:
         return configure_pool(self.h, slots_per_rank)
+
+    def configure_check(self, mode=0) -> int:
+        return configure_check(self.h, mode)
 
     @property
     def info(self) -> dict:

@@ -85,6 +85,15 @@ struct dip_sim {
   int64_t retry_seen_n = 0;
   int64_t retry_cap = 0;
   int check_blocks_per_cu = 1;
+  bool wc_ok = false;                  // the wave-per-candidate check fits
+  int check_mode = 0;                  // 0 automatic, 1 wave per candidate, 2 tiles
+  // tile check (lane = candidate, waves splitting the ranks)
+  bool tc_ok = false;
+  int tc_nw = 1;
+  int32_t tc_max_nr = 0;
+  int64_t tc_lds = 0;
+  int tc_blocks_per_cu = 1;
+  int32_t *d_tc_plan = nullptr;        // [nw+1] offsets, then [P] ranks
   void *d_scratch_fb = nullptr;        // general kernel (list mode) end tables
   int64_t scratch_fb_bytes = 0;
   int fb_blocks = 1;
@@ -222,6 +231,66 @@ int ensure_scratch(dip_sim *h, int v, int64_t need) {
 }
 
 // The pool kernel's fallback: the general kernel with end tables in device
+// Tile check plan: the ranks split between the waves of a block, longest
+// section first onto the least loaded wave, as many waves as keep every wave
+// near the longest section (at most 16) and the block within 64 KiB of LDS
+// (one wave may take more, up to the device's limit).  Leaves tc_ok false
+// when a rank's section does not fit.
+int plan_tile_check(dip_sim *h) {
+  h->tc_ok = false;
+  int32_t max_nr = 0;
+  for (int r = 0; r < h->P; ++r) max_nr = std::max(max_nr, h->n_ops[r]);
+  if (int64_t(h->stride) * 2 * kWave > int64_t(INT32_MAX)) return DIP_OK;
+  const int64_t region = tile_region_bytes(max_nr);
+  int nw = int(std::min<int64_t>({16, int64_t(h->P),
+                                  (int64_t(h->N) + std::max(max_nr, 1) - 1) / std::max(max_nr, 1)}));
+  nw = int(std::min<int64_t>(nw, (65536 - kTileFlagBytes) / region));
+  if (nw < 1) {
+    if (kTileFlagBytes + region > h->lds_block_max) return DIP_OK;
+    nw = 1;
+  }
+  nw = std::max(nw, 1);
+  std::vector<int32_t> order(h->P), load(nw, 0), wave_of(h->P, 0);
+  for (int r = 0; r < h->P; ++r) order[r] = r;
+  std::stable_sort(order.begin(), order.end(),
+                   [&](int32_t x, int32_t y) { return h->n_ops[x] > h->n_ops[y]; });
+  for (int32_t r : order) {
+    const int w = int(std::min_element(load.begin(), load.end()) - load.begin());
+    wave_of[r] = w;
+    load[w] += h->n_ops[r];
+  }
+  std::vector<int32_t> plan(size_t(nw) + 1 + size_t(h->P));
+  int k = 0;
+  for (int w = 0; w < nw; ++w) {
+    plan[w] = k;
+    for (int r = 0; r < h->P; ++r)
+      if (wave_of[r] == w) plan[nw + 1 + k++] = r;
+  }
+  plan[nw] = k;
+  const int64_t lds = kTileFlagBytes + int64_t(nw) * region;
+  if (lds > 65536 && hipFuncSetAttribute(tile_check_kernel_ptr(),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize,
+                                         int(lds)) != hipSuccess) {
+    (void)hipGetLastError();
+    return DIP_OK;
+  }
+  int nb = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, tile_check_kernel_ptr(), nw * kWave,
+                                                   size_t(lds)) != hipSuccess ||
+      nb <= 0) {
+    (void)hipGetLastError();
+    return DIP_OK;
+  }
+  if (!h->d_tc_plan) DIP_HIP(hipMalloc(&h->d_tc_plan, plan.size() * 4));
+  DIP_HIP(hipMemcpy(h->d_tc_plan, plan.data(), plan.size() * 4, hipMemcpyHostToDevice));
+  h->tc_nw = nw;
+  h->tc_max_nr = max_nr;
+  h->tc_lds = lds;
+  h->tc_blocks_per_cu = nb;
+  h->tc_ok = true;
+  return DIP_OK;
+}
+
 // scratch (variant 4), one wave per block, in list mode.
 int ensure_fallback(dip_sim *h) {
   h->fb_blocks = h->n_cu;
@@ -239,22 +308,75 @@ int ensure_fallback(dip_sim *h) {
     }
     h->scratch_fb_bytes = need;
   }
+  // the wave-per-candidate check: one op-id bitmap of N bits per wave
+  h->wc_ok = false;
   int nb = 0;
   const int64_t lds = 4 * check_lds_per_group(h->N);
-  if (lds > h->lds_block_max) return DIP_E_UNSUPPORTED;
-  if (lds > 65536 && hipFuncSetAttribute(check_kernel_ptr(h->pwl),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize,
-                                         int(lds)) != hipSuccess) {
-    (void)hipGetLastError();
-    return DIP_E_UNSUPPORTED;
+  if (lds <= h->lds_block_max &&
+      (lds <= 65536 || hipFuncSetAttribute(check_kernel_ptr(h->pwl),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           int(lds)) == hipSuccess) &&
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, check_kernel_ptr(h->pwl), 4 * kWave,
+                                                   size_t(lds)) == hipSuccess &&
+      nb > 0) {
+    h->check_blocks_per_cu = nb;
+    h->wc_ok = true;
   }
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, check_kernel_ptr(h->pwl), 4 * kWave,
-                                                   size_t(lds)) != hipSuccess ||
-      nb <= 0) {
-    (void)hipGetLastError();
-    return DIP_E_UNSUPPORTED;
-  }
-  h->check_blocks_per_cu = nb;
+  (void)hipGetLastError();
+  return (h->wc_ok || h->tc_ok) ? DIP_OK : DIP_E_UNSUPPORTED;
+}
+
+bool use_tile_check(const dip_sim *h) {
+  return h->check_mode == 2 || (h->check_mode == 0 && h->tc_ok) || !h->wc_ok;
+}
+
+int run_tile_check(dip_sim *h, const int16_t *orders, int64_t n_cand, int32_t *out_ms,
+                   int32_t *out_bub, int32_t *out_peak, uint8_t *out_flags, hipStream_t stream) {
+  TileCheckArgs c{};
+  c.orders = orders;
+  c.n_cand = n_cand;
+  c.stride = h->stride;
+  c.out_ms = out_ms;
+  c.out_bub = out_bub;
+  c.out_peak = out_peak;
+  c.out_flags = out_flags;
+  c.md = h->d_md;
+  c.rank_off = h->d_rank_off;
+  c.cap = h->d_cap;
+  c.plan = h->d_tc_plan;
+  c.P = h->P;
+  c.nw = h->tc_nw;
+  c.md_bytes = tile_md_bytes(h->tc_max_nr);
+  c.region_bytes = tile_region_bytes(h->tc_max_nr);
+  c.retry_count = h->d_retry_count;
+  const int64_t tiles = (n_cand + kWave - 1) / kWave;
+  const int blocks = int(std::min<int64_t>(tiles, int64_t(h->tc_blocks_per_cu) * h->n_cu));
+  DIP_HIP(launch_tile_check(std::max(blocks, 1), h->tc_nw, size_t(h->tc_lds), stream, c));
+  return DIP_OK;
+}
+
+int run_wave_check(dip_sim *h, const int16_t *orders, int64_t n_cand, int32_t *out_ms,
+                   int32_t *out_bub, int32_t *out_peak, uint8_t *out_flags, hipStream_t stream) {
+  CheckArgs c{};
+  c.orders = orders;
+  c.n_cand = n_cand;
+  c.stride = h->stride;
+  c.out_ms = out_ms;
+  c.out_bub = out_bub;
+  c.out_peak = out_peak;
+  c.out_flags = out_flags;
+  c.md = h->d_md;
+  c.rank_off = h->d_rank_off;
+  c.cap = h->d_cap;
+  c.P = h->P;
+  c.N = h->N;
+  c.wpb = 4;
+  c.retry_count = h->d_retry_count;
+  const int64_t c_lds = 4 * check_lds_per_group(h->N);
+  const int64_t c_per_block = 4;
+  const int c_blocks = int(std::min<int64_t>((n_cand + c_per_block - 1) / c_per_block,
+                                             int64_t(h->check_blocks_per_cu) * h->n_cu));
+  DIP_HIP(launch_check(h->pwl, std::max(c_blocks, 1), 4, size_t(c_lds), stream, c));
   return DIP_OK;
 }
 
@@ -526,6 +648,7 @@ void release(dip_sim *h) {
   if (h->d_rank_off) (void)hipFree(h->d_rank_off);
   if (h->d_busy) (void)hipFree(h->d_busy);
   if (h->d_cap) (void)hipFree(h->d_cap);
+  if (h->d_tc_plan) (void)hipFree(h->d_tc_plan);
   if (h->d_scratch_gen) (void)hipFree(h->d_scratch_gen);
   if (h->d_scratch_fb) (void)hipFree(h->d_scratch_fb);
   if (h->d_pool_rec) (void)hipFree(h->d_pool_rec);
@@ -684,6 +807,10 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
     return hip_fail(e);
   if ((e = hipEventCreateWithFlags(&h->stage_done, hipEventDisableTiming)) != hipSuccess)
     return hip_fail(e);
+  if (h->pool_ok && (rc = plan_tile_check(h)) != DIP_OK) {
+    release(h);
+    return rc;
+  }
   rc = choose_config(h);
   if (rc != DIP_OK) {
     release(h);
@@ -725,6 +852,13 @@ int dip_sim_configure_pool(dip_sim *h, int32_t slots_per_rank) {
   return rc;
 }
 
+int dip_sim_configure_check(dip_sim *h, int32_t mode) {
+  if (!h || mode < 0 || mode > 2) return DIP_E_INVAL;
+  if (!h->pool_ok || (mode == 1 && !h->wc_ok) || (mode == 2 && !h->tc_ok)) return DIP_E_UNSUPPORTED;
+  h->check_mode = mode;
+  return DIP_OK;
+}
+
 int dip_sim_get_info(const dip_sim *h, dip_sim_info *info) {
   if (!h || !info) return DIP_E_INVAL;
   const bool pipe_off = h->costs_set &&
@@ -743,6 +877,7 @@ int dip_sim_get_info(const dip_sim *h, dip_sim_info *info) {
   info->scratch_bytes = h->scratch_gen_bytes + h->scratch_pipe_bytes + h->scratch_fb_bytes +
                         h->retry_cap * 8;
   info->pool_slots = h->variant == 8 ? h->pool_slots : 0;
+  info->check_kernel = h->variant == 8 ? (use_tile_check(h) ? 2 : 1) : 0;
   return DIP_OK;
 }
 
@@ -787,26 +922,11 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     int rc = ensure_retry(h, n_cand);
     if (rc != DIP_OK) return rc;
     DIP_HIP(mark(0));
-    CheckArgs c{};
-    c.orders = orders;
-    c.n_cand = n_cand;
-    c.stride = h->stride;
-    c.out_ms = out_makespan;
-    c.out_bub = out_bubble;
-    c.out_peak = out_peakmem;
-    c.out_flags = out_flags;
-    c.md = h->d_md;
-    c.rank_off = h->d_rank_off;
-    c.cap = h->d_cap;
-    c.P = h->P;
-    c.N = h->N;
-    c.wpb = 4;
-    c.retry_count = h->d_retry_count;
-    const int64_t c_lds = 4 * check_lds_per_group(h->N);
-    const int64_t c_per_block = 4;
-    const int c_blocks = int(std::min<int64_t>((n_cand + c_per_block - 1) / c_per_block,
-                                               int64_t(h->check_blocks_per_cu) * h->n_cu));
-    DIP_HIP(launch_check(h->pwl, std::max(c_blocks, 1), 4, size_t(c_lds), stream, c));
+    rc = use_tile_check(h) ? run_tile_check(h, orders, n_cand, out_makespan, out_bubble,
+                                            out_peakmem, out_flags, stream)
+                           : run_wave_check(h, orders, n_cand, out_makespan, out_bubble,
+                                            out_peakmem, out_flags, stream);
+    if (rc != DIP_OK) return rc;
     DIP_HIP(mark(1));
 
     PoolArgs a{};

@@ -112,6 +112,39 @@ const void *check_kernel_ptr(int pwl);
 hipError_t launch_check(int pwl, int blocks, int wpb, size_t lds, hipStream_t s,
                         const CheckArgs &a);
 
+// Order-only verdict by tiles of 64 consecutive candidates, lane = candidate:
+// the waves of a block split the ranks between them (plan), and for each of
+// its ranks a wave streams the rank's section of the 64 rows, with the rank's
+// memory deltas and a per-lane op-id bitmap in the wave's LDS region.
+struct TileCheckArgs {
+  const int16_t *orders;
+  int64_t n_cand;
+  int64_t stride;
+  int32_t *out_ms;
+  int32_t *out_bub;
+  int32_t *out_peak;
+  uint8_t *out_flags;
+  const int32_t *md;        // [N] +act at a forward, -act at a backward
+  const int32_t *rank_off;  // [P+1]
+  const int32_t *cap;       // [P]
+  const int32_t *plan;      // [nw+1] offsets into the rank list, then the list [P]
+  int32_t P, nw;
+  int32_t md_bytes;         // bytes of a wave's delta area (16-aligned)
+  int32_t region_bytes;     // bytes per wave: delta area + bitmap of 64 lanes
+  uint32_t *retry_count;    // zeroed by the kernel when not null
+};
+
+// LDS of a tile-check block: the 64 candidates' flag words, then the waves'
+// regions
+constexpr int kTileFlagBytes = 256;
+// (deltas and bits of ids 0 .. max_nr: the last one the overflow entry)
+__host__ __device__ inline int32_t tile_md_bytes(int32_t max_nr) { return ((max_nr + 1) * 4 + 15) & ~15; }
+__host__ __device__ inline int32_t tile_region_bytes(int32_t max_nr) {
+  return tile_md_bytes(max_nr) + ((max_nr + 32) / 32) * 64 * 4;
+}
+const void *tile_check_kernel_ptr();
+hipError_t launch_tile_check(int blocks, int nw, size_t lds, hipStream_t s, const TileCheckArgs &a);
+
 // ---------------------------------------------------------------- pool
 // Timing simulation with per-rank slot pools holding the end times still to
 // be read (see kern_pool.hip).

@@ -154,12 +154,167 @@ __global__ __launch_bounds__(256) void check_kernel(CheckArgs a) {
   }
 }
 
+// ---------------------------------------------------------------- tile check
+// Lane = candidate: the 64 lanes of a wave hold 64 consecutive candidates and
+// walk one rank's section of their rows in lockstep, so section boundaries
+// are the same for every lane and only the ids differ.
+//
+//   * A section is a permutation of 0 .. n_r-1 iff its n_r ids set n_r
+//     distinct bits of a map of bits 0 .. n_r, with an id above n_r - 1
+//     clamped to the overflow bit n_r and that bit left clear (n_r ids, all
+//     in range and pairwise distinct).  A lane's map lives in LDS word-major
+//     (word w of lane l at 64 w + l), so the 64 lanes of one OR touch 64
+//     distinct words and no two of them share a bank within a half-wave.
+//   * The running memory is the sum of the deltas of the ops taken so far,
+//     read from the wave's copy of the rank's deltas in LDS; the peak is its
+//     maximum, starting from 0 (Sec. 5.3).
+// The verdict of a candidate needs all of its ranks: each wave ORs its
+// findings into the candidates' flag words in LDS, and after a block barrier
+// the outputs of an invalid candidate are overwritten with -1.
+
+// orders the LDS accesses of the lanes of one wave around this point
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+__global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  uint32_t *flg = reinterpret_cast<uint32_t *>(c_lds);
+  unsigned char *region = c_lds + kTileFlagBytes + wave * a.region_bytes;
+  int32_t *mdl = reinterpret_cast<int32_t *>(region);
+  uint32_t *bm = reinterpret_cast<uint32_t *>(region + a.md_bytes) + lane;   // word w at bm[64 w]
+  if (a.retry_count && blockIdx.x == 0 && threadIdx.x == 0) *a.retry_count = 0u;
+
+  const int kb = a.plan[wave], ke = a.plan[wave + 1];
+  const int32_t *ranks = a.plan + a.nw + 1;
+  const int64_t n_tiles = (a.n_cand + kWave - 1) / kWave;
+  const uint32_t row_bytes = uint32_t(a.stride) * 2u;
+  for (int64_t tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+    if (wave == 0) flg[lane] = 0u;
+    __syncthreads();
+    const int64_t c0 = tile * kWave;
+    const int n_live = int(min<int64_t>(a.n_cand - c0, kWave));
+    const bool live = lane < n_live;
+    const int64_t cand = c0 + lane;
+    // the tile's rows behind one buffer descriptor; a lane past the end of
+    // the batch reads the last row
+    const uint64_t base = reinterpret_cast<uint64_t>(a.orders + c0 * a.stride);
+    const uint64_t base_u = uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(base)))) |
+                            (uint64_t(uint32_t(__builtin_amdgcn_readfirstlane(uint32_t(base >> 32)))) << 32);
+    const __amdgpu_buffer_rsrc_t rows = __builtin_amdgcn_make_buffer_rsrc(
+        reinterpret_cast<void *>(base_u), 0,
+        __builtin_amdgcn_readfirstlane(int(uint32_t(n_live) * row_bytes)), kBufferWord3);
+    const uint32_t voff = uint32_t(live ? lane : n_live - 1) * row_bytes;
+    uint32_t fl = 0;
+    for (int k = kb; k < ke; ++k) {
+      const int r = ranks[k];
+      const int rb = a.rank_off[r], re = a.rank_off[r + 1];
+      const int nr = re - rb;
+      const int n_words = (nr + 32) >> 5;   // bits 0 .. nr
+      // the rank's deltas into the wave's region (entry nr, the overflow
+      // entry, is 0), the lanes' bitmaps cleared
+      wave_sync();
+      for (int i = lane; i <= nr; i += 4 * kWave) {
+        int32_t v[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) v[t] = i + t * kWave < nr ? a.md[rb + i + t * kWave] : 0;
+#pragma unroll
+        for (int t = 0; t < 4; ++t)
+          if (i + t * kWave <= nr) mdl[i + t * kWave] = v[t];
+      }
+      for (int w = 0; w < n_words; ++w) bm[w * kWave] = 0u;
+      wave_sync();
+
+      const uint32_t lim = uint32_t(nr);
+      int run = 0, peak = 0;
+      auto take = [&](uint32_t id) {
+        const uint32_t c = min(id, lim);
+        // word index c >> 5, kept as one shift (the byte offset is then one
+        // shift-add instead of a shift, a mask and an add)
+        uint32_t w;
+        asm("v_lshrrev_b32 %0, 5, %1" : "=v"(w) : "v"(c));
+        __hip_atomic_fetch_or(bm + w * kWave, 1u << (c & 31u), __ATOMIC_RELAXED,
+                              __HIP_MEMORY_SCOPE_WORKGROUP);
+        run += mdl[c];
+        peak = max(peak, run);
+      };
+      // positions lo .. hi-1 of a unit of 8 (lo, hi uniform)
+      auto unit = [&](const uint4 v, int lo, int hi) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const uint32_t w = q < 2 ? v.x : q < 4 ? v.y : q < 6 ? v.z : v.w;
+          if (q >= lo && q < hi) take((q & 1) ? (w >> 16) : (w & 0xffffu));
+        }
+      };
+      if (nr > 0) {
+        const int u0 = rb >> 3, u1 = (re - 1) >> 3;   // first and last unit of 8 ids
+        auto ld = [&](int u) {
+          const auto x = __builtin_amdgcn_raw_buffer_load_b128(rows, voff, uint32_t(min(u, u1)) * 16u, 0);
+          return make_uint4(uint32_t(x[0]), uint32_t(x[1]), uint32_t(x[2]), uint32_t(x[3]));
+        };
+        auto step = [&](int u, const uint4 v) {
+          const int lo = max(rb - 8 * u, 0), hi = min(re - 8 * u, 8);
+          if (lo == 0 && hi == 8)
+            unit(v, 0, 8);
+          else
+            unit(v, lo, hi);
+        };
+        // four units per iteration, the next four loaded one iteration ahead
+        uint4 b[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) b[i] = ld(u0 + i);
+        for (int u = u0; u <= u1; u += 4) {
+          uint4 nb[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) nb[i] = ld(u + 4 + i);
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (u + i <= u1) step(u + i, b[i]);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) b[i] = nb[i];
+        }
+      }
+      uint32_t bits = 0;
+      for (int w = 0; w < n_words; ++w) bits += uint32_t(__builtin_popcount(bm[w * kWave]));
+      const bool ovf = (bm[(nr >> 5) * kWave] >> (nr & 31)) & 1u;
+      const bool bad = ovf || bits != lim;
+      const int cap_r = a.cap[r];
+      const bool over = cap_r >= 0 && peak > cap_r;
+      if (live) a.out_peak[cand * a.P + r] = peak;
+      fl |= (bad ? 1u : 0u) | (over ? 2u : 0u);
+    }
+    if (fl) __hip_atomic_fetch_or(flg + lane, fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+    __syncthreads();
+    const uint32_t f = flg[lane];
+    if (live && (f & 1u))
+      for (int k = kb; k < ke; ++k) a.out_peak[cand * a.P + ranks[k]] = -1;
+    if (wave == 0 && live) {
+      a.out_flags[cand] = (f & 1u) ? uint8_t(DIP_FLAG_INVALID) : uint8_t((f & 2u) ? DIP_FLAG_CAP : 0u);
+      if (f & 1u) {
+        a.out_ms[cand] = -1;
+        for (int q = 0; q < a.P; ++q) a.out_bub[cand * a.P + q] = -1;
+      }
+    }
+    __syncthreads();   // the flag words are cleared for the next tile
+  }
+}
+
 }  // namespace
 
 const void *check_kernel_ptr(int) { return reinterpret_cast<const void *>(check_kernel); }
 
 hipError_t launch_check(int, int blocks, int wpb, size_t lds, hipStream_t s, const CheckArgs &a) {
   check_kernel<<<dim3(blocks), dim3(wpb * kWave), lds, s>>>(a);
+  return hipGetLastError();
+}
+
+const void *tile_check_kernel_ptr() { return reinterpret_cast<const void *>(tile_check_kernel); }
+
+hipError_t launch_tile_check(int blocks, int nw, size_t lds, hipStream_t s, const TileCheckArgs &a) {
+  tile_check_kernel<<<dim3(blocks), dim3(nw * kWave), lds, s>>>(a);
   return hipGetLastError();
 }
 

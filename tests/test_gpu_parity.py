@@ -1,5 +1,7 @@
 """GPU parity: the HIP path through the C ABI against the CPU oracle,
 element by element and bit-exact (all quantities are integers)."""
+import dataclasses
+
 import numpy as np
 import pytest
 
@@ -112,6 +114,79 @@ def test_pool_fallback_when_pools_fill():
         dip.evaluate(sim.h, sim.costs, orders, len(rows), *out)
         torch.cuda.synchronize()
         assert_same(tuple(t.cpu().numpy() for t in out), want)
+    sim.close()
+
+
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
+def test_check_kernels_caps_and_invalid_ids(cid):
+    """Both kernels of the order-only verdict (one wave per candidate; tiles of
+    64 candidates with the ranks split between the waves of a block) against
+    the oracle, with per-rank caps at the median peak (so some candidates are
+    capped and some are not) and ids out of range (n_r itself, the overflow
+    bit of the tile kernel), negative or repeated, planted on random ranks and
+    on the last rank."""
+    need_gpu()
+    prob = W.make_problem(cid)
+    n = SMALL[cid]
+    rows = W.generator_for(prob, cid).generate(1, n).copy()
+    peaks = O.evaluate(prob, rows[:64], threads=16).peak
+    cap = np.median(peaks, axis=0).astype(np.int32)
+    prob = dataclasses.replace(prob, mem_cap=cap)
+    rng = np.random.default_rng(cid)
+    P, ro = prob.n_ranks, prob.rank_off
+    for i in rng.choice(n, size=max(3, n // 16), replace=False):
+        r = int(rng.integers(P)) if i % 2 else P - 1
+        b, e = int(ro[r]), int(ro[r + 1])
+        p = int(rng.integers(b, e))
+        if i % 3 == 0:
+            rows[i, p] = e - b
+        elif i % 3 == 1:
+            rows[i, p] = -1 - int(rng.integers(100))
+        else:
+            rows[i, p] = rows[i, b if p != b else e - 1]
+    want = O.evaluate(prob, rows, threads=16)
+    assert (want.flags & O.FLAG_INVALID).any() and (want.flags & O.FLAG_CAP).any()
+    sim = dip.Sim(prob)
+    tried = 0
+    for mode in (1, 2):
+        rc = sim.configure_check(mode)
+        if rc == dip.E_UNSUPPORTED:
+            continue
+        assert rc == dip.OK
+        assert sim.info["check_kernel"] == mode
+        print(f"config {cid} check kernel {mode}", flush=True)
+        assert_same(run_gpu(sim, rows), want)
+        tried += 1
+    assert tried >= 1
+    sim.close()
+
+
+def test_check_kernels_empty_rank():
+    """A rank with no ops between two that have some: its peak is 0, it never
+    flags a candidate, and the other ranks keep their sections."""
+    need_gpu()
+    M = 4
+    base = W.compile_instance(W.pipeline_instance(3, M, [[4, 6, 5, 7], [5, 5, 6, 6], [7, 3, 4, 5]],
+                                                  comm=2))
+    ro = np.asarray(base.rank_off)
+    prob = dataclasses.replace(
+        base, n_ranks=4, n_ops=np.array([base.n_ops[0], base.n_ops[1], 0, base.n_ops[2]], np.int32),
+        rank_off=np.array([ro[0], ro[1], ro[2], ro[2], ro[3]], ro.dtype),
+        mem_cap=np.array([-1, 0, 0, -1], np.int32))
+    one = np.zeros(prob.stride, np.int16)
+    for r in range(3):
+        k = int(base.n_ops[r])
+        one[ro[r]:ro[r] + k] = np.arange(k)
+    rows = np.stack([one] * 130)
+    rows[7, int(ro[2])] = int(base.n_ops[2])          # out of range on the rank after the empty one
+    want = O.evaluate(prob, rows)
+    assert want.flags[7] == O.FLAG_INVALID and (want.flags[:7] == O.FLAG_CAP).all()
+    assert (want.peak[:, 2] <= 0).all()
+    sim = dip.Sim(prob)
+    for mode in (1, 2):
+        if sim.configure_check(mode) == dip.E_UNSUPPORTED:
+            continue
+        assert_same(run_gpu(sim, rows), want)
     sim.close()
 
 
