@@ -157,7 +157,7 @@ int64_t lds_for(const dip_sim *h, int v, int wpb) {
     const int64_t per_wave = int64_t(h->G) * (int64_t(h->tab_stride) * 4 + h->stride * 2);
     return int64_t(wpb) * per_wave + (v == 7 ? align16(int64_t(h->N) * 16) : 0);
   }
-  if (v == 8) return int64_t(wpb) * h->G * h->P * pool_bytes(h->pool_slots);
+  if (v == 8) return int64_t(wpb) * h->G * pool_group_bytes(1 << h->pwl, h->pool_slots);
   return 0;
 }
 

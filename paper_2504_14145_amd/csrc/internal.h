@@ -175,14 +175,29 @@ constexpr int kBufferWord3 = 0x00020000;
 constexpr uint32_t kEdgeTagMask = 0xffffu;
 constexpr uint32_t kEdgeRankShift = 16;
 
-// pool of S <= 16 slots: 16 bytes of reader counts (one nibble per slot),
-// S 16-bit tags (padded to 16 bytes), S 32-bit end times
-__host__ __device__ constexpr int64_t pool_head_bytes(int) { return 16; }
-__host__ __device__ constexpr int64_t pool_ends_offset(int slots) {
-  return pool_head_bytes(slots) + ((2 * int64_t(slots) + 15) / 16) * 16;
+// The pools of one candidate (a group of PW lanes, P <= PW ranks) in LDS, as
+// arrays over the ranks so that lanes reading their own or a neighbour's pool
+// fall in distinct banks:
+//   counts [PW][C] words, C = ceil(S / 8): a 4-bit reader count per slot
+//                          (0 = free slot)
+//   tags   [PW][S] 16-bit, 16-byte aligned
+//   ends   [PW][S + 1] words (the extra word makes the stride odd in words)
+// padded so that the group's size in words is congruent to PW modulo the 32
+// banks: the count words of consecutive groups then tile the banks.
+__host__ __device__ constexpr int64_t pool_count_words(int slots) { return (slots + 7) / 8; }
+__host__ __device__ constexpr int64_t pool_tags_offset(int pw, int slots) {
+  return (int64_t(pw) * 4 * pool_count_words(slots) + 15) / 16 * 16;
 }
-__host__ __device__ constexpr int64_t pool_bytes(int slots) {
-  return pool_ends_offset(slots) + 4 * int64_t(slots);
+__host__ __device__ constexpr int64_t pool_ends_offset(int pw, int slots) {
+  return pool_tags_offset(pw, slots) + int64_t(pw) * 2 * slots;
+}
+__host__ __device__ constexpr int64_t pool_end_stride(int slots) { return 4 * int64_t(slots) + 4; }
+__host__ __device__ constexpr int64_t pool_group_bytes(int pw, int slots) {
+  const int64_t raw = pool_ends_offset(pw, slots) + int64_t(pw) * pool_end_stride(slots);
+  const int64_t want = pw >= 32 ? 0 : 4 * (pw < 4 ? 4 : pw);   // residue modulo 128 bytes
+  int64_t x = (raw + 15) / 16 * 16;
+  while (x % 128 != want) x += 16;
+  return x;
 }
 bool pool_slots_ok(int slots);
 const void *pool_kernel_ptr(int pwl, int slots);

@@ -12,11 +12,11 @@
 // through "items": the end time of an op that has consumers, tagged with the
 // op's rank-local id + 1 (16 bits: the tag only has to be unique within its
 // owner's pool).  An op's item lives in a small pool of S slots owned by the
-// rank that ran the op:
-//
-//     counts (16 bytes): per slot, a 4-bit count of the readers still to
-//                        come (0 = free)
-//     tags (2 S bytes, padded to 16), ends (4 S bytes)
+// rank that ran the op: per slot a 4-bit count of the readers still to come
+// (0 = free), a tag and an end time.  The pools of a candidate are laid out as
+// arrays over its ranks (counts, then tags, then ends with an odd stride in
+// words), so the lanes of a wave reading their own or a neighbour's pool hit
+// distinct LDS banks.
 //
 // A consumer compares its predecessor's tag with the S tags of that rank's
 // pool (one predecessor per round), reads the matching end, folds end + comm
@@ -27,7 +27,7 @@
 // back-pressure.
 //
 // Only a few items are live at a time (an item dies once its consumers ran),
-// so a candidate needs P pools of under 150 bytes, where a table of end times
+// so a candidate needs P pools of under 120 bytes, where a table of end times
 // by op would need 4 bytes per op: many more candidates stay resident per CU,
 // which is what hides the LDS and cache latencies of the round loop.
 //
@@ -48,11 +48,17 @@ namespace {
 
 extern __shared__ __align__(16) unsigned char p_lds[];
 
+// a 32-bit word in global memory
+typedef const __attribute__((address_space(1))) uint32_t *gword_ptr;
+
 __device__ __forceinline__ uint32_t ld32(uint32_t addr) {
   return *reinterpret_cast<const uint32_t *>(p_lds + addr);
 }
 __device__ __forceinline__ uint4 ld128(uint32_t addr) {
   return *reinterpret_cast<const uint4 *>(p_lds + addr);
+}
+__device__ __forceinline__ uint2 ld64(uint32_t addr) {
+  return *reinterpret_cast<const uint2 *>(p_lds + addr);
 }
 __device__ __forceinline__ void st32(uint32_t addr, uint32_t v) {
   *reinterpret_cast<uint32_t *>(p_lds + addr) = v;
@@ -74,9 +80,11 @@ template <int PWL, int S>
 __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   constexpr int PW = 1 << PWL;
   constexpr int G = kWave / PW;
-  constexpr uint32_t kTags = uint32_t(pool_head_bytes(S));
-  constexpr uint32_t kEnds = uint32_t(pool_ends_offset(S));
-  constexpr uint32_t kPool = uint32_t(pool_bytes(S));
+  constexpr int kC = int(pool_count_words(S));   // count words per pool
+  constexpr uint32_t kTags = uint32_t(pool_tags_offset(PW, S));
+  constexpr uint32_t kEnds = uint32_t(pool_ends_offset(PW, S));
+  constexpr uint32_t kEndStride = uint32_t(pool_end_stride(S));
+  constexpr uint32_t kGroup = uint32_t(pool_group_bytes(PW, S));
   static_assert(S >= 4 && S <= 16 && (S & (S - 1)) == 0, "pool size");
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = threadIdx.x / kWave;
@@ -85,8 +93,13 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   const bool on = r < a.P;
   const int gbit = grp << PWL;
   const int64_t n_slots = int64_t(gridDim.x) * a.wpb * G;
-  const uint32_t gbase = uint32_t(wave * G + grp) * uint32_t(a.P) * kPool;
-  const uint32_t my_pool = gbase + uint32_t(on ? r : 0) * kPool;
+  const uint32_t gbase = uint32_t(wave * G + grp) * kGroup;
+  const uint32_t rr = uint32_t(on ? r : 0);
+  const uint32_t my_cnt = gbase + rr * 4u * kC;
+  // my tags and ends, from my counts' address and my rank (kept out of
+  // registers: the compiler folds the constants)
+  auto my_tag = [&]() { return gbase + kTags + rr * 2u * S; };
+  auto my_end = [&]() { return gbase + kEnds + rr * kEndStride; };
 
   int rb = 0, nr = 0, busy_r = 0;
   if (on) {
@@ -95,6 +108,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     busy_r = a.busy[r];
   }
   const int last = max(nr - 1, 0);
+  const int rb2 = rb + 2, last_abs = rb + last;
 
   int64_t cand = (int64_t(blockIdx.x) * a.wpb + wave) * G + grp;
   uint32_t rnd = 0;          // rounds so far
@@ -116,6 +130,17 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   int2 n1 = no_edge;                      // ... and its first edge
   int id2 = 0;                            // id at ptr + 2
   const int16_t *row0 = a.orders;         // this candidate's row
+  // the word read by lanes that did not advance, kept in registers (a select
+  // between two registers is one instruction), in the global address space
+  // (a generic pointer would turn the load into a flat load, which every LDS
+  // wait would then also wait for)
+  gword_ptr idle_w;
+  {
+    const uint64_t v = reinterpret_cast<uint64_t>(a.orders);
+    uint32_t lo = uint32_t(v), hi = uint32_t(v >> 32);
+    asm volatile("" : "+v"(lo), "+v"(hi));
+    idle_w = reinterpret_cast<gword_ptr>(uint64_t(lo) | (uint64_t(hi) << 32));
+  }
   auto clamp_id = [&](int id) { return min(max(id, 0), last); };
   // records and edges through buffer descriptors: 32-bit byte offsets, and a
   // read past the end returns zeros instead of faulting
@@ -142,8 +167,8 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   // so no round waits for a load it issued itself.
   int4 s0 = n0;
   int2 s1 = n1, se = no_edge;
-  uint32_t s2 = 0;   // the aligned 32-bit word holding the next id ...
-  int s2_hi = 0;     // ... in its upper half
+  uint32_t s2 = 0;      // the aligned 32-bit word holding the next id ...
+  uint32_t s2_hi = 0;   // ... in its upper half
   bool take_rec = false, take_edge = false;
 
   // All lanes of the group call this together.
@@ -157,10 +182,16 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     if (!has) return;
     fl = a.out_flags[cand];
     cand_round = rnd;
-    if (on) {
-      uint4 *p = reinterpret_cast<uint4 *>(p_lds + my_pool);
+    if (on) {   // counts and tags cleared (ends are read only under a tag)
 #pragma unroll
-      for (int i = 0; i < int(kPool / 16); ++i) p[i] = make_uint4(0, 0, 0, 0);
+      for (int i = 0; i < kC; ++i) st32(my_cnt + 4u * i, 0u);
+      if constexpr (S == 4) {
+        *reinterpret_cast<uint2 *>(p_lds + my_tag()) = make_uint2(0, 0);
+      } else {
+#pragma unroll
+        for (int i = 0; i < S / 8; ++i)
+          *reinterpret_cast<uint4 *>(p_lds + my_tag() + 16u * i) = make_uint4(0, 0, 0, 0);
+      }
     }
     ptr = 0;
     tfree = 0;
@@ -185,27 +216,33 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   uint64_t g_has = any_in_group<PWL>(__builtin_amdgcn_ballot_w64(has));
 
   while (g_has) {
-    // ---- what the previous round fetched
-    if (take_rec) {
-      n0 = s0;
-      n1 = s1;
-      id2 = int(int16_t(s2_hi ? (s2 >> 16) : (s2 & 0xffffu)));
-    }
+    // ---- the edge fetched by the previous round
     if (take_edge) ce = se;
-    asm volatile("" : "+v"(n0.x), "+v"(n0.y), "+v"(n0.z), "+v"(n0.w), "+v"(n1.x), "+v"(n1.y),
-                 "+v"(id2), "+v"(ce.x), "+v"(ce.y)::"memory");
+    asm volatile("" : "+v"(ce.x), "+v"(ce.y)::"memory");
 
     // ---- reads: the tags of the predecessor's pool, my reader counts
     const uint32_t want = uint32_t(ce.x) & kEdgeTagMask;
-    const uint32_t pa = gbase + ((uint32_t(ce.x) >> kEdgeRankShift) & 63u) * kPool;
-    constexpr int kQ = (S + 7) / 8;   // 16-byte loads of tags
-    uint4 q[kQ];
+    const uint32_t rp = (uint32_t(ce.x) >> kEdgeRankShift) & 63u;   // the predecessor's rank
+    const uint32_t p_cnt = gbase + rp * 4u * kC;
+    const uint32_t p_end = gbase + kEnds + rp * kEndStride;
+    uint32_t tw[S / 2];   // the S tags of its pool, two per word
+    if constexpr (S == 4) {
+      const uint2 v = ld64(gbase + kTags + rp * 2u * S);
+      tw[0] = v.x;
+      tw[1] = v.y;
+    } else {
 #pragma unroll
-    for (int i = 0; i < kQ; ++i) q[i] = ld128(pa + kTags + 16u * i);
-    constexpr int kC = (S + 7) / 8;   // count words (8 nibbles each)
-    uint32_t cnt[kC];
+      for (int i = 0; i < S / 8; ++i) {
+        const uint4 v = ld128(gbase + kTags + rp * 2u * S + 16u * i);
+        tw[4 * i] = v.x;
+        tw[4 * i + 1] = v.y;
+        tw[4 * i + 2] = v.z;
+        tw[4 * i + 3] = v.w;
+      }
+    }
+    uint32_t cnt[kC];   // my reader counts, 8 nibbles per word
 #pragma unroll
-    for (int i = 0; i < kC; ++i) cnt[i] = ld32(my_pool + 4u * i);
+    for (int i = 0; i < kC; ++i) cnt[i] = ld32(my_cnt + 4u * i);
     // prefetch the op's next edge (taken if this round finds the current one)
     {
       const bool more = act && j + 1 < cur.z;
@@ -216,9 +253,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     bool found = false, b0 = false, b1 = false, b2 = false, b3 = false;
 #pragma unroll
     for (int i = 0; i < S; ++i) {
-      const uint4 w = q[i / 8];
-      const int k = (i / 2) & 3;
-      const uint32_t pair = k == 0 ? w.x : k == 1 ? w.y : k == 2 ? w.z : w.w;
+      const uint32_t pair = tw[i / 2];
       const uint32_t t = (i & 1) ? (pair >> 16) : (pair & 0xffffu);
       const bool m = t == want;
       found = found || m;
@@ -227,32 +262,53 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
       if (i & 4) b2 = b2 || m;
       if (i & 8) b3 = b3 || m;
     }
-    const uint32_t hit = (b0 ? 1u : 0u) | (b1 ? 2u : 0u) | (b2 ? 4u : 0u) | (b3 ? 8u : 0u);
-    const uint32_t hit_v = ld32(pa + kEnds + 4u * hit);
-    // a slot is free when its reader count is zero: the first such slot
-    int free_s = -1;
+    const uint32_t hit4 = (b0 ? 4u : 0u) | (b1 ? 8u : 0u) | (b2 ? 16u : 0u) | (b3 ? 32u : 0u);   // 4 x slot
+    const uint32_t hit = hit4 >> 2;
+    const uint32_t hit_v = ld32(p_end + hit4);
+    // a slot is free when its reader count is zero: the first such slot (sl,
+    // meaningful when has_free)
+    bool has_free = false;
+    uint32_t sl = 0;
 #pragma unroll
     for (int i = kC - 1; i >= 0; --i) {
       const uint32_t w = i * 8 + 8 <= S ? cnt[i] : (cnt[i] | (0xffffffffu << (4 * (S - i * 8))));
       const uint32_t z = ~(((w & 0x77777777u) + 0x77777777u) | w | 0x77777777u);   // 0x8 in zero nibbles
-      free_s = z ? int(8 * i) + int(__builtin_ctz(z) >> 2) : free_s;
+      if constexpr (kC == 1) {
+        has_free = z != 0u;
+        sl = uint32_t(__builtin_ctz(z)) >> 2;
+      } else {
+        sl = z ? 8u * uint32_t(i) + (uint32_t(__builtin_ctz(z)) >> 2) : sl;
+        has_free = has_free || z != 0u;
+      }
     }
     const uint32_t acc_n = found ? max(acc, hit_v + uint32_t(ce.y)) : acc;
     const int j_n = j + (found ? 1 : 0);
     const bool ready = act && j_n >= cur.z;
     const bool need_out = cur.y != 0;
-    const bool fire = ready && (!need_out || free_s >= 0);
+    const bool fire = ready && (!need_out || has_free);
     const bool held = ready && !fire;
     const uint32_t en = max(tfree, acc_n) + uint32_t(cur.x);
 
     // ---- writes: release what was read, publish what was produced
-    if (found) lds_sub(pa + 4u * (hit >> 3), 1u << (4u * (hit & 7u)));
+    // (with one count word, every slot index is below 8)
+    if (found) lds_sub(p_cnt + (kC > 1 ? 4u * (hit >> 3) : 0u), 1u << (kC > 1 ? 4u * (hit & 7u) : hit4));
     if (fire && need_out) {
-      const uint32_t sl = uint32_t(free_s);
-      lds_add(my_pool + 4u * (sl >> 3), (uint32_t(cur.w) >> 24) << (4u * (sl & 7u)));
-      st32(my_pool + kEnds + 4u * sl, en);
-      st16(my_pool + kTags + 2u * sl, uint32_t(cur.y));
+      lds_add(my_cnt + (kC > 1 ? 4u * (sl >> 3) : 0u),
+              (uint32_t(cur.w) >> 24) << (4u * (kC > 1 ? (sl & 7u) : sl)));
+      st32(my_end() + 4u * sl, en);
+      st16(my_tag() + 2u * sl, uint32_t(cur.y));
     }
+
+    // ---- the record and id fetched after the previous round's advance: taken
+    // here, where they are first needed, so that the loads (issued at the end
+    // of that round) overlap this round's pool reads
+    if (take_rec) {
+      n0 = s0;
+      n1 = s1;
+      id2 = int(int16_t(s2_hi ? (s2 >> 16) : (s2 & 0xffffu)));
+    }
+    asm volatile("" : "+v"(n0.x), "+v"(n0.y), "+v"(n0.z), "+v"(n0.w), "+v"(n1.x), "+v"(n1.y),
+                 "+v"(id2)::"memory");
 
     // ---- register state
     bool fin = false;
@@ -277,14 +333,19 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     // fetch, for an advance, the record of the op after the new current one
     // and the id after that
     take_rec = adv;
+    // (a lane that did not advance reads the first record and the first word
+    // of the batch, one line shared by all such lanes; the ids of a candidate
+    // that reaches this kernel are in range, and the record table is read
+    // through its descriptor all the same)
     {
-      const int g = adv ? rb + clamp_id(id2) : 0;
+      const int g = adv ? rb + id2 : 0;
       s0 = rec_lo(g);
       s1 = rec_hi(g);
       // ids are read as aligned 32-bit words (rows are 16-byte aligned)
-      const int pos = rb + min(ptr + 2, last);
-      s2_hi = adv ? (pos & 1) : 0;
-      s2 = *reinterpret_cast<const uint32_t *>(adv ? row0 + (pos & ~1) : a.orders);
+      const uint32_t pos = uint32_t(min(rb2 + ptr, last_abs));
+      s2_hi = pos & 1u;
+      const gword_ptr wp = reinterpret_cast<gword_ptr>(reinterpret_cast<uint64_t>(row0)) + (pos >> 1);
+      s2 = *(adv ? wp : idle_w);
     }
 
     ++rnd;
