@@ -71,6 +71,7 @@ struct dip_sim {
   std::vector<int32_t> rank_of;        // [N] rank running each op
   std::vector<int32_t> n_cons;         // [N] consumers of each op
   bool pool_ok = false;                // topology fits the pool kernel
+  int32_t n_extra = 0;                 // pool kernel: edges after each op's first
   int pool_slots = 8, forced_pool_slots = 0;
   int4 *d_pool_rec = nullptr;          // pool records [N][2]
   int2 *d_pool_edge = nullptr;         // pool edges [E]
@@ -524,8 +525,8 @@ StageLayout stage_layout(const dip_sim *h) {
   L.md = off; off += align16(int64_t(h->N) * 4);
   L.rec16 = off; off += h->pipe_ok ? align16(int64_t(h->N) * 16) : 0;
   L.jk = off; off += h->pipe_ok ? align16(int64_t(std::max(h->n_joins, 1)) * 4) : 0;
-  L.prec8 = off; off += h->pool_ok ? align16(int64_t(h->N) * 32) : 0;
-  L.pedge = off; off += h->pool_ok ? align16(int64_t(std::max(h->E, 1)) * 8) : 0;
+  L.prec8 = off; off += h->pool_ok ? align16(int64_t(h->N) * 16) : 0;
+  L.pedge = off; off += h->pool_ok ? align16(int64_t(std::max(h->n_extra, 1)) * 8) : 0;
   L.total = off;
   return L;
 }
@@ -564,26 +565,30 @@ int upload_costs(dip_sim *h, const dip_costs *c, hipStream_t stream) {
     DIP_HIP(hipMemcpyAsync(h->d_md, md, size_t(h->N) * 4, hipMemcpyHostToDevice, stream));
   }
   if (h->pool_ok) {
-    // pool records {cost, item tag or 0, preds, first edge | readers << 24},
-    // {first edge word, comm}; edges {pred tag | pred rank << 16, comm}; tags
-    // are rank-local ids + 1
+    // pool records {cost, first edge's comm, first edge word | readers << 24,
+    // item tag or 0 | index of the op's extra edges << 16}; edge words are
+    // {pred tag | pred rank << 16 | last}; tags are rank-local ids + 1
     int4 *pr = reinterpret_cast<int4 *>(h->h_stage + L.prec8);
     int2 *pe = reinterpret_cast<int2 *>(h->h_stage + L.pedge);
-    for (int32_t e = 0; e < h->E; ++e) {
-      const int32_t p = h->pred_op[e];
+    auto word = [&](int32_t k, bool last) {
+      const int32_t p = h->pred_op[k];
       const int32_t rp = h->rank_of[p];
-      const uint32_t w = uint32_t(p - h->rank_off[rp] + 1) | (uint32_t(rp) << kEdgeRankShift);
-      pe[e] = make_int2(int32_t(w), c->edge_comm[e]);
-    }
+      return uint32_t(p - h->rank_off[rp] + 1) | (uint32_t(rp) << kEdgeRankShift) |
+             (last ? kEdgeLast : 0u);
+    };
+    int32_t xi = 0;
     for (int32_t g = 0; g < h->N; ++g) {
       const int32_t b = h->pred_ptr[g], np = h->pred_ptr[g + 1] - b;
       const int32_t tag = h->n_cons[g] > 0 ? g - h->rank_off[h->rank_of[g]] + 1 : 0;
-      pr[2 * g] = make_int4(c->op_cost[g], tag, np, int32_t(uint32_t(b) | (uint32_t(h->n_cons[g]) << 24)));
-      pr[2 * g + 1] = np > 0 ? make_int4(pe[b].x, pe[b].y, 0, 0) : make_int4(0, 0, 0, 0);
+      const uint32_t w0 = np > 0 ? word(b, np == 1) : kNoEdgeWord;
+      pr[g] = make_int4(c->op_cost[g], np > 0 ? c->edge_comm[b] : 0,
+                        int32_t(w0 | (uint32_t(h->n_cons[g]) << 24)),
+                        int32_t(uint32_t(tag) | (uint32_t(xi) << 16)));
+      for (int32_t k = 1; k < np; ++k) pe[xi++] = make_int2(int32_t(word(b + k, k == np - 1)), c->edge_comm[b + k]);
     }
-    DIP_HIP(hipMemcpyAsync(h->d_pool_rec, pr, size_t(h->N) * 32, hipMemcpyHostToDevice, stream));
-    if (h->E > 0)
-      DIP_HIP(hipMemcpyAsync(h->d_pool_edge, pe, size_t(h->E) * 8, hipMemcpyHostToDevice, stream));
+    DIP_HIP(hipMemcpyAsync(h->d_pool_rec, pr, size_t(h->N) * 16, hipMemcpyHostToDevice, stream));
+    if (h->n_extra > 0)
+      DIP_HIP(hipMemcpyAsync(h->d_pool_edge, pe, size_t(h->n_extra) * 8, hipMemcpyHostToDevice, stream));
   }
   h->pipe_costs_ok = false;
   if (h->pipe_ok) {
@@ -735,14 +740,18 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
     for (int r = 0; r < h->P; ++r)
       for (int32_t g = h->rank_off[r]; g < h->rank_off[r + 1]; ++g) rank_of[g] = r;
     // pool kernel eligibility: at most 15 consumers per op (4-bit reader
-    // counts), edge indices below 2^24 (tags are rank-local ids + 1 <= 32768
-    // by construction)
+    // counts), fewer than 2^16 edges after the ops' first ones (16-bit index
+    // in the record; tags are rank-local ids + 1 <= 32768 by construction)
     h->n_cons.assign(h->N, 0);
-    bool pool = h->E < (1 << 24) && int64_t(h->N) * 32 < INT32_MAX;
-    for (int32_t g = 0; g < h->N && pool; ++g)
+    bool pool = int64_t(h->N) * 16 < INT32_MAX;
+    int64_t extra = 0;
+    for (int32_t g = 0; g < h->N && pool; ++g) {
+      extra += std::max(h->pred_ptr[g + 1] - h->pred_ptr[g] - 1, 0);
       for (int32_t k = h->pred_ptr[g]; k < h->pred_ptr[g + 1]; ++k)
         if (++h->n_cons[h->pred_op[k]] > 15) pool = false;
-    h->pool_ok = pool;
+    }
+    h->pool_ok = pool && extra < (1 << 16);
+    h->n_extra = int32_t(std::min<int64_t>(extra, INT32_MAX));
     h->join_of.assign(h->N, -1);
     h->feeds_join.assign(h->N, -1);
     h->feed_edge.assign(h->N, -1);
@@ -783,8 +792,8 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
   if ((e = hipMalloc(&h->d_edge, size_t(std::max(h->E, 1)) * 8)) != hipSuccess) return hip_fail(e);
   if ((e = hipMalloc(&h->d_md, size_t(h->N) * 4)) != hipSuccess) return hip_fail(e);
   if (h->pool_ok) {
-    if ((e = hipMalloc(&h->d_pool_rec, size_t(h->N) * 32)) != hipSuccess) return hip_fail(e);
-    if ((e = hipMalloc(&h->d_pool_edge, size_t(std::max(h->E, 1)) * 8)) != hipSuccess)
+    if ((e = hipMalloc(&h->d_pool_rec, size_t(h->N) * 16)) != hipSuccess) return hip_fail(e);
+    if ((e = hipMalloc(&h->d_pool_edge, size_t(std::max(h->n_extra, 1)) * 8)) != hipSuccess)
       return hip_fail(e);
   }
   if (h->pipe_ok) {
@@ -944,8 +953,8 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     a.wpb = h->wpb;
     a.retry = h->d_retry;
     a.retry_count = h->d_retry_count;
-    a.rec_bytes = h->N * 32;
-    a.edge_bytes = std::max(h->E, 1) * 8;
+    a.rec_bytes = h->N * 16;
+    a.edge_bytes = std::max(h->n_extra, 1) * 8;
     a.round_limit = uint32_t(h->N) + uint32_t(h->E) + 16u;
     const int64_t per_block = int64_t(h->wpb) * h->G;
     const int blocks = int(std::min<int64_t>((n_cand + per_block - 1) / per_block, h->max_blocks));

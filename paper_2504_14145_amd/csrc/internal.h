@@ -155,10 +155,10 @@ struct PoolArgs {
   int32_t *out_ms;
   int32_t *out_bub;
   uint8_t *out_flags;       // the check kernel's verdicts, extended here
-  const int4 *rec;          // [N][2] {cost, item tag (rank-local id + 1) or 0, preds,
-                            //         first edge | readers << 24},
-                            //        {first edge word, its comm, 0, 0}
-  const int2 *edge;         // [E] {edge word, comm}
+  const int4 *rec;          // [N] {cost, first edge's comm,
+                            //      first edge word | readers << 24,
+                            //      item tag (rank-local id + 1) or 0 | extra edges << 16}
+  const int2 *edge;         // extra edges (an op's second to last), {edge word, comm}
   const int32_t *rank_off;  // [P+1]
   const int32_t *busy;      // [P]
   int32_t P, wpb;
@@ -171,9 +171,13 @@ struct PoolArgs {
 // dword 3 of a raw buffer descriptor on CDNA
 constexpr int kBufferWord3 = 0x00020000;
 
-// edge word: predecessor tag (its rank-local id + 1) | its rank << 16
+// edge word: predecessor tag (its rank-local id + 1) | its rank << 16 |
+// kEdgeLast on an op's last predecessor edge; an op without predecessors
+// starts on kNoEdgeWord (a tag no item carries, marked last)
 constexpr uint32_t kEdgeTagMask = 0xffffu;
 constexpr uint32_t kEdgeRankShift = 16;
+constexpr uint32_t kEdgeLast = 1u << 22;
+constexpr uint32_t kNoEdgeWord = kEdgeTagMask | kEdgeLast;
 
 // The pools of one candidate (a group of PW lanes, P <= PW ranks) in LDS, as
 // arrays over the ranks so that lanes reading their own or a neighbour's pool

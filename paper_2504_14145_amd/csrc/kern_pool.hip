@@ -118,16 +118,16 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   uint8_t fl = 0;     // the check kernel's flags for the candidate
   int ptr = 0;
   uint32_t tfree = 0, acc = 0;
-  int j = 0;
-  // no predecessor to wait for: a tag no item carries (items are tagged
-  // rank-local id + 1 <= 32768 < kEdgeTagMask; free slots hold 0 or a dead tag)
-  const int2 no_edge = make_int2(int(kEdgeTagMask), 0);
-  // record {cost, item tag (rank-local id + 1; 0: no consumers), preds,
-  //         first edge | readers << 24}
+  // nothing (more) to wait for: a tag no item carries (items are tagged
+  // rank-local id + 1 <= 32768 < kEdgeTagMask; free slots hold 0 or a dead
+  // tag), marked as the last edge
+  const int2 no_edge = make_int2(int(kNoEdgeWord), 0);
+  // record {cost, first edge's comm, first edge word | readers << 24,
+  //         item tag (rank-local id + 1; 0: no consumers) | extra edges << 16}
   int4 cur = make_int4(0, 0, 0, 0);
   int2 ce = no_edge;                      // current edge {pred edge word, comm}
-  int4 n0 = cur;                          // record of the op at ptr + 1 ...
-  int2 n1 = no_edge;                      // ... and its first edge
+  uint32_t ea = 0;                        // byte offset of the op's next extra edge
+  int4 n0 = cur;                          // record of the op at ptr + 1
   int id2 = 0;                            // id at ptr + 2
   const int16_t *row0 = a.orders;         // this candidate's row
   // the word read by lanes that did not advance, kept in registers (a select
@@ -148,25 +148,24 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
       __builtin_amdgcn_make_buffer_rsrc(const_cast<int4 *>(a.rec), 0, a.rec_bytes, kBufferWord3);
   const __amdgpu_buffer_rsrc_t edge_rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<int2 *>(a.edge), 0, a.edge_bytes, kBufferWord3);
-  auto rec_lo = [&](int g) {
-    const auto v = __builtin_amdgcn_raw_buffer_load_b128(rec_rs, uint32_t(g) * 32u, 0, 0);
+  auto rec_at = [&](int g) {
+    const auto v = __builtin_amdgcn_raw_buffer_load_b128(rec_rs, uint32_t(g) * 16u, 0, 0);
     return make_int4(int(v[0]), int(v[1]), int(v[2]), int(v[3]));
   };
-  auto rec_hi = [&](int g) {
-    const auto v = __builtin_amdgcn_raw_buffer_load_b64(rec_rs, uint32_t(g) * 32u + 16u, 0, 0);
+  auto edge_at = [&](uint32_t off) {   // byte offset
+    const auto v = __builtin_amdgcn_raw_buffer_load_b64(edge_rs, off, 0, 0);
     return make_int2(int(v[0]), int(v[1]));
   };
-  auto edge_at = [&](uint32_t e) {
-    const auto v = __builtin_amdgcn_raw_buffer_load_b64(edge_rs, e * 8u, 0, 0);
-    return make_int2(int(v[0]), int(v[1]));
-  };
+  // the first edge of a record, and the byte offset of its extra edges
+  auto first_edge = [](const int4 &rc) { return make_int2(rc.z, rc.y); };
+  auto extra_off = [](const int4 &rc) { return (uint32_t(rc.w) >> 16) * 8u; };
 
   // Global loads are staged: every round every lane issues the same loads
   // into the staging registers below (lanes with nothing to fetch read one
   // shared line), and only the next round moves what was fetched into place,
   // so no round waits for a load it issued itself.
   int4 s0 = n0;
-  int2 s1 = n1, se = no_edge;
+  int2 se = no_edge;
   uint32_t s2 = 0;      // the aligned 32-bit word holding the next id ...
   uint32_t s2_hi = 0;   // ... in its upper half
   bool take_rec = false, take_edge = false;
@@ -196,18 +195,16 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     ptr = 0;
     tfree = 0;
     acc = 0;
-    j = 0;
     if (on && nr > 0) {
       row0 = a.orders + cand * a.stride;
       const int16_t *row = row0 + rb;
       const int id0 = clamp_id(row[0]);
       const int id1 = clamp_id(row[min(1, last)]);
       id2 = row[min(2, last)];
-      cur = rec_lo(rb + id0);
-      const int2 c1 = rec_hi(rb + id0);
-      n0 = rec_lo(rb + id1);
-      n1 = rec_hi(rb + id1);
-      ce = cur.z > 0 ? c1 : no_edge;
+      cur = rec_at(rb + id0);
+      n0 = rec_at(rb + id1);
+      ce = first_edge(cur);
+      ea = extra_off(cur);
       act = true;
     }
   };
@@ -243,11 +240,10 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     uint32_t cnt[kC];   // my reader counts, 8 nibbles per word
 #pragma unroll
     for (int i = 0; i < kC; ++i) cnt[i] = ld32(my_cnt + 4u * i);
-    // prefetch the op's next edge (taken if this round finds the current one)
-    {
-      const bool more = act && j + 1 < cur.z;
-      se = edge_at(more ? uint32_t(cur.w & 0xffffff) + j + 1 : 0u);
-    }
+    // prefetch the op's next edge (taken if this round finds the current one;
+    // lanes on their last edge read the table's first entry)
+    const bool last_edge = (uint32_t(ce.x) & kEdgeLast) != 0u;
+    se = edge_at(act && !last_edge ? ea : 0u);
 
     // the matching slot, as index bits
     bool found = false, b0 = false, b1 = false, b2 = false, b3 = false;
@@ -282,9 +278,10 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
       }
     }
     const uint32_t acc_n = found ? max(acc, hit_v + uint32_t(ce.y)) : acc;
-    const int j_n = j + (found ? 1 : 0);
-    const bool ready = act && j_n >= cur.z;
-    const bool need_out = cur.y != 0;
+    // ready: the last edge found now, or none left to find (no predecessors,
+    // or the last one found in an earlier round)
+    const bool ready = act && (found ? last_edge : want == kEdgeTagMask);
+    const bool need_out = (uint32_t(cur.w) & 0xffffu) != 0u;
     const bool fire = ready && (!need_out || has_free);
     const bool held = ready && !fire;
     const uint32_t en = max(tfree, acc_n) + uint32_t(cur.x);
@@ -294,9 +291,9 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     if (found) lds_sub(p_cnt + (kC > 1 ? 4u * (hit >> 3) : 0u), 1u << (kC > 1 ? 4u * (hit & 7u) : hit4));
     if (fire && need_out) {
       lds_add(my_cnt + (kC > 1 ? 4u * (sl >> 3) : 0u),
-              (uint32_t(cur.w) >> 24) << (4u * (kC > 1 ? (sl & 7u) : sl)));
+              (uint32_t(cur.z) >> 24) << (4u * (kC > 1 ? (sl & 7u) : sl)));
       st32(my_end() + 4u * sl, en);
-      st16(my_tag() + 2u * sl, uint32_t(cur.y));
+      st16(my_tag() + 2u * sl, uint32_t(cur.w));
     }
 
     // ---- the record and id fetched after the previous round's advance: taken
@@ -304,11 +301,9 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     // of that round) overlap this round's pool reads
     if (take_rec) {
       n0 = s0;
-      n1 = s1;
       id2 = int(int16_t(s2_hi ? (s2 >> 16) : (s2 & 0xffffu)));
     }
-    asm volatile("" : "+v"(n0.x), "+v"(n0.y), "+v"(n0.z), "+v"(n0.w), "+v"(n1.x), "+v"(n1.y),
-                 "+v"(id2)::"memory");
+    asm volatile("" : "+v"(n0.x), "+v"(n0.y), "+v"(n0.z), "+v"(n0.w), "+v"(id2)::"memory");
 
     // ---- register state
     bool fin = false;
@@ -317,18 +312,23 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     if (fire) {
       tfree = en;
       acc = 0;
-      j = 0;
       ++ptr;
       fin = ptr == nr;
       act = !fin;
       adv = !fin;
-      ce = (adv && n0.z > 0) ? n1 : no_edge;
-      if (adv) cur = n0;
+      if (adv) {
+        cur = n0;
+        ce = first_edge(n0);
+        ea = extra_off(n0);
+      }
     } else if (found) {
       acc = acc_n;
-      j = j_n;
-      take_edge = j_n < cur.z;
-      if (!take_edge) ce = no_edge;
+      take_edge = !last_edge;
+      if (last_edge) {
+        ce = no_edge;
+      } else {
+        ea += 8u;
+      }
     }
     // fetch, for an advance, the record of the op after the new current one
     // and the id after that
@@ -339,8 +339,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     // through its descriptor all the same)
     {
       const int g = adv ? rb + id2 : 0;
-      s0 = rec_lo(g);
-      s1 = rec_hi(g);
+      s0 = rec_at(g);
       // ids are read as aligned 32-bit words (rows are 16-byte aligned)
       const uint32_t pos = uint32_t(min(rb2 + ptr, last_abs));
       s2_hi = pos & 1u;
