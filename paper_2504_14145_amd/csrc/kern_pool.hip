@@ -48,8 +48,8 @@ namespace {
 
 extern __shared__ __align__(16) unsigned char p_lds[];
 
-// a 32-bit word in global memory
-typedef const __attribute__((address_space(1))) uint32_t *gword_ptr;
+// 4 ids (8 bytes) in global memory
+typedef const __attribute__((address_space(1))) uint64_t *gblock_ptr;
 
 __device__ __forceinline__ uint32_t ld32(uint32_t addr) {
   return *reinterpret_cast<const uint32_t *>(p_lds + addr);
@@ -128,19 +128,30 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   int2 ce = no_edge;                      // current edge {pred edge word, comm}
   uint32_t ea = 0;                        // byte offset of the op's next extra edge
   int4 n0 = cur;                          // record of the op at ptr + 1
+  // ids come from 8-byte blocks of the row (4 ids): blk holds the block with
+  // the id at ptr + 2 (the order's last id past its end), nblk the block
+  // after it, loaded when the lane entered blk
   int id2 = 0;                            // id at ptr + 2
+  uint64_t blk = 0, nblk = 0;
   const int16_t *row0 = a.orders;         // this candidate's row
-  // the word read by lanes that did not advance, kept in registers (a select
+  // the block read by lanes that do not need one, kept in registers (a select
   // between two registers is one instruction), in the global address space
   // (a generic pointer would turn the load into a flat load, which every LDS
   // wait would then also wait for)
-  gword_ptr idle_w;
+  gblock_ptr idle_b;
   {
     const uint64_t v = reinterpret_cast<uint64_t>(a.orders);
     uint32_t lo = uint32_t(v), hi = uint32_t(v >> 32);
     asm volatile("" : "+v"(lo), "+v"(hi));
-    idle_w = reinterpret_cast<gword_ptr>(uint64_t(lo) | (uint64_t(hi) << 32));
+    idle_b = reinterpret_cast<gblock_ptr>(uint64_t(lo) | (uint64_t(hi) << 32));
   }
+  auto block_at = [&](uint32_t b) {   // block b of the candidate's row
+    return reinterpret_cast<gblock_ptr>(reinterpret_cast<uint64_t>(row0)) + b;
+  };
+  // the id at absolute position pos, from the block holding it
+  auto id_in = [](uint64_t bk, uint32_t pos) {
+    return int(uint32_t(bk >> ((pos & 3u) * 16u)) & 0xffffu);
+  };
   auto clamp_id = [&](int id) { return min(max(id, 0), last); };
   // records and edges through buffer descriptors: 32-bit byte offsets, and a
   // read past the end returns zeros instead of faulting
@@ -166,9 +177,8 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   // so no round waits for a load it issued itself.
   int4 s0 = n0;
   int2 se = no_edge;
-  uint32_t s2 = 0;      // the aligned 32-bit word holding the next id ...
-  uint32_t s2_hi = 0;   // ... in its upper half
-  bool take_rec = false, take_edge = false;
+  uint64_t sb = 0;     // a row block, for lanes that entered a new block
+  bool take_rec = false, take_edge = false, take_blk = false;
 
   // All lanes of the group call this together.
   auto start_candidate = [&]() {
@@ -178,6 +188,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     ce = no_edge;
     take_rec = false;
     take_edge = false;
+    take_blk = false;
     if (!has) return;
     fl = a.out_flags[cand];
     cand_round = rnd;
@@ -200,7 +211,10 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
       const int16_t *row = row0 + rb;
       const int id0 = clamp_id(row[0]);
       const int id1 = clamp_id(row[min(1, last)]);
-      id2 = row[min(2, last)];
+      const uint32_t pos2 = uint32_t(rb + min(2, last));
+      blk = *block_at(pos2 >> 2);
+      nblk = *block_at(min((pos2 >> 2) + 1u, uint32_t(last_abs) >> 2));
+      id2 = id_in(blk, pos2);
       cur = rec_at(rb + id0);
       n0 = rec_at(rb + id1);
       ce = first_edge(cur);
@@ -299,11 +313,9 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     // ---- the record and id fetched after the previous round's advance: taken
     // here, where they are first needed, so that the loads (issued at the end
     // of that round) overlap this round's pool reads
-    if (take_rec) {
-      n0 = s0;
-      id2 = int(int16_t(s2_hi ? (s2 >> 16) : (s2 & 0xffffu)));
-    }
-    asm volatile("" : "+v"(n0.x), "+v"(n0.y), "+v"(n0.z), "+v"(n0.w), "+v"(id2)::"memory");
+    if (take_rec) n0 = s0;
+    if (take_blk) nblk = sb;
+    asm volatile("" : "+v"(n0.x), "+v"(n0.y), "+v"(n0.z), "+v"(n0.w), "+v"(nblk)::"memory");
 
     // ---- register state
     bool fin = false;
@@ -333,18 +345,19 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     // fetch, for an advance, the record of the op after the new current one
     // and the id after that
     take_rec = adv;
-    // (a lane that did not advance reads the first record and the first word
-    // of the batch, one line shared by all such lanes; the ids of a candidate
-    // that reaches this kernel are in range, and the record table is read
-    // through its descriptor all the same)
     {
+      // the record of the op now at ptr + 1 (its id was at ptr + 2)
       const int g = adv ? rb + id2 : 0;
       s0 = rec_at(g);
-      // ids are read as aligned 32-bit words (rows are 16-byte aligned)
+      // the id now at ptr + 2; entering a new block, take the one fetched
+      // ahead and fetch the block after it
       const uint32_t pos = uint32_t(min(rb2 + ptr, last_abs));
-      s2_hi = pos & 1u;
-      const gword_ptr wp = reinterpret_cast<gword_ptr>(reinterpret_cast<uint64_t>(row0)) + (pos >> 1);
-      s2 = *(adv ? wp : idle_w);
+      const bool cross = adv && (pos & 3u) == 0u && rb2 + ptr <= last_abs;
+      if (cross) blk = nblk;
+      if (adv) id2 = id_in(blk, pos);
+      take_blk = cross;
+      const uint32_t nb = min((pos >> 2) + 1u, uint32_t(last_abs) >> 2);
+      sb = *(cross ? block_at(nb) : idle_b);
     }
 
     ++rnd;
