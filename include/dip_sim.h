@@ -135,7 +135,8 @@ int dip_sim_check_costs(const dip_topology *topo, const dip_costs *costs);
 int dip_sim_create(const dip_topology *topo, dip_sim **out);
 
 /* Force a kernel variant (0 = automatic choice) and waves per block
- * (0 = automatic).  DIP_E_UNSUPPORTED if the variant does not fit the device
+ * (0 = automatic; 1, 2 or 4, and 8 for the pool kernel when its tables fit in
+ * LDS).  DIP_E_UNSUPPORTED if the variant does not fit the device
  * or the topology.  General kernels (any dependence DAG): 1 tables, orders
  * and end times in LDS; 2 tables in global memory, orders and end times in
  * LDS; 3 end times in LDS only; 4 nothing in LDS (end times in device

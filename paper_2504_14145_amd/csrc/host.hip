@@ -72,6 +72,8 @@ struct dip_sim {
   std::vector<int32_t> n_cons;         // [N] consumers of each op
   bool pool_ok = false;                // topology fits the pool kernel
   int32_t n_extra = 0;                 // pool kernel: edges after each op's first
+  bool pool_tab = false;               // pool kernel: tables copied into LDS
+  int64_t pool_tab_bytes = 0;          // their bytes (records, then extra edges)
   int pool_slots = 8, forced_pool_slots = 0;
   int4 *d_pool_rec = nullptr;          // pool records [N][2]
   int2 *d_pool_edge = nullptr;         // pool edges [E]
@@ -158,14 +160,15 @@ int64_t lds_for(const dip_sim *h, int v, int wpb) {
     const int64_t per_wave = int64_t(h->G) * (int64_t(h->tab_stride) * 4 + h->stride * 2);
     return int64_t(wpb) * per_wave + (v == 7 ? align16(int64_t(h->N) * 16) : 0);
   }
-  if (v == 8) return int64_t(wpb) * h->G * pool_group_bytes(1 << h->pwl, h->pool_slots);
+  if (v == 8)
+    return h->pool_tab_bytes + int64_t(wpb) * h->G * pool_group_bytes(1 << h->pwl, h->pool_slots);
   return 0;
 }
 
 const void *kernel_ptr(const dip_sim *h, int v) {
   if (v <= 4) return general_kernel_ptr(v);
   if (v == 6) return pipe_kernel_ptr(h->pwl, true);
-  if (v == 8) return pool_kernel_ptr(h->pwl, h->pool_slots);
+  if (v == 8) return pool_kernel_ptr(h->pwl, h->pool_slots, h->pool_tab);
   return pipe_lds_kernel_ptr(h->pwl, v == 7);
 }
 
@@ -405,8 +408,9 @@ struct Pick {
 Pick best_of(dip_sim *h, int v_lo, int v_hi, int forced_wpb) {
   Pick best;
   for (int v = v_lo; v <= v_hi; ++v) {
-    for (int w : {4, 2, 1}) {
+    for (int w : {8, 4, 2, 1}) {
       if (forced_wpb && w != forced_wpb) continue;
+      if (w == 8 && !(v == 8 && h->pool_tab)) continue;   // only the tables-in-LDS pool kernel
       const int nb = blocks_per_cu(h, v, w);
       if (nb <= 0) continue;
       const int waves = nb * w;
@@ -752,6 +756,10 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
     }
     h->pool_ok = pool && extra < (1 << 16);
     h->n_extra = int32_t(std::min<int64_t>(extra, INT32_MAX));
+    // small tables go to each block's LDS, read once per block
+    const int64_t tab = align16(int64_t(h->N) * 16) + align16(int64_t(std::max(h->n_extra, 1)) * 8);
+    h->pool_tab = h->pool_ok && tab <= kPoolTabMax;
+    h->pool_tab_bytes = h->pool_tab ? tab : 0;
     h->join_of.assign(h->N, -1);
     h->feeds_join.assign(h->N, -1);
     h->feed_edge.assign(h->N, -1);
@@ -832,7 +840,7 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
 int dip_sim_configure(dip_sim *h, int32_t variant, int32_t waves_per_block) {
   if (!h || variant < 0 || variant > 8) return DIP_E_INVAL;
   if (!(waves_per_block == 0 || waves_per_block == 1 || waves_per_block == 2 ||
-        waves_per_block == 4))
+        waves_per_block == 4 || waves_per_block == 8))
     return DIP_E_INVAL;
   const int old_v = h->forced_variant, old_w = h->forced_wpb;
   h->forced_variant = variant;
@@ -955,10 +963,13 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     a.retry_count = h->d_retry_count;
     a.rec_bytes = h->N * 16;
     a.edge_bytes = std::max(h->n_extra, 1) * 8;
+    a.tab_edges = uint32_t(align16(int64_t(h->N) * 16));
+    a.pool_base = uint32_t(h->pool_tab_bytes);
     a.round_limit = uint32_t(h->N) + uint32_t(h->E) + 16u;
     const int64_t per_block = int64_t(h->wpb) * h->G;
     const int blocks = int(std::min<int64_t>((n_cand + per_block - 1) / per_block, h->max_blocks));
-    DIP_HIP(launch_pool(h->pwl, h->pool_slots, blocks, h->wpb, size_t(h->lds_bytes), stream, a));
+    DIP_HIP(launch_pool(h->pwl, h->pool_slots, h->pool_tab, blocks, h->wpb, size_t(h->lds_bytes),
+                        stream, a));
     DIP_HIP(mark(2));
 
     GeneralArgs f{};

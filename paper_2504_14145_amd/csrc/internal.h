@@ -166,18 +166,24 @@ struct PoolArgs {
   uint32_t *retry_count;
   int32_t rec_bytes, edge_bytes;  // sizes of rec and edge (buffer descriptors)
   uint32_t round_limit;           // rounds a candidate may take (N + E + 16)
+  uint32_t tab_edges;             // tables in LDS: byte offset of the extra edges
+  uint32_t pool_base;             // byte offset of the pools in LDS
 };
 
 // dword 3 of a raw buffer descriptor on CDNA
 constexpr int kBufferWord3 = 0x00020000;
 
 // edge word: predecessor tag (its rank-local id + 1) | its rank << 16 |
-// kEdgeLast on an op's last predecessor edge; an op without predecessors
-// starts on kNoEdgeWord (a tag no item carries, marked last)
+// kEdgeLast (the sign bit) on an op's last predecessor edge; an op without
+// predecessors starts on kNoEdgeWord (a tag no item carries, marked last).
+// In a pool record the word also carries the op's reader count in bits 24-27.
 constexpr uint32_t kEdgeTagMask = 0xffffu;
 constexpr uint32_t kEdgeRankShift = 16;
-constexpr uint32_t kEdgeLast = 1u << 22;
+constexpr uint32_t kEdgeLast = 1u << 31;
 constexpr uint32_t kNoEdgeWord = kEdgeTagMask | kEdgeLast;
+// the edge word of a lane with no op to run: a tag no item carries, not last
+// (so the lane is never ready)
+constexpr uint32_t kDeadEdgeWord = kEdgeTagMask - 1;
 
 // The pools of one candidate (a group of PW lanes, P <= PW ranks) in LDS, as
 // arrays over the ranks so that lanes reading their own or a neighbour's pool
@@ -204,8 +210,10 @@ __host__ __device__ constexpr int64_t pool_group_bytes(int pw, int slots) {
   return x;
 }
 bool pool_slots_ok(int slots);
-const void *pool_kernel_ptr(int pwl, int slots);
-hipError_t launch_pool(int pwl, int slots, int blocks, int wpb, size_t lds, hipStream_t s,
+// tables in LDS when they take at most this many bytes
+constexpr int64_t kPoolTabMax = 16384;
+const void *pool_kernel_ptr(int pwl, int slots, bool tab);
+hipError_t launch_pool(int pwl, int slots, bool tab, int blocks, int wpb, size_t lds, hipStream_t s,
                        const PoolArgs &a);
 
 // ---------------------------------------------------------------- argmin

@@ -76,8 +76,10 @@ __device__ __forceinline__ void lds_sub(uint32_t addr, uint32_t v) {
   (void)__hip_atomic_fetch_sub(lds_word(addr), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
 }
 
-template <int PWL, int S>
-__global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
+// TAB: the record and extra-edge tables are copied into the block's LDS (small
+// topologies), ahead of the pools; otherwise they are read from global memory.
+template <int PWL, int S, bool TAB>
+__global__ __launch_bounds__(TAB ? 512 : 256) void pool_kernel(PoolArgs a) {
   constexpr int PW = 1 << PWL;
   constexpr int G = kWave / PW;
   constexpr int kC = int(pool_count_words(S));   // count words per pool
@@ -93,7 +95,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   const bool on = r < a.P;
   const int gbit = grp << PWL;
   const int64_t n_slots = int64_t(gridDim.x) * a.wpb * G;
-  const uint32_t gbase = uint32_t(wave * G + grp) * kGroup;
+  const uint32_t gbase = a.pool_base + uint32_t(wave * G + grp) * kGroup;
   const uint32_t rr = uint32_t(on ? r : 0);
   const uint32_t my_cnt = gbase + rr * 4u * kC;
   // my tags and ends, from my counts' address and my rank (kept out of
@@ -122,10 +124,11 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   // rank-local id + 1 <= 32768 < kEdgeTagMask; free slots hold 0 or a dead
   // tag), marked as the last edge
   const int2 no_edge = make_int2(int(kNoEdgeWord), 0);
+  const int2 dead_edge = make_int2(int(kDeadEdgeWord), 0);   // no op to run
   // record {cost, first edge's comm, first edge word | readers << 24,
   //         item tag (rank-local id + 1; 0: no consumers) | extra edges << 16}
   int4 cur = make_int4(0, 0, 0, 0);
-  int2 ce = no_edge;                      // current edge {pred edge word, comm}
+  int2 ce = dead_edge;                    // current edge {pred edge word, comm}
   uint32_t ea = 0;                        // byte offset of the op's next extra edge
   int4 n0 = cur;                          // record of the op at ptr + 1
   // ids come from 8-byte blocks of the row (4 ids): blk holds the block with
@@ -159,13 +162,31 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
       __builtin_amdgcn_make_buffer_rsrc(const_cast<int4 *>(a.rec), 0, a.rec_bytes, kBufferWord3);
   const __amdgpu_buffer_rsrc_t edge_rs =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<int2 *>(a.edge), 0, a.edge_bytes, kBufferWord3);
-  auto rec_at = [&](int g) {
-    const auto v = __builtin_amdgcn_raw_buffer_load_b128(rec_rs, uint32_t(g) * 16u, 0, 0);
-    return make_int4(int(v[0]), int(v[1]), int(v[2]), int(v[3]));
+  if constexpr (TAB) {   // the tables into LDS, once per block
+    for (uint32_t i = threadIdx.x; i < uint32_t(a.rec_bytes) / 16u; i += blockDim.x)
+      *reinterpret_cast<int4 *>(p_lds + 16u * i) = a.rec[i];
+    for (uint32_t i = threadIdx.x; i < uint32_t(a.edge_bytes) / 8u; i += blockDim.x)
+      *reinterpret_cast<int2 *>(p_lds + a.tab_edges + 8u * i) = a.edge[i];
+    __syncthreads();
+  }
+  auto rec_at_off = [&](uint32_t off) {   // byte offset
+    if constexpr (TAB) {
+      const uint4 v = ld128(off);
+      return make_int4(int(v.x), int(v.y), int(v.z), int(v.w));
+    } else {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b128(rec_rs, off, 0, 0);
+      return make_int4(int(v[0]), int(v[1]), int(v[2]), int(v[3]));
+    }
   };
+  auto rec_at = [&](int g) { return rec_at_off(uint32_t(g) * 16u); };
   auto edge_at = [&](uint32_t off) {   // byte offset
-    const auto v = __builtin_amdgcn_raw_buffer_load_b64(edge_rs, off, 0, 0);
-    return make_int2(int(v[0]), int(v[1]));
+    if constexpr (TAB) {
+      const uint2 v = ld64(a.tab_edges + off);
+      return make_int2(int(v.x), int(v.y));
+    } else {
+      const auto v = __builtin_amdgcn_raw_buffer_load_b64(edge_rs, off, 0, 0);
+      return make_int2(int(v[0]), int(v[1]));
+    }
   };
   // the first edge of a record, and the byte offset of its extra edges
   auto first_edge = [](const int4 &rc) { return make_int2(rc.z, rc.y); };
@@ -185,7 +206,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     while (cand < a.n_cand && (a.out_flags[cand] & DIP_FLAG_INVALID)) cand += n_slots;
     has = cand < a.n_cand;
     act = false;
-    ce = no_edge;
+    ce = dead_edge;
     take_rec = false;
     take_edge = false;
     take_blk = false;
@@ -256,23 +277,28 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     for (int i = 0; i < kC; ++i) cnt[i] = ld32(my_cnt + 4u * i);
     // prefetch the op's next edge (taken if this round finds the current one;
     // lanes on their last edge read the table's first entry)
-    const bool last_edge = (uint32_t(ce.x) & kEdgeLast) != 0u;
+    const bool last_edge = ce.x < 0;   // kEdgeLast is the sign bit
     se = edge_at(act && !last_edge ? ea : 0u);
 
     // the matching slot, as index bits
-    bool found = false, b0 = false, b1 = false, b2 = false, b3 = false;
+    // (as wave masks: each compare's lanes, combined with scalar ops)
+    uint64_t m_found = 0, mb0 = 0, mb1 = 0, mb2 = 0, mb3 = 0;
 #pragma unroll
     for (int i = 0; i < S; ++i) {
       const uint32_t pair = tw[i / 2];
       const uint32_t t = (i & 1) ? (pair >> 16) : (pair & 0xffffu);
-      const bool m = t == want;
-      found = found || m;
-      if (i & 1) b0 = b0 || m;
-      if (i & 2) b1 = b1 || m;
-      if (i & 4) b2 = b2 || m;
-      if (i & 8) b3 = b3 || m;
+      const uint64_t m = __builtin_amdgcn_ballot_w64(t == want);
+      m_found |= m;
+      if (i & 1) mb0 |= m;
+      if (i & 2) mb1 |= m;
+      if (i & 4) mb2 |= m;
+      if (i & 8) mb3 |= m;
     }
-    const uint32_t hit4 = (b0 ? 4u : 0u) | (b1 ? 8u : 0u) | (b2 ? 16u : 0u) | (b3 ? 32u : 0u);   // 4 x slot
+    const bool found = __builtin_amdgcn_inverse_ballot_w64(m_found);
+    const uint32_t hit4 = (__builtin_amdgcn_inverse_ballot_w64(mb0) ? 4u : 0u) |
+                          (__builtin_amdgcn_inverse_ballot_w64(mb1) ? 8u : 0u) |
+                          (__builtin_amdgcn_inverse_ballot_w64(mb2) ? 16u : 0u) |
+                          (__builtin_amdgcn_inverse_ballot_w64(mb3) ? 32u : 0u);   // 4 x slot
     const uint32_t hit = hit4 >> 2;
     const uint32_t hit_v = ld32(p_end + hit4);
     // a slot is free when its reader count is zero: the first such slot (sl,
@@ -294,18 +320,23 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     const uint32_t acc_n = found ? max(acc, hit_v + uint32_t(ce.y)) : acc;
     // ready: the last edge found now, or none left to find (no predecessors,
     // or the last one found in an earlier round)
-    const bool ready = act && (found ? last_edge : want == kEdgeTagMask);
-    const bool need_out = (uint32_t(cur.w) & 0xffffu) != 0u;
-    const bool fire = ready && (!need_out || has_free);
-    const bool held = ready && !fire;
+    // (the decisions are taken on wave masks, one bit per lane, so that they
+    // cost scalar instructions only; a lane with no op to run is on the dead
+    // edge word, neither found nor last nor empty)
+    const uint64_t m_ready = (m_found & __builtin_amdgcn_ballot_w64(last_edge)) |
+                             (~m_found & __builtin_amdgcn_ballot_w64(want == kEdgeTagMask));
+    const uint64_t m_need = __builtin_amdgcn_ballot_w64((uint32_t(cur.w) & 0xffffu) != 0u);
+    const uint64_t m_fire = m_ready & (~m_need | __builtin_amdgcn_ballot_w64(has_free));
+    const bool fire = __builtin_amdgcn_inverse_ballot_w64(m_fire);
+    const bool held = __builtin_amdgcn_inverse_ballot_w64(m_ready & ~m_fire);
     const uint32_t en = max(tfree, acc_n) + uint32_t(cur.x);
 
     // ---- writes: release what was read, publish what was produced
     // (with one count word, every slot index is below 8)
     if (found) lds_sub(p_cnt + (kC > 1 ? 4u * (hit >> 3) : 0u), 1u << (kC > 1 ? 4u * (hit & 7u) : hit4));
-    if (fire && need_out) {
+    if (__builtin_amdgcn_inverse_ballot_w64(m_fire & m_need)) {
       lds_add(my_cnt + (kC > 1 ? 4u * (sl >> 3) : 0u),
-              (uint32_t(cur.z) >> 24) << (4u * (kC > 1 ? (sl & 7u) : sl)));
+              ((uint32_t(cur.z) >> 24) & 15u) << (4u * (kC > 1 ? (sl & 7u) : sl)));   // readers
       st32(my_end() + 4u * sl, en);
       st16(my_tag() + 2u * sl, uint32_t(cur.w));
     }
@@ -328,6 +359,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
       fin = ptr == nr;
       act = !fin;
       adv = !fin;
+      if (fin) ce.x = dead_edge.x;
       if (adv) {
         cur = n0;
         ce = first_edge(n0);
@@ -336,25 +368,23 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     } else if (found) {
       acc = acc_n;
       take_edge = !last_edge;
-      if (last_edge) {
-        ce = no_edge;
-      } else {
-        ea += 8u;
-      }
+      ea += 8u;   // (unused once the last edge is found)
+      // found the last edge but held: nothing left to find (the comm is read
+      // only with a found edge)
+      if (last_edge) ce.x = no_edge.x;
     }
     // fetch, for an advance, the record of the op after the new current one
     // and the id after that
     take_rec = adv;
     {
       // the record of the op now at ptr + 1 (its id was at ptr + 2)
-      const int g = adv ? rb + id2 : 0;
-      s0 = rec_at(g);
+      s0 = rec_at_off(adv ? uint32_t(rb + id2) * 16u : 0u);
       // the id now at ptr + 2; entering a new block, take the one fetched
       // ahead and fetch the block after it
       const uint32_t pos = uint32_t(min(rb2 + ptr, last_abs));
       const bool cross = adv && (pos & 3u) == 0u && rb2 + ptr <= last_abs;
       if (cross) blk = nblk;
-      if (adv) id2 = id_in(blk, pos);
+      id2 = id_in(blk, pos);   // (the same id again when the lane did not advance)
       take_blk = cross;
       const uint32_t nb = min((pos >> 2) + 1u, uint32_t(last_abs) >> 2);
       sb = *(cross ? block_at(nb) : idle_b);
@@ -368,7 +398,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     const uint64_t ev_done = g_has & ~g_run;
     uint64_t ev_stall = 0, ev_over = 0;
     if (stall_check) {
-      ev_stall = g_run & ~any_in_group<PWL>(__builtin_amdgcn_ballot_w64(fire || found));
+      ev_stall = g_run & ~any_in_group<PWL>(m_fire | m_found);
       // every round of a running group fires an op or reads an item, at most
       // N + E of them per candidate; a group past that bound is handed to the
       // general kernel rather than left running
@@ -379,7 +409,7 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
     if (ev == 0) continue;
 
     // ---- some groups finished their candidate
-    const uint64_t g_held = any_in_group<PWL>(__builtin_amdgcn_ballot_w64(held));
+    const uint64_t g_held = any_in_group<PWL>(__builtin_amdgcn_ballot_w64(held));   // (held as computed above)
     const bool mine_ev = (ev >> gbit) & 1;
     if (mine_ev) {
       const bool stalled = (ev_stall >> gbit) & 1;
@@ -406,29 +436,47 @@ __global__ __launch_bounds__(256) void pool_kernel(PoolArgs a) {
   }
 }
 
-template <int S>
+template <int S, bool TAB>
 const void *ptr_s(int pwl) {
   switch (pwl) {
-    case 0: return reinterpret_cast<const void *>(pool_kernel<0, S>);
-    case 1: return reinterpret_cast<const void *>(pool_kernel<1, S>);
-    case 2: return reinterpret_cast<const void *>(pool_kernel<2, S>);
-    case 3: return reinterpret_cast<const void *>(pool_kernel<3, S>);
-    case 4: return reinterpret_cast<const void *>(pool_kernel<4, S>);
-    case 5: return reinterpret_cast<const void *>(pool_kernel<5, S>);
-    default: return reinterpret_cast<const void *>(pool_kernel<6, S>);
+    case 0: return reinterpret_cast<const void *>(pool_kernel<0, S, TAB>);
+    case 1: return reinterpret_cast<const void *>(pool_kernel<1, S, TAB>);
+    case 2: return reinterpret_cast<const void *>(pool_kernel<2, S, TAB>);
+    case 3: return reinterpret_cast<const void *>(pool_kernel<3, S, TAB>);
+    case 4: return reinterpret_cast<const void *>(pool_kernel<4, S, TAB>);
+    case 5: return reinterpret_cast<const void *>(pool_kernel<5, S, TAB>);
+    default: return reinterpret_cast<const void *>(pool_kernel<6, S, TAB>);
   }
 }
 
-template <int S>
+template <int S, bool TAB>
 void launch_s(int pwl, dim3 grid, dim3 block, size_t lds, hipStream_t s, const PoolArgs &a) {
   switch (pwl) {
-    case 0: pool_kernel<0, S><<<grid, block, lds, s>>>(a); break;
-    case 1: pool_kernel<1, S><<<grid, block, lds, s>>>(a); break;
-    case 2: pool_kernel<2, S><<<grid, block, lds, s>>>(a); break;
-    case 3: pool_kernel<3, S><<<grid, block, lds, s>>>(a); break;
-    case 4: pool_kernel<4, S><<<grid, block, lds, s>>>(a); break;
-    case 5: pool_kernel<5, S><<<grid, block, lds, s>>>(a); break;
-    default: pool_kernel<6, S><<<grid, block, lds, s>>>(a); break;
+    case 0: pool_kernel<0, S, TAB><<<grid, block, lds, s>>>(a); break;
+    case 1: pool_kernel<1, S, TAB><<<grid, block, lds, s>>>(a); break;
+    case 2: pool_kernel<2, S, TAB><<<grid, block, lds, s>>>(a); break;
+    case 3: pool_kernel<3, S, TAB><<<grid, block, lds, s>>>(a); break;
+    case 4: pool_kernel<4, S, TAB><<<grid, block, lds, s>>>(a); break;
+    case 5: pool_kernel<5, S, TAB><<<grid, block, lds, s>>>(a); break;
+    default: pool_kernel<6, S, TAB><<<grid, block, lds, s>>>(a); break;
+  }
+}
+
+template <bool TAB>
+const void *ptr_t(int pwl, int slots) {
+  switch (slots) {
+    case 4: return ptr_s<4, TAB>(pwl);
+    case 16: return ptr_s<16, TAB>(pwl);
+    default: return ptr_s<8, TAB>(pwl);
+  }
+}
+
+template <bool TAB>
+void launch_t(int pwl, int slots, dim3 grid, dim3 block, size_t lds, hipStream_t s, const PoolArgs &a) {
+  switch (slots) {
+    case 4: launch_s<4, TAB>(pwl, grid, block, lds, s, a); break;
+    case 16: launch_s<16, TAB>(pwl, grid, block, lds, s, a); break;
+    default: launch_s<8, TAB>(pwl, grid, block, lds, s, a); break;
   }
 }
 
@@ -436,22 +484,17 @@ void launch_s(int pwl, dim3 grid, dim3 block, size_t lds, hipStream_t s, const P
 
 bool pool_slots_ok(int slots) { return slots == 4 || slots == 8 || slots == 16; }
 
-const void *pool_kernel_ptr(int pwl, int slots) {
-  switch (slots) {
-    case 4: return ptr_s<4>(pwl);
-    case 16: return ptr_s<16>(pwl);
-    default: return ptr_s<8>(pwl);
-  }
+const void *pool_kernel_ptr(int pwl, int slots, bool tab) {
+  return tab ? ptr_t<true>(pwl, slots) : ptr_t<false>(pwl, slots);
 }
 
-hipError_t launch_pool(int pwl, int slots, int blocks, int wpb, size_t lds, hipStream_t s,
+hipError_t launch_pool(int pwl, int slots, bool tab, int blocks, int wpb, size_t lds, hipStream_t s,
                        const PoolArgs &a) {
   const dim3 grid(blocks), block(wpb * kWave);
-  switch (slots) {
-    case 4: launch_s<4>(pwl, grid, block, lds, s, a); break;
-    case 16: launch_s<16>(pwl, grid, block, lds, s, a); break;
-    default: launch_s<8>(pwl, grid, block, lds, s, a); break;
-  }
+  if (tab)
+    launch_t<true>(pwl, slots, grid, block, lds, s, a);
+  else
+    launch_t<false>(pwl, slots, grid, block, lds, s, a);
   return hipGetLastError();
 }
 
