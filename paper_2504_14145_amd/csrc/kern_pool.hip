@@ -179,6 +179,20 @@ __global__ __launch_bounds__(TAB ? 512 : 256) void pool_kernel(PoolArgs a) {
     }
   };
   auto rec_at = [&](int g) { return rec_at_off(uint32_t(g) * 16u); };
+  // the record of this lane's op with rank-local id `id` (the lane's part of
+  // the table starts at its rank's first op)
+  const unsigned char *rec_lane = p_lds + 16u * uint32_t(rb);
+  const uint32_t rec_lane_off = 16u * uint32_t(rb);
+  // (for lanes with nothing to fetch: LDS reads the lane's first record;
+  // global reads the table's first record, one line shared by all such lanes)
+  auto rec_of = [&](bool fetch, uint32_t id) {
+    if constexpr (TAB) {
+      const uint4 v = *reinterpret_cast<const uint4 *>(rec_lane + 16u * (fetch ? id : 0u));
+      return make_int4(int(v.x), int(v.y), int(v.z), int(v.w));
+    } else {
+      return rec_at_off(fetch ? rec_lane_off + 16u * id : 0u);
+    }
+  };
   auto edge_at = [&](uint32_t off) {   // byte offset
     if constexpr (TAB) {
       const uint2 v = ld64(a.tab_edges + off);
@@ -323,7 +337,8 @@ __global__ __launch_bounds__(TAB ? 512 : 256) void pool_kernel(PoolArgs a) {
     // (the decisions are taken on wave masks, one bit per lane, so that they
     // cost scalar instructions only; a lane with no op to run is on the dead
     // edge word, neither found nor last nor empty)
-    const uint64_t m_ready = (m_found & __builtin_amdgcn_ballot_w64(last_edge)) |
+    const uint64_t m_last = __builtin_amdgcn_ballot_w64(last_edge);
+    const uint64_t m_ready = (m_found & m_last) |
                              (~m_found & __builtin_amdgcn_ballot_w64(want == kEdgeTagMask));
     const uint64_t m_need = __builtin_amdgcn_ballot_w64((uint32_t(cur.w) & 0xffffu) != 0u);
     const uint64_t m_fire = m_ready & (~m_need | __builtin_amdgcn_ballot_w64(has_free));
@@ -348,41 +363,42 @@ __global__ __launch_bounds__(TAB ? 512 : 256) void pool_kernel(PoolArgs a) {
     if (take_blk) nblk = sb;
     asm volatile("" : "+v"(n0.x), "+v"(n0.y), "+v"(n0.z), "+v"(n0.w), "+v"(nblk)::"memory");
 
-    // ---- register state
-    bool fin = false;
-    bool adv = false;
-    take_edge = false;
+    // ---- register state (fin: fired its last op; adv: fired another)
+    const uint64_t m_fin = m_fire & __builtin_amdgcn_ballot_w64(ptr + 1 == nr);
+    const bool fin = __builtin_amdgcn_inverse_ballot_w64(m_fin);
+    const bool adv = __builtin_amdgcn_inverse_ballot_w64(m_fire & ~m_fin);
+    take_edge = __builtin_amdgcn_inverse_ballot_w64(m_found & ~m_fire & ~m_last);
     if (fire) {
+      // (a lane that fired its last op copies a record it never uses)
       tfree = en;
       acc = 0;
       ++ptr;
-      fin = ptr == nr;
-      act = !fin;
-      adv = !fin;
-      if (fin) ce.x = dead_edge.x;
-      if (adv) {
-        cur = n0;
-        ce = first_edge(n0);
-        ea = extra_off(n0);
-      }
+      cur = n0;
+      ce = first_edge(n0);
+      ea = extra_off(n0);
     } else if (found) {
       acc = acc_n;
-      take_edge = !last_edge;
       ea += 8u;   // (unused once the last edge is found)
       // found the last edge but held: nothing left to find (the comm is read
       // only with a found edge)
       if (last_edge) ce.x = no_edge.x;
+    }
+    if (fin) {
+      act = false;
+      ce.x = dead_edge.x;
     }
     // fetch, for an advance, the record of the op after the new current one
     // and the id after that
     take_rec = adv;
     {
       // the record of the op now at ptr + 1 (its id was at ptr + 2)
-      s0 = rec_at_off(adv ? uint32_t(rb + id2) * 16u : 0u);
+      s0 = rec_of(adv, uint32_t(id2));
       // the id now at ptr + 2; entering a new block, take the one fetched
       // ahead and fetch the block after it
       const uint32_t pos = uint32_t(min(rb2 + ptr, last_abs));
-      const bool cross = adv && (pos & 3u) == 0u && rb2 + ptr <= last_abs;
+      // (past the order's end pos stays on its last id, and a crossing there
+      // takes and fetches that last block again)
+      const bool cross = adv && (pos & 3u) == 0u;
       if (cross) blk = nblk;
       id2 = id_in(blk, pos);   // (the same id again when the lane did not advance)
       take_blk = cross;
@@ -391,7 +407,7 @@ __global__ __launch_bounds__(TAB ? 512 : 256) void pool_kernel(PoolArgs a) {
     }
 
     ++rnd;
-    const uint64_t b_fin = __builtin_amdgcn_ballot_w64(fin);
+    const uint64_t b_fin = m_fin;
     const bool stall_check = (rnd & 7u) == 0u;
     if (!b_fin && !stall_check) continue;
     const uint64_t g_run = any_in_group<PWL>(__builtin_amdgcn_ballot_w64(act));
