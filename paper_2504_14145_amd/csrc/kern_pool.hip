@@ -206,10 +206,13 @@ __global__ __launch_bounds__(TAB ? 512 : 256) void pool_kernel(PoolArgs a) {
   auto first_edge = [](const int4 &rc) { return make_int2(rc.z, rc.y); };
   auto extra_off = [](const int4 &rc) { return (uint32_t(rc.w) >> 16) * 8u; };
 
-  // Global loads are staged: every round every lane issues the same loads
-  // into the staging registers below (lanes with nothing to fetch read one
-  // shared line), and only the next round moves what was fetched into place,
-  // so no round waits for a load it issued itself.
+  // Loads are staged: every round every lane issues the same loads into the
+  // staging registers below (lanes with nothing to fetch read one shared
+  // line), and a later point takes what was fetched: the next edge at the top
+  // of the next round, the record just before the next round's state update,
+  // the row block at the end of the next round (the order in which they are
+  // issued keeps each of those waits off the younger loads), so no round
+  // waits for a load it issued itself.
   int4 s0 = n0;
   int2 se = no_edge;
   uint64_t sb = 0;     // a row block, for lanes that entered a new block
@@ -360,8 +363,7 @@ __global__ __launch_bounds__(TAB ? 512 : 256) void pool_kernel(PoolArgs a) {
     // here, where they are first needed, so that the loads (issued at the end
     // of that round) overlap this round's pool reads
     if (take_rec) n0 = s0;
-    if (take_blk) nblk = sb;
-    asm volatile("" : "+v"(n0.x), "+v"(n0.y), "+v"(n0.z), "+v"(n0.w), "+v"(nblk)::"memory");
+    asm volatile("" : "+v"(n0.x), "+v"(n0.y), "+v"(n0.z), "+v"(n0.w)::"memory");
 
     // ---- register state (fin: fired its last op; adv: fired another)
     const uint64_t m_fin = m_fire & __builtin_amdgcn_ballot_w64(ptr + 1 == nr);
@@ -395,6 +397,9 @@ __global__ __launch_bounds__(TAB ? 512 : 256) void pool_kernel(PoolArgs a) {
       s0 = rec_of(adv, uint32_t(id2));
       // the id now at ptr + 2; entering a new block, take the one fetched
       // ahead and fetch the block after it
+      // the block fetched at the previous crossing, taken a full round after
+      // its load (just before sb is reloaded)
+      if (take_blk) nblk = sb;
       const uint32_t pos = uint32_t(min(rb2 + ptr, last_abs));
       // (past the order's end pos stays on its last id, and a crossing there
       // takes and fetches that last block again)
