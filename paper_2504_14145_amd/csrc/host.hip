@@ -236,24 +236,41 @@ int ensure_scratch(dip_sim *h, int v, int64_t need) {
 
 // The pool kernel's fallback: the general kernel with end tables in device
 // Tile check plan: the ranks split between the waves of a block, longest
-// section first onto the least loaded wave, as many waves as keep every wave
-// near the longest section (at most 16) and the block within 64 KiB of LDS
-// (one wave may take more, up to the device's limit).  Leaves tc_ok false
-// when a rank's section does not fit.
+// section first onto the least loaded wave.  The number of waves per block is
+// the one (up to 16, and not above the ranks or what keeps every wave near the
+// longest section) that keeps the most waves resident per CU.  Leaves tc_ok
+// false when a rank's section does not fit.
 int plan_tile_check(dip_sim *h) {
   h->tc_ok = false;
   int32_t max_nr = 0;
   for (int r = 0; r < h->P; ++r) max_nr = std::max(max_nr, h->n_ops[r]);
   if (int64_t(h->stride) * 2 * kWave > int64_t(INT32_MAX)) return DIP_OK;
   const int64_t region = tile_region_bytes(max_nr);
-  int nw = int(std::min<int64_t>({16, int64_t(h->P),
-                                  (int64_t(h->N) + std::max(max_nr, 1) - 1) / std::max(max_nr, 1)}));
-  nw = int(std::min<int64_t>(nw, (65536 - kTileFlagBytes) / region));
-  if (nw < 1) {
-    if (kTileFlagBytes + region > h->lds_block_max) return DIP_OK;
-    nw = 1;
+  const int nw_max = int(std::min<int64_t>(
+      {16, int64_t(h->P), (int64_t(h->N) + std::max(max_nr, 1) - 1) / std::max(max_nr, 1)}));
+  int nw = 0, nb = 0, best_waves = 0;
+  for (int w = 1; w <= std::max(nw_max, 1); ++w) {
+    const int64_t lds = kTileFlagBytes + int64_t(w) * region;
+    if (lds > h->lds_block_max) break;
+    if (lds > 65536 && hipFuncSetAttribute(tile_check_kernel_ptr(),
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           int(lds)) != hipSuccess) {
+      (void)hipGetLastError();
+      break;
+    }
+    int b = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, tile_check_kernel_ptr(), w * kWave,
+                                                     size_t(lds)) != hipSuccess) {
+      (void)hipGetLastError();
+      break;
+    }
+    if (b > 0 && b * w >= best_waves) {
+      best_waves = b * w;
+      nw = w;
+      nb = b;
+    }
   }
-  nw = std::max(nw, 1);
+  if (nw == 0) return DIP_OK;
   std::vector<int32_t> order(h->P), load(nw, 0), wave_of(h->P, 0);
   for (int r = 0; r < h->P; ++r) order[r] = r;
   std::stable_sort(order.begin(), order.end(),
@@ -275,13 +292,6 @@ int plan_tile_check(dip_sim *h) {
   if (lds > 65536 && hipFuncSetAttribute(tile_check_kernel_ptr(),
                                          hipFuncAttributeMaxDynamicSharedMemorySize,
                                          int(lds)) != hipSuccess) {
-    (void)hipGetLastError();
-    return DIP_OK;
-  }
-  int nb = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, tile_check_kernel_ptr(), nw * kWave,
-                                                   size_t(lds)) != hipSuccess ||
-      nb <= 0) {
     (void)hipGetLastError();
     return DIP_OK;
   }

@@ -135,12 +135,13 @@ struct TileCheckArgs {
 };
 
 // LDS of a tile-check block: the 64 candidates' flag words, then the waves'
-// regions
+// regions (deltas and bits of ids 0 .. max_nr, the last one the overflow
+// entry; then the staging of 8 units of the 64 rows)
 constexpr int kTileFlagBytes = 256;
-// (deltas and bits of ids 0 .. max_nr: the last one the overflow entry)
+constexpr int kTileStageBytes = 64 * 8 * 16;
 __host__ __device__ inline int32_t tile_md_bytes(int32_t max_nr) { return ((max_nr + 1) * 4 + 15) & ~15; }
 __host__ __device__ inline int32_t tile_region_bytes(int32_t max_nr) {
-  return tile_md_bytes(max_nr) + ((max_nr + 32) / 32) * 64 * 4;
+  return tile_md_bytes(max_nr) + ((max_nr + 32) / 32) * 64 * 4 + kTileStageBytes;
 }
 const void *tile_check_kernel_ptr();
 hipError_t launch_tile_check(int blocks, int nw, size_t lds, hipStream_t s, const TileCheckArgs &a);

@@ -186,6 +186,10 @@ __global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
   unsigned char *region = c_lds + kTileFlagBytes + wave * a.region_bytes;
   int32_t *mdl = reinterpret_cast<int32_t *>(region);
   uint32_t *bm = reinterpret_cast<uint32_t *>(region + a.md_bytes) + lane;   // word w at bm[64 w]
+  // staging of 8 units of the 64 rows (8 KB), unit k of row l at slot
+  // k ^ (l & 7) of the row's 8, so the reads of one unit by 8 lanes hit 8
+  // distinct bank groups
+  unsigned char *stg = region + a.region_bytes - kTileStageBytes;
   if (a.retry_count && blockIdx.x == 0 && threadIdx.x == 0) *a.retry_count = 0u;
 
   const int kb = a.plan[wave], ke = a.plan[wave + 1];
@@ -207,7 +211,6 @@ __global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
     const __amdgpu_buffer_rsrc_t rows = __builtin_amdgcn_make_buffer_rsrc(
         reinterpret_cast<void *>(base_u), 0,
         __builtin_amdgcn_readfirstlane(int(uint32_t(n_live) * row_bytes)), kBufferWord3);
-    const uint32_t voff = uint32_t(live ? lane : n_live - 1) * row_bytes;
     uint32_t fl = 0;
     for (int k = kb; k < ke; ++k) {
       const int r = ranks[k];
@@ -251,10 +254,6 @@ __global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
       };
       if (nr > 0) {
         const int u0 = rb >> 3, u1 = (re - 1) >> 3;   // first and last unit of 8 ids
-        auto ld = [&](int u) {
-          const auto x = __builtin_amdgcn_raw_buffer_load_b128(rows, voff, uint32_t(min(u, u1)) * 16u, 0);
-          return make_uint4(uint32_t(x[0]), uint32_t(x[1]), uint32_t(x[2]), uint32_t(x[3]));
-        };
         auto step = [&](int u, const uint4 v) {
           const int lo = max(rb - 8 * u, 0), hi = min(re - 8 * u, 8);
           if (lo == 0 && hi == 8)
@@ -262,19 +261,37 @@ __global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
           else
             unit(v, lo, hi);
         };
-        // four units per iteration, the next four loaded one iteration ahead
-        uint4 b[4];
+        // Rows are read 8 units (128 bytes) at a time, cooperatively: load i
+        // brings rows 8i .. 8i+7, lane l reading unit (l & 7) of row
+        // 8i + (l >> 3), so 8 lanes share each line; the units go through
+        // the wave's staging area to the lane that owns the row.  A lane past
+        // the end of the batch reads the last row; units past the section
+        // are read (clamped to its last unit) but not processed.
+        auto load_chunk = [&](int cu, uint4 (&r)[8]) {
+          const uint32_t ub = uint32_t(min(cu + (lane & 7), u1)) * 16u;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) b[i] = ld(u0 + i);
-        for (int u = u0; u <= u1; u += 4) {
-          uint4 nb[4];
+          for (int i = 0; i < 8; ++i) {
+            const uint32_t row = uint32_t(min(8 * i + (lane >> 3), n_live - 1));
+            const auto x = __builtin_amdgcn_raw_buffer_load_b128(rows, row * row_bytes + ub, 0, 0);
+            r[i] = make_uint4(uint32_t(x[0]), uint32_t(x[1]), uint32_t(x[2]), uint32_t(x[3]));
+          }
+        };
+        const uint32_t put = uint32_t(((lane >> 3) * 8 + ((lane & 7) ^ ((lane >> 3) & 7))) * 16);
+        uint4 nb[8];
+        load_chunk(u0, nb);
+        for (int cu = u0; cu <= u1; cu += 8) {
+          wave_sync();   // the previous chunk's reads are done
 #pragma unroll
-          for (int i = 0; i < 4; ++i) nb[i] = ld(u + 4 + i);
+          for (int i = 0; i < 8; ++i) *reinterpret_cast<uint4 *>(stg + 1024u * i + put) = nb[i];
+          wave_sync();
+          uint4 b[8];
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
-            if (u + i <= u1) step(u + i, b[i]);
+          for (int q = 0; q < 8; ++q)
+            b[q] = *reinterpret_cast<const uint4 *>(stg + uint32_t((lane * 8 + (q ^ (lane & 7))) * 16));
+          if (cu + 8 <= u1) load_chunk(cu + 8, nb);   // the next chunk, while this one runs
 #pragma unroll
-          for (int i = 0; i < 4; ++i) b[i] = nb[i];
+          for (int q = 0; q < 8; ++q)
+            if (cu + q <= u1) step(cu + q, b[q]);
         }
       }
       uint32_t bits = 0;
