@@ -978,6 +978,12 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     a.round_limit = uint32_t(h->N) + uint32_t(h->E) + 16u;
     const int64_t per_block = int64_t(h->wpb) * h->G;
     const int blocks = int(std::min<int64_t>((n_cand + per_block - 1) / per_block, h->max_blocks));
+    // candidates past the resident slots: handed out on demand when every
+    // slot runs several in sequence (fixed successors let unlucky slots pile
+    // up long candidates); with fewer, fixed successors keep the second ones
+    // in few waves, and the other waves exit
+    const int64_t n_slots = int64_t(blocks) * per_block;
+    a.next_cand = n_cand >= 2 * n_slots ? h->d_retry_count + 1 : nullptr;
     DIP_HIP(launch_pool(h->pwl, h->pool_slots, h->pool_tab, blocks, h->wpb, size_t(h->lds_bytes),
                         stream, a));
     DIP_HIP(mark(2));

@@ -103,7 +103,8 @@ struct CheckArgs {
   const int32_t *rank_off;  // [P+1]
   const int32_t *cap;       // [P]
   int32_t P, N, wpb;
-  uint32_t *retry_count;    // zeroed by the kernel when not null
+  uint32_t *retry_count;    // [2] zeroed by the kernel when not null (the pool
+                            // kernel's retry count and candidate counter)
 };
 
 // bytes of one candidate's op-id bitmap
@@ -131,7 +132,8 @@ struct TileCheckArgs {
   int32_t P, nw;
   int32_t md_bytes;         // bytes of a wave's delta area (16-aligned)
   int32_t region_bytes;     // bytes per wave: delta area + bitmap of 64 lanes
-  uint32_t *retry_count;    // zeroed by the kernel when not null
+  uint32_t *retry_count;    // [2] zeroed by the kernel when not null (the pool
+                            // kernel's retry count and candidate counter)
 };
 
 // LDS of a tile-check block: the 64 candidates' flag words, then the waves'
@@ -169,6 +171,8 @@ struct PoolArgs {
   uint32_t round_limit;           // rounds a candidate may take (N + E + 16)
   uint32_t tab_edges;             // tables in LDS: byte offset of the extra edges
   uint32_t pool_base;             // byte offset of the pools in LDS
+  uint32_t *next_cand;            // null: slot k takes k, k + n_slots, ...; else a
+                                  // counter of the candidates handed out past n_slots
 };
 
 // dword 3 of a raw buffer descriptor on CDNA

@@ -218,9 +218,20 @@ __global__ __launch_bounds__(TAB ? 512 : 256) void pool_kernel(PoolArgs a) {
   uint64_t sb = 0;     // a row block, for lanes that entered a new block
   bool take_rec = false, take_edge = false, take_blk = false;
 
+  // Candidates: group slot k (of n_slots) starts on candidate k; the later
+  // ones are either its fixed successors k + n_slots, k + 2 n_slots, ... or,
+  // with a.next_cand, handed out in the order groups ask for them.  All lanes
+  // of the group call this together.
+  auto next_cand = [&]() -> int64_t {
+    if (!a.next_cand) return cand + n_slots;
+    uint32_t k = 0;
+    if (r == 0) k = atomicAdd(a.next_cand, 1u);
+    k = uint32_t(__shfl(int(k), gbit, kWave));
+    return n_slots + int64_t(k);
+  };
   // All lanes of the group call this together.
   auto start_candidate = [&]() {
-    while (cand < a.n_cand && (a.out_flags[cand] & DIP_FLAG_INVALID)) cand += n_slots;
+    while (cand < a.n_cand && (a.out_flags[cand] & DIP_FLAG_INVALID)) cand = next_cand();
     has = cand < a.n_cand;
     act = false;
     ce = dead_edge;
@@ -450,7 +461,7 @@ __global__ __launch_bounds__(TAB ? 512 : 256) void pool_kernel(PoolArgs a) {
           if (stalled) a.out_flags[cand] = uint8_t(fl | DIP_FLAG_DEADLOCK);
         }
       }
-      cand += n_slots;
+      cand = next_cand();
       start_candidate();
     }
     g_has = any_in_group<PWL>(__builtin_amdgcn_ballot_w64(has));
