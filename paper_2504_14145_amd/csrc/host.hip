@@ -98,6 +98,8 @@ struct dip_sim {
   int tc_blocks_per_cu = 1;
   int32_t *d_tc_plan = nullptr;        // [nw+1] offsets, then [P] ranks
   void *d_scratch_fb = nullptr;        // general kernel (list mode) end tables
+  int fb_variant = 4;                  // retry kernel: 3 (end times in LDS) when they fit, else 4
+  int64_t fb_lds = 0;
   int64_t scratch_fb_bytes = 0;
   int fb_blocks = 1;
   // device tables
@@ -308,6 +310,25 @@ int plan_tile_check(dip_sim *h) {
 // scratch (variant 4), one wave per block, in list mode.
 int ensure_fallback(dip_sim *h) {
   h->fb_blocks = h->n_cu;
+  // the retry kernel keeps its candidates' end times in LDS when one wave's
+  // tables fit (much shorter waits per op than device scratch)
+  h->fb_variant = 4;
+  h->fb_lds = 0;
+  {
+    const int64_t lds3 = lds_for(h, 3, 1);
+    int nb3 = 0;
+    if (lds3 <= h->lds_block_max &&
+        (lds3 <= 65536 || hipFuncSetAttribute(general_kernel_ptr(3),
+                                              hipFuncAttributeMaxDynamicSharedMemorySize,
+                                              int(lds3)) == hipSuccess) &&
+        hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb3, general_kernel_ptr(3), kWave,
+                                                     size_t(lds3)) == hipSuccess &&
+        nb3 > 0) {
+      h->fb_variant = 3;
+      h->fb_lds = lds3;
+    }
+    (void)hipGetLastError();
+  }
   const int64_t need = int64_t(h->fb_blocks) * h->G * int64_t(h->N) * 4;
   if (need > h->scratch_fb_bytes) {
     if (h->d_scratch_fb) {
@@ -1010,7 +1031,7 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     f.wpb = 1;
     f.list = h->d_retry;
     f.list_count = h->d_retry_count;
-    DIP_HIP(launch_general(4, h->fb_blocks, 1, 0, stream, f));
+    DIP_HIP(launch_general(h->fb_variant, h->fb_blocks, 1, size_t(h->fb_lds), stream, f));
     DIP_HIP(mark(3));
     if (!h->forced_pool_slots && h->pool_slots < 16 && !h->retry_seen_pending) {
       if (!h->h_retry_seen) {
