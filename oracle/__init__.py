@@ -3,8 +3,9 @@
 TEST INFRASTRUCTURE ONLY: the test suite, the smoke check and the benchmark's
 CPU-baseline leg are the only callers.  The GPU library never loads it, and it
 shares no code with the GPU library.  The simulator itself is ``dip_oracle.c``
-(a single-threaded discrete-event simulation per candidate); its header states
-what it computes and which passages of the paper each step follows.
+(a single-threaded discrete-event simulation per candidate) and the dual-queue
+stage interleaving is ``dip_greedy.c``; each header states what it computes
+and which passages of the paper each step follows.
 """
 from __future__ import annotations
 
@@ -16,7 +17,7 @@ from dataclasses import dataclass
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "dip_oracle.c")
+_SRCS = [os.path.join(_HERE, "dip_oracle.c"), os.path.join(_HERE, "dip_greedy.c")]
 _LIB = os.path.join(_HERE, "libdip_oracle.so")
 
 FLAG_DEADLOCK = 1
@@ -28,7 +29,7 @@ def build(force: bool = True) -> str:
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-shared",
-                               "-fPIC", "-pthread", "-o", tmp, _SRC])
+                               "-fPIC", "-pthread", "-o", tmp] + _SRCS)
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -59,6 +60,12 @@ def _load():
         lib.dor_timeline.argtypes = [ctypes.POINTER(_Inst), vp, vp, vp, vp, vp, vp, vp]
         lib.dor_argmin.restype = ctypes.c_int64
         lib.dor_argmin.argtypes = [vp, vp, ctypes.c_int64, ctypes.c_int64, vp]
+        lib.dgr_greedy.restype = ctypes.c_int
+        lib.dgr_greedy.argtypes = [ctypes.POINTER(_Inst), vp, ctypes.c_int32, vp, ctypes.c_int64,
+                                   ctypes.c_int64, vp, vp, vp, vp, vp, ctypes.c_int32]
+        lib.dgr_greedy_timeline.restype = ctypes.c_int
+        lib.dgr_greedy_timeline.argtypes = [ctypes.POINTER(_Inst), vp, vp, vp, vp, vp, vp, vp,
+                                            vp, vp]
         _lib = lib
     return _lib
 
@@ -156,3 +163,64 @@ def argmin(makespan: np.ndarray, flags: np.ndarray, index_base: int = 0):
     idx = _load().dor_argmin(ms.ctypes.data, fl.ctypes.data, ms.size, int(index_base),
                              best.ctypes.data)
     return int(idx), int(best[0])
+
+
+def _groups(inst, op_group, n_groups):
+    g = np.ascontiguousarray(op_group, np.int32).reshape(-1)
+    if g.size != inst.n_total:
+        raise ValueError("op_group needs one entry per op")
+    if g.size and (g.min() < 0 or g.max() >= n_groups):
+        raise ValueError("op_group entries must lie in [0, n_groups)")
+    return g
+
+
+def greedy(prob, op_group, n_groups: int, prio: np.ndarray, stride: int | None = None,
+           threads: int = 1):
+    """Dual-queue interleaving (Sec. 5.2) of every candidate priority row.
+
+    ``prio`` is int32 [n, n_groups] (larger first).  Returns (orders int16
+    [n, stride], Result) where Result is the greedy's own timeline summary."""
+    inst = _inst(prob)
+    g = _groups(inst, op_group, n_groups)
+    prio = np.ascontiguousarray(prio, np.int32)
+    if prio.ndim == 1:
+        prio = prio[None, :]
+    n = prio.shape[0]
+    if prio.shape[1] != n_groups:
+        raise ValueError("prio needs one column per group")
+    stride = inst.n_total if stride is None else int(stride)
+    P = inst.P
+    orders = np.zeros((n, max(stride, 1)), np.int16)
+    res = Result(np.zeros(n, np.int32), np.zeros((n, P), np.int32),
+                 np.zeros((n, P), np.int32), np.zeros(n, np.uint8))
+    rc = _load().dgr_greedy(ctypes.byref(inst.c), g.ctypes.data, int(n_groups),
+                            prio.ctypes.data, n, orders.shape[1], orders.ctypes.data,
+                            res.makespan.ctypes.data, res.bubble.ctypes.data,
+                            res.peak.ctypes.data, res.flags.ctypes.data, int(threads))
+    if rc != 0:
+        raise RuntimeError(f"greedy oracle failed with code {rc}")
+    return orders[:, :stride], res
+
+
+def greedy_timeline(prob, op_group, n_groups: int, prio: np.ndarray):
+    """One candidate: (order int16 [N], Result of size 1, start[N], end[N])."""
+    inst = _inst(prob)
+    g = _groups(inst, op_group, n_groups)
+    prio = np.ascontiguousarray(prio, np.int32).reshape(-1)
+    if prio.size != n_groups:
+        raise ValueError("prio needs one entry per group")
+    N, P = inst.n_total, inst.P
+    order = np.zeros(max(N, 1), np.int16)
+    ms = np.zeros(1, np.int32)
+    bub = np.zeros((1, P), np.int32)
+    pk = np.zeros((1, P), np.int32)
+    fl = np.zeros(1, np.uint8)
+    st = np.zeros(max(N, 1), np.int32)
+    en = np.zeros(max(N, 1), np.int32)
+    rc = _load().dgr_greedy_timeline(ctypes.byref(inst.c), g.ctypes.data, prio.ctypes.data,
+                                     order.ctypes.data, ms.ctypes.data, bub.ctypes.data,
+                                     pk.ctypes.data, fl.ctypes.data, st.ctypes.data,
+                                     en.ctypes.data)
+    if rc != 0:
+        raise RuntimeError(f"greedy oracle failed with code {rc}")
+    return order[:N], Result(ms, bub, pk, fl), st[:N], en[:N]

@@ -18,3 +18,6 @@ __all__ = [
     "pipeline_instance", "MODE_1F1B", "MODE_LIST", "OrderGenerator", "build",
     "generator_for", "gpipe_rank", "one_f_one_b_rank", "op_id", "pack", "unpack",
 ]
+from .priorities import fifo_priorities, priority_groups, rollout_priorities  # noqa: E402
+
+__all__ += ["fifo_priorities", "priority_groups", "rollout_priorities"]
