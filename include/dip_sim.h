@@ -20,6 +20,9 @@
  *                       ("bubble"), per-rank peak activation memory, flags;
  *   dip_sim_argmin   -- fold the best (makespan, index) of a batch into a
  *                       running 64-bit key, so chunked batches reduce exactly;
+ *   dip_sim_greedy   -- build candidates instead of reading them: Sec. 5.2's
+ *                       dual-queue interleaving of one priority vector per
+ *                       candidate, with the same outputs as evaluate;
  *   dip_sim_destroy.
  *
  * Semantics per candidate (all integers; results are exact):
@@ -56,7 +59,7 @@
 extern "C" {
 #endif
 
-#define DIP_SIM_ABI_VERSION 3
+#define DIP_SIM_ABI_VERSION 4
 
 enum {
   DIP_OK = 0,
@@ -204,12 +207,47 @@ int dip_sim_argmin(dip_sim *h, const int32_t *makespan, const uint8_t *flags,
                    int64_t n_cand, int64_t index_base, uint64_t *inout_best_key,
                    void *stream);
 
+/* Dual-queue stage interleaving (Sec. 5.2), set-up.  op_group[N] (host,
+ * read during the call) puts every op in one of n_groups priority groups --
+ * Sec. 5.1's pipeline segments, which the candidates of dip_sim_greedy
+ * prioritise.  A group holds ops of one kind, at most one per rank; the data
+ * edges must be acyclic.  1 <= n_groups <= 65535, and at most 512 groups of
+ * either kind.  DIP_E_TOPO if a rule is broken, DIP_E_UNSUPPORTED if the
+ * groups or the per-candidate tables do not fit the kernel.  Replaces any
+ * earlier grouping; the next dip_sim_greedy call must then pass costs. */
+int dip_sim_configure_greedy(dip_sim *h, int32_t n_groups, const int32_t *op_group);
+
+/* Build and score one candidate per priority vector.
+ *   prio        device, int32 [n_cand][n_groups]: larger is scheduled first;
+ *               equal priorities go by group index, then by rank-local id.
+ *   costs       as in evaluate (NULL reuses the last ones; DIP_E_STATE if the
+ *               records of this grouping were never built).
+ *   out_orders  device int16 [n_cand][cand_stride], the orders the greedy
+ *               emits (evaluate's layout; entries past N untouched), or NULL.
+ *   out_*       as evaluate's, for the emitted orders: the greedy's own
+ *               timeline equals the simulation of those orders.
+ * Per rank the greedy keeps t_last (end of its last stage) and its queued
+ * stages (all predecessors scheduled), each with t_start = max over
+ * predecessors of end + comm (0 without any).  A rank's next start is
+ * t_min = max(t_last, least queued t_start).  If a forward and a backward
+ * were both queued before t_last it alternates kinds (1F1B); otherwise it
+ * takes the highest-priority stage able to start at t_min.  A forward that
+ * would raise the rank's live activation (forwards scheduled, backwards not
+ * yet) above a cap >= 0 disables the forward queue for that decision.  The
+ * rank with the least t_min (lowest index on ties) schedules its stage; if
+ * every rank is held back by its cap, the cap is lifted for one decision and
+ * the result is flagged DIP_FLAG_CAP.  flags is otherwise 0.  Enqueued on
+ * stream; n_cand == 0 is a no-op; n_cand <= 2^31 - 1. */
+int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int64_t n_cand,
+                   int16_t *out_orders, int32_t *out_makespan, int32_t *out_bubble,
+                   int32_t *out_peakmem, uint8_t *out_flags, void *stream);
+
 /* Per-kernel timing of evaluate (for measurement).  With enable != 0, each
  * later evaluate records HIP events on its stream around each kernel it
  * launches; dip_sim_last_profile then waits for the last of them and writes
  * the kernel times in milliseconds, in launch order, to out_ms[0 .. *n_out-1]
  * (n_out <= 3: variant 8 launches the check, pool and retry kernels, the
- * others one kernel).  *n_out = 0 if the last evaluate recorded nothing. */
+ * others one kernel; dip_sim_greedy records its two launches the same way).  *n_out = 0 if the last evaluate recorded nothing. */
 int dip_sim_profile(dip_sim *h, int32_t enable);
 int dip_sim_last_profile(dip_sim *h, float *out_ms, int32_t *n_out);
 

@@ -26,7 +26,8 @@ NO_KEY = (1 << 64) - 1
 EXPORTS = ("dip_sim_abi_version", "dip_sim_check_topology", "dip_sim_check_costs",
            "dip_sim_create", "dip_sim_configure", "dip_sim_configure_pool",
            "dip_sim_configure_check", "dip_sim_get_info", "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
-           "dip_sim_argmin", "dip_sim_destroy", "dip_sim_strerror")
+           "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_greedy", "dip_sim_destroy",
+           "dip_sim_strerror")
 
 
 class DipSimError(RuntimeError):
@@ -84,6 +85,8 @@ def load():
         lib.dip_sim_get_info.argtypes = [vp, ctypes.POINTER(Info)]
         lib.dip_sim_evaluate.argtypes = [vp, ctypes.POINTER(Costs), vp, i64, vp, vp, vp, vp, vp]
         lib.dip_sim_argmin.argtypes = [vp, vp, vp, i64, i64, vp, vp]
+        lib.dip_sim_configure_greedy.argtypes = [vp, i32, vp]
+        lib.dip_sim_greedy.argtypes = [vp, ctypes.POINTER(Costs), vp, i64, vp, vp, vp, vp, vp, vp]
         lib.dip_sim_destroy.argtypes = [vp]
         lib.dip_sim_destroy.restype = None
         lib.dip_sim_strerror.argtypes = [ctypes.c_int]
@@ -92,7 +95,7 @@ def load():
                      "dip_sim_configure", "dip_sim_configure_pool", "dip_sim_configure_check",
                      "dip_sim_get_info",
                      "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
-                     "dip_sim_argmin"):
+                     "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_greedy"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -216,6 +219,24 @@ def argmin(h, makespan, flags, n_cand, index_base, inout_best_key, stream=None) 
     _check(rc, "dip_sim_argmin")
 
 
+def configure_greedy(h, n_groups: int, op_group) -> int:
+    """``op_group``: host int32 [N]; returns the ABI code."""
+    g = np.ascontiguousarray(op_group, np.int32)
+    return load().dip_sim_configure_greedy(h, int(n_groups), g.ctypes.data)
+
+
+def greedy(h, costs, prio, n_cand, out_orders, out_makespan, out_bubble, out_peakmem,
+           out_flags, stream=None) -> None:
+    """Priorities (device int32 [n, G]) in, orders and scores out (device);
+    ``out_orders`` may be None."""
+    rc = load().dip_sim_greedy(
+        h, ctypes.byref(costs.c) if costs is not None else None, prio.data_ptr(), int(n_cand),
+        out_orders.data_ptr() if out_orders is not None else None, out_makespan.data_ptr(),
+        out_bubble.data_ptr(), out_peakmem.data_ptr(), out_flags.data_ptr(),
+        _stream_ptr(stream))
+    _check(rc, "dip_sim_greedy")
+
+
 def destroy(h) -> None:
     if h:
         load().dip_sim_destroy(h)
@@ -282,6 +303,25 @@ class Sim:
         evaluate(self.h, send, orders, n, *out, stream=stream)
         self._costs_sent = True
         return out
+
+    def configure_greedy(self, n_groups, op_group) -> int:
+        rc = configure_greedy(self.h, n_groups, op_group)
+        if rc == OK:
+            self._greedy_costs = False
+        return rc
+
+    def greedy(self, prio, out=None, orders=True, stream=None):
+        """Interleave every priority row; returns (orders or None, outputs)."""
+        import torch
+        n = int(prio.shape[0])
+        assert prio.dtype == torch.int32 and prio.is_contiguous()
+        out = self.outputs(n, prio.device) if out is None else out
+        ords = torch.empty((n, self.stride), dtype=torch.int16, device=prio.device) if orders else None
+        send = self.costs if not getattr(self, "_greedy_costs", False) else None
+        greedy(self.h, send, prio, n, ords, *out, stream=stream)
+        self._greedy_costs = True
+        self._costs_sent = True
+        return ords, out
 
     def argmin(self, makespan, flags, index_base=0, key=None, stream=None):
         import torch

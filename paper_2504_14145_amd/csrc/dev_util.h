@@ -26,4 +26,11 @@ __device__ __forceinline__ uint64_t any_in_group(uint64_t m) {
 // Waits for this wave's outstanding LDS (and scalar-load) operations.
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
+// Orders the LDS accesses of the lanes of one wave around this point.
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
 }  // namespace dipsim

@@ -136,6 +136,33 @@ struct dip_sim {
   // the costs of a call exceed its time bound)
   int gen_variant = 0, gen_wpb = 1, gen_max_blocks = 1;
   int64_t gen_lds = 0;
+  // greedy stage interleaving (dip_sim_configure_greedy / dip_sim_greedy)
+  bool gr_ok = false;                  // groups configured
+  bool gr_costs_ok = false;            // records hold the current costs
+  int32_t gr_G = 0, gr_GF = 0, gr_J = 0, gr_max_nr = 0;
+  int gr_pwl = 3, gr_nw = 1;
+  std::vector<int32_t> gr_op;          // [G*P] global op of (internal group, rank), -1 none
+  std::vector<int32_t> gr_ig;          // [N] internal group of each op
+  std::vector<int32_t> gr_join;        // [N] join index of an op with several predecessors
+  std::vector<int32_t> gr_succ_ptr;    // [N+1] successors of each op ...
+  std::vector<int32_t> gr_succ_op;     // ... and the edge they come through
+  std::vector<int32_t> gr_succ_edge;
+  int32_t gr_n_extra = 0;              // successors after each op's first
+  int32_t *d_gr_caller = nullptr;      // [G]
+  int32_t *d_gr_src = nullptr;         // [P+1] offsets, then the source groups
+  int4 *d_gr_rec = nullptr;            // [G*P*2]
+  int4 *d_gr_succ = nullptr;           // [max(extra, 1)]
+  unsigned char *h_gr_stage = nullptr; // pinned staging of the records
+  int64_t *d_gr_retry = nullptr;
+  uint32_t *d_gr_retry_count = nullptr;
+  int64_t gr_retry_cap = 0;
+  struct GrLaunch {
+    int pwl = 3, wpb = 1, K = 8, blocks_per_cu = 1;
+    int32_t cand_bytes = 0, off_pend = 0, off_npend = 0, off_join = 0, off_gpos = 0,
+            off_ord = 0, off_grk = 0;
+    int64_t lds = 0;
+  } gr_main, gr_retry;
+  int32_t gr_meta_bytes = 0;
 };
 
 namespace {
@@ -566,6 +593,45 @@ StageLayout stage_layout(const dip_sim *h) {
   return L;
 }
 
+// Greedy records per (internal group, rank): {cost, act, local id |
+// successors << 16, index of the second successor}, then the first successor
+// {internal group | kind << 16 | rank << 17, comm, join index or -1, the
+// join's predecessor count}; further successors in the same 16-byte form.
+// The staging area is guarded by the caller's wait on stage_done.
+int upload_greedy_records(dip_sim *h, const dip_costs *c, hipStream_t stream) {
+  const int32_t P = h->P, G = h->gr_G;
+  int4 *rec = reinterpret_cast<int4 *>(h->h_gr_stage);
+  int4 *ext = rec + int64_t(G) * P * 2;
+  auto succ_entry = [&](int32_t k) {
+    const int32_t o = h->gr_succ_op[k], e = h->gr_succ_edge[k];
+    const uint32_t w = uint32_t(h->gr_ig[o]) | (uint32_t(h->kind[o]) << 16) |
+                       (uint32_t(h->rank_of[o]) << 17);
+    const int32_t j = h->gr_join[o];
+    return make_int4(int32_t(w), c->edge_comm[e], j,
+                     j >= 0 ? h->pred_ptr[o + 1] - h->pred_ptr[o] : 0);
+  };
+  int32_t xi = 0;
+  for (int32_t ig = 0; ig < G; ++ig)
+    for (int32_t r = 0; r < P; ++r) {
+      int4 *q = rec + (int64_t(ig) * P + r) * 2;
+      const int32_t g = h->gr_op[int64_t(ig) * P + r];
+      if (g < 0) {
+        q[0] = make_int4(0, 0, int32_t(kGreedyNoStage), 0);
+        q[1] = make_int4(0, 0, -1, 0);
+        continue;
+      }
+      const int32_t b = h->gr_succ_ptr[g], ns = h->gr_succ_ptr[g + 1] - b;
+      q[0] = make_int4(c->op_cost[g], c->slot_act[h->op_slot[g]],
+                       int32_t(uint32_t(g - h->rank_off[r]) | (uint32_t(ns) << 16)), xi);
+      q[1] = ns > 0 ? succ_entry(b) : make_int4(0, 0, -1, 0);
+      for (int32_t k = 1; k < ns; ++k) ext[xi++] = succ_entry(b + k);
+    }
+  DIP_HIP(hipMemcpyAsync(h->d_gr_rec, rec, size_t(G) * P * 32, hipMemcpyHostToDevice, stream));
+  if (xi > 0) DIP_HIP(hipMemcpyAsync(h->d_gr_succ, ext, size_t(xi) * 16, hipMemcpyHostToDevice, stream));
+  h->gr_costs_ok = true;
+  return DIP_OK;
+}
+
 int upload_costs(dip_sim *h, const dip_costs *c, hipStream_t stream) {
   int64_t total = 0;
   int rc = check_costs_against(h->P, h->n_ops.data(), h->pred_ptr.data(), h->op_slot.data(),
@@ -670,10 +736,61 @@ int upload_costs(dip_sim *h, const dip_costs *c, hipStream_t stream) {
       DIP_HIP(hipMemcpyAsync(h->d_jk, jk, size_t(h->n_joins) * 4, hipMemcpyHostToDevice, stream));
     h->lds16_costs_ok = h->pipe_costs_ok && fits;
   }
+  if (h->gr_ok) {
+    rc = upload_greedy_records(h, c, stream);
+    if (rc != DIP_OK) return rc;
+  }
   DIP_HIP(hipEventRecord(h->stage_done, stream));
   h->stage_pending = true;
   h->costs_set = true;
   return DIP_OK;
+}
+
+// LDS plan of one greedy candidate with inboxes of K entries: the inboxes,
+// their counts and the join accumulators overlay the priorities, which only
+// the set-up reads; then positions, position -> group and position -> global
+// rank (16-bit each).
+bool greedy_layout(const dip_sim *h, int K, int pwl, dip_sim::GrLaunch *L) {
+  const int64_t G = h->gr_G, P = h->P, J = h->gr_J;
+  L->pwl = pwl;
+  L->K = K;
+  L->wpb = 1;
+  L->off_pend = 0;
+  L->off_npend = int32_t(P * K * 8);
+  L->off_join = int32_t(P * K * 8 + 4 * P);
+  const int64_t head = align16(std::max<int64_t>(4 * G, L->off_join + 8 * J));
+  L->off_gpos = int32_t(head);
+  L->off_ord = int32_t(head + align16(2 * G));
+  L->off_grk = int32_t(head + 2 * align16(2 * G));
+  L->cand_bytes = int32_t(head + 3 * align16(2 * G));
+  L->lds = h->gr_meta_bytes + int64_t(kWave >> pwl) * L->cand_bytes;
+  if (L->lds > h->lds_block_max) return false;
+  int bpc = 0;
+  const void *k = greedy_kernel_ptr(pwl, h->gr_nw);
+  if (!k || hipOccupancyMaxActiveBlocksPerMultiprocessor(&bpc, k, kWave * L->wpb,
+                                                         size_t(L->lds)) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  L->blocks_per_cu = std::max(1, bpc);
+  return true;
+}
+
+void release_greedy(dip_sim *h) {
+  if (h->d_gr_caller) (void)hipFree(h->d_gr_caller);
+  if (h->d_gr_src) (void)hipFree(h->d_gr_src);
+  if (h->d_gr_rec) (void)hipFree(h->d_gr_rec);
+  if (h->d_gr_succ) (void)hipFree(h->d_gr_succ);
+  if (h->h_gr_stage) (void)hipHostFree(h->h_gr_stage);
+  if (h->d_gr_retry) (void)hipFree(h->d_gr_retry);
+  if (h->d_gr_retry_count) (void)hipFree(h->d_gr_retry_count);
+  h->d_gr_caller = h->d_gr_src = nullptr;
+  h->d_gr_rec = h->d_gr_succ = nullptr;
+  h->h_gr_stage = nullptr;
+  h->d_gr_retry = nullptr;
+  h->d_gr_retry_count = nullptr;
+  h->gr_retry_cap = 0;
+  h->gr_ok = h->gr_costs_ok = false;
 }
 
 void release(dip_sim *h) {
@@ -698,6 +815,7 @@ void release(dip_sim *h) {
   if (h->h_retry_seen) (void)hipHostFree(h->h_retry_seen);
   if (h->retry_seen_ev) (void)hipEventDestroy(h->retry_seen_ev);
   if (h->d_scratch_pipe) (void)hipFree(h->d_scratch_pipe);
+  release_greedy(h);
   if (h->h_stage) (void)hipHostFree(h->h_stage);
   if (h->stage_done) (void)hipEventDestroy(h->stage_done);
   for (hipEvent_t &ev : h->prof_ev)
@@ -1123,6 +1241,217 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
   DIP_HIP(mark(0));
   DIP_HIP(launch_general(v, blocks, wpb, size_t(lds), stream, a));
   DIP_HIP(mark(1));
+  return DIP_OK;
+}
+
+int dip_sim_configure_greedy(dip_sim *h, int32_t n_groups, const int32_t *op_group) {
+  if (!h || !op_group || n_groups < 1 || n_groups > 65535) return DIP_E_INVAL;
+  const int32_t N = h->N, P = h->P;
+  // every group holds stages of one kind, at most one per rank
+  std::vector<int8_t> gk(n_groups, -1);
+  std::vector<int32_t> at(int64_t(n_groups) * P, -1);
+  for (int32_t g = 0; g < N; ++g) {
+    const int32_t q = op_group[g];
+    if (q < 0 || q >= n_groups) return DIP_E_TOPO;
+    if (gk[q] >= 0 && gk[q] != int8_t(h->kind[g])) return DIP_E_TOPO;
+    gk[q] = int8_t(h->kind[g]);
+    int32_t &slot = at[int64_t(q) * P + h->rank_of[g]];
+    if (slot >= 0) return DIP_E_TOPO;
+    slot = g;
+  }
+  // the data edges must be acyclic (Kahn)
+  std::vector<int32_t> succ_ptr(N + 1, 0), succ_op(std::max(h->E, 1)), succ_edge(std::max(h->E, 1));
+  for (int32_t e = 0; e < h->E; ++e) ++succ_ptr[h->pred_op[e] + 1];
+  for (int32_t g = 0; g < N; ++g) succ_ptr[g + 1] += succ_ptr[g];
+  {
+    std::vector<int32_t> fill(succ_ptr.begin(), succ_ptr.end() - 1);
+    for (int32_t g = 0; g < N; ++g)
+      for (int32_t e = h->pred_ptr[g]; e < h->pred_ptr[g + 1]; ++e) {
+        const int32_t k = fill[h->pred_op[e]]++;
+        succ_op[k] = g;
+        succ_edge[k] = e;
+      }
+    std::vector<int32_t> left(N), stack;
+    for (int32_t g = 0; g < N; ++g) {
+      left[g] = h->pred_ptr[g + 1] - h->pred_ptr[g];
+      if (left[g] == 0) stack.push_back(g);
+    }
+    int32_t seen = 0;
+    while (!stack.empty()) {
+      const int32_t g = stack.back();
+      stack.pop_back();
+      ++seen;
+      for (int32_t k = succ_ptr[g]; k < succ_ptr[g + 1]; ++k)
+        if (--left[succ_op[k]] == 0) stack.push_back(succ_op[k]);
+    }
+    if (seen != N) return DIP_E_TOPO;
+  }
+  // internal numbering: forward groups (and empty ones), then backward groups
+  std::vector<int32_t> caller, internal(n_groups);
+  for (int pass = 0; pass < 2; ++pass)
+    for (int32_t q = 0; q < n_groups; ++q)
+      if ((gk[q] == 1) == (pass == 1)) {
+        internal[q] = int32_t(caller.size());
+        caller.push_back(q);
+      }
+  int32_t GF = 0;
+  while (GF < n_groups && gk[caller[GF]] != 1) ++GF;
+  const int32_t wmax = (std::max(GF, n_groups - GF) + 63) / 64;
+  int nw = 1;
+  while (nw < wmax) nw *= 2;
+  if (nw > 8) return DIP_E_UNSUPPORTED;
+
+  (void)hipDeviceSynchronize();   // no call may still read the old tables
+  release_greedy(h);
+  h->gr_G = n_groups;
+  h->gr_GF = GF;
+  h->gr_nw = nw;
+  h->gr_ig.assign(N, 0);
+  h->gr_op.assign(int64_t(n_groups) * P, -1);
+  for (int32_t g = 0; g < N; ++g) {
+    h->gr_ig[g] = internal[op_group[g]];
+    h->gr_op[int64_t(h->gr_ig[g]) * P + h->rank_of[g]] = g;
+  }
+  h->gr_join.assign(N, -1);
+  h->gr_J = 0;
+  for (int32_t g = 0; g < N; ++g)
+    if (h->pred_ptr[g + 1] - h->pred_ptr[g] >= 2) h->gr_join[g] = h->gr_J++;
+  h->gr_succ_ptr = succ_ptr;
+  h->gr_succ_op = succ_op;
+  h->gr_succ_edge = succ_edge;
+  h->gr_n_extra = 0;
+  for (int32_t g = 0; g < N; ++g) h->gr_n_extra += std::max(succ_ptr[g + 1] - succ_ptr[g] - 1, 0);
+  std::vector<int32_t> src(P + 1, 0), src_list;
+  h->gr_max_nr = 0;
+  for (int32_t r = 0; r < P; ++r) {
+    h->gr_max_nr = std::max(h->gr_max_nr, h->n_ops[r]);
+    for (int32_t g = h->rank_off[r]; g < h->rank_off[r + 1]; ++g)
+      if (h->pred_ptr[g + 1] == h->pred_ptr[g]) src_list.push_back(h->gr_ig[g]);
+    src[r + 1] = int32_t(src_list.size());
+  }
+  src.insert(src.end(), src_list.begin(), src_list.end());
+  h->gr_meta_bytes = int32_t(align16(2 * int64_t(n_groups)));
+  // inboxes of 8 stages; the second launch sizes them to a whole rank
+  const int pwl = std::max(2, h->pwl);
+  if (!greedy_layout(h, 8, pwl, &h->gr_main)) return DIP_E_UNSUPPORTED;
+  int pr = pwl;
+  while (pr <= 6 && !greedy_layout(h, std::max(h->gr_max_nr, 1), pr, &h->gr_retry)) ++pr;
+  if (pr > 6) return DIP_E_UNSUPPORTED;
+
+  auto fail = [&](hipError_t e) {
+    g_last_hip = e;
+    release_greedy(h);
+    return int(DIP_E_HIP);
+  };
+  hipError_t e;
+  const int64_t rec_bytes = int64_t(n_groups) * P * 32;
+  const int64_t ext_bytes = int64_t(std::max(h->gr_n_extra, 1)) * 16;
+  if ((e = hipMalloc(&h->d_gr_caller, size_t(n_groups) * 4)) != hipSuccess) return fail(e);
+  if ((e = hipMalloc(&h->d_gr_src, src.size() * 4)) != hipSuccess) return fail(e);
+  if ((e = hipMalloc(&h->d_gr_rec, size_t(rec_bytes))) != hipSuccess) return fail(e);
+  if ((e = hipMalloc(&h->d_gr_succ, size_t(ext_bytes))) != hipSuccess) return fail(e);
+  if ((e = hipHostMalloc(reinterpret_cast<void **>(&h->h_gr_stage), size_t(rec_bytes + ext_bytes),
+                         hipHostMallocDefault)) != hipSuccess)
+    return fail(e);
+  if ((e = hipMemcpy(h->d_gr_caller, caller.data(), size_t(n_groups) * 4, hipMemcpyHostToDevice)) !=
+      hipSuccess)
+    return fail(e);
+  if ((e = hipMemcpy(h->d_gr_src, src.data(), src.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
+    return fail(e);
+  h->gr_ok = true;
+  h->gr_costs_ok = false;
+  return DIP_OK;
+}
+
+int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int64_t n_cand,
+                   int16_t *out_orders, int32_t *out_makespan, int32_t *out_bubble,
+                   int32_t *out_peakmem, uint8_t *out_flags, void *stream_) {
+  if (!h || n_cand < 0) return DIP_E_INVAL;
+  if (!h->gr_ok) return DIP_E_STATE;
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  if (costs) {
+    int rc = upload_costs(h, costs, stream);
+    if (rc != DIP_OK) return rc;
+  }
+  if (!h->gr_costs_ok) return DIP_E_STATE;
+  if (n_cand == 0) return DIP_OK;
+  if (n_cand > INT32_MAX) return DIP_E_INVAL;
+  if (!prio || !out_makespan || !out_bubble || !out_peakmem || !out_flags) return DIP_E_INVAL;
+  if ((reinterpret_cast<uintptr_t>(prio) | reinterpret_cast<uintptr_t>(out_makespan) |
+       reinterpret_cast<uintptr_t>(out_bubble) | reinterpret_cast<uintptr_t>(out_peakmem)) & 3)
+    return DIP_E_INVAL;
+  if (reinterpret_cast<uintptr_t>(out_orders) & 1) return DIP_E_INVAL;
+  if (h->gr_retry_cap < n_cand) {
+    if (h->d_gr_retry) (void)hipFree(h->d_gr_retry);
+    h->d_gr_retry = nullptr;
+    h->gr_retry_cap = 0;
+    DIP_HIP(hipMalloc(&h->d_gr_retry, size_t(n_cand) * 8));
+    h->gr_retry_cap = n_cand;
+  }
+  if (!h->d_gr_retry_count) DIP_HIP(hipMalloc(&h->d_gr_retry_count, 16));
+  h->prof_n = 0;
+  auto mark = [&](int i) -> hipError_t {
+    if (!h->profile) return hipSuccess;
+    h->prof_n = i + 1;
+    return hipEventRecord(h->prof_ev[i], stream);
+  };
+  (void)hipGetLastError();
+  DIP_HIP(hipMemsetAsync(h->d_gr_retry_count, 0, 4, stream));
+  GreedyArgs a{};
+  a.prio = prio;
+  a.n_cand = n_cand;
+  a.out_orders = out_orders;
+  a.stride = h->stride;
+  a.out_ms = out_makespan;
+  a.out_bub = out_bubble;
+  a.out_peak = out_peakmem;
+  a.out_flags = out_flags;
+  a.rec = h->d_gr_rec;
+  a.succ = h->d_gr_succ;
+  a.caller = h->d_gr_caller;
+  a.src = h->d_gr_src;
+  a.rank_off = h->d_rank_off;
+  a.busy = h->d_busy;
+  a.cap = h->d_cap;
+  a.P = h->P;
+  a.G = h->gr_G;
+  a.GF = h->gr_GF;
+  a.J = h->gr_J;
+  a.n_rounds = h->N;
+  a.has_cap = 0;
+  for (int r = 0; r < h->P; ++r) a.has_cap |= h->cap[r] >= 0 ? 1 : 0;
+  a.meta_bytes = h->gr_meta_bytes;
+  auto set_layout = [&](const dip_sim::GrLaunch &L) {
+    a.K = L.K;
+    a.wpb = L.wpb;
+    a.cand_bytes = L.cand_bytes;
+    a.off_pend = L.off_pend;
+    a.off_npend = L.off_npend;
+    a.off_join = L.off_join;
+    a.off_gpos = L.off_gpos;
+    a.off_ord = L.off_ord;
+    a.off_grk = L.off_grk;
+  };
+  set_layout(h->gr_main);
+  a.retry = h->d_gr_retry;
+  a.retry_count = h->d_gr_retry_count;
+  const int64_t per_block = int64_t(h->gr_main.wpb) * (kWave >> h->gr_main.pwl);
+  const int64_t blocks = (n_cand + per_block - 1) / per_block;
+  if (blocks > INT32_MAX) return DIP_E_INVAL;
+  DIP_HIP(mark(0));
+  DIP_HIP(launch_greedy(h->gr_main.pwl, h->gr_nw, int(blocks), h->gr_main.wpb,
+                        size_t(h->gr_main.lds), stream, a));
+  DIP_HIP(mark(1));
+  // candidates whose inboxes overflowed, with inboxes as large as a rank
+  set_layout(h->gr_retry);
+  a.list = h->d_gr_retry;
+  a.list_count = h->d_gr_retry_count;
+  a.retry = nullptr;
+  a.retry_count = nullptr;
+  const int rblocks = int(std::min<int64_t>(int64_t(h->n_cu) * h->gr_retry.blocks_per_cu, blocks));
+  DIP_HIP(launch_greedy(h->gr_retry.pwl, h->gr_nw, rblocks, h->gr_retry.wpb,
+                        size_t(h->gr_retry.lds), stream, a));
+  DIP_HIP(mark(2));
   return DIP_OK;
 }
 

@@ -221,6 +221,47 @@ const void *pool_kernel_ptr(int pwl, int slots, bool tab);
 hipError_t launch_pool(int pwl, int slots, bool tab, int blocks, int wpb, size_t lds, hipStream_t s,
                        const PoolArgs &a);
 
+// ---------------------------------------------------------------- greedy
+// Dual-queue stage interleaving (see kern_greedy.hip).  Groups are numbered
+// internally forward groups first, then backward ones, each in the caller's
+// order; "position" is a group's rank among the groups of its kind under the
+// candidate's priorities.
+struct GreedyArgs {
+  const int32_t *prio;      // [n_cand][G] caller-indexed priorities
+  int64_t n_cand;
+  int16_t *out_orders;      // [n_cand][stride] or null
+  int64_t stride;
+  int32_t *out_ms;
+  int32_t *out_bub;
+  int32_t *out_peak;
+  uint8_t *out_flags;
+  const int4 *rec;          // [G][P][2] per (internal group, rank):
+                            //   {cost, act, local id | successors << 16 (0xffff: no stage),
+                            //    index of the second successor in succ},
+                            //   {first successor: word, comm, join or -1, join's predecessors}
+  const int4 *succ;         // further successors, same form as the second half of rec
+  const int32_t *caller;    // [G] caller index of each internal group
+  const int32_t *src;       // [P+1] offsets, then the internal groups of each rank's sources
+  const int32_t *rank_off;  // [P+1]
+  const int32_t *busy;      // [P]
+  const int32_t *cap;       // [P]
+  int32_t P, G, GF, J, K, wpb;
+  int32_t n_rounds;         // N: every round schedules one stage of every candidate
+  int32_t has_cap;          // some rank has a cap
+  int32_t meta_bytes;       // block-shared LDS: caller index of each group (u16)
+  int32_t cand_bytes;       // LDS per candidate, 16-aligned
+  int32_t off_gpos, off_ord, off_grk, off_pend, off_npend, off_join;  // within a candidate
+  const int64_t *list;      // list mode: candidates list[0 .. *list_count-1]
+  const uint32_t *list_count;
+  int64_t *retry;           // candidates whose inbox overflowed
+  uint32_t *retry_count;
+};
+// successor word: internal group | kind << 16 | rank << 17
+constexpr uint32_t kGreedyNoStage = 0xffffu;
+const void *greedy_kernel_ptr(int pwl, int nw);
+hipError_t launch_greedy(int pwl, int nw, int blocks, int wpb, size_t lds, hipStream_t s,
+                         const GreedyArgs &a);
+
 // ---------------------------------------------------------------- argmin
 hipError_t launch_argmin(int blocks, hipStream_t s, const int32_t *ms, const uint8_t *flags,
                          int64_t n, uint64_t base, unsigned long long *key);

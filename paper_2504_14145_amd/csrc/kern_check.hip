@@ -172,13 +172,6 @@ __global__ __launch_bounds__(256) void check_kernel(CheckArgs a) {
 // findings into the candidates' flag words in LDS, and after a block barrier
 // the outputs of an invalid candidate are overwritten with -1.
 
-// orders the LDS accesses of the lanes of one wave around this point
-__device__ __forceinline__ void wave_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-}
-
 __global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
