@@ -126,6 +126,9 @@ typedef struct {
   int64_t scratch_bytes;     /* device scratch owned by the handle               */
   int32_t pool_slots;        /* variant 8: end-time slots per rank pool, else 0  */
   int32_t check_kernel;      /* variant 8: 1 wave per candidate, 2 tiles, else 0 */
+  int32_t greedy_inbox;      /* dip_sim_greedy: stages a rank's inbox holds (0:
+                                not configured); grows when many overflow     */
+  int32_t greedy_lds_bytes;  /* dip_sim_greedy: LDS per block of its launch    */
 } dip_sim_info;
 
 /* Host-only checks, no device access: the same checks create / evaluate run

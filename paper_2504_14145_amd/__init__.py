@@ -56,7 +56,8 @@ class Info(ctypes.Structure):
                 ("groups_per_wave", ctypes.c_int32), ("waves_per_block", ctypes.c_int32),
                 ("lds_bytes", ctypes.c_int32), ("max_blocks", ctypes.c_int32),
                 ("scratch_bytes", ctypes.c_int64), ("pool_slots", ctypes.c_int32),
-                ("check_kernel", ctypes.c_int32)]
+                ("check_kernel", ctypes.c_int32), ("greedy_inbox", ctypes.c_int32),
+                ("greedy_lds_bytes", ctypes.c_int32)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}

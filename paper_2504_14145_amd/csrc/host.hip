@@ -156,6 +156,14 @@ struct dip_sim {
   int64_t *d_gr_retry = nullptr;
   uint32_t *d_gr_retry_count = nullptr;
   int64_t gr_retry_cap = 0;
+  // adaptive inbox size: a call's retry count is copied back asynchronously
+  // and read by a later call, which doubles the inboxes when more than 1/64
+  // of its candidates needed the second launch
+  int gr_K = 16;
+  uint32_t *h_gr_seen = nullptr;       // pinned
+  hipEvent_t gr_seen_ev = nullptr;
+  bool gr_seen_pending = false;
+  int64_t gr_seen_n = 0;
   struct GrLaunch {
     int pwl = 3, wpb = 1, K = 8, blocks_per_cu = 1;
     int32_t cand_bytes = 0, off_pend = 0, off_npend = 0, off_join = 0, off_gpos = 0,
@@ -755,9 +763,11 @@ bool greedy_layout(const dip_sim *h, int K, int pwl, dip_sim::GrLaunch *L) {
   L->pwl = pwl;
   L->K = K;
   L->wpb = 1;
+  // two rings per rank; two head/count words per lane (padding lanes' stay 0)
+  const int64_t lanes = int64_t(1) << pwl;
   L->off_pend = 0;
-  L->off_npend = int32_t(P * K * 8);
-  L->off_join = int32_t(P * K * 8 + 4 * P);
+  L->off_npend = int32_t(P * 2 * K * 8);
+  L->off_join = int32_t(P * 2 * K * 8 + 8 * lanes);
   const int64_t head = align16(std::max<int64_t>(4 * G, L->off_join + 8 * J));
   L->off_gpos = int32_t(head);
   L->off_ord = int32_t(head + align16(2 * G));
@@ -784,6 +794,11 @@ void release_greedy(dip_sim *h) {
   if (h->h_gr_stage) (void)hipHostFree(h->h_gr_stage);
   if (h->d_gr_retry) (void)hipFree(h->d_gr_retry);
   if (h->d_gr_retry_count) (void)hipFree(h->d_gr_retry_count);
+  if (h->h_gr_seen) (void)hipHostFree(h->h_gr_seen);
+  if (h->gr_seen_ev) (void)hipEventDestroy(h->gr_seen_ev);
+  h->h_gr_seen = nullptr;
+  h->gr_seen_ev = nullptr;
+  h->gr_seen_pending = false;
   h->d_gr_caller = h->d_gr_src = nullptr;
   h->d_gr_rec = h->d_gr_succ = nullptr;
   h->h_gr_stage = nullptr;
@@ -1044,6 +1059,8 @@ int dip_sim_get_info(const dip_sim *h, dip_sim_info *info) {
                         h->retry_cap * 8;
   info->pool_slots = h->variant == 8 ? h->pool_slots : 0;
   info->check_kernel = h->variant == 8 ? (use_tile_check(h) ? 2 : 1) : 0;
+  info->greedy_inbox = h->gr_ok ? h->gr_K : 0;
+  info->greedy_lds_bytes = h->gr_ok ? int32_t(h->gr_main.lds) : 0;
   return DIP_OK;
 }
 
@@ -1331,11 +1348,16 @@ int dip_sim_configure_greedy(dip_sim *h, int32_t n_groups, const int32_t *op_gro
   }
   src.insert(src.end(), src_list.begin(), src_list.end());
   h->gr_meta_bytes = int32_t(align16(2 * int64_t(n_groups)));
-  // inboxes of 8 stages; the second launch sizes them to a whole rank
+  // inboxes of 8 stages per kind to start with; the second launch sizes them
+  // to a whole rank
   const int pwl = std::max(2, h->pwl);
-  if (!greedy_layout(h, 8, pwl, &h->gr_main)) return DIP_E_UNSUPPORTED;
+  h->gr_K = 8;
+  if (!greedy_layout(h, h->gr_K, pwl, &h->gr_main)) return DIP_E_UNSUPPORTED;
+  // inboxes are rings of a power of two entries
+  int kr = 1;
+  while (kr < h->gr_max_nr) kr *= 2;
   int pr = pwl;
-  while (pr <= 6 && !greedy_layout(h, std::max(h->gr_max_nr, 1), pr, &h->gr_retry)) ++pr;
+  while (pr <= 6 && !greedy_layout(h, kr, pr, &h->gr_retry)) ++pr;
   if (pr > 6) return DIP_E_UNSUPPORTED;
 
   auto fail = [&](hipError_t e) {
@@ -1389,6 +1411,16 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
     h->gr_retry_cap = n_cand;
   }
   if (!h->d_gr_retry_count) DIP_HIP(hipMalloc(&h->d_gr_retry_count, 16));
+  if (h->gr_seen_pending && hipEventQuery(h->gr_seen_ev) == hipSuccess) {
+    h->gr_seen_pending = false;
+    dip_sim::GrLaunch bigger;
+    if (h->gr_K < 256 && int64_t(*h->h_gr_seen) * 64 > h->gr_seen_n &&
+        greedy_layout(h, 2 * h->gr_K, h->gr_main.pwl, &bigger)) {
+      h->gr_K *= 2;
+      h->gr_main = bigger;
+    }
+  }
+  (void)hipGetLastError();
   h->prof_n = 0;
   auto mark = [&](int i) -> hipError_t {
     if (!h->profile) return hipSuccess;
@@ -1452,6 +1484,16 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
   DIP_HIP(launch_greedy(h->gr_retry.pwl, h->gr_nw, rblocks, h->gr_retry.wpb,
                         size_t(h->gr_retry.lds), stream, a));
   DIP_HIP(mark(2));
+  if (h->gr_K < 256 && !h->gr_seen_pending) {
+    if (!h->h_gr_seen) {
+      DIP_HIP(hipHostMalloc(reinterpret_cast<void **>(&h->h_gr_seen), 16, hipHostMallocDefault));
+      DIP_HIP(hipEventCreateWithFlags(&h->gr_seen_ev, hipEventDisableTiming));
+    }
+    DIP_HIP(hipMemcpyAsync(h->h_gr_seen, h->d_gr_retry_count, 4, hipMemcpyDeviceToHost, stream));
+    DIP_HIP(hipEventRecord(h->gr_seen_ev, stream));
+    h->gr_seen_pending = true;
+    h->gr_seen_n = n_cand;
+  }
   return DIP_OK;
 }
 

@@ -22,12 +22,14 @@
 // candidates per wave.  A rank's queued stages are kept by priority position
 // (the group's rank among groups of its kind under the candidate's
 // priorities):
-//   E  bitmap (registers) of queued stages with t_start <  t_last,
-//   Z  bitmap (registers) of queued stages with t_start == t_last,
-//   inbox (LDS) of stages whose t_start is still ahead: (t_start, kind, pos).
-// Lanes touch only their own bitmaps; the committing lane appends the stages
-// its commit completes to the target ranks' inboxes, and each lane sorts its
-// inbox into E / Z at the start of the next round.  A group min over the
+//   E      bitmap (registers) of queued stages with t_start < t_last (and the
+//          stages without predecessors while t_last is 0);
+//   inbox  two rings (LDS), forward and backward, of the other queued
+//          stages, sorted by (t_start, position): a ring's front is its
+//          kind's least t_start and, among equal ones, its best priority.
+// Lanes touch only their own bitmaps; the committing lane inserts the stages
+// its commit completes into the target ranks' inboxes, and each lane moves
+// the entries that came due into E at the start of the next round.  A group min over the
 // lanes' t_min picks the committing rank.  An inbox that fills up sends the
 // candidate to a list that a second launch, with inboxes as large as a rank's
 // stage count, simulates again.
@@ -55,58 +57,70 @@ struct Bits {
 #pragma unroll
     for (int i = 0; i < NW; ++i) w[i] = 0;
   }
-  __device__ __forceinline__ void set(uint32_t p) {
-    const uint32_t k = p >> 6;
-    const uint64_t b = uint64_t(1) << (p & 63u);
-#pragma unroll
-    for (int i = 0; i < NW; ++i) w[i] |= uint32_t(i) == k ? b : uint64_t(0);
-  }
   __device__ __forceinline__ void clear(uint32_t p) {
     const uint32_t k = p >> 6;
     const uint64_t b = ~(uint64_t(1) << (p & 63u));
 #pragma unroll
     for (int i = 0; i < NW; ++i) w[i] &= uint32_t(i) == k ? b : ~uint64_t(0);
   }
-  __device__ __forceinline__ bool any() const {
-    uint64_t m = 0;
-#pragma unroll
-    for (int i = 0; i < NW; ++i) m |= w[i];
-    return m != 0;
-  }
-  // this |= z, z = {}
-  __device__ __forceinline__ void absorb(Bits &z) {
-#pragma unroll
-    for (int i = 0; i < NW; ++i) {
-      w[i] |= z.w[i];
-      z.w[i] = 0;
-    }
-  }
 };
 
-// lowest position in a | b, kNoPos if both are empty
+// lowest position in a, kNoPos if empty
 template <int NW>
-__device__ __forceinline__ uint32_t first_of(const Bits<NW> &a, const Bits<NW> &b) {
+__device__ __forceinline__ uint32_t first_in(const Bits<NW> &a) {
   uint32_t r = kNoPos;
 #pragma unroll
-  for (int i = NW - 1; i >= 0; --i) {
-    const uint64_t m = a.w[i] | b.w[i];
-    if (m != 0) r = uint32_t(i) * 64u + uint32_t(__builtin_ctzll(m));
-  }
+  for (int i = NW - 1; i >= 0; --i)
+    if (a.w[i] != 0) r = uint32_t(i) * 64u + uint32_t(__builtin_ctzll(a.w[i]));
   return r;
 }
 
-template <int PWL>
-__device__ __forceinline__ uint32_t group_min(uint32_t v) {
+// sets position p in f (kind 0) or b (kind 1) without branching
+template <int NW>
+__device__ __forceinline__ void set_kind(Bits<NW> &f, Bits<NW> &b, uint32_t kind, uint32_t p) {
+  const uint32_t k = p >> 6;
+  const uint64_t bit = uint64_t(1) << (p & 63u);
 #pragma unroll
-  for (int s = 1; s < (1 << PWL); s <<= 1) v = min(v, uint32_t(__shfl_xor(int(v), s)));
-  return v;
+  for (int i = 0; i < NW; ++i) {
+    const uint64_t m = uint32_t(i) == k ? bit : uint64_t(0);
+    f.w[i] |= kind ? uint64_t(0) : m;
+    b.w[i] |= kind ? m : uint64_t(0);
+  }
 }
 
-template <int PWL>
-__device__ __forceinline__ uint32_t group_max(uint32_t v) {
-#pragma unroll
-  for (int s = 1; s < (1 << PWL); s <<= 1) v = max(v, uint32_t(__shfl_xor(int(v), s)));
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp(uint32_t v) {
+  return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), CTRL, 0xf, 0xf, false));
+}
+
+// min / max over the 2^PWL lanes of a group: quad permutations, then the
+// half-row and row mirrors (each lane meets the other half), then shuffles
+template <int PWL, bool MAX>
+__device__ __forceinline__ uint32_t group_reduce(uint32_t v) {
+  auto op = [](uint32_t x, uint32_t y) { return MAX ? max(x, y) : min(x, y); };
+  if constexpr (PWL >= 1) v = op(v, dpp<0xb1>(v));    // quad_perm [1,0,3,2]
+  if constexpr (PWL >= 2) v = op(v, dpp<0x4e>(v));    // quad_perm [2,3,0,1]
+  if constexpr (PWL >= 3) v = op(v, dpp<0x141>(v));   // row_half_mirror
+  if constexpr (PWL >= 4) v = op(v, dpp<0x140>(v));   // row_mirror
+  if constexpr (PWL >= 5) v = op(v, uint32_t(__shfl_xor(int(v), 16)));
+  if constexpr (PWL >= 6) v = op(v, uint32_t(__shfl_xor(int(v), 32)));
   return v;
+}
+template <int PWL>
+__device__ __forceinline__ uint32_t group_min(uint32_t v) { return group_reduce<PWL, false>(v); }
+template <int PWL>
+__device__ __forceinline__ uint32_t group_max(uint32_t v) { return group_reduce<PWL, true>(v); }
+
+// Orders the LDS accesses of the wave's lanes around this point without
+// waiting for its global stores.
+__device__ __forceinline__ void lds_sync() {
+  lds_wait();
+  __builtin_amdgcn_wave_barrier();
+}
+
+// ranking key: priority, then lower caller index first
+__device__ __forceinline__ uint64_t rank_key(int32_t prio, uint32_t caller) {
+  return (uint64_t(uint32_t(prio) ^ 0x80000000u) << 32) | uint64_t(0xffffu - caller);
 }
 
 // bits of this lane's group in a wave-wide mask, lowest rank at bit 0
@@ -141,9 +155,13 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
 
   unsigned char *cb = lds + a.meta_bytes + int64_t(wave * GW + grp) * a.cand_bytes;
   int32_t *prio = reinterpret_cast<int32_t *>(cb);               // setup only ...
-  uint64_t *pend0 = reinterpret_cast<uint64_t *>(cb + a.off_pend);  // ... then inboxes
-  uint64_t *pend = pend0 + int64_t(r) * K;
-  uint32_t *npend = reinterpret_cast<uint32_t *>(cb + a.off_npend);
+  // ... then the inboxes: per rank a forward ring and a backward ring of K
+  // entries each; per lane (padding lanes included) a word {head, count << 16}
+  // per kind
+  uint64_t *ring0 = reinterpret_cast<uint64_t *>(cb + a.off_pend);
+  uint64_t *ringF = ring0 + int64_t(r < P ? r : 0) * 2 * K;
+  uint64_t *ringB = ringF + K;
+  uint32_t *hcw = reinterpret_cast<uint32_t *>(cb + a.off_npend);
   uint32_t *jtab = reinterpret_cast<uint32_t *>(cb + a.off_join);
   uint16_t *gpos = reinterpret_cast<uint16_t *>(cb + a.off_gpos);
   uint16_t *ord = reinterpret_cast<uint16_t *>(cb + a.off_ord);
@@ -168,144 +186,148 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
     }
     wave_sync();
     if (has) {
-      for (int g = r; g < G; g += PW) {
-        const int32_t pg = prio[g];
-        const uint32_t cg = meta[g];
-        const bool fg = g < GF;
-        uint32_t before = 0, same = 0;
-        for (int h = 0; h < G; ++h) {
-          const int32_t ph = prio[h];
-          const bool ahead = ph > pg || (ph == pg && uint32_t(meta[h]) < cg);
-          before += ahead ? 1u : 0u;
-          same += (ahead && ((h < GF) == fg)) ? 1u : 0u;
+      // rank of every group among all groups and among its kind, eight of
+      // this lane's groups against each group in turn
+      constexpr int B = 8;
+      for (int g0 = r; g0 < G; g0 += B * PW) {
+        uint64_t kg[B];
+        uint32_t nf[B], nb[B];
+#pragma unroll
+        for (int t = 0; t < B; ++t) {
+          const int g = g0 + t * PW;
+          kg[t] = g < G ? rank_key(prio[g], meta[g]) : ~uint64_t(0);
+          nf[t] = nb[t] = 0;
         }
-        gpos[g] = uint16_t(same);
-        const int at = fg ? int(same) : GF + int(same);
-        ord[at] = uint16_t(g);
-        grk[at] = uint16_t(before);
+        for (int h = 0; h < GF; ++h) {
+          const uint64_t kh = rank_key(prio[h], meta[h]);
+#pragma unroll
+          for (int t = 0; t < B; ++t) nf[t] += kh > kg[t] ? 1u : 0u;
+        }
+        for (int h = GF; h < G; ++h) {
+          const uint64_t kh = rank_key(prio[h], meta[h]);
+#pragma unroll
+          for (int t = 0; t < B; ++t) nb[t] += kh > kg[t] ? 1u : 0u;
+        }
+#pragma unroll
+        for (int t = 0; t < B; ++t) {
+          const int g = g0 + t * PW;
+          if (g < G) {
+            const bool fg = g < GF;
+            const uint32_t same = fg ? nf[t] : nb[t];
+            gpos[g] = uint16_t(same);
+            const int at = fg ? int(same) : GF + int(same);
+            ord[at] = uint16_t(g);
+            grk[at] = uint16_t(nf[t] + nb[t]);
+          }
+        }
       }
     }
     wave_sync();
-    if (has) {
+    if (has)
       for (int j = r; j < 2 * a.J; j += PW) jtab[j] = 0;
-      if (r < P) npend[r] = 0;
-    }
-    Bits<NW> eF, eB, zF, zB;
+    hcw[2 * r] = 0;
+    hcw[2 * r + 1] = 0;
+    // E: queued stages with t_start < t_last (and the stages without
+    // predecessors while t_last is still 0, their t_start); a stage with
+    // t_start >= t_last waits in its kind's inbox
+    Bits<NW> eF, eB;
     eF.zero();
     eB.zero();
-    zF.zero();
-    zB.zero();
     if (real) {
-      // stages without predecessors: queued at t_start 0 = t_last
       const int32_t *src_list = a.src + P + 1;
       for (int s = a.src[r]; s < a.src[r + 1]; ++s) {
         const int g = src_list[s];
-        if (g < GF) zF.set(gpos[g]);
-        else zB.set(gpos[g]);
+        set_kind(eF, eB, g < GF ? 0u : 1u, gpos[g]);
       }
     }
     wave_sync();
 
-    uint32_t t_last = 0, tl_seen = 0, last_kind = 0, n_emit = 0;
+    uint32_t t_last = 0, last_kind = 0, n_emit = 0;
+    uint32_t rec_key = kNever;
+    int4 q0 = make_int4(0, 0, 0, 0), q1 = q0;
     int32_t live = 0, peak = 0;
     bool ovf = false, stuck = false;
     const int32_t capr = real ? a.cap[r] : -1;
     const int64_t row = real ? cand * a.stride + a.rank_off[r] : 0;
     const uint32_t n_own = real ? uint32_t(a.rank_off[r + 1] - a.rank_off[r]) : 0u;
+    const uint32_t mask = uint32_t(K) - 1u;
 
     for (int it = 0; it < a.n_rounds; ++it) {
-      // ---- 1. inbox: stages whose t_start has come move into E / Z
-      uint32_t pmF = kNever, pmB = kNever, ppF = kNoPos, ppB = kNoPos, psF = 0, psB = 0;
-      if (real) {
-        if (t_last != tl_seen) {
-          eF.absorb(zF);
-          eB.absorb(zB);
-          tl_seen = t_last;
-        }
-        const uint32_t n = npend[r];
-        uint32_t j = 0;
-        for (uint32_t i = 0; i < n; ++i) {
-          const uint64_t e = pend[i];
-          const uint32_t t = uint32_t(e >> 17);
-          const uint32_t p = uint32_t(e) & 0xffffu;
-          const bool bk = ((uint32_t(e) >> 16) & 1u) != 0;
-          if (t < t_last) {
-            if (bk) eB.set(p);
-            else eF.set(p);
-          } else if (t == t_last) {
-            if (bk) zB.set(p);
-            else zF.set(p);
-          } else {
-            if (j != i) pend[j] = e;
-            if (bk) {
-              if (t < pmB || (t == pmB && p < ppB)) {
-                pmB = t;
-                ppB = p;
-                psB = j;
-              }
-            } else if (t < pmF || (t == pmF && p < ppF)) {
-              pmF = t;
-              ppF = p;
-              psF = j;
-            }
-            ++j;
-          }
-        }
-        if (j != n) npend[r] = j;
+      // ---- 1. inboxes: entries that came due move into E; the fronts are
+      // each kind's least t_start (best position among equal ones)
+      const uint32_t cF0 = hcw[2 * r], cB0 = hcw[2 * r + 1];
+      uint32_t hF = cF0 & 0xffffu, nF = cF0 >> 16, hB = cB0 & 0xffffu, nB = cB0 >> 16;
+      uint64_t frF = ~uint64_t(0), frB = ~uint64_t(0);
+      for (; nF > 0; ++hF, --nF) {
+        frF = ringF[hF & mask];
+        if (uint32_t(frF >> 17) >= t_last) break;
+        set_kind(eF, eB, 0u, uint32_t(frF >> 1) & 0xffffu);
+        frF = ~uint64_t(0);
       }
+      for (; nB > 0; ++hB, --nB) {
+        frB = ringB[hB & mask];
+        if (uint32_t(frB >> 17) >= t_last) break;
+        set_kind(eF, eB, 1u, uint32_t(frB >> 1) & 0xffffu);
+        frB = ~uint64_t(0);
+      }
+      const uint32_t cF = (hF & 0xffffu) | (nF << 16), cB = (hB & 0xffffu) | (nB << 16);
+      if (cF != cF0) hcw[2 * r] = cF;
+      if (cB != cB0) hcw[2 * r + 1] = cB;
+      const uint32_t pmF = nF ? uint32_t(frF >> 17) : kNever, pmB = nB ? uint32_t(frB >> 17) : kNever;
+      const uint32_t ppF = nF ? uint32_t(frF >> 1) & 0xffffu : kNoPos;
+      const uint32_t ppB = nB ? uint32_t(frB >> 1) & 0xffffu : kNoPos;
 
       // ---- 2. this rank's choice
-      const uint32_t fF = first_of(eF, zF), fB = first_of(eB, zB);
-      const bool xF = eF.any(), xB = eB.any();
-      uint32_t gF = kNoPos, gB = kNoPos, hF = kNoPos, hB = kNoPos;
-      if (real) {
-        if (fF != kNoPos) gF = grk[fF];
-        if (fB != kNoPos) gB = grk[GF + fB];
-        if (ppF != kNoPos) hF = grk[ppF];
-        if (ppB != kNoPos) hB = grk[GF + ppB];
-      }
+      const uint32_t fF = first_in(eF), fB = first_in(eB);
+      const bool xF = fF != kNoPos && t_last > 0, xB = fB != kNoPos && t_last > 0;
+      // the best stage of each kind able to start at tau: E's first (E is
+      // non-empty only when tau == t_last) or the inbox front if due then
       auto decide = [&](bool fw) {
         Choice c;
-        const bool nF = fw && fF != kNoPos, nB = fB != kNoPos;
-        c.slot = kNever;
-        if (nF || nB) {
-          c.tau = t_last;
-          if (fw && xF && xB) c.kind = last_kind ^ 1u;
-          else c.kind = (nF && (!nB || gF < gB)) ? 0u : 1u;
-          c.pos = c.kind ? fB : fF;
-        } else {
-          const uint32_t tF = fw ? pmF : kNever;
-          c.tau = min(tF, pmB);
-          if (c.tau == kNever) {
-            c.pos = kNoPos;
-            c.kind = 0;
-          } else {
-            c.kind = (tF == c.tau && (pmB != c.tau || hF < hB)) ? 0u : 1u;
-            c.pos = c.kind ? ppB : ppF;
-            c.slot = c.kind ? psB : psF;
-          }
-        }
+        const uint32_t eF_ = fw ? fF : kNoPos, pF = fw ? pmF : kNever;
+        const bool anyE = eF_ != kNoPos || fB != kNoPos;
+        c.tau = anyE ? t_last : min(pF, pmB);
+        const bool inF = pF == c.tau && ppF < eF_;
+        const bool inB = pmB == c.tau && ppB < fB;
+        const uint32_t bF = inF ? ppF : eF_, bB = inB ? ppB : fB;
+        const uint32_t gF = grk[bF < uint32_t(GF) ? bF : 0u];
+        const uint32_t gB = grk[bB < uint32_t(G - GF) ? GF + bB : 0u];
+        const bool alt = fw && xF && xB;                           // 1F1B
+        const uint32_t k = bF == kNoPos ? 1u : (bB == kNoPos ? 0u : (gF < gB ? 0u : 1u));
+        c.kind = alt ? (last_kind ^ 1u) : k;
+        c.pos = c.kind ? bB : bF;
+        c.slot = (c.kind ? inB : inF) ? 1u : 0u;    // 1: the kind's inbox front
         return c;
+      };
+      // the record of a choice: {cost, act, local id | successors << 16,
+      // second successor's index}, {first successor}; kept while the choice
+      // stays the same
+      auto fetch = [&](const Choice &c) {
+        const uint32_t k = (c.kind << 16) | c.pos;
+        if (k != rec_key) {
+          const int4 *rp = a.rec + (int64_t(ord[c.kind ? GF + c.pos : c.pos]) * P + r) * 2;
+          q0 = rp[0];
+          q1 = rp[1];
+          rec_key = k;
+        }
       };
       const Choice ce = decide(true);
       Choice cd = ce;
-      int4 q0e = make_int4(0, 0, 0, 0), q1e = q0e;
-      bool have_e = false;
-      if (a.has_cap && real && ce.pos != kNoPos && ce.kind == 0 && capr >= 0) {
-        const int4 *rp = a.rec + (int64_t(ord[ce.pos]) * P + r) * 2;
-        q0e = rp[0];
-        q1e = rp[1];
-        have_e = true;
-        if (live + q0e.y > capr) cd = decide(false);   // forward queue disabled
+      if (ce.pos != kNoPos) {
+        fetch(ce);
+        if (a.has_cap && ce.kind == 0 && capr >= 0 && live + q0.y > capr) {
+          cd = decide(false);                   // forward queue disabled
+          if (cd.pos != kNoPos) fetch(cd);
+        }
       }
 
       // ---- 3. the rank with the smallest t_min commits
-      const uint32_t key_d = (real && cd.pos != kNoPos) ? cd.tau : kNever;
+      const uint32_t key_d = cd.pos != kNoPos ? cd.tau : kNever;
       uint32_t m = group_min<PWL>(key_d);
       uint32_t key = key_d;
       bool forced = false;
       if (__any(has && m == kNever)) {
-        const uint32_t key_e = (real && ce.pos != kNoPos) ? ce.tau : kNever;
+        const uint32_t key_e = ce.pos != kNoPos ? ce.tau : kNever;
         const uint32_t m2 = group_min<PWL>(key_e);
         if (m == kNever) {
           forced = true;
@@ -319,28 +341,15 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
 
       if (win) {
         const Choice c = forced ? ce : cd;
-        int4 q0, q1;
-        if (have_e && c.kind == ce.kind && c.pos == ce.pos) {
-          q0 = q0e;
-          q1 = q1e;
-        } else {
-          const int4 *rp = a.rec + (int64_t(ord[c.kind ? GF + c.pos : c.pos]) * P + r) * 2;
-          q0 = rp[0];
-          q1 = rp[1];
-        }
+        if (forced) fetch(c);
         const uint32_t end = c.tau + uint32_t(q0.x);
-        if (c.slot == kNever) {
-          if (c.kind) {
-            eB.clear(c.pos);
-            zB.clear(c.pos);
-          } else {
-            eF.clear(c.pos);
-            zF.clear(c.pos);
-          }
+        if (c.slot == 0) {
+          if (c.kind) eB.clear(c.pos);
+          else eF.clear(c.pos);
         } else {
-          const uint32_t n = npend[r] - 1;
-          if (c.slot != n) pend[c.slot] = pend[n];
-          npend[r] = n;
+          // the kind's inbox front: one step on
+          const uint32_t hw = hcw[2 * r + c.kind];
+          hcw[2 * r + c.kind] = (((hw & 0xffffu) + 1u) & 0xffffu) | ((hw >> 16) - 1u) << 16;
         }
         t_last = end;
         last_kind = c.kind;
@@ -356,7 +365,8 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
           ovf = true;     // more commits than stages: never with consistent tables
         }
         ++n_emit;
-        // successors whose last predecessor this was join the target inboxes
+        // successors whose last predecessor this was join the target inboxes,
+        // kept sorted by (t_start, position)
         const uint32_t ns = uint32_t(q0.z) >> 16;
         for (uint32_t s = 0; s < ns; ++s) {
           const int4 e = s == 0 ? q1 : a.succ[q0.w + int32_t(s) - 1];
@@ -370,18 +380,26 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
             t = acc;
           }
           const uint32_t w = uint32_t(e.x);
-          const uint32_t tr = (w >> 17) & 63u;
-          const uint32_t k = npend[tr];
-          if (k >= uint32_t(K)) {
+          const uint32_t tr = (w >> 17) & 63u, tk = (w >> 16) & 1u;
+          const uint32_t h = hcw[2 * tr + tk];
+          const uint32_t head = h & 0xffffu, n = h >> 16;
+          if (n >= uint32_t(K)) {
             ovf = true;
             continue;
           }
-          pend0[int64_t(tr) * K + k] =
-              (uint64_t(t) << 17) | (uint64_t((w >> 16) & 1u) << 16) | uint64_t(gpos[w & 0xffffu]);
-          npend[tr] = k + 1;
+          uint64_t *rt = ring0 + int64_t(tr) * 2 * K + (tk ? K : 0);
+          const uint64_t x = (uint64_t(t) << 17) | (uint64_t(gpos[w & 0xffffu]) << 1) | uint64_t(tk);
+          uint32_t i = n;
+          for (; i > 0; --i) {
+            const uint64_t prev = rt[(head + i - 1) & mask];
+            if (prev <= x) break;
+            rt[(head + i) & mask] = prev;
+          }
+          rt[(head + i) & mask] = x;
+          hcw[2 * tr + tk] = h + (1u << 16);
         }
       }
-      wave_sync();
+      lds_sync();
     }
 
     // ---- outputs

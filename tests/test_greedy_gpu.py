@@ -113,11 +113,18 @@ def test_greedy_memory_caps(cap):
 
 def test_greedy_inbox_overflow_goes_through_retry():
     """A long transfer latency piles many future arrivals into one rank's
-    inbox: those candidates are finished by the second launch."""
+    inbox: those candidates are finished by the second launch, and later
+    calls get larger inboxes."""
     need_gpu()
-    prob, g, G, cls = _pipeline(2, 20, 10, comm=1000)
+    prob, g, G, cls = _pipeline(2, 40, 10, comm=1000)
     prio = W.rollout_priorities(cls, 19, seed=2)
-    check_against_oracle(prob, (g, G), prio, tag="overflow")
+    sim = dip.Sim(prob)
+    assert sim.configure_greedy(G, g) == dip.OK
+    k0 = sim.info["greedy_inbox"]
+    for call in range(3):
+        check_against_oracle(prob, (g, G), prio, sim=sim, tag=f"overflow call {call}")
+    assert sim.info["greedy_inbox"] > k0
+    sim.close()
 
 
 def test_greedy_interleaved_and_single_rank():
