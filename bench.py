@@ -42,25 +42,33 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pool_kernel_traffic.md")
-POOL_SOURCES = [os.path.join(ROOT, "paper_2504_14145_amd", "csrc", f)
-                for f in ("kern_pool.hip", "internal.h", "dev_util.h")]
+GREEDY_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "greedy_kernel_traffic.md")
+CSRC = os.path.join(ROOT, "paper_2504_14145_amd", "csrc")
+POOL_SOURCES = [os.path.join(CSRC, f) for f in ("kern_pool.hip", "internal.h", "dev_util.h")]
+GREEDY_SOURCES = [os.path.join(CSRC, f) for f in ("kern_greedy.hip", "internal.h", "dev_util.h")]
 
 
-def pool_source_hash() -> str:
+def source_hash(files) -> str:
     h = hashlib.sha256()
-    for f in POOL_SOURCES:
+    for f in files:
         with open(f, "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str, n_cand: int, slots: int):
-    """HBM bytes per pool-kernel launch from the committed counter summary,
-    if it was taken on this kernel source, workload, batch and pool size."""
-    if not os.path.exists(TRAFFIC_FILE):
+def pool_source_hash() -> str:
+    return source_hash(POOL_SOURCES)
+
+
+def measured_traffic(workload: str, n_cand: int, slots: int, path: str = TRAFFIC_FILE,
+                     sources=POOL_SOURCES):
+    """HBM bytes per launch of a kernel from its committed counter summary, if
+    it was taken on this kernel source, workload, batch and size parameter
+    (pool slots, or the greedy's inbox size)."""
+    if not os.path.exists(path):
         return None
-    want = f"{pool_source_hash()} {workload} {n_cand} {slots}"
-    for line in open(TRAFFIC_FILE):
+    want = f"{source_hash(sources)} {workload} {n_cand} {slots}"
+    for line in open(path):
         m = re.match(r"\s*traffic:\s*(\S+ \S+ \d+ \d+)\s+fetch_bytes=(\d+)\s+write_bytes=(\d+)", line)
         if m and m.group(1) == want:
             return int(m.group(2)) + int(m.group(3))
@@ -347,6 +355,15 @@ def run_greedy(args, cfg):
         ", ".join(f"{n} {t:.4f}" for n, t in zip(names, kern_avg_ms)) +
         f"; inbox {info['greedy_inbox']}; best {best}; cap {np.mean(flags & 2 > 0):.3f}")
 
+    if args.calib_copy_mib:
+        nb = args.calib_copy_mib << 20
+        src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copies: 3 x {nb} bytes")
+
     P = prob.n_ranks
     # per candidate: its priority vector read, its orders and scores written
     bytes_per_cand = 4 * G + 2 * prob.n_total + 4 + 8 * P + 1
@@ -395,7 +412,9 @@ def run_greedy(args, cfg):
         "best": {"index": best[0], "makespan_us": best[1]},
         "roofline": {"bound": "hbm", "kernel": "greedy", "achieved": achieved_gbs,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved_gbs / HBM_PEAK_GBS,
-                     "traffic": None, "algorithmic_bytes": algo_bytes},
+                     "traffic": measured_traffic(cfg.name, n_cand, info["greedy_inbox"],
+                                                 GREEDY_TRAFFIC_FILE, GREEDY_SOURCES),
+                     "algorithmic_bytes": algo_bytes},
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)

@@ -766,8 +766,8 @@ bool greedy_layout(const dip_sim *h, int K, int pwl, dip_sim::GrLaunch *L) {
   // two rings per rank; two head/count words per lane (padding lanes' stay 0)
   const int64_t lanes = int64_t(1) << pwl;
   L->off_pend = 0;
-  L->off_npend = int32_t(P * 2 * K * 8);
-  L->off_join = int32_t(P * 2 * K * 8 + 8 * lanes);
+  L->off_npend = int32_t(P * (2 * K + 1) * 8);
+  L->off_join = int32_t(P * (2 * K + 1) * 8 + 8 * lanes);
   const int64_t head = align16(std::max<int64_t>(4 * G, L->off_join + 8 * J));
   L->off_gpos = int32_t(head);
   L->off_ord = int32_t(head + align16(2 * G));

@@ -156,10 +156,12 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
   unsigned char *cb = lds + a.meta_bytes + int64_t(wave * GW + grp) * a.cand_bytes;
   int32_t *prio = reinterpret_cast<int32_t *>(cb);               // setup only ...
   // ... then the inboxes: per rank a forward ring and a backward ring of K
-  // entries each; per lane (padding lanes included) a word {head, count << 16}
-  // per kind
+  // entries each (and one spare entry); per lane (padding lanes included) a
+  // word {head, count << 16} per kind
   uint64_t *ring0 = reinterpret_cast<uint64_t *>(cb + a.off_pend);
-  uint64_t *ringF = ring0 + int64_t(r < P ? r : 0) * 2 * K;
+  // rank stride 2K + 1 entries, so that the lanes' rings start in different banks
+  const int64_t rstride = 2 * int64_t(K) + 1;
+  uint64_t *ringF = ring0 + int64_t(r < P ? r : 0) * rstride;
   uint64_t *ringB = ringF + K;
   uint32_t *hcw = reinterpret_cast<uint32_t *>(cb + a.off_npend);
   uint32_t *jtab = reinterpret_cast<uint32_t *>(cb + a.off_join);
@@ -387,7 +389,7 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
             ovf = true;
             continue;
           }
-          uint64_t *rt = ring0 + int64_t(tr) * 2 * K + (tk ? K : 0);
+          uint64_t *rt = ring0 + int64_t(tr) * rstride + (tk ? K : 0);
           const uint64_t x = (uint64_t(t) << 17) | (uint64_t(gpos[w & 0xffffu]) << 1) | uint64_t(tk);
           uint32_t i = n;
           for (; i > 0; --i) {
