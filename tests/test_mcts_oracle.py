@@ -1,0 +1,107 @@
+"""Pins of the MCTS oracle (oracle/mcts.py, Sec. 5.1): SplitMix64's published
+outputs, uniformity of the rollout shuffles, a UCB selection worked out by
+hand, brute force over every class sequence of a tiny instance, and the
+backpropagation invariants of the finished tree."""
+import itertools
+import math
+
+import numpy as np
+import pytest
+
+import oracle as O
+import oracle.mcts as M
+import workloads as W
+
+
+def test_splitmix64_reference_outputs():
+    # the reference generator's first outputs from state 0
+    assert M.splitmix64(0, 3) == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F]
+
+
+def test_shuffle_is_uniform():
+    counts = {}
+    n = 24000
+    for i in range(n):
+        p = tuple(M.shuffled([0, 1, 2, 3], seed=5, draw=1, index=i))
+        counts[p] = counts.get(p, 0) + 1
+    assert len(counts) == 24
+    exp = n / 24
+    chi2 = sum((c - exp) ** 2 / exp for c in counts.values())
+    assert chi2 < 49.7          # 23 degrees of freedom, p = 0.001
+
+
+def test_priorities_follow_positions():
+    seq = [2, 0, 3, 1]
+    group_class = [0, 0, 1, 2, 3, 3]
+    assert M.priorities_of(seq, group_class, 4).tolist() == [3, 3, 1, 4, 2, 2]
+
+
+def test_ucb_choice_by_hand():
+    """root N=10, s=100; children a (s=100, N=5), b (s=120, N=2), c (no score,
+    N=1); alpha 1, beta 0.5:
+      a: 1       + 0.5*sqrt(ln 10 / 5) = 1.3393
+      b: 100/120 + 0.5*sqrt(ln 10 / 2) = 1.3698
+      c: 0       + 0.5*sqrt(ln 10 / 1) = 0.7587   -> b."""
+    root = M.Node(None, None, 3)
+    root.untried = []
+    root.N, root.s = 10, 100.0
+    for cls, (s, n) in zip((0, 1, 2), ((100.0, 5), (120.0, 2), (M.INF, 1))):
+        v = M.Node(cls, root, 3)
+        v.s, v.N = s, n
+        root.children[cls] = v
+    assert abs(M.ucb(root.s, root.N, root.children[0], 1.0, 0.5) - 1.3393) < 1e-4
+    assert abs(M.ucb(root.s, root.N, root.children[1], 1.0, 0.5) - 1.3698) < 1e-4
+    assert abs(M.ucb(root.s, root.N, root.children[2], 1.0, 0.5) - 0.7587) < 1e-4
+    assert M.select(root, 1.0, 0.5).cls == 1
+
+
+def _tiny():
+    inst = W.pipeline_instance(2, 2, np.array([[3, 7], [5, 2]]), comm=1)
+    prob = W.compile_instance(inst)
+    g, G, cls = W.priority_groups(prob)
+    return prob, g, G, cls
+
+
+def test_exhaustive_search_finds_the_brute_force_optimum():
+    prob, g, G, cls = _tiny()
+    n = int(cls.max()) + 1
+    assert n == 4
+    all_seq = list(itertools.permutations(range(n)))
+    prio = np.stack([M.priorities_of(q, cls, n) for q in all_seq])
+    _, res = O.greedy(prob, g, G, prio)
+    brute = min(res.makespan)
+    traj, best, root = M.search(prob, g, G, cls, iterations=500, rollouts=3, seed=1)
+    assert len(traj) == 4 + 12 + 24 + 24       # every tree node expanded once, then stop
+    assert root.done
+    assert best[0] == brute
+    # the best sequence reproduces its score
+    _, r1 = O.greedy(prob, g, G, M.priorities_of(best[1], cls, n)[None, :])
+    assert r1.makespan[0] == brute
+
+
+def test_backpropagation_invariants():
+    prob = W.make_problem(1)
+    g, G, cls = W.priority_groups(prob)
+    traj, best, root = M.search(prob, g, G, cls, iterations=40, rollouts=8, seed=2)
+    # s and N of every node equal the min and the count over the iterations
+    # whose rolled-out node lies in its subtree
+    def walk(v):
+        pre = tuple(v.prefix())
+        hits = [sc for (p, sc, _) in traj if p[:len(pre)] == pre]
+        assert v.N == len(hits)
+        assert v.s == min(hits)
+        assert v.N == (1 if v.cls is not None else 0) + sum(c.N for c in v.children.values())
+        for c in v.children.values():
+            walk(c)
+    walk(root)
+    assert best[0] == min(sc for (_, sc, _) in traj)
+    assert root.s == best[0]
+
+
+def test_caps_make_rollouts_infeasible():
+    inst = W.pipeline_instance(2, 3, 4, comm=1, mem_cap=0)
+    prob = W.compile_instance(inst)
+    g, G, cls = W.priority_groups(prob)
+    traj, best, root = M.search(prob, g, G, cls, iterations=5, rollouts=4, seed=3)
+    assert all(sc == M.INF for (_, sc, _) in traj)
+    assert best[1] is None and root.s == M.INF

@@ -18,6 +18,7 @@ __all__ = [
     "pipeline_instance", "MODE_1F1B", "MODE_LIST", "OrderGenerator", "build",
     "generator_for", "gpipe_rank", "one_f_one_b_rank", "op_id", "pack", "unpack",
 ]
-from .priorities import fifo_priorities, priority_groups, rollout_priorities  # noqa: E402
+from .priorities import (expansion_draw, fifo_priorities, priority_groups,  # noqa: E402
+                         rollout_priorities)
 
-__all__ += ["fifo_priorities", "priority_groups", "rollout_priorities"]
+__all__ += ["expansion_draw", "fifo_priorities", "priority_groups", "rollout_priorities"]

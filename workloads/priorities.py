@@ -65,3 +65,13 @@ def fifo_priorities(prob: Problem, group_class: np.ndarray, op_group: np.ndarray
     mb = np.zeros(n_groups, np.int64)
     mb[op_group] = prob.op_mb
     return (int(mb.max()) + 1 - mb).astype(np.int32) if n_groups else np.zeros(0, np.int32)
+
+
+def expansion_draw(seed: int, iteration: int, n_untried: int) -> int:
+    """Index (into the ascending list of a node's untried classes) of the child
+    an MCTS expansion adds at this iteration: uniform, drawn from
+    (seed, iteration)."""
+    if n_untried <= 0:
+        raise ValueError("nothing to expand")
+    rng = np.random.default_rng(np.random.SeedSequence([seed, 93, iteration]))
+    return int(rng.integers(n_untried))
