@@ -245,6 +245,35 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
                    int16_t *out_orders, int32_t *out_makespan, int32_t *out_bubble,
                    int32_t *out_peakmem, uint8_t *out_flags, void *stream);
 
+/* MCTS rollouts (Sec. 5.1), set-up, after dip_sim_configure_greedy:
+ * group_class[n_groups] (host) puts every priority group in one of n_classes
+ * segment classes -- the elements of the sequence the search orders (the
+ * pieces of one module in one microbatch share a class, Sec. 5.1's search-
+ * space reduction).  The class at position i of a sequence gets priority
+ * n_classes - i, and every group its class's priority.  DIP_E_STATE without a
+ * grouping, DIP_E_TOPO for a class out of range.  A new grouping drops it. */
+int dip_sim_configure_rollouts(dip_sim *h, int32_t n_classes, const int32_t *group_class);
+
+/* Score n_rollouts random completions of a class prefix (Sec. 5.1's
+ * rollouts), each interleaved by dip_sim_greedy, and fold the best
+ * (makespan, rollout index) of the unflagged ones into *inout_best_key as
+ * dip_sim_argmin does (index_base 0).
+ *   prefix      host int32 [depth], distinct classes (positions 0..depth-1).
+ *   seed, draw  rollout i shuffles the other classes (ascending to start)
+ *               with Durstenfeld's Fisher-Yates: for j = m-1 down to 1 it
+ *               swaps position j with k = (hi32(u) * (j + 1)) >> 32, u the
+ *               next output of SplitMix64 (Steele, Lea, Flood 2014) started
+ *               from mix(mix(seed + (draw+1)*G) + (i+1)*G), G =
+ *               0x9E3779B97F4A7C15, mix = SplitMix64's output function.
+ *   out_prio    device int32 [n_rollouts][n_groups]: the rollouts' priorities.
+ *   out_makespan, out_flags  device [n_rollouts], as dip_sim_greedy's.
+ *   inout_best_key  device uint64.
+ * Costs are those of the last call that passed them (DIP_E_STATE if none since
+ * the grouping).  Enqueued on stream; the prefix is copied before return. */
+int dip_sim_rollouts(dip_sim *h, const int32_t *prefix, int32_t depth, int64_t n_rollouts,
+                     uint64_t seed, uint64_t draw, int32_t *out_prio, int32_t *out_makespan,
+                     uint8_t *out_flags, uint64_t *inout_best_key, void *stream);
+
 /* Per-kernel timing of evaluate (for measurement).  With enable != 0, each
  * later evaluate records HIP events on its stream around each kernel it
  * launches; dip_sim_last_profile then waits for the last of them and writes

@@ -159,13 +159,15 @@ def search(prob, op_group, n_groups, group_class, iterations, rollouts, seed,
         _, res = _greedy(prob, op_group, n_groups, prio, threads=threads)
         scores = [float(m) if f == 0 else INF for m, f in zip(res.makespan, res.flags)]
         b = min(range(rollouts), key=lambda i: (scores[i], i))
-        traj.append((tuple(prefix), scores[b], b))
-        if scores[b] < best[0]:
+        if scores[b] == INF:
+            b = -1                       # no feasible rollout
+        traj.append((tuple(prefix), scores[b] if b >= 0 else INF, b))
+        if b >= 0 and scores[b] < best[0]:
             best = (scores[b], seqs[b], t, b)
         v = x
         while v is not None:
             v.N += 1
-            v.s = min(v.s, scores[b])
+            v.s = min(v.s, scores[b] if b >= 0 else INF)
             v = v.parent
         mark_done(x, n)
     return traj, best, root

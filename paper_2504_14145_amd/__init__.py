@@ -26,7 +26,8 @@ NO_KEY = (1 << 64) - 1
 EXPORTS = ("dip_sim_abi_version", "dip_sim_check_topology", "dip_sim_check_costs",
            "dip_sim_create", "dip_sim_configure", "dip_sim_configure_pool",
            "dip_sim_configure_check", "dip_sim_get_info", "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
-           "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_greedy", "dip_sim_destroy",
+           "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_greedy",
+           "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_sim_destroy",
            "dip_sim_strerror")
 
 
@@ -88,6 +89,9 @@ def load():
         lib.dip_sim_argmin.argtypes = [vp, vp, vp, i64, i64, vp, vp]
         lib.dip_sim_configure_greedy.argtypes = [vp, i32, vp]
         lib.dip_sim_greedy.argtypes = [vp, ctypes.POINTER(Costs), vp, i64, vp, vp, vp, vp, vp, vp]
+        lib.dip_sim_configure_rollouts.argtypes = [vp, i32, vp]
+        lib.dip_sim_rollouts.argtypes = [vp, vp, i32, i64, ctypes.c_uint64, ctypes.c_uint64,
+                                         vp, vp, vp, vp, vp]
         lib.dip_sim_destroy.argtypes = [vp]
         lib.dip_sim_destroy.restype = None
         lib.dip_sim_strerror.argtypes = [ctypes.c_int]
@@ -96,7 +100,8 @@ def load():
                      "dip_sim_configure", "dip_sim_configure_pool", "dip_sim_configure_check",
                      "dip_sim_get_info",
                      "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
-                     "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_greedy"):
+                     "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_greedy",
+                     "dip_sim_configure_rollouts", "dip_sim_rollouts"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -236,6 +241,23 @@ def greedy(h, costs, prio, n_cand, out_orders, out_makespan, out_bubble, out_pea
         out_bubble.data_ptr(), out_peakmem.data_ptr(), out_flags.data_ptr(),
         _stream_ptr(stream))
     _check(rc, "dip_sim_greedy")
+
+
+def configure_rollouts(h, n_classes: int, group_class) -> int:
+    c = np.ascontiguousarray(group_class, np.int32)
+    return load().dip_sim_configure_rollouts(h, int(n_classes), c.ctypes.data)
+
+
+def rollouts(h, prefix, n_rollouts, seed, draw, out_prio, out_makespan, out_flags,
+             inout_best_key, stream=None) -> None:
+    """``prefix``: host sequence of classes; outputs are device tensors."""
+    pre = np.ascontiguousarray(prefix, np.int32)
+    rc = load().dip_sim_rollouts(h, pre.ctypes.data if pre.size else None, int(pre.size),
+                                 int(n_rollouts), int(seed) & ((1 << 64) - 1),
+                                 int(draw) & ((1 << 64) - 1), out_prio.data_ptr(),
+                                 out_makespan.data_ptr(), out_flags.data_ptr(),
+                                 inout_best_key.data_ptr(), _stream_ptr(stream))
+    _check(rc, "dip_sim_rollouts")
 
 
 def destroy(h) -> None:

@@ -171,6 +171,18 @@ struct dip_sim {
     int64_t lds = 0;
   } gr_main, gr_retry;
   int32_t gr_meta_bytes = 0;
+  // MCTS rollouts (dip_sim_configure_rollouts / dip_sim_rollouts)
+  bool rl_ok = false;
+  int32_t rl_n = 0;                    // classes
+  std::vector<int32_t> rl_class;       // [G] caller-indexed class of each group
+  int32_t *d_rl_class = nullptr;       // [G]
+  int32_t *d_rl_seq = nullptr;         // [n] prefix, then the other classes
+  int32_t *h_rl_seq = nullptr;         // pinned staging of it
+  hipEvent_t rl_seq_ev = nullptr;
+  bool rl_seq_pending = false;
+  int32_t *d_rl_scratch = nullptr;     // [cap][2n] shuffle and class priorities
+  int32_t *d_rl_bub = nullptr, *d_rl_peak = nullptr;  // [cap][P] greedy outputs
+  int64_t rl_cap = 0;
 };
 
 namespace {
@@ -786,6 +798,22 @@ bool greedy_layout(const dip_sim *h, int K, int pwl, dip_sim::GrLaunch *L) {
   return true;
 }
 
+void release_rollouts(dip_sim *h) {
+  if (h->d_rl_class) (void)hipFree(h->d_rl_class);
+  if (h->d_rl_seq) (void)hipFree(h->d_rl_seq);
+  if (h->h_rl_seq) (void)hipHostFree(h->h_rl_seq);
+  if (h->rl_seq_ev) (void)hipEventDestroy(h->rl_seq_ev);
+  if (h->d_rl_scratch) (void)hipFree(h->d_rl_scratch);
+  if (h->d_rl_bub) (void)hipFree(h->d_rl_bub);
+  if (h->d_rl_peak) (void)hipFree(h->d_rl_peak);
+  h->d_rl_class = h->d_rl_seq = h->h_rl_seq = nullptr;
+  h->rl_seq_ev = nullptr;
+  h->rl_seq_pending = false;
+  h->d_rl_scratch = h->d_rl_bub = h->d_rl_peak = nullptr;
+  h->rl_cap = 0;
+  h->rl_ok = false;
+}
+
 void release_greedy(dip_sim *h) {
   if (h->d_gr_caller) (void)hipFree(h->d_gr_caller);
   if (h->d_gr_src) (void)hipFree(h->d_gr_src);
@@ -830,6 +858,7 @@ void release(dip_sim *h) {
   if (h->h_retry_seen) (void)hipHostFree(h->h_retry_seen);
   if (h->retry_seen_ev) (void)hipEventDestroy(h->retry_seen_ev);
   if (h->d_scratch_pipe) (void)hipFree(h->d_scratch_pipe);
+  release_rollouts(h);
   release_greedy(h);
   if (h->h_stage) (void)hipHostFree(h->h_stage);
   if (h->stage_done) (void)hipEventDestroy(h->stage_done);
@@ -1319,6 +1348,7 @@ int dip_sim_configure_greedy(dip_sim *h, int32_t n_groups, const int32_t *op_gro
   if (nw > 8) return DIP_E_UNSUPPORTED;
 
   (void)hipDeviceSynchronize();   // no call may still read the old tables
+  release_rollouts(h);             // the classes belong to the old grouping
   release_greedy(h);
   h->gr_G = n_groups;
   h->gr_GF = GF;
@@ -1495,6 +1525,99 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
     h->gr_seen_n = n_cand;
   }
   return DIP_OK;
+}
+
+int dip_sim_configure_rollouts(dip_sim *h, int32_t n_classes, const int32_t *group_class) {
+  if (!h || !group_class || n_classes < 1) return DIP_E_INVAL;
+  if (!h->gr_ok) return DIP_E_STATE;
+  const int32_t G = h->gr_G;
+  std::vector<int32_t> cls(group_class, group_class + G);
+  std::vector<char> used(n_classes, 0);
+  for (int32_t g = 0; g < G; ++g) {
+    if (cls[g] < 0 || cls[g] >= n_classes) return DIP_E_TOPO;
+    used[cls[g]] = 1;
+  }
+  (void)hipDeviceSynchronize();
+  release_rollouts(h);
+  auto fail = [&](hipError_t e) {
+    g_last_hip = e;
+    release_rollouts(h);
+    return int(DIP_E_HIP);
+  };
+  hipError_t e;
+  if ((e = hipMalloc(&h->d_rl_class, size_t(G) * 4)) != hipSuccess) return fail(e);
+  if ((e = hipMalloc(&h->d_rl_seq, size_t(n_classes) * 4)) != hipSuccess) return fail(e);
+  if ((e = hipHostMalloc(reinterpret_cast<void **>(&h->h_rl_seq), size_t(n_classes) * 4,
+                         hipHostMallocDefault)) != hipSuccess)
+    return fail(e);
+  if ((e = hipEventCreateWithFlags(&h->rl_seq_ev, hipEventDisableTiming)) != hipSuccess) return fail(e);
+  if ((e = hipMemcpy(h->d_rl_class, cls.data(), size_t(G) * 4, hipMemcpyHostToDevice)) != hipSuccess)
+    return fail(e);
+  h->rl_class = cls;
+  h->rl_n = n_classes;
+  h->rl_ok = true;
+  return DIP_OK;
+}
+
+int dip_sim_rollouts(dip_sim *h, const int32_t *prefix, int32_t depth, int64_t n_rollouts,
+                     uint64_t seed, uint64_t draw, int32_t *out_prio, int32_t *out_makespan,
+                     uint8_t *out_flags, uint64_t *inout_best_key, void *stream_) {
+  if (!h || n_rollouts < 0 || depth < 0) return DIP_E_INVAL;
+  if (!h->rl_ok || !h->gr_ok) return DIP_E_STATE;
+  if (!h->gr_costs_ok) return DIP_E_STATE;
+  const int32_t n = h->rl_n;
+  if (depth > n || (depth > 0 && !prefix)) return DIP_E_INVAL;
+  if (n_rollouts == 0) return DIP_OK;
+  if (n_rollouts > INT32_MAX || !out_prio || !out_makespan || !out_flags || !inout_best_key)
+    return DIP_E_INVAL;
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  std::vector<char> on(n, 0);
+  for (int32_t d = 0; d < depth; ++d) {
+    if (prefix[d] < 0 || prefix[d] >= n || on[prefix[d]]) return DIP_E_INVAL;
+    on[prefix[d]] = 1;
+  }
+  if (h->rl_cap < n_rollouts) {
+    if (h->d_rl_scratch) (void)hipFree(h->d_rl_scratch);
+    if (h->d_rl_bub) (void)hipFree(h->d_rl_bub);
+    if (h->d_rl_peak) (void)hipFree(h->d_rl_peak);
+    h->d_rl_scratch = h->d_rl_bub = h->d_rl_peak = nullptr;
+    h->rl_cap = 0;
+    // per rollout: the shuffled classes (m <= n) and the class priorities (n)
+    DIP_HIP(hipMalloc(&h->d_rl_scratch, size_t(n_rollouts) * 2 * n * 4));
+    DIP_HIP(hipMalloc(&h->d_rl_bub, size_t(n_rollouts) * h->P * 4));
+    DIP_HIP(hipMalloc(&h->d_rl_peak, size_t(n_rollouts) * h->P * 4));
+    h->rl_cap = n_rollouts;
+  }
+  // the prefix, then the other classes ascending, through pinned staging
+  if (h->rl_seq_pending) {
+    DIP_HIP(hipEventSynchronize(h->rl_seq_ev));
+    h->rl_seq_pending = false;
+  }
+  int32_t k = 0;
+  for (int32_t d = 0; d < depth; ++d) h->h_rl_seq[k++] = prefix[d];
+  for (int32_t c = 0; c < n; ++c)
+    if (!on[c]) h->h_rl_seq[k++] = c;
+  DIP_HIP(hipMemcpyAsync(h->d_rl_seq, h->h_rl_seq, size_t(n) * 4, hipMemcpyHostToDevice, stream));
+  DIP_HIP(hipEventRecord(h->rl_seq_ev, stream));
+  h->rl_seq_pending = true;
+  RolloutArgs a{};
+  a.n = n_rollouts;
+  a.out_prio = out_prio;
+  a.prefix = h->d_rl_seq;
+  a.rest = h->d_rl_seq + depth;
+  a.group_class = h->d_rl_class;
+  a.scratch = h->d_rl_scratch;
+  a.seed = seed;
+  a.draw = draw;
+  a.depth = depth;
+  a.m = n - depth;
+  a.n_classes = n;
+  a.G = h->gr_G;
+  DIP_HIP(launch_rollout_prio(stream, a));
+  int rc = dip_sim_greedy(h, nullptr, out_prio, n_rollouts, nullptr, out_makespan, h->d_rl_bub,
+                          h->d_rl_peak, out_flags, stream_);
+  if (rc != DIP_OK) return rc;
+  return dip_sim_argmin(h, out_makespan, out_flags, n_rollouts, 0, inout_best_key, stream_);
 }
 
 int dip_sim_argmin(dip_sim *h, const int32_t *makespan, const uint8_t *flags, int64_t n_cand,

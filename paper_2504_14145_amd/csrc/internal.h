@@ -262,6 +262,21 @@ const void *greedy_kernel_ptr(int pwl, int nw);
 hipError_t launch_greedy(int pwl, int nw, int blocks, int wpb, size_t lds, hipStream_t s,
                          const GreedyArgs &a);
 
+// ---------------------------------------------------------------- rollouts
+// Random completions of a class prefix (MCTS rollouts) turned into priority
+// vectors (see kern_rollout.hip).
+struct RolloutArgs {
+  int64_t n;                 // rollouts
+  int32_t *out_prio;         // [n][G] caller-indexed group priorities
+  const int32_t *prefix;     // [depth] classes at positions 0 .. depth-1
+  const int32_t *rest;       // [m] the other classes, ascending
+  const int32_t *group_class;// [G] caller-indexed
+  int32_t *scratch;          // [n][2 * n_classes]; rollout i uses m + n_classes from i * 2 * n_classes
+  uint64_t seed, draw;
+  int32_t depth, m, n_classes, G;
+};
+hipError_t launch_rollout_prio(hipStream_t s, const RolloutArgs &a);
+
 // ---------------------------------------------------------------- argmin
 hipError_t launch_argmin(int blocks, hipStream_t s, const int32_t *ms, const uint8_t *flags,
                          int64_t n, uint64_t base, unsigned long long *key);

@@ -1,0 +1,105 @@
+"""GPU parity of the MCTS rollouts (dip_sim_rollouts) and of the GPU-batched
+search (paper_2504_14145_amd.mcts) against the CPU oracle: rollout
+priorities, scores and argmin bit-exact; whole search trajectories equal."""
+import numpy as np
+import pytest
+
+import oracle as O
+import oracle.mcts as OM
+import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2504_14145_amd as dip
+    from paper_2504_14145_amd.mcts import Search
+
+DEV = "cuda:0"
+
+
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def _sim(prob):
+    g, G, cls = W.priority_groups(prob)
+    sim = dip.Sim(prob)
+    assert sim.configure_greedy(G, g) == dip.OK
+    # upload the costs once (a zero-candidate call records nothing)
+    sim.greedy(torch.zeros((1, G), dtype=torch.int32, device=DEV))
+    return sim, g, G, cls
+
+
+@pytest.mark.parametrize("cid,depth,R", [(1, 0, 300), (1, 5, 257), (2, 17, 300), (1, 16, 9)])
+def test_rollouts_match_oracle(cid, depth, R):
+    need_gpu()
+    prob = W.make_problem(cid)
+    sim, g, G, cls = _sim(prob)
+    n = int(cls.max()) + 1
+    depth = min(depth, n)
+    rng = np.random.default_rng(depth)
+    prefix = [int(c) for c in rng.permutation(n)[:depth]]
+    assert dip.configure_rollouts(sim.h, n, cls) == dip.OK
+    prio = torch.empty((R, G), dtype=torch.int32, device=DEV)
+    ms = torch.empty(R, dtype=torch.int32, device=DEV)
+    fl = torch.empty(R, dtype=torch.uint8, device=DEV)
+    key = torch.full((1,), -1, dtype=torch.int64, device=DEV)
+    print(f"config {cid} depth {depth} rollouts {R}", flush=True)
+    dip.rollouts(sim.h, prefix, R, 12345, 7, prio, ms, fl, key)
+    torch.cuda.synchronize()
+    rest = [c for c in range(n) if c not in set(prefix)]
+    want = np.stack([OM.priorities_of(prefix + OM.shuffled(rest, 12345, 7, i), cls, n)
+                     for i in range(R)])
+    np.testing.assert_array_equal(prio.cpu().numpy(), want)
+    _, res = O.greedy(prob, g, G, want, threads=16)
+    np.testing.assert_array_equal(ms.cpu().numpy(), res.makespan)
+    np.testing.assert_array_equal(fl.cpu().numpy(), res.flags)
+    assert dip.decode_key(int(key.item())) == O.argmin(res.makespan, res.flags)[::1]
+    sim.close()
+
+
+def test_rollouts_reject_bad_prefixes_and_report_infeasible():
+    need_gpu()
+    inst = W.pipeline_instance(2, 3, 4, comm=1, mem_cap=0)
+    prob = W.compile_instance(inst)
+    sim, g, G, cls = _sim(prob)
+    n = int(cls.max()) + 1
+    assert dip.configure_rollouts(sim.h, n, cls) == dip.OK
+    prio = torch.empty((8, G), dtype=torch.int32, device=DEV)
+    ms = torch.empty(8, dtype=torch.int32, device=DEV)
+    fl = torch.empty(8, dtype=torch.uint8, device=DEV)
+    key = torch.full((1,), -1, dtype=torch.int64, device=DEV)
+    with pytest.raises(dip.DipSimError):
+        dip.rollouts(sim.h, [0, 0], 8, 1, 0, prio, ms, fl, key)      # repeated class
+    with pytest.raises(dip.DipSimError):
+        dip.rollouts(sim.h, [n], 8, 1, 0, prio, ms, fl, key)         # out of range
+    dip.rollouts(sim.h, [], 8, 1, 0, prio, ms, fl, key)
+    torch.cuda.synchronize()
+    assert (fl.cpu().numpy() == dip.FLAG_CAP).all()
+    assert dip.decode_key(int(key.item())) == (-1, -1)
+    sim.close()
+
+
+def _tiny():
+    inst = W.pipeline_instance(2, 2, np.array([[3, 7], [5, 2]]), comm=1)
+    return W.compile_instance(inst)
+
+
+@pytest.mark.parametrize("case", ["tiny", "c1", "c2", "c3"])
+def test_search_trajectory_matches_oracle(case):
+    need_gpu()
+    prob = _tiny() if case == "tiny" else W.make_problem(int(case[1]))
+    iters, R = {"tiny": (200, 3), "c1": (40, 64), "c2": (12, 128), "c3": (4, 12)}[case]
+    sim, g, G, cls = _sim(prob)
+    print(f"{case}: {iters} iterations x {R} rollouts", flush=True)
+    srch = Search(sim, cls, R, seed=21)
+    traj, best = srch.run(iters)
+    want_traj, want_best, root = OM.search(prob, g, G, cls, iters, R, seed=21, threads=16)
+    assert traj == want_traj
+    assert best[0] == want_best[0] and best[2:] == want_best[2:]
+    assert best[1] == list(want_best[1])
+    if case == "tiny":
+        assert root.done and srch.done[0] and len(traj) == 64
+    sim.close()
