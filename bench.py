@@ -9,6 +9,12 @@ synthetic candidates already resident in device memory when timing starts.
 Default workload: the 8-rank vision-language instance (ViT on ranks 0-1, LLM
 on ranks 2-7, 32 samples), 65,536 candidates per batch.
 
+With --path mcts a step is one iteration of the MCTS segment reordering
+(Sec. 5.1): tree selection and expansion on the host, then one batch of
+rollouts -- random completions drawn, interleaved and scored on the GPU --
+and backpropagation; the line also compares the best makespan found with
+random exploration given the same number of rollouts.
+
 With --path greedy a step is instead the dual-queue interleaving (Sec. 5.2)
 of one batch of priority vectors -- build every candidate's orders, score
 them -- followed by the same argmin; the priority vectors stand in for MCTS
@@ -98,8 +104,11 @@ def main():
                     help="also stream the configuration's full candidate count from pinned host "
                          "memory in chunks on two streams (copy/compute overlap); reported "
                          "separately, host-link inclusive")
-    ap.add_argument("--path", choices=("simulate", "greedy"), default="simulate",
-                    help="simulate given orders (default) or build them with the greedy")
+    ap.add_argument("--path", choices=("simulate", "greedy", "mcts"), default="simulate",
+                    help="simulate given orders (default), build them with the greedy, or "
+                         "search priorities with MCTS over GPU-batched greedy rollouts")
+    ap.add_argument("--rollouts", type=int, default=16384,
+                    help="mcts: rollouts per expansion")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, run plain device copies of this many MiB (a known-size "
                          "kernel for scaling HBM byte counters)")
@@ -122,6 +131,8 @@ def main():
     cfg = W.get(args.config)
     if args.path == "greedy":
         return run_greedy(args, cfg)
+    if args.path == "mcts":
+        return run_mcts(args, cfg)
     n_cand = args.n_cand or (cfg.chunk or cfg.n_cand)
     t0 = time.time()
     prob = W.make_problem(cfg)
@@ -415,6 +426,118 @@ def run_greedy(args, cfg):
                      "traffic": measured_traffic(cfg.name, n_cand, info["greedy_inbox"],
                                                  GREEDY_TRAFFIC_FILE, GREEDY_SOURCES),
                      "algorithmic_bytes": algo_bytes},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+    sim.close()
+
+
+def run_mcts(args, cfg):
+    """Steps = MCTS iterations with args.rollouts GPU rollouts each."""
+    import numpy as np
+    import torch
+
+    import paper_2504_14145_amd as dip
+    from paper_2504_14145_amd.mcts import Search
+    import workloads as W
+
+    R = args.rollouts
+    prob = W.make_problem(cfg)
+    op_group, G, cls = W.priority_groups(prob)
+    n_cls = int(cls.max()) + 1
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sim = dip.Sim(prob)
+    rc = sim.configure_greedy(G, op_group)
+    if rc != dip.OK:
+        raise SystemExit(f"greedy unsupported on {cfg.name}: {dip.strerror(rc)}")
+    sim.greedy(torch.zeros((1, G), dtype=torch.int32, device=dev))      # uploads the costs
+    log(f"[bench] mcts on {cfg.name}: {n_cls} segment classes, {G} groups, "
+        f"{prob.n_total} stages, {R} rollouts per expansion")
+
+    search = Search(sim, cls, R, seed=cfg.seed)
+    for t in range(args.warmup):            # warm-up iterations are part of the search
+        search.step(t)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(args.warmup, args.warmup + args.steps):
+        search.step(t)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    iters = args.warmup + args.steps
+    mcts_best = search.best[0]
+
+    # per-kernel times of one more iteration's batch
+    dip.profile(sim.h, True)
+    key = torch.full((1,), -1, dtype=torch.int64, device=dev)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    dip.rollouts(sim.h, [], R, cfg.seed, 10**6, search.prio, search.ms, search.fl, key)
+    ev[1].record()
+    torch.cuda.synchronize()
+    k_ms = dip.last_profile(sim.h)
+    batch_ms = ev[0].elapsed_time(ev[1])
+    dip.profile(sim.h, False)
+
+    # random exploration with the same number of rollouts (empty prefix)
+    best_rand = float("inf")
+    for t in range(iters):
+        key.fill_(-1)
+        dip.rollouts(sim.h, [], R, cfg.seed + 1, t, search.prio, search.ms, search.fl, key)
+        k = dip.decode_key(int(key.item()))
+        if k[0] >= 0:
+            best_rand = min(best_rand, float(k[1]))
+    log(f"[bench] {args.steps} iterations in {wall * 1e3:.1f} ms; batch {batch_ms:.3f} ms "
+        f"(greedy kernels {k_ms}); best makespan mcts {mcts_best} vs random {best_rand} "
+        f"after {iters * R} rollouts each")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle.mcts as OM
+        cores = max(1, min(16, len(os.sched_getaffinity(0))))
+        r_cpu = min(R, 1024)
+        tc = time.perf_counter()
+        it_cpu = 0
+        while True:
+            it_cpu += 1
+            OM.search(prob, op_group, G, cls, it_cpu, r_cpu, seed=cfg.seed, threads=cores)
+            if time.perf_counter() - tc >= args.cpu_seconds:
+                break
+        dt = time.perf_counter() - tc
+        done = r_cpu * it_cpu * (it_cpu + 1) // 2      # searches of 1 .. it_cpu iterations
+        cpu = {"value": done / dt, "unit": "rollouts/s", "cores": cores, "kind": "oracle",
+               "sample": f"oracle searches of 1..{it_cpu} iterations x {r_cpu} rollouts "
+                         f"({dt:.2f} s wall on {cores} threads)"}
+        log(f"[bench] cpu oracle {done / dt:.0f} rollouts/s on {cores} threads")
+
+    P = prob.n_ranks
+    bytes_per_rollout = 4 * G + 4 + 8 * P + 1 + 4 * G     # priorities written then read, scores
+    greedy_ms = k_ms[0] if k_ms else batch_ms
+    rec = {
+        "metric": "MCTS rollouts interleaved and scored/sec (segment reordering, Sec. 5.1)",
+        "value": R * args.steps / wall,
+        "unit": "rollouts/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "rollouts_per_iteration": R, "segment_classes": n_cls,
+                   "priority_groups": G, "stages_per_candidate": prob.n_total,
+                   "parallelism": "single GPU"},
+        "batch_ms": batch_ms,
+        "kernel_us": {n: t * 1e3 for n, t in zip(["greedy", "greedy_retry"], k_ms)},
+        "search": {"iterations": iters, "rollouts_each": iters * R,
+                   "mcts_best_makespan_us": mcts_best, "random_best_makespan_us": best_rand},
+        "roofline": {"bound": "hbm", "kernel": "greedy",
+                     "achieved": R * bytes_per_rollout / (greedy_ms / 1e3) / 1e9,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": R * bytes_per_rollout / (greedy_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+                     "traffic": None, "algorithmic_bytes": R * bytes_per_rollout},
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
