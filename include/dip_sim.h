@@ -251,7 +251,8 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
  * pieces of one module in one microbatch share a class, Sec. 5.1's search-
  * space reduction).  The class at position i of a sequence gets priority
  * n_classes - i, and every group its class's priority.  DIP_E_STATE without a
- * grouping, DIP_E_TOPO for a class out of range.  A new grouping drops it. */
+ * grouping, DIP_E_TOPO for a class out of range, DIP_E_UNSUPPORTED above 8192
+ * classes.  A new grouping drops it. */
 int dip_sim_configure_rollouts(dip_sim *h, int32_t n_classes, const int32_t *group_class);
 
 /* Score n_rollouts random completions of a class prefix (Sec. 5.1's

@@ -180,7 +180,6 @@ struct dip_sim {
   int32_t *h_rl_seq = nullptr;         // pinned staging of it
   hipEvent_t rl_seq_ev = nullptr;
   bool rl_seq_pending = false;
-  int32_t *d_rl_scratch = nullptr;     // [cap][2n] shuffle and class priorities
   int32_t *d_rl_bub = nullptr, *d_rl_peak = nullptr;  // [cap][P] greedy outputs
   int64_t rl_cap = 0;
 };
@@ -803,13 +802,12 @@ void release_rollouts(dip_sim *h) {
   if (h->d_rl_seq) (void)hipFree(h->d_rl_seq);
   if (h->h_rl_seq) (void)hipHostFree(h->h_rl_seq);
   if (h->rl_seq_ev) (void)hipEventDestroy(h->rl_seq_ev);
-  if (h->d_rl_scratch) (void)hipFree(h->d_rl_scratch);
   if (h->d_rl_bub) (void)hipFree(h->d_rl_bub);
   if (h->d_rl_peak) (void)hipFree(h->d_rl_peak);
   h->d_rl_class = h->d_rl_seq = h->h_rl_seq = nullptr;
   h->rl_seq_ev = nullptr;
   h->rl_seq_pending = false;
-  h->d_rl_scratch = h->d_rl_bub = h->d_rl_peak = nullptr;
+  h->d_rl_bub = h->d_rl_peak = nullptr;
   h->rl_cap = 0;
   h->rl_ok = false;
 }
@@ -1530,6 +1528,7 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
 int dip_sim_configure_rollouts(dip_sim *h, int32_t n_classes, const int32_t *group_class) {
   if (!h || !group_class || n_classes < 1) return DIP_E_INVAL;
   if (!h->gr_ok) return DIP_E_STATE;
+  if (n_classes > 8192) return DIP_E_UNSUPPORTED;   // a rollout's tables in 64 KiB of LDS
   const int32_t G = h->gr_G;
   std::vector<int32_t> cls(group_class, group_class + G);
   std::vector<char> used(n_classes, 0);
@@ -1577,13 +1576,10 @@ int dip_sim_rollouts(dip_sim *h, const int32_t *prefix, int32_t depth, int64_t n
     on[prefix[d]] = 1;
   }
   if (h->rl_cap < n_rollouts) {
-    if (h->d_rl_scratch) (void)hipFree(h->d_rl_scratch);
     if (h->d_rl_bub) (void)hipFree(h->d_rl_bub);
     if (h->d_rl_peak) (void)hipFree(h->d_rl_peak);
-    h->d_rl_scratch = h->d_rl_bub = h->d_rl_peak = nullptr;
+    h->d_rl_bub = h->d_rl_peak = nullptr;
     h->rl_cap = 0;
-    // per rollout: the shuffled classes (m <= n) and the class priorities (n)
-    DIP_HIP(hipMalloc(&h->d_rl_scratch, size_t(n_rollouts) * 2 * n * 4));
     DIP_HIP(hipMalloc(&h->d_rl_bub, size_t(n_rollouts) * h->P * 4));
     DIP_HIP(hipMalloc(&h->d_rl_peak, size_t(n_rollouts) * h->P * 4));
     h->rl_cap = n_rollouts;
@@ -1606,7 +1602,6 @@ int dip_sim_rollouts(dip_sim *h, const int32_t *prefix, int32_t depth, int64_t n
   a.prefix = h->d_rl_seq;
   a.rest = h->d_rl_seq + depth;
   a.group_class = h->d_rl_class;
-  a.scratch = h->d_rl_scratch;
   a.seed = seed;
   a.draw = draw;
   a.depth = depth;

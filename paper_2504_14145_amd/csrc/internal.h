@@ -271,7 +271,6 @@ struct RolloutArgs {
   const int32_t *prefix;     // [depth] classes at positions 0 .. depth-1
   const int32_t *rest;       // [m] the other classes, ascending
   const int32_t *group_class;// [G] caller-indexed
-  int32_t *scratch;          // [n][2 * n_classes]; rollout i uses m + n_classes from i * 2 * n_classes
   uint64_t seed, draw;
   int32_t depth, m, n_classes, G;
 };
