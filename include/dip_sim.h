@@ -275,6 +275,33 @@ int dip_sim_rollouts(dip_sim *h, const int32_t *prefix, int32_t depth, int64_t n
                      uint64_t seed, uint64_t draw, int32_t *out_prio, int32_t *out_makespan,
                      uint8_t *out_flags, uint64_t *inout_best_key, void *stream);
 
+/* Operator-level cost tables (Sec. 6.1), independent of any handle.  An item
+ * (a pipeline stage, a data edge, ...) is a run of operator rows; each row
+ * has a FLOP count, bytes of memory traffic, bytes sent, and a kind.  For
+ * configuration b, coef[b][kind] = {c_fop, c_mem, c_net} are seconds per
+ * unit (alpha / capacity: the efficiency factor over the FLOP rate, memory
+ * bandwidth, network bandwidth).  A row's latency is
+ * max(c_fop N_fop, c_mem N_mem, c_net N_net); an item's entry is
+ * ceil(1e6 * the sum of its rows' latencies in row order) microseconds,
+ * computed in float64 without fused multiply-adds; -1 if above 2^31 - 1 or
+ * if a row's kind is >= n_kinds.  Rows outside [0, n_rows) are ignored. */
+typedef struct {
+  int32_t n_items;
+  int32_t n_rows;
+  int32_t n_kinds;           /* 1 .. 256                                       */
+  const int32_t *item_ptr;   /* device [n_items+1] row range of each item      */
+  const double *n_fop;       /* device [n_rows], 8-byte aligned                */
+  const double *n_mem;       /* device [n_rows]                                */
+  const double *n_net;       /* device [n_rows]                                */
+  const uint8_t *kind;       /* device [n_rows]                                */
+} dip_op_table;
+
+/* out: device int32 [n_configs][n_items]; coef: device double
+ * [n_configs][n_kinds][3].  Enqueued on stream; DIP_E_INVAL for bad sizes,
+ * null or misaligned pointers. */
+int dip_cost_tables(const dip_op_table *t, int64_t n_configs, const double *coef, int32_t *out,
+                    void *stream);
+
 /* Per-kernel timing of evaluate (for measurement).  With enable != 0, each
  * later evaluate records HIP events on its stream around each kernel it
  * launches; dip_sim_last_profile then waits for the last of them and writes

@@ -27,8 +27,8 @@ EXPORTS = ("dip_sim_abi_version", "dip_sim_check_topology", "dip_sim_check_costs
            "dip_sim_create", "dip_sim_configure", "dip_sim_configure_pool",
            "dip_sim_configure_check", "dip_sim_get_info", "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
            "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_greedy",
-           "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_sim_destroy",
-           "dip_sim_strerror")
+           "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_cost_tables",
+           "dip_sim_destroy", "dip_sim_strerror")
 
 
 class DipSimError(RuntimeError):
@@ -48,6 +48,13 @@ class Topology(ctypes.Structure):
 class Costs(ctypes.Structure):
     _fields_ = [("op_cost", ctypes.c_void_p), ("edge_comm", ctypes.c_void_p),
                 ("slot_act", ctypes.c_void_p)]
+
+
+class OpTable(ctypes.Structure):
+    _fields_ = [("n_items", ctypes.c_int32), ("n_rows", ctypes.c_int32),
+                ("n_kinds", ctypes.c_int32), ("item_ptr", ctypes.c_void_p),
+                ("n_fop", ctypes.c_void_p), ("n_mem", ctypes.c_void_p),
+                ("n_net", ctypes.c_void_p), ("kind", ctypes.c_void_p)]
 
 
 class Info(ctypes.Structure):
@@ -90,6 +97,7 @@ def load():
         lib.dip_sim_configure_greedy.argtypes = [vp, i32, vp]
         lib.dip_sim_greedy.argtypes = [vp, ctypes.POINTER(Costs), vp, i64, vp, vp, vp, vp, vp, vp]
         lib.dip_sim_configure_rollouts.argtypes = [vp, i32, vp]
+        lib.dip_cost_tables.argtypes = [ctypes.POINTER(OpTable), i64, vp, vp, vp]
         lib.dip_sim_rollouts.argtypes = [vp, vp, i32, i64, ctypes.c_uint64, ctypes.c_uint64,
                                          vp, vp, vp, vp, vp]
         lib.dip_sim_destroy.argtypes = [vp]
@@ -101,7 +109,7 @@ def load():
                      "dip_sim_get_info",
                      "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
                      "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_greedy",
-                     "dip_sim_configure_rollouts", "dip_sim_rollouts"):
+                     "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_cost_tables"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -258,6 +266,32 @@ def rollouts(h, prefix, n_rollouts, seed, draw, out_prio, out_makespan, out_flag
                                  out_makespan.data_ptr(), out_flags.data_ptr(),
                                  inout_best_key.data_ptr(), _stream_ptr(stream))
     _check(rc, "dip_sim_rollouts")
+
+
+class DeviceOpTable:
+    """Device copies of an operator table (workloads.operators.OperatorTable
+    or any object with item_ptr, n_fop, n_mem, n_net, kind)."""
+
+    def __init__(self, table, n_kinds: int, device="cuda"):
+        import torch
+        self.t = dict(
+            item_ptr=torch.from_numpy(np.ascontiguousarray(table.item_ptr, np.int32)).to(device),
+            n_fop=torch.from_numpy(np.ascontiguousarray(table.n_fop, np.float64)).to(device),
+            n_mem=torch.from_numpy(np.ascontiguousarray(table.n_mem, np.float64)).to(device),
+            n_net=torch.from_numpy(np.ascontiguousarray(table.n_net, np.float64)).to(device),
+            kind=torch.from_numpy(np.ascontiguousarray(table.kind, np.uint8)).to(device))
+        d = self.t
+        self.n_items = int(d["item_ptr"].numel()) - 1
+        self.c = OpTable(self.n_items, int(d["kind"].numel()), int(n_kinds),
+                         d["item_ptr"].data_ptr(), d["n_fop"].data_ptr(), d["n_mem"].data_ptr(),
+                         d["n_net"].data_ptr(), d["kind"].data_ptr())
+
+
+def cost_tables(table: DeviceOpTable, coef, out, stream=None) -> None:
+    """coef: device float64 [n_configs][n_kinds][3]; out: device int32 [n_configs][n_items]."""
+    rc = load().dip_cost_tables(ctypes.byref(table.c), int(coef.shape[0]), coef.data_ptr(),
+                                out.data_ptr(), _stream_ptr(stream))
+    _check(rc, "dip_cost_tables")
 
 
 def destroy(h) -> None:
