@@ -15,6 +15,10 @@ rollouts -- random completions drawn, interleaved and scored on the GPU --
 and backpropagation; the line also compares the best makespan found with
 random exploration given the same number of rollouts.
 
+With --path cost a step builds the operator-level cost tables (Sec. 6.1) of
+a batch of configurations (efficiency factors swept per operator kind) for
+every stage and cross-rank edge of the workload.
+
 With --path greedy a step is instead the dual-queue interleaving (Sec. 5.2)
 of one batch of priority vectors -- build every candidate's orders, score
 them -- followed by the same argmin; the priority vectors stand in for MCTS
@@ -104,7 +108,7 @@ def main():
                     help="also stream the configuration's full candidate count from pinned host "
                          "memory in chunks on two streams (copy/compute overlap); reported "
                          "separately, host-link inclusive")
-    ap.add_argument("--path", choices=("simulate", "greedy", "mcts"), default="simulate",
+    ap.add_argument("--path", choices=("simulate", "greedy", "mcts", "cost"), default="simulate",
                     help="simulate given orders (default), build them with the greedy, or "
                          "search priorities with MCTS over GPU-batched greedy rollouts")
     ap.add_argument("--rollouts", type=int, default=16384,
@@ -133,6 +137,8 @@ def main():
         return run_greedy(args, cfg)
     if args.path == "mcts":
         return run_mcts(args, cfg)
+    if args.path == "cost":
+        return run_cost(args, cfg)
     n_cand = args.n_cand or (cfg.chunk or cfg.n_cand)
     t0 = time.time()
     prob = W.make_problem(cfg)
@@ -430,6 +436,89 @@ def run_greedy(args, cfg):
     }
     print(json.dumps(rec), flush=True)
     sim.close()
+
+
+FP64_OPS_PEAK = 78.6e12 / 2   # vector float64: 78.6 TFLOP/s counts an FMA as two
+
+
+def run_cost(args, cfg):
+    """Steps = dip_cost_tables over args.n_cand configurations (default 16384)."""
+    import numpy as np
+    import torch
+
+    import paper_2504_14145_amd as dip
+    import workloads as W
+    from workloads.operators import N_KINDS, coefficient_sweep, operator_table
+
+    n_conf = args.n_cand or 16384
+    prob = W.make_problem(cfg)
+    tab = operator_table(prob)
+    rows, items = len(tab.kind), len(tab.item_ptr) - 1
+    coef_np = coefficient_sweep(n_conf, seed=cfg.seed)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    dt = dip.DeviceOpTable(tab, N_KINDS, dev)
+    coef = torch.from_numpy(coef_np).to(dev)
+    out = torch.empty((n_conf, items), dtype=torch.int32, device=dev)
+    log(f"[bench] cost tables on {cfg.name}: {items} items ({prob.n_total} stages, "
+        f"{prob.n_edges} edges), {rows} operator rows, {n_conf} configurations")
+    for _ in range(max(args.warmup, 1)):
+        dip.cost_tables(dt, coef, out)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for a, b in ev:
+        a.record()
+        dip.cost_tables(dt, coef, out)
+        b.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    k_s = sum(a.elapsed_time(b) for a, b in ev) / len(ev) / 1e3
+    ops = 6.0 * rows * n_conf        # per row: three products, two maxima, one sum
+    log(f"[bench] {args.steps} steps in {wall * 1e3:.2f} ms; kernel {k_s * 1e3:.3f} ms; "
+        f"{ops / k_s / 1e12:.2f} T float64 ops/s")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle.costmodel as OC
+        sample = 2
+        tc = time.perf_counter()
+        done = 0
+        while True:
+            OC.cost_tables(tab, coef_np[:sample])
+            done += sample
+            if time.perf_counter() - tc >= args.cpu_seconds:
+                break
+        dt_c = time.perf_counter() - tc
+        cpu = {"value": done * items / dt_c, "unit": "table entries/s", "cores": 1,
+               "kind": "oracle",
+               "sample": f"{done} configurations x {items} items ({dt_c:.2f} s wall, one thread)"}
+        log(f"[bench] cpu oracle {done * items / dt_c:.0f} entries/s")
+
+    rec = {
+        "metric": "operator-level cost-table entries built/sec (Sec. 6.1)",
+        "value": n_conf * items * args.steps / wall,
+        "unit": "table entries/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f64",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "configurations": n_conf, "items": items,
+                   "operator_rows": rows, "parallelism": "single GPU"},
+        "kernel_us": {"cost_table": k_s * 1e6},
+        "roofline": {"bound": "alu", "kernel": "cost_table", "achieved": ops / k_s / 1e12,
+                     "peak": FP64_OPS_PEAK / 1e12, "unit": "T float64 ops/s",
+                     "frac": ops / k_s / FP64_OPS_PEAK, "traffic": None,
+                     "algorithmic_bytes": n_conf * items * 4 + coef_np.nbytes + rows * 25},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
 
 
 def run_mcts(args, cfg):

@@ -297,8 +297,8 @@ typedef struct {
 } dip_op_table;
 
 /* out: device int32 [n_configs][n_items]; coef: device double
- * [n_configs][n_kinds][3].  Enqueued on stream; DIP_E_INVAL for bad sizes,
- * null or misaligned pointers. */
+ * [n_configs][n_kinds][3].  Enqueued on stream; DIP_E_INVAL for bad sizes
+ * (n_configs above 65535 * 256), null or misaligned pointers. */
 int dip_cost_tables(const dip_op_table *t, int64_t n_configs, const double *coef, int32_t *out,
                     void *stream);
 

@@ -52,7 +52,7 @@ def test_edge_cases_and_many_configurations():
     a = np.array(rows, np.float64)
     tab = OperatorTable(ptr, a[:, 1].copy(), a[:, 2].copy(), a[:, 3].copy(),
                         a[:, 0].astype(np.uint8), 4, 0)
-    coef = coefficient_sweep(70001, seed=3)          # more than one grid row of configurations
+    coef = coefficient_sweep(70001, seed=3)          # many blocks of configurations
     got = run(tab, coef)
     assert (got[:, 1] == -1).all() and (got[:, 2] == 0).all() and (got[:, 3] == -1).all()
     # items 0 and 3 against the oracle (it has no notion of a bad kind)
