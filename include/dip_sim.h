@@ -275,6 +275,39 @@ int dip_sim_rollouts(dip_sim *h, const int32_t *prefix, int32_t depth, int64_t n
                      uint64_t seed, uint64_t draw, int32_t *out_prio, int32_t *out_makespan,
                      uint8_t *out_flags, uint64_t *inout_best_key, void *stream);
 
+/* Per-layer memory optimisation (Sec. 5.3), set-up.  A stage pair is an
+ * activation slot (its forward and backward, one rank).  Its layers are
+ * slot_layers[s] .. slot_layers[s+1]-1 (host, [n_slots+1], from 0), and layer
+ * l's strategies cost layer_time[l][k] microseconds (forward and backward
+ * together) and hold layer_mem[l][k] memory units (host int64, >= 0,
+ * k < n_strategies).  Per pair the library keeps up to n_candidates (2 .. 8)
+ * candidates: the exact (time, memory) Pareto front of its layers' choices,
+ * its fastest point, its leanest point, and for each of the n_candidates - 2
+ * equal buckets of the memory range between them the least time whose memory
+ * is at most the bucket's upper edge lo + floor((hi - lo) k / (n - 2))
+ * (Sec. 5.3's multiple-choice knapsack); equal points once, by time.
+ * DIP_E_TOPO unless every slot has one forward and one backward on one rank;
+ * DIP_E_RANGE for a negative entry or a candidate memory above 2^31 - 1. */
+int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64_t *layer_time,
+                             const int64_t *layer_mem, int32_t n_strategies,
+                             int32_t n_candidates);
+
+/* For every candidate schedule (orders as dip_sim_evaluate reads them) and
+ * rank, choose one candidate per stage pair of the rank so that the memory at
+ * every forward start -- the pairs whose forward comes no later and whose
+ * backward no earlier in the rank's order -- stays within mem_cap[r] (none if
+ * negative), by the greedy warm start of Sec. 5.3's ILP: every pair on its
+ * fastest candidate; while the most loaded forward start (the earliest pair
+ * among equal loads) is over the cap, move the live pair whose next
+ * candidate adds the least time per memory unit freed (lowest pair on ties);
+ * stop when none can move.  Outputs, device [n_cand][P]: out_time (int64,
+ * the rank's total pair time), out_peak (memory at the most loaded forward
+ * start), out_status (1 within the cap, 0 the cap cannot be met, 2 the rank's
+ * section is not a permutation: time and peak -1).  Pairs are numbered per
+ * rank in slot order. */
+int dip_sim_memopt(dip_sim *h, const int16_t *orders, int64_t n_cand, int64_t *out_time,
+                   int32_t *out_peak, uint8_t *out_status, void *stream);
+
 /* Operator-level cost tables (Sec. 6.1), independent of any handle.  An item
  * (a pipeline stage, a data edge, ...) is a run of operator rows; each row
  * has a FLOP count, bytes of memory traffic, bytes sent, and a kind.  For

@@ -10,7 +10,7 @@ CSRC = os.path.join(HERE, "csrc")
 SOURCES = [os.path.join(CSRC, f) for f in
            ("host.hip", "kern_general.hip", "kern_pipe.hip", "kern_pipe_lds.hip",
             "kern_check.hip", "kern_pool.hip", "kern_greedy.hip", "kern_rollout.hip",
-            "kern_costmodel.hip", "kern_argmin.hip")]
+            "kern_costmodel.hip", "kern_memopt.hip", "kern_argmin.hip")]
 LIB = os.path.join(HERE, "libdip_sim.so")
 INCLUDE = os.path.join(ROOT, "include")
 

@@ -182,6 +182,12 @@ struct dip_sim {
   bool rl_seq_pending = false;
   int32_t *d_rl_bub = nullptr, *d_rl_peak = nullptr;  // [cap][P] greedy outputs
   int64_t rl_cap = 0;
+  // per-layer memory optimisation (dip_sim_configure_memopt / dip_sim_memopt)
+  bool mo_ok = false;
+  int32_t mo_max_pairs = 0;
+  int32_t *d_mo_pair_off = nullptr, *d_mo_lid_pair = nullptr, *d_mo_ncand = nullptr;
+  int64_t *d_mo_time = nullptr;
+  int32_t *d_mo_mem = nullptr;
 };
 
 namespace {
@@ -812,6 +818,18 @@ void release_rollouts(dip_sim *h) {
   h->rl_ok = false;
 }
 
+void release_memopt(dip_sim *h) {
+  if (h->d_mo_pair_off) (void)hipFree(h->d_mo_pair_off);
+  if (h->d_mo_lid_pair) (void)hipFree(h->d_mo_lid_pair);
+  if (h->d_mo_ncand) (void)hipFree(h->d_mo_ncand);
+  if (h->d_mo_time) (void)hipFree(h->d_mo_time);
+  if (h->d_mo_mem) (void)hipFree(h->d_mo_mem);
+  h->d_mo_pair_off = h->d_mo_lid_pair = h->d_mo_ncand = nullptr;
+  h->d_mo_time = nullptr;
+  h->d_mo_mem = nullptr;
+  h->mo_ok = false;
+}
+
 void release_greedy(dip_sim *h) {
   if (h->d_gr_caller) (void)hipFree(h->d_gr_caller);
   if (h->d_gr_src) (void)hipFree(h->d_gr_src);
@@ -858,6 +876,7 @@ void release(dip_sim *h) {
   if (h->d_scratch_pipe) (void)hipFree(h->d_scratch_pipe);
   release_rollouts(h);
   release_greedy(h);
+  release_memopt(h);
   if (h->h_stage) (void)hipHostFree(h->h_stage);
   if (h->stage_done) (void)hipEventDestroy(h->stage_done);
   for (hipEvent_t &ev : h->prof_ev)
@@ -1613,6 +1632,149 @@ int dip_sim_rollouts(dip_sim *h, const int32_t *prefix, int32_t depth, int64_t n
                           h->d_rl_peak, out_flags, stream_);
   if (rc != DIP_OK) return rc;
   return dip_sim_argmin(h, out_makespan, out_flags, n_rollouts, 0, inout_best_key, stream_);
+}
+
+int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64_t *layer_time,
+                             const int64_t *layer_mem, int32_t n_strategies, int32_t n_candidates) {
+  if (!h || !slot_layers || n_strategies < 1 || n_candidates < 2 ||
+      n_candidates > kMemoptMaxCands)
+    return DIP_E_INVAL;
+  const int32_t P = h->P, N = h->N, ns = h->n_slots;
+  // every slot: one forward and one backward on one rank
+  std::vector<int32_t> f_of(ns, -1), b_of(ns, -1);
+  for (int32_t g = 0; g < N; ++g) {
+    int32_t &x = h->kind[g] ? b_of[h->op_slot[g]] : f_of[h->op_slot[g]];
+    if (x >= 0) return DIP_E_TOPO;
+    x = g;
+  }
+  for (int32_t q = 0; q < ns; ++q)
+    if (f_of[q] < 0 || b_of[q] < 0 || h->rank_of[f_of[q]] != h->rank_of[b_of[q]]) return DIP_E_TOPO;
+  if (slot_layers[0] != 0) return DIP_E_INVAL;
+  for (int32_t q = 0; q < ns; ++q)
+    if (slot_layers[q + 1] < slot_layers[q]) return DIP_E_INVAL;
+  if (slot_layers[ns] > 0 && (!layer_time || !layer_mem)) return DIP_E_INVAL;
+  // candidates per slot: exact Pareto front of the layers' choices, then the
+  // fastest, the leanest and one knapsack answer per bucket edge
+  struct Pt {
+    int64_t t, m;
+  };
+  std::vector<std::vector<Pt>> cand(ns);
+  for (int32_t q = 0; q < ns; ++q) {
+    std::vector<Pt> front{{0, 0}}, pts;
+    for (int32_t l = slot_layers[q]; l < slot_layers[q + 1]; ++l) {
+      pts.clear();
+      for (const Pt &p : front)
+        for (int32_t k = 0; k < n_strategies; ++k) {
+          const int64_t t = layer_time[int64_t(l) * n_strategies + k];
+          const int64_t m = layer_mem[int64_t(l) * n_strategies + k];
+          if (t < 0 || m < 0) return DIP_E_RANGE;
+          pts.push_back({p.t + t, p.m + m});
+        }
+      std::sort(pts.begin(), pts.end(),
+                [](const Pt &x, const Pt &y) { return x.m != y.m ? x.m < y.m : x.t < y.t; });
+      front.clear();
+      for (const Pt &p : pts)
+        if (front.empty() || (p.t < front.back().t && p.m != front.back().m)) front.push_back(p);
+      if (front.size() > (size_t(1) << 20)) return DIP_E_UNSUPPORTED;
+    }
+    std::vector<Pt> pick{front.back(), front.front()};
+    const int64_t lo = front.front().m, hi = front.back().m;
+    for (int32_t k = 1; k + 1 < n_candidates; ++k) {
+      const int64_t edge = lo + ((hi - lo) * k) / (n_candidates - 2);
+      size_t j = 0;
+      while (j + 1 < front.size() && front[j + 1].m <= edge) ++j;
+      pick.push_back(front[j]);
+    }
+    std::sort(pick.begin(), pick.end(),
+              [](const Pt &x, const Pt &y) { return x.t != y.t ? x.t < y.t : x.m < y.m; });
+    std::vector<Pt> uniq;
+    for (const Pt &p : pick)
+      if (uniq.empty() || uniq.back().t != p.t || uniq.back().m != p.m) uniq.push_back(p);
+    for (const Pt &p : uniq)
+      if (p.m > INT32_MAX) return DIP_E_RANGE;
+    cand[q] = uniq;
+  }
+  // pairs per rank in slot order; each op's pair index and kind
+  std::vector<int32_t> pair_off(P + 1, 0), lid_pair(N, 0), slot_pair(ns, 0);
+  std::vector<int32_t> ncand, mem;
+  std::vector<int64_t> tim;
+  int32_t max_pairs = 0;
+  for (int32_t r = 0; r < P; ++r) {
+    int32_t i = 0;
+    for (int32_t q = 0; q < ns; ++q) {
+      if (h->rank_of[f_of[q]] != r) continue;
+      slot_pair[q] = i++;
+      ncand.push_back(int32_t(cand[q].size()));
+      for (int32_t j = 0; j < kMemoptMaxCands; ++j) {
+        const bool in = j < int32_t(cand[q].size());
+        tim.push_back(in ? cand[q][j].t : 0);
+        mem.push_back(in ? int32_t(cand[q][j].m) : 0);
+      }
+    }
+    pair_off[r + 1] = pair_off[r] + i;
+    max_pairs = std::max(max_pairs, i);
+  }
+  for (int32_t g = 0; g < N; ++g)
+    lid_pair[g] = int32_t(uint32_t(slot_pair[h->op_slot[g]]) | (uint32_t(h->kind[g]) << 31));
+  (void)hipDeviceSynchronize();
+  release_memopt(h);
+  auto fail = [&](hipError_t e) {
+    g_last_hip = e;
+    release_memopt(h);
+    return int(DIP_E_HIP);
+  };
+  hipError_t e;
+  const size_t npairs = std::max<size_t>(ncand.size(), 1);
+  if ((e = hipMalloc(&h->d_mo_pair_off, size_t(P + 1) * 4)) != hipSuccess) return fail(e);
+  if ((e = hipMalloc(&h->d_mo_lid_pair, size_t(std::max(N, 1)) * 4)) != hipSuccess) return fail(e);
+  if ((e = hipMalloc(&h->d_mo_ncand, npairs * 4)) != hipSuccess) return fail(e);
+  if ((e = hipMalloc(&h->d_mo_time, npairs * kMemoptMaxCands * 8)) != hipSuccess) return fail(e);
+  if ((e = hipMalloc(&h->d_mo_mem, npairs * kMemoptMaxCands * 4)) != hipSuccess) return fail(e);
+  if ((e = hipMemcpy(h->d_mo_pair_off, pair_off.data(), size_t(P + 1) * 4, hipMemcpyHostToDevice)) ||
+      (N > 0 && (e = hipMemcpy(h->d_mo_lid_pair, lid_pair.data(), size_t(N) * 4, hipMemcpyHostToDevice))) ||
+      (!ncand.empty() &&
+       ((e = hipMemcpy(h->d_mo_ncand, ncand.data(), ncand.size() * 4, hipMemcpyHostToDevice)) ||
+        (e = hipMemcpy(h->d_mo_time, tim.data(), tim.size() * 8, hipMemcpyHostToDevice)) ||
+        (e = hipMemcpy(h->d_mo_mem, mem.data(), mem.size() * 4, hipMemcpyHostToDevice)))))
+    return fail(e);
+  h->mo_max_pairs = max_pairs;
+  h->mo_ok = true;
+  return DIP_OK;
+}
+
+int dip_sim_memopt(dip_sim *h, const int16_t *orders, int64_t n_cand, int64_t *out_time,
+                   int32_t *out_peak, uint8_t *out_status, void *stream) {
+  if (!h || n_cand < 0) return DIP_E_INVAL;
+  if (!h->mo_ok) return DIP_E_STATE;
+  if (n_cand == 0) return DIP_OK;
+  if (!orders || !out_time || !out_peak || !out_status) return DIP_E_INVAL;
+  if ((reinterpret_cast<uintptr_t>(out_time) & 7) || (reinterpret_cast<uintptr_t>(out_peak) & 3) ||
+      (reinterpret_cast<uintptr_t>(orders) & 1))
+    return DIP_E_INVAL;
+  MemoptArgs a{};
+  a.orders = orders;
+  a.n_cand = n_cand;
+  a.stride = h->stride;
+  a.out_time = out_time;
+  a.out_peak = out_peak;
+  a.out_status = out_status;
+  a.rank_off = h->d_rank_off;
+  a.pair_off = h->d_mo_pair_off;
+  a.lid_pair = h->d_mo_lid_pair;
+  a.n_cands = h->d_mo_ncand;
+  a.cand_time = h->d_mo_time;
+  a.cand_mem = h->d_mo_mem;
+  a.cap = h->d_cap;
+  a.P = h->P;
+  a.max_pairs = std::max(h->mo_max_pairs, 1);
+  a.bytes_per_thread = int32_t(align16(int64_t(a.max_pairs) * 9));
+  int tpb = 256;
+  while (tpb > 1 && int64_t(tpb) * a.bytes_per_thread > 65536) tpb /= 2;
+  if (int64_t(tpb) * a.bytes_per_thread > 65536) return DIP_E_UNSUPPORTED;
+  if (n_cand * h->P / tpb + 1 > INT32_MAX) return DIP_E_INVAL;
+  (void)hipGetLastError();
+  DIP_HIP(launch_memopt(tpb, static_cast<hipStream_t>(stream), a));
+  return DIP_OK;
 }
 
 int dip_sim_argmin(dip_sim *h, const int32_t *makespan, const uint8_t *flags, int64_t n_cand,

@@ -276,6 +276,29 @@ struct RolloutArgs {
 };
 hipError_t launch_rollout_prio(hipStream_t s, const RolloutArgs &a);
 
+// ---------------------------------------------------------------- memory optimisation
+// Per (candidate schedule, rank): one memory candidate per stage pair (see
+// kern_memopt.hip).
+constexpr int kMemoptMaxCands = 8;
+struct MemoptArgs {
+  const int16_t *orders;
+  int64_t n_cand;
+  int64_t stride;
+  int64_t *out_time;          // [n][P]
+  int32_t *out_peak;          // [n][P]
+  uint8_t *out_status;        // [n][P] 1 within the cap, 0 not reachable, 2 order not a permutation
+  const int32_t *rank_off;    // [P+1] ops
+  const int32_t *pair_off;    // [P+1] pairs of each rank (slot order)
+  const int32_t *lid_pair;    // [N] pair index on its rank | kind << 31 (by global op)
+  const int32_t *n_cands;     // [pairs]
+  const int64_t *cand_time;   // [pairs][kMemoptMaxCands], time ascending
+  const int32_t *cand_mem;    // [pairs][kMemoptMaxCands]
+  const int32_t *cap;         // [P]
+  int32_t P, max_pairs;
+  int32_t bytes_per_thread;   // LDS per thread (16-aligned)
+};
+hipError_t launch_memopt(int threads_per_block, hipStream_t s, const MemoptArgs &a);
+
 // ---------------------------------------------------------------- argmin
 hipError_t launch_argmin(int blocks, hipStream_t s, const int32_t *ms, const uint8_t *flags,
                          int64_t n, uint64_t base, unsigned long long *key);
