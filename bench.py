@@ -15,6 +15,11 @@ rollouts -- random completions drawn, interleaved and scored on the GPU --
 and backpropagation; the line also compares the best makespan found with
 random exploration given the same number of rollouts.
 
+With --path memopt a step is Sec. 5.3's per-layer memory optimisation of a
+batch of candidate schedules: for every schedule and rank, one memory
+candidate per stage pair under a cap that binds (60 % of the median
+keep-everything peak).
+
 With --path cost a step builds the operator-level cost tables (Sec. 6.1) of
 a batch of configurations (efficiency factors swept per operator kind) for
 every stage and cross-rank edge of the workload.
@@ -108,7 +113,8 @@ def main():
                     help="also stream the configuration's full candidate count from pinned host "
                          "memory in chunks on two streams (copy/compute overlap); reported "
                          "separately, host-link inclusive")
-    ap.add_argument("--path", choices=("simulate", "greedy", "mcts", "cost"), default="simulate",
+    ap.add_argument("--path", choices=("simulate", "greedy", "mcts", "cost", "memopt"),
+                    default="simulate",
                     help="simulate given orders (default), build them with the greedy, or "
                          "search priorities with MCTS over GPU-batched greedy rollouts")
     ap.add_argument("--rollouts", type=int, default=16384,
@@ -139,6 +145,8 @@ def main():
         return run_mcts(args, cfg)
     if args.path == "cost":
         return run_cost(args, cfg)
+    if args.path == "memopt":
+        return run_memopt(args, cfg)
     n_cand = args.n_cand or (cfg.chunk or cfg.n_cand)
     t0 = time.time()
     prob = W.make_problem(cfg)
@@ -432,6 +440,100 @@ def run_greedy(args, cfg):
                      "traffic": measured_traffic(cfg.name, n_cand, info["greedy_inbox"],
                                                  GREEDY_TRAFFIC_FILE, GREEDY_SOURCES),
                      "algorithmic_bytes": algo_bytes},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+    sim.close()
+
+
+def run_memopt(args, cfg):
+    """Steps = dip_sim_memopt over a batch of candidate schedules."""
+    import numpy as np
+    import torch
+
+    import oracle
+    import paper_2504_14145_amd as dip
+    import workloads as W
+    from workloads.strategies import strategy_table
+
+    n_cand = args.n_cand or (cfg.chunk or cfg.n_cand)
+    S = 6
+    prob = W.make_problem(cfg)
+    tab = strategy_table(prob)
+    rows = W.generator_for(prob, cfg).generate(0, n_cand)
+    # a cap that binds: 60 % of the median keep-everything peak of a sample
+    peak = oracle.evaluate(prob, rows[:min(n_cand, 2048)], threads=16).peak
+    prob.mem_cap[:] = int(np.median(peak) * 0.6)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sim = dip.Sim(prob)
+    rc = dip.configure_memopt(sim.h, tab.slot_layers, tab.time, tab.mem, S)
+    if rc != dip.OK:
+        raise SystemExit(f"memopt unsupported on {cfg.name}: {dip.strerror(rc)}")
+    orders = torch.from_numpy(rows).to(dev)
+    P = prob.n_ranks
+    t_out = torch.empty((n_cand, P), dtype=torch.int64, device=dev)
+    p_out = torch.empty((n_cand, P), dtype=torch.int32, device=dev)
+    s_out = torch.empty((n_cand, P), dtype=torch.uint8, device=dev)
+    log(f"[bench] memopt on {cfg.name}: {n_cand} schedules x {P} ranks, {prob.n_slots} stage "
+        f"pairs, {len(tab.time)} layers, cap {prob.mem_cap[0]}, {S} candidates per pair")
+    for _ in range(max(args.warmup, 1)):
+        dip.memopt(sim.h, orders, n_cand, t_out, p_out, s_out)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for a, b in ev:
+        a.record()
+        dip.memopt(sim.h, orders, n_cand, t_out, p_out, s_out)
+        b.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    k_s = sum(a.elapsed_time(b) for a, b in ev) / len(ev) / 1e3
+    st = s_out.cpu().numpy()
+    log(f"[bench] {args.steps} steps in {wall * 1e3:.2f} ms; kernel {k_s * 1e3:.3f} ms; "
+        f"within cap {np.mean(st == 1):.3f}, out of reach {np.mean(st == 0):.3f}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle.memopt as MO
+        cands = MO.pair_candidates(tab, S)
+        sample = min(n_cand, 64)
+        tc = time.perf_counter()
+        done = 0
+        while True:
+            MO.optimise(prob, tab, cands, rows[:sample])
+            done += sample
+            if time.perf_counter() - tc >= args.cpu_seconds:
+                break
+        dt = time.perf_counter() - tc
+        cpu = {"value": done / dt, "unit": "schedules/s", "cores": 1, "kind": "oracle",
+               "sample": f"first {sample} schedules, {done // sample}x ({dt:.2f} s, one thread)"}
+        log(f"[bench] cpu oracle {done / dt:.0f} schedules/s")
+
+    bytes_per = 2 * prob.n_total + P * (8 + 4 + 1)
+    rec = {
+        "metric": "candidate schedules memory-optimised/sec (per-layer strategies, Sec. 5.3)",
+        "value": n_cand * args.steps / wall,
+        "unit": "schedules/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": wall / args.steps * 1e3,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "n_cand": n_cand, "ranks": P,
+                   "stage_pairs": prob.n_slots, "candidates_per_pair": S,
+                   "cap_units": int(prob.mem_cap[0]), "parallelism": "single GPU"},
+        "kernel_us": {"memopt": k_s * 1e6},
+        "within_cap": float(np.mean(st == 1)),
+        "roofline": {"bound": "hbm", "kernel": "memopt",
+                     "achieved": n_cand * bytes_per / k_s / 1e9, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": n_cand * bytes_per / k_s / 1e9 / HBM_PEAK_GBS,
+                     "traffic": None, "algorithmic_bytes": n_cand * bytes_per},
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
