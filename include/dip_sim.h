@@ -287,7 +287,8 @@ int dip_sim_rollouts(dip_sim *h, const int32_t *prefix, int32_t depth, int64_t n
  * is at most the bucket's upper edge lo + floor((hi - lo) k / (n - 2))
  * (Sec. 5.3's multiple-choice knapsack); equal points once, by time.
  * DIP_E_TOPO unless every slot has one forward and one backward on one rank;
- * DIP_E_RANGE for a negative entry or a candidate memory above 2^31 - 1. */
+ * DIP_E_RANGE for a negative entry or a candidate memory above 2^31 - 1;
+ * DIP_E_UNSUPPORTED for a rank of 16384 pairs or more. */
 int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64_t *layer_time,
                              const int64_t *layer_mem, int32_t n_strategies,
                              int32_t n_candidates);
@@ -304,7 +305,9 @@ int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64
  * the rank's total pair time), out_peak (memory at the most loaded forward
  * start), out_status (1 within the cap, 0 the cap cannot be met, 2 the rank's
  * section is not a permutation: time and peak -1).  Pairs are numbered per
- * rank in slot order. */
+ * rank in slot order.  Enqueued on stream; DIP_E_STATE before
+ * dip_sim_configure_memopt, DIP_E_INVAL for null or misaligned outputs,
+ * DIP_E_UNSUPPORTED when a rank's state does not fit in LDS. */
 int dip_sim_memopt(dip_sim *h, const int16_t *orders, int64_t n_cand, int64_t *out_time,
                    int32_t *out_peak, uint8_t *out_status, void *stream);
 

@@ -33,4 +33,28 @@ __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
 }
 
+// min / max of one value over all 64 lanes of a wave, returned to every lane
+// as a uniform value: quad permutations and the half-row and row mirrors
+// reduce each row of 16 lanes, then the four row results are read out.
+// Every lane of the wave must be active.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_row(uint32_t v) {
+  return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), CTRL, 0xf, 0xf, false));
+}
+template <bool MAX>
+__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v) {
+  auto op = [](uint32_t x, uint32_t y) { return MAX ? max(x, y) : min(x, y); };
+  v = op(v, dpp_row<0xb1>(v));    // quad_perm [1,0,3,2]
+  v = op(v, dpp_row<0x4e>(v));    // quad_perm [2,3,0,1]
+  v = op(v, dpp_row<0x141>(v));   // row_half_mirror
+  v = op(v, dpp_row<0x140>(v));   // row_mirror
+  const uint32_t r0 = uint32_t(__builtin_amdgcn_readlane(int(v), 0));
+  const uint32_t r1 = uint32_t(__builtin_amdgcn_readlane(int(v), 16));
+  const uint32_t r2 = uint32_t(__builtin_amdgcn_readlane(int(v), 32));
+  const uint32_t r3 = uint32_t(__builtin_amdgcn_readlane(int(v), 48));
+  return op(op(r0, r1), op(r2, r3));
+}
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t v) { return wave_reduce_u32<false>(v); }
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) { return wave_reduce_u32<true>(v); }
+
 }  // namespace dipsim

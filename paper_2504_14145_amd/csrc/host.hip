@@ -185,9 +185,10 @@ struct dip_sim {
   // per-layer memory optimisation (dip_sim_configure_memopt / dip_sim_memopt)
   bool mo_ok = false;
   int32_t mo_max_pairs = 0;
-  int32_t *d_mo_pair_off = nullptr, *d_mo_lid_pair = nullptr, *d_mo_ncand = nullptr;
+  int32_t *d_mo_pair_off = nullptr, *d_mo_lid_pair = nullptr;
   int64_t *d_mo_time = nullptr;
-  int32_t *d_mo_mem = nullptr;
+  int32_t *d_mo_mem = nullptr, *d_mo_dm = nullptr;
+  uint32_t *d_mo_key = nullptr;
 };
 
 namespace {
@@ -821,12 +822,14 @@ void release_rollouts(dip_sim *h) {
 void release_memopt(dip_sim *h) {
   if (h->d_mo_pair_off) (void)hipFree(h->d_mo_pair_off);
   if (h->d_mo_lid_pair) (void)hipFree(h->d_mo_lid_pair);
-  if (h->d_mo_ncand) (void)hipFree(h->d_mo_ncand);
   if (h->d_mo_time) (void)hipFree(h->d_mo_time);
   if (h->d_mo_mem) (void)hipFree(h->d_mo_mem);
-  h->d_mo_pair_off = h->d_mo_lid_pair = h->d_mo_ncand = nullptr;
+  if (h->d_mo_key) (void)hipFree(h->d_mo_key);
+  if (h->d_mo_dm) (void)hipFree(h->d_mo_dm);
+  h->d_mo_pair_off = h->d_mo_lid_pair = nullptr;
   h->d_mo_time = nullptr;
-  h->d_mo_mem = nullptr;
+  h->d_mo_mem = h->d_mo_dm = nullptr;
+  h->d_mo_key = nullptr;
   h->mo_ok = false;
 }
 
@@ -1696,20 +1699,47 @@ int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64
   }
   // pairs per rank in slot order; each op's pair index and kind
   std::vector<int32_t> pair_off(P + 1, 0), lid_pair(N, 0), slot_pair(ns, 0);
-  std::vector<int32_t> ncand, mem;
+  std::vector<int32_t> mem, mdm;
   std::vector<int64_t> tim;
+  std::vector<uint32_t> mkey;
   int32_t max_pairs = 0;
+  struct Move {
+    int64_t dt, dm;
+    int32_t at;                  // index into the rank's [pair][candidate] slice
+  };
+  std::vector<Move> moves;
   for (int32_t r = 0; r < P; ++r) {
     int32_t i = 0;
+    const size_t first = tim.size();
+    moves.clear();
     for (int32_t q = 0; q < ns; ++q) {
       if (h->rank_of[f_of[q]] != r) continue;
-      slot_pair[q] = i++;
-      ncand.push_back(int32_t(cand[q].size()));
+      slot_pair[q] = i;
+      const int32_t nc = int32_t(cand[q].size());
       for (int32_t j = 0; j < kMemoptMaxCands; ++j) {
-        const bool in = j < int32_t(cand[q].size());
+        const bool in = j < nc;
         tim.push_back(in ? cand[q][j].t : 0);
         mem.push_back(in ? int32_t(cand[q][j].m) : 0);
+        mkey.push_back(kMemoptNoMove);
+        mdm.push_back(0);
+        if (j + 1 < nc)
+          moves.push_back({cand[q][j + 1].t - cand[q][j].t, cand[q][j].m - cand[q][j + 1].m,
+                           i * kMemoptMaxCands + j});
       }
+      ++i;
+    }
+    if (i >= (1 << kMemoptPairBits)) return DIP_E_UNSUPPORTED;
+    // exact ratio order of the rank's moves: dt_a / dm_a < dt_b / dm_b (dm > 0)
+    auto less = [](const Move &x, const Move &y) {
+      return __int128(x.dt) * y.dm < __int128(y.dt) * x.dm;
+    };
+    std::stable_sort(moves.begin(), moves.end(), less);
+    uint32_t dense = 0;
+    for (size_t k = 0; k < moves.size(); ++k) {
+      if (k > 0 && less(moves[k - 1], moves[k])) ++dense;
+      const int32_t pair = moves[k].at / kMemoptMaxCands;
+      mkey[first + size_t(moves[k].at)] = (dense << kMemoptPairBits) | uint32_t(pair);
+      mdm[first + size_t(moves[k].at)] = int32_t(moves[k].dm);
     }
     pair_off[r + 1] = pair_off[r] + i;
     max_pairs = std::max(max_pairs, i);
@@ -1724,18 +1754,20 @@ int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64
     return int(DIP_E_HIP);
   };
   hipError_t e;
-  const size_t npairs = std::max<size_t>(ncand.size(), 1);
+  const size_t cells = std::max<size_t>(tim.size(), 1);       // pairs x candidates
   if ((e = hipMalloc(&h->d_mo_pair_off, size_t(P + 1) * 4)) != hipSuccess) return fail(e);
   if ((e = hipMalloc(&h->d_mo_lid_pair, size_t(std::max(N, 1)) * 4)) != hipSuccess) return fail(e);
-  if ((e = hipMalloc(&h->d_mo_ncand, npairs * 4)) != hipSuccess) return fail(e);
-  if ((e = hipMalloc(&h->d_mo_time, npairs * kMemoptMaxCands * 8)) != hipSuccess) return fail(e);
-  if ((e = hipMalloc(&h->d_mo_mem, npairs * kMemoptMaxCands * 4)) != hipSuccess) return fail(e);
+  if ((e = hipMalloc(&h->d_mo_time, cells * 8)) != hipSuccess) return fail(e);
+  if ((e = hipMalloc(&h->d_mo_mem, cells * 4)) != hipSuccess) return fail(e);
+  if ((e = hipMalloc(&h->d_mo_key, cells * 4)) != hipSuccess) return fail(e);
+  if ((e = hipMalloc(&h->d_mo_dm, cells * 4)) != hipSuccess) return fail(e);
   if ((e = hipMemcpy(h->d_mo_pair_off, pair_off.data(), size_t(P + 1) * 4, hipMemcpyHostToDevice)) ||
       (N > 0 && (e = hipMemcpy(h->d_mo_lid_pair, lid_pair.data(), size_t(N) * 4, hipMemcpyHostToDevice))) ||
-      (!ncand.empty() &&
-       ((e = hipMemcpy(h->d_mo_ncand, ncand.data(), ncand.size() * 4, hipMemcpyHostToDevice)) ||
-        (e = hipMemcpy(h->d_mo_time, tim.data(), tim.size() * 8, hipMemcpyHostToDevice)) ||
-        (e = hipMemcpy(h->d_mo_mem, mem.data(), mem.size() * 4, hipMemcpyHostToDevice)))))
+      (!tim.empty() &&
+       ((e = hipMemcpy(h->d_mo_time, tim.data(), tim.size() * 8, hipMemcpyHostToDevice)) ||
+        (e = hipMemcpy(h->d_mo_mem, mem.data(), mem.size() * 4, hipMemcpyHostToDevice)) ||
+        (e = hipMemcpy(h->d_mo_key, mkey.data(), mkey.size() * 4, hipMemcpyHostToDevice)) ||
+        (e = hipMemcpy(h->d_mo_dm, mdm.data(), mdm.size() * 4, hipMemcpyHostToDevice)))))
     return fail(e);
   h->mo_max_pairs = max_pairs;
   h->mo_ok = true;
@@ -1761,18 +1793,29 @@ int dip_sim_memopt(dip_sim *h, const int16_t *orders, int64_t n_cand, int64_t *o
   a.rank_off = h->d_rank_off;
   a.pair_off = h->d_mo_pair_off;
   a.lid_pair = h->d_mo_lid_pair;
-  a.n_cands = h->d_mo_ncand;
   a.cand_time = h->d_mo_time;
   a.cand_mem = h->d_mo_mem;
+  a.move_key = h->d_mo_key;
+  a.move_dm = h->d_mo_dm;
   a.cap = h->d_cap;
   a.P = h->P;
   a.max_pairs = std::max(h->mo_max_pairs, 1);
-  a.bytes_per_thread = int32_t(align16(int64_t(a.max_pairs) * 9));
-  int tpb = 256;
+  (void)hipGetLastError();
+  if (a.max_pairs <= 512) {
+    // a wave per (schedule, rank), pairs in registers
+    constexpr int kWaves = 4;
+    int ppl = 1;
+    while (64 * ppl < a.max_pairs) ppl *= 2;
+    if ((n_cand + kWaves - 1) / kWaves > INT32_MAX || h->P > 65535) return DIP_E_INVAL;
+    if (memopt_wave_lds(a.max_pairs, kWaves) > 65536) return DIP_E_UNSUPPORTED;
+    DIP_HIP(launch_memopt_wave(ppl, kWaves, static_cast<hipStream_t>(stream), a));
+    return DIP_OK;
+  }
+  a.bytes_per_thread = int32_t(int64_t(a.max_pairs) * 9);
+  int tpb = 64;
   while (tpb > 1 && int64_t(tpb) * a.bytes_per_thread > 65536) tpb /= 2;
   if (int64_t(tpb) * a.bytes_per_thread > 65536) return DIP_E_UNSUPPORTED;
   if (n_cand * h->P / tpb + 1 > INT32_MAX) return DIP_E_INVAL;
-  (void)hipGetLastError();
   DIP_HIP(launch_memopt(tpb, static_cast<hipStream_t>(stream), a));
   return DIP_OK;
 }

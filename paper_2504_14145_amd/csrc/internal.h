@@ -280,6 +280,12 @@ hipError_t launch_rollout_prio(hipStream_t s, const RolloutArgs &a);
 // Per (candidate schedule, rank): one memory candidate per stage pair (see
 // kern_memopt.hip).
 constexpr int kMemoptMaxCands = 8;
+// A move takes a pair from its candidate j to j + 1.  Its key orders the moves
+// of one rank as the greedy compares them: the dense rank of the added time
+// per freed unit (dt / dm, compared exactly) above kMemoptPairBits bits of
+// pair index, so the least key is the least ratio, lowest pair on ties.
+constexpr int kMemoptPairBits = 14;
+constexpr uint32_t kMemoptNoMove = 0xffffffffu;
 struct MemoptArgs {
   const int16_t *orders;
   int64_t n_cand;
@@ -290,14 +296,20 @@ struct MemoptArgs {
   const int32_t *rank_off;    // [P+1] ops
   const int32_t *pair_off;    // [P+1] pairs of each rank (slot order)
   const int32_t *lid_pair;    // [N] pair index on its rank | kind << 31 (by global op)
-  const int32_t *n_cands;     // [pairs]
   const int64_t *cand_time;   // [pairs][kMemoptMaxCands], time ascending
   const int32_t *cand_mem;    // [pairs][kMemoptMaxCands]
+  const uint32_t *move_key;   // [pairs][kMemoptMaxCands] move j -> j + 1; kMemoptNoMove past the last
+  const int32_t *move_dm;     // [pairs][kMemoptMaxCands] memory it frees; 0 past the last
   const int32_t *cap;         // [P]
   int32_t P, max_pairs;
-  int32_t bytes_per_thread;   // LDS per thread (16-aligned)
+  int32_t bytes_per_thread;   // LDS per thread: 9 bytes per pair
 };
 hipError_t launch_memopt(int threads_per_block, hipStream_t s, const MemoptArgs &a);
+// a wave per (schedule, rank), waves_per_block schedules of one rank per block,
+// up to 64 * ppl pairs per rank (ppl 1, 2, 4, 8); LDS per block:
+// (68 + 4 * waves_per_block) bytes per pair
+hipError_t launch_memopt_wave(int ppl, int waves_per_block, hipStream_t s, const MemoptArgs &a);
+size_t memopt_wave_lds(int32_t max_pairs, int waves_per_block);
 
 // ---------------------------------------------------------------- argmin
 hipError_t launch_argmin(int blocks, hipStream_t s, const int32_t *ms, const uint8_t *flags,

@@ -12,17 +12,42 @@
 // pair can move.  Pair i is live at pair k's forward start when its forward
 // comes no later and its backward no earlier in the rank's order.
 //
-// One thread per (schedule, rank); its forward and backward positions,
-// checkpoint loads and choices sit in LDS.
+// The comparison of moves depends on the candidates only, not on the
+// schedule, so the host ranks every move of a rank once (exact 128-bit cross
+// products) and hands each a 32-bit key: the least key is the greedy's
+// choice.  Two kernels:
+//   memopt_wave_kernel  a wave per (schedule, rank), lane j owning pairs
+//                       j, j + 64, ... in registers; the most loaded
+//                       checkpoint and the best move are one DPP wave
+//                       reduction each; a block holds schedules of one rank
+//                       and shares that rank's move tables in LDS.
+//   memopt_kernel       a thread per (schedule, rank), for ranks of more
+//                       than 512 pairs; its state sits in LDS,
+//                       element-major across the block.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
 
+#include "dev_util.h"
 #include "internal.h"
 
 namespace dipsim {
 
 namespace {
+
+__device__ __forceinline__ void lds_sync_wave() {
+  lds_wait();
+  __builtin_amdgcn_wave_barrier();
+}
+
+__device__ __forceinline__ void write_out(const MemoptArgs &a, int64_t o, int64_t t, int32_t pk,
+                                          uint8_t st) {
+  a.out_time[o] = t;
+  a.out_peak[o] = pk;
+  a.out_status[o] = st;
+}
+
+// ---------------------------------------------------------------- thread per problem
 
 __global__ __launch_bounds__(256) void memopt_kernel(MemoptArgs a) {
   extern __shared__ __align__(16) unsigned char sh[];
@@ -32,15 +57,22 @@ __global__ __launch_bounds__(256) void memopt_kernel(MemoptArgs a) {
   const int r = int(id % a.P);
   const int32_t np = a.pair_off[r + 1] - a.pair_off[r];
   const int32_t pbase = a.pair_off[r];
-  unsigned char *mine = sh + int64_t(threadIdx.x) * a.bytes_per_thread;
-  int32_t *load = reinterpret_cast<int32_t *>(mine);
-  uint16_t *pf = reinterpret_cast<uint16_t *>(mine + 4 * a.max_pairs);
-  uint16_t *pb = pf + a.max_pairs;
-  uint8_t *cur = reinterpret_cast<uint8_t *>(pb + a.max_pairs);
+  // element-major arrays, [element][thread], so that the lanes of a wave
+  // touch consecutive words
+  const int T = blockDim.x, t = threadIdx.x;
+  const int64_t m = a.max_pairs;
+  int32_t *load_ = reinterpret_cast<int32_t *>(sh) + t;
+  uint16_t *pf_ = reinterpret_cast<uint16_t *>(sh + 4 * m * T) + t;
+  uint16_t *pb_ = pf_ + m * T;
+  uint8_t *cur_ = reinterpret_cast<uint8_t *>(sh + 8 * m * T) + t;
+#define load(i) load_[int64_t(i) * T]
+#define pf(i) pf_[int64_t(i) * T]
+#define pb(i) pb_[int64_t(i) * T]
+#define cur(i) cur_[int64_t(i) * T]
   for (int32_t i = 0; i < np; ++i) {
-    pf[i] = 0xffffu;
-    pb[i] = 0xffffu;
-    cur[i] = 0;
+    pf(i) = 0xffffu;
+    pb(i) = 0xffffu;
+    cur(i) = 0;
   }
   // positions of each pair's forward and backward in the rank's order
   const int32_t base = a.rank_off[r], nr = a.rank_off[r + 1] - base;
@@ -53,29 +85,27 @@ __global__ __launch_bounds__(256) void memopt_kernel(MemoptArgs a) {
       break;
     }
     const uint32_t w = uint32_t(a.lid_pair[base + lid]);
-    uint16_t *slot = (w >> 31) ? pb : pf;
-    const uint32_t i = w & 0x7fffffffu;
-    if (slot[i] != 0xffffu) {
+    uint16_t *slot = ((w >> 31) ? pb_ : pf_) + int64_t(w & 0x7fffffffu) * T;
+    if (*slot != 0xffffu) {
       valid = false;
       break;
     }
-    slot[i] = uint16_t(p);
+    *slot = uint16_t(p);
   }
   const int64_t o = c * a.P + r;
   if (!valid) {
-    a.out_time[o] = -1;
-    a.out_peak[o] = -1;
-    a.out_status[o] = 2;
+    write_out(a, o, -1, -1, 2);
     return;
   }
   const int64_t *ct = a.cand_time + int64_t(pbase) * kMemoptMaxCands;
   const int32_t *cm = a.cand_mem + int64_t(pbase) * kMemoptMaxCands;
-  const int32_t *nc = a.n_cands + pbase;
+  const uint32_t *mk = a.move_key + int64_t(pbase) * kMemoptMaxCands;
+  const int32_t *md = a.move_dm + int64_t(pbase) * kMemoptMaxCands;
   for (int32_t k = 0; k < np; ++k) {
     int32_t s = 0;
     for (int32_t i = 0; i < np; ++i)
-      if (pf[i] <= pf[k] && pf[k] <= pb[i]) s += cm[i * kMemoptMaxCands];
-    load[k] = s;
+      if (pf(i) <= pf(k) && pf(k) <= pb(i)) s += cm[i * kMemoptMaxCands];
+    load(k) = s;
   }
   const int32_t cap = a.cap[r];
   bool ok = true;
@@ -83,49 +113,217 @@ __global__ __launch_bounds__(256) void memopt_kernel(MemoptArgs a) {
     for (;;) {
       int32_t kk = 0;
       for (int32_t k = 1; k < np; ++k)
-        if (load[k] > load[kk]) kk = k;
-      if (np == 0 || load[kk] <= cap) break;
-      int32_t best = -1;
-      int64_t bdt = 0, bdm = 1;
-      for (int32_t i = 0; i < np; ++i) {
-        if (!(pf[i] <= pf[kk] && pf[kk] <= pb[i])) continue;
-        const int32_t j = cur[i];
-        if (j + 1 >= nc[i]) continue;
-        const int64_t dt = ct[i * kMemoptMaxCands + j + 1] - ct[i * kMemoptMaxCands + j];
-        const int64_t dm = int64_t(cm[i * kMemoptMaxCands + j]) - cm[i * kMemoptMaxCands + j + 1];
-        if (best < 0 || dt * bdm < bdt * dm) {
-          best = i;
-          bdt = dt;
-          bdm = dm;
-        }
-      }
-      if (best < 0) {
+        if (load(k) > load(kk)) kk = k;
+      if (np == 0 || load(kk) <= cap) break;
+      uint32_t best = kMemoptNoMove;
+      for (int32_t i = 0; i < np; ++i)
+        if (pf(i) <= pf(kk) && pf(kk) <= pb(i)) best = min(best, mk[i * kMemoptMaxCands + cur(i)]);
+      if (best == kMemoptNoMove) {
         ok = false;
         break;
       }
-      cur[best] += 1;
+      const int32_t bi = int32_t(best & ((1u << kMemoptPairBits) - 1));
+      const int32_t dm = md[bi * kMemoptMaxCands + cur(bi)];
+      cur(bi) += 1;
       for (int32_t k = 0; k < np; ++k)
-        if (pf[best] <= pf[k] && pf[k] <= pb[best]) load[k] -= int32_t(bdm);
+        if (pf(bi) <= pf(k) && pf(k) <= pb(bi)) load(k) -= dm;
     }
   }
   int64_t total = 0;
   int32_t peak = 0;
   for (int32_t i = 0; i < np; ++i) {
-    total += ct[i * kMemoptMaxCands + cur[i]];
-    peak = max(peak, load[i]);
+    total += ct[i * kMemoptMaxCands + cur(i)];
+    peak = max(peak, load(i));
   }
-  a.out_time[o] = total;
-  a.out_peak[o] = peak;
-  a.out_status[o] = ok ? 1 : 0;
+  write_out(a, o, total, peak, ok ? 1 : 0);
+}
+#undef load
+#undef pf
+#undef pb
+#undef cur
+
+// ---------------------------------------------------------------- wave per problem
+
+template <int PPL>
+__global__ __launch_bounds__(256) void memopt_wave_kernel(MemoptArgs a) {
+  extern __shared__ __align__(16) unsigned char sh[];
+  const int lane = threadIdx.x & 63;
+  const int wv = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  const int r = blockIdx.y;
+  const int64_t c = int64_t(blockIdx.x) * nw + wv;
+  const int32_t pbase = a.pair_off[r];
+  const int32_t np = a.pair_off[r + 1] - pbase;
+  const int64_t mp = a.max_pairs;
+  // the rank's tables, shared by the block: move keys and freed memory
+  // [pair][candidate], memory of the fastest candidate [pair]
+  uint32_t *tkey = reinterpret_cast<uint32_t *>(sh);
+  int32_t *tdm = reinterpret_cast<int32_t *>(sh + 32 * mp);
+  int32_t *tm0 = reinterpret_cast<int32_t *>(sh + 64 * mp);
+  // this wave's positions of each pair's forward and backward
+  uint16_t *pfa = reinterpret_cast<uint16_t *>(sh + 68 * mp) + int64_t(wv) * 2 * mp;
+  uint16_t *pba = pfa + mp;
+  {
+    const uint32_t *gk = a.move_key + int64_t(pbase) * kMemoptMaxCands;
+    const int32_t *gd = a.move_dm + int64_t(pbase) * kMemoptMaxCands;
+    const int32_t *gm = a.cand_mem + int64_t(pbase) * kMemoptMaxCands;
+    for (int32_t x = threadIdx.x; x < np * kMemoptMaxCands; x += blockDim.x) {
+      tkey[x] = gk[x];
+      tdm[x] = gd[x];
+    }
+    for (int32_t i = threadIdx.x; i < np; i += blockDim.x) tm0[i] = gm[i * kMemoptMaxCands];
+  }
+  __syncthreads();
+  if (c >= a.n_cand) return;                        // whole waves, after the last barrier
+  for (int32_t i = lane; i < np; i += 64) {
+    pfa[i] = 0xffffu;
+    pba[i] = 0xffffu;
+  }
+  lds_sync_wave();
+  const int32_t base = a.rank_off[r], nr = a.rank_off[r + 1] - base;
+  const int16_t *row = a.orders + c * a.stride + base;
+  bool bad = false;
+  for (int32_t p = lane; p < nr; p += 64) {
+    const int32_t lid = row[p];
+    if (lid < 0 || lid >= nr) {
+      bad = true;
+      continue;
+    }
+    const uint32_t w = uint32_t(a.lid_pair[base + lid]);
+    ((w >> 31) ? pba : pfa)[w & 0x7fffffffu] = uint16_t(p);
+  }
+  lds_sync_wave();
+  // every rank op is one end of one pair, so with all nr ids in range a
+  // repeated id leaves some end unfilled
+  for (int32_t i = lane; i < np; i += 64)
+    if (pfa[i] == 0xffffu || pba[i] == 0xffffu) bad = true;
+  const int64_t o = c * a.P + r;
+  if (__any(bad)) {
+    if (lane == 0) write_out(a, o, -1, -1, 2);
+    return;
+  }
+  // own pairs: positions, current candidate, its next move (key, freed
+  // memory), load of the own checkpoint under the fastest candidates
+  uint32_t pf[PPL], pb[PPL], key[PPL];
+  int32_t cur[PPL], dm[PPL], load[PPL];
+#pragma unroll
+  for (int q = 0; q < PPL; ++q) {
+    const int32_t i = lane + 64 * q;
+    const bool own = i < np;
+    pf[q] = own ? pfa[i] : 0xffffu;
+    pb[q] = own ? pba[i] : 0u;
+    cur[q] = 0;
+    key[q] = own ? tkey[i * kMemoptMaxCands] : kMemoptNoMove;
+    dm[q] = own ? tdm[i * kMemoptMaxCands] : 0;
+    int32_t s = 0;
+    if (own)
+      for (int32_t j = 0; j < np; ++j)
+        if (pfa[j] <= pf[q] && pf[q] <= pba[j]) s += tm0[j];
+    load[q] = s;
+  }
+  const int32_t cap = a.cap[r];
+  bool ok = true;
+  if (cap >= 0) {
+    for (;;) {
+      // most loaded checkpoint (order-preserving unsigned image of the load)
+      uint32_t mx = 0;
+#pragma unroll
+      for (int q = 0; q < PPL; ++q)
+        if (lane + 64 * q < np) mx = max(mx, uint32_t(load[q]) ^ 0x80000000u);
+      mx = wave_max_u32(mx);
+      const int32_t top = int32_t(mx ^ 0x80000000u);
+      if (np == 0 || top <= cap) break;
+      // its forward position: the lowest pair index holding that load
+      uint32_t pfk = 0;
+      bool found = false;
+#pragma unroll
+      for (int q = 0; q < PPL; ++q) {
+        const uint64_t b = __ballot(lane + 64 * q < np && load[q] == top);
+        if (!found && b) {
+          pfk = uint32_t(__builtin_amdgcn_readlane(int(pf[q]), __builtin_ctzll(b)));
+          found = true;
+        }
+      }
+      // best move among the pairs live there
+      uint32_t m = kMemoptNoMove;
+#pragma unroll
+      for (int q = 0; q < PPL; ++q)
+        if (pf[q] <= pfk && pfk <= pb[q]) m = min(m, key[q]);
+      m = wave_min_u32(m);
+      if (m == kMemoptNoMove) {
+        ok = false;
+        break;
+      }
+      const int32_t bi = int32_t(m & ((1u << kMemoptPairBits) - 1));
+      const int qb = bi >> 6, ob = bi & 63;
+      uint32_t spf = 0, spb = 0;
+      int32_t sdm = 0;
+#pragma unroll
+      for (int q = 0; q < PPL; ++q)
+        if (q == qb) {
+          spf = pf[q];
+          spb = pb[q];
+          sdm = dm[q];
+        }
+      spf = uint32_t(__builtin_amdgcn_readlane(int(spf), ob));
+      spb = uint32_t(__builtin_amdgcn_readlane(int(spb), ob));
+      sdm = __builtin_amdgcn_readlane(sdm, ob);
+      // every checkpoint the moved pair is live at drops; its owner steps on
+#pragma unroll
+      for (int q = 0; q < PPL; ++q) {
+        if (spf <= pf[q] && pf[q] <= spb) load[q] -= sdm;
+        if (q == qb && lane == ob) {
+          const int32_t x = bi * kMemoptMaxCands + ++cur[q];
+          key[q] = tkey[x];
+          dm[q] = tdm[x];
+        }
+      }
+    }
+  }
+  const int64_t *ct = a.cand_time + int64_t(pbase) * kMemoptMaxCands;
+  int64_t total = 0;
+  uint32_t pk = 0x80000000u;                        // image of load 0
+#pragma unroll
+  for (int q = 0; q < PPL; ++q) {
+    const int32_t i = lane + 64 * q;
+    if (i < np) {
+      total += ct[i * kMemoptMaxCands + cur[q]];
+      pk = max(pk, uint32_t(load[q]) ^ 0x80000000u);
+    }
+  }
+  pk = wave_max_u32(pk);
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1)
+    total += (int64_t(__shfl_xor(int(total >> 32), s)) << 32) |
+             uint32_t(__shfl_xor(int(uint32_t(total)), s));
+  if (lane == 0) write_out(a, o, total, int32_t(pk ^ 0x80000000u), ok ? 1 : 0);
 }
 
 }  // namespace
 
+size_t memopt_wave_lds(int32_t max_pairs, int waves_per_block) {
+  return size_t(max_pairs) * (68 + 4 * size_t(waves_per_block));
+}
+
+hipError_t launch_memopt_wave(int ppl, int waves_per_block, hipStream_t s, const MemoptArgs &a) {
+  const int64_t bx = (a.n_cand + waves_per_block - 1) / waves_per_block;
+  const size_t lds = memopt_wave_lds(a.max_pairs, waves_per_block);
+  const dim3 grid{unsigned(bx), unsigned(a.P)}, block{unsigned(64 * waves_per_block)};
+  switch (ppl) {
+    case 1: hipLaunchKernelGGL(memopt_wave_kernel<1>, grid, block, lds, s, a); break;
+    case 2: hipLaunchKernelGGL(memopt_wave_kernel<2>, grid, block, lds, s, a); break;
+    case 4: hipLaunchKernelGGL(memopt_wave_kernel<4>, grid, block, lds, s, a); break;
+    case 8: hipLaunchKernelGGL(memopt_wave_kernel<8>, grid, block, lds, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_memopt(int threads_per_block, hipStream_t s, const MemoptArgs &a) {
   const int64_t n = a.n_cand * a.P;
   const int64_t blocks = (n + threads_per_block - 1) / threads_per_block;
-  hipLaunchKernelGGL(memopt_kernel, dim3(unsigned(blocks)), dim3(threads_per_block),
-                     size_t(threads_per_block) * a.bytes_per_thread, s, a);
+  const size_t lds = size_t(threads_per_block) * size_t(a.bytes_per_thread);
+  hipLaunchKernelGGL(memopt_kernel, dim3(unsigned(blocks)), dim3(unsigned(threads_per_block)), lds,
+                     s, a);
   return hipGetLastError();
 }
 

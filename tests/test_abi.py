@@ -17,7 +17,7 @@ HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "di
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(dip_sim_\w+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(dip_\w+)\s*\(", text)))
 
 
 def test_library_exports_every_declared_symbol():

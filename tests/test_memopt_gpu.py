@@ -73,3 +73,23 @@ def test_memopt_flags_invalid_orders():
     assert st[1, 0] == 2 and t[1, 0] == -1 and pk[1, 0] == -1
     assert st[2, 5] == 2
     assert (st[0] != 2).all() and (st[3] != 2).all()
+
+
+@pytest.mark.parametrize("frac", [0.5, 0.85])
+def test_memopt_ranks_with_many_pairs(frac):
+    """Ranks of more than 512 stage pairs take the one-thread-per-rank kernel;
+    a rank of fewer takes the wave kernel in the same problem family."""
+    need_gpu()
+    for M in (520, 200):
+        inst = W.pipeline_instance(2, M, np.arange(2 * M).reshape(2, M) % 9 + 2, comm=3, act=2)
+        prob = W.compile_instance(inst)
+        g, G, cls = W.priority_groups(prob)
+        rows, res = O.greedy(prob, g, G, W.rollout_priorities(cls, 3, seed=4), stride=prob.stride)
+        tab = strategy_table(prob)
+        prob.mem_cap[:] = (np.median(res.peak, axis=0) * frac).astype(prob.mem_cap.dtype)
+        print(f"pipeline M {M}: caps {prob.mem_cap.tolist()}", flush=True)
+        got_t, got_p, got_s = run(prob, tab, rows, 6)
+        want = MO.optimise(prob, tab, MO.pair_candidates(tab, 6), rows)
+        np.testing.assert_array_equal(got_s, [[1 if x[1] else 0 for x in per] for per in want])
+        np.testing.assert_array_equal(got_t, [[x[0] for x in per] for per in want])
+        np.testing.assert_array_equal(got_p, [[x[2] for x in per] for per in want])
