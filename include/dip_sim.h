@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define DIP_SIM_ABI_VERSION 4
+#define DIP_SIM_ABI_VERSION 5
 
 enum {
   DIP_OK = 0,
@@ -129,6 +129,8 @@ typedef struct {
   int32_t greedy_inbox;      /* dip_sim_greedy: stages a rank's inbox holds (0:
                                 not configured); grows when many overflow     */
   int32_t greedy_lds_bytes;  /* dip_sim_greedy: LDS per block of its launch    */
+  int64_t greedy_retry_ring_bytes; /* dip_sim_greedy: device memory holding the
+                                second launch's inboxes where LDS cannot, else 0 */
 } dip_sim_info;
 
 /* Host-only checks, no device access: the same checks create / evaluate run
@@ -214,11 +216,23 @@ int dip_sim_argmin(dip_sim *h, const int32_t *makespan, const uint8_t *flags,
  * read during the call) puts every op in one of n_groups priority groups --
  * Sec. 5.1's pipeline segments, which the candidates of dip_sim_greedy
  * prioritise.  A group holds ops of one kind, at most one per rank; the data
- * edges must be acyclic.  1 <= n_groups <= 65535, and at most 512 groups of
+ * edges must be acyclic.  1 <= n_groups <= 65535, and at most 2048 groups of
  * either kind.  DIP_E_TOPO if a rule is broken, DIP_E_UNSUPPORTED if the
- * groups or the per-candidate tables do not fit the kernel.  Replaces any
+ * groups or the per-candidate tables do not fit the kernel.  Where a rank's
+ * whole inboxes do not fit in LDS, the handle allocates device memory for
+ * them (up to 1 GiB; dip_sim_info.greedy_retry_ring_bytes).  Replaces any
  * earlier grouping; the next dip_sim_greedy call must then pass costs. */
 int dip_sim_configure_greedy(dip_sim *h, int32_t n_groups, const int32_t *op_group);
+
+/* Stages each rank's forward and backward inbox holds in dip_sim_greedy's
+ * first launch (a candidate that overflows one is simulated again by the
+ * second launch, whose inboxes hold a whole rank): k a power of two from 1 to
+ * 256 fixes it; k = 0 restores the default, 8 to start with and doubled by
+ * a later call when more than 1/64 of a call's candidates overflowed.
+ * Results do not depend on k.  DIP_E_STATE before dip_sim_configure_greedy,
+ * DIP_E_INVAL for another k, DIP_E_UNSUPPORTED if the inboxes do not fit in
+ * LDS.  Reset by dip_sim_configure_greedy. */
+int dip_sim_set_greedy_inbox(dip_sim *h, int32_t k);
 
 /* Build and score one candidate per priority vector.
  *   prio        device, int32 [n_cand][n_groups]: larger is scheduled first;

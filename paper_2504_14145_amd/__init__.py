@@ -26,7 +26,7 @@ NO_KEY = (1 << 64) - 1
 EXPORTS = ("dip_sim_abi_version", "dip_sim_check_topology", "dip_sim_check_costs",
            "dip_sim_create", "dip_sim_configure", "dip_sim_configure_pool",
            "dip_sim_configure_check", "dip_sim_get_info", "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
-           "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_greedy",
+           "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_set_greedy_inbox", "dip_sim_greedy",
            "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_cost_tables",
            "dip_sim_configure_memopt", "dip_sim_memopt", "dip_sim_destroy", "dip_sim_strerror")
 
@@ -65,7 +65,7 @@ class Info(ctypes.Structure):
                 ("lds_bytes", ctypes.c_int32), ("max_blocks", ctypes.c_int32),
                 ("scratch_bytes", ctypes.c_int64), ("pool_slots", ctypes.c_int32),
                 ("check_kernel", ctypes.c_int32), ("greedy_inbox", ctypes.c_int32),
-                ("greedy_lds_bytes", ctypes.c_int32)]
+                ("greedy_lds_bytes", ctypes.c_int32), ("greedy_retry_ring_bytes", ctypes.c_int64)]
 
     def as_dict(self):
         return {k: getattr(self, k) for k, _ in self._fields_}
@@ -95,6 +95,7 @@ def load():
         lib.dip_sim_evaluate.argtypes = [vp, ctypes.POINTER(Costs), vp, i64, vp, vp, vp, vp, vp]
         lib.dip_sim_argmin.argtypes = [vp, vp, vp, i64, i64, vp, vp]
         lib.dip_sim_configure_greedy.argtypes = [vp, i32, vp]
+        lib.dip_sim_set_greedy_inbox.argtypes = [vp, i32]
         lib.dip_sim_greedy.argtypes = [vp, ctypes.POINTER(Costs), vp, i64, vp, vp, vp, vp, vp, vp]
         lib.dip_sim_configure_rollouts.argtypes = [vp, i32, vp]
         lib.dip_cost_tables.argtypes = [ctypes.POINTER(OpTable), i64, vp, vp, vp]
@@ -110,7 +111,7 @@ def load():
                      "dip_sim_configure", "dip_sim_configure_pool", "dip_sim_configure_check",
                      "dip_sim_get_info",
                      "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
-                     "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_greedy",
+                     "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_set_greedy_inbox", "dip_sim_greedy",
                      "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_cost_tables",
                      "dip_sim_configure_memopt", "dip_sim_memopt"):
             getattr(lib, name).restype = ctypes.c_int
@@ -240,6 +241,11 @@ def configure_greedy(h, n_groups: int, op_group) -> int:
     """``op_group``: host int32 [N]; returns the ABI code."""
     g = np.ascontiguousarray(op_group, np.int32)
     return load().dip_sim_configure_greedy(h, int(n_groups), g.ctypes.data)
+
+
+def set_greedy_inbox(h, k: int) -> int:
+    """Fix the first launch's inbox size (power of two, 1..256); 0: adaptive."""
+    return load().dip_sim_set_greedy_inbox(h, int(k))
 
 
 def greedy(h, costs, prio, n_cand, out_orders, out_makespan, out_bubble, out_peakmem,
@@ -386,6 +392,9 @@ class Sim:
         if rc == OK:
             self._greedy_costs = False
         return rc
+
+    def set_greedy_inbox(self, k) -> int:
+        return set_greedy_inbox(self.h, k)
 
     def greedy(self, prio, out=None, orders=True, stream=None):
         """Interleave every priority row; returns (orders or None, outputs)."""

@@ -160,17 +160,22 @@ struct dip_sim {
   // and read by a later call, which doubles the inboxes when more than 1/64
   // of its candidates needed the second launch
   int gr_K = 16;
+  bool gr_K_fixed = false;             // dip_sim_set_greedy_inbox fixed it
   uint32_t *h_gr_seen = nullptr;       // pinned
   hipEvent_t gr_seen_ev = nullptr;
   bool gr_seen_pending = false;
   int64_t gr_seen_n = 0;
   struct GrLaunch {
     int pwl = 3, wpb = 1, K = 8, blocks_per_cu = 1;
+    bool gring = false;                // inboxes in device memory (d_gr_ring)
+    int max_blocks = 0;                // gring: blocks the ring memory has slots for
     int32_t cand_bytes = 0, off_pend = 0, off_npend = 0, off_join = 0, off_gpos = 0,
             off_ord = 0, off_grk = 0;
     int64_t lds = 0;
   } gr_main, gr_retry;
   int32_t gr_meta_bytes = 0;
+  uint64_t *d_gr_ring = nullptr;       // retry launch's inboxes when LDS cannot hold them
+  int64_t gr_ring_bytes = 0;
   // MCTS rollouts (dip_sim_configure_rollouts / dip_sim_rollouts)
   bool rl_ok = false;
   int32_t rl_n = 0;                    // classes
@@ -776,16 +781,20 @@ int upload_costs(dip_sim *h, const dip_costs *c, hipStream_t stream) {
 // their counts and the join accumulators overlay the priorities, which only
 // the set-up reads; then positions, position -> group and position -> global
 // rank (16-bit each).
-bool greedy_layout(const dip_sim *h, int K, int pwl, dip_sim::GrLaunch *L) {
+bool greedy_layout(const dip_sim *h, int K, int pwl, dip_sim::GrLaunch *L, bool gring = false) {
   const int64_t G = h->gr_G, P = h->P, J = h->gr_J;
   L->pwl = pwl;
   L->K = K;
   L->wpb = 1;
-  // two rings per rank; two head/count words per lane (padding lanes' stay 0)
+  L->gring = gring;
+  L->max_blocks = 0;
+  // two rings per rank (none in LDS with gring); two head/count words per
+  // lane (padding lanes' stay 0)
   const int64_t lanes = int64_t(1) << pwl;
+  const int64_t rings = gring ? 0 : P * (2 * K + 1) * 8;
   L->off_pend = 0;
-  L->off_npend = int32_t(P * (2 * K + 1) * 8);
-  L->off_join = int32_t(P * (2 * K + 1) * 8 + 8 * lanes);
+  L->off_npend = int32_t(rings);
+  L->off_join = int32_t(rings + 8 * lanes);
   const int64_t head = align16(std::max<int64_t>(4 * G, L->off_join + 8 * J));
   L->off_gpos = int32_t(head);
   L->off_ord = int32_t(head + align16(2 * G));
@@ -794,9 +803,11 @@ bool greedy_layout(const dip_sim *h, int K, int pwl, dip_sim::GrLaunch *L) {
   L->lds = h->gr_meta_bytes + int64_t(kWave >> pwl) * L->cand_bytes;
   if (L->lds > h->lds_block_max) return false;
   int bpc = 0;
-  const void *k = greedy_kernel_ptr(pwl, h->gr_nw);
-  if (!k || hipOccupancyMaxActiveBlocksPerMultiprocessor(&bpc, k, kWave * L->wpb,
-                                                         size_t(L->lds)) != hipSuccess) {
+  const void *k = greedy_kernel_ptr(pwl, h->gr_nw, gring);
+  if (!k || (L->lds > 65536 && hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                                   int(L->lds)) != hipSuccess) ||
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&bpc, k, kWave * L->wpb,
+                                                   size_t(L->lds)) != hipSuccess) {
     (void)hipGetLastError();
     return false;
   }
@@ -843,6 +854,9 @@ void release_greedy(dip_sim *h) {
   if (h->d_gr_retry_count) (void)hipFree(h->d_gr_retry_count);
   if (h->h_gr_seen) (void)hipHostFree(h->h_gr_seen);
   if (h->gr_seen_ev) (void)hipEventDestroy(h->gr_seen_ev);
+  if (h->d_gr_ring) (void)hipFree(h->d_gr_ring);
+  h->d_gr_ring = nullptr;
+  h->gr_ring_bytes = 0;
   h->h_gr_seen = nullptr;
   h->gr_seen_ev = nullptr;
   h->gr_seen_pending = false;
@@ -1110,6 +1124,7 @@ int dip_sim_get_info(const dip_sim *h, dip_sim_info *info) {
   info->check_kernel = h->variant == 8 ? (use_tile_check(h) ? 2 : 1) : 0;
   info->greedy_inbox = h->gr_ok ? h->gr_K : 0;
   info->greedy_lds_bytes = h->gr_ok ? int32_t(h->gr_main.lds) : 0;
+  info->greedy_retry_ring_bytes = h->gr_ok ? h->gr_ring_bytes : 0;
   return DIP_OK;
 }
 
@@ -1365,7 +1380,7 @@ int dip_sim_configure_greedy(dip_sim *h, int32_t n_groups, const int32_t *op_gro
   const int32_t wmax = (std::max(GF, n_groups - GF) + 63) / 64;
   int nw = 1;
   while (nw < wmax) nw *= 2;
-  if (nw > 8) return DIP_E_UNSUPPORTED;
+  if (nw > 32) return DIP_E_UNSUPPORTED;
 
   (void)hipDeviceSynchronize();   // no call may still read the old tables
   release_rollouts(h);             // the classes belong to the old grouping
@@ -1402,13 +1417,30 @@ int dip_sim_configure_greedy(dip_sim *h, int32_t n_groups, const int32_t *op_gro
   // to a whole rank
   const int pwl = std::max(2, h->pwl);
   h->gr_K = 8;
+  h->gr_K_fixed = false;
   if (!greedy_layout(h, h->gr_K, pwl, &h->gr_main)) return DIP_E_UNSUPPORTED;
-  // inboxes are rings of a power of two entries
+  // a stage joins its rank's inbox of its kind once, so a ring of a power
+  // of two entries no fewer than the rank's stages of that kind never fills
+  int32_t most = 1;
+  {
+    std::vector<int32_t> per(2 * int64_t(P), 0);
+    for (int32_t g = 0; g < N; ++g) most = std::max(most, ++per[2 * h->rank_of[g] + h->kind[g]]);
+  }
   int kr = 1;
-  while (kr < h->gr_max_nr) kr *= 2;
+  while (kr < most) kr *= 2;
+  if (kr > 0x8000) return DIP_E_UNSUPPORTED;      // 16-bit ring heads and counts
   int pr = pwl;
   while (pr <= 6 && !greedy_layout(h, kr, pr, &h->gr_retry)) ++pr;
-  if (pr > 6) return DIP_E_UNSUPPORTED;
+  int64_t ring_bytes = 0;
+  if (pr > 6) {
+    // rings in device memory, one region per resident candidate slot; at
+    // most 1 GiB of them (fewer resident blocks if need be)
+    if (!greedy_layout(h, kr, pwl, &h->gr_retry, true)) return DIP_E_UNSUPPORTED;
+    const int64_t per_block = int64_t(h->gr_retry.wpb) * (kWave >> pwl) * P * (2 * int64_t(kr) + 1) * 8;
+    const int64_t want = int64_t(h->n_cu) * h->gr_retry.blocks_per_cu;
+    h->gr_retry.max_blocks = int(std::max<int64_t>(1, std::min<int64_t>(want, (int64_t(1) << 30) / per_block)));
+    ring_bytes = int64_t(h->gr_retry.max_blocks) * per_block;
+  }
 
   auto fail = [&](hipError_t e) {
     g_last_hip = e;
@@ -1430,6 +1462,10 @@ int dip_sim_configure_greedy(dip_sim *h, int32_t n_groups, const int32_t *op_gro
     return fail(e);
   if ((e = hipMemcpy(h->d_gr_src, src.data(), src.size() * 4, hipMemcpyHostToDevice)) != hipSuccess)
     return fail(e);
+  if (ring_bytes > 0) {
+    if ((e = hipMalloc(&h->d_gr_ring, size_t(ring_bytes))) != hipSuccess) return fail(e);
+    h->gr_ring_bytes = ring_bytes;
+  }
   h->gr_ok = true;
   h->gr_costs_ok = false;
   return DIP_OK;
@@ -1464,7 +1500,7 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
   if (h->gr_seen_pending && hipEventQuery(h->gr_seen_ev) == hipSuccess) {
     h->gr_seen_pending = false;
     dip_sim::GrLaunch bigger;
-    if (h->gr_K < 256 && int64_t(*h->h_gr_seen) * 64 > h->gr_seen_n &&
+    if (!h->gr_K_fixed && h->gr_K < 256 && int64_t(*h->h_gr_seen) * 64 > h->gr_seen_n &&
         greedy_layout(h, 2 * h->gr_K, h->gr_main.pwl, &bigger)) {
       h->gr_K *= 2;
       h->gr_main = bigger;
@@ -1521,7 +1557,7 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
   const int64_t blocks = (n_cand + per_block - 1) / per_block;
   if (blocks > INT32_MAX) return DIP_E_INVAL;
   DIP_HIP(mark(0));
-  DIP_HIP(launch_greedy(h->gr_main.pwl, h->gr_nw, int(blocks), h->gr_main.wpb,
+  DIP_HIP(launch_greedy(h->gr_main.pwl, h->gr_nw, false, int(blocks), h->gr_main.wpb,
                         size_t(h->gr_main.lds), stream, a));
   DIP_HIP(mark(1));
   // candidates whose inboxes overflowed, with inboxes as large as a rank
@@ -1530,11 +1566,15 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
   a.list_count = h->d_gr_retry_count;
   a.retry = nullptr;
   a.retry_count = nullptr;
-  const int rblocks = int(std::min<int64_t>(int64_t(h->n_cu) * h->gr_retry.blocks_per_cu, blocks));
-  DIP_HIP(launch_greedy(h->gr_retry.pwl, h->gr_nw, rblocks, h->gr_retry.wpb,
+  int64_t rb = std::min<int64_t>(int64_t(h->n_cu) * h->gr_retry.blocks_per_cu, blocks);
+  if (h->gr_retry.gring) {
+    rb = std::min<int64_t>(rb, h->gr_retry.max_blocks);   // one ring region per resident slot
+    a.gring = h->d_gr_ring;
+  }
+  DIP_HIP(launch_greedy(h->gr_retry.pwl, h->gr_nw, h->gr_retry.gring, int(rb), h->gr_retry.wpb,
                         size_t(h->gr_retry.lds), stream, a));
   DIP_HIP(mark(2));
-  if (h->gr_K < 256 && !h->gr_seen_pending) {
+  if (!h->gr_K_fixed && h->gr_K < 256 && !h->gr_seen_pending) {
     if (!h->h_gr_seen) {
       DIP_HIP(hipHostMalloc(reinterpret_cast<void **>(&h->h_gr_seen), 16, hipHostMallocDefault));
       DIP_HIP(hipEventCreateWithFlags(&h->gr_seen_ev, hipEventDisableTiming));
@@ -1544,6 +1584,18 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
     h->gr_seen_pending = true;
     h->gr_seen_n = n_cand;
   }
+  return DIP_OK;
+}
+
+int dip_sim_set_greedy_inbox(dip_sim *h, int32_t k) {
+  if (!h || k < 0 || k > 256 || (k & (k - 1)) != 0) return DIP_E_INVAL;
+  if (!h->gr_ok) return DIP_E_STATE;
+  const int kk = k ? k : 8;
+  dip_sim::GrLaunch L;
+  if (!greedy_layout(h, kk, h->gr_main.pwl, &L)) return DIP_E_UNSUPPORTED;
+  h->gr_K = kk;
+  h->gr_main = L;
+  h->gr_K_fixed = k != 0;
   return DIP_OK;
 }
 

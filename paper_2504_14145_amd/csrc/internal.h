@@ -255,11 +255,15 @@ struct GreedyArgs {
   const uint32_t *list_count;
   int64_t *retry;           // candidates whose inbox overflowed
   uint32_t *retry_count;
+  uint64_t *gring;          // device-memory inboxes: P * (2K + 1) entries per resident
+                            // candidate slot, slot = (block * wpb + wave) * (64 >> pwl) + group
 };
 // successor word: internal group | kind << 16 | rank << 17
 constexpr uint32_t kGreedyNoStage = 0xffffu;
-const void *greedy_kernel_ptr(int pwl, int nw);
-hipError_t launch_greedy(int pwl, int nw, int blocks, int wpb, size_t lds, hipStream_t s,
+// nw: bitmap words per kind (1, 2, 4, 8, 16, 32); gring: inboxes in device
+// memory (GreedyArgs::gring) rather than LDS
+const void *greedy_kernel_ptr(int pwl, int nw, bool gring);
+hipError_t launch_greedy(int pwl, int nw, bool gring, int blocks, int wpb, size_t lds, hipStream_t s,
                          const GreedyArgs &a);
 
 // ---------------------------------------------------------------- rollouts

@@ -32,7 +32,9 @@
 // the entries that came due into E at the start of the next round.  A group min over the
 // lanes' t_min picks the committing rank.  An inbox that fills up sends the
 // candidate to a list that a second launch, with inboxes as large as a rank's
-// stage count, simulates again.
+// stage count of that kind, simulates again; where such inboxes do not fit in
+// LDS, that launch keeps them in device memory (GRING), one region per
+// resident candidate slot.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -138,7 +140,7 @@ struct Choice {
 
 }  // namespace
 
-template <int PWL, int NW>
+template <int PWL, int NW, bool GRING>
 __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
   constexpr int PW = 1 << PWL;
   constexpr int GW = kWave >> PWL;
@@ -158,9 +160,13 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
   // ... then the inboxes: per rank a forward ring and a backward ring of K
   // entries each (and one spare entry); per lane (padding lanes included) a
   // word {head, count << 16} per kind
-  uint64_t *ring0 = reinterpret_cast<uint64_t *>(cb + a.off_pend);
   // rank stride 2K + 1 entries, so that the lanes' rings start in different banks
   const int64_t rstride = 2 * int64_t(K) + 1;
+  uint64_t *ring0;
+  if constexpr (GRING)
+    ring0 = a.gring + ((int64_t(blockIdx.x) * a.wpb + wave) * GW + grp) * P * rstride;
+  else
+    ring0 = reinterpret_cast<uint64_t *>(cb + a.off_pend);
   uint64_t *ringF = ring0 + int64_t(r < P ? r : 0) * rstride;
   uint64_t *ringB = ringF + K;
   uint32_t *hcw = reinterpret_cast<uint32_t *>(cb + a.off_npend);
@@ -401,7 +407,10 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
           hcw[2 * tr + tk] = h + (1u << 16);
         }
       }
-      lds_sync();
+      if constexpr (GRING)
+        wave_sync();      // the inboxes' device-memory writes too
+      else
+        lds_sync();
     }
 
     // ---- outputs
@@ -439,53 +448,43 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
 
 namespace {
 
-template <int PWL>
+template <int PWL, bool GRING>
 const void *ptr_nw(int nw) {
   switch (nw) {
-    case 1: return reinterpret_cast<const void *>(&greedy_kernel<PWL, 1>);
-    case 2: return reinterpret_cast<const void *>(&greedy_kernel<PWL, 2>);
-    case 4: return reinterpret_cast<const void *>(&greedy_kernel<PWL, 4>);
-    case 8: return reinterpret_cast<const void *>(&greedy_kernel<PWL, 8>);
+    case 1: return reinterpret_cast<const void *>(&greedy_kernel<PWL, 1, GRING>);
+    case 2: return reinterpret_cast<const void *>(&greedy_kernel<PWL, 2, GRING>);
+    case 4: return reinterpret_cast<const void *>(&greedy_kernel<PWL, 4, GRING>);
+    case 8: return reinterpret_cast<const void *>(&greedy_kernel<PWL, 8, GRING>);
+    case 16: return reinterpret_cast<const void *>(&greedy_kernel<PWL, 16, GRING>);
+    case 32: return reinterpret_cast<const void *>(&greedy_kernel<PWL, 32, GRING>);
     default: return nullptr;
   }
 }
 
 template <int PWL>
-hipError_t launch_nw(int nw, int blocks, int wpb, size_t lds, hipStream_t s, const GreedyArgs &a) {
-  const dim3 grid(blocks), block(wpb * kWave);
-  switch (nw) {
-    case 1: hipLaunchKernelGGL((greedy_kernel<PWL, 1>), grid, block, lds, s, a); break;
-    case 2: hipLaunchKernelGGL((greedy_kernel<PWL, 2>), grid, block, lds, s, a); break;
-    case 4: hipLaunchKernelGGL((greedy_kernel<PWL, 4>), grid, block, lds, s, a); break;
-    case 8: hipLaunchKernelGGL((greedy_kernel<PWL, 8>), grid, block, lds, s, a); break;
-    default: return hipErrorInvalidValue;
-  }
-  return hipGetLastError();
+const void *ptr_pwl(int nw, bool gring) {
+  return gring ? ptr_nw<PWL, true>(nw) : ptr_nw<PWL, false>(nw);
 }
 
 }  // namespace
 
-const void *greedy_kernel_ptr(int pwl, int nw) {
+const void *greedy_kernel_ptr(int pwl, int nw, bool gring) {
   switch (pwl) {
-    case 2: return ptr_nw<2>(nw);
-    case 3: return ptr_nw<3>(nw);
-    case 4: return ptr_nw<4>(nw);
-    case 5: return ptr_nw<5>(nw);
-    case 6: return ptr_nw<6>(nw);
+    case 2: return ptr_pwl<2>(nw, gring);
+    case 3: return ptr_pwl<3>(nw, gring);
+    case 4: return ptr_pwl<4>(nw, gring);
+    case 5: return ptr_pwl<5>(nw, gring);
+    case 6: return ptr_pwl<6>(nw, gring);
     default: return nullptr;
   }
 }
 
-hipError_t launch_greedy(int pwl, int nw, int blocks, int wpb, size_t lds, hipStream_t s,
-                         const GreedyArgs &a) {
-  switch (pwl) {
-    case 2: return launch_nw<2>(nw, blocks, wpb, lds, s, a);
-    case 3: return launch_nw<3>(nw, blocks, wpb, lds, s, a);
-    case 4: return launch_nw<4>(nw, blocks, wpb, lds, s, a);
-    case 5: return launch_nw<5>(nw, blocks, wpb, lds, s, a);
-    case 6: return launch_nw<6>(nw, blocks, wpb, lds, s, a);
-    default: return hipErrorInvalidValue;
-  }
+hipError_t launch_greedy(int pwl, int nw, bool gring, int blocks, int wpb, size_t lds,
+                         hipStream_t s, const GreedyArgs &a) {
+  const void *k = greedy_kernel_ptr(pwl, nw, gring);
+  if (!k) return hipErrorInvalidValue;
+  void *args[] = {const_cast<GreedyArgs *>(&a)};
+  return hipLaunchKernel(k, dim3(unsigned(blocks)), dim3(unsigned(wpb * kWave)), args, lds, s);
 }
 
 }  // namespace dipsim

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(dip.EXPORTS)
-    assert lib.dip_sim_abi_version() == 4
+    assert lib.dip_sim_abi_version() == 5
 
 
 def test_strerror_strings():
@@ -94,6 +94,7 @@ def test_null_pointers_rejected():
     assert lib.dip_sim_create(None, ctypes.byref(h)) == dip.E_INVAL
     assert lib.dip_sim_evaluate(None, None, None, 0, None, None, None, None, None) == dip.E_INVAL
     assert lib.dip_sim_argmin(None, None, None, 0, 0, None, None) == dip.E_INVAL
+    assert lib.dip_sim_set_greedy_inbox(None, 8) == dip.E_INVAL
     lib.dip_sim_destroy(None)     # no-op
 
 

@@ -48,10 +48,10 @@ def check_against_oracle(prob, groups, prio, sim=None, tag=""):
     return ords, ms, bub, pk, fl
 
 
-SMALL = {1: 300, 2: 203, 3: 37}
+SMALL = {1: 300, 2: 203, 3: 37, 4: 67, 5: 21}
 
 
-@pytest.mark.parametrize("cid", [1, 2, 3])
+@pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
 def test_greedy_parity_rollouts(cid):
     """Random rollout priorities (ragged counts) on the workload shapes."""
     need_gpu()
@@ -124,6 +124,30 @@ def test_greedy_inbox_overflow_goes_through_retry():
     for call in range(3):
         check_against_oracle(prob, (g, G), prio, sim=sim, tag=f"overflow call {call}")
     assert sim.info["greedy_inbox"] > k0
+    sim.close()
+
+
+@pytest.mark.parametrize("cid", [2, 3, 4, 5])
+def test_greedy_second_launch_for_every_candidate(cid):
+    """Inboxes of one stage in the first launch: nearly every candidate
+    overflows and is simulated by the second launch, whose inboxes hold a
+    whole rank -- in LDS on configs 2 and 3, in device memory on configs 4
+    and 5 (594 and 1,413 groups per kind)."""
+    need_gpu()
+    prob = W.make_problem(cid)
+    g, G, cls = W.priority_groups(prob)
+    sim = dip.Sim(prob)
+    assert sim.configure_greedy(G, g) == dip.OK
+    assert sim.set_greedy_inbox(1) == dip.OK
+    assert sim.set_greedy_inbox(3) == dip.E_INVAL
+    assert sim.info["greedy_inbox"] == 1
+    ring = sim.info["greedy_retry_ring_bytes"]
+    assert (ring > 0) == (cid >= 4), ring
+    prio = W.rollout_priorities(cls, {2: 70, 3: 19, 4: 9, 5: 5}[cid], seed=31)
+    for call in range(2):                    # fixed size: no growth between calls
+        check_against_oracle(prob, (g, G), prio, sim=sim, tag=f"config {cid} inbox 1 call {call}")
+    assert sim.info["greedy_inbox"] == 1
+    assert sim.set_greedy_inbox(0) == dip.OK and sim.info["greedy_inbox"] == 8
     sim.close()
 
 

@@ -32,7 +32,8 @@ def _sim(prob):
     return sim, g, G, cls
 
 
-@pytest.mark.parametrize("cid,depth,R", [(1, 0, 300), (1, 5, 257), (2, 17, 300), (1, 16, 9)])
+@pytest.mark.parametrize("cid,depth,R", [(1, 0, 300), (1, 5, 257), (2, 17, 300), (1, 16, 9),
+                                         (4, 40, 33), (5, 100, 17)])
 def test_rollouts_match_oracle(cid, depth, R):
     need_gpu()
     prob = W.make_problem(cid)
@@ -87,11 +88,12 @@ def _tiny():
     return W.compile_instance(inst)
 
 
-@pytest.mark.parametrize("case", ["tiny", "c1", "c2", "c3"])
+@pytest.mark.parametrize("case", ["tiny", "c1", "c2", "c3", "c4", "c5"])
 def test_search_trajectory_matches_oracle(case):
     need_gpu()
     prob = _tiny() if case == "tiny" else W.make_problem(int(case[1]))
-    iters, R = {"tiny": (200, 3), "c1": (40, 64), "c2": (12, 128), "c3": (4, 12)}[case]
+    iters, R = {"tiny": (200, 3), "c1": (40, 64), "c2": (12, 128), "c3": (4, 12), "c4": (3, 8),
+                "c5": (2, 5)}[case]
     sim, g, G, cls = _sim(prob)
     print(f"{case}: {iters} iterations x {R} rollouts", flush=True)
     srch = Search(sim, cls, R, seed=21)
