@@ -113,12 +113,17 @@ def main():
                     help="also stream the configuration's full candidate count from pinned host "
                          "memory in chunks on two streams (copy/compute overlap); reported "
                          "separately, host-link inclusive")
-    ap.add_argument("--path", choices=("simulate", "greedy", "mcts", "cost", "memopt"),
+    ap.add_argument("--path", choices=("simulate", "greedy", "mcts", "search", "cost", "memopt"),
                     default="simulate",
-                    help="simulate given orders (default), build them with the greedy, or "
-                         "search priorities with MCTS over GPU-batched greedy rollouts")
+                    help="simulate given orders (default), build them with the greedy, "
+                         "search priorities with MCTS over GPU-batched greedy rollouts, or "
+                         "compare MCTS with depth-first and random exploration (search)")
     ap.add_argument("--rollouts", type=int, default=16384,
                     help="mcts: rollouts per expansion")
+    ap.add_argument("--alpha", type=float, default=1.0, help="mcts/search: UCB exponent")
+    ap.add_argument("--beta", type=float, default=0.1, help="mcts/search: UCB exploration weight")
+    ap.add_argument("--policies", default="ucb,dfs,random",
+                    help="search: strategies to run (ucb, dfs, random)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="after timing, run plain device copies of this many MiB (a known-size "
                          "kernel for scaling HBM byte counters)")
@@ -143,6 +148,8 @@ def main():
         return run_greedy(args, cfg)
     if args.path == "mcts":
         return run_mcts(args, cfg)
+    if args.path == "search":
+        return run_search(args, cfg)
     if args.path == "cost":
         return run_cost(args, cfg)
     if args.path == "memopt":
@@ -646,7 +653,7 @@ def run_mcts(args, cfg):
     log(f"[bench] mcts on {cfg.name}: {n_cls} segment classes, {G} groups, "
         f"{prob.n_total} stages, {R} rollouts per expansion")
 
-    search = Search(sim, cls, R, seed=cfg.seed)
+    search = Search(sim, cls, R, seed=cfg.seed, alpha=args.alpha, beta=args.beta)
     for t in range(args.warmup):            # warm-up iterations are part of the search
         search.step(t)
     torch.cuda.synchronize()
@@ -728,6 +735,124 @@ def run_mcts(args, cfg):
                      "achieved": R * bytes_per_rollout / (greedy_ms / 1e3) / 1e9,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": R * bytes_per_rollout / (greedy_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
+                     "traffic": None, "algorithmic_bytes": R * bytes_per_rollout},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(rec), flush=True)
+    sim.close()
+
+
+def run_search(args, cfg):
+    """The search-efficiency comparison: the segment search with MCTS (UCB),
+    depth-first and random exploration, each for args.steps iterations of
+    args.rollouts GPU rollouts; best makespan found against wall time."""
+    import numpy as np
+    import torch
+
+    import paper_2504_14145_amd as dip
+    from paper_2504_14145_amd.mcts import Search
+    import workloads as W
+
+    R = args.rollouts
+    prob = W.make_problem(cfg)
+    op_group, G, cls = W.priority_groups(prob)
+    n_cls = int(cls.max()) + 1
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    sim = dip.Sim(prob)
+    rc = sim.configure_greedy(G, op_group)
+    if rc != dip.OK:
+        raise SystemExit(f"greedy unsupported on {cfg.name}: {dip.strerror(rc)}")
+    sim.greedy(torch.zeros((1, G), dtype=torch.int32, device=dev))      # uploads the costs
+    log(f"[bench] search comparison on {cfg.name}: {n_cls} segment classes, {prob.n_total} "
+        f"stages, {args.steps} iterations x {R} rollouts per strategy")
+    # warm-up: one short search (kernels loaded, inbox size settled)
+    Search(sim, cls, R, seed=cfg.seed + 7).run(max(args.warmup, 1))
+    torch.cuda.synchronize()
+    curves, final, secs, rates, iters_done = {}, {}, {}, {}, {}
+    policies = [p for p in args.policies.split(",") if p]
+    for policy in policies:
+        srch = Search(sim, cls, R, seed=cfg.seed, alpha=args.alpha, beta=args.beta, policy=policy)
+        pts = []
+        n_it = 0
+        t0 = time.perf_counter()
+        for t in range(args.steps):
+            if srch.done[0]:
+                break
+            srch.step(t)
+            b = srch.best[0] if srch.best[0] != float("inf") else None     # None: none feasible yet
+            if not pts or b != pts[-1][2]:      # the points where the best improves
+                pts.append([t + 1, round(time.perf_counter() - t0, 4), b])
+            n_it = t + 1
+        torch.cuda.synchronize()
+        secs[policy] = time.perf_counter() - t0
+        rates[policy] = R * n_it / secs[policy]
+        curves[policy] = pts
+        final[policy] = srch.best[0] if srch.best[0] != float("inf") else None
+        iters_done[policy] = n_it
+        log(f"[bench] {policy}: best makespan {srch.best[0]} after {n_it} iterations "
+            f"({secs[policy]:.2f} s, {rates[policy]:.3g} rollouts/s)")
+    # the order a plain first-in first-out priority gives, for reference
+    fifo = torch.from_numpy(W.fifo_priorities(prob, cls, op_group)[None, :].astype(np.int32)).to(dev)
+    _, (ms, _, _, fl) = sim.greedy(fifo, orders=False)
+    fifo_ms = int(ms.item()) if int(fl.item()) == 0 else None
+    log(f"[bench] first-in first-out priorities: makespan {fifo_ms}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        import oracle.mcts as OM
+        cores = max(1, min(16, len(os.sched_getaffinity(0))))
+        tc = time.perf_counter()
+        it_cpu = 0
+        while True:
+            it_cpu += 1
+            OM.search(prob, op_group, G, cls, it_cpu, R, seed=cfg.seed, threads=cores)
+            if time.perf_counter() - tc >= args.cpu_seconds:
+                break
+        dt = time.perf_counter() - tc
+        done = R * it_cpu * (it_cpu + 1) // 2
+        cpu = {"value": done / dt, "unit": "rollouts/s", "cores": cores, "kind": "oracle",
+               "sample": f"oracle MCTS searches of 1..{it_cpu} iterations x {R} rollouts "
+                         f"({dt:.2f} s wall on {cores} threads)"}
+        log(f"[bench] cpu oracle {done / dt:.0f} rollouts/s on {cores} threads")
+
+    # per-kernel times of one batch, for the greedy kernel's line
+    dip.profile(sim.h, True)
+    key = torch.full((1,), -1, dtype=torch.int64, device=dev)
+    srch = Search(sim, cls, R, seed=cfg.seed)
+    dip.rollouts(sim.h, [], R, cfg.seed, 10**6, srch.prio, srch.ms, srch.fl, key)
+    torch.cuda.synchronize()
+    k_ms = dip.last_profile(sim.h)
+    dip.profile(sim.h, False)
+    P = prob.n_ranks
+    bytes_per_rollout = 4 * G + 4 + 8 * P + 1 + 4 * G
+    greedy_ms = k_ms[0]
+    achieved = R * bytes_per_rollout / (greedy_ms / 1e3) / 1e9
+    rec = {
+        "metric": "best makespan found by the segment search in a fixed budget "
+                  "(MCTS vs depth-first vs random exploration, Sec. 5.1)",
+        "value": final[policies[0]],
+        "unit": "us",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": secs[policies[0]] / max(1, iters_done[policies[0]]) * 1e3,
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int32",
+        "data": "synthetic",
+        "config": {"workload": cfg.name, "rollouts_per_iteration": R, "iterations": args.steps,
+                   "segment_classes": n_cls, "alpha": args.alpha, "beta": args.beta,
+                   "policies": policies, "parallelism": "single GPU"},
+        "final_best_us": final,
+        "fifo_makespan_us": fifo_ms,
+        "seconds": secs,
+        "rollouts_per_s": rates,
+        "iterations_run": iters_done,
+        "curves": {"columns": ["iteration", "seconds", "best_makespan_us"], **curves},
+        "roofline": {"bound": "hbm", "kernel": "greedy", "achieved": achieved,
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": None, "algorithmic_bytes": R * bytes_per_rollout},
         "cpu_baseline": cpu,
     }

@@ -28,6 +28,18 @@ Python, one node object per tree node, following the paper's loop:
   is mix(mix(seed + (t + 1) G) + (i + 1) G), G = 0x9E3779B97F4A7C15.
 * Backpropagation: the best rollout score (lowest index among equal ones)
   updates s and N of the new node and of every ancestor.
+
+The two other exploration strategies the paper compares its search with
+(depth-first search and random exploration, in its search-efficiency
+evaluation) replace selection and expansion and keep the rollouts and the
+backpropagation:
+
+* policy "dfs": the tree is walked depth first, children in ascending class
+  order: the next node expanded is the lowest untried class of the deepest
+  node on the current path that still has one (after a complete sequence,
+  the walk backs up);
+* policy "random": every iteration rolls out from the root (random complete
+  sequences; the tree does not grow).
 """
 from __future__ import annotations
 
@@ -134,24 +146,42 @@ def mark_done(v, n_classes):
 
 
 def search(prob, op_group, n_groups, group_class, iterations, rollouts, seed,
-           alpha=1.0, beta=0.1, threads=8):
+           alpha=1.0, beta=0.1, threads=8, policy="ucb"):
     """Run the search; returns (trajectory, best, root) where trajectory[t] =
     (prefix of the rolled-out node, best score of its rollouts, index of the
-    best rollout) and best = (score, sequence, iteration, index)."""
+    best rollout) and best = (score, sequence, iteration, index).  policy:
+    "ucb" (the paper's MCTS), "dfs" or "random"."""
+    if policy not in ("ucb", "dfs", "random"):
+        raise ValueError(policy)
     group_class = [int(c) for c in group_class]
     n = max(group_class) + 1 if group_class else 0
     root = Node(None, None, n)
     traj = []
     best = (INF, None, -1, -1)
+    cursor = root                        # dfs: the node expanded last
     for t in range(iterations):
         if root.done:
             break
-        x = select(root, alpha, beta)
-        if x.untried:
-            c = x.untried.pop(_expansion(seed, t, len(x.untried)))
+        if policy == "random":
+            x = root
+        elif policy == "dfs":
+            x = cursor
+            while x is not None and not x.untried:
+                x = x.parent
+            if x is None:
+                break
+            c = min(x.untried)
+            x.untried.remove(c)
             child = Node(c, x, n)
             x.children[c] = child
-            x = child
+            x = cursor = child
+        else:
+            x = select(root, alpha, beta)
+            if x.untried:
+                c = x.untried.pop(_expansion(seed, t, len(x.untried)))
+                child = Node(c, x, n)
+                x.children[c] = child
+                x = child
         prefix = x.prefix()
         rest = [c for c in range(n) if c not in set(prefix)]
         seqs = [prefix + shuffled(rest, seed, t, i) for i in range(rollouts)]

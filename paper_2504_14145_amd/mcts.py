@@ -16,6 +16,11 @@ read back per iteration.  Tree steps, per iteration:
 * expansion: one untried class, drawn by workloads.expansion_draw;
 * rollouts: n_rollouts completions (draw = iteration number);
 * backpropagation: the batch's best score to the new node and its ancestors.
+
+policy "dfs" and "random" are the two exploration strategies the paper
+compares its search with: depth-first (the lowest untried class of the
+deepest node on the current path that has one) and random exploration
+(every batch rolled out from the root); rollouts and backpropagation stay.
 """
 from __future__ import annotations
 
@@ -29,7 +34,7 @@ INF = float("inf")
 class Search:
     """One search over the classes of a Sim configured for the greedy."""
 
-    def __init__(self, sim, group_class, rollouts, seed, alpha=1.0, beta=0.1):
+    def __init__(self, sim, group_class, rollouts, seed, alpha=1.0, beta=0.1, policy="ucb"):
         import torch
 
         from . import configure_rollouts, OK, strerror
@@ -42,6 +47,10 @@ class Search:
         rc = configure_rollouts(sim.h, self.n, self.cls_of_group)
         if rc != OK:
             raise RuntimeError(f"dip_sim_configure_rollouts: {strerror(rc)}")
+        if policy not in ("ucb", "dfs", "random"):
+            raise ValueError(policy)
+        self.policy = policy
+        self.cursor = 0                  # dfs: the node expanded last
         self.R = int(rollouts)
         self.seed = int(seed)
         self.alpha, self.beta = float(alpha), float(beta)
@@ -118,10 +127,23 @@ class Search:
         """One iteration (t = its number, which also names its random draws)."""
         from . import NO_KEY, decode_key, rollouts
 
-        v = self._select()
-        if self.todo[v]:
-            c = self.todo[v].pop(self.draw_child(self.seed, t, len(self.todo[v])))
-            v = self._add(v, c)
+        if self.policy == "random":
+            v = 0
+        elif self.policy == "dfs":
+            v = self.cursor
+            while v >= 0 and not self.todo[v]:
+                v = self.parent[v]
+            if v < 0:
+                self.done[0] = True      # every sequence visited
+                return
+            c = min(self.todo[v])
+            self.todo[v].remove(c)
+            v = self.cursor = self._add(v, c)
+        else:
+            v = self._select()
+            if self.todo[v]:
+                c = self.todo[v].pop(self.draw_child(self.seed, t, len(self.todo[v])))
+                v = self._add(v, c)
         prefix = self._path(v)
         self.key.fill_(-1)
         rollouts(self.sim.h, prefix, self.R, self.seed, t, self.prio, self.ms, self.fl, self.key)

@@ -105,3 +105,25 @@ def test_search_trajectory_matches_oracle(case):
     if case == "tiny":
         assert root.done and srch.done[0] and len(traj) == 64
     sim.close()
+
+
+@pytest.mark.parametrize("policy", ["dfs", "random"])
+@pytest.mark.parametrize("case", ["tiny", "c2", "c3"])
+def test_other_policies_match_oracle(case, policy):
+    """Depth-first and random exploration (the strategies the paper compares
+    its search with) drive the same rollouts: trajectories equal the oracle's."""
+    need_gpu()
+    prob = _tiny() if case == "tiny" else W.make_problem(int(case[1]))
+    iters, R = {"tiny": (80, 3), "c2": (10, 64), "c3": (4, 12)}[case]
+    sim, g, G, cls = _sim(prob)
+    print(f"{case} {policy}: {iters} iterations x {R} rollouts", flush=True)
+    srch = Search(sim, cls, R, seed=5, policy=policy)
+    traj, best = srch.run(iters)
+    want_traj, want_best, root = OM.search(prob, g, G, cls, iters, R, seed=5, threads=16,
+                                           policy=policy)
+    assert traj == want_traj
+    assert best[0] == want_best[0] and best[2:] == want_best[2:]
+    assert best[1] == list(want_best[1])
+    if case == "tiny" and policy == "dfs":
+        assert len(traj) == 64 and srch.done[0]
+    sim.close()

@@ -105,3 +105,54 @@ def test_caps_make_rollouts_infeasible():
     traj, best, root = M.search(prob, g, G, cls, iterations=5, rollouts=4, seed=3)
     assert all(sc == M.INF for (_, sc, _) in traj)
     assert best[1] is None and root.s == M.INF
+
+
+def _dfs_prefixes(n):
+    """Depth-first visiting order of the tree of class sequences, children in
+    ascending class order: every proper and complete prefix, parents first."""
+    out = []
+
+    def walk(prefix):
+        for c in range(n):
+            if c not in prefix:
+                out.append(tuple(prefix + [c]))
+                walk(prefix + [c])
+    walk([])
+    return out
+
+
+def test_dfs_policy_walks_the_tree_depth_first():
+    """Depth-first search expands every node of the 4-class tree in DFS order
+    (64 nodes), then stops, and its best is the brute-force optimum."""
+    prob, g, G, cls = _tiny()
+    n = int(cls.max()) + 1
+    traj, best, root = M.search(prob, g, G, cls, iterations=500, rollouts=2, seed=4, policy="dfs")
+    assert [p for (p, _, _) in traj] == _dfs_prefixes(n)
+    assert len(traj) == 64 and root.done
+    all_seq = list(itertools.permutations(range(n)))
+    _, res = O.greedy(prob, g, G, np.stack([M.priorities_of(q, cls, n) for q in all_seq]))
+    assert best[0] == min(res.makespan)
+    # each complete prefix is scored exactly (every rollout is that sequence)
+    by_seq = dict(zip(all_seq, res.makespan))
+    for p, sc, _ in traj:
+        if len(p) == n:
+            assert sc == by_seq[p]
+
+
+def test_random_policy_rolls_out_from_the_root():
+    """Random exploration: every iteration R uniform sequences of all classes,
+    the same shuffles as the rollouts of an empty prefix; the tree never grows."""
+    prob = W.make_problem(1)
+    g, G, cls = W.priority_groups(prob)
+    n = int(cls.max()) + 1
+    R = 6
+    traj, best, root = M.search(prob, g, G, cls, iterations=5, rollouts=R, seed=9, policy="random")
+    assert all(p == () for (p, _, _) in traj) and not root.children and root.N == 5
+    for t, (_, sc, idx) in enumerate(traj):
+        seqs = [M.shuffled(range(n), 9, t, i) for i in range(R)]
+        _, res = O.greedy(prob, g, G, np.stack([M.priorities_of(q, cls, n) for q in seqs]))
+        scores = [m if f == 0 else M.INF for m, f in zip(res.makespan, res.flags)]
+        assert sc == min(scores) and idx == scores.index(min(scores))
+    assert best[0] == min(sc for (_, sc, _) in traj)
+    with pytest.raises(ValueError):
+        M.search(prob, g, G, cls, iterations=1, rollouts=1, seed=0, policy="bfs")
