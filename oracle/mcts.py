@@ -40,6 +40,15 @@ backpropagation:
   the walk backs up);
 * policy "random": every iteration rolls out from the root (random complete
   sequences; the tree does not grow).
+
+Parallel search (Sec. 6.2: workers explore at once and merge their results
+into shared tree statistics after each round of rollouts): with W workers, a
+round lets worker 0, 1, ..., W-1 select and expand in turn, each adding a
+virtual visit (N + 1, s unchanged) to its node and every ancestor, so that
+later workers see the earlier ones' choices; the rollouts of all W nodes then
+run, and their best scores update s in worker order (the virtual visits stand
+as the visits).  Leaves are numbered across rounds; leaf k's expansion draw
+and rollout draws use k.  W = 1 is the sequential loop above.
 """
 from __future__ import annotations
 
@@ -146,60 +155,75 @@ def mark_done(v, n_classes):
 
 
 def search(prob, op_group, n_groups, group_class, iterations, rollouts, seed,
-           alpha=1.0, beta=0.1, threads=8, policy="ucb"):
-    """Run the search; returns (trajectory, best, root) where trajectory[t] =
-    (prefix of the rolled-out node, best score of its rollouts, index of the
-    best rollout) and best = (score, sequence, iteration, index).  policy:
-    "ucb" (the paper's MCTS), "dfs" or "random"."""
+           alpha=1.0, beta=0.1, threads=8, policy="ucb", workers=1):
+    """Run the search for ``iterations`` rounds of ``workers`` leaves; returns
+    (trajectory, best, root) where trajectory[k] = (prefix of leaf k, best score
+    of its rollouts, index of the best rollout) and best = (score, sequence,
+    leaf, index).  policy: "ucb" (the paper's MCTS), "dfs" or "random"."""
     if policy not in ("ucb", "dfs", "random"):
         raise ValueError(policy)
+    if workers < 1:
+        raise ValueError(workers)
     group_class = [int(c) for c in group_class]
     n = max(group_class) + 1 if group_class else 0
     root = Node(None, None, n)
     traj = []
     best = (INF, None, -1, -1)
     cursor = root                        # dfs: the node expanded last
-    for t in range(iterations):
-        if root.done:
-            break
-        if policy == "random":
-            x = root
-        elif policy == "dfs":
-            x = cursor
-            while x is not None and not x.untried:
-                x = x.parent
-            if x is None:
+    k = 0                                # leaves so far
+    for _ in range(iterations):
+        leaves = []
+        for _w in range(workers):
+            if root.done:
                 break
-            c = min(x.untried)
-            x.untried.remove(c)
-            child = Node(c, x, n)
-            x.children[c] = child
-            x = cursor = child
-        else:
-            x = select(root, alpha, beta)
-            if x.untried:
-                c = x.untried.pop(_expansion(seed, t, len(x.untried)))
+            if policy == "random":
+                x = root
+            elif policy == "dfs":
+                x = cursor
+                while x is not None and not x.untried:
+                    x = x.parent
+                if x is None:
+                    break
+                c = min(x.untried)
+                x.untried.remove(c)
                 child = Node(c, x, n)
                 x.children[c] = child
-                x = child
-        prefix = x.prefix()
-        rest = [c for c in range(n) if c not in set(prefix)]
-        seqs = [prefix + shuffled(rest, seed, t, i) for i in range(rollouts)]
-        prio = np.stack([priorities_of(q, group_class, n) for q in seqs])
-        _, res = _greedy(prob, op_group, n_groups, prio, threads=threads)
-        scores = [float(m) if f == 0 else INF for m, f in zip(res.makespan, res.flags)]
-        b = min(range(rollouts), key=lambda i: (scores[i], i))
-        if scores[b] == INF:
-            b = -1                       # no feasible rollout
-        traj.append((tuple(prefix), scores[b] if b >= 0 else INF, b))
-        if b >= 0 and scores[b] < best[0]:
-            best = (scores[b], seqs[b], t, b)
-        v = x
-        while v is not None:
-            v.N += 1
-            v.s = min(v.s, scores[b] if b >= 0 else INF)
-            v = v.parent
-        mark_done(x, n)
+                x = cursor = child
+            else:
+                x = select(root, alpha, beta)
+                if x.untried:
+                    c = x.untried.pop(_expansion(seed, k, len(x.untried)))
+                    child = Node(c, x, n)
+                    x.children[c] = child
+                    x = child
+            v = x
+            while v is not None:         # the (virtual) visit
+                v.N += 1
+                v = v.parent
+            if x.depth == n:
+                mark_done(x, n)          # a complete sequence: nothing below it
+            leaves.append((x, k))
+            k += 1
+        if not leaves:
+            break
+        for x, kk in leaves:
+            prefix = x.prefix()
+            rest = [c for c in range(n) if c not in set(prefix)]
+            seqs = [prefix + shuffled(rest, seed, kk, i) for i in range(rollouts)]
+            prio = np.stack([priorities_of(q, group_class, n) for q in seqs])
+            _, res = _greedy(prob, op_group, n_groups, prio, threads=threads)
+            scores = [float(m) if f == 0 else INF for m, f in zip(res.makespan, res.flags)]
+            b = min(range(rollouts), key=lambda i: (scores[i], i))
+            if scores[b] == INF:
+                b = -1                       # no feasible rollout
+            traj.append((tuple(prefix), scores[b] if b >= 0 else INF, b))
+            if b >= 0 and scores[b] < best[0]:
+                best = (scores[b], seqs[b], kk, b)
+            v = x
+            while v is not None:
+                v.s = min(v.s, scores[b] if b >= 0 else INF)
+                v = v.parent
+            mark_done(x, n)
     return traj, best, root
 
 

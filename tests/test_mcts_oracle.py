@@ -156,3 +156,44 @@ def test_random_policy_rolls_out_from_the_root():
     assert best[0] == min(sc for (_, sc, _) in traj)
     with pytest.raises(ValueError):
         M.search(prob, g, G, cls, iterations=1, rollouts=1, seed=0, policy="bfs")
+
+
+def test_parallel_workers_explore_the_whole_tree():
+    """Five workers per round on the 4-class tree: every node is expanded once
+    (64 leaves), the search stops, and it finds the brute-force optimum."""
+    prob, g, G, cls = _tiny()
+    n = int(cls.max()) + 1
+    traj, best, root = M.search(prob, g, G, cls, iterations=100, rollouts=2, seed=6, workers=5)
+    assert root.done
+    assert sorted(p for (p, _, _) in traj) == sorted(_dfs_prefixes(n))
+    all_seq = list(itertools.permutations(range(n)))
+    _, res = O.greedy(prob, g, G, np.stack([M.priorities_of(q, cls, n) for q in all_seq]))
+    assert best[0] == min(res.makespan)
+
+
+def test_parallel_workers_invariants():
+    """W = 8 on config 1: the first round's leaves are 8 distinct children of
+    the root (virtual visits never send two workers to one untried slot); in
+    the finished tree N counts the leaves of each subtree and s is their best
+    score; the best is the least leaf score."""
+    prob = W.make_problem(1)
+    g, G, cls = W.priority_groups(prob)
+    n = int(cls.max()) + 1
+    traj, best, root = M.search(prob, g, G, cls, iterations=6, rollouts=4, seed=8, workers=8)
+    assert len(traj) == 48
+    first = [p for (p, _, _) in traj[:8]]
+    assert all(len(p) == 1 for p in first) and len(set(first)) == 8
+
+    def walk(v):
+        pre = tuple(v.prefix())
+        hits = [sc for (p, sc, _) in traj if p[:len(pre)] == pre]
+        assert v.N == len(hits)
+        assert v.s == min(hits)
+        for c in v.children.values():
+            walk(c)
+    walk(root)
+    assert best[0] == min(sc for (_, sc, _) in traj)
+    # one worker is the sequential search
+    t1, b1, _ = M.search(prob, g, G, cls, iterations=12, rollouts=4, seed=8, workers=1)
+    t2, b2, _ = M.search(prob, g, G, cls, iterations=12, rollouts=4, seed=8)
+    assert t1 == t2 and b1[0] == b2[0]
