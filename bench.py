@@ -122,6 +122,8 @@ def main():
                     help="mcts: rollouts per expansion")
     ap.add_argument("--alpha", type=float, default=1.0, help="mcts/search: UCB exponent")
     ap.add_argument("--beta", type=float, default=0.1, help="mcts/search: UCB exploration weight")
+    ap.add_argument("--workers", type=int, default=1,
+                    help="mcts/search: tree nodes rolled out per round (parallel search)")
     ap.add_argument("--policies", default="ucb,dfs,random",
                     help="search: strategies to run (ucb, dfs, random)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -653,15 +655,18 @@ def run_mcts(args, cfg):
     log(f"[bench] mcts on {cfg.name}: {n_cls} segment classes, {G} groups, "
         f"{prob.n_total} stages, {R} rollouts per expansion")
 
-    search = Search(sim, cls, R, seed=cfg.seed, alpha=args.alpha, beta=args.beta)
-    for t in range(args.warmup):            # warm-up iterations are part of the search
+    search = Search(sim, cls, R, seed=cfg.seed, alpha=args.alpha, beta=args.beta,
+                    workers=args.workers)
+    for t in range(args.warmup):            # warm-up rounds are part of the search
         search.step(t)
     torch.cuda.synchronize()
+    leaves0 = search.leaves
     t0 = time.perf_counter()
     for t in range(args.warmup, args.warmup + args.steps):
         search.step(t)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    timed_rollouts = (search.leaves - leaves0) * R
     iters = args.warmup + args.steps
     mcts_best = search.best[0]
 
@@ -679,15 +684,19 @@ def run_mcts(args, cfg):
 
     # random exploration with the same number of rollouts (empty prefix)
     best_rand = float("inf")
-    for t in range(iters):
+    left, t = search.leaves * R, 0
+    while left > 0:
+        b = min(left, R * args.workers)
         key.fill_(-1)
-        dip.rollouts(sim.h, [], R, cfg.seed + 1, t, search.prio, search.ms, search.fl, key)
+        dip.rollouts(sim.h, [], b, cfg.seed + 1, t, search.prio, search.ms, search.fl, key)
         k = dip.decode_key(int(key.item()))
         if k[0] >= 0:
             best_rand = min(best_rand, float(k[1]))
-    log(f"[bench] {args.steps} iterations in {wall * 1e3:.1f} ms; batch {batch_ms:.3f} ms "
-        f"(greedy kernels {k_ms}); best makespan mcts {mcts_best} vs random {best_rand} "
-        f"after {iters * R} rollouts each")
+        left -= b
+        t += 1
+    log(f"[bench] {args.steps} rounds of {args.workers} leaves in {wall * 1e3:.1f} ms; batch "
+        f"{batch_ms:.3f} ms (greedy kernels {k_ms}); best makespan mcts {mcts_best} vs random "
+        f"{best_rand} after {search.leaves * R} rollouts each")
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -713,7 +722,7 @@ def run_mcts(args, cfg):
     greedy_ms = k_ms[0] if k_ms else batch_ms
     rec = {
         "metric": "MCTS rollouts interleaved and scored/sec (segment reordering, Sec. 5.1)",
-        "value": R * args.steps / wall,
+        "value": timed_rollouts / wall,
         "unit": "rollouts/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -724,12 +733,12 @@ def run_mcts(args, cfg):
         "vs_baseline": None,
         "dtype": "int32",
         "data": "synthetic",
-        "config": {"workload": cfg.name, "rollouts_per_iteration": R, "segment_classes": n_cls,
+        "config": {"workload": cfg.name, "rollouts_per_leaf": R, "workers": args.workers, "segment_classes": n_cls,
                    "priority_groups": G, "stages_per_candidate": prob.n_total,
                    "parallelism": "single GPU"},
         "batch_ms": batch_ms,
         "kernel_us": {n: t * 1e3 for n, t in zip(["greedy", "greedy_retry"], k_ms)},
-        "search": {"iterations": iters, "rollouts_each": iters * R,
+        "search": {"rounds": iters, "workers": args.workers, "rollouts_each": search.leaves * R,
                    "mcts_best_makespan_us": mcts_best, "random_best_makespan_us": best_rand},
         "roofline": {"bound": "hbm", "kernel": "greedy",
                      "achieved": R * bytes_per_rollout / (greedy_ms / 1e3) / 1e9,
@@ -772,7 +781,8 @@ def run_search(args, cfg):
     curves, final, secs, rates, iters_done = {}, {}, {}, {}, {}
     policies = [p for p in args.policies.split(",") if p]
     for policy in policies:
-        srch = Search(sim, cls, R, seed=cfg.seed, alpha=args.alpha, beta=args.beta, policy=policy)
+        srch = Search(sim, cls, R, seed=cfg.seed, alpha=args.alpha, beta=args.beta, policy=policy,
+                      workers=args.workers)
         pts = []
         n_it = 0
         t0 = time.perf_counter()
@@ -786,7 +796,7 @@ def run_search(args, cfg):
             n_it = t + 1
         torch.cuda.synchronize()
         secs[policy] = time.perf_counter() - t0
-        rates[policy] = R * n_it / secs[policy]
+        rates[policy] = R * srch.leaves / secs[policy]
         curves[policy] = pts
         final[policy] = srch.best[0] if srch.best[0] != float("inf") else None
         iters_done[policy] = n_it
@@ -842,7 +852,8 @@ def run_search(args, cfg):
         "vs_baseline": None,
         "dtype": "int32",
         "data": "synthetic",
-        "config": {"workload": cfg.name, "rollouts_per_iteration": R, "iterations": args.steps,
+        "config": {"workload": cfg.name, "rollouts_per_leaf": R, "workers": args.workers,
+                   "rounds": args.steps,
                    "segment_classes": n_cls, "alpha": args.alpha, "beta": args.beta,
                    "policies": policies, "parallelism": "single GPU"},
         "final_best_us": final,

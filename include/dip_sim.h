@@ -289,6 +289,22 @@ int dip_sim_rollouts(dip_sim *h, const int32_t *prefix, int32_t depth, int64_t n
                      uint64_t seed, uint64_t draw, int32_t *out_prio, int32_t *out_makespan,
                      uint8_t *out_flags, uint64_t *inout_best_key, void *stream);
 
+/* The rollouts of several tree nodes in one launch, for a search whose
+ * workers (Sec. 6.2's parallel search) each pick a node per round: leaf l
+ * (0 <= l < n_leaves <= 65535) has the class prefix of length depths[l]
+ * (host; the prefixes concatenated in prefixes, host) and rows
+ * l*per_leaf .. l*per_leaf + per_leaf - 1 of out_prio, out_makespan and
+ * out_flags; its rollouts are exactly those dip_sim_rollouts makes for that
+ * prefix with draw = draw_base + l.  inout_keys (device uint64 [n_leaves],
+ * 8-byte aligned): key l folds in leaf l's best unflagged (makespan, rollout
+ * index within the leaf).  DIP_E_INVAL for a repeated or out-of-range class
+ * in a prefix, null pointers or per_leaf * n_leaves above 2^31 - 1.  Enqueued
+ * on stream; the prefixes are copied before return. */
+int dip_sim_rollouts_batch(dip_sim *h, int32_t n_leaves, const int32_t *depths,
+                           const int32_t *prefixes, int64_t per_leaf, uint64_t seed,
+                           uint64_t draw_base, int32_t *out_prio, int32_t *out_makespan,
+                           uint8_t *out_flags, uint64_t *inout_keys, void *stream);
+
 /* Per-layer memory optimisation (Sec. 5.3), set-up.  A stage pair is an
  * activation slot (its forward and backward, one rank).  Its layers are
  * slot_layers[s] .. slot_layers[s+1]-1 (host, [n_slots+1], from 0), and layer

@@ -27,7 +27,8 @@ EXPORTS = ("dip_sim_abi_version", "dip_sim_check_topology", "dip_sim_check_costs
            "dip_sim_create", "dip_sim_configure", "dip_sim_configure_pool",
            "dip_sim_configure_check", "dip_sim_get_info", "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
            "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_set_greedy_inbox", "dip_sim_greedy",
-           "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_cost_tables",
+           "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_sim_rollouts_batch",
+           "dip_cost_tables",
            "dip_sim_configure_memopt", "dip_sim_memopt", "dip_sim_destroy", "dip_sim_strerror")
 
 
@@ -103,6 +104,8 @@ def load():
         lib.dip_sim_memopt.argtypes = [vp, vp, i64, vp, vp, vp, vp]
         lib.dip_sim_rollouts.argtypes = [vp, vp, i32, i64, ctypes.c_uint64, ctypes.c_uint64,
                                          vp, vp, vp, vp, vp]
+        lib.dip_sim_rollouts_batch.argtypes = [vp, i32, vp, vp, i64, ctypes.c_uint64,
+                                               ctypes.c_uint64, vp, vp, vp, vp, vp]
         lib.dip_sim_destroy.argtypes = [vp]
         lib.dip_sim_destroy.restype = None
         lib.dip_sim_strerror.argtypes = [ctypes.c_int]
@@ -112,7 +115,8 @@ def load():
                      "dip_sim_get_info",
                      "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
                      "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_set_greedy_inbox", "dip_sim_greedy",
-                     "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_cost_tables",
+                     "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_sim_rollouts_batch",
+           "dip_cost_tables",
                      "dip_sim_configure_memopt", "dip_sim_memopt"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
@@ -275,6 +279,21 @@ def rollouts(h, prefix, n_rollouts, seed, draw, out_prio, out_makespan, out_flag
                                  out_makespan.data_ptr(), out_flags.data_ptr(),
                                  inout_best_key.data_ptr(), _stream_ptr(stream))
     _check(rc, "dip_sim_rollouts")
+
+
+def rollouts_batch(h, prefixes, per_leaf, seed, draw_base, out_prio, out_makespan, out_flags,
+                   inout_keys, stream=None) -> None:
+    """``prefixes``: host list of class sequences, one per leaf; leaf l's
+    rollouts are rows l*per_leaf.. of the device outputs, drawn with
+    draw_base + l; inout_keys: device int64 [len(prefixes)]."""
+    depths = np.ascontiguousarray([len(p) for p in prefixes], np.int32)
+    flat = np.ascontiguousarray([c for p in prefixes for c in p], np.int32)
+    rc = load().dip_sim_rollouts_batch(
+        h, int(depths.size), depths.ctypes.data, flat.ctypes.data if flat.size else None,
+        int(per_leaf), int(seed) & ((1 << 64) - 1), int(draw_base) & ((1 << 64) - 1),
+        out_prio.data_ptr(), out_makespan.data_ptr(), out_flags.data_ptr(), inout_keys.data_ptr(),
+        _stream_ptr(stream))
+    _check(rc, "dip_sim_rollouts_batch")
 
 
 class DeviceOpTable:

@@ -181,8 +181,9 @@ struct dip_sim {
   int32_t rl_n = 0;                    // classes
   std::vector<int32_t> rl_class;       // [G] caller-indexed class of each group
   int32_t *d_rl_class = nullptr;       // [G]
-  int32_t *d_rl_seq = nullptr;         // [n] prefix, then the other classes
+  int32_t *d_rl_seq = nullptr;         // [leaves][n] prefix, then the other classes; [leaves] depths
   int32_t *h_rl_seq = nullptr;         // pinned staging of it
+  int32_t rl_leaf_cap = 0;             // leaves the two hold
   hipEvent_t rl_seq_ev = nullptr;
   bool rl_seq_pending = false;
   int32_t *d_rl_bub = nullptr, *d_rl_peak = nullptr;  // [cap][P] greedy outputs
@@ -823,6 +824,7 @@ void release_rollouts(dip_sim *h) {
   if (h->d_rl_bub) (void)hipFree(h->d_rl_bub);
   if (h->d_rl_peak) (void)hipFree(h->d_rl_peak);
   h->d_rl_class = h->d_rl_seq = h->h_rl_seq = nullptr;
+  h->rl_leaf_cap = 0;
   h->rl_seq_ev = nullptr;
   h->rl_seq_pending = false;
   h->d_rl_bub = h->d_rl_peak = nullptr;
@@ -1619,10 +1621,11 @@ int dip_sim_configure_rollouts(dip_sim *h, int32_t n_classes, const int32_t *gro
   };
   hipError_t e;
   if ((e = hipMalloc(&h->d_rl_class, size_t(G) * 4)) != hipSuccess) return fail(e);
-  if ((e = hipMalloc(&h->d_rl_seq, size_t(n_classes) * 4)) != hipSuccess) return fail(e);
-  if ((e = hipHostMalloc(reinterpret_cast<void **>(&h->h_rl_seq), size_t(n_classes) * 4,
+  if ((e = hipMalloc(&h->d_rl_seq, size_t(n_classes + 1) * 4)) != hipSuccess) return fail(e);
+  if ((e = hipHostMalloc(reinterpret_cast<void **>(&h->h_rl_seq), size_t(n_classes + 1) * 4,
                          hipHostMallocDefault)) != hipSuccess)
     return fail(e);
+  h->rl_leaf_cap = 1;
   if ((e = hipEventCreateWithFlags(&h->rl_seq_ev, hipEventDisableTiming)) != hipSuccess) return fail(e);
   if ((e = hipMemcpy(h->d_rl_class, cls.data(), size_t(G) * 4, hipMemcpyHostToDevice)) != hipSuccess)
     return fail(e);
@@ -1632,61 +1635,111 @@ int dip_sim_configure_rollouts(dip_sim *h, int32_t n_classes, const int32_t *gro
   return DIP_OK;
 }
 
-int dip_sim_rollouts(dip_sim *h, const int32_t *prefix, int32_t depth, int64_t n_rollouts,
-                     uint64_t seed, uint64_t draw, int32_t *out_prio, int32_t *out_makespan,
-                     uint8_t *out_flags, uint64_t *inout_best_key, void *stream_) {
-  if (!h || n_rollouts < 0 || depth < 0) return DIP_E_INVAL;
+int dip_sim_rollouts_batch(dip_sim *h, int32_t n_leaves, const int32_t *depths,
+                           const int32_t *prefixes, int64_t per_leaf, uint64_t seed,
+                           uint64_t draw_base, int32_t *out_prio, int32_t *out_makespan,
+                           uint8_t *out_flags, uint64_t *inout_keys, void *stream_) {
+  if (!h || n_leaves < 1 || n_leaves > 65535 || per_leaf < 0 || !depths) return DIP_E_INVAL;
   if (!h->rl_ok || !h->gr_ok) return DIP_E_STATE;
   if (!h->gr_costs_ok) return DIP_E_STATE;
   const int32_t n = h->rl_n;
-  if (depth > n || (depth > 0 && !prefix)) return DIP_E_INVAL;
-  if (n_rollouts == 0) return DIP_OK;
-  if (n_rollouts > INT32_MAX || !out_prio || !out_makespan || !out_flags || !inout_best_key)
-    return DIP_E_INVAL;
-  hipStream_t stream = static_cast<hipStream_t>(stream_);
-  std::vector<char> on(n, 0);
-  for (int32_t d = 0; d < depth; ++d) {
-    if (prefix[d] < 0 || prefix[d] >= n || on[prefix[d]]) return DIP_E_INVAL;
-    on[prefix[d]] = 1;
+  // every prefix: distinct classes in range
+  int64_t total = 0;
+  for (int32_t l = 0; l < n_leaves; ++l) {
+    if (depths[l] < 0 || depths[l] > n) return DIP_E_INVAL;
+    total += depths[l];
   }
-  if (h->rl_cap < n_rollouts) {
+  if (total > 0 && !prefixes) return DIP_E_INVAL;
+  {
+    std::vector<int32_t> seen(n, -1);
+    int64_t k = 0;
+    for (int32_t l = 0; l < n_leaves; ++l)
+      for (int32_t d = 0; d < depths[l]; ++d, ++k) {
+        const int32_t c = prefixes[k];
+        if (c < 0 || c >= n || seen[c] == l) return DIP_E_INVAL;
+        seen[c] = l;
+      }
+  }
+  if (per_leaf == 0) return DIP_OK;
+  if (per_leaf > INT32_MAX / n_leaves || !out_prio || !out_makespan || !out_flags || !inout_keys)
+    return DIP_E_INVAL;
+  if (reinterpret_cast<uintptr_t>(inout_keys) & 7) return DIP_E_INVAL;
+  const int64_t rows = per_leaf * n_leaves;
+  hipStream_t stream = static_cast<hipStream_t>(stream_);
+  if (h->rl_cap < rows) {
     if (h->d_rl_bub) (void)hipFree(h->d_rl_bub);
     if (h->d_rl_peak) (void)hipFree(h->d_rl_peak);
     h->d_rl_bub = h->d_rl_peak = nullptr;
     h->rl_cap = 0;
-    DIP_HIP(hipMalloc(&h->d_rl_bub, size_t(n_rollouts) * h->P * 4));
-    DIP_HIP(hipMalloc(&h->d_rl_peak, size_t(n_rollouts) * h->P * 4));
-    h->rl_cap = n_rollouts;
+    DIP_HIP(hipMalloc(&h->d_rl_bub, size_t(rows) * h->P * 4));
+    DIP_HIP(hipMalloc(&h->d_rl_peak, size_t(rows) * h->P * 4));
+    h->rl_cap = rows;
   }
-  // the prefix, then the other classes ascending, through pinned staging
+  // per leaf its prefix, then the other classes ascending; then the depths;
+  // through pinned staging
   if (h->rl_seq_pending) {
     DIP_HIP(hipEventSynchronize(h->rl_seq_ev));
     h->rl_seq_pending = false;
   }
-  int32_t k = 0;
-  for (int32_t d = 0; d < depth; ++d) h->h_rl_seq[k++] = prefix[d];
-  for (int32_t c = 0; c < n; ++c)
-    if (!on[c]) h->h_rl_seq[k++] = c;
-  DIP_HIP(hipMemcpyAsync(h->d_rl_seq, h->h_rl_seq, size_t(n) * 4, hipMemcpyHostToDevice, stream));
+  const size_t words = size_t(n_leaves) * size_t(n + 1);
+  if (h->rl_leaf_cap < n_leaves) {
+    DIP_HIP(hipDeviceSynchronize());              // no launch may still read the old buffer
+    if (h->d_rl_seq) (void)hipFree(h->d_rl_seq);
+    if (h->h_rl_seq) (void)hipHostFree(h->h_rl_seq);
+    h->d_rl_seq = h->h_rl_seq = nullptr;
+    h->rl_leaf_cap = 0;
+    DIP_HIP(hipMalloc(&h->d_rl_seq, words * 4));
+    DIP_HIP(hipHostMalloc(reinterpret_cast<void **>(&h->h_rl_seq), words * 4, hipHostMallocDefault));
+    h->rl_leaf_cap = n_leaves;
+  }
+  {
+    std::vector<char> on(n);
+    int64_t k = 0;
+    for (int32_t l = 0; l < n_leaves; ++l) {
+      int32_t *row = h->h_rl_seq + int64_t(l) * n;
+      std::fill(on.begin(), on.end(), 0);
+      int32_t w = 0;
+      for (int32_t d = 0; d < depths[l]; ++d, ++k) {
+        row[w++] = prefixes[k];
+        on[prefixes[k]] = 1;
+      }
+      for (int32_t c = 0; c < n; ++c)
+        if (!on[c]) row[w++] = c;
+      h->h_rl_seq[int64_t(n_leaves) * n + l] = depths[l];
+    }
+  }
+  DIP_HIP(hipMemcpyAsync(h->d_rl_seq, h->h_rl_seq, words * 4, hipMemcpyHostToDevice, stream));
   DIP_HIP(hipEventRecord(h->rl_seq_ev, stream));
   h->rl_seq_pending = true;
   RolloutArgs a{};
-  a.n = n_rollouts;
+  a.n = rows;
+  a.per_leaf = per_leaf;
   a.out_prio = out_prio;
-  a.prefix = h->d_rl_seq;
-  a.rest = h->d_rl_seq + depth;
+  a.seqs = h->d_rl_seq;
+  a.depths = h->d_rl_seq + int64_t(n_leaves) * n;
   a.group_class = h->d_rl_class;
   a.seed = seed;
-  a.draw = draw;
-  a.depth = depth;
-  a.m = n - depth;
+  a.draw = draw_base;
   a.n_classes = n;
   a.G = h->gr_G;
   DIP_HIP(launch_rollout_prio(stream, a));
-  int rc = dip_sim_greedy(h, nullptr, out_prio, n_rollouts, nullptr, out_makespan, h->d_rl_bub,
+  int rc = dip_sim_greedy(h, nullptr, out_prio, rows, nullptr, out_makespan, h->d_rl_bub,
                           h->d_rl_peak, out_flags, stream_);
   if (rc != DIP_OK) return rc;
-  return dip_sim_argmin(h, out_makespan, out_flags, n_rollouts, 0, inout_best_key, stream_);
+  // the best unflagged rollout of each leaf, indexed within the leaf
+  const int64_t want = (per_leaf + 255) / 256;
+  const int blocks = int(std::max<int64_t>(1, std::min<int64_t>(want, int64_t(h->n_cu) * 8 / n_leaves)));
+  DIP_HIP(launch_argmin(blocks, stream, out_makespan, out_flags, rows, per_leaf, n_leaves, 0,
+                        reinterpret_cast<unsigned long long *>(inout_keys)));
+  return DIP_OK;
+}
+
+int dip_sim_rollouts(dip_sim *h, const int32_t *prefix, int32_t depth, int64_t n_rollouts,
+                     uint64_t seed, uint64_t draw, int32_t *out_prio, int32_t *out_makespan,
+                     uint8_t *out_flags, uint64_t *inout_best_key, void *stream_) {
+  if (!h || n_rollouts < 0 || depth < 0) return DIP_E_INVAL;
+  return dip_sim_rollouts_batch(h, 1, &depth, prefix, n_rollouts, seed, draw, out_prio,
+                                out_makespan, out_flags, inout_best_key, stream_);
 }
 
 int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64_t *layer_time,
@@ -1883,7 +1936,7 @@ int dip_sim_argmin(dip_sim *h, const int32_t *makespan, const uint8_t *flags, in
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   const int64_t want = (n_cand + 255) / 256;
   const int blocks = int(std::min<int64_t>(want, int64_t(h->n_cu) * 8));
-  DIP_HIP(launch_argmin(blocks, stream, makespan, flags, n_cand, uint64_t(index_base),
+  DIP_HIP(launch_argmin(blocks, stream, makespan, flags, n_cand, n_cand, 1, uint64_t(index_base),
                         reinterpret_cast<unsigned long long *>(inout_best_key)));
   return DIP_OK;
 }

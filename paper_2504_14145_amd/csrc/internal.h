@@ -270,13 +270,14 @@ hipError_t launch_greedy(int pwl, int nw, bool gring, int blocks, int wpb, size_
 // Random completions of a class prefix (MCTS rollouts) turned into priority
 // vectors (see kern_rollout.hip).
 struct RolloutArgs {
-  int64_t n;                 // rollouts
+  int64_t n;                 // rollouts (rows), all leaves
+  int64_t per_leaf;          // rows per leaf: leaf l has rows l * per_leaf ...
   int32_t *out_prio;         // [n][G] caller-indexed group priorities
-  const int32_t *prefix;     // [depth] classes at positions 0 .. depth-1
-  const int32_t *rest;       // [m] the other classes, ascending
+  const int32_t *seqs;       // [leaves][n_classes]: the leaf's prefix, then the other classes ascending
+  const int32_t *depths;     // [leaves] prefix lengths
   const int32_t *group_class;// [G] caller-indexed
-  uint64_t seed, draw;
-  int32_t depth, m, n_classes, G;
+  uint64_t seed, draw;       // leaf l draws with draw + l
+  int32_t n_classes, G;
 };
 hipError_t launch_rollout_prio(hipStream_t s, const RolloutArgs &a);
 
@@ -316,7 +317,11 @@ hipError_t launch_memopt_wave(int ppl, int waves_per_block, hipStream_t s, const
 size_t memopt_wave_lds(int32_t max_pairs, int waves_per_block);
 
 // ---------------------------------------------------------------- argmin
+// Least (makespan << 32 | base + index) over unflagged rows into *key, per
+// segment of seg_len rows (index counted within the segment; key[s] for
+// segment s); one segment: seg_len = n.
 hipError_t launch_argmin(int blocks, hipStream_t s, const int32_t *ms, const uint8_t *flags,
-                         int64_t n, uint64_t base, unsigned long long *key);
+                         int64_t n, int64_t seg_len, int n_seg, uint64_t base,
+                         unsigned long long *key);
 
 }  // namespace dipsim

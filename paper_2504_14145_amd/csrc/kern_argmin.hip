@@ -10,16 +10,18 @@ namespace {
 // reduction with cross-lane shuffles, block reduction through LDS, then one
 // 64-bit atomic min per block into the caller's running key.
 __global__ __launch_bounds__(256) void argmin_kernel(const int32_t *ms, const uint8_t *flags,
-                                                     int64_t n, uint64_t base,
+                                                     int64_t n, int64_t seg_len, uint64_t base,
                                                      unsigned long long *key) {
   __shared__ unsigned long long s_best[256 / kWave];
   unsigned long long best = ~0ull;
+  const int64_t s0 = int64_t(blockIdx.y) * seg_len;
+  const int64_t s1 = n - s0 < seg_len ? n : s0 + seg_len;
   const int64_t stride = int64_t(gridDim.x) * blockDim.x;
-  for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < n; i += stride) {
+  for (int64_t i = s0 + int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < s1; i += stride) {
     if (flags[i] == 0) {
       const unsigned long long k =
           (static_cast<unsigned long long>(static_cast<uint32_t>(ms[i])) << 32) |
-          static_cast<uint32_t>(base + uint64_t(i));
+          static_cast<uint32_t>(base + uint64_t(i - s0));
       best = k < best ? k : best;
     }
   }
@@ -35,15 +37,17 @@ __global__ __launch_bounds__(256) void argmin_kernel(const int32_t *ms, const ui
   if (threadIdx.x == 0) {
     unsigned long long b = s_best[0];
     for (int w = 1; w < int(blockDim.x / kWave); ++w) b = s_best[w] < b ? s_best[w] : b;
-    if (b != ~0ull) atomicMin(key, b);
+    if (b != ~0ull) atomicMin(key + blockIdx.y, b);
   }
 }
 
 }  // namespace
 
 hipError_t launch_argmin(int blocks, hipStream_t s, const int32_t *ms, const uint8_t *flags,
-                         int64_t n, uint64_t base, unsigned long long *key) {
-  argmin_kernel<<<dim3(blocks), dim3(256), 0, s>>>(ms, flags, n, base, key);
+                         int64_t n, int64_t seg_len, int n_seg, uint64_t base,
+                         unsigned long long *key) {
+  argmin_kernel<<<dim3(unsigned(blocks), unsigned(n_seg)), dim3(256), 0, s>>>(ms, flags, n, seg_len,
+                                                                             base, key);
   return hipGetLastError();
 }
 

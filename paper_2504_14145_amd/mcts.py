@@ -21,9 +21,17 @@ policy "dfs" and "random" are the two exploration strategies the paper
 compares its search with: depth-first (the lowest untried class of the
 deepest node on the current path that has one) and random exploration
 (every batch rolled out from the root); rollouts and backpropagation stay.
+
+workers = W > 1 is Sec. 6.2's parallel search on one GPU: in a round, W
+workers select and expand in turn, each leaving a virtual visit on its path
+for the later ones; one dip_sim_rollouts_batch call rolls out all W nodes;
+their best scores then update the tree in worker order.  Leaves are numbered
+across rounds, and leaf k's expansion and rollout draws use k (W = 1 is the
+sequential search).
 """
 from __future__ import annotations
 
+import bisect
 import math
 
 import numpy as np
@@ -34,7 +42,8 @@ INF = float("inf")
 class Search:
     """One search over the classes of a Sim configured for the greedy."""
 
-    def __init__(self, sim, group_class, rollouts, seed, alpha=1.0, beta=0.1, policy="ucb"):
+    def __init__(self, sim, group_class, rollouts, seed, alpha=1.0, beta=0.1, policy="ucb",
+                 workers=1):
         import torch
 
         from . import configure_rollouts, OK, strerror
@@ -51,25 +60,35 @@ class Search:
             raise ValueError(policy)
         self.policy = policy
         self.cursor = 0                  # dfs: the node expanded last
+        self.W = int(workers)
+        if self.W < 1:
+            raise ValueError(workers)
+        self.leaves = 0                  # leaves so far (names their draws)
+        self.rounds = 0
         self.R = int(rollouts)
         self.seed = int(seed)
         self.alpha, self.beta = float(alpha), float(beta)
         self.draw_child = workloads.expansion_draw
         dev = torch.device("cuda", torch.cuda.current_device())
         G = self.cls_of_group.size
-        self.prio = torch.empty((self.R, G), dtype=torch.int32, device=dev)
-        self.ms = torch.empty(self.R, dtype=torch.int32, device=dev)
-        self.fl = torch.empty(self.R, dtype=torch.uint8, device=dev)
-        self.key = torch.empty(1, dtype=torch.int64, device=dev)
-        # node arrays; node 0 is the root
+        self.prio = torch.empty((self.W * self.R, G), dtype=torch.int32, device=dev)
+        self.ms = torch.empty(self.W * self.R, dtype=torch.int32, device=dev)
+        self.fl = torch.empty(self.W * self.R, dtype=torch.uint8, device=dev)
+        self.key = torch.empty(self.W, dtype=torch.int64, device=dev)
+        # per node (node 0 is the root): parent, class, depth, untried classes
+        # (ascending), children sorted by class (classes, node ids); visits,
+        # best score and done flag in arrays, so that a selection step scores
+        # all children of a node at once
         self.parent = [-1]
         self.cls = [-1]
-        self.visits = [0]
-        self.score = [INF]
-        self.done = [False]
-        self.kids = [{}]
-        self.todo = [list(range(self.n))]
         self.depth = [0]
+        self.todo = [list(range(self.n))]
+        self.kid_cls = [[]]
+        self.kid_ids = [[]]
+        self.nodes = 1
+        self.visits = np.zeros(1024, np.int64)
+        self.score = np.full(1024, INF)
+        self.done = np.zeros(1024, bool)
         self.trajectory = []
         self.best = (INF, None, -1, -1)
 
@@ -81,95 +100,136 @@ class Search:
         return out[::-1]
 
     def _select(self):
+        # the oracle's rule, evaluated per node over all children at once: the
+        # same float64 operations in the same order (division and square root
+        # are correctly rounded; ln N and, unless alpha is 1, the powers are
+        # taken with Python floats), first maximum in class order
         v = 0
-        while not self.todo[v] and self.kids[v]:
-            pick, top = -1, -INF
-            s_root = self.score[0]
-            for c in sorted(self.kids[v]):
-                w = self.kids[v][c]
-                if self.done[w]:
-                    continue
-                s_w = self.score[w]
-                exploit = (s_root / s_w) ** self.alpha if (s_w < INF and s_root < INF) else 0.0
-                u = exploit + self.beta * math.sqrt(math.log(self.visits[v]) / self.visits[w])
-                if u > top:
-                    pick, top = w, u
-            if pick < 0:
+        while not self.todo[v] and self.kid_ids[v]:
+            ids = np.asarray(self.kid_ids[v], np.int64)
+            live = ~self.done[ids]
+            if not live.any():
                 break
-            v = pick
+            s_root = float(self.score[0])
+            s_w = self.score[ids]
+            if s_root < INF:
+                fin = s_w < INF
+                ratio = np.where(fin, s_root / np.where(fin, s_w, 1.0), 0.0)
+                if self.alpha == 1.0:
+                    exploit = ratio
+                else:
+                    exploit = np.array([float(r) ** self.alpha if f else 0.0
+                                        for r, f in zip(ratio, fin)])
+            else:
+                exploit = np.zeros(ids.size)
+            u = exploit + self.beta * np.sqrt(math.log(int(self.visits[v])) / self.visits[ids])
+            u[~live] = -INF
+            v = int(ids[int(np.argmax(u))])
         return v
 
     def _add(self, v, c):
-        w = len(self.parent)
+        w = self.nodes
+        if w == self.visits.size:
+            self.visits = np.concatenate([self.visits, np.zeros(w, np.int64)])
+            self.score = np.concatenate([self.score, np.full(w, INF)])
+            self.done = np.concatenate([self.done, np.zeros(w, bool)])
+        self.nodes += 1
         self.parent.append(v)
         self.cls.append(c)
-        self.visits.append(0)
-        self.score.append(INF)
-        self.done.append(False)
-        self.kids.append({})
         self.depth.append(self.depth[v] + 1)
         on = set(self._path(v))
         on.add(c)
         self.todo.append([k for k in range(self.n) if k not in on])
-        self.kids[v][c] = w
+        self.kid_cls.append([])
+        self.kid_ids.append([])
+        i = bisect.bisect_left(self.kid_cls[v], c)
+        self.kid_cls[v].insert(i, c)
+        self.kid_ids[v].insert(i, w)
         return w
 
     def _finish(self, v):
         while v >= 0:
             if self.depth[v] == self.n or (not self.todo[v] and
-                                           all(self.done[w] for w in self.kids[v].values())):
+                                           bool(np.all(self.done[self.kid_ids[v]]))):
                 self.done[v] = True
                 v = self.parent[v]
             else:
                 break
 
-    def step(self, t):
-        """One iteration (t = its number, which also names its random draws)."""
-        from . import NO_KEY, decode_key, rollouts
-
+    def _pick(self, k):
+        """One worker's node (expanded if need be), or -1 if there is none."""
         if self.policy == "random":
-            v = 0
-        elif self.policy == "dfs":
+            return 0
+        if self.policy == "dfs":
             v = self.cursor
             while v >= 0 and not self.todo[v]:
                 v = self.parent[v]
             if v < 0:
-                self.done[0] = True      # every sequence visited
-                return
+                return -1                # every sequence visited
             c = min(self.todo[v])
             self.todo[v].remove(c)
             v = self.cursor = self._add(v, c)
-        else:
-            v = self._select()
-            if self.todo[v]:
-                c = self.todo[v].pop(self.draw_child(self.seed, t, len(self.todo[v])))
-                v = self._add(v, c)
-        prefix = self._path(v)
-        self.key.fill_(-1)
-        rollouts(self.sim.h, prefix, self.R, self.seed, t, self.prio, self.ms, self.fl, self.key)
-        k = int(self.key.item()) & NO_KEY
-        if k == NO_KEY:
-            sc, idx = INF, -1
-        else:
-            idx, ms = decode_key(k)
-            sc = float(ms)
-        self.trajectory.append((tuple(prefix), sc, idx))
-        if idx >= 0 and sc < self.best[0]:
-            row = self.prio[idx].cpu().numpy()
-            prio_of_class = np.zeros(self.n, np.int64)
-            prio_of_class[self.cls_of_group] = row
-            self.best = (sc, [int(c) for c in np.argsort(-prio_of_class, kind="stable")], t, idx)
-        w = v
-        while w >= 0:
-            self.visits[w] += 1
-            if sc < self.score[w]:
-                self.score[w] = sc
-            w = self.parent[w]
-        self._finish(v)
+            return v
+        v = self._select()
+        if self.todo[v]:
+            c = self.todo[v].pop(self.draw_child(self.seed, k, len(self.todo[v])))
+            v = self._add(v, c)
+        return v
 
-    def run(self, iterations):
-        for t in range(len(self.trajectory), iterations):
+    def step(self, t=None):
+        """One round: up to W leaves, one batch of rollouts."""
+        from . import NO_KEY, decode_key, rollouts_batch
+
+        self.rounds += 1
+        picked = []
+        for _ in range(self.W):
             if self.done[0]:
                 break
-            self.step(t)
+            v = self._pick(self.leaves)
+            if v < 0:
+                self.done[0] = True
+                break
+            w = v
+            while w >= 0:                # the (virtual) visit
+                self.visits[w] += 1
+                w = self.parent[w]
+            if self.depth[v] == self.n:
+                self._finish(v)          # a complete sequence: nothing below it
+            picked.append((v, self.leaves))
+            self.leaves += 1
+        if not picked:
+            return
+        prefixes = [self._path(v) for v, _ in picked]
+        L = len(picked)
+        self.key[:L].fill_(-1)
+        rollouts_batch(self.sim.h, prefixes, self.R, self.seed, picked[0][1], self.prio,
+                       self.ms, self.fl, self.key)
+        keys = self.key[:L].cpu().tolist()
+        for (v, k), prefix, key in zip(picked, prefixes, keys):
+            key &= NO_KEY
+            if key == NO_KEY:
+                sc, idx = INF, -1
+            else:
+                idx, ms = decode_key(key)
+                sc = float(ms)
+            self.trajectory.append((tuple(prefix), sc, idx))
+            if idx >= 0 and sc < self.best[0]:
+                l = k - picked[0][1]
+                row = self.prio[l * self.R + idx].cpu().numpy()
+                prio_of_class = np.zeros(self.n, np.int64)
+                prio_of_class[self.cls_of_group] = row
+                self.best = (sc, [int(c) for c in np.argsort(-prio_of_class, kind="stable")], k,
+                             idx)
+            w = v
+            while w >= 0:
+                if sc < self.score[w]:
+                    self.score[w] = sc
+                w = self.parent[w]
+            self._finish(v)
+
+    def run(self, rounds):
+        """Run rounds until ``rounds`` have been made in all (or the tree is
+        exhausted); returns (trajectory, best), one trajectory entry per leaf."""
+        while self.rounds < rounds and not self.done[0]:
+            self.step()
         return self.trajectory, self.best

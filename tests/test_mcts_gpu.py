@@ -127,3 +127,67 @@ def test_other_policies_match_oracle(case, policy):
     if case == "tiny" and policy == "dfs":
         assert len(traj) == 64 and srch.done[0]
     sim.close()
+
+
+def test_rollouts_batch_equals_one_call_per_leaf():
+    """dip_sim_rollouts_batch: leaf l's rows and key are those of
+    dip_sim_rollouts on its prefix with draw_base + l; ragged prefixes
+    (empty, partial, complete), and the oracle's shuffles."""
+    need_gpu()
+    prob = W.make_problem(2)
+    sim, g, G, cls = _sim(prob)
+    n = int(cls.max()) + 1
+    assert dip.configure_rollouts(sim.h, n, cls) == dip.OK
+    rng = np.random.default_rng(3)
+    perm = [int(c) for c in rng.permutation(n)]
+    prefixes = [[], perm[:5], perm[:n], [perm[7]], perm[:n - 1]]
+    L, R = len(prefixes), 37
+    prio = torch.empty((L * R, G), dtype=torch.int32, device=DEV)
+    ms = torch.empty(L * R, dtype=torch.int32, device=DEV)
+    fl = torch.empty(L * R, dtype=torch.uint8, device=DEV)
+    keys = torch.full((L,), -1, dtype=torch.int64, device=DEV)
+    print(f"batch of {L} leaves x {R}", flush=True)
+    dip.rollouts_batch(sim.h, prefixes, R, 99, 40, prio, ms, fl, keys)
+    torch.cuda.synchronize()
+    want = []
+    for l, p in enumerate(prefixes):
+        rest = [c for c in range(n) if c not in set(p)]
+        want += [OM.priorities_of(p + OM.shuffled(rest, 99, 40 + l, i), cls, n) for i in range(R)]
+    want = np.stack(want)
+    np.testing.assert_array_equal(prio.cpu().numpy(), want)
+    _, res = O.greedy(prob, g, G, want, threads=16)
+    np.testing.assert_array_equal(ms.cpu().numpy(), res.makespan)
+    np.testing.assert_array_equal(fl.cpu().numpy(), res.flags)
+    for l in range(L):
+        seg = slice(l * R, (l + 1) * R)
+        assert dip.decode_key(int(keys[l].item())) == O.argmin(res.makespan[seg], res.flags[seg])
+        one = torch.full((1,), -1, dtype=torch.int64, device=DEV)
+        dip.rollouts(sim.h, prefixes[l], R, 99, 40 + l, prio[:R], ms[:R], fl[:R], one)
+        torch.cuda.synchronize()
+        assert int(one.item()) == int(keys[l].item())
+    with pytest.raises(dip.DipSimError):
+        dip.rollouts_batch(sim.h, [[0], [1, 1]], R, 1, 0, prio, ms, fl, keys)   # repeated class
+    sim.close()
+
+
+@pytest.mark.parametrize("case,workers,policy", [("tiny", 5, "ucb"), ("c1", 8, "ucb"),
+                                                 ("c2", 16, "ucb"), ("c3", 4, "ucb"),
+                                                 ("c2", 6, "dfs"), ("c2", 3, "random")])
+def test_parallel_search_matches_oracle(case, workers, policy):
+    """W workers per round with virtual visits: trajectories equal the oracle's."""
+    need_gpu()
+    prob = _tiny() if case == "tiny" else W.make_problem(int(case[1]))
+    rounds, R = {"tiny": (30, 3), "c1": (8, 16), "c2": (5, 64), "c3": (2, 8)}[case]
+    sim, g, G, cls = _sim(prob)
+    print(f"{case} {policy} x{workers}: {rounds} rounds x {R} rollouts", flush=True)
+    srch = Search(sim, cls, R, seed=13, policy=policy, workers=workers)
+    traj, best = srch.run(rounds)
+    want_traj, want_best, root = OM.search(prob, g, G, cls, rounds, R, seed=13, threads=16,
+                                           policy=policy, workers=workers)
+    assert traj == want_traj
+    assert best[0] == want_best[0] and best[2:] == want_best[2:]
+    if want_best[1] is not None:
+        assert best[1] == list(want_best[1])
+    if case == "tiny":
+        assert srch.done[0] and len(traj) == 64
+    sim.close()
