@@ -90,6 +90,32 @@ def measured_traffic(workload: str, n_cand: int, slots: int, path: str = TRAFFIC
     return None
 
 
+N_SIMD = 1024          # 256 CUs x 4 SIMDs
+N_XCD = 8
+VALU_CYCLES = 4        # a wave-wide vector instruction on a 16-lane SIMD
+
+
+def measured_issue(workload: str, n_cand: int, slots: int, path: str = TRAFFIC_FILE,
+                   sources=POOL_SOURCES):
+    """Share of the launch the SIMDs spent issuing vector instructions, from
+    the committed counter summary (SQ_INSTS_VALU x 4 cycles over 1,024 SIMDs
+    and GRBM_GUI_ACTIVE / 8 cycles), if taken on this kernel source, workload,
+    batch and size parameter."""
+    if not os.path.exists(path):
+        return None
+    want = f"{source_hash(sources)} {workload} {n_cand} {slots}"
+    for line in open(path):
+        m = re.match(r"\s*issue:\s*(\S+ \S+ \d+ \d+)\s+valu_insts=(\d+)\s+salu_insts=(\d+)"
+                     r"\s+gui_active=(\d+)", line)
+        if m and m.group(1) == want:
+            valu, salu, gui = int(m.group(2)), int(m.group(3)), int(m.group(4))
+            cycles = gui / N_XCD
+            return {"valu_busy": valu * VALU_CYCLES / (N_SIMD * cycles), "valu_insts": valu,
+                    "salu_insts": salu, "cycles": cycles,
+                    "source": os.path.relpath(path, ROOT)}
+    return None
+
+
 def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
@@ -321,6 +347,8 @@ def main():
         "roofline": {"bound": "hbm", "kernel": "simulate", "achieved": achieved_gbs,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved_gbs / HBM_PEAK_GBS,
                      "traffic": traffic, "algorithmic_bytes": algo_bytes},
+        # the kernel's measured bound: vector issue (from the committed counters)
+        "issue": measured_issue(cfg.name, n_cand, slots) if info["variant"] == 8 else None,
         "cpu_baseline": cpu,
     }
     if stream_rec is not None:
@@ -449,6 +477,8 @@ def run_greedy(args, cfg):
                      "traffic": measured_traffic(cfg.name, n_cand, info["greedy_inbox"],
                                                  GREEDY_TRAFFIC_FILE, GREEDY_SOURCES),
                      "algorithmic_bytes": algo_bytes},
+        "issue": measured_issue(cfg.name, n_cand, info["greedy_inbox"], GREEDY_TRAFFIC_FILE,
+                                GREEDY_SOURCES),
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
