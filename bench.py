@@ -61,6 +61,10 @@ GREEDY_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "greedy_kernel_traffic.md")
 CSRC = os.path.join(ROOT, "paper_2504_14145_amd", "csrc")
 POOL_SOURCES = [os.path.join(CSRC, f) for f in ("kern_pool.hip", "internal.h", "dev_util.h")]
 GREEDY_SOURCES = [os.path.join(CSRC, f) for f in ("kern_greedy.hip", "internal.h", "dev_util.h")]
+MEMOPT_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "memopt_wave_kernel_traffic.md")
+MEMOPT_SOURCES = [os.path.join(CSRC, f) for f in ("kern_memopt.hip", "internal.h", "dev_util.h")]
+COST_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "cost_table_kernel_traffic.md")
+COST_SOURCES = [os.path.join(CSRC, "kern_costmodel.hip"), os.path.join(ROOT, "include", "dip_sim.h")]
 
 
 def source_hash(files) -> str:
@@ -114,6 +118,20 @@ def measured_issue(workload: str, n_cand: int, slots: int, path: str = TRAFFIC_F
                     "salu_insts": salu, "cycles": cycles,
                     "source": os.path.relpath(path, ROOT)}
     return None
+
+
+def calib_copies(args, dev):
+    """Plain device copies of args.calib_copy_mib MiB (a kernel of known size
+    for scaling HBM byte counters), after the timed work."""
+    import torch
+    if args.calib_copy_mib:
+        nb = args.calib_copy_mib << 20
+        src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copies: 3 x {nb} bytes")
 
 
 def log(msg):
@@ -255,14 +273,7 @@ def main():
     dom_s = kern_avg_ms[dom] / 1e3
     log(f"[bench] per-kernel avg ms: " + ", ".join(f"{n} {t:.4f}" for n, t in zip(names, kern_avg_ms)))
 
-    if args.calib_copy_mib:
-        nb = args.calib_copy_mib << 20
-        src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"[bench] calibration copies: 3 x {nb} bytes")
+    calib_copies(args, dev)
 
     stream_rec = None
     if args.stream:
@@ -417,14 +428,7 @@ def run_greedy(args, cfg):
         ", ".join(f"{n} {t:.4f}" for n, t in zip(names, kern_avg_ms)) +
         f"; inbox {info['greedy_inbox']}; best {best}; cap {np.mean(flags & 2 > 0):.3f}")
 
-    if args.calib_copy_mib:
-        nb = args.calib_copy_mib << 20
-        src = torch.empty(nb, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"[bench] calibration copies: 3 x {nb} bytes")
+    calib_copies(args, dev)
 
     P = prob.n_ranks
     # per candidate: its priority vector read, its orders and scores written
@@ -532,6 +536,7 @@ def run_memopt(args, cfg):
     st = s_out.cpu().numpy()
     log(f"[bench] {args.steps} steps in {wall * 1e3:.2f} ms; kernel {k_s * 1e3:.3f} ms; "
         f"within cap {np.mean(st == 1):.3f}, out of reach {np.mean(st == 0):.3f}")
+    calib_copies(args, dev)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -572,7 +577,10 @@ def run_memopt(args, cfg):
         "roofline": {"bound": "hbm", "kernel": "memopt",
                      "achieved": n_cand * bytes_per / k_s / 1e9, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": n_cand * bytes_per / k_s / 1e9 / HBM_PEAK_GBS,
-                     "traffic": None, "algorithmic_bytes": n_cand * bytes_per},
+                     "traffic": measured_traffic(cfg.name, n_cand, S, MEMOPT_TRAFFIC_FILE,
+                                                 MEMOPT_SOURCES),
+                     "algorithmic_bytes": n_cand * bytes_per},
+        "issue": measured_issue(cfg.name, n_cand, S, MEMOPT_TRAFFIC_FILE, MEMOPT_SOURCES),
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
@@ -619,6 +627,7 @@ def run_cost(args, cfg):
     ops = 6.0 * rows * n_conf        # per row: three products, two maxima, one sum
     log(f"[bench] {args.steps} steps in {wall * 1e3:.2f} ms; kernel {k_s * 1e3:.3f} ms; "
         f"{ops / k_s / 1e12:.2f} T float64 ops/s")
+    calib_copies(args, dev)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -655,8 +664,11 @@ def run_cost(args, cfg):
         "kernel_us": {"cost_table": k_s * 1e6},
         "roofline": {"bound": "alu", "kernel": "cost_table", "achieved": ops / k_s / 1e12,
                      "peak": FP64_OPS_PEAK / 1e12, "unit": "T float64 ops/s",
-                     "frac": ops / k_s / FP64_OPS_PEAK, "traffic": None,
+                     "frac": ops / k_s / FP64_OPS_PEAK,
+                     "traffic": measured_traffic(cfg.name, n_conf, N_KINDS, COST_TRAFFIC_FILE,
+                                                 COST_SOURCES),
                      "algorithmic_bytes": n_conf * items * 4 + coef_np.nbytes + rows * 25},
+        "issue": measured_issue(cfg.name, n_conf, N_KINDS, COST_TRAFFIC_FILE, COST_SOURCES),
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
@@ -727,6 +739,8 @@ def run_mcts(args, cfg):
     log(f"[bench] {args.steps} rounds of {args.workers} leaves in {wall * 1e3:.1f} ms; batch "
         f"{batch_ms:.3f} ms (greedy kernels {k_ms}); best makespan mcts {mcts_best} vs random "
         f"{best_rand} after {search.leaves * R} rollouts each")
+    inbox = sim.info["greedy_inbox"]
+    calib_copies(args, dev)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -767,6 +781,7 @@ def run_mcts(args, cfg):
                    "priority_groups": G, "stages_per_candidate": prob.n_total,
                    "parallelism": "single GPU"},
         "batch_ms": batch_ms,
+        "greedy_inbox": inbox,
         "kernel_us": {n: t * 1e3 for n, t in zip(["greedy", "greedy_retry"], k_ms)},
         "search": {"rounds": iters, "workers": args.workers, "rollouts_each": search.leaves * R,
                    "mcts_best_makespan_us": mcts_best, "random_best_makespan_us": best_rand},
@@ -774,7 +789,10 @@ def run_mcts(args, cfg):
                      "achieved": R * bytes_per_rollout / (greedy_ms / 1e3) / 1e9,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": R * bytes_per_rollout / (greedy_ms / 1e3) / 1e9 / HBM_PEAK_GBS,
-                     "traffic": None, "algorithmic_bytes": R * bytes_per_rollout},
+                     "traffic": measured_traffic(cfg.name, R, inbox, GREEDY_TRAFFIC_FILE,
+                                                 GREEDY_SOURCES),
+                     "algorithmic_bytes": R * bytes_per_rollout},
+        "issue": measured_issue(cfg.name, R, inbox, GREEDY_TRAFFIC_FILE, GREEDY_SOURCES),
         "cpu_baseline": cpu,
     }
     print(json.dumps(rec), flush=True)
