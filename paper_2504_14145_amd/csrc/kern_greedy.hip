@@ -248,6 +248,9 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
         set_kind(eF, eB, g < GF ? 0u : 1u, gpos[g]);
       }
     }
+    // first (best) position in each E, kept up to date: an entry moving in
+    // can only lower it; the commit that takes it scans again
+    uint32_t eF1 = first_in(eF), eB1 = first_in(eB);
     wave_sync();
 
     uint32_t t_last = 0, last_kind = 0, n_emit = 0;
@@ -269,13 +272,17 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
       for (; nF > 0; ++hF, --nF) {
         frF = ringF[hF & mask];
         if (uint32_t(frF >> 17) >= t_last) break;
-        set_kind(eF, eB, 0u, uint32_t(frF >> 1) & 0xffffu);
+        const uint32_t p = uint32_t(frF >> 1) & 0xffffu;
+        set_kind(eF, eB, 0u, p);
+        eF1 = min(eF1, p);
         frF = ~uint64_t(0);
       }
       for (; nB > 0; ++hB, --nB) {
         frB = ringB[hB & mask];
         if (uint32_t(frB >> 17) >= t_last) break;
-        set_kind(eF, eB, 1u, uint32_t(frB >> 1) & 0xffffu);
+        const uint32_t p = uint32_t(frB >> 1) & 0xffffu;
+        set_kind(eF, eB, 1u, p);
+        eB1 = min(eB1, p);
         frB = ~uint64_t(0);
       }
       const uint32_t cF = (hF & 0xffffu) | (nF << 16), cB = (hB & 0xffffu) | (nB << 16);
@@ -286,7 +293,7 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
       const uint32_t ppB = nB ? uint32_t(frB >> 1) & 0xffffu : kNoPos;
 
       // ---- 2. this rank's choice
-      const uint32_t fF = first_in(eF), fB = first_in(eB);
+      const uint32_t fF = eF1, fB = eB1;
       const bool xF = fF != kNoPos && t_last > 0, xB = fB != kNoPos && t_last > 0;
       // the best stage of each kind able to start at tau: E's first (E is
       // non-empty only when tau == t_last) or the inbox front if due then
@@ -352,8 +359,13 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
         if (forced) fetch(c);
         const uint32_t end = c.tau + uint32_t(q0.x);
         if (c.slot == 0) {
-          if (c.kind) eB.clear(c.pos);
-          else eF.clear(c.pos);
+          if (c.kind) {
+            eB.clear(c.pos);
+            eB1 = first_in(eB);
+          } else {
+            eF.clear(c.pos);
+            eF1 = first_in(eF);
+          }
         } else {
           // the kind's inbox front: one step on
           const uint32_t hw = hcw[2 * r + c.kind];
