@@ -95,6 +95,8 @@ def test_null_pointers_rejected():
     assert lib.dip_sim_evaluate(None, None, None, 0, None, None, None, None, None) == dip.E_INVAL
     assert lib.dip_sim_argmin(None, None, None, 0, 0, None, None) == dip.E_INVAL
     assert lib.dip_sim_set_greedy_inbox(None, 8) == dip.E_INVAL
+    assert lib.dip_sim_rollouts_batch(None, 1, None, None, 4, 0, 0, None, None, None, None,
+                                      None) == dip.E_INVAL
     lib.dip_sim_destroy(None)     # no-op
 
 
