@@ -40,6 +40,23 @@ __device__ __forceinline__ void lds_sync_wave() {
   __builtin_amdgcn_wave_barrier();
 }
 
+// min / max of one value over the 64 lanes of a wave, read out of lane 63:
+// the row reduction of dpp_row, then the row broadcasts (lane 15 of each row
+// into the next row, lane 31 into rows 2 and 3), rows outside the mask
+// keeping their value (the identity as the old value)
+template <bool MAX>
+__device__ __forceinline__ uint32_t wave_reduce63(uint32_t v) {
+  auto op = [](uint32_t x, uint32_t y) { return MAX ? max(x, y) : min(x, y); };
+  constexpr int kId = MAX ? 0 : -1;
+  v = op(v, dpp_row<0xb1>(v));    // quad_perm [1,0,3,2]
+  v = op(v, dpp_row<0x4e>(v));    // quad_perm [2,3,0,1]
+  v = op(v, dpp_row<0x141>(v));   // row_half_mirror
+  v = op(v, dpp_row<0x140>(v));   // row_mirror
+  v = op(v, uint32_t(__builtin_amdgcn_update_dpp(kId, int(v), 0x142, 0xa, 0xf, false)));  // row_bcast:15
+  v = op(v, uint32_t(__builtin_amdgcn_update_dpp(kId, int(v), 0x143, 0xc, 0xf, false)));  // row_bcast:31
+  return uint32_t(__builtin_amdgcn_readlane(int(v), 63));
+}
+
 __device__ __forceinline__ void write_out(const MemoptArgs &a, int64_t o, int64_t t, int32_t pk,
                                           uint8_t st) {
   a.out_time[o] = t;
@@ -229,7 +246,7 @@ __global__ __launch_bounds__(256) void memopt_wave_kernel(MemoptArgs a) {
 #pragma unroll
       for (int q = 0; q < PPL; ++q)
         if (lane + 64 * q < np) mx = max(mx, uint32_t(load[q]) ^ 0x80000000u);
-      mx = wave_max_u32(mx);
+      mx = wave_reduce63<true>(mx);
       const int32_t top = int32_t(mx ^ 0x80000000u);
       if (np == 0 || top <= cap) break;
       // its forward position: the lowest pair index holding that load
@@ -248,24 +265,20 @@ __global__ __launch_bounds__(256) void memopt_wave_kernel(MemoptArgs a) {
 #pragma unroll
       for (int q = 0; q < PPL; ++q)
         if (pf[q] <= pfk && pfk <= pb[q]) m = min(m, key[q]);
-      m = wave_min_u32(m);
+      m = wave_reduce63<false>(m);
       if (m == kMemoptNoMove) {
         ok = false;
         break;
       }
       const int32_t bi = int32_t(m & ((1u << kMemoptPairBits) - 1));
       const int qb = bi >> 6, ob = bi & 63;
-      uint32_t spf = 0, spb = 0;
+      // the moved pair's positions from the wave's tables, its freed memory
+      // from its owner lane
+      const uint32_t spf = pfa[bi], spb = pba[bi];
       int32_t sdm = 0;
 #pragma unroll
       for (int q = 0; q < PPL; ++q)
-        if (q == qb) {
-          spf = pf[q];
-          spb = pb[q];
-          sdm = dm[q];
-        }
-      spf = uint32_t(__builtin_amdgcn_readlane(int(spf), ob));
-      spb = uint32_t(__builtin_amdgcn_readlane(int(spb), ob));
+        if (q == qb) sdm = dm[q];
       sdm = __builtin_amdgcn_readlane(sdm, ob);
       // every checkpoint the moved pair is live at drops; its owner steps on
 #pragma unroll
@@ -290,7 +303,7 @@ __global__ __launch_bounds__(256) void memopt_wave_kernel(MemoptArgs a) {
       pk = max(pk, uint32_t(load[q]) ^ 0x80000000u);
     }
   }
-  pk = wave_max_u32(pk);
+  pk = wave_reduce63<true>(pk);
 #pragma unroll
   for (int s = 1; s < 64; s <<= 1)
     total += (int64_t(__shfl_xor(int(total >> 32), s)) << 32) |
