@@ -172,7 +172,9 @@ struct PoolArgs {
   uint32_t tab_edges;             // tables in LDS: byte offset of the extra edges
   uint32_t pool_base;             // byte offset of the pools in LDS
   uint32_t *next_cand;            // null: slot k takes k, k + n_slots, ...; else a
-                                  // counter of the candidates handed out past n_slots
+                                  // counter of those handed out on demand
+  int64_t static_end;             // with next_cand: candidates below it (a multiple of
+                                  // n_slots) go to fixed successors, the rest on demand
 };
 
 // dword 3 of a raw buffer descriptor on CDNA

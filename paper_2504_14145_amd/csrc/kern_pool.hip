@@ -218,16 +218,19 @@ __global__ __launch_bounds__(TAB ? 512 : 256) void pool_kernel(PoolArgs a) {
   uint64_t sb = 0;     // a row block, for lanes that entered a new block
   bool take_rec = false, take_edge = false, take_blk = false;
 
-  // Candidates: group slot k (of n_slots) starts on candidate k; the later
-  // ones are either its fixed successors k + n_slots, k + 2 n_slots, ... or,
-  // with a.next_cand, handed out in the order groups ask for them.  All lanes
-  // of the group call this together.
+  // Candidates: group slot k (of n_slots) starts on candidate k and goes on
+  // with its fixed successors k + n_slots, k + 2 n_slots, ...; with
+  // a.next_cand, the candidates from a.static_end (a multiple of n_slots) are
+  // handed out instead in the order groups ask for them, which evens out
+  // slots that drew long candidates.  All lanes of the group call this
+  // together.
   auto next_cand = [&]() -> int64_t {
-    if (!a.next_cand) return cand + n_slots;
+    const int64_t succ = cand + n_slots;
+    if (!a.next_cand || succ < a.static_end) return succ;
     uint32_t k = 0;
     if (r == 0) k = atomicAdd(a.next_cand, 1u);
     k = uint32_t(__shfl(int(k), gbit, kWave));
-    return n_slots + int64_t(k);
+    return a.static_end + int64_t(k);
   };
   // All lanes of the group call this together.
   auto start_candidate = [&]() {
