@@ -491,6 +491,10 @@ int ensure_retry(dip_sim *h, int64_t n) {
   return DIP_OK;
 }
 
+// tables (records, extra edges) up to this size go to each block's LDS,
+// beside the pools of up to 16 waves
+constexpr int64_t kPoolTabLimit = 131072;
+
 struct Pick {
   int v = 0, wpb = 0, nb = 0, waves = 0;
 };
@@ -498,9 +502,9 @@ struct Pick {
 Pick best_of(dip_sim *h, int v_lo, int v_hi, int forced_wpb) {
   Pick best;
   for (int v = v_lo; v <= v_hi; ++v) {
-    for (int w : {8, 4, 2, 1}) {
+    for (int w : {16, 8, 4, 2, 1}) {
       if (forced_wpb && w != forced_wpb) continue;
-      if (w == 8 && !(v == 8 && h->pool_tab)) continue;   // only the tables-in-LDS pool kernel
+      if (w >= 8 && !(v == 8 && h->pool_tab)) continue;   // only the tables-in-LDS pool kernel
       const int nb = blocks_per_cu(h, v, w);
       if (nb <= 0) continue;
       const int waves = nb * w;
@@ -987,7 +991,7 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
     h->n_extra = int32_t(std::min<int64_t>(extra, INT32_MAX));
     // small tables go to each block's LDS, read once per block
     const int64_t tab = align16(int64_t(h->N) * 16) + align16(int64_t(std::max(h->n_extra, 1)) * 8);
-    h->pool_tab = h->pool_ok && tab <= kPoolTabMax;
+    h->pool_tab = h->pool_ok && tab <= kPoolTabLimit;
     h->pool_tab_bytes = h->pool_tab ? tab : 0;
     h->join_of.assign(h->N, -1);
     h->feeds_join.assign(h->N, -1);

@@ -79,7 +79,7 @@ __device__ __forceinline__ void lds_sub(uint32_t addr, uint32_t v) {
 // TAB: the record and extra-edge tables are copied into the block's LDS (small
 // topologies), ahead of the pools; otherwise they are read from global memory.
 template <int PWL, int S, bool TAB>
-__global__ __launch_bounds__(TAB ? 512 : 256) void pool_kernel(PoolArgs a) {
+__global__ __launch_bounds__(TAB ? 1024 : 256) void pool_kernel(PoolArgs a) {
   constexpr int PW = 1 << PWL;
   constexpr int G = kWave / PW;
   constexpr int kC = int(pool_count_words(S));   // count words per pool
