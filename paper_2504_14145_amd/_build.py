@@ -28,9 +28,26 @@ def hipcc() -> str:
     return "hipcc"
 
 
-def build() -> str:
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-I", INCLUDE, "-I", CSRC, "-o", tmp, *SOURCES]
-    subprocess.check_call(cmd)
+def build(jobs: int | None = None) -> str:
+    """Each source to an object in parallel (the translation units share no
+    device code), then one link into the shared library."""
+    import concurrent.futures
+    import tempfile
+
+    cc = hipcc()
+    compile_flags = [f for f in HIPCC_FLAGS if f != "-shared"]
+    jobs = jobs or max(1, min(8, os.cpu_count() or 1))
+    with tempfile.TemporaryDirectory(prefix="dip_sim_build_") as tmpdir:
+        objs = [os.path.join(tmpdir, os.path.basename(src) + ".o") for src in SOURCES]
+
+        def compile_one(src_obj):
+            src, obj = src_obj
+            subprocess.check_call([cc, *compile_flags, "-I", INCLUDE, "-I", CSRC, "-c", src,
+                                   "-o", obj])
+
+        with concurrent.futures.ThreadPoolExecutor(max_workers=jobs) as ex:
+            list(ex.map(compile_one, zip(SOURCES, objs)))
+        tmp = LIB + ".tmp"
+        subprocess.check_call([cc, "--offload-arch=gfx950", "-fPIC", "-shared", "-o", tmp, *objs])
     os.replace(tmp, LIB)
     return LIB
