@@ -1,0 +1,54 @@
+"""bench.py's host-side contract, on the CPU: one GPU only, and the
+committed counter summaries it reads (traffic and vector issue per launch),
+taken only when they match the kernel's sources, workload, batch and size."""
+import glob
+import json
+import os
+import re
+import subprocess
+import sys
+
+import bench
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_more_than_one_gpu_is_refused():
+    p = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=120)
+    assert p.returncode == 2
+    msg = json.loads(p.stdout.strip().splitlines()[-1])
+    assert "one GPU" in msg["error"]
+
+
+def test_summaries_are_read_only_for_their_sources(tmp_path):
+    src = tmp_path / "kern.hip"
+    src.write_text("// a kernel\n")
+    h = bench.source_hash([str(src)])
+    summary = tmp_path / "summary.md"
+    summary.write_text(f"notes\n\ntraffic: {h} wl 1024 8 fetch_bytes=100 write_bytes=20\n"
+                       f"issue: {h} wl 1024 8 valu_insts=4096 salu_insts=10 gui_active=8192\n")
+    assert bench.measured_traffic("wl", 1024, 8, str(summary), [str(src)]) == 120
+    iss = bench.measured_issue("wl", 1024, 8, str(summary), [str(src)])
+    # 4096 instructions x 4 cycles over 1,024 SIMDs and 8192 / 8 cycles
+    assert abs(iss["valu_busy"] - 4096 * 4 / (1024 * 1024)) < 1e-12
+    assert bench.measured_traffic("wl", 2048, 8, str(summary), [str(src)]) is None
+    assert bench.measured_traffic("wl", 1024, 16, str(summary), [str(src)]) is None
+    src.write_text("// the kernel changed\n")
+    assert bench.measured_traffic("wl", 1024, 8, str(summary), [str(src)]) is None
+    assert bench.measured_issue("wl", 1024, 8, str(summary), [str(src)]) is None
+
+
+def test_committed_summary_lines_parse():
+    found = 0
+    for path in glob.glob(os.path.join(ROOT, "profiles", "*.md")):
+        for line in open(path):
+            if line.startswith("traffic:"):
+                assert re.match(r"traffic: [0-9a-f]{16} \S+ \d+ \d+ fetch_bytes=\d+ write_bytes=\d+$",
+                                line.strip()), (path, line)
+                found += 1
+            elif line.startswith("issue:"):
+                assert re.match(r"issue: [0-9a-f]{16} \S+ \d+ \d+ valu_insts=\d+ salu_insts=\d+ "
+                                r"gui_active=\d+$", line.strip()), (path, line)
+                found += 1
+    assert found >= 10
