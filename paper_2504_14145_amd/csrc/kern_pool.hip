@@ -116,7 +116,6 @@ __global__ __launch_bounds__(TAB ? 1024 : 256) void pool_kernel(PoolArgs a) {
   uint32_t rnd = 0;          // rounds so far
   uint32_t cand_round = 0;   // round at which the group took its candidate
   bool has = false;   // the group holds a candidate
-  bool act = false;   // this lane has an op to run
   uint8_t fl = 0;     // the check kernel's flags for the candidate
   int ptr = 0;
   uint32_t tfree = 0, acc = 0;
@@ -130,7 +129,6 @@ __global__ __launch_bounds__(TAB ? 1024 : 256) void pool_kernel(PoolArgs a) {
   int4 cur = make_int4(0, 0, 0, 0);
   int2 ce = dead_edge;                    // current edge {pred edge word, comm}
   uint32_t ea = 0;                        // byte offset of the op's next extra edge
-  int4 n0 = cur;                          // record of the op at ptr + 1
   // ids come from 8-byte blocks of the row (4 ids): blk holds the block with
   // the id at ptr + 2 (the order's last id past its end), nblk the block
   // after it, loaded when the lane entered blk
@@ -183,14 +181,12 @@ __global__ __launch_bounds__(TAB ? 1024 : 256) void pool_kernel(PoolArgs a) {
   // the table starts at its rank's first op)
   const unsigned char *rec_lane = p_lds + 16u * uint32_t(rb);
   const uint32_t rec_lane_off = 16u * uint32_t(rb);
-  // (for lanes with nothing to fetch: LDS reads the lane's first record;
-  // global reads the table's first record, one line shared by all such lanes)
-  auto rec_of = [&](bool fetch, uint32_t id) {
+  auto rec_of = [&](uint32_t id) {
     if constexpr (TAB) {
-      const uint4 v = *reinterpret_cast<const uint4 *>(rec_lane + 16u * (fetch ? id : 0u));
+      const uint4 v = *reinterpret_cast<const uint4 *>(rec_lane + 16u * id);
       return make_int4(int(v.x), int(v.y), int(v.z), int(v.w));
     } else {
-      return rec_at_off(fetch ? rec_lane_off + 16u * id : 0u);
+      return rec_at_off(rec_lane_off + 16u * id);
     }
   };
   auto edge_at = [&](uint32_t off) {   // byte offset
@@ -206,17 +202,19 @@ __global__ __launch_bounds__(TAB ? 1024 : 256) void pool_kernel(PoolArgs a) {
   auto first_edge = [](const int4 &rc) { return make_int2(rc.z, rc.y); };
   auto extra_off = [](const int4 &rc) { return (uint32_t(rc.w) >> 16) * 8u; };
 
-  // Loads are staged: every round every lane issues the same loads into the
-  // staging registers below (lanes with nothing to fetch read one shared
-  // line), and a later point takes what was fetched: the next edge at the top
-  // of the next round, the record just before the next round's state update,
-  // the row block at the end of the next round (the order in which they are
-  // issued keeps each of those waits off the younger loads), so no round
-  // waits for a load it issued itself.
-  int4 s0 = n0;
+  // Loads are staged, so that no round waits for a load it issued itself:
+  // the next edge and a row block are fetched by every lane (lanes with none
+  // to fetch read the table's first entry, resp. one shared block) and taken
+  // at the top of the next round, resp. at its end; the record of the op at
+  // ptr + 1 is fetched only by the lanes that advanced, into a register that
+  // keeps its value otherwise, and first used by the next round's state
+  // update (the order in which they are issued keeps each of those waits off
+  // the younger loads).  (A block fetched under the lane mask would need a
+  // second register and a wait for the load just issued.)
+  int4 s0 = cur;       // record of the op at ptr + 1
   int2 se = no_edge;
   uint64_t sb = 0;     // a row block, for lanes that entered a new block
-  bool take_rec = false, take_edge = false, take_blk = false;
+  bool take_edge = false, take_blk = false;
 
   // Candidates: group slot k (of n_slots) starts on candidate k and goes on
   // with its fixed successors k + n_slots, k + 2 n_slots, ...; with
@@ -236,15 +234,14 @@ __global__ __launch_bounds__(TAB ? 1024 : 256) void pool_kernel(PoolArgs a) {
   auto start_candidate = [&]() {
     while (cand < a.n_cand && (a.out_flags[cand] & DIP_FLAG_INVALID)) cand = next_cand();
     has = cand < a.n_cand;
-    act = false;
     ce = dead_edge;
-    take_rec = false;
+    ea = 0;   // (lanes on the dead edge fetch edges at ea)
     take_edge = false;
     take_blk = false;
-    if (!has) return;
-    fl = a.out_flags[cand];
-    cand_round = rnd;
-    if (on) {   // counts and tags cleared (ends are read only under a tag)
+    // counts and tags cleared (ends are read only under a tag), also by a
+    // group left without a candidate: its lanes sit on the dead edge and
+    // compare its tag with rank 0's, which must then hold no stale data
+    if (on) {
 #pragma unroll
       for (int i = 0; i < kC; ++i) st32(my_cnt + 4u * i, 0u);
       if constexpr (S == 4) {
@@ -255,6 +252,9 @@ __global__ __launch_bounds__(TAB ? 1024 : 256) void pool_kernel(PoolArgs a) {
           *reinterpret_cast<uint4 *>(p_lds + my_tag() + 16u * i) = make_uint4(0, 0, 0, 0);
       }
     }
+    if (!has) return;
+    fl = a.out_flags[cand];
+    cand_round = rnd;
     ptr = 0;
     tfree = 0;
     acc = 0;
@@ -268,10 +268,9 @@ __global__ __launch_bounds__(TAB ? 1024 : 256) void pool_kernel(PoolArgs a) {
       nblk = *block_at(min((pos2 >> 2) + 1u, uint32_t(last_abs) >> 2));
       id2 = id_in(blk, pos2);
       cur = rec_at(rb + id0);
-      n0 = rec_at(rb + id1);
+      s0 = rec_at(rb + id1);
       ce = first_edge(cur);
       ea = extra_off(cur);
-      act = true;
     }
   };
 
@@ -309,7 +308,7 @@ __global__ __launch_bounds__(TAB ? 1024 : 256) void pool_kernel(PoolArgs a) {
     // prefetch the op's next edge (taken if this round finds the current one;
     // lanes on their last edge read the table's first entry)
     const bool last_edge = ce.x < 0;   // kEdgeLast is the sign bit
-    se = edge_at(act && !last_edge ? ea : 0u);
+    se = edge_at(!last_edge ? ea : 0u);
 
     // the matching slot, as index bits
     // (as wave masks: each compare's lanes, combined with scalar ops)
@@ -373,25 +372,20 @@ __global__ __launch_bounds__(TAB ? 1024 : 256) void pool_kernel(PoolArgs a) {
       st16(my_tag() + 2u * sl, uint32_t(cur.w));
     }
 
-    // ---- the record and id fetched after the previous round's advance: taken
-    // here, where they are first needed, so that the loads (issued at the end
-    // of that round) overlap this round's pool reads
-    if (take_rec) n0 = s0;
-    asm volatile("" : "+v"(n0.x), "+v"(n0.y), "+v"(n0.z), "+v"(n0.w)::"memory");
-
     // ---- register state (fin: fired its last op; adv: fired another)
     const uint64_t m_fin = m_fire & __builtin_amdgcn_ballot_w64(ptr + 1 == nr);
     const bool fin = __builtin_amdgcn_inverse_ballot_w64(m_fin);
     const bool adv = __builtin_amdgcn_inverse_ballot_w64(m_fire & ~m_fin);
     take_edge = __builtin_amdgcn_inverse_ballot_w64(m_found & ~m_fire & ~m_last);
     if (fire) {
-      // (a lane that fired its last op copies a record it never uses)
+      // (s0 arrived a round ago at the latest; a lane that fired its last op
+      // copies a record it never uses)
       tfree = en;
       acc = 0;
       ++ptr;
-      cur = n0;
-      ce = first_edge(n0);
-      ea = extra_off(n0);
+      cur = s0;
+      ce = first_edge(s0);
+      ea = extra_off(s0);
     } else if (found) {
       acc = acc_n;
       ea += 8u;   // (unused once the last edge is found)
@@ -400,15 +394,14 @@ __global__ __launch_bounds__(TAB ? 1024 : 256) void pool_kernel(PoolArgs a) {
       if (last_edge) ce.x = no_edge.x;
     }
     if (fin) {
-      act = false;
       ce.x = dead_edge.x;
+      ea = 0;
     }
     // fetch, for an advance, the record of the op after the new current one
     // and the id after that
-    take_rec = adv;
     {
       // the record of the op now at ptr + 1 (its id was at ptr + 2)
-      s0 = rec_of(adv, uint32_t(id2));
+      if (adv) s0 = rec_of(uint32_t(id2));
       // the id now at ptr + 2; entering a new block, take the one fetched
       // ahead and fetch the block after it
       // the block fetched at the previous crossing, taken a full round after
@@ -429,7 +422,7 @@ __global__ __launch_bounds__(TAB ? 1024 : 256) void pool_kernel(PoolArgs a) {
     const uint64_t b_fin = m_fin;
     const bool stall_check = (rnd & 7u) == 0u;
     if (!b_fin && !stall_check) continue;
-    const uint64_t g_run = any_in_group<PWL>(__builtin_amdgcn_ballot_w64(act));
+    const uint64_t g_run = any_in_group<PWL>(__builtin_amdgcn_ballot_w64(has && ce.x != dead_edge.x));
     const uint64_t ev_done = g_has & ~g_run;
     uint64_t ev_stall = 0, ev_over = 0;
     if (stall_check) {
