@@ -6,8 +6,11 @@ of the batch (makespan, per-rank bubble, per-rank peak activation memory,
 flags) and reduce the batch to its best (makespan, index).  Inputs are seeded
 synthetic candidates already resident in device memory when timing starts.
 
-Default workload: the 8-rank vision-language instance (ViT on ranks 0-1, LLM
-on ranks 2-7, 32 samples), 65,536 candidates per batch.
+Default workload: the large 16-rank x 4-virtual-stage instance (vision
+encoder, LLM and DiT decoder segments, 256 mixed samples, 34,896 ops per
+candidate), one resident 262,144-candidate chunk of its 4,194,304-candidate
+stream per batch.  --stream additionally streams all 4,194,304 candidates
+from pinned host memory (reported under its own key, host-link inclusive).
 
 With --path mcts a step is one iteration of the MCTS segment reordering
 (Sec. 5.1): tree selection and expansion on the host, then one batch of
@@ -38,8 +41,12 @@ Prints one JSON line.  Besides the throughput it carries
                 bytes per launch measured with rocprofv3 counters for the same
                 kernel source (a summary under profiles/ keyed by the source
                 hash), null when the source changed since;
-  cpu_baseline  the CPU oracle timed on this host on a bounded sample of the
-                same workload.
+  issue         the same kernel's simulated ops per second against the
+                integer-issue ceiling (about 5 int32 operations per simulated
+                op at 256 CUs x 64 lanes x 2.4 GHz = 7.9e12 simulated ops/s);
+  cpu_baseline  the CPU oracle timed on this host on bounded samples of the
+                same workload: all host cores (the value), one core, and the
+                CPU model.
 """
 from __future__ import annotations
 
@@ -138,18 +145,73 @@ def log(msg):
     print(msg, file=sys.stderr, flush=True)
 
 
+# 256 CUs x 64 lanes x 2.4 GHz int32 lane operations per second, over about 5
+# int32 operations per simulated op (add the latency, max with the rank's free
+# time, add the cost, the memory delta, the running peak)
+ISSUE_PEAK_OPS = 256 * 64 * 2.4e9 / 5
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_oracle_baseline(prob, rows, seconds: float) -> dict:
+    """The CPU oracle on this host's cores, on consecutive candidates of the
+    batch (never repeated), each leg bounded by ``seconds`` of wall time:
+    candidate-parallel on every core this process may use (the value), then
+    single-threaded."""
+    import oracle
+
+    visible = len(os.sched_getaffinity(0))
+    # the host's CPU share for this process: OMP_NUM_THREADS where the
+    # machine sets it (one GPU's share of a shared host), else every core
+    share = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    cores = max(1, min(visible, share) if share > 0 else visible)
+    n = int(rows.shape[0])
+
+    def leg(threads, block, start):
+        done, t0, i = 0, time.perf_counter(), start
+        while True:
+            b = min(block, n - i) if i < n else 0
+            if b == 0:
+                i, b = 0, min(block, n)
+            oracle.evaluate(prob, rows[i:i + b], threads=threads)
+            done += b
+            i += b
+            dt = time.perf_counter() - t0
+            if dt >= seconds:
+                return done, dt, i
+
+    d_all, t_all, nxt = leg(cores, 64 * cores, 0)
+    d_one, t_one, _ = leg(1, 16, nxt)
+    return {"value": d_all / t_all, "unit": "candidates/s", "cores": cores, "kind": "oracle",
+            "ops_per_s": d_all * prob.n_total / t_all,
+            "sample": f"{d_all} consecutive candidates of the batch on {cores} threads "
+                      f"({t_all:.1f} s wall)",
+            "one_core": {"value": d_one / t_one, "unit": "candidates/s",
+                         "ops_per_s": d_one * prob.n_total / t_one,
+                         "sample": f"the next {d_one} candidates on one thread ({t_one:.1f} s)"},
+            "cpu_model": cpu_model(), "host_cpus_visible": visible}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, help="workload id 1-5")
+    ap.add_argument("--config", type=int, default=5, help="workload id 1-5")
     ap.add_argument("--n-cand", type=int, default=0, help="override candidates per batch")
     ap.add_argument("--variant", type=int, default=0)
     ap.add_argument("--wpb", type=int, default=0)
     ap.add_argument("--slots", type=int, default=0, help="pool slots per rank (pool kernel)")
-    ap.add_argument("--cpu-seconds", type=float, default=1.5,
-                    help="wall-time bound of the CPU oracle baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=6.0,
+                    help="wall-time bound of each CPU oracle baseline leg (all cores, one core)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-steps", type=int, default=10,
                     help="steps re-run after the timed region with per-kernel events")
@@ -343,27 +405,15 @@ def main():
     bytes_per_cand = 2 * prob.n_total + 4 + 4 * P + 4 * P + 1
     algo_bytes = n_cand * bytes_per_cand
     achieved_gbs = algo_bytes / dom_s / 1e9
+    kern_ops_per_s = n_cand * prob.n_total / dom_s
     slots = info.get("pool_slots", 0)
     traffic = measured_traffic(cfg.name, n_cand, slots) if info["variant"] == 8 else None
 
     cpu = None
     if not args.no_cpu_baseline:
-        import oracle
-        cores = max(1, min(16, len(os.sched_getaffinity(0))))
-        sample = min(n_cand, 8192)
-        done = 0
-        tc = time.perf_counter()
-        while True:
-            oracle.evaluate(prob, rows[:sample], threads=cores)
-            done += sample
-            if time.perf_counter() - tc >= args.cpu_seconds:
-                break
-        dt = time.perf_counter() - tc
-        cpu = {"value": done / dt, "unit": "candidates/s", "cores": cores, "kind": "oracle",
-               "ops_per_s": done * prob.n_total / dt,
-               "sample": f"first {sample} candidates of the batch, repeated "
-                         f"{done // sample}x ({dt:.2f} s wall on {cores} threads)"}
-        log(f"[bench] cpu oracle {done / dt:.0f} candidates/s on {cores} threads")
+        cpu = cpu_oracle_baseline(prob, rows, args.cpu_seconds)
+        log(f"[bench] cpu oracle: {cpu['value']:.4g} candidates/s on {cpu['cores']} threads, "
+            f"{cpu['one_core']['value']:.4g} on one ({cpu['cpu_model']})")
 
     rec = {
         "metric": "candidate schedules simulated/sec",
@@ -389,9 +439,14 @@ def main():
         "best": {"index": best[0], "makespan_us": best[1]},
         "roofline": {"bound": "hbm", "kernel": "simulate", "achieved": achieved_gbs,
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": achieved_gbs / HBM_PEAK_GBS,
-                     "traffic": traffic, "algorithmic_bytes": algo_bytes},
-        # the kernel's measured bound: vector issue (from the committed counters)
-        "issue": measured_issue(cfg.name, n_cand, slots) if info["variant"] == 8 else None,
+                     "traffic": traffic, "algorithmic_bytes": algo_bytes,
+                     "bytes_per_candidate": bytes_per_cand, "kernel_ms": dom_s * 1e3},
+        # the second ceiling: simulated ops per second of the same kernel
+        # against the integer-issue bound (about 5 int32 operations per op)
+        "issue": {"achieved": kern_ops_per_s, "peak": ISSUE_PEAK_OPS, "unit": "simulated ops/s",
+                  "frac": kern_ops_per_s / ISSUE_PEAK_OPS,
+                  "counters": measured_issue(cfg.name, n_cand, slots)
+                  if info["variant"] == 8 else None},
         "steady_state": steady,
         "cpu_baseline": cpu,
     }
@@ -469,6 +524,7 @@ def run_greedy(args, cfg):
     algo_bytes = n_cand * bytes_per_cand
     dom_s = kern_avg_ms[0] / 1e3
     achieved_gbs = algo_bytes / dom_s / 1e9
+    kern_ops_per_s = n_cand * prob.n_total / dom_s
     cand_per_s = n_cand * args.steps / wall
 
     cpu = None

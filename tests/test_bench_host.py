@@ -52,3 +52,17 @@ def test_committed_summary_lines_parse():
                                 r"gui_active=\d+$", line.strip()), (path, line)
                 found += 1
     assert found >= 10
+
+
+def test_cpu_baseline_legs_and_fields():
+    """Both legs of the CPU baseline (all cores, one core) on consecutive
+    candidates of a small batch, with the CPU model reported."""
+    import workloads as W
+    prob = W.make_problem(1)
+    rows = W.generator_for(prob, 1).generate(0, 256)
+    cpu = bench.cpu_oracle_baseline(prob, rows, 0.2)
+    assert cpu["kind"] == "oracle" and cpu["unit"] == "candidates/s"
+    assert cpu["cores"] >= 1 and cpu["value"] > 0 and cpu["one_core"]["value"] > 0
+    assert cpu["ops_per_s"] == cpu["value"] * prob.n_total or abs(
+        cpu["ops_per_s"] / (cpu["value"] * prob.n_total) - 1) < 1e-9
+    assert isinstance(cpu["cpu_model"], str) and cpu["cpu_model"]

@@ -1,0 +1,178 @@
+"""Full-size GPU parity: every candidate of the larger workloads against the
+oracle, element by element, plus the batch argmin against the oracle's own
+argmin (never against the GPU's makespans).
+
+* 16 ranks x 2 virtual stages: all 262,144 candidates in one evaluate.
+* 32-rank diffusion: all 1,048,576 candidates in one evaluate (the launch the
+  benchmark times for that workload); the oracle runs chunk by chunk.
+* 16 x 4 large: one full 262,144-candidate chunk (the benchmark's workload).
+* A regression case for groups of the simulation kernel that get no
+  candidate: a launch that leaves the LDS dirty runs first, then batches far
+  smaller than the resident groups, written into slices of sentinel-filled
+  buffers whose guard elements must stay untouched.
+* Optionally (DIPSIM_FULL_STREAM=1), the whole 4,194,304-candidate large
+  workload streamed in chunks, its folded argmin against the oracle's.
+"""
+import os
+import time
+
+import numpy as np
+import pytest
+
+import oracle as O
+import workloads as W
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+if torch.cuda.is_available():
+    import paper_2504_14145_amd as dip
+
+DEV = "cuda:0"
+THREADS = 16
+ORACLE_CHUNK = 65536
+
+
+def need_gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def say(msg):
+    print(f"[{time.strftime('%H:%M:%S')}] {msg}", flush=True)
+
+
+def compare_rows(got, want, lo, hi, what):
+    ms, bub, pk, fl = got
+    for name, g, w in (("flags", fl[lo:hi], want.flags), ("makespan", ms[lo:hi], want.makespan),
+                       ("bubble", bub[lo:hi], want.bubble), ("peak", pk[lo:hi], want.peak)):
+        bad = np.nonzero(np.any((g != w).reshape(len(g), -1), axis=1))[0]
+        assert len(bad) == 0, (f"{what}: {name} differs on {len(bad)} candidates, first "
+                               f"{lo + int(bad[0])}: gpu {g[bad[0]]} oracle {w[bad[0]]}")
+
+
+def full_batch_parity(cid, n):
+    prob = W.make_problem(cid)
+    gen = W.generator_for(prob, cid)
+    say(f"config {cid}: generating {n} candidates x {prob.n_total} ops")
+    rows = gen.generate(0, n)
+    sim = dip.Sim(prob)
+    say(f"config {cid}: evaluate on the GPU ({sim.info})")
+    orders = torch.from_numpy(rows).to(DEV)
+    ms, bub, pk, fl = sim.evaluate(orders)
+    key = sim.argmin(ms, fl)
+    torch.cuda.synchronize()
+    got = (ms.cpu().numpy(), bub.cpu().numpy(), pk.cpu().numpy(), fl.cpu().numpy())
+    del orders
+    all_ms = np.empty(n, np.int32)
+    all_fl = np.empty(n, np.uint8)
+    for lo in range(0, n, ORACLE_CHUNK):
+        hi = min(n, lo + ORACLE_CHUNK)
+        want = O.evaluate(prob, rows[lo:hi], threads=THREADS)
+        compare_rows(got, want, lo, hi, f"config {cid} rows {lo}..{hi - 1}")
+        all_ms[lo:hi] = want.makespan
+        all_fl[lo:hi] = want.flags
+        if (lo // ORACLE_CHUNK) % 4 == 3 or hi == n:
+            say(f"config {cid}: oracle agrees on rows 0..{hi - 1}")
+    best = O.argmin(all_ms, all_fl)
+    assert dip.decode_key(int(key.item())) == best
+    say(f"config {cid}: argmin {best} equals the oracle's; deadlocked "
+        f"{np.mean(all_fl & O.FLAG_DEADLOCK > 0):.3f}, capped {np.mean(all_fl & O.FLAG_CAP > 0):.3f}")
+    sim.close()
+
+
+def test_full_parity_interleaved_16x2():
+    need_gpu()
+    full_batch_parity(3, W.get(3).n_cand)
+
+
+def test_full_parity_large_16x4_chunk():
+    need_gpu()
+    full_batch_parity(5, W.get(5).chunk)
+
+
+def test_full_parity_diffusion_s32():
+    need_gpu()
+    full_batch_parity(4, W.get(4).n_cand)
+
+
+@pytest.mark.parametrize("cid", [2, 3, 5])
+def test_idle_groups_over_dirty_lds(cid):
+    """Batches much smaller than the simulation kernel's resident candidate
+    groups, right after launches that fill the LDS with other data (the
+    greedy interleaving, and evaluate of a full batch of another workload):
+    groups without a candidate must write nothing, and the candidates they
+    do hold must equal the oracle's, at every pool size."""
+    need_gpu()
+    prob = W.make_problem(cid)
+    rows = W.generator_for(prob, cid).generate(5, 40)
+    sim = dip.Sim(prob)
+    other = W.make_problem(2)
+    osim = dip.Sim(other)
+    g, G, cls = W.priority_groups(other)
+    assert osim.configure_greedy(G, g) == dip.OK
+    prio = torch.from_numpy(W.rollout_priorities(cls, 1024, seed=3)).to(DEV)
+    orows = torch.from_numpy(W.generator_for(other, 2).generate(0, 8192)).to(DEV)
+    guard = 64
+    sizes = (1, 3, 17, 40)
+    for slots in (4, 8, 16):
+        if sim.configure_pool(slots) != dip.OK:
+            continue
+        for n in sizes:
+            osim.greedy(prio)                 # leaves its inboxes in the LDS
+            osim.evaluate(orows)
+            torch.cuda.synchronize()
+            ms = torch.full((n + guard,), -77, dtype=torch.int32, device=DEV)
+            bub = torch.full((n + guard, prob.n_ranks), -77, dtype=torch.int32, device=DEV)
+            pk = torch.full((n + guard, prob.n_ranks), -77, dtype=torch.int32, device=DEV)
+            fl = torch.full((n + guard,), 0x5A, dtype=torch.uint8, device=DEV)
+            orders = torch.from_numpy(np.ascontiguousarray(rows[:n])).to(DEV)
+            dip.evaluate(sim.h, sim.costs if not sim._costs_sent else None, orders, n,
+                         ms, bub, pk, fl)
+            sim._costs_sent = True
+            torch.cuda.synchronize()
+            got = tuple(t.cpu().numpy() for t in (ms, bub, pk, fl))
+            assert (got[0][n:] == -77).all() and (got[1][n:] == -77).all()
+            assert (got[2][n:] == -77).all() and (got[3][n:] == 0x5A).all()
+            want = O.evaluate(prob, rows[:n], threads=THREADS)
+            compare_rows(got, want, 0, n, f"config {cid} slots {slots} n {n}")
+    sim.close()
+    osim.close()
+
+
+@pytest.mark.skipif(os.environ.get("DIPSIM_FULL_STREAM") != "1",
+                    reason="the whole 4,194,304-candidate stream runs only on request "
+                           "(DIPSIM_FULL_STREAM=1): about 3 minutes of oracle time")
+def test_full_stream_large_16x4_argmin():
+    """All 16 chunks of the large workload through the two-stream chunked
+    evaluation; the folded argmin equals the oracle's over all candidates."""
+    need_gpu()
+    from paper_2504_14145_amd.stream import ChunkStream
+    cfg = W.get(5)
+    prob = W.make_problem(5)
+    gen = W.generator_for(prob, 5)
+    sim = dip.Sim(prob)
+    chunk = cfg.chunk
+    cs = ChunkStream(sim, chunk)
+    all_ms = np.empty(cfg.n_cand, np.int32)
+    all_fl = np.empty(cfg.n_cand, np.uint8)
+    hosts = []
+    for k in range(cfg.n_cand // chunk):
+        lo = k * chunk
+        rows = gen.generate(lo, chunk)
+        host = torch.from_numpy(rows).pin_memory()
+        cs.submit(host, lo)
+        hosts.append(host)
+        if len(hosts) > 2:
+            hosts.pop(0)
+        for a in range(0, chunk, ORACLE_CHUNK):
+            want = O.evaluate(prob, rows[a:a + ORACLE_CHUNK], threads=THREADS)
+            all_ms[lo + a:lo + a + ORACLE_CHUNK] = want.makespan
+            all_fl[lo + a:lo + a + ORACLE_CHUNK] = want.flags
+        say(f"chunk {k}: submitted; oracle done")
+    key = cs.finish()
+    best = O.argmin(all_ms, all_fl)
+    got = dip.decode_key(int(key.item()))
+    say(f"streamed argmin {got}, oracle {best}; valid {np.mean(all_fl == 0):.4f}")
+    assert got == best
+    sim.close()

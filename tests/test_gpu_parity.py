@@ -208,36 +208,6 @@ def test_parity_full_bench_workload():
     sim.close()
 
 
-@pytest.mark.parametrize("cid", [3, 4, 5])
-def test_parity_full_size_sampled(cid):
-    """Each larger configuration at the batch size the benchmark evaluates
-    (its full candidate count; one 262,144-candidate chunk for the streamed
-    16 x 4 configuration), in the launch configuration the benchmark uses:
-    every output of a sample of candidates (first, last, a random spread)
-    against the oracle run on just those rows, and the batch argmin against
-    a scan of the outputs the sample fixes."""
-    need_gpu()
-    cfg = W.get(cid)
-    n = cfg.chunk or cfg.n_cand
-    prob = W.make_problem(cid)
-    rows = W.generator_for(prob, cid).generate(0, n)
-    print(f"config {cid}: {n} candidates generated", flush=True)
-    sim = dip.Sim(prob)
-    got = run_gpu(sim, rows)
-    rng = np.random.default_rng(cid)
-    idx = np.unique(np.concatenate([[0, n - 1], rng.choice(n, size=384, replace=False)]))
-    want = O.evaluate(prob, rows[idx], threads=16)
-    assert_same(got, want, idx)
-    # the argmin over the whole batch is the lexicographic minimum of the
-    # GPU makespans over unflagged candidates (their values are pinned above)
-    key = sim.argmin(torch.from_numpy(got[0]).to(DEV), torch.from_numpy(got[3]).to(DEV))
-    torch.cuda.synchronize()
-    ok = np.nonzero(got[3] == 0)[0]
-    best = ok[np.lexsort((ok, got[0][ok]))[0]] if len(ok) else -1
-    assert dip.decode_key(int(key.item()))[0] == best
-    sim.close()
-
-
 def test_edge_cases_invalid_deadlock_single():
     need_gpu()
     prob = W.make_problem(1)
