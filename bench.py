@@ -333,7 +333,9 @@ def main():
     dip.profile(sim.h, False)
     nk = min(len(p) for p in per_kernel)
     kern_avg_ms = [sum(p[i] for p in per_kernel) / len(per_kernel) for i in range(nk)]
-    names = (["check", "simulate", "retry"] if info["variant"] == 8 else ["simulate"])[:nk]
+    names = {8: ["check", "simulate", "retry"],
+             9: ["check", "simulate", "simulate_16", "retry"]}.get(info["variant"],
+                                                                 ["simulate"])[:nk]
     dom = names.index("simulate")
     dom_s = kern_avg_ms[dom] / 1e3
     log(f"[bench] per-kernel avg ms: " + ", ".join(f"{n} {t:.4f}" for n, t in zip(names, kern_avg_ms)))
@@ -407,7 +409,7 @@ def main():
     achieved_gbs = algo_bytes / dom_s / 1e9
     kern_ops_per_s = n_cand * prob.n_total / dom_s
     slots = info.get("pool_slots", 0)
-    traffic = measured_traffic(cfg.name, n_cand, slots) if info["variant"] == 8 else None
+    traffic = measured_traffic(cfg.name, n_cand, slots) if info["variant"] in (8, 9) else None
 
     cpu = None
     if not args.no_cpu_baseline:

@@ -372,10 +372,19 @@ int dip_cost_tables(const dip_op_table *t, int64_t n_configs, const double *coef
  * later evaluate records HIP events on its stream around each kernel it
  * launches; dip_sim_last_profile then waits for the last of them and writes
  * the kernel times in milliseconds, in launch order, to out_ms[0 .. *n_out-1]
- * (n_out <= 3: variant 8 launches the check, pool and retry kernels, the
- * others one kernel; dip_sim_greedy records its two launches the same way).  *n_out = 0 if the last evaluate recorded nothing. */
+ * (n_out <= 4: variant 8 launches the check, pool and retry kernels;
+ * variant 9 the check kernel, the simulation kernel, its second pass with
+ * 16-slot pools over the candidates whose pools filled, and the retry
+ * kernel; variants 1-4 one kernel; dip_sim_greedy records its two launches
+ * the same way).  *n_out = 0 if the last evaluate recorded nothing. */
 int dip_sim_profile(dip_sim *h, int32_t enable);
 int dip_sim_last_profile(dip_sim *h, float *out_ms, int32_t *n_out);
+
+/* Diagnostics of the last evaluate (variants 8 and 9): *out_first = the
+ * candidates whose pools filled in the first simulation pass; *out_second =
+ * those left to the general kernel (variant 9: the ones its second pass, with
+ * 16-slot pools, could not finish either).  Waits for that call's stream. */
+int dip_sim_last_retries(dip_sim *h, int64_t *out_first, int64_t *out_second);
 
 /* Release the handle's device memory.  Waits for the device first. */
 void dip_sim_destroy(dip_sim *h);

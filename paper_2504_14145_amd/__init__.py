@@ -26,7 +26,7 @@ NO_KEY = (1 << 64) - 1
 EXPORTS = ("dip_sim_abi_version", "dip_sim_check_topology", "dip_sim_check_costs",
            "dip_sim_create", "dip_sim_configure", "dip_sim_configure_pool",
            "dip_sim_configure_check", "dip_sim_get_info", "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
-           "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_set_greedy_inbox", "dip_sim_greedy",
+           "dip_sim_last_retries", "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_set_greedy_inbox", "dip_sim_greedy",
            "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_sim_rollouts_batch",
            "dip_cost_tables",
            "dip_sim_configure_memopt", "dip_sim_memopt", "dip_sim_destroy", "dip_sim_strerror")
@@ -92,6 +92,7 @@ def load():
         lib.dip_sim_configure_check.argtypes = [vp, i32]
         lib.dip_sim_profile.argtypes = [vp, i32]
         lib.dip_sim_last_profile.argtypes = [vp, vp, vp]
+        lib.dip_sim_last_retries.argtypes = [vp, vp, vp]
         lib.dip_sim_get_info.argtypes = [vp, ctypes.POINTER(Info)]
         lib.dip_sim_evaluate.argtypes = [vp, ctypes.POINTER(Costs), vp, i64, vp, vp, vp, vp, vp]
         lib.dip_sim_argmin.argtypes = [vp, vp, vp, i64, i64, vp, vp]
@@ -114,6 +115,7 @@ def load():
                      "dip_sim_configure", "dip_sim_configure_pool", "dip_sim_configure_check",
                      "dip_sim_get_info",
                      "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
+                     "dip_sim_last_retries",
                      "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_set_greedy_inbox", "dip_sim_greedy",
                      "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_sim_rollouts_batch",
            "dip_cost_tables",
@@ -208,6 +210,14 @@ def last_profile(h) -> list:
     n = ctypes.c_int32(0)
     _check(load().dip_sim_last_profile(h, buf, ctypes.byref(n)), "dip_sim_last_profile")
     return [float(buf[i]) for i in range(n.value)]
+
+
+def last_retries(h) -> tuple:
+    """(candidates whose pools filled in the first simulation pass, those left
+    to the general kernel) of the last evaluate; waits for its stream."""
+    a, b = ctypes.c_int64(0), ctypes.c_int64(0)
+    _check(load().dip_sim_last_retries(h, ctypes.byref(a), ctypes.byref(b)), "dip_sim_last_retries")
+    return int(a.value), int(b.value)
 
 
 def get_info(h) -> dict:

@@ -23,6 +23,15 @@ __device__ __forceinline__ uint64_t any_in_group(uint64_t m) {
   return m & group_low_lanes<PWL>();
 }
 
+// Every lane of group g is set iff bit (g << PWL) of m is (m holds group bits
+// only, as any_in_group returns them).
+template <int PWL>
+__device__ __forceinline__ uint64_t any_lane_of_group(uint64_t m) {
+#pragma unroll
+  for (int s = 1; s < (1 << PWL); s <<= 1) m |= m << s;
+  return m;
+}
+
 // Waits for this wave's outstanding LDS (and scalar-load) operations.
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 

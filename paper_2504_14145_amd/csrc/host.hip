@@ -1,26 +1,26 @@
 // host.hip -- the C ABI of include/dip_sim.h: validation, device tables,
 // kernel-variant choice and stream-ordered launches.
 //
-// Kernel families (see kern_general.hip, kern_pipe.hip, kern_pipe_lds.hip):
+// Kernel families (see kern_general.hip, kern_pool.hip, kern_sim.hip):
 //   variants 1-4  general kernel, any predecessor count, tables placed per
 //                 variant (all in LDS ... end times in device scratch);
-//   variant 5     pipeline kernel with end-time tables and order rows in LDS,
-//                 op records read through the caches;
-//   variant 6     pipeline kernel with end-time tables in device scratch;
-//   variant 7     as 5, with the op records in LDS too;
 //   variant 8     check kernel (permutation, memory) + pool kernel (end times
-//                 handed between ranks through small per-rank slot pools) +
-//                 the general kernel in list mode for candidates whose pools
-//                 filled up.
-// The pipeline kernel needs every op with several predecessors to have them
-// all on one rank, every op to feed at most one such op, and every time
-// below 2^30 (the sum of all costs and latencies bounds every time), so the
-// time bound is re-checked whenever costs change.
+//                 handed between ranks through small per-rank slot pools, op
+//                 records through the caches) + the general kernel in list
+//                 mode for candidates whose pools filled up;
+//   variant 9     as 8 with the simulation kernel of kern_sim.hip in place of
+//                 the pool kernel: compact op records resident in LDS and the
+//                 orders staged through per-lane LDS rings.  It needs at most
+//                 8192 ops per rank, and per call costs below 2^20 and
+//                 latencies below 2^11 (checked whenever costs change; a call
+//                 outside them runs variant 8).
 #include <algorithm>
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
 #include <new>
+#include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "dip_sim.h"
@@ -35,6 +35,9 @@ thread_local hipError_t g_last_hip = hipSuccess;
 constexpr int kMaxRanks = 64;
 constexpr int32_t kMaxOpsPerRank = 32768;
 constexpr int64_t kScratchCap = int64_t(2) << 30;  // device scratch ceiling
+// simulation-kernel records up to this size are stored one per op, larger
+// tables as deduplicated pages (one more LDS read per record)
+constexpr int64_t kSimDirectMax = 32768;
 
 #define DIP_HIP(expr)          \
   do {                         \
@@ -60,43 +63,61 @@ struct dip_sim {
   std::vector<int32_t> n_ops, rank_off, pred_ptr, pred_op, op_slot, cap;
   std::vector<uint8_t> kind;
   int32_t pwl = 0, G = 0;
-  bool pipe_ok = false;                // topology fits the pipeline kernel
-  bool pipe_costs_ok = false;          // last costs keep every time below 2^30
-  int32_t tab_stride = 0;              // pipeline kernel: words per end-time table
-  int32_t n_joins = 0;                 // ops with several predecessors
-  uint32_t join_base = 0;              // byte offset of the join blocks in a table
-  std::vector<int32_t> join_of;        // [N] join index of an op, -1 if none
-  std::vector<int32_t> feeds_join;     // [N] the join op this op feeds, -1 if none
-  std::vector<int32_t> feed_edge;      // [N] edge index of that feed
   std::vector<int32_t> rank_of;        // [N] rank running each op
+  // own-rank predecessors: the tile check verifies their order, and the
+  // simulation kernel then drops those edges when their latency is zero
+  bool self_ok = false;                // at most one own-rank predecessor per op
+  uint64_t self_ranks = 0;             // bit r: rank r has ops with one
+  std::vector<int32_t> self_pred;      // [N] its local id + 1, 0 if none
+  int32_t *d_selfp = nullptr;
+  bool sim_drop_self = false;          // the current sim tables dropped them
+  std::vector<int32_t> last_cost, last_comm, last_act;   // the last costs (host copies)
   std::vector<int32_t> n_cons;         // [N] consumers of each op
   bool pool_ok = false;                // topology fits the pool kernel
   int32_t n_extra = 0;                 // pool kernel: edges after each op's first
   bool pool_tab = false;               // pool kernel: tables copied into LDS
   int64_t pool_tab_bytes = 0;          // their bytes (records, then extra edges)
-  int pool_slots = 8, forced_pool_slots = 0;
+  int pool_slots = 8, forced_pool_slots = 0;   // slots per rank pool (variants 8, 9)
+  // simulation kernel (variant 9)
+  bool sim_ok = false;                 // topology fits it
+  bool sim_costs_ok = false;           // the last costs fit its records
+  bool sim_paged = false;              // records stored as deduplicated pages
+  int32_t sim_n_extra = 0;             // extra-edge words (edges of multi-predecessor ops)
+  int64_t sim_tab_cap = 0;             // bytes of d_sim_tab
+  int32_t sim_tab_vec = 0;             // 16-byte units of the current table image
+  uint32_t sim_off_pmap = 0, sim_off_extra = 0;
+  uint4 *d_sim_tab = nullptr;          // LDS image: records, page map, extra edges
+  int4 *d_sim_lane = nullptr;          // [P] {first op, ops, busy, record base}
+  int sim_wpb = 1, sim_max_blocks = 1;
+  int64_t sim_lds = 0;
+  int64_t sim_state_base = 0;
+  // second pass over the first pass's retry list, with 16-slot pools
+  bool sim2_ok = false;
+  int sim2_wpb = 1, sim2_max_blocks = 1;
+  int64_t sim2_lds = 0;
+  int64_t *d_retry2 = nullptr;         // candidates the second pass could not hold
+  hipStream_t last_stream = nullptr;   // stream of the last evaluate (diagnostics)
+  bool last_pass2 = false;             // it ran the second simulation pass
   int4 *d_pool_rec = nullptr;          // pool records [N][2]
   int2 *d_pool_edge = nullptr;         // pool edges [E]
   int64_t *d_retry = nullptr;          // candidates re-run by the general kernel
-  uint32_t *d_retry_count = nullptr;
-  // adaptive pool size: the retry count of a call is copied back
-  // asynchronously and read by a later call, which doubles the pool when more
-  // than 1/256 of the candidates needed the retry kernel
-  uint32_t *h_retry_seen = nullptr;    // pinned
-  hipEvent_t retry_seen_ev = nullptr;
-  bool retry_seen_pending = false;
-  int64_t retry_seen_n = 0;
+  uint32_t *d_retry_count = nullptr;   // [2] retry count, on-demand candidate counter
   int64_t retry_cap = 0;
   int check_blocks_per_cu = 1;
   bool wc_ok = false;                  // the wave-per-candidate check fits
   int check_mode = 0;                  // 0 automatic, 1 wave per candidate, 2 tiles
   // tile check (lane = candidate, waves splitting the ranks)
-  bool tc_ok = false;
-  int tc_nw = 1;
-  int32_t tc_max_nr = 0;
-  int64_t tc_lds = 0;
-  int tc_blocks_per_cu = 1;
-  int32_t *d_tc_plan = nullptr;        // [nw+1] offsets, then [P] ranks
+  struct TilePlan {
+    int nw = 1;                        // waves per block
+    int32_t max_nr = 0;
+    int64_t lds = 0;
+    int blocks_per_cu = 1;
+    int32_t *d_plan = nullptr;         // [nw+1] offsets, then the ranks
+  };
+  bool tc_ok = false;                  // the main pass (every rank)
+  TilePlan tc;
+  bool to_ok = false;                  // the order pass (ranks with own-rank predecessors)
+  TilePlan to;
   void *d_scratch_fb = nullptr;        // general kernel (list mode) end tables
   int fb_variant = 4;                  // retry kernel: 3 (end times in LDS) when they fit, else 4
   int64_t fb_lds = 0;
@@ -105,23 +126,17 @@ struct dip_sim {
   // device tables
   int4 *d_rec = nullptr;               // general records [N]
   int2 *d_edge = nullptr;              // general edges [E]
-  int4 *d_prec = nullptr;              // pipeline records [N][2]
-  int4 *d_rec16 = nullptr;             // compact pipeline records [N]
-  int32_t *d_jk = nullptr;             // [n_joins] predecessors of each join
-  bool lds16_costs_ok = false;         // compact records hold the last costs
-  int32_t *d_md = nullptr;             // pipeline memory deltas [N]
+  int32_t *d_md = nullptr;             // memory deltas [N] (+act at F, -act at B)
   int32_t *d_rank_off = nullptr, *d_busy = nullptr, *d_cap = nullptr;
   void *d_scratch_gen = nullptr;       // variant 4: end tables per resident wave
   int64_t scratch_gen_bytes = 0;
-  void *d_scratch_pipe = nullptr;      // variant 6: epoch-stamped tables + epoch bytes
-  int64_t scratch_pipe_bytes = 0;
   // pinned staging for cost uploads
   unsigned char *h_stage = nullptr;
   int64_t stage_bytes = 0;
   hipEvent_t stage_done = nullptr;
   // optional per-kernel timing of evaluate: events before each kernel and after the last
   bool profile = false;
-  hipEvent_t prof_ev[4] = {nullptr, nullptr, nullptr, nullptr};
+  hipEvent_t prof_ev[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
   int prof_n = 0;                      // events recorded by the last evaluate
   bool stage_pending = false;
   bool costs_set = false;
@@ -132,8 +147,7 @@ struct dip_sim {
   int n_cu = 1;
   int64_t lds_block_max = 65536;
   int forced_variant = 0, forced_wpb = 0;
-  // fallback general configuration (when the pipeline kernel is chosen but
-  // the costs of a call exceed its time bound)
+  // general configuration (always available)
   int gen_variant = 0, gen_wpb = 1, gen_max_blocks = 1;
   int64_t gen_lds = 0;
   // greedy stage interleaving (dip_sim_configure_greedy / dip_sim_greedy)
@@ -217,10 +231,6 @@ int64_t lds_for(const dip_sim *h, int v, int wpb) {
     GenBytes b = general_bytes(h, v);
     return b.tab + int64_t(wpb) * (b.ord + b.end);
   }
-  if (v == 5 || v == 7) {
-    const int64_t per_wave = int64_t(h->G) * (int64_t(h->tab_stride) * 4 + h->stride * 2);
-    return int64_t(wpb) * per_wave + (v == 7 ? align16(int64_t(h->N) * 16) : 0);
-  }
   if (v == 8)
     return h->pool_tab_bytes + int64_t(wpb) * h->G * pool_group_bytes(1 << h->pwl, h->pool_slots);
   return 0;
@@ -228,20 +238,12 @@ int64_t lds_for(const dip_sim *h, int v, int wpb) {
 
 const void *kernel_ptr(const dip_sim *h, int v) {
   if (v <= 4) return general_kernel_ptr(v);
-  if (v == 6) return pipe_kernel_ptr(h->pwl, true);
-  if (v == 8) return pool_kernel_ptr(h->pwl, h->pool_slots, h->pool_tab);
-  return pipe_lds_kernel_ptr(h->pwl, v == 7);
+  return pool_kernel_ptr(h->pwl, h->pool_slots, h->pool_tab);
 }
-
-// LDS-resident pipeline kernel: compact records address a table by 16-bit
-// byte offsets.
-bool lds16_shape_ok(const dip_sim *h) { return h->pipe_ok && int64_t(h->tab_stride) * 4 <= 0xffff; }
 
 // Resident blocks per CU for (variant, waves per block); 0 if it does not fit.
 int blocks_per_cu(dip_sim *h, int v, int wpb) {
-  if (v >= 5 && v <= 7 && !h->pipe_ok) return 0;
   if (v == 8 && !h->pool_ok) return 0;
-  if ((v == 5 || v == 7) && !lds16_shape_ok(h)) return 0;
   const int64_t lds = lds_for(h, v, wpb);
   if (lds > h->lds_block_max) return 0;
   const void *k = kernel_ptr(h, v);
@@ -261,19 +263,13 @@ int blocks_per_cu(dip_sim *h, int v, int wpb) {
 
 int64_t scratch_need(const dip_sim *h, int v, int wpb, int blocks) {
   if (v == 4) return int64_t(blocks) * wpb * h->G * int64_t(h->N) * 4;
-  if (v == 6) {
-    const int64_t slots = int64_t(blocks) * wpb * h->G;
-    return slots * int64_t(h->tab_stride) * 4 + align16(slots);
-  }
   return 0;
 }
 
-// Device scratch for variant 4 (general) or 6 (pipeline).  The pipeline
-// scratch is zeroed whenever a configuration is applied: zero is "every table
-// stamped with epoch 0 and every epoch byte 0", the state its kernel expects.
-int ensure_scratch(dip_sim *h, int v, int64_t need) {
-  void **buf = v == 6 ? &h->d_scratch_pipe : &h->d_scratch_gen;
-  int64_t *have = v == 6 ? &h->scratch_pipe_bytes : &h->scratch_gen_bytes;
+// Device scratch for variant 4 (general): end tables per resident wave.
+int ensure_scratch(dip_sim *h, int64_t need) {
+  void **buf = &h->d_scratch_gen;
+  int64_t *have = &h->scratch_gen_bytes;
   if (need > *have) {
     if (*buf) {
       DIP_HIP(hipDeviceSynchronize());
@@ -287,41 +283,38 @@ int ensure_scratch(dip_sim *h, int v, int64_t need) {
     }
     *have = need;
   }
-  if (v == 6) {
-    DIP_HIP(hipDeviceSynchronize());
-    DIP_HIP(hipMemset(*buf, 0, size_t(*have)));
-    DIP_HIP(hipDeviceSynchronize());
-  }
   return DIP_OK;
 }
 
 // The pool kernel's fallback: the general kernel with end tables in device
-// Tile check plan: the ranks split between the waves of a block, longest
-// section first onto the least loaded wave.  The number of waves per block is
-// the one (up to 16, and not above the ranks or what keeps every wave near the
-// longest section) that keeps the most waves resident per CU.  Leaves tc_ok
-// false when a rank's section does not fit.
-int plan_tile_check(dip_sim *h) {
-  h->tc_ok = false;
+// Tile check plan over a set of ranks: they are split between the waves of a
+// block, longest section first onto the least loaded wave.  The number of
+// waves per block is the one (up to 16, and not above the ranks or what keeps
+// every wave near the longest section) that keeps the most waves resident per
+// CU.  false when a rank's section does not fit.
+bool plan_tiles(dip_sim *h, const std::vector<int32_t> &rks, bool order, dip_sim::TilePlan *T) {
   int32_t max_nr = 0;
-  for (int r = 0; r < h->P; ++r) max_nr = std::max(max_nr, h->n_ops[r]);
-  if (int64_t(h->stride) * 2 * kWave > int64_t(INT32_MAX)) return DIP_OK;
+  int64_t n_sum = 0;
+  for (int32_t r : rks) {
+    max_nr = std::max(max_nr, h->n_ops[r]);
+    n_sum += h->n_ops[r];
+  }
+  if (rks.empty() || int64_t(h->stride) * 2 * kWave > int64_t(INT32_MAX)) return false;
+  const void *kern = tile_check_kernel_ptr(order);
   const int64_t region = tile_region_bytes(max_nr);
   const int nw_max = int(std::min<int64_t>(
-      {16, int64_t(h->P), (int64_t(h->N) + std::max(max_nr, 1) - 1) / std::max(max_nr, 1)}));
+      {16, int64_t(rks.size()), (n_sum + std::max(max_nr, 1) - 1) / std::max(max_nr, 1)}));
   int nw = 0, nb = 0, best_waves = 0;
   for (int w = 1; w <= std::max(nw_max, 1); ++w) {
     const int64_t lds = kTileFlagBytes + int64_t(w) * region;
     if (lds > h->lds_block_max) break;
-    if (lds > 65536 && hipFuncSetAttribute(tile_check_kernel_ptr(),
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           int(lds)) != hipSuccess) {
+    if (lds > 65536 &&
+        hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess) {
       (void)hipGetLastError();
       break;
     }
     int b = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, tile_check_kernel_ptr(), w * kWave,
-                                                     size_t(lds)) != hipSuccess) {
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, kern, w * kWave, size_t(lds)) != hipSuccess) {
       (void)hipGetLastError();
       break;
     }
@@ -331,17 +324,16 @@ int plan_tile_check(dip_sim *h) {
       nb = b;
     }
   }
-  if (nw == 0) return DIP_OK;
-  std::vector<int32_t> order(h->P), load(nw, 0), wave_of(h->P, 0);
-  for (int r = 0; r < h->P; ++r) order[r] = r;
-  std::stable_sort(order.begin(), order.end(),
+  if (nw == 0) return false;
+  std::vector<int32_t> sorted(rks), load(nw, 0), wave_of(h->P, -1);
+  std::stable_sort(sorted.begin(), sorted.end(),
                    [&](int32_t x, int32_t y) { return h->n_ops[x] > h->n_ops[y]; });
-  for (int32_t r : order) {
+  for (int32_t r : sorted) {
     const int w = int(std::min_element(load.begin(), load.end()) - load.begin());
     wave_of[r] = w;
     load[w] += h->n_ops[r];
   }
-  std::vector<int32_t> plan(size_t(nw) + 1 + size_t(h->P));
+  std::vector<int32_t> plan(size_t(nw) + 1 + rks.size());
   int k = 0;
   for (int w = 0; w < nw; ++w) {
     plan[w] = k;
@@ -350,19 +342,37 @@ int plan_tile_check(dip_sim *h) {
   }
   plan[nw] = k;
   const int64_t lds = kTileFlagBytes + int64_t(nw) * region;
-  if (lds > 65536 && hipFuncSetAttribute(tile_check_kernel_ptr(),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize,
-                                         int(lds)) != hipSuccess) {
+  if (lds > 65536 &&
+      hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess) {
     (void)hipGetLastError();
-    return DIP_OK;
+    return false;
   }
-  if (!h->d_tc_plan) DIP_HIP(hipMalloc(&h->d_tc_plan, plan.size() * 4));
-  DIP_HIP(hipMemcpy(h->d_tc_plan, plan.data(), plan.size() * 4, hipMemcpyHostToDevice));
-  h->tc_nw = nw;
-  h->tc_max_nr = max_nr;
-  h->tc_lds = lds;
-  h->tc_blocks_per_cu = nb;
-  h->tc_ok = true;
+  if (!T->d_plan && hipMalloc(&T->d_plan, size_t(h->P + 17) * 4) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  if (hipMemcpy(T->d_plan, plan.data(), plan.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  T->nw = nw;
+  T->max_nr = max_nr;
+  T->lds = lds;
+  T->blocks_per_cu = nb;
+  return true;
+}
+
+// The main tile check over every rank, and the order pass over the ranks
+// with own-rank predecessors (when there are any).
+int plan_tile_check(dip_sim *h) {
+  std::vector<int32_t> all(h->P), own;
+  for (int r = 0; r < h->P; ++r) {
+    all[r] = r;
+    if ((h->self_ranks >> r) & 1u) own.push_back(r);
+  }
+  h->tc_ok = plan_tiles(h, all, false, &h->tc);
+  // (without the order pass the simulation kernel keeps those edges)
+  h->to_ok = h->tc_ok && h->self_ok && !own.empty() && plan_tiles(h, own, true, &h->to);
   return DIP_OK;
 }
 
@@ -437,15 +447,19 @@ int run_tile_check(dip_sim *h, const int16_t *orders, int64_t n_cand, int32_t *o
   c.md = h->d_md;
   c.rank_off = h->d_rank_off;
   c.cap = h->d_cap;
-  c.plan = h->d_tc_plan;
+  c.selfp = h->d_selfp;
   c.P = h->P;
-  c.nw = h->tc_nw;
-  c.md_bytes = tile_md_bytes(h->tc_max_nr);
-  c.region_bytes = tile_region_bytes(h->tc_max_nr);
   c.retry_count = h->d_retry_count;
   const int64_t tiles = (n_cand + kWave - 1) / kWave;
-  const int blocks = int(std::min<int64_t>(tiles, int64_t(h->tc_blocks_per_cu) * h->n_cu));
-  DIP_HIP(launch_tile_check(std::max(blocks, 1), h->tc_nw, size_t(h->tc_lds), stream, c));
+  for (int pass = 0; pass < (h->to_ok ? 2 : 1); ++pass) {
+    const dip_sim::TilePlan &T = pass ? h->to : h->tc;
+    c.plan = T.d_plan;
+    c.nw = T.nw;
+    c.md_bytes = tile_md_bytes(T.max_nr);
+    c.region_bytes = tile_region_bytes(T.max_nr);
+    const int blocks = int(std::min<int64_t>(tiles, int64_t(T.blocks_per_cu) * h->n_cu));
+    DIP_HIP(launch_tile_check(std::max(blocks, 1), T.nw, size_t(T.lds), stream, c, pass == 1));
+  }
   return DIP_OK;
 }
 
@@ -483,7 +497,12 @@ int ensure_retry(dip_sim *h, int64_t n) {
     h->d_retry = nullptr;
   }
   h->retry_cap = 0;
-  if (hipMalloc(&h->d_retry, size_t(n) * 8) != hipSuccess) {
+  if (h->d_retry2) {
+    DIP_HIP(hipFree(h->d_retry2));
+    h->d_retry2 = nullptr;
+  }
+  if (hipMalloc(&h->d_retry, size_t(n) * 8) != hipSuccess ||
+      (h->sim_ok && hipMalloc(&h->d_retry2, size_t(n) * 8) != hipSuccess)) {
     (void)hipGetLastError();
     return DIP_E_NOMEM;
   }
@@ -525,52 +544,104 @@ int apply_pick(dip_sim *h, const Pick &p, int *variant, int *wpb, int *max_block
   *wpb = p.wpb;
   *lds = lds_for(h, p.v, p.wpb);
   int mb = p.nb * h->n_cu;
-  if (p.v == 4 || p.v == 6) {
+  if (p.v == 4) {
     const int64_t per_block = scratch_need(h, p.v, p.wpb, 1);
     mb = int(std::min<int64_t>(mb, std::max<int64_t>(1, kScratchCap / per_block)));
-    int rc = ensure_scratch(h, p.v, scratch_need(h, p.v, p.wpb, mb));
+    int rc = ensure_scratch(h, scratch_need(h, p.v, p.wpb, mb));
     if (rc != DIP_OK) return rc;
   }
   *max_blocks = mb;
   return DIP_OK;
 }
 
+// Launch shape of the simulation kernel for the current table image and a
+// pool size: the waves per block (one table copy per block) that keep the
+// most waves resident per CU, fewer blocks on ties.  false if nothing fits.
+bool sim_shape(dip_sim *h, int slots, int forced_wpb, int *wpb, int *max_blocks, int64_t *lds_out) {
+  const int64_t tab = int64_t(h->sim_tab_vec) * 16;
+  const int64_t grp = sim_group_bytes(1 << h->pwl, slots);
+  const void *k = sim_kernel_ptr(h->pwl, slots, h->sim_paged);
+  int best_w = 0, best_nb = 0;
+  for (int w = 16; w >= 1; --w) {
+    if (forced_wpb && w != forced_wpb) continue;
+    const int64_t lds = tab + int64_t(w) * h->G * grp;
+    if (lds > h->lds_block_max) continue;
+    if (lds > 65536 &&
+        hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess) {
+      (void)hipGetLastError();
+      continue;
+    }
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, k, w * kWave, size_t(lds)) != hipSuccess) {
+      (void)hipGetLastError();
+      continue;
+    }
+    if (nb > 0 && nb * w > best_nb * best_w) {
+      best_w = w;
+      best_nb = nb;
+    }
+  }
+  if (best_w == 0) return false;
+  const int64_t lds = tab + int64_t(best_w) * h->G * grp;
+  if (lds > 65536 &&
+      hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  *wpb = best_w;
+  *max_blocks = best_nb * h->n_cu;
+  *lds_out = lds;
+  return true;
+}
+
+// Both passes' shapes; sim_costs_ok false when the first does not fit.
+int sim_plan(dip_sim *h) {
+  h->sim_costs_ok = false;
+  h->sim2_ok = false;
+  h->sim_state_base = int64_t(h->sim_tab_vec) * 16;
+  if (!sim_shape(h, h->pool_slots, h->forced_variant == 9 ? h->forced_wpb : 0, &h->sim_wpb,
+                 &h->sim_max_blocks, &h->sim_lds))
+    return DIP_OK;
+  h->sim_costs_ok = true;
+  if (h->pool_slots < 16)
+    h->sim2_ok = sim_shape(h, 16, 0, &h->sim2_wpb, &h->sim2_max_blocks, &h->sim2_lds);
+  return DIP_OK;
+}
+
 int choose_config(dip_sim *h) {
-  // general fallback first (always available)
+  // general configuration first (always available)
   const bool force_gen = h->forced_variant >= 1 && h->forced_variant <= 4;
   Pick g = best_of(h, force_gen ? h->forced_variant : 1, force_gen ? h->forced_variant : 4,
                    force_gen ? h->forced_wpb : 0);
   if (g.v == 0) return DIP_E_UNSUPPORTED;
   int rc = apply_pick(h, g, &h->gen_variant, &h->gen_wpb, &h->gen_max_blocks, &h->gen_lds);
   if (rc != DIP_OK) return rc;
-  if (force_gen || (!h->pipe_ok && !h->pool_ok)) {
-    if (h->forced_variant >= 5) return DIP_E_UNSUPPORTED;
+  if (force_gen || !h->pool_ok) {
+    if (h->forced_variant >= 8) return DIP_E_UNSUPPORTED;
     h->variant = h->gen_variant;
     h->wpb = h->gen_wpb;
     h->max_blocks = h->gen_max_blocks;
     h->lds_bytes = h->gen_lds;
     return DIP_OK;
   }
-  Pick p;
-  if (h->forced_variant >= 5) {
-    p = best_of(h, h->forced_variant, h->forced_variant, h->forced_wpb);
-  } else if (h->pool_ok && best_of(h, 8, 8, h->forced_wpb).v == 8) {
-    p = best_of(h, 8, 8, h->forced_wpb);
-  } else {
-    // LDS-resident if at least 4 waves stay resident (records in LDS when that
-    // keeps as many waves), else tables in device scratch
-    Pick rl = best_of(h, 7, 7, h->forced_wpb);
-    Pick gl = best_of(h, 5, 5, h->forced_wpb);
-    Pick lds = (rl.v && rl.waves >= gl.waves) ? rl : gl;
-    Pick glob = best_of(h, 6, 6, h->forced_wpb);
-    p = (lds.v && lds.waves >= 4) ? lds : (glob.v ? glob : lds);
-  }
+  if (h->forced_variant == 9 && !h->sim_ok) return DIP_E_UNSUPPORTED;
+  // variant 8's shape: also what variant 9 runs for costs outside its records
+  Pick p = best_of(h, 8, 8, h->forced_variant == 8 ? h->forced_wpb : 0);
   if (p.v == 0) return DIP_E_UNSUPPORTED;
-  if (p.v == 8) {
-    rc = ensure_fallback(h);
-    if (rc != DIP_OK) return rc;
+  rc = ensure_fallback(h);
+  if (rc != DIP_OK) return rc;
+  rc = apply_pick(h, p, &h->variant, &h->wpb, &h->max_blocks, &h->lds_bytes);
+  if (rc != DIP_OK) return rc;
+  if (h->sim_ok && h->forced_variant != 8) {
+    h->variant = 9;
+    if (h->costs_set) {
+      rc = sim_plan(h);
+      if (rc != DIP_OK) return rc;
+      // a forced shape the current costs or the LDS do not allow
+      if (h->forced_variant == 9 && !h->sim_costs_ok) return DIP_E_UNSUPPORTED;
+    }
   }
-  return apply_pick(h, p, &h->variant, &h->wpb, &h->max_blocks, &h->lds_bytes);
+  return DIP_OK;
 }
 
 int check_costs_against(int32_t P, const int32_t *n_ops, const int32_t *pred_ptr,
@@ -610,8 +681,17 @@ int check_costs_against(int32_t P, const int32_t *n_ops, const int32_t *pred_ptr
 }
 
 struct StageLayout {
-  int64_t rec, edge, busy, prec, md, rec16, jk, prec8, pedge, total;
+  int64_t rec, edge, busy, md, prec8, pedge, stab, slane, total;
 };
+
+// bytes of the simulation kernel's table image at most (direct records, or
+// pages with a page map, then the extra edges)
+int64_t sim_tab_bound(const dip_sim *h) {
+  const int64_t direct = align16(int64_t(h->N) * 8);
+  const int64_t pages = int64_t(h->N) / kSimPage + h->P;
+  const int64_t paged = pages * kSimPage * 8 + align16(pages * 2);
+  return std::max(direct, paged) + align16(int64_t(std::max(h->sim_n_extra, 1)) * 4);
+}
 
 StageLayout stage_layout(const dip_sim *h) {
   StageLayout L{};
@@ -619,12 +699,11 @@ StageLayout stage_layout(const dip_sim *h) {
   L.rec = off; off += align16(int64_t(h->N) * 16);
   L.edge = off; off += align16(int64_t(std::max(h->E, 1)) * 8);
   L.busy = off; off += align16(int64_t(h->P) * 4);
-  L.prec = off; off += h->pipe_ok ? align16(int64_t(h->N) * 32) : 0;
   L.md = off; off += align16(int64_t(h->N) * 4);
-  L.rec16 = off; off += h->pipe_ok ? align16(int64_t(h->N) * 16) : 0;
-  L.jk = off; off += h->pipe_ok ? align16(int64_t(std::max(h->n_joins, 1)) * 4) : 0;
   L.prec8 = off; off += h->pool_ok ? align16(int64_t(h->N) * 16) : 0;
   L.pedge = off; off += h->pool_ok ? align16(int64_t(std::max(h->n_extra, 1)) * 8) : 0;
+  L.stab = off; off += h->sim_ok ? sim_tab_bound(h) : 0;
+  L.slane = off; off += h->sim_ok ? align16(int64_t(h->P) * 16) : 0;
   L.total = off;
   return L;
 }
@@ -668,6 +747,126 @@ int upload_greedy_records(dip_sim *h, const dip_costs *c, hipStream_t stream) {
   return DIP_OK;
 }
 
+// The simulation kernel's tables for these costs (see kern_sim.hip and
+// internal.h for the record and edge-word formats): records relative to their
+// op, stored directly when small, else as pages of kSimPage records of one
+// rank with equal pages kept once; then the extra edges.  Leaves
+// sim_costs_ok false (evaluate then runs variant 8) when a cost or latency is
+// outside the record's fields or the tables do not fit in LDS.
+int upload_sim_tables(dip_sim *h, const dip_costs *c, const int32_t *busy, const StageLayout &L,
+                      hipStream_t stream) {
+  h->sim_costs_ok = false;
+  for (int32_t g = 0; g < h->N; ++g)
+    if (uint32_t(c->op_cost[g]) > kSimCostMax) return DIP_OK;
+  for (int32_t e = 0; e < h->E; ++e)
+    if (uint32_t(c->edge_comm[e]) > kSimCommMax) return DIP_OK;
+  const int32_t P = h->P;
+  // an edge between two ops of one rank with zero latency holds by the order
+  // alone once the tile check has verified that the predecessor comes first
+  // (it flags the candidate deadlocked otherwise): dropped, its producer then
+  // publishes no end time for it
+  h->sim_drop_self = h->to_ok && use_tile_check(h);
+  auto dropped = [&](int32_t g, int32_t k) {
+    return h->sim_drop_self && h->rank_of[h->pred_op[k]] == h->rank_of[g] && c->edge_comm[k] == 0;
+  };
+  std::vector<int32_t> readers(size_t(h->N), 0);
+  for (int32_t g = 0; g < h->N; ++g)
+    for (int32_t k = h->pred_ptr[g]; k < h->pred_ptr[g + 1]; ++k)
+      if (!dropped(g, k)) ++readers[h->pred_op[k]];
+  std::vector<uint32_t> rec(size_t(h->N) * 2), extra;
+  extra.reserve(size_t(std::max(h->sim_n_extra, 1)));
+  std::vector<int32_t> kept;
+  auto edge_word = [&](int32_t g, int32_t k, bool last) {
+    const int32_t p = h->pred_op[k];
+    const int32_t r = h->rank_of[g], rp = h->rank_of[p];
+    const int32_t d = (p - h->rank_off[rp]) - (g - h->rank_off[r]);
+    const uint32_t dr = uint32_t((rp - r + P) % P);
+    return (uint32_t(d) & 0x3fffu) | (dr << 14) | (uint32_t(c->edge_comm[k]) << 20) |
+           (last ? kSimLast : 0u);
+  };
+  for (int32_t g = 0; g < h->N; ++g) {
+    kept.clear();
+    for (int32_t k = h->pred_ptr[g]; k < h->pred_ptr[g + 1]; ++k)
+      if (!dropped(g, k)) kept.push_back(k);
+    const int32_t np = int32_t(kept.size());
+    rec[2 * g] = uint32_t(c->op_cost[g]) | (uint32_t(readers[g]) << 20) |
+                 (np > 1 ? kSimMulti : 0u) | (np > 0 ? kSimHasPred : 0u);
+    if (np == 1) {
+      rec[2 * g + 1] = edge_word(g, kept[0], true);
+    } else if (np > 1) {
+      rec[2 * g + 1] = uint32_t(extra.size());
+      for (int32_t i = 0; i < np; ++i) extra.push_back(edge_word(g, kept[i], i == np - 1));
+    } else {
+      rec[2 * g + 1] = 0;
+    }
+  }
+  unsigned char *img = h->h_stage + L.stab;
+  int32_t *lane = reinterpret_cast<int32_t *>(h->h_stage + L.slane);
+  const int64_t direct = align16(int64_t(h->N) * 8);
+  int64_t off_pmap = 0, recs_bytes = direct;
+  std::vector<uint16_t> pmap;
+  std::vector<int32_t> recb(P);
+  // pages: each rank's records in runs of kSimPage local ids, equal runs once
+  bool paged = false;
+  if (direct > kSimDirectMax) {
+    std::unordered_map<std::string, int32_t> seen;
+    std::vector<uint32_t> pages;
+    bool ok = true;
+    for (int r = 0; r < P && ok; ++r) {
+      recb[r] = int32_t(pmap.size());
+      for (int32_t p0 = 0; p0 < h->n_ops[r]; p0 += kSimPage) {
+        std::string key(size_t(kSimPage) * 8, '\0');
+        const int32_t n = std::min(kSimPage, h->n_ops[r] - p0);
+        std::memcpy(&key[0], &rec[2 * size_t(h->rank_off[r] + p0)], size_t(n) * 8);
+        auto it = seen.find(key);
+        int32_t id;
+        if (it == seen.end()) {
+          id = int32_t(seen.size());
+          seen.emplace(key, id);
+          const size_t at = pages.size();
+          pages.resize(at + size_t(kSimPage) * 2);
+          std::memcpy(&pages[at], key.data(), key.size());
+        } else {
+          id = it->second;
+        }
+        if (id > 0xffff) ok = false;
+        pmap.push_back(uint16_t(id));
+      }
+    }
+    const int64_t pbytes = int64_t(pages.size()) * 4;
+    if (ok && pbytes + align16(int64_t(pmap.size()) * 2) < direct) {
+      paged = true;
+      recs_bytes = pbytes;
+      std::memcpy(img, pages.data(), size_t(pbytes));
+      off_pmap = pbytes;
+      std::memcpy(img + off_pmap, pmap.data(), pmap.size() * 2);
+      recs_bytes = pbytes + align16(int64_t(pmap.size()) * 2);
+    }
+  }
+  if (!paged) {
+    std::memcpy(img, rec.data(), size_t(h->N) * 8);
+    for (int r = 0; r < P; ++r) recb[r] = h->rank_off[r];
+    recs_bytes = direct;
+  }
+  const int64_t off_extra = recs_bytes;
+  if (!extra.empty()) std::memcpy(img + off_extra, extra.data(), extra.size() * 4);
+  const int64_t total = off_extra + align16(int64_t(std::max<size_t>(extra.size(), 1)) * 4);
+  if (total > L.slane - L.stab || total > h->sim_tab_cap) return DIP_OK;
+  for (int r = 0; r < P; ++r) {
+    lane[4 * r] = h->rank_off[r];
+    lane[4 * r + 1] = h->n_ops[r];
+    lane[4 * r + 2] = busy[r];
+    lane[4 * r + 3] = recb[r];
+  }
+  h->sim_paged = paged;
+  h->sim_off_pmap = uint32_t(off_pmap);
+  h->sim_off_extra = uint32_t(off_extra);
+  h->sim_tab_vec = int32_t(total / 16);
+  DIP_HIP(hipMemcpyAsync(h->d_sim_tab, img, size_t(total), hipMemcpyHostToDevice, stream));
+  DIP_HIP(hipMemcpyAsync(h->d_sim_lane, lane, size_t(P) * 16, hipMemcpyHostToDevice, stream));
+  return sim_plan(h);
+}
+
 int upload_costs(dip_sim *h, const dip_costs *c, hipStream_t stream) {
   int64_t total = 0;
   int rc = check_costs_against(h->P, h->n_ops.data(), h->pred_ptr.data(), h->op_slot.data(),
@@ -676,6 +875,11 @@ int upload_costs(dip_sim *h, const dip_costs *c, hipStream_t stream) {
   if (h->stage_pending) {
     DIP_HIP(hipEventSynchronize(h->stage_done));
     h->stage_pending = false;
+  }
+  if (c->op_cost != h->last_cost.data()) {
+    h->last_cost.assign(c->op_cost, c->op_cost + h->N);
+    h->last_comm.assign(c->edge_comm, c->edge_comm + h->E);
+    h->last_act.assign(c->slot_act, c->slot_act + h->n_slots);
   }
   const StageLayout L = stage_layout(h);
   int4 *rec = reinterpret_cast<int4 *>(h->h_stage + L.rec);
@@ -727,50 +931,9 @@ int upload_costs(dip_sim *h, const dip_costs *c, hipStream_t stream) {
     if (h->n_extra > 0)
       DIP_HIP(hipMemcpyAsync(h->d_pool_edge, pe, size_t(h->n_extra) * 8, hipMemcpyHostToDevice, stream));
   }
-  h->pipe_costs_ok = false;
-  if (h->pipe_ok) {
-    // pipeline records: {cost, memdelta, polled entry (byte offset), comm}
-    // and {join block fed (byte offset, 0 = none), its k, comm into it}
-    int32_t *pr = reinterpret_cast<int32_t *>(h->h_stage + L.prec);
-    for (int32_t g = 0; g < h->N; ++g) {
-      int32_t *q = pr + int64_t(g) * 8;
-      const int32_t np = h->pred_ptr[g + 1] - h->pred_ptr[g];
-      q[0] = rec[g].x;
-      q[1] = rec[g].y;
-      if (np == 0) {
-        q[2] = h->N * 4;
-        q[3] = 0;
-      } else if (np == 1) {
-        q[2] = h->pred_op[h->pred_ptr[g]] * 4;
-        q[3] = c->edge_comm[h->pred_ptr[g]];
-      } else {
-        q[2] = int32_t(h->join_base) + h->join_of[g] * 16;
-        q[3] = 0;
-      }
-      const int32_t o = h->feeds_join[g];
-      q[4] = o < 0 ? 0 : int32_t(h->join_base) + h->join_of[o] * 16;
-      q[5] = o < 0 ? 0 : h->pred_ptr[o + 1] - h->pred_ptr[o];
-      q[6] = o < 0 ? 0 : c->edge_comm[h->feed_edge[g]];
-      q[7] = 0;
-    }
-    DIP_HIP(hipMemcpyAsync(h->d_prec, pr, size_t(h->N) * 32, hipMemcpyHostToDevice, stream));
-    h->pipe_costs_ok = total < int64_t(kValueLimit);
-    // compact records: offsets and latencies in 16 bits
-    int4 *r16 = reinterpret_cast<int4 *>(h->h_stage + L.rec16);
-    int32_t *jk = reinterpret_cast<int32_t *>(h->h_stage + L.jk);
-    bool fits = lds16_shape_ok(h);
-    for (int32_t g = 0; g < h->N; ++g) {
-      const int32_t *q = pr + int64_t(g) * 8;
-      fits = fits && q[3] <= 0xffff && q[6] <= 0xffff;
-      r16[g] = make_int4(q[0], q[1], int32_t(uint32_t(q[2]) | (uint32_t(q[3]) << 16)),
-                         int32_t(uint32_t(q[4]) | (uint32_t(q[6]) << 16)));
-    }
-    for (int32_t g = 0; g < h->N; ++g)
-      if (h->join_of[g] >= 0) jk[h->join_of[g]] = h->pred_ptr[g + 1] - h->pred_ptr[g];
-    DIP_HIP(hipMemcpyAsync(h->d_rec16, r16, size_t(h->N) * 16, hipMemcpyHostToDevice, stream));
-    if (h->n_joins > 0)
-      DIP_HIP(hipMemcpyAsync(h->d_jk, jk, size_t(h->n_joins) * 4, hipMemcpyHostToDevice, stream));
-    h->lds16_costs_ok = h->pipe_costs_ok && fits;
+  if (h->sim_ok) {
+    rc = upload_sim_tables(h, c, busy, L, stream);
+    if (rc != DIP_OK) return rc;
   }
   if (h->gr_ok) {
     rc = upload_greedy_records(h, c, stream);
@@ -880,23 +1043,22 @@ void release(dip_sim *h) {
   (void)hipDeviceSynchronize();
   if (h->d_rec) (void)hipFree(h->d_rec);
   if (h->d_edge) (void)hipFree(h->d_edge);
-  if (h->d_prec) (void)hipFree(h->d_prec);
   if (h->d_md) (void)hipFree(h->d_md);
-  if (h->d_rec16) (void)hipFree(h->d_rec16);
-  if (h->d_jk) (void)hipFree(h->d_jk);
+  if (h->d_selfp) (void)hipFree(h->d_selfp);
+  if (h->d_sim_tab) (void)hipFree(h->d_sim_tab);
+  if (h->d_sim_lane) (void)hipFree(h->d_sim_lane);
   if (h->d_rank_off) (void)hipFree(h->d_rank_off);
   if (h->d_busy) (void)hipFree(h->d_busy);
   if (h->d_cap) (void)hipFree(h->d_cap);
-  if (h->d_tc_plan) (void)hipFree(h->d_tc_plan);
+  if (h->tc.d_plan) (void)hipFree(h->tc.d_plan);
+  if (h->to.d_plan) (void)hipFree(h->to.d_plan);
   if (h->d_scratch_gen) (void)hipFree(h->d_scratch_gen);
   if (h->d_scratch_fb) (void)hipFree(h->d_scratch_fb);
   if (h->d_pool_rec) (void)hipFree(h->d_pool_rec);
   if (h->d_pool_edge) (void)hipFree(h->d_pool_edge);
   if (h->d_retry) (void)hipFree(h->d_retry);
+  if (h->d_retry2) (void)hipFree(h->d_retry2);
   if (h->d_retry_count) (void)hipFree(h->d_retry_count);
-  if (h->h_retry_seen) (void)hipHostFree(h->h_retry_seen);
-  if (h->retry_seen_ev) (void)hipEventDestroy(h->retry_seen_ev);
-  if (h->d_scratch_pipe) (void)hipFree(h->d_scratch_pipe);
   release_rollouts(h);
   release_greedy(h);
   release_memopt(h);
@@ -969,8 +1131,7 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
   h->cap.assign(t->mem_cap, t->mem_cap + h->P);
   h->pwl = ceil_pow2_log2(h->P);
   h->G = kWave >> h->pwl;
-  // pipeline kernel eligibility: the predecessors of a multi-predecessor op
-  // run on one rank, and no op feeds two such ops
+  // kernel eligibility
   {
     std::vector<int32_t> &rank_of = h->rank_of;
     rank_of.assign(h->N, 0);
@@ -979,6 +1140,16 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
     // pool kernel eligibility: at most 15 consumers per op (4-bit reader
     // counts), fewer than 2^16 edges after the ops' first ones (16-bit index
     // in the record; tags are rank-local ids + 1 <= 32768 by construction)
+    h->self_pred.assign(h->N, 0);
+    h->self_ok = true;
+    for (int32_t g = 0; g < h->N; ++g)
+      for (int32_t k = h->pred_ptr[g]; k < h->pred_ptr[g + 1]; ++k) {
+        const int32_t p = h->pred_op[k];
+        if (rank_of[p] != rank_of[g]) continue;
+        if (h->self_pred[g] != 0) h->self_ok = false;
+        h->self_pred[g] = p - h->rank_off[rank_of[p]] + 1;
+        h->self_ranks |= uint64_t(1) << rank_of[g];
+      }
     h->n_cons.assign(h->N, 0);
     bool pool = int64_t(h->N) * 16 < INT32_MAX;
     int64_t extra = 0;
@@ -993,27 +1164,20 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
     const int64_t tab = align16(int64_t(h->N) * 16) + align16(int64_t(std::max(h->n_extra, 1)) * 8);
     h->pool_tab = h->pool_ok && tab <= kPoolTabLimit;
     h->pool_tab_bytes = h->pool_tab ? tab : 0;
-    h->join_of.assign(h->N, -1);
-    h->feeds_join.assign(h->N, -1);
-    h->feed_edge.assign(h->N, -1);
-    bool ok = true;
-    for (int32_t g = 0; g < h->N && ok; ++g) {
-      const int32_t b = h->pred_ptr[g], e = h->pred_ptr[g + 1];
-      if (e - b < 2) continue;
-      h->join_of[g] = h->n_joins++;
-      for (int32_t k = b; k < e && ok; ++k) {
-        const int32_t p = h->pred_op[k];
-        if (rank_of[p] != rank_of[h->pred_op[b]] || h->feeds_join[p] >= 0) ok = false;
-        h->feeds_join[p] = g;
-        h->feed_edge[p] = k;
-      }
+    // simulation kernel eligibility: local ids below 8192 (14-bit id
+    // differences), at most 15 consumers per op (as the pool kernel)
+    int32_t max_nr = 0;
+    for (int r = 0; r < h->P; ++r) max_nr = std::max(max_nr, h->n_ops[r]);
+    int64_t sim_extra = 0;
+    for (int32_t g = 0; g < h->N; ++g) {
+      const int32_t np = h->pred_ptr[g + 1] - h->pred_ptr[g];
+      if (np > 1) sim_extra += np;
     }
-    // op entries, the zero cell (index N), the never-ready cell (index N + 1)
-    const int64_t base_words = (int64_t(h->N) + 2 + 3) & ~int64_t(3);
-    const int64_t stride = base_words + 4 * int64_t(h->n_joins);
-    h->pipe_ok = ok && stride * 4 < int64_t(INT32_MAX);
-    h->join_base = uint32_t(base_words * 4);
-    h->tab_stride = int32_t(stride);
+    h->sim_ok = h->pool_ok && max_nr <= kSimDeltaMax + 1 && sim_extra < (int64_t(1) << 24);
+    h->sim_n_extra = int32_t(std::min<int64_t>(sim_extra, INT32_MAX));
+    // pools: 8 slots per rank (the simulation kernel's candidates that fill
+    // them go through a second pass with 16)
+    h->pool_slots = 8;
   }
 
   auto hip_fail = [&](hipError_t e) { g_last_hip = e; release(h); return int(DIP_E_HIP); };
@@ -1032,16 +1196,21 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
   if ((e = hipMalloc(&h->d_rec, size_t(h->N) * 16)) != hipSuccess) return hip_fail(e);
   if ((e = hipMalloc(&h->d_edge, size_t(std::max(h->E, 1)) * 8)) != hipSuccess) return hip_fail(e);
   if ((e = hipMalloc(&h->d_md, size_t(h->N) * 4)) != hipSuccess) return hip_fail(e);
+  if (h->self_ok) {
+    if ((e = hipMalloc(&h->d_selfp, size_t(h->N) * 4)) != hipSuccess) return hip_fail(e);
+    if ((e = hipMemcpy(h->d_selfp, h->self_pred.data(), size_t(h->N) * 4,
+                       hipMemcpyHostToDevice)) != hipSuccess)
+      return hip_fail(e);
+  }
   if (h->pool_ok) {
     if ((e = hipMalloc(&h->d_pool_rec, size_t(h->N) * 16)) != hipSuccess) return hip_fail(e);
     if ((e = hipMalloc(&h->d_pool_edge, size_t(std::max(h->n_extra, 1)) * 8)) != hipSuccess)
       return hip_fail(e);
   }
-  if (h->pipe_ok) {
-    if ((e = hipMalloc(&h->d_prec, size_t(h->N) * 32)) != hipSuccess) return hip_fail(e);
-    if ((e = hipMalloc(&h->d_rec16, size_t(h->N) * 16)) != hipSuccess) return hip_fail(e);
-    if ((e = hipMalloc(&h->d_jk, size_t(std::max(h->n_joins, 1)) * 4)) != hipSuccess)
-      return hip_fail(e);
+  if (h->sim_ok) {
+    h->sim_tab_cap = sim_tab_bound(h);
+    if ((e = hipMalloc(&h->d_sim_tab, size_t(h->sim_tab_cap))) != hipSuccess) return hip_fail(e);
+    if ((e = hipMalloc(&h->d_sim_lane, size_t(h->P) * 16)) != hipSuccess) return hip_fail(e);
   }
   if ((e = hipMalloc(&h->d_rank_off, size_t(h->P + 1) * 4)) != hipSuccess) return hip_fail(e);
   if ((e = hipMalloc(&h->d_busy, size_t(h->P) * 4)) != hipSuccess) return hip_fail(e);
@@ -1071,9 +1240,9 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
 }
 
 int dip_sim_configure(dip_sim *h, int32_t variant, int32_t waves_per_block) {
-  if (!h || variant < 0 || variant > 8) return DIP_E_INVAL;
+  if (!h || variant < 0 || variant > 9 || (variant >= 5 && variant <= 7)) return DIP_E_INVAL;
   if (!(waves_per_block == 0 || waves_per_block == 1 || waves_per_block == 2 ||
-        waves_per_block == 4 || waves_per_block == 8))
+        waves_per_block == 4 || waves_per_block == 8 || (variant == 9 && waves_per_block == 16)))
     return DIP_E_INVAL;
   const int old_v = h->forced_variant, old_w = h->forced_wpb;
   h->forced_variant = variant;
@@ -1106,28 +1275,36 @@ int dip_sim_configure_check(dip_sim *h, int32_t mode) {
   if (!h || mode < 0 || mode > 2) return DIP_E_INVAL;
   if (!h->pool_ok || (mode == 1 && !h->wc_ok) || (mode == 2 && !h->tc_ok)) return DIP_E_UNSUPPORTED;
   h->check_mode = mode;
+  // the simulation kernel's tables drop own-rank edges only behind the tile
+  // check: rebuild them from the last costs when that changes
+  if (h->sim_ok && h->costs_set && h->sim_drop_self != (h->to_ok && use_tile_check(h))) {
+    const dip_costs c{h->last_cost.data(), h->last_comm.data(), h->last_act.data()};
+    int rc = upload_costs(h, &c, nullptr);
+    if (rc != DIP_OK) return rc;
+    DIP_HIP(hipStreamSynchronize(nullptr));
+  }
   return DIP_OK;
 }
 
 int dip_sim_get_info(const dip_sim *h, dip_sim_info *info) {
   if (!h || !info) return DIP_E_INVAL;
-  const bool pipe_off = h->costs_set &&
-                        ((h->variant == 6 && !h->pipe_costs_ok) ||
-                         ((h->variant == 5 || h->variant == 7) && !h->lds16_costs_ok));
+  // variant 9 reports its shape for the current costs; before any costs it
+  // has none yet (0 waves), and for costs outside its records variant 8 runs
+  const bool sim = h->variant == 9 && (!h->costs_set || h->sim_costs_ok);
+  const int v = h->variant == 9 && !sim ? 8 : h->variant;
   info->n_ranks = h->P;
   info->n_ops_total = h->N;
   info->n_edges = h->E;
-  info->variant = pipe_off ? h->gen_variant : h->variant;
+  info->variant = v;
   info->cand_stride = h->stride;
   info->lanes_per_group = 1 << h->pwl;
   info->groups_per_wave = h->G;
-  info->waves_per_block = pipe_off ? h->gen_wpb : h->wpb;
-  info->lds_bytes = int32_t(pipe_off ? h->gen_lds : h->lds_bytes);
-  info->max_blocks = pipe_off ? h->gen_max_blocks : h->max_blocks;
-  info->scratch_bytes = h->scratch_gen_bytes + h->scratch_pipe_bytes + h->scratch_fb_bytes +
-                        h->retry_cap * 8;
-  info->pool_slots = h->variant == 8 ? h->pool_slots : 0;
-  info->check_kernel = h->variant == 8 ? (use_tile_check(h) ? 2 : 1) : 0;
+  info->waves_per_block = sim ? (h->sim_costs_ok ? h->sim_wpb : 0) : h->wpb;
+  info->lds_bytes = int32_t(sim ? (h->sim_costs_ok ? h->sim_lds : 0) : h->lds_bytes);
+  info->max_blocks = sim ? (h->sim_costs_ok ? h->sim_max_blocks : 0) : h->max_blocks;
+  info->scratch_bytes = h->scratch_gen_bytes + h->scratch_fb_bytes + h->retry_cap * 8;
+  info->pool_slots = v >= 8 ? h->pool_slots : 0;
+  info->check_kernel = v >= 8 ? (use_tile_check(h) ? 2 : 1) : 0;
   info->greedy_inbox = h->gr_ok ? h->gr_K : 0;
   info->greedy_lds_bytes = h->gr_ok ? int32_t(h->gr_main.lds) : 0;
   info->greedy_retry_ring_bytes = h->gr_ok ? h->gr_ring_bytes : 0;
@@ -1157,21 +1334,8 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     h->prof_n = i + 1;
     return hipEventRecord(h->prof_ev[i], stream);
   };
-  if (h->variant == 8 && h->retry_seen_pending && hipEventQuery(h->retry_seen_ev) == hipSuccess) {
-    h->retry_seen_pending = false;
-    const int64_t retried = int64_t(*h->h_retry_seen);
-    if (!h->forced_pool_slots && h->pool_slots < 16 && retried * 256 > h->retry_seen_n) {
-      const int old_s = h->pool_slots;
-      h->pool_slots *= 2;
-      if (choose_config(h) != DIP_OK || h->variant != 8) {
-        h->pool_slots = old_s;
-        int rc = choose_config(h);
-        if (rc != DIP_OK) return rc;
-      }
-    }
-  }
   (void)hipGetLastError();
-  if (h->variant == 8) {
+  if (h->variant >= 8) {
     int rc = ensure_retry(h, n_cand);
     if (rc != DIP_OK) return rc;
     DIP_HIP(mark(0));
@@ -1181,45 +1345,95 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
                                             out_peakmem, out_flags, stream);
     if (rc != DIP_OK) return rc;
     DIP_HIP(mark(1));
-
-    PoolArgs a{};
-    a.orders = orders;
-    a.n_cand = n_cand;
-    a.stride = h->stride;
-    a.out_ms = out_makespan;
-    a.out_bub = out_bubble;
-    a.out_flags = out_flags;
-    a.rec = h->d_pool_rec;
-    a.edge = h->d_pool_edge;
-    a.rank_off = h->d_rank_off;
-    a.busy = h->d_busy;
-    a.P = h->P;
-    a.wpb = h->wpb;
-    a.retry = h->d_retry;
-    a.retry_count = h->d_retry_count;
-    a.rec_bytes = h->N * 16;
-    a.edge_bytes = std::max(h->n_extra, 1) * 8;
-    a.tab_edges = uint32_t(align16(int64_t(h->N) * 16));
-    a.pool_base = uint32_t(h->pool_tab_bytes);
-    a.round_limit = uint32_t(h->N) + uint32_t(h->E) + 16u;
-    const int64_t per_block = int64_t(h->wpb) * h->G;
-    const int blocks = int(std::min<int64_t>((n_cand + per_block - 1) / per_block, h->max_blocks));
-    // candidates past the resident slots: handed out on demand when every
-    // slot runs several in sequence (fixed successors let unlucky slots pile
-    // up long candidates); with fewer, fixed successors keep the second ones
-    // in few waves, and the other waves exit
-    const int64_t n_slots = int64_t(blocks) * per_block;
-    a.next_cand = n_cand >= 2 * n_slots ? h->d_retry_count + 1 : nullptr;
-    // short candidates finish often, and one counter serving every request
-    // becomes the bottleneck (2.4x on the 656-op workload at 850 K
-    // candidates): there the first 90 % of the batch goes to fixed
-    // successors and only the rest on demand; long ones take all on demand
-    a.static_end = !a.next_cand ? 0
-                   : h->N <= 4096 ? n_slots * ((n_cand / 10 * 9) / n_slots)
-                                  : n_slots;   // the first n_slots are every slot's first
-    DIP_HIP(launch_pool(h->pwl, h->pool_slots, h->pool_tab, blocks, h->wpb, size_t(h->lds_bytes),
-                        stream, a));
-    DIP_HIP(mark(2));
+    const uint32_t round_limit = uint32_t(h->N) + uint32_t(h->E) + 16u;
+    // candidates past the resident groups: long ones are handed out on demand
+    // when every group runs several in sequence (fixed successors let unlucky
+    // groups pile up long candidates); with fewer, fixed successors keep the
+    // second ones in few waves, and the other waves exit.  Short candidates
+    // finish so often that one counter serving every request becomes the
+    // bottleneck: they take fixed successors unless the batch holds at least
+    // four per group, and then only the last 10 % go on demand.
+    auto static_end_for = [&](int64_t n_slots) -> int64_t {
+      if (h->N > 4096) return n_cand >= 2 * n_slots ? n_slots : INT64_MAX;
+      return n_cand >= 4 * n_slots ? n_slots * ((n_cand / 10 * 9) / n_slots) : INT64_MAX;
+    };
+    const int64_t *retry_list = h->d_retry;
+    const uint32_t *retry_count = h->d_retry_count;
+    h->last_stream = stream;
+    h->last_pass2 = false;
+    if (h->variant == 9 && h->sim_costs_ok) {
+      SimArgs a{};
+      a.orders = orders;
+      a.n_cand = n_cand;
+      a.stride = h->stride;
+      a.out_ms = out_makespan;
+      a.out_bub = out_bubble;
+      a.out_flags = out_flags;
+      a.tab = h->d_sim_tab;
+      a.tab_vec = h->sim_tab_vec;
+      a.off_pmap = h->sim_off_pmap;
+      a.off_extra = h->sim_off_extra;
+      a.lane_info = reinterpret_cast<const int32_t *>(h->d_sim_lane);
+      a.state_base = uint32_t(h->sim_state_base);
+      a.P = h->P;
+      a.wpb = h->sim_wpb;
+      a.retry = h->d_retry;
+      a.retry_count = h->d_retry_count;
+      a.round_limit = round_limit;
+      const int64_t per_block = int64_t(h->sim_wpb) * h->G;
+      const int blocks =
+          int(std::min<int64_t>((n_cand + per_block - 1) / per_block, h->sim_max_blocks));
+      a.static_end = static_end_for(int64_t(blocks) * per_block);
+      DIP_HIP(launch_sim(h->pwl, h->pool_slots, h->sim_paged, blocks, h->sim_wpb,
+                         size_t(h->sim_lds), stream, a));
+      DIP_HIP(mark(2));
+      if (h->sim2_ok) {
+        // the candidates whose pools filled, again with 16 slots per pool
+        // (deadlocked orders fill small pools too; larger ones tell them
+        // from merely crowded ones); its own retries go to the general kernel
+        a.list = h->d_retry;
+        a.list_count = h->d_retry_count;
+        a.retry = h->d_retry2;
+        a.retry_count = h->d_retry_count + 2;
+        a.wpb = h->sim2_wpb;
+        a.static_end = INT64_MAX;
+        DIP_HIP(launch_sim(h->pwl, 16, h->sim_paged, h->sim2_max_blocks, h->sim2_wpb,
+                           size_t(h->sim2_lds), stream, a));
+        retry_list = h->d_retry2;
+        retry_count = h->d_retry_count + 2;
+        h->last_pass2 = true;
+      }
+      DIP_HIP(mark(3));
+    } else {
+      PoolArgs a{};
+      a.orders = orders;
+      a.n_cand = n_cand;
+      a.stride = h->stride;
+      a.out_ms = out_makespan;
+      a.out_bub = out_bubble;
+      a.out_flags = out_flags;
+      a.rec = h->d_pool_rec;
+      a.edge = h->d_pool_edge;
+      a.rank_off = h->d_rank_off;
+      a.busy = h->d_busy;
+      a.P = h->P;
+      a.wpb = h->wpb;
+      a.retry = h->d_retry;
+      a.retry_count = h->d_retry_count;
+      a.rec_bytes = h->N * 16;
+      a.edge_bytes = std::max(h->n_extra, 1) * 8;
+      a.tab_edges = uint32_t(align16(int64_t(h->N) * 16));
+      a.pool_base = uint32_t(h->pool_tab_bytes);
+      a.round_limit = round_limit;
+      const int64_t per_block = int64_t(h->wpb) * h->G;
+      const int blocks = int(std::min<int64_t>((n_cand + per_block - 1) / per_block, h->max_blocks));
+      const int64_t se = static_end_for(int64_t(blocks) * per_block);
+      a.next_cand = se == INT64_MAX ? nullptr : h->d_retry_count + 1;
+      a.static_end = se == INT64_MAX ? 0 : se;
+      DIP_HIP(launch_pool(h->pwl, h->pool_slots, h->pool_tab, blocks, h->wpb,
+                          size_t(h->lds_bytes), stream, a));
+      DIP_HIP(mark(2));
+    }
 
     GeneralArgs f{};
     f.orders = orders;
@@ -1241,63 +1455,10 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
     f.N = h->N;
     f.E = h->E;
     f.wpb = 1;
-    f.list = h->d_retry;
-    f.list_count = h->d_retry_count;
+    f.list = retry_list;
+    f.list_count = retry_count;
     DIP_HIP(launch_general(h->fb_variant, h->fb_blocks, 1, size_t(h->fb_lds), stream, f));
-    DIP_HIP(mark(3));
-    if (!h->forced_pool_slots && h->pool_slots < 16 && !h->retry_seen_pending) {
-      if (!h->h_retry_seen) {
-        DIP_HIP(hipHostMalloc(reinterpret_cast<void **>(&h->h_retry_seen), 16, hipHostMallocDefault));
-        DIP_HIP(hipEventCreateWithFlags(&h->retry_seen_ev, hipEventDisableTiming));
-      }
-      DIP_HIP(hipMemcpyAsync(h->h_retry_seen, h->d_retry_count, 4, hipMemcpyDeviceToHost, stream));
-      DIP_HIP(hipEventRecord(h->retry_seen_ev, stream));
-      h->retry_seen_pending = true;
-      h->retry_seen_n = n_cand;
-    }
-    return DIP_OK;
-  }
-
-  const bool lds_pipe = (h->variant == 5 || h->variant == 7) && h->lds16_costs_ok;
-  const bool pipe = lds_pipe || (h->variant == 6 && h->pipe_costs_ok);
-  if (pipe) {
-    PipeArgs a{};
-    a.orders = orders;
-    a.n_cand = n_cand;
-    a.stride = h->stride;
-    a.out_ms = out_makespan;
-    a.out_bub = out_bubble;
-    a.out_peak = out_peakmem;
-    a.out_flags = out_flags;
-    a.rec = h->d_prec;
-    a.md = h->d_md;
-    a.rank_off = h->d_rank_off;
-    a.busy = h->d_busy;
-    a.cap = h->d_cap;
-    const bool gs = h->variant == 6;
-    if (gs) {
-      const int64_t slots = int64_t(h->max_blocks) * h->wpb * h->G;
-      a.gtab = static_cast<int32_t *>(h->d_scratch_pipe);
-      a.gepoch = static_cast<uint8_t *>(h->d_scratch_pipe) + slots * int64_t(h->tab_stride) * 4;
-    }
-    a.P = h->P;
-    a.N = h->N;
-    a.wpb = h->wpb;
-    a.tab_stride = h->tab_stride;
-    a.n_joins = h->n_joins;
-    a.join_base = h->join_base;
-    a.rec16 = h->d_rec16;
-    a.jk = h->d_jk;
-    const int64_t per_block = int64_t(h->wpb) * h->G;
-    const int64_t want = (n_cand + per_block - 1) / per_block;
-    const int blocks = int(std::min<int64_t>(want, h->max_blocks));
-    DIP_HIP(mark(0));
-    if (lds_pipe)
-      DIP_HIP(launch_pipe_lds(h->pwl, h->variant == 7, blocks, h->wpb, size_t(h->lds_bytes),
-                              stream, a));
-    else
-      DIP_HIP(launch_pipe(h->pwl, true, blocks, h->wpb, size_t(h->lds_bytes), stream, a));
-    DIP_HIP(mark(1));
+    DIP_HIP(mark(h->prof_n));
     return DIP_OK;
   }
 
@@ -1969,6 +2130,18 @@ int dip_sim_last_profile(dip_sim *h, float *out_ms, int32_t *n_out) {
   for (int i = 0; i + 1 < h->prof_n; ++i)
     DIP_HIP(hipEventElapsedTime(out_ms + i, h->prof_ev[i], h->prof_ev[i + 1]));
   *n_out = h->prof_n - 1;
+  return DIP_OK;
+}
+
+int dip_sim_last_retries(dip_sim *h, int64_t *out_first, int64_t *out_second) {
+  if (!h || !out_first || !out_second) return DIP_E_INVAL;
+  *out_first = *out_second = 0;
+  if (h->variant < 8 || !h->d_retry_count) return DIP_OK;
+  DIP_HIP(hipStreamSynchronize(h->last_stream));
+  uint32_t cnt[4] = {0, 0, 0, 0};
+  DIP_HIP(hipMemcpy(cnt, h->d_retry_count, sizeof(cnt), hipMemcpyDeviceToHost));
+  *out_first = cnt[0];
+  *out_second = h->last_pass2 ? cnt[2] : cnt[0];
   return DIP_OK;
 }
 

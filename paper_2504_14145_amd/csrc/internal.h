@@ -44,50 +44,6 @@ const void *general_kernel_ptr(int variant);
 hipError_t launch_general(int variant, int blocks, int wpb, size_t lds, hipStream_t s,
                           const GeneralArgs &a);
 
-// ---------------------------------------------------------------- pipe
-// Pipeline kernel: every op has one predecessor, none, or several that all
-// run on one rank (folded through a join block), and every time stays below
-// 2^30 so bit 30 of an end-time entry can carry the candidate epoch.
-constexpr int32_t kEpochShift = 30;
-constexpr uint32_t kValueLimit = 1u << kEpochShift;
-
-struct PipeArgs {
-  const int16_t *orders;
-  int64_t n_cand;
-  int64_t stride;           // int16 elements per candidate row
-  int32_t *out_ms;
-  int32_t *out_bub;
-  int32_t *out_peak;
-  uint8_t *out_flags;
-  const int4 *rec;          // [N][2] {cost, memdelta, poll byte offset, comm},
-                            //        {join block byte offset or 0, join k, join comm, 0}
-  const int32_t *md;        // [N] memory delta (+act at F, -act at B)
-  const int32_t *rank_off;  // [P+1]
-  const int32_t *busy;      // [P]
-  const int32_t *cap;       // [P]
-  int32_t *gtab;            // device-scratch tables [slots][tab_stride] (global store)
-  uint8_t *gepoch;          // [slots] epoch bit of each scratch table
-  int32_t P, N, wpb;
-  int32_t tab_stride;       // int32 words per candidate table
-  int32_t n_joins;          // join blocks (4 words each) ...
-  uint32_t join_base;       // ... starting at this byte offset of a table
-  // compact form for the LDS-resident kernel (tables under 64 KiB, latencies
-  // under 2^16): {cost, memdelta, poll offset | comm << 16,
-  //               join block offset | join comm << 16}
-  const int4 *rec16;        // [N]
-  const int32_t *jk;        // [n_joins] predecessors of each join
-};
-
-const void *pipe_kernel_ptr(int pwl, bool global_store);
-hipError_t launch_pipe(int pwl, bool global_store, int blocks, int wpb, size_t lds,
-                       hipStream_t s, const PipeArgs &a);
-
-// LDS-resident pipeline kernel: end-time tables and order rows in LDS,
-// records in LDS (rec_lds) or read through the caches.
-const void *pipe_lds_kernel_ptr(int pwl, bool rec_lds);
-hipError_t launch_pipe_lds(int pwl, bool rec_lds, int blocks, int wpb, size_t lds,
-                           hipStream_t s, const PipeArgs &a);
-
 // ---------------------------------------------------------------- check
 // Order-only verdict of each candidate: permutation check, per-rank peak
 // memory, cap flag (one wavefront per candidate; an op-id bitmap in LDS).
@@ -103,8 +59,9 @@ struct CheckArgs {
   const int32_t *rank_off;  // [P+1]
   const int32_t *cap;       // [P]
   int32_t P, N, wpb;
-  uint32_t *retry_count;    // [2] zeroed by the kernel when not null (the pool
-                            // kernel's retry count and candidate counter)
+  uint32_t *retry_count;    // [4] zeroed by the kernel when not null (retry
+                            // counts and the on-demand candidate counter of
+                            // the simulation passes)
 };
 
 // bytes of one candidate's op-id bitmap
@@ -129,11 +86,14 @@ struct TileCheckArgs {
   const int32_t *rank_off;  // [P+1]
   const int32_t *cap;       // [P]
   const int32_t *plan;      // [nw+1] offsets into the rank list, then the list [P]
+  const int32_t *selfp;     // [N] local id + 1 of the op's predecessor on its own rank
+                            // (0: none): what the order pass reads in place of md
   int32_t P, nw;
   int32_t md_bytes;         // bytes of a wave's delta area (16-aligned)
   int32_t region_bytes;     // bytes per wave: delta area + bitmap of 64 lanes
-  uint32_t *retry_count;    // [2] zeroed by the kernel when not null (the pool
-                            // kernel's retry count and candidate counter)
+  uint32_t *retry_count;    // [4] zeroed by the kernel when not null (retry
+                            // counts and the on-demand candidate counter of
+                            // the simulation passes)
 };
 
 // LDS of a tile-check block: the 64 candidates' flag words, then the waves'
@@ -145,8 +105,13 @@ __host__ __device__ inline int32_t tile_md_bytes(int32_t max_nr) { return ((max_
 __host__ __device__ inline int32_t tile_region_bytes(int32_t max_nr) {
   return tile_md_bytes(max_nr) + ((max_nr + 32) / 32) * 64 * 4 + kTileStageBytes;
 }
-const void *tile_check_kernel_ptr();
-hipError_t launch_tile_check(int blocks, int nw, size_t lds, hipStream_t s, const TileCheckArgs &a);
+// order: the pass over the ranks that run ops with an own-rank predecessor
+// (plan lists only those), after the main pass: a candidate in which such an
+// op comes before its predecessor deadlocks (flag added, makespan and bubbles
+// -1); nothing else is written
+const void *tile_check_kernel_ptr(bool order = false);
+hipError_t launch_tile_check(int blocks, int nw, size_t lds, hipStream_t s, const TileCheckArgs &a,
+                             bool order = false);
 
 // ---------------------------------------------------------------- pool
 // Timing simulation with per-rank slot pools holding the end times still to
@@ -222,6 +187,93 @@ constexpr int64_t kPoolTabMax = 16384;
 const void *pool_kernel_ptr(int pwl, int slots, bool tab);
 hipError_t launch_pool(int pwl, int slots, bool tab, int blocks, int wpb, size_t lds, hipStream_t s,
                        const PoolArgs &a);
+
+// ---------------------------------------------------------------- sim
+// Timing simulation with LDS-resident compact op records and per-lane order
+// rings (see kern_sim.hip).
+//
+// Record (8 bytes) of an op, relative to the op itself so that ops of
+// identically placed model chunks share records:
+//   w0 = cost (bits 0-19) | consumers (20-23) | several predecessors (24) |
+//        has predecessors (25)
+//   w1 = the edge word of its only predecessor, or, with several, the index
+//        of its first edge word in the extra-edge table (the rest follow, the
+//        last one marked)
+// Edge word: pred local id - own local id (bits 0-13, two's complement) |
+//   (pred rank - own rank) mod P (14-19) | latency (20-30) | last (31).
+constexpr uint32_t kSimCostBits = 20;
+constexpr uint32_t kSimCostMax = (1u << kSimCostBits) - 1;
+constexpr uint32_t kSimCommMax = 2047;
+constexpr int32_t kSimDeltaMax = 8191;          // |pred local id - own local id|
+constexpr uint32_t kSimMulti = 1u << 24;
+constexpr uint32_t kSimHasPred = 1u << 25;
+constexpr uint32_t kSimLast = 1u << 31;
+// ops per record page (paged tables: a rank's records come in pages of 16
+// consecutive local ids, equal pages stored once)
+constexpr int kSimPage = 16;
+
+// Per-candidate LDS state of the simulation kernel, for a group of PW lanes:
+//   counts [PW][C] words (4-bit reader count per pool slot, C = ceil(S / 8))
+//   tags   [S / 8][PW][8] 16-bit (local id + 1 of the op whose end time a slot
+//          holds; slots 8h .. 8h + 7 of all ranks together, 16 bytes per rank;
+//          with S = 4, [PW][4])
+//   ends   [PW][S + 1] words
+//   rings  [PW] 40-byte order rings (4 blocks of 4 ids; 8-byte stride pad)
+constexpr int64_t kSimRingStride = 40;
+__host__ __device__ constexpr int64_t sim_count_words(int slots) { return (slots + 7) / 8; }
+__host__ __device__ constexpr int64_t sim_tags_offset(int pw, int slots) {
+  return (int64_t(pw) * 4 * sim_count_words(slots) + 15) / 16 * 16;
+}
+__host__ __device__ constexpr int64_t sim_ends_offset(int pw, int slots) {
+  return sim_tags_offset(pw, slots) + (int64_t(pw) * 2 * slots + 15) / 16 * 16;
+}
+__host__ __device__ constexpr int64_t sim_end_stride(int slots) { return 4 * int64_t(slots) + 4; }
+__host__ __device__ constexpr int64_t sim_ring_offset(int pw, int slots) {
+  return (sim_ends_offset(pw, slots) + int64_t(pw) * sim_end_stride(slots) + 15) / 16 * 16;
+}
+// padded so that the group's size in words is congruent to PW modulo the 32
+// banks (4 words below 4 lanes): the same word of consecutive groups then
+// falls in different banks, and a half-wave's reads of its groups' counts and
+// tags tile the banks
+__host__ __device__ constexpr int64_t sim_group_bytes(int pw, int slots) {
+  const int64_t raw = sim_ring_offset(pw, slots) + int64_t(pw) * kSimRingStride;
+  const int64_t want = pw >= 32 ? 0 : 4 * (pw < 4 ? 4 : pw);   // residue modulo 128 bytes
+  int64_t x = (raw + 15) / 16 * 16;
+  while (x % 128 != want) x += 16;
+  return x;
+}
+
+struct SimArgs {
+  const int16_t *orders;
+  int64_t n_cand;
+  int64_t stride;
+  int32_t *out_ms;
+  int32_t *out_bub;
+  uint8_t *out_flags;        // the check kernel's verdicts, extended here
+  const uint4 *tab;          // LDS image of the tables: records, page map, extra edges
+  int32_t tab_vec;           // its size in 16-byte units
+  uint32_t off_pmap;         // byte offset of the page map (paged records)
+  uint32_t off_extra;        // byte offset of the extra edges
+  const int32_t *lane_info;  // [P][4] {first global op, ops, busy time, record base}
+                             // record base: first record (direct) or first page-map entry
+  uint32_t state_base;       // byte offset of the first group's state
+  int32_t P, wpb;
+  int64_t *retry;            // candidates the pools could not hold
+  uint32_t *retry_count;     // [2] their count, candidates handed out on demand
+  // list mode (list != null): simulate list[0 .. *list_count - 1] instead of
+  // 0 .. n_cand - 1 (a second pass, with larger pools, over the first pass's
+  // retry list); candidates are then taken by fixed successors only
+  const int64_t *list;
+  const uint32_t *list_count;
+  int64_t static_end;        // candidates below it (a multiple of the resident groups)
+                             // go to fixed successors, the rest are handed out on
+                             // demand through retry_count[1]; INT64_MAX: none
+  uint32_t round_limit;      // rounds one candidate may take
+};
+bool sim_slots_ok(int slots);
+const void *sim_kernel_ptr(int pwl, int slots, bool paged);
+hipError_t launch_sim(int pwl, int slots, bool paged, int blocks, int wpb, size_t lds,
+                      hipStream_t s, const SimArgs &a);
 
 // ---------------------------------------------------------------- greedy
 // Dual-queue stage interleaving (see kern_greedy.hip).  Groups are numbered

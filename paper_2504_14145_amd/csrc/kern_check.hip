@@ -62,7 +62,7 @@ __global__ __launch_bounds__(256) void check_kernel(CheckArgs a) {
   const int wave = threadIdx.x / kWave;
   const int wpw = int(check_lds_per_group(a.N) / 4);
   uint32_t *bm = reinterpret_cast<uint32_t *>(c_lds) + wave * wpw;
-  if (a.retry_count && blockIdx.x == 0 && threadIdx.x < 2) a.retry_count[threadIdx.x] = 0u;
+  if (a.retry_count && blockIdx.x == 0 && threadIdx.x < 4) a.retry_count[threadIdx.x] = 0u;
 
   const int cap_l = lane < a.P ? a.cap[lane] : -1;
   // section offsets in a register, lane k holding rank_off[k] (read with
@@ -168,22 +168,31 @@ __global__ __launch_bounds__(256) void check_kernel(CheckArgs a) {
 //   * The running memory is the sum of the deltas of the ops taken so far,
 //     read from the wave's copy of the rank's deltas in LDS; the peak is its
 //     maximum, starting from 0 (Sec. 5.3).
+//   * (ORDER pass, over the ranks that need it) An op whose predecessor runs
+//     on its own rank must come after it in the rank's order: the
+//     predecessor's bit is tested before the op's own bit is set.  If it
+//     comes first, the two wait for each other (the data edge one way, the
+//     order the other): the candidate deadlocks, and its makespan and bubbles
+//     are -1 here already.  This pass reads the predecessors where the main
+//     pass reads the memory deltas.
 // The verdict of a candidate needs all of its ranks: each wave ORs its
 // findings into the candidates' flag words in LDS, and after a block barrier
-// the outputs of an invalid candidate are overwritten with -1.
+// the outputs of an invalid candidate are overwritten with -1 (makespan and
+// bubbles only, for one deadlocked on its own order).
 
+template <bool ORDER>
 __global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   uint32_t *flg = reinterpret_cast<uint32_t *>(c_lds);
   unsigned char *region = c_lds + kTileFlagBytes + wave * a.region_bytes;
-  int32_t *mdl = reinterpret_cast<int32_t *>(region);
+  int32_t *mdl = reinterpret_cast<int32_t *>(region);   // deltas, or predecessors (ORDER)
   uint32_t *bm = reinterpret_cast<uint32_t *>(region + a.md_bytes) + lane;   // word w at bm[64 w]
   // staging of 8 units of the 64 rows (8 KB), unit k of row l at slot
   // k ^ (l & 7) of the row's 8, so the reads of one unit by 8 lanes hit 8
   // distinct bank groups
   unsigned char *stg = region + a.region_bytes - kTileStageBytes;
-  if (a.retry_count && blockIdx.x == 0 && threadIdx.x < 2) a.retry_count[threadIdx.x] = 0u;
+  if (!ORDER && a.retry_count && blockIdx.x == 0 && threadIdx.x < 4) a.retry_count[threadIdx.x] = 0u;
 
   const int kb = a.plan[wave], ke = a.plan[wave + 1];
   const int32_t *ranks = a.plan + a.nw + 1;
@@ -210,13 +219,14 @@ __global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
       const int rb = a.rank_off[r], re = a.rank_off[r + 1];
       const int nr = re - rb;
       const int n_words = (nr + 32) >> 5;   // bits 0 .. nr
+      const int32_t *src = ORDER ? a.selfp : a.md;
       // the rank's deltas into the wave's region (entry nr, the overflow
       // entry, is 0), the lanes' bitmaps cleared
       wave_sync();
       for (int i = lane; i <= nr; i += 4 * kWave) {
         int32_t v[4];
 #pragma unroll
-        for (int t = 0; t < 4; ++t) v[t] = i + t * kWave < nr ? a.md[rb + i + t * kWave] : 0;
+        for (int t = 0; t < 4; ++t) v[t] = i + t * kWave < nr ? src[rb + i + t * kWave] : 0;
 #pragma unroll
         for (int t = 0; t < 4; ++t)
           if (i + t * kWave <= nr) mdl[i + t * kWave] = v[t];
@@ -226,16 +236,23 @@ __global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
 
       const uint32_t lim = uint32_t(nr);
       int run = 0, peak = 0;
+      bool late = false;   // an op before its own-rank predecessor
       auto take = [&](uint32_t id) {
         const uint32_t c = min(id, lim);
+        if constexpr (ORDER) {
+          const uint32_t sp = uint32_t(mdl[c]);
+          if (sp != 0u) late = late || !((bm[((sp - 1u) >> 5) * kWave] >> ((sp - 1u) & 31u)) & 1u);
+        }
         // word index c >> 5, kept as one shift (the byte offset is then one
         // shift-add instead of a shift, a mask and an add)
         uint32_t w;
         asm("v_lshrrev_b32 %0, 5, %1" : "=v"(w) : "v"(c));
         __hip_atomic_fetch_or(bm + w * kWave, 1u << (c & 31u), __ATOMIC_RELAXED,
                               __HIP_MEMORY_SCOPE_WORKGROUP);
-        run += mdl[c];
-        peak = max(peak, run);
+        if constexpr (!ORDER) {
+          run += mdl[c];
+          peak = max(peak, run);
+        }
       };
       // positions lo .. hi-1 of a unit of 8 (lo, hi uniform)
       auto unit = [&](const uint4 v, int lo, int hi) {
@@ -291,21 +308,36 @@ __global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
       for (int w = 0; w < n_words; ++w) bits += uint32_t(__builtin_popcount(bm[w * kWave]));
       const bool ovf = (bm[(nr >> 5) * kWave] >> (nr & 31)) & 1u;
       const bool bad = ovf || bits != lim;
-      const int cap_r = a.cap[r];
-      const bool over = cap_r >= 0 && peak > cap_r;
-      if (live) a.out_peak[cand * a.P + r] = peak;
-      fl |= (bad ? 1u : 0u) | (over ? 2u : 0u);
+      if constexpr (ORDER) {
+        fl |= late ? 4u : 0u;
+      } else {
+        const int cap_r = a.cap[r];
+        const bool over = cap_r >= 0 && peak > cap_r;
+        if (live) a.out_peak[cand * a.P + r] = peak;
+        fl |= (bad ? 1u : 0u) | (over ? 2u : 0u);
+      }
     }
     if (fl) __hip_atomic_fetch_or(flg + lane, fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     __syncthreads();
     const uint32_t f = flg[lane];
-    if (live && (f & 1u))
-      for (int k = kb; k < ke; ++k) a.out_peak[cand * a.P + ranks[k]] = -1;
-    if (wave == 0 && live) {
-      a.out_flags[cand] = (f & 1u) ? uint8_t(DIP_FLAG_INVALID) : uint8_t((f & 2u) ? DIP_FLAG_CAP : 0u);
-      if (f & 1u) {
-        a.out_ms[cand] = -1;
-        for (int q = 0; q < a.P; ++q) a.out_bub[cand * a.P + q] = -1;
+    if constexpr (ORDER) {
+      if (wave == 0 && live && (f & 4u)) {
+        const uint8_t old = a.out_flags[cand];
+        if (!(old & DIP_FLAG_INVALID)) {
+          a.out_flags[cand] = uint8_t(old | DIP_FLAG_DEADLOCK);
+          a.out_ms[cand] = -1;
+          for (int q = 0; q < a.P; ++q) a.out_bub[cand * a.P + q] = -1;
+        }
+      }
+    } else {
+      if (live && (f & 1u))
+        for (int k = kb; k < ke; ++k) a.out_peak[cand * a.P + ranks[k]] = -1;
+      if (wave == 0 && live) {
+        a.out_flags[cand] = (f & 1u) ? uint8_t(DIP_FLAG_INVALID) : uint8_t((f & 2u) ? DIP_FLAG_CAP : 0u);
+        if (f & 1u) {
+          a.out_ms[cand] = -1;
+          for (int q = 0; q < a.P; ++q) a.out_bub[cand * a.P + q] = -1;
+        }
       }
     }
     __syncthreads();   // the flag words are cleared for the next tile
@@ -321,10 +353,17 @@ hipError_t launch_check(int, int blocks, int wpb, size_t lds, hipStream_t s, con
   return hipGetLastError();
 }
 
-const void *tile_check_kernel_ptr() { return reinterpret_cast<const void *>(tile_check_kernel); }
+const void *tile_check_kernel_ptr(bool order) {
+  return order ? reinterpret_cast<const void *>(tile_check_kernel<true>)
+               : reinterpret_cast<const void *>(tile_check_kernel<false>);
+}
 
-hipError_t launch_tile_check(int blocks, int nw, size_t lds, hipStream_t s, const TileCheckArgs &a) {
-  tile_check_kernel<<<dim3(blocks), dim3(nw * kWave), lds, s>>>(a);
+hipError_t launch_tile_check(int blocks, int nw, size_t lds, hipStream_t s, const TileCheckArgs &a,
+                             bool order) {
+  if (order)
+    tile_check_kernel<true><<<dim3(blocks), dim3(nw * kWave), lds, s>>>(a);
+  else
+    tile_check_kernel<false><<<dim3(blocks), dim3(nw * kWave), lds, s>>>(a);
   return hipGetLastError();
 }
 

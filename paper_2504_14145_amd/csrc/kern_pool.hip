@@ -232,7 +232,8 @@ __global__ __launch_bounds__(TAB ? 1024 : 256) void pool_kernel(PoolArgs a) {
   };
   // All lanes of the group call this together.
   auto start_candidate = [&]() {
-    while (cand < a.n_cand && (a.out_flags[cand] & DIP_FLAG_INVALID)) cand = next_cand();
+    while (cand < a.n_cand && (a.out_flags[cand] & (DIP_FLAG_INVALID | DIP_FLAG_DEADLOCK)))
+      cand = next_cand();
     has = cand < a.n_cand;
     ce = dead_edge;
     ea = 0;   // (lanes on the dead edge fetch edges at ea)

@@ -1,0 +1,468 @@
+// kern_sim.hip -- timing simulation of candidate schedules, one wavefront
+// holding 64 / PW candidates, lane r of a candidate's group playing rank r.
+//
+// What is simulated (Sec. 5.2 and 6.1): every rank runs its ops one at a
+// time in its given order, each op as soon as the rank is free and the
+// outputs of all of its predecessors have arrived,
+//     start = max(free, max_p end(p) + comm(p, o)),   end = start + cost,
+// and a candidate deadlocks when no op can ever start while ops remain.
+//
+// Rounds: every round each lane looks at the current op of its order.  End
+// times travel between ranks as items: an op with consumers writes its end
+// time, tagged with its rank-local id + 1, into a free slot of a pool of S
+// slots owned by its rank, with a 4-bit count of the readers still to come
+// (0 = free).  A consumer compares its predecessor's tag with the S tags of
+// that rank's pool (one predecessor per round), folds end + comm into a
+// running maximum and decrements the slot's count.  A producer whose pool is
+// full waits (back-pressure).
+//
+// What is resident in LDS, and why:
+//   * the op records, 8 bytes each and relative to the op (predecessor given
+//     as a local-id and rank difference), so the records of model chunks
+//     placed alike coincide; large tables are stored as pages of 16 records
+//     with equal pages kept once and a page map per rank.  Every round's
+//     record read is then an LDS read instead of a gather through the
+//     vector-memory path;
+//   * the pools of the candidates in flight (a few items per rank are live at
+//     once, so a pool of 8 or 16 slots per rank suffices where a table of end
+//     times by op would need 4 bytes per op);
+//   * each lane's order ring: 4 blocks of 4 ids of its rank's section.  Every
+//     4 rounds (the same rounds for all lanes, so that one wait covers the
+//     loads) each lane that has room loads its next 8-byte block from HBM
+//     into registers; 3 rounds later the block is stored into the ring.  A
+//     lane fires at most one op per round, so with two blocks ahead at every
+//     load round the id it reads two positions ahead is always in the ring.
+//
+// Verdicts: a group is done when all of its lanes ran their whole order.  A
+// round in which no lane of a group fired an op or read an item leaves its
+// state unchanged for good: if no lane was held by back-pressure the orders
+// deadlock; otherwise the bounded pools may be what stalls it, and the
+// candidate goes to a retry list that the general kernel re-simulates.  The
+// permutation check and the memory scan ran before, in the check kernel,
+// whose flags this kernel reads (invalid candidates are skipped) and extends.
+#include "dip_sim.h"
+#include "dev_util.h"
+#include "internal.h"
+
+namespace dipsim {
+namespace {
+
+extern __shared__ __align__(16) unsigned char s_lds[];
+
+__device__ __forceinline__ uint32_t lds32(uint32_t a) {
+  return *reinterpret_cast<const uint32_t *>(s_lds + a);
+}
+__device__ __forceinline__ uint32_t lds16(uint32_t a) {
+  return *reinterpret_cast<const uint16_t *>(s_lds + a);
+}
+__device__ __forceinline__ uint2 lds64(uint32_t a) {
+  return *reinterpret_cast<const uint2 *>(s_lds + a);
+}
+__device__ __forceinline__ uint4 lds128(uint32_t a) {
+  return *reinterpret_cast<const uint4 *>(s_lds + a);
+}
+__device__ __forceinline__ void st32(uint32_t a, uint32_t v) {
+  *reinterpret_cast<uint32_t *>(s_lds + a) = v;
+}
+__device__ __forceinline__ void st16(uint32_t a, uint32_t v) {
+  *reinterpret_cast<uint16_t *>(s_lds + a) = uint16_t(v);
+}
+__device__ __forceinline__ void st64(uint32_t a, uint32_t x, uint32_t y) {
+  *reinterpret_cast<uint2 *>(s_lds + a) = make_uint2(x, y);
+}
+__device__ __forceinline__ uint32_t *lds_word(uint32_t a) {
+  return reinterpret_cast<uint32_t *>(__builtin_assume_aligned(s_lds + a, 4));
+}
+__device__ __forceinline__ void lds_add(uint32_t a, uint32_t v) {
+  (void)__hip_atomic_fetch_add(lds_word(a), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+}
+__device__ __forceinline__ void lds_sub(uint32_t a, uint32_t v) {
+  (void)__hip_atomic_fetch_sub(lds_word(a), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+}
+__device__ __forceinline__ bool lane_in(uint64_t m) { return __builtin_amdgcn_inverse_ballot_w64(m); }
+__device__ __forceinline__ uint64_t ballot(bool b) { return __builtin_amdgcn_ballot_w64(b); }
+
+template <int PWL, int S, bool PAGED>
+__global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
+  constexpr int PW = 1 << PWL;
+  constexpr int G = kWave / PW;
+  constexpr int kC = int(sim_count_words(S));
+  constexpr uint32_t kTags = uint32_t(sim_tags_offset(PW, S));
+  constexpr uint32_t kEnds = uint32_t(sim_ends_offset(PW, S));
+  constexpr uint32_t kEndStride = uint32_t(sim_end_stride(S));
+  constexpr uint32_t kRing = uint32_t(sim_ring_offset(PW, S));
+  constexpr uint32_t kGroup = uint32_t(sim_group_bytes(PW, S));
+  static_assert(S == 4 || S == 8 || S == 16, "pool size");
+
+  // the tables into LDS, once per block
+  for (int i = threadIdx.x; i < a.tab_vec; i += blockDim.x)
+    *reinterpret_cast<uint4 *>(s_lds + 16u * uint32_t(i)) = a.tab[i];
+  __syncthreads();
+
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = threadIdx.x / kWave;
+  const int grp = lane >> PWL;
+  const int r = lane & (PW - 1);
+  const uint32_t P = uint32_t(a.P);
+  const bool on = uint32_t(r) < P;
+  const int gbit = grp << PWL;
+  const int64_t n_slots = int64_t(gridDim.x) * a.wpb * G;
+  const uint32_t gbase = a.state_base + uint32_t(wave * G + grp) * kGroup;
+  const uint32_t rr = on ? uint32_t(r) : 0u;
+  const uint32_t my_cnt = gbase + rr * 4u * kC;
+  const uint32_t my_tags = gbase + kTags + rr * (S == 4 ? 8u : 16u);
+  const uint32_t my_ends = gbase + kEnds + rr * kEndStride;
+  const uint32_t my_ring = gbase + kRing + rr * uint32_t(kSimRingStride);
+  int rb = 0, nr = 0, busy_r = 0, recb = 0;
+  if (on) {
+    const int4 li = reinterpret_cast<const int4 *>(a.lane_info)[r];
+    rb = li.x;
+    nr = li.y;
+    busy_r = li.z;
+    recb = li.w;
+  }
+  // absolute row positions of this lane's section, and its last 8-byte block
+  const uint32_t a_last = uint32_t(rb + max(nr - 1, 0));
+  const uint32_t blk_last = a_last >> 2;
+
+  // the record of local id `id` of this lane's rank
+  auto rec_of = [&](uint32_t id) -> uint2 {
+    uint32_t addr;
+    if constexpr (PAGED) {
+      const uint32_t pg = lds16(a.off_pmap + 2u * (uint32_t(recb) + (id >> 4)));
+      addr = (pg << 7) | ((id & 15u) << 3);
+    } else {
+      addr = (uint32_t(recb) + id) << 3;
+    }
+    return lds64(addr);
+  };
+  auto ring_id = [&](uint32_t pos) { return lds16(my_ring + ((pos & 15u) << 1)); };
+
+  // candidates: positions k < n of the batch, or of the list in list mode
+  const int64_t n_todo = a.list ? int64_t(*a.list_count) : a.n_cand;
+  int64_t k = (int64_t(blockIdx.x) * a.wpb + wave) * G + grp;
+  auto cand_at = [&](int64_t i) { return a.list ? a.list[i] : i; };
+
+  // per-lane state
+  int64_t cand = 0;
+  bool has = false;        // the group holds a candidate
+  uint8_t fl = 0;          // the check kernel's flags for it
+  uint32_t cand_round = 0;
+  uint32_t ptr = 0;        // position of the current op in the section
+  uint32_t tfree = 0, acc = 0;
+  uint32_t lid = 0, cur0 = 0;   // current op: local id, record word 0
+  uint32_t ce = 0, xi = 0;      // current edge word; index of the op's next extra edge
+  uint32_t nid = 0, nxt0 = 0, nce = 0, nxi = 0;   // the op after it, likewise
+  uint32_t lb = 0;         // next absolute 8-byte block of the row to load
+  uint2 blk = make_uint2(0, 0);   // a loaded block waiting to be stored
+  const int16_t *row = a.orders;
+
+  // wave-uniform lane masks
+  uint64_t m_live = 0;     // lanes running an op sequence
+  uint64_t m_npend = 0;    // live lanes whose current op waits for no edge
+  uint64_t m_blk = 0;      // lanes holding a loaded block for the ring
+
+  auto next_k = [&]() -> int64_t {
+    const int64_t succ = k + n_slots;
+    if (succ < a.static_end) return succ;
+    uint32_t k = 0;
+    if (r == 0) k = atomicAdd(a.retry_count + 1, 1u);
+    k = uint32_t(__shfl(int(k), gbit, kWave));
+    return a.static_end + int64_t(k);
+  };
+
+  // The lanes of one group call this together (a group without a candidate
+  // keeps its lanes out of m_live, so its pool contents are never read).
+  auto start_candidate = [&](uint32_t rnd) {
+    // (candidates whose verdict the check kernel already settled: not a
+    // permutation, or an op ordered before its own-rank predecessor)
+    while (k < n_todo && (a.out_flags[cand_at(k)] & (DIP_FLAG_INVALID | DIP_FLAG_DEADLOCK)))
+      k = next_k();
+    has = k < n_todo;
+    if (on) {
+#pragma unroll
+      for (int i = 0; i < kC; ++i) st32(my_cnt + 4u * i, 0u);
+#pragma unroll
+      for (int i = 0; i < S / 2; ++i) st32(my_tags + 16u * PW * (i >> 2) + 4u * (i & 3), 0u);
+    }
+    if (!has) return;
+    cand = cand_at(k);
+    fl = a.out_flags[cand];
+    cand_round = rnd;
+    ptr = 0;
+    tfree = 0;
+    acc = 0;
+    if (!on || nr == 0) return;
+    row = a.orders + cand * a.stride;
+    // the first three blocks of the section into the ring
+    const uint32_t b0 = uint32_t(rb) >> 2;
+    const uint32_t bn = min(b0 + 2u, blk_last);
+    for (uint32_t b = b0; b <= bn; ++b) {
+      const uint2 v = *reinterpret_cast<const uint2 *>(row + 4 * int64_t(b));
+      st64(my_ring + (b & 3u) * 8u, v.x, v.y);
+    }
+    lb = bn + 1;
+    lid = ring_id(uint32_t(rb));
+    nid = ring_id(min(uint32_t(rb) + 1u, a_last));
+    const uint2 c = rec_of(lid);
+    const uint2 n = rec_of(nid);
+    cur0 = c.x;
+    nxt0 = n.x;
+    ce = c.y;
+    xi = c.y + 1;
+    if (c.x & kSimMulti) ce = lds32(a.off_extra + 4u * c.y);
+    nce = n.y;
+    nxi = n.y + 1;
+    if (n.x & kSimMulti) nce = lds32(a.off_extra + 4u * n.y);
+  };
+
+  start_candidate(0);
+  {
+    const bool live = has && on && nr > 0;
+    m_live = ballot(live);
+    m_npend = m_live & ballot((cur0 & kSimHasPred) == 0);
+  }
+  uint64_t g_has = any_in_group<PWL>(ballot(has));
+
+  uint32_t rnd = 0;
+  while (g_has) {
+    // ---- order blocks: loaded every 4 rounds, stored 3 rounds later
+    const uint32_t phase = rnd & 3u;
+    if (phase == 3u && m_blk) {
+      if (lane_in(m_blk)) {
+        st64(my_ring + (lb & 3u) * 8u, blk.x, blk.y);
+        ++lb;
+      }
+      m_blk = 0;
+    }
+
+    // ---- reads: the predecessor's pool tags, my counts, the id two ahead
+    const uint32_t dr = (ce >> 14) & 63u;
+    uint32_t pr = rr + dr;
+    pr = min(pr, pr - P);   // (rr + dr) mod P, dr < P
+    const uint32_t p_tags = gbase + kTags + pr * (S == 4 ? 8u : 16u);
+    const uint32_t p_ends = gbase + kEnds + pr * kEndStride;
+    const uint32_t p_cnt = gbase + pr * 4u * kC;
+    const uint32_t want = lid + uint32_t(int32_t(ce << 18) >> 18) + 1u;
+    uint32_t tw[S / 2];
+    if constexpr (S == 4) {
+      const uint2 v = lds64(p_tags);
+      tw[0] = v.x;
+      tw[1] = v.y;
+    } else {
+#pragma unroll
+      for (int i = 0; i < S / 8; ++i) {   // slots 8i .. 8i + 7 of every rank side by side
+        const uint4 v = lds128(p_tags + 16u * PW * i);
+        tw[4 * i] = v.x;
+        tw[4 * i + 1] = v.y;
+        tw[4 * i + 2] = v.z;
+        tw[4 * i + 3] = v.w;
+      }
+    }
+    uint32_t cnt[kC];
+#pragma unroll
+    for (int i = 0; i < kC; ++i) cnt[i] = lds32(my_cnt + 4u * i);
+    const uint32_t idn = ring_id(min(uint32_t(rb) + ptr + 2u, a_last));
+
+    // the matching slot (tags are unique within a pool): 4 x its index, or
+    // kNoHit; one compare and one select per slot, all vector instructions
+    constexpr uint32_t kNoHit = 0x80u;
+    uint32_t hit4 = kNoHit;
+#pragma unroll
+    for (int i = 0; i < S; ++i) {
+      const uint32_t pair = tw[i / 2];
+      const uint32_t t = (i & 1) ? (pair >> 16) : (pair & 0xffffu);
+      hit4 = t == want ? 4u * uint32_t(i) : hit4;
+    }
+    const uint64_t m_found = ballot(hit4 != kNoHit) & m_live & ~m_npend;
+    hit4 &= 0x7cu;
+    const uint32_t hit_end = lds32(p_ends + hit4);
+    const bool found = lane_in(m_found);
+    const uint32_t acc_n = found ? max(acc, hit_end + ((ce >> 20) & 0x7ffu)) : acc;
+    // a free slot of my pool (reader count zero): the first one
+    bool has_free = false;
+    uint32_t sl = 0;
+#pragma unroll
+    for (int i = kC - 1; i >= 0; --i) {
+      const uint32_t w = i * 8 + 8 <= S ? cnt[i] : (cnt[i] | (0xffffffffu << (4 * (S - i * 8))));
+      const uint32_t z = ~(((w & 0x77777777u) + 0x77777777u) | w | 0x77777777u);   // 8 in zero nibbles
+      if constexpr (kC == 1) {
+        has_free = z != 0u;
+        sl = uint32_t(__builtin_ctz(z | 0x80000000u)) >> 2;
+      } else {
+        sl = z ? 8u * uint32_t(i) + (uint32_t(__builtin_ctz(z)) >> 2) : sl;
+        has_free = has_free || z != 0u;
+      }
+    }
+    const uint32_t readers = (cur0 >> 20) & 15u;
+    const uint64_t m_last = ballot(int32_t(ce) < 0);
+    const uint64_t m_ready = (m_found & m_last) | m_npend;
+    const uint64_t m_need = ballot(readers != 0u);
+    const uint64_t m_fire = m_ready & (~m_need | ballot(has_free));
+    const uint64_t m_held = m_ready & ~m_fire;
+    const bool fire = lane_in(m_fire);
+    const uint32_t en = max(tfree, acc_n) + (cur0 & kSimCostMax);
+
+    // ---- writes: release what was read, publish what was produced
+    if (found) {
+      const uint32_t slot = hit4 >> 2;
+      lds_sub(p_cnt + (kC > 1 ? 4u * (slot >> 3) : 0u), 1u << (4u * (slot & 7u)));
+    }
+    if (lane_in(m_fire & m_need)) {
+      lds_add(my_cnt + (kC > 1 ? 4u * (sl >> 3) : 0u), readers << (4u * (sl & 7u)));
+      st32(my_ends + 4u * sl, en);
+      st16(my_tags + (S > 8 ? 16u * PW * (sl >> 3) : 0u) + 2u * (sl & 7u), lid + 1u);
+    }
+
+    // ---- register state
+    const uint64_t m_fin = m_fire & ballot(ptr + 1u == uint32_t(nr));
+    const uint64_t m_adv = m_fire & ~m_fin;
+    const bool adv = lane_in(m_adv);
+    const bool more = lane_in(m_found & ~m_fire & ~m_last);   // found, another edge to go
+    if (fire) {
+      tfree = en;
+      acc = 0;
+      ++ptr;
+    } else if (found) {
+      acc = acc_n;
+    }
+    if (more) {   // the op's next predecessor edge
+      ce = lds32(a.off_extra + 4u * xi);
+      ++xi;
+    }
+    m_npend = ((m_npend & ~m_fire) | (m_found & m_last & ~m_fire) |
+               (m_adv & ballot((nxt0 & kSimHasPred) == 0))) & ~m_fin;
+    m_live &= ~m_fin;
+    if (adv) {
+      lid = nid;
+      cur0 = nxt0;
+      ce = nce;
+      xi = nxi;
+      // the op after the new current one
+      nid = idn;
+      const uint2 n = rec_of(idn);
+      nxt0 = n.x;
+      nce = n.y;
+      nxi = n.y + 1u;
+      if (n.x & kSimMulti) nce = lds32(a.off_extra + 4u * n.y);
+    }
+
+    // ---- order blocks: every 4 rounds, a lane with room loads its next block
+    if (phase == 0u) {
+      const uint32_t cur_blk = (uint32_t(rb) + ptr) >> 2;
+      const bool load = lane_in(m_live) && lb <= blk_last && lb < cur_blk + 3u;
+      m_blk = ballot(load);
+      if (load) blk = *reinterpret_cast<const uint2 *>(row + 4 * int64_t(lb));
+    }
+
+    // ---- verdicts, every 8 rounds (a group that finished or stalled waits
+    // for the next check; its state does not change meanwhile)
+    ++rnd;
+    if ((rnd & 7u) != 0u) continue;
+    const uint64_t g_run = any_in_group<PWL>(m_live);
+    const uint64_t g_done = g_has & ~g_run;   // every lane ran its whole order
+    const uint64_t g_stall = g_run & ~any_in_group<PWL>(m_fire | m_found);
+    const uint64_t g_over = g_run & ~g_stall &
+                            any_in_group<PWL>(ballot(has && rnd - cand_round > a.round_limit));
+    const uint64_t ev = g_done | g_stall | g_over;
+    if (ev == 0) continue;
+
+    // ---- some groups finished their candidate
+    const uint64_t g_held = any_in_group<PWL>(m_held);
+    const uint64_t m_ev = any_lane_of_group<PWL>(ev);
+    if (lane_in(m_ev)) {
+      const bool stalled = (g_stall >> gbit) & 1;
+      const bool retry = (stalled && ((g_held >> gbit) & 1)) || ((g_over >> gbit) & 1);
+      uint32_t T = on ? tfree : 0u;
+#pragma unroll
+      for (int off = 1; off < PW; off <<= 1) T = max(T, uint32_t(__shfl_xor(int(T), off, kWave)));
+      if (has) {
+        if (retry) {
+          if (r == 0) {
+            const uint32_t k = atomicAdd(a.retry_count, 1u);
+            a.retry[k] = cand;
+          }
+        } else if (on) {
+          a.out_bub[cand * a.P + r] = stalled ? -1 : int32_t(T) - busy_r;
+          if (r == 0) {
+            a.out_ms[cand] = stalled ? -1 : int32_t(T);
+            if (stalled) a.out_flags[cand] = uint8_t(fl | DIP_FLAG_DEADLOCK);
+          }
+        }
+      }
+      k = next_k();
+      start_candidate(rnd);
+    }
+    // the restarted groups' lanes: live and edge state from their new records
+    const bool live_new = has && on && nr > 0;
+    m_live = (m_live & ~m_ev) | (m_ev & ballot(live_new));
+    m_npend = (m_npend & ~m_ev) | (m_ev & m_live & ballot((cur0 & kSimHasPred) == 0));
+    m_blk &= ~m_ev;
+    g_has = any_in_group<PWL>(ballot(has));
+  }
+}
+
+template <int S, bool PAGED>
+const void *ptr_s(int pwl) {
+  switch (pwl) {
+    case 0: return reinterpret_cast<const void *>(sim_kernel<0, S, PAGED>);
+    case 1: return reinterpret_cast<const void *>(sim_kernel<1, S, PAGED>);
+    case 2: return reinterpret_cast<const void *>(sim_kernel<2, S, PAGED>);
+    case 3: return reinterpret_cast<const void *>(sim_kernel<3, S, PAGED>);
+    case 4: return reinterpret_cast<const void *>(sim_kernel<4, S, PAGED>);
+    case 5: return reinterpret_cast<const void *>(sim_kernel<5, S, PAGED>);
+    default: return reinterpret_cast<const void *>(sim_kernel<6, S, PAGED>);
+  }
+}
+
+template <int S, bool PAGED>
+void launch_s(int pwl, dim3 grid, dim3 block, size_t lds, hipStream_t s, const SimArgs &a) {
+  switch (pwl) {
+    case 0: sim_kernel<0, S, PAGED><<<grid, block, lds, s>>>(a); break;
+    case 1: sim_kernel<1, S, PAGED><<<grid, block, lds, s>>>(a); break;
+    case 2: sim_kernel<2, S, PAGED><<<grid, block, lds, s>>>(a); break;
+    case 3: sim_kernel<3, S, PAGED><<<grid, block, lds, s>>>(a); break;
+    case 4: sim_kernel<4, S, PAGED><<<grid, block, lds, s>>>(a); break;
+    case 5: sim_kernel<5, S, PAGED><<<grid, block, lds, s>>>(a); break;
+    default: sim_kernel<6, S, PAGED><<<grid, block, lds, s>>>(a); break;
+  }
+}
+
+template <bool PAGED>
+const void *ptr_p(int pwl, int slots) {
+  switch (slots) {
+    case 4: return ptr_s<4, PAGED>(pwl);
+    case 16: return ptr_s<16, PAGED>(pwl);
+    default: return ptr_s<8, PAGED>(pwl);
+  }
+}
+
+template <bool PAGED>
+void launch_p(int pwl, int slots, dim3 grid, dim3 block, size_t lds, hipStream_t s,
+              const SimArgs &a) {
+  switch (slots) {
+    case 4: launch_s<4, PAGED>(pwl, grid, block, lds, s, a); break;
+    case 16: launch_s<16, PAGED>(pwl, grid, block, lds, s, a); break;
+    default: launch_s<8, PAGED>(pwl, grid, block, lds, s, a); break;
+  }
+}
+
+}  // namespace
+
+bool sim_slots_ok(int slots) { return slots == 4 || slots == 8 || slots == 16; }
+
+const void *sim_kernel_ptr(int pwl, int slots, bool paged) {
+  return paged ? ptr_p<true>(pwl, slots) : ptr_p<false>(pwl, slots);
+}
+
+hipError_t launch_sim(int pwl, int slots, bool paged, int blocks, int wpb, size_t lds,
+                      hipStream_t s, const SimArgs &a) {
+  const dim3 grid(blocks), block(wpb * kWave);
+  if (paged)
+    launch_p<true>(pwl, slots, grid, block, lds, s, a);
+  else
+    launch_p<false>(pwl, slots, grid, block, lds, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace dipsim

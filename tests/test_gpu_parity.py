@@ -53,7 +53,7 @@ def test_parity_small_all_variants(cid):
     sim = dip.Sim(prob)
     print(f"config {cid} auto variant: {sim.info}", flush=True)
     tried = 0
-    for variant in (0, 1, 2, 3, 4, 5, 6, 7):
+    for variant in (0, 1, 2, 3, 4, 8, 9):
         for wpb in (0, 1, 4):
             if sim.configure(variant, wpb) != dip.OK:
                 continue
@@ -66,21 +66,27 @@ def test_parity_small_all_variants(cid):
 
 @pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
 def test_parity_pool_kernel_slots(cid):
-    """The pool kernel (check + pools + list-mode fallback) at every pool
-    size and block shape; the smallest pools send many candidates through the
-    fallback, the results must not change."""
+    """The pool kernel and the simulation kernel (each after the check kernel,
+    with the list-mode fallback) at every pool size and block shape; the
+    smallest pools send many candidates through the fallback, the results
+    must not change."""
     need_gpu()
     prob = W.make_problem(cid)
     rows = W.generator_for(prob, cid).generate(0, SMALL[cid])
     want = O.evaluate(prob, rows, threads=16)
     sim = dip.Sim(prob)
     for slots in (4, 8, 16):
+        assert sim.configure(0, 0) == dip.OK      # drop the last forced shape first
         assert sim.configure_pool(slots) == dip.OK
-        for wpb in (0, 1, 4):
-            assert sim.configure(8, wpb) == dip.OK
+        for variant, wpb in ((8, 0), (8, 1), (8, 4), (9, 0), (9, 1), (9, 4), (9, 16)):
+            rc = sim.configure(variant, wpb)
+            if variant == 9 and wpb == 16 and rc == dip.E_UNSUPPORTED:
+                continue
+            assert rc == dip.OK
+            run_gpu(sim, rows[:1])            # costs uploaded, the shape is known
             info = sim.info
-            assert info["variant"] == 8 and info["pool_slots"] == slots
-            print(f"  slots {slots} wpb {wpb}: {info}", flush=True)
+            assert info["variant"] == variant and info["pool_slots"] == slots
+            print(f"  slots {slots} variant {variant} wpb {wpb}: {info}", flush=True)
             assert_same(run_gpu(sim, rows), want)
     sim.close()
 
@@ -104,9 +110,9 @@ def test_pool_fallback_when_pools_fill():
     want = O.evaluate(prob, rows)
     assert (want.flags == 0).all()
     sim = dip.Sim(prob)
-    for slots in (4, 8):
+    for slots, variant in ((4, 8), (8, 8), (4, 9), (8, 9)):
         assert sim.configure_pool(slots) == dip.OK
-        assert sim.configure(8, 0) == dip.OK
+        assert sim.configure(variant, 0) == dip.OK
         orders = torch.from_numpy(rows).to(DEV)
         out = sim.outputs(len(rows))
         for t in out:
