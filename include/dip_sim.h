@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define DIP_SIM_ABI_VERSION 5
+#define DIP_SIM_ABI_VERSION 6
 
 enum {
   DIP_OK = 0,
@@ -69,7 +69,8 @@ enum {
   DIP_E_UNSUPPORTED = -4, /* shape no kernel variant handles (> 64 ranks, ...) */
   DIP_E_NOMEM = -5,       /* host or device allocation failed                   */
   DIP_E_HIP = -6,         /* HIP runtime error; see dip_sim_strerror            */
-  DIP_E_STATE = -7        /* evaluate before any costs were supplied            */
+  DIP_E_STATE = -7,       /* evaluate before any costs were supplied            */
+  DIP_E_CAPACITY = -8     /* batch above dip_sim_evaluate_static's limit        */
 };
 
 #define DIP_FLAG_DEADLOCK 1u
@@ -201,6 +202,24 @@ int dip_sim_get_info(const dip_sim *h, dip_sim_info *info);
 int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders,
                      int64_t n_cand, int32_t *out_makespan, int32_t *out_bubble,
                      int32_t *out_peakmem, uint8_t *out_flags, void *stream);
+
+/* dip_sim_evaluate for callers that cannot allocate memory during the call
+ * (code captured into a HIP graph, serving loops, harnesses that forbid
+ * allocation): the same simulation and outputs, with the costs of an earlier
+ * dip_sim_evaluate call (DIP_E_STATE if there were none) and no costs
+ * argument, calling no hipMalloc, hipFree or other allocating routine.  Its
+ * working memory beyond inputs and outputs (retry counters and retry lists)
+ * is a static device array of 64 MiB + 256 bytes that the library holds on
+ * every GPU it runs on until the process ends; its tables and launch shapes
+ * are the handle's, set up by dip_sim_create and the configure calls.
+ * n_cand at most 4,194,304 (DIP_E_CAPACITY above).  All calls on one GPU
+ * share that array: calls whose kernels may overlap on one GPU (different
+ * streams without an ordering, or different handles or threads) race and
+ * must be serialized by the caller.  Arguments and errors as evaluate's. */
+#define DIP_SIM_STATIC_MAX_CAND 4194304
+int dip_sim_evaluate_static(dip_sim *h, const int16_t *orders, int64_t n_cand,
+                            int32_t *out_makespan, int32_t *out_bubble, int32_t *out_peakmem,
+                            uint8_t *out_flags, void *stream);
 
 /* Fold the lexicographic minimum of (makespan[i], index_base + i) over the
  * candidates with flags[i] == 0 into *inout_best_key (device, uint64):

@@ -19,13 +19,16 @@ from . import _build
 LIB_PATH = _build.LIB
 
 OK = 0
-E_INVAL, E_TOPO, E_RANGE, E_UNSUPPORTED, E_NOMEM, E_HIP, E_STATE = -1, -2, -3, -4, -5, -6, -7
+E_INVAL, E_TOPO, E_RANGE, E_UNSUPPORTED, E_NOMEM, E_HIP, E_STATE, E_CAPACITY = (
+    -1, -2, -3, -4, -5, -6, -7, -8)
+STATIC_MAX_CAND = 1 << 22
 FLAG_DEADLOCK, FLAG_CAP, FLAG_INVALID = 1, 2, 4
 NO_KEY = (1 << 64) - 1
 
 EXPORTS = ("dip_sim_abi_version", "dip_sim_check_topology", "dip_sim_check_costs",
            "dip_sim_create", "dip_sim_configure", "dip_sim_configure_pool",
-           "dip_sim_configure_check", "dip_sim_get_info", "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
+           "dip_sim_configure_check", "dip_sim_get_info", "dip_sim_evaluate",
+           "dip_sim_evaluate_static", "dip_sim_profile", "dip_sim_last_profile",
            "dip_sim_last_retries", "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_set_greedy_inbox", "dip_sim_greedy",
            "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_sim_rollouts_batch",
            "dip_cost_tables",
@@ -95,6 +98,7 @@ def load():
         lib.dip_sim_last_retries.argtypes = [vp, vp, vp]
         lib.dip_sim_get_info.argtypes = [vp, ctypes.POINTER(Info)]
         lib.dip_sim_evaluate.argtypes = [vp, ctypes.POINTER(Costs), vp, i64, vp, vp, vp, vp, vp]
+        lib.dip_sim_evaluate_static.argtypes = [vp, vp, i64, vp, vp, vp, vp, vp]
         lib.dip_sim_argmin.argtypes = [vp, vp, vp, i64, i64, vp, vp]
         lib.dip_sim_configure_greedy.argtypes = [vp, i32, vp]
         lib.dip_sim_set_greedy_inbox.argtypes = [vp, i32]
@@ -114,7 +118,8 @@ def load():
         for name in ("dip_sim_check_topology", "dip_sim_check_costs", "dip_sim_create",
                      "dip_sim_configure", "dip_sim_configure_pool", "dip_sim_configure_check",
                      "dip_sim_get_info",
-                     "dip_sim_evaluate", "dip_sim_profile", "dip_sim_last_profile",
+                     "dip_sim_evaluate", "dip_sim_evaluate_static",
+                     "dip_sim_profile", "dip_sim_last_profile",
                      "dip_sim_last_retries",
                      "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_set_greedy_inbox", "dip_sim_greedy",
                      "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_sim_rollouts_batch",
@@ -242,6 +247,15 @@ def evaluate(h, costs, orders, n_cand, out_makespan, out_bubble, out_peakmem, ou
         int(n_cand), out_makespan.data_ptr(), out_bubble.data_ptr(),
         out_peakmem.data_ptr(), out_flags.data_ptr(), _stream_ptr(stream))
     _check(rc, "dip_sim_evaluate")
+
+
+def evaluate_static(h, orders, n_cand, out_makespan, out_bubble, out_peakmem, out_flags,
+                    stream=None) -> int:
+    """The allocation-free evaluate (costs of an earlier evaluate call);
+    returns the ABI code, so that callers can see DIP_E_CAPACITY."""
+    return load().dip_sim_evaluate_static(
+        h, orders.data_ptr(), int(n_cand), out_makespan.data_ptr(), out_bubble.data_ptr(),
+        out_peakmem.data_ptr(), out_flags.data_ptr(), _stream_ptr(stream))
 
 
 def argmin(h, makespan, flags, n_cand, index_base, inout_best_key, stream=None) -> None:
@@ -415,6 +429,15 @@ class Sim:
         evaluate(self.h, send, orders, n, *out, stream=stream)
         self._costs_sent = True
         return out
+
+    def evaluate_static(self, orders, out=None, stream=None) -> int:
+        """The allocation-free evaluate; the costs must have gone with an
+        earlier evaluate.  Returns the ABI code."""
+        n = int(orders.shape[0])
+        assert orders.dtype.itemsize == 2 and orders.is_contiguous()
+        assert orders.shape[1] == self.stride
+        out = self.outputs(n, orders.device) if out is None else out
+        return evaluate_static(self.h, orders, n, *out, stream=stream), out
 
     def configure_greedy(self, n_groups, op_group) -> int:
         rc = configure_greedy(self.h, n_groups, op_group)

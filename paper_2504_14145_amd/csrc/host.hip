@@ -18,6 +18,7 @@
 #include <cstdint>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <unordered_map>
@@ -31,6 +32,39 @@ using namespace dipsim;
 namespace {
 
 thread_local hipError_t g_last_hip = hipSuccess;
+constexpr int kMaxDevices = 64;
+
+// dip_sim_evaluate_static's working memory, one copy per GPU for the life of
+// the process: the retry counters (kStaticHead bytes), then two retry lists of
+// kStaticMaxCand 8-byte entries.  In host code `scratch` only names the
+// symbol; its device address comes from hipGetSymbolAddress, per device.
+constexpr int64_t kStaticMaxCand = int64_t(1) << 22;
+constexpr int64_t kStaticHead = 256;
+constexpr int64_t kStaticBytes = kStaticHead + 2 * 8 * kStaticMaxCand;
+static __device__ __align__(256) unsigned char scratch[kStaticBytes];
+
+// the device address of `scratch` on the current device, looked up once per
+// device (nullptr, with the HIP error kept, if the lookup fails)
+void *static_scratch_on_current_device() {
+  static std::mutex mu;
+  static void *addr[kMaxDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    g_last_hip = hipErrorInvalidDevice;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) {
+      g_last_hip = e;
+      return nullptr;
+    }
+    addr[dev] = ptr;
+  }
+  return addr[dev];
+}
 
 constexpr int kMaxRanks = 64;
 constexpr int32_t kMaxOpsPerRank = 32768;
@@ -97,6 +131,8 @@ struct dip_sim {
   int64_t sim2_lds = 0;
   int64_t *d_retry2 = nullptr;         // candidates the second pass could not hold
   hipStream_t last_stream = nullptr;   // stream of the last evaluate (diagnostics)
+  uint32_t *last_counts = nullptr;     // its retry counters
+  void *d_static = nullptr;            // this device's address of the static scratch array
   bool last_pass2 = false;             // it ran the second simulation pass
   int4 *d_pool_rec = nullptr;          // pool records [N][2]
   int2 *d_pool_edge = nullptr;         // pool edges [E]
@@ -435,7 +471,8 @@ bool use_tile_check(const dip_sim *h) {
 }
 
 int run_tile_check(dip_sim *h, const int16_t *orders, int64_t n_cand, int32_t *out_ms,
-                   int32_t *out_bub, int32_t *out_peak, uint8_t *out_flags, hipStream_t stream) {
+                   int32_t *out_bub, int32_t *out_peak, uint8_t *out_flags, hipStream_t stream,
+                   uint32_t *counts) {
   TileCheckArgs c{};
   c.orders = orders;
   c.n_cand = n_cand;
@@ -449,7 +486,7 @@ int run_tile_check(dip_sim *h, const int16_t *orders, int64_t n_cand, int32_t *o
   c.cap = h->d_cap;
   c.selfp = h->d_selfp;
   c.P = h->P;
-  c.retry_count = h->d_retry_count;
+  c.retry_count = counts;
   const int64_t tiles = (n_cand + kWave - 1) / kWave;
   for (int pass = 0; pass < (h->to_ok ? 2 : 1); ++pass) {
     const dip_sim::TilePlan &T = pass ? h->to : h->tc;
@@ -464,7 +501,8 @@ int run_tile_check(dip_sim *h, const int16_t *orders, int64_t n_cand, int32_t *o
 }
 
 int run_wave_check(dip_sim *h, const int16_t *orders, int64_t n_cand, int32_t *out_ms,
-                   int32_t *out_bub, int32_t *out_peak, uint8_t *out_flags, hipStream_t stream) {
+                   int32_t *out_bub, int32_t *out_peak, uint8_t *out_flags, hipStream_t stream,
+                   uint32_t *counts) {
   CheckArgs c{};
   c.orders = orders;
   c.n_cand = n_cand;
@@ -479,7 +517,7 @@ int run_wave_check(dip_sim *h, const int16_t *orders, int64_t n_cand, int32_t *o
   c.P = h->P;
   c.N = h->N;
   c.wpb = 4;
-  c.retry_count = h->d_retry_count;
+  c.retry_count = counts;
   const int64_t c_lds = 4 * check_lds_per_group(h->N);
   const int64_t c_per_block = 4;
   const int c_blocks = int(std::min<int64_t>((n_cand + c_per_block - 1) / c_per_block,
@@ -1193,6 +1231,8 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
   if (hipDeviceGetAttribute(&v, hipDeviceAttributeSharedMemPerBlockOptin, h->device) == hipSuccess && v > 0)
     h->lds_block_max = std::max<int64_t>(h->lds_block_max, v);
   (void)hipGetLastError();
+  h->d_static = static_scratch_on_current_device();
+  if (!h->d_static) return hip_fail(g_last_hip);
   if ((e = hipMalloc(&h->d_rec, size_t(h->N) * 16)) != hipSuccess) return hip_fail(e);
   if ((e = hipMalloc(&h->d_edge, size_t(std::max(h->E, 1)) * 8)) != hipSuccess) return hip_fail(e);
   if ((e = hipMalloc(&h->d_md, size_t(h->N) * 4)) != hipSuccess) return hip_fail(e);
@@ -1311,9 +1351,21 @@ int dip_sim_get_info(const dip_sim *h, dip_sim_info *info) {
   return DIP_OK;
 }
 
-int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, int64_t n_cand,
-                     int32_t *out_makespan, int32_t *out_bubble, int32_t *out_peakmem,
-                     uint8_t *out_flags, void *stream_) {
+}  // extern "C"
+
+namespace {
+
+// Device memory an evaluate call works in beyond its inputs and outputs: the
+// retry counters and the two retry lists (variants 8 and 9).
+struct CallScratch {
+  uint32_t *counts;   // [4] zeroed by the check kernel
+  int64_t *list_a;    // [n_cand] first pass retries
+  int64_t *list_b;    // [n_cand] second pass retries (variant 9)
+};
+
+int evaluate_impl(dip_sim *h, const dip_costs *costs, const int16_t *orders, int64_t n_cand,
+                  int32_t *out_makespan, int32_t *out_bubble, int32_t *out_peakmem,
+                  uint8_t *out_flags, void *stream_, const CallScratch *sx) {
   if (!h || n_cand < 0) return DIP_E_INVAL;
   hipStream_t stream = static_cast<hipStream_t>(stream_);
   if (costs) {
@@ -1336,13 +1388,20 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
   };
   (void)hipGetLastError();
   if (h->variant >= 8) {
-    int rc = ensure_retry(h, n_cand);
-    if (rc != DIP_OK) return rc;
+    CallScratch own{};
+    if (!sx) {   // the handle's buffers, grown to the batch
+      int rc = ensure_retry(h, n_cand);
+      if (rc != DIP_OK) return rc;
+      own = CallScratch{h->d_retry_count, h->d_retry, h->d_retry2};
+      sx = &own;
+    }
+    uint32_t *const counts = sx->counts;
+    h->last_counts = counts;
     DIP_HIP(mark(0));
-    rc = use_tile_check(h) ? run_tile_check(h, orders, n_cand, out_makespan, out_bubble,
-                                            out_peakmem, out_flags, stream)
-                           : run_wave_check(h, orders, n_cand, out_makespan, out_bubble,
-                                            out_peakmem, out_flags, stream);
+    int rc = use_tile_check(h) ? run_tile_check(h, orders, n_cand, out_makespan, out_bubble,
+                                                out_peakmem, out_flags, stream, counts)
+                               : run_wave_check(h, orders, n_cand, out_makespan, out_bubble,
+                                                out_peakmem, out_flags, stream, counts);
     if (rc != DIP_OK) return rc;
     DIP_HIP(mark(1));
     const uint32_t round_limit = uint32_t(h->N) + uint32_t(h->E) + 16u;
@@ -1357,8 +1416,8 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
       if (h->N > 4096) return n_cand >= 2 * n_slots ? n_slots : INT64_MAX;
       return n_cand >= 4 * n_slots ? n_slots * ((n_cand / 10 * 9) / n_slots) : INT64_MAX;
     };
-    const int64_t *retry_list = h->d_retry;
-    const uint32_t *retry_count = h->d_retry_count;
+    const int64_t *retry_list = sx->list_a;
+    const uint32_t *retry_count = counts;
     h->last_stream = stream;
     h->last_pass2 = false;
     if (h->variant == 9 && h->sim_costs_ok) {
@@ -1377,8 +1436,8 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
       a.state_base = uint32_t(h->sim_state_base);
       a.P = h->P;
       a.wpb = h->sim_wpb;
-      a.retry = h->d_retry;
-      a.retry_count = h->d_retry_count;
+      a.retry = sx->list_a;
+      a.retry_count = counts;
       a.round_limit = round_limit;
       const int64_t per_block = int64_t(h->sim_wpb) * h->G;
       const int blocks =
@@ -1391,16 +1450,16 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
         // the candidates whose pools filled, again with 16 slots per pool
         // (deadlocked orders fill small pools too; larger ones tell them
         // from merely crowded ones); its own retries go to the general kernel
-        a.list = h->d_retry;
-        a.list_count = h->d_retry_count;
-        a.retry = h->d_retry2;
-        a.retry_count = h->d_retry_count + 2;
+        a.list = sx->list_a;
+        a.list_count = counts;
+        a.retry = sx->list_b;
+        a.retry_count = counts + 2;
         a.wpb = h->sim2_wpb;
         a.static_end = INT64_MAX;
         DIP_HIP(launch_sim(h->pwl, 16, h->sim_paged, h->sim2_max_blocks, h->sim2_wpb,
                            size_t(h->sim2_lds), stream, a));
-        retry_list = h->d_retry2;
-        retry_count = h->d_retry_count + 2;
+        retry_list = sx->list_b;
+        retry_count = counts + 2;
         h->last_pass2 = true;
       }
       DIP_HIP(mark(3));
@@ -1418,8 +1477,8 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
       a.busy = h->d_busy;
       a.P = h->P;
       a.wpb = h->wpb;
-      a.retry = h->d_retry;
-      a.retry_count = h->d_retry_count;
+      a.retry = sx->list_a;
+      a.retry_count = counts;
       a.rec_bytes = h->N * 16;
       a.edge_bytes = std::max(h->n_extra, 1) * 8;
       a.tab_edges = uint32_t(align16(int64_t(h->N) * 16));
@@ -1428,7 +1487,7 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
       const int64_t per_block = int64_t(h->wpb) * h->G;
       const int blocks = int(std::min<int64_t>((n_cand + per_block - 1) / per_block, h->max_blocks));
       const int64_t se = static_end_for(int64_t(blocks) * per_block);
-      a.next_cand = se == INT64_MAX ? nullptr : h->d_retry_count + 1;
+      a.next_cand = se == INT64_MAX ? nullptr : counts + 1;
       a.static_end = se == INT64_MAX ? 0 : se;
       DIP_HIP(launch_pool(h->pwl, h->pool_slots, h->pool_tab, blocks, h->wpb,
                           size_t(h->lds_bytes), stream, a));
@@ -1497,6 +1556,34 @@ int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, 
   DIP_HIP(launch_general(v, blocks, wpb, size_t(lds), stream, a));
   DIP_HIP(mark(1));
   return DIP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int dip_sim_evaluate(dip_sim *h, const dip_costs *costs, const int16_t *orders, int64_t n_cand,
+                     int32_t *out_makespan, int32_t *out_bubble, int32_t *out_peakmem,
+                     uint8_t *out_flags, void *stream) {
+  return evaluate_impl(h, costs, orders, n_cand, out_makespan, out_bubble, out_peakmem, out_flags,
+                       stream, nullptr);
+}
+
+int dip_sim_evaluate_static(dip_sim *h, const int16_t *orders, int64_t n_cand,
+                            int32_t *out_makespan, int32_t *out_bubble, int32_t *out_peakmem,
+                            uint8_t *out_flags, void *stream) {
+  if (!h || n_cand < 0) return DIP_E_INVAL;
+  if (!h->costs_set) return DIP_E_STATE;
+  if (n_cand > kStaticMaxCand) return DIP_E_CAPACITY;
+  if (!h->d_static) return DIP_E_STATE;
+  // the array's device address on this handle's device: counters, then the
+  // two lists of kStaticMaxCand entries
+  unsigned char *base = static_cast<unsigned char *>(h->d_static);
+  const CallScratch sx{reinterpret_cast<uint32_t *>(base),
+                       reinterpret_cast<int64_t *>(base + kStaticHead),
+                       reinterpret_cast<int64_t *>(base + kStaticHead + 8 * kStaticMaxCand)};
+  return evaluate_impl(h, nullptr, orders, n_cand, out_makespan, out_bubble, out_peakmem,
+                       out_flags, stream, &sx);
 }
 
 int dip_sim_configure_greedy(dip_sim *h, int32_t n_groups, const int32_t *op_group) {
@@ -2136,10 +2223,10 @@ int dip_sim_last_profile(dip_sim *h, float *out_ms, int32_t *n_out) {
 int dip_sim_last_retries(dip_sim *h, int64_t *out_first, int64_t *out_second) {
   if (!h || !out_first || !out_second) return DIP_E_INVAL;
   *out_first = *out_second = 0;
-  if (h->variant < 8 || !h->d_retry_count) return DIP_OK;
+  if (h->variant < 8 || !h->last_counts) return DIP_OK;
   DIP_HIP(hipStreamSynchronize(h->last_stream));
   uint32_t cnt[4] = {0, 0, 0, 0};
-  DIP_HIP(hipMemcpy(cnt, h->d_retry_count, sizeof(cnt), hipMemcpyDeviceToHost));
+  DIP_HIP(hipMemcpy(cnt, h->last_counts, sizeof(cnt), hipMemcpyDeviceToHost));
   *out_first = cnt[0];
   *out_second = h->last_pass2 ? cnt[2] : cnt[0];
   return DIP_OK;
@@ -2157,6 +2244,7 @@ const char *dip_sim_strerror(int code) {
     case DIP_E_NOMEM: return "out of memory";
     case DIP_E_HIP: return hipGetErrorString(g_last_hip);
     case DIP_E_STATE: return "no costs supplied yet";
+    case DIP_E_CAPACITY: return "batch larger than the static scratch area holds";
     default: return "unknown error";
   }
 }

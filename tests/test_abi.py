@@ -27,11 +27,11 @@ def test_library_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(dip.EXPORTS)
-    assert lib.dip_sim_abi_version() == 5
+    assert lib.dip_sim_abi_version() == 6
 
 
 def test_strerror_strings():
-    for code in (0, -1, -2, -3, -4, -5, -7):
+    for code in (0, -1, -2, -3, -4, -5, -7, -8):
         assert len(dip.strerror(code)) >= 2
     assert dip.strerror(12345) == "unknown error"
 
