@@ -65,8 +65,10 @@ if ROOT not in sys.path:
 HBM_PEAK_GBS = 8000.0
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "pool_kernel_traffic.md")
 GREEDY_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "greedy_kernel_traffic.md")
+SIM_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "sim_kernel_traffic.md")
 CSRC = os.path.join(ROOT, "paper_2504_14145_amd", "csrc")
 POOL_SOURCES = [os.path.join(CSRC, f) for f in ("kern_pool.hip", "internal.h", "dev_util.h")]
+SIM_SOURCES = [os.path.join(CSRC, f) for f in ("kern_sim.hip", "internal.h", "dev_util.h")]
 GREEDY_SOURCES = [os.path.join(CSRC, f) for f in ("kern_greedy.hip", "internal.h", "dev_util.h")]
 MEMOPT_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "memopt_wave_kernel_traffic.md")
 MEMOPT_SOURCES = [os.path.join(CSRC, f) for f in ("kern_memopt.hip", "internal.h", "dev_util.h")]
@@ -409,7 +411,11 @@ def main():
     achieved_gbs = algo_bytes / dom_s / 1e9
     kern_ops_per_s = n_cand * prob.n_total / dom_s
     slots = info.get("pool_slots", 0)
-    traffic = measured_traffic(cfg.name, n_cand, slots) if info["variant"] in (8, 9) else None
+    # the counter summary of the simulation kernel that ran (variant 9: the
+    # compact-record kernel, variant 8: the pool kernel)
+    prof_file, prof_src = {8: (TRAFFIC_FILE, POOL_SOURCES),
+                           9: (SIM_TRAFFIC_FILE, SIM_SOURCES)}.get(info["variant"], (None, None))
+    traffic = measured_traffic(cfg.name, n_cand, slots, prof_file, prof_src) if prof_file else None
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -447,8 +453,8 @@ def main():
         # against the integer-issue bound (about 5 int32 operations per op)
         "issue": {"achieved": kern_ops_per_s, "peak": ISSUE_PEAK_OPS, "unit": "simulated ops/s",
                   "frac": kern_ops_per_s / ISSUE_PEAK_OPS,
-                  "counters": measured_issue(cfg.name, n_cand, slots)
-                  if info["variant"] == 8 else None},
+                  "counters": measured_issue(cfg.name, n_cand, slots, prof_file, prof_src)
+                  if prof_file else None},
         "steady_state": steady,
         "cpu_baseline": cpu,
     }

@@ -1211,7 +1211,9 @@ int dip_sim_create(const dip_topology *t, dip_sim **out) {
       const int32_t np = h->pred_ptr[g + 1] - h->pred_ptr[g];
       if (np > 1) sim_extra += np;
     }
-    h->sim_ok = h->pool_ok && max_nr <= kSimDeltaMax + 1 && sim_extra < (int64_t(1) << 24);
+    // (the simulation kernel plays rank r on lane r of a power-of-two group)
+    h->sim_ok = h->pool_ok && (h->P & (h->P - 1)) == 0 && max_nr <= kSimDeltaMax + 1 &&
+                sim_extra < (int64_t(1) << 24);
     h->sim_n_extra = int32_t(std::min<int64_t>(sim_extra, INT32_MAX));
     // pools: 8 slots per rank (the simulation kernel's candidates that fill
     // them go through a second pass with 16)

@@ -212,31 +212,37 @@ constexpr uint32_t kSimLast = 1u << 31;
 // consecutive local ids, equal pages stored once)
 constexpr int kSimPage = 16;
 
-// Per-candidate LDS state of the simulation kernel, for a group of PW lanes:
-//   counts [PW][C] words (4-bit reader count per pool slot, C = ceil(S / 8))
-//   tags   [S / 8][PW][8] 16-bit (local id + 1 of the op whose end time a slot
-//          holds; slots 8h .. 8h + 7 of all ranks together, 16 bytes per rank;
-//          with S = 4, [PW][4])
-//   ends   [PW][S + 1] words
-//   rings  [PW] 40-byte order rings (4 blocks of 4 ids; 8-byte stride pad)
-constexpr int64_t kSimRingStride = 40;
+// Per-candidate LDS state of the simulation kernel, for a group of PW lanes
+// (one per rank; the kernel requires P == PW):
+//   tags   [S / 8][PW][8] 16-bit (local id + 1 of the op whose end time a pool
+//          slot holds; slots 8h .. 8h + 7 of all ranks together, 16 bytes per
+//          rank, so that a group's 16-byte tag reads tile the banks; with
+//          S = 4, [PW][4])
+//   pools  [PW] sim_pool_bytes(S) each: C = ceil(S / 8) count words (4-bit
+//          reader count per slot), then S end-time words; padded to an odd
+//          number of words so that different ranks' pools start in different
+//          banks
+//   rings  [PW] order rings of kSimRingBytes: two 16-byte blocks of 8 ids
+//          (and an 8-byte pad)
+constexpr int64_t kSimBlockIds = 8;
+constexpr int64_t kSimRingBytes = 40;
 __host__ __device__ constexpr int64_t sim_count_words(int slots) { return (slots + 7) / 8; }
-__host__ __device__ constexpr int64_t sim_tags_offset(int pw, int slots) {
-  return (int64_t(pw) * 4 * sim_count_words(slots) + 15) / 16 * 16;
+__host__ __device__ constexpr int64_t sim_tag_bytes(int pw, int slots) { return int64_t(pw) * 2 * slots; }
+__host__ __device__ constexpr int64_t sim_pool_bytes(int slots) {
+  const int64_t words = sim_count_words(slots) + slots;
+  return 4 * (words % 2 == 0 ? words + 1 : words);
 }
-__host__ __device__ constexpr int64_t sim_ends_offset(int pw, int slots) {
-  return sim_tags_offset(pw, slots) + (int64_t(pw) * 2 * slots + 15) / 16 * 16;
+__host__ __device__ constexpr int64_t sim_pool_offset(int pw, int slots) {
+  return (sim_tag_bytes(pw, slots) + 15) / 16 * 16;
 }
-__host__ __device__ constexpr int64_t sim_end_stride(int slots) { return 4 * int64_t(slots) + 4; }
 __host__ __device__ constexpr int64_t sim_ring_offset(int pw, int slots) {
-  return (sim_ends_offset(pw, slots) + int64_t(pw) * sim_end_stride(slots) + 15) / 16 * 16;
+  return (sim_pool_offset(pw, slots) + int64_t(pw) * sim_pool_bytes(slots) + 15) / 16 * 16;
 }
 // padded so that the group's size in words is congruent to PW modulo the 32
 // banks (4 words below 4 lanes): the same word of consecutive groups then
-// falls in different banks, and a half-wave's reads of its groups' counts and
-// tags tile the banks
+// falls in different banks
 __host__ __device__ constexpr int64_t sim_group_bytes(int pw, int slots) {
-  const int64_t raw = sim_ring_offset(pw, slots) + int64_t(pw) * kSimRingStride;
+  const int64_t raw = sim_ring_offset(pw, slots) + int64_t(pw) * kSimRingBytes;
   const int64_t want = pw >= 32 ? 0 : 4 * (pw < 4 ? 4 : pw);   // residue modulo 128 bytes
   int64_t x = (raw + 15) / 16 * 16;
   while (x % 128 != want) x += 16;

@@ -1,5 +1,6 @@
 // kern_sim.hip -- timing simulation of candidate schedules, one wavefront
-// holding 64 / PW candidates, lane r of a candidate's group playing rank r.
+// holding 64 / PW candidates, lane r of a candidate's group playing rank r
+// (the number of ranks P is a power of two, PW = P).
 //
 // What is simulated (Sec. 5.2 and 6.1): every rank runs its ops one at a
 // time in its given order, each op as soon as the rank is free and the
@@ -26,18 +27,20 @@
 //   * the pools of the candidates in flight (a few items per rank are live at
 //     once, so a pool of 8 or 16 slots per rank suffices where a table of end
 //     times by op would need 4 bytes per op);
-//   * each lane's order ring: 4 blocks of 4 ids of its rank's section.  Every
-//     4 rounds (the same rounds for all lanes, so that one wait covers the
-//     loads) each lane that has room loads its next 8-byte block from HBM
-//     into registers; 3 rounds later the block is stored into the ring.  A
-//     lane fires at most one op per round, so with two blocks ahead at every
-//     load round the id it reads two positions ahead is always in the ring.
+//   * each lane's order ring: two 16-byte blocks of 8 ids of its rank's
+//     section.  Every 4 rounds (the same rounds for all lanes, so that one
+//     wait covers the loads) each lane that has moved into the later of its
+//     two blocks loads the block after it from HBM into registers; 3 rounds
+//     later the block is stored into the ring, over the one the lane left.
+//     A lane fires at most one op per round and needs the id after its
+//     current one, so the at most 6 rounds a block takes to arrive end before
+//     the lane has used up the block it is in.
 //
 // Verdicts: a group is done when all of its lanes ran their whole order.  A
 // round in which no lane of a group fired an op or read an item leaves its
 // state unchanged for good: if no lane was held by back-pressure the orders
 // deadlock; otherwise the bounded pools may be what stalls it, and the
-// candidate goes to a retry list that the general kernel re-simulates.  The
+// candidate goes to a retry list that a later pass re-simulates.  The
 // permutation check and the memory scan ran before, in the check kernel,
 // whose flags this kernel reads (invalid candidates are skipped) and extends.
 #include "dip_sim.h"
@@ -57,9 +60,6 @@ __device__ __forceinline__ uint32_t lds16(uint32_t a) {
 }
 __device__ __forceinline__ uint2 lds64(uint32_t a) {
   return *reinterpret_cast<const uint2 *>(s_lds + a);
-}
-__device__ __forceinline__ uint4 lds128(uint32_t a) {
-  return *reinterpret_cast<const uint4 *>(s_lds + a);
 }
 __device__ __forceinline__ void st32(uint32_t a, uint32_t v) {
   *reinterpret_cast<uint32_t *>(s_lds + a) = v;
@@ -82,14 +82,25 @@ __device__ __forceinline__ void lds_sub(uint32_t a, uint32_t v) {
 __device__ __forceinline__ bool lane_in(uint64_t m) { return __builtin_amdgcn_inverse_ballot_w64(m); }
 __device__ __forceinline__ uint64_t ballot(bool b) { return __builtin_amdgcn_ballot_w64(b); }
 
+// A 16-byte order block of 8 ids (rows are padded to 8 ids, so a block of
+// a row never reaches past it).
+__device__ __forceinline__ uint4 load_block(const int16_t *row, uint32_t b) {
+  return *reinterpret_cast<const uint4 *>(row + int64_t(b) * kSimBlockIds);
+}
+__device__ __forceinline__ void store_block(uint32_t at, const uint4 &v) {
+  st64(at, v.x, v.y);
+  st64(at + 8, v.z, v.w);
+}
+
 template <int PWL, int S, bool PAGED>
 __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
   constexpr int PW = 1 << PWL;
   constexpr int G = kWave / PW;
   constexpr int kC = int(sim_count_words(S));
-  constexpr uint32_t kTags = uint32_t(sim_tags_offset(PW, S));
-  constexpr uint32_t kEnds = uint32_t(sim_ends_offset(PW, S));
-  constexpr uint32_t kEndStride = uint32_t(sim_end_stride(S));
+  constexpr uint32_t kPool = uint32_t(sim_pool_bytes(S));
+  constexpr uint32_t kPools = uint32_t(sim_pool_offset(PW, S));
+  constexpr uint32_t kTagRank = S == 4 ? 8u : 16u;   // a rank's tag bytes in one tag array
+  constexpr uint32_t kEndAt = 4u * uint32_t(kC);      // end times after a pool's counts
   constexpr uint32_t kRing = uint32_t(sim_ring_offset(PW, S));
   constexpr uint32_t kGroup = uint32_t(sim_group_bytes(PW, S));
   static_assert(S == 4 || S == 8 || S == 16, "pool size");
@@ -103,16 +114,17 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
   const int wave = threadIdx.x / kWave;
   const int grp = lane >> PWL;
   const int r = lane & (PW - 1);
-  const uint32_t P = uint32_t(a.P);
-  const bool on = uint32_t(r) < P;
+  const bool on = r < a.P;
   const int gbit = grp << PWL;
   const int64_t n_slots = int64_t(gridDim.x) * a.wpb * G;
   const uint32_t gbase = a.state_base + uint32_t(wave * G + grp) * kGroup;
   const uint32_t rr = on ? uint32_t(r) : 0u;
-  const uint32_t my_cnt = gbase + rr * 4u * kC;
-  const uint32_t my_tags = gbase + kTags + rr * (S == 4 ? 8u : 16u);
-  const uint32_t my_ends = gbase + kEnds + rr * kEndStride;
-  const uint32_t my_ring = gbase + kRing + rr * uint32_t(kSimRingStride);
+  const uint32_t my_pool = gbase + kPools + rr * kPool;
+  const uint32_t my_tags = gbase + rr * kTagRank;
+  const uint32_t my_ring = gbase + kRing + rr * uint32_t(kSimRingBytes);
+  // the rank in the edge word's rank-difference field: adding it there and
+  // keeping the field's low PWL bits gives the predecessor's rank
+  const uint32_t rank_sh = rr << 14;
   int rb = 0, nr = 0, busy_r = 0, recb = 0;
   if (on) {
     const int4 li = reinterpret_cast<const int4 *>(a.lane_info)[r];
@@ -121,22 +133,23 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     busy_r = li.z;
     recb = li.w;
   }
-  // absolute row positions of this lane's section, and its last 8-byte block
-  const uint32_t a_last = uint32_t(rb + max(nr - 1, 0));
-  const uint32_t blk_last = a_last >> 2;
+  // absolute row positions: past this lane's section, its last block
+  const uint32_t a_end = uint32_t(rb + nr);
+  const uint32_t blk_last = uint32_t(rb + max(nr - 1, 0)) / uint32_t(kSimBlockIds);
+  const uint32_t pmap_lane = a.off_pmap + 2u * uint32_t(recb);
 
   // the record of local id `id` of this lane's rank
   auto rec_of = [&](uint32_t id) -> uint2 {
     uint32_t addr;
     if constexpr (PAGED) {
-      const uint32_t pg = lds16(a.off_pmap + 2u * (uint32_t(recb) + (id >> 4)));
+      const uint32_t pg = lds16(pmap_lane + 2u * (id >> 4));
       addr = (pg << 7) | ((id & 15u) << 3);
     } else {
       addr = (uint32_t(recb) + id) << 3;
     }
     return lds64(addr);
   };
-  auto ring_id = [&](uint32_t pos) { return lds16(my_ring + ((pos & 15u) << 1)); };
+  auto ring_at = [&](uint32_t pos) { return my_ring + ((pos & 15u) << 1); };
 
   // candidates: positions k < n of the batch, or of the list in list mode
   const int64_t n_todo = a.list ? int64_t(*a.list_count) : a.n_cand;
@@ -148,19 +161,26 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
   bool has = false;        // the group holds a candidate
   uint8_t fl = 0;          // the check kernel's flags for it
   uint32_t cand_round = 0;
-  uint32_t ptr = 0;        // position of the current op in the section
+  uint32_t apos1 = 0;      // absolute row position of the op after the current one
   uint32_t tfree = 0, acc = 0;
-  uint32_t lid = 0, cur0 = 0;   // current op: local id, record word 0
-  uint32_t ce = 0, xi = 0;      // current edge word; index of the op's next extra edge
-  uint32_t nid = 0, nxt0 = 0, nce = 0, nxi = 0;   // the op after it, likewise
-  uint32_t lb = 0;         // next absolute 8-byte block of the row to load
-  uint2 blk = make_uint2(0, 0);   // a loaded block waiting to be stored
+  uint32_t lid1 = 0, cur0 = 0;  // current op: local id + 1, record word 0
+  uint32_t ce = 0, xi = 0;      // its current edge word; index of its next extra edge
+  uint32_t lb = 0;         // next absolute order block to load
+  uint4 blk{};             // a loaded block waiting to be stored
   const int16_t *row = a.orders;
 
   // wave-uniform lane masks
   uint64_t m_live = 0;     // lanes running an op sequence
   uint64_t m_npend = 0;    // live lanes whose current op waits for no edge
   uint64_t m_blk = 0;      // lanes holding a loaded block for the ring
+
+  auto set_current = [&](uint32_t id, uint2 c) {
+    lid1 = id + 1u;
+    cur0 = c.x;
+    ce = c.y;
+    xi = c.y + 1u;
+    if (c.x & kSimMulti) ce = lds32(a.off_extra + 4u * c.y);
+  };
 
   auto next_k = [&]() -> int64_t {
     const int64_t succ = k + n_slots;
@@ -179,9 +199,9 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     while (k < n_todo && (a.out_flags[cand_at(k)] & (DIP_FLAG_INVALID | DIP_FLAG_DEADLOCK)))
       k = next_k();
     has = k < n_todo;
-    if (on) {
+    if (on) {   // empty pool: counts and tags zero
 #pragma unroll
-      for (int i = 0; i < kC; ++i) st32(my_cnt + 4u * i, 0u);
+      for (int i = 0; i < kC; ++i) st32(my_pool + 4u * i, 0u);
 #pragma unroll
       for (int i = 0; i < S / 2; ++i) st32(my_tags + 16u * PW * (i >> 2) + 4u * (i & 3), 0u);
     }
@@ -189,31 +209,18 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     cand = cand_at(k);
     fl = a.out_flags[cand];
     cand_round = rnd;
-    ptr = 0;
     tfree = 0;
     acc = 0;
     if (!on || nr == 0) return;
     row = a.orders + cand * a.stride;
-    // the first three blocks of the section into the ring
-    const uint32_t b0 = uint32_t(rb) >> 2;
-    const uint32_t bn = min(b0 + 2u, blk_last);
-    for (uint32_t b = b0; b <= bn; ++b) {
-      const uint2 v = *reinterpret_cast<const uint2 *>(row + 4 * int64_t(b));
-      st64(my_ring + (b & 3u) * 8u, v.x, v.y);
-    }
-    lb = bn + 1;
-    lid = ring_id(uint32_t(rb));
-    nid = ring_id(min(uint32_t(rb) + 1u, a_last));
-    const uint2 c = rec_of(lid);
-    const uint2 n = rec_of(nid);
-    cur0 = c.x;
-    nxt0 = n.x;
-    ce = c.y;
-    xi = c.y + 1;
-    if (c.x & kSimMulti) ce = lds32(a.off_extra + 4u * c.y);
-    nce = n.y;
-    nxi = n.y + 1;
-    if (n.x & kSimMulti) nce = lds32(a.off_extra + 4u * n.y);
+    // the first two blocks of the section into the ring
+    const uint32_t b0 = uint32_t(rb) / uint32_t(kSimBlockIds);
+    const uint32_t bn = min(b0 + 1u, blk_last);
+    for (uint32_t b = b0; b <= bn; ++b) store_block(my_ring + (b & 1u) * 16u, load_block(row, b));
+    lb = bn + 1u;
+    apos1 = uint32_t(rb) + 1u;
+    const uint32_t id0 = lds16(ring_at(uint32_t(rb)));
+    set_current(id0, rec_of(id0));
   };
 
   start_candidate(0);
@@ -230,20 +237,17 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     const uint32_t phase = rnd & 3u;
     if (phase == 3u && m_blk) {
       if (lane_in(m_blk)) {
-        st64(my_ring + (lb & 3u) * 8u, blk.x, blk.y);
+        store_block(my_ring + (lb & 1u) * 16u, blk);
         ++lb;
       }
       m_blk = 0;
     }
 
-    // ---- reads: the predecessor's pool tags, my counts, the id two ahead
-    const uint32_t dr = (ce >> 14) & 63u;
-    uint32_t pr = rr + dr;
-    pr = min(pr, pr - P);   // (rr + dr) mod P, dr < P
-    const uint32_t p_tags = gbase + kTags + pr * (S == 4 ? 8u : 16u);
-    const uint32_t p_ends = gbase + kEnds + pr * kEndStride;
-    const uint32_t p_cnt = gbase + pr * 4u * kC;
-    const uint32_t want = lid + uint32_t(int32_t(ce << 18) >> 18) + 1u;
+    // ---- reads: the predecessor's pool, my counts, the next id
+    const uint32_t pr = ((ce + rank_sh) >> 14) & uint32_t(PW - 1);
+    const uint32_t pool = gbase + kPools + pr * kPool;
+    const uint32_t p_tags = gbase + pr * kTagRank;
+    const uint32_t want = lid1 + uint32_t(int32_t(ce << 18) >> 18);
     uint32_t tw[S / 2];
     if constexpr (S == 4) {
       const uint2 v = lds64(p_tags);
@@ -252,7 +256,7 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     } else {
 #pragma unroll
       for (int i = 0; i < S / 8; ++i) {   // slots 8i .. 8i + 7 of every rank side by side
-        const uint4 v = lds128(p_tags + 16u * PW * i);
+        const uint4 v = *reinterpret_cast<const uint4 *>(s_lds + p_tags + 16u * PW * i);
         tw[4 * i] = v.x;
         tw[4 * i + 1] = v.y;
         tw[4 * i + 2] = v.z;
@@ -261,8 +265,10 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     }
     uint32_t cnt[kC];
 #pragma unroll
-    for (int i = 0; i < kC; ++i) cnt[i] = lds32(my_cnt + 4u * i);
-    const uint32_t idn = ring_id(min(uint32_t(rb) + ptr + 2u, a_last));
+    for (int i = 0; i < kC; ++i) cnt[i] = lds32(my_pool + 4u * i);
+    const uint32_t idn = lds16(ring_at(apos1));
+    // the next op's record, read ahead (used by the lanes that advance)
+    const uint2 nrec = rec_of(idn);
 
     // the matching slot (tags are unique within a pool): 4 x its index, or
     // kNoHit; one compare and one select per slot, all vector instructions
@@ -276,7 +282,7 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     }
     const uint64_t m_found = ballot(hit4 != kNoHit) & m_live & ~m_npend;
     hit4 &= 0x7cu;
-    const uint32_t hit_end = lds32(p_ends + hit4);
+    const uint32_t hit_end = lds32(pool + kEndAt + hit4);
     const bool found = lane_in(m_found);
     const uint32_t acc_n = found ? max(acc, hit_end + ((ce >> 20) & 0x7ffu)) : acc;
     // a free slot of my pool (reader count zero): the first one
@@ -306,23 +312,22 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     // ---- writes: release what was read, publish what was produced
     if (found) {
       const uint32_t slot = hit4 >> 2;
-      lds_sub(p_cnt + (kC > 1 ? 4u * (slot >> 3) : 0u), 1u << (4u * (slot & 7u)));
+      lds_sub(pool + (kC > 1 ? 4u * (slot >> 3) : 0u), 1u << (4u * (slot & 7u)));
     }
     if (lane_in(m_fire & m_need)) {
-      lds_add(my_cnt + (kC > 1 ? 4u * (sl >> 3) : 0u), readers << (4u * (sl & 7u)));
-      st32(my_ends + 4u * sl, en);
-      st16(my_tags + (S > 8 ? 16u * PW * (sl >> 3) : 0u) + 2u * (sl & 7u), lid + 1u);
+      lds_add(my_pool + (kC > 1 ? 4u * (sl >> 3) : 0u), readers << (4u * (sl & 7u)));
+      st32(my_pool + kEndAt + 4u * sl, en);
+      st16(my_tags + (S > 8 ? 16u * PW * (sl >> 3) : 0u) + 2u * (sl & 7u), lid1);
     }
 
     // ---- register state
-    const uint64_t m_fin = m_fire & ballot(ptr + 1u == uint32_t(nr));
+    const uint64_t m_fin = m_fire & ballot(apos1 == a_end);
     const uint64_t m_adv = m_fire & ~m_fin;
     const bool adv = lane_in(m_adv);
     const bool more = lane_in(m_found & ~m_fire & ~m_last);   // found, another edge to go
     if (fire) {
       tfree = en;
       acc = 0;
-      ++ptr;
     } else if (found) {
       acc = acc_n;
     }
@@ -330,29 +335,21 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
       ce = lds32(a.off_extra + 4u * xi);
       ++xi;
     }
-    m_npend = ((m_npend & ~m_fire) | (m_found & m_last & ~m_fire) |
-               (m_adv & ballot((nxt0 & kSimHasPred) == 0))) & ~m_fin;
-    m_live &= ~m_fin;
-    if (adv) {
-      lid = nid;
-      cur0 = nxt0;
-      ce = nce;
-      xi = nxi;
-      // the op after the new current one
-      nid = idn;
-      const uint2 n = rec_of(idn);
-      nxt0 = n.x;
-      nce = n.y;
-      nxi = n.y + 1u;
-      if (n.x & kSimMulti) nce = lds32(a.off_extra + 4u * n.y);
+    if (adv) {   // the next op becomes current
+      set_current(idn, nrec);
+      ++apos1;
     }
+    m_npend = ((m_npend & ~m_fire) | (m_found & m_last & ~m_fire) |
+               (m_adv & ballot((cur0 & kSimHasPred) == 0))) & ~m_fin;
+    m_live &= ~m_fin;
 
-    // ---- order blocks: every 4 rounds, a lane with room loads its next block
+    // ---- order blocks: every 4 rounds, a lane in the later of its two
+    // blocks loads the one after it
     if (phase == 0u) {
-      const uint32_t cur_blk = (uint32_t(rb) + ptr) >> 2;
-      const bool load = lane_in(m_live) && lb <= blk_last && lb < cur_blk + 3u;
+      const uint32_t cur_blk = (apos1 - 1u) / uint32_t(kSimBlockIds);
+      const bool load = lane_in(m_live) && lb <= blk_last && lb <= cur_blk + 1u;
       m_blk = ballot(load);
-      if (load) blk = *reinterpret_cast<const uint2 *>(row + 4 * int64_t(lb));
+      if (load) blk = load_block(row, lb);
     }
 
     // ---- verdicts, every 8 rounds (a group that finished or stalled waits
