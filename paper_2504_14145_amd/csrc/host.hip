@@ -819,7 +819,7 @@ int upload_sim_tables(dip_sim *h, const dip_costs *c, const int32_t *busy, const
     const int32_t r = h->rank_of[g], rp = h->rank_of[p];
     const int32_t d = (p - h->rank_off[rp]) - (g - h->rank_off[r]);
     const uint32_t dr = uint32_t((rp - r + P) % P);
-    return (uint32_t(d) & 0x3fffu) | (dr << 14) | (uint32_t(c->edge_comm[k]) << 20) |
+    return dr | ((uint32_t(d) & 0x3fffu) << 6) | (uint32_t(c->edge_comm[k]) << 20) |
            (last ? kSimLast : 0u);
   };
   for (int32_t g = 0; g < h->N; ++g) {
@@ -867,8 +867,8 @@ int upload_sim_tables(dip_sim *h, const dip_costs *c, const int32_t *busy, const
         } else {
           id = it->second;
         }
-        if (id > 0xffff) ok = false;
-        pmap.push_back(uint16_t(id));
+        if (id >= kSimMaxPages) ok = false;
+        pmap.push_back(uint16_t(id * kSimPage));
       }
     }
     const int64_t pbytes = int64_t(pages.size()) * 4;

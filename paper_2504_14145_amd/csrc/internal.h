@@ -199,8 +199,8 @@ hipError_t launch_pool(int pwl, int slots, bool tab, int blocks, int wpb, size_t
 //   w1 = the edge word of its only predecessor, or, with several, the index
 //        of its first edge word in the extra-edge table (the rest follow, the
 //        last one marked)
-// Edge word: pred local id - own local id (bits 0-13, two's complement) |
-//   (pred rank - own rank) mod P (14-19) | latency (20-30) | last (31).
+// Edge word: (pred rank - own rank) mod P (bits 0-5) | pred local id - own
+//   local id (6-19, two's complement) | latency (20-30) | last (31).
 constexpr uint32_t kSimCostBits = 20;
 constexpr uint32_t kSimCostMax = (1u << kSimCostBits) - 1;
 constexpr uint32_t kSimCommMax = 2047;
@@ -209,8 +209,10 @@ constexpr uint32_t kSimMulti = 1u << 24;
 constexpr uint32_t kSimHasPred = 1u << 25;
 constexpr uint32_t kSimLast = 1u << 31;
 // ops per record page (paged tables: a rank's records come in pages of 16
-// consecutive local ids, equal pages stored once)
+// consecutive local ids, equal pages stored once); the page map holds each
+// page's first record index (page number x 16), so at most kSimMaxPages pages
 constexpr int kSimPage = 16;
+constexpr int kSimMaxPages = 4096;
 
 // Per-candidate LDS state of the simulation kernel, for a group of PW lanes
 // (one per rank; the kernel requires P == PW):

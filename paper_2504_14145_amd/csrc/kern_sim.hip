@@ -92,6 +92,33 @@ __device__ __forceinline__ void store_block(uint32_t at, const uint4 &v) {
   st64(at + 8, v.z, v.w);
 }
 
+typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+
+// Which of a pool's S 16-bit tags (two to a word) equals `want`: with a
+// weight of 16 + s for slot s, the sum over the slots whose tag differs,
+// tag_miss_sum(S) - (16 + s) when slot s matches (tags are unique in a pool)
+// and tag_miss_sum(S) when none does.  Per tag word: a packed XOR (equal
+// halves become 0), a packed minimum with 1 (0 where equal, else 1) and a
+// two-way dot product with the slots' weights.
+template <int S>
+__host__ __device__ constexpr uint32_t tag_miss_sum() {
+  return uint32_t(S * (S - 1) / 2 + 16 * S);
+}
+template <int S>
+__device__ __forceinline__ uint32_t tag_weighted_misses(const uint32_t (&tw)[S / 2], uint32_t want) {
+  const uint32_t both = want * 0x10001u;
+  uint32_t sum = 0;
+#pragma unroll
+  for (int i = 0; i < S / 2; ++i) {
+    uint32_t y;
+    asm("v_pk_min_u16 %0, %1, %2" : "=v"(y) : "v"(tw[i] ^ both), "s"(0x00010001u));
+    const uint32_t w = (16u + 2u * i) | ((17u + 2u * i) << 16);
+    sum = __builtin_amdgcn_udot2(__builtin_bit_cast(u16x2, y), __builtin_bit_cast(u16x2, w), sum,
+                                 false);
+  }
+  return sum;
+}
+
 template <int PWL, int S, bool PAGED>
 __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
   constexpr int PW = 1 << PWL;
@@ -122,9 +149,6 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
   const uint32_t my_pool = gbase + kPools + rr * kPool;
   const uint32_t my_tags = gbase + rr * kTagRank;
   const uint32_t my_ring = gbase + kRing + rr * uint32_t(kSimRingBytes);
-  // the rank in the edge word's rank-difference field: adding it there and
-  // keeping the field's low PWL bits gives the predecessor's rank
-  const uint32_t rank_sh = rr << 14;
   int rb = 0, nr = 0, busy_r = 0, recb = 0;
   if (on) {
     const int4 li = reinterpret_cast<const int4 *>(a.lane_info)[r];
@@ -140,14 +164,13 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
 
   // the record of local id `id` of this lane's rank
   auto rec_of = [&](uint32_t id) -> uint2 {
-    uint32_t addr;
+    uint32_t first;   // record index of the page's first op, or of the rank's
     if constexpr (PAGED) {
-      const uint32_t pg = lds16(pmap_lane + 2u * (id >> 4));
-      addr = (pg << 7) | ((id & 15u) << 3);
+      first = lds16(pmap_lane + (__builtin_amdgcn_ubfe(id, 4u, 12u) << 1)) + (id & 15u);
     } else {
-      addr = (uint32_t(recb) + id) << 3;
+      first = uint32_t(recb) + id;
     }
-    return lds64(addr);
+    return lds64(first << 3);
   };
   auto ring_at = [&](uint32_t pos) { return my_ring + ((pos & 15u) << 1); };
 
@@ -244,10 +267,12 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     }
 
     // ---- reads: the predecessor's pool, my counts, the next id
-    const uint32_t pr = ((ce + rank_sh) >> 14) & uint32_t(PW - 1);
+    // (the predecessor's rank: the rank difference sits in the edge word's
+    // low bits, and P == PW)
+    const uint32_t pr = (ce + rr) & uint32_t(PW - 1);
     const uint32_t pool = gbase + kPools + pr * kPool;
     const uint32_t p_tags = gbase + pr * kTagRank;
-    const uint32_t want = lid1 + uint32_t(int32_t(ce << 18) >> 18);
+    const uint32_t want = lid1 + uint32_t(int32_t(ce << 12) >> 18);
     uint32_t tw[S / 2];
     if constexpr (S == 4) {
       const uint2 v = lds64(p_tags);
@@ -270,31 +295,24 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     // the next op's record, read ahead (used by the lanes that advance)
     const uint2 nrec = rec_of(idn);
 
-    // the matching slot (tags are unique within a pool): 4 x its index, or
-    // kNoHit; one compare and one select per slot, all vector instructions
-    constexpr uint32_t kNoHit = 0x80u;
-    uint32_t hit4 = kNoHit;
-#pragma unroll
-    for (int i = 0; i < S; ++i) {
-      const uint32_t pair = tw[i / 2];
-      const uint32_t t = (i & 1) ? (pair >> 16) : (pair & 0xffffu);
-      hit4 = t == want ? 4u * uint32_t(i) : hit4;
-    }
-    const uint64_t m_found = ballot(hit4 != kNoHit) & m_live & ~m_npend;
-    hit4 &= 0x7cu;
-    const uint32_t hit_end = lds32(pool + kEndAt + hit4);
+    // the matching slot (tags are unique within a pool)
+    const uint32_t wsum = tag_weighted_misses<S>(tw, want);
+    const uint64_t m_found = ballot(wsum != tag_miss_sum<S>()) & m_live & ~m_npend;
+    const uint32_t slot = (tag_miss_sum<S>() - 16u - wsum) & uint32_t(S - 1);
+    const uint32_t hit_end = lds32(pool + kEndAt + 4u * slot);
     const bool found = lane_in(m_found);
     const uint32_t acc_n = found ? max(acc, hit_end + ((ce >> 20) & 0x7ffu)) : acc;
     // a free slot of my pool (reader count zero): the first one
     bool has_free = false;
     uint32_t sl = 0;
+    uint32_t zfree = 0;   // (one count word) bit 4 s + 3 set for each free slot s
 #pragma unroll
     for (int i = kC - 1; i >= 0; --i) {
       const uint32_t w = i * 8 + 8 <= S ? cnt[i] : (cnt[i] | (0xffffffffu << (4 * (S - i * 8))));
       const uint32_t z = ~(((w & 0x77777777u) + 0x77777777u) | w | 0x77777777u);   // 8 in zero nibbles
       if constexpr (kC == 1) {
         has_free = z != 0u;
-        sl = uint32_t(__builtin_ctz(z | 0x80000000u)) >> 2;
+        zfree = z;
       } else {
         sl = z ? 8u * uint32_t(i) + (uint32_t(__builtin_ctz(z)) >> 2) : sl;
         has_free = has_free || z != 0u;
@@ -311,13 +329,19 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
 
     // ---- writes: release what was read, publish what was produced
     if (found) {
-      const uint32_t slot = hit4 >> 2;
       lds_sub(pool + (kC > 1 ? 4u * (slot >> 3) : 0u), 1u << (4u * (slot & 7u)));
     }
     if (lane_in(m_fire & m_need)) {
-      lds_add(my_pool + (kC > 1 ? 4u * (sl >> 3) : 0u), readers << (4u * (sl & 7u)));
-      st32(my_pool + kEndAt + 4u * sl, en);
-      st16(my_tags + (S > 8 ? 16u * PW * (sl >> 3) : 0u) + 2u * (sl & 7u), lid1);
+      if constexpr (kC == 1) {   // 4 x the first free slot (zfree is not 0 here)
+        const uint32_t sl4 = uint32_t(__builtin_ctz(zfree)) - 3u;
+        lds_add(my_pool, readers << sl4);
+        st32(my_pool + kEndAt + sl4, en);
+        st16(my_tags + (sl4 >> 1), lid1);
+      } else {
+        lds_add(my_pool + 4u * (sl >> 3), readers << (4u * (sl & 7u)));
+        st32(my_pool + kEndAt + 4u * sl, en);
+        st16(my_tags + 16u * PW * (sl >> 3) + 2u * (sl & 7u), lid1);
+      }
     }
 
     // ---- register state
