@@ -207,7 +207,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=5, help="workload id 1-5")
+    ap.add_argument("--config", type=int, default=0,
+                    help="workload id 1-5 (default: 5 for the simulation, 2 for the other paths)")
     ap.add_argument("--n-cand", type=int, default=0, help="override candidates per batch")
     ap.add_argument("--variant", type=int, default=0)
     ap.add_argument("--wpb", type=int, default=0)
@@ -256,6 +257,8 @@ def main():
     import paper_2504_14145_amd as dip
     import workloads as W
 
+    if not args.config:
+        args.config = 5 if args.path == "simulate" else 2
     cfg = W.get(args.config)
     if args.path == "greedy":
         return run_greedy(args, cfg)
@@ -632,7 +635,8 @@ def run_memopt(args, cfg):
     k_s = sum(a.elapsed_time(b) for a, b in ev) / len(ev) / 1e3
     st = s_out.cpu().numpy()
     log(f"[bench] {args.steps} steps in {wall * 1e3:.2f} ms; kernel {k_s * 1e3:.3f} ms; "
-        f"within cap {np.mean(st == 1):.3f}, out of reach {np.mean(st == 0):.3f}")
+        f"within cap {np.mean((st == 1) | (st == 3)):.3f} (proven within 5 %: "
+        f"{np.mean(st == 1):.3f}), out of reach {np.mean(st == 0):.3f}")
     calib_copies(args, dev)
 
     cpu = None
@@ -670,7 +674,8 @@ def run_memopt(args, cfg):
                    "stage_pairs": prob.n_slots, "candidates_per_pair": S,
                    "cap_units": int(prob.mem_cap[0]), "parallelism": "single GPU"},
         "kernel_us": {"memopt": k_s * 1e6},
-        "within_cap": float(np.mean(st == 1)),
+        "within_cap": float(np.mean((st == 1) | (st == 3))),
+        "proven_within_5pct": float(np.mean(st == 1)),
         "roofline": {"bound": "hbm", "kernel": "memopt",
                      "achieved": n_cand * bytes_per / k_s / 1e9, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": n_cand * bytes_per / k_s / 1e9 / HBM_PEAK_GBS,

@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define DIP_SIM_ABI_VERSION 6
+#define DIP_SIM_ABI_VERSION 7
 
 enum {
   DIP_OK = 0,
@@ -335,30 +335,63 @@ int dip_sim_rollouts_batch(dip_sim *h, int32_t n_leaves, const int32_t *depths,
  * equal buckets of the memory range between them the least time whose memory
  * is at most the bucket's upper edge lo + floor((hi - lo) k / (n - 2))
  * (Sec. 5.3's multiple-choice knapsack); equal points once, by time.
+ * bb_nodes bounds the branch and bound of dip_sim_memopt: the placements it
+ * may examine per (schedule, rank), 0 for 512.
  * DIP_E_TOPO unless every slot has one forward and one backward on one rank;
- * DIP_E_RANGE for a negative entry or a candidate memory above 2^31 - 1;
- * DIP_E_UNSUPPORTED for a rank of 16384 pairs or more. */
+ * DIP_E_RANGE for a negative entry, a candidate memory above 2^31 - 1, a
+ * candidate time above 2^40, or fastest memories of a rank summing above
+ * 2^31 - 1;
+ * DIP_E_INVAL for bb_nodes < 0; DIP_E_UNSUPPORTED for a rank of 16384 pairs
+ * or more. */
 int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64_t *layer_time,
                              const int64_t *layer_mem, int32_t n_strategies,
-                             int32_t n_candidates);
+                             int32_t n_candidates, int32_t bb_nodes);
 
 /* For every candidate schedule (orders as dip_sim_evaluate reads them) and
  * rank, choose one candidate per stage pair of the rank so that the memory at
  * every forward start -- the pairs whose forward comes no later and whose
  * backward no earlier in the rank's order -- stays within mem_cap[r] (none if
- * negative), by the greedy warm start of Sec. 5.3's ILP: every pair on its
- * fastest candidate; while the most loaded forward start (the earliest pair
- * among equal loads) is over the cap, move the live pair whose next
- * candidate adds the least time per memory unit freed (lowest pair on ties);
- * stop when none can move.  Outputs, device [n_cand][P]: out_time (int64,
- * the rank's total pair time), out_peak (memory at the most loaded forward
- * start), out_status (1 within the cap, 0 the cap cannot be met, 2 the rank's
- * section is not a permutation: time and peak -1).  Pairs are numbered per
- * rank in slot order.  Enqueued on stream; DIP_E_STATE before
- * dip_sim_configure_memopt, DIP_E_INVAL for null or misaligned outputs,
- * DIP_E_UNSUPPORTED when a rank's state does not fit in LDS. */
+ * negative), with the least total time (Sec. 5.3's ILP, solved to within the
+ * 5 % gap the paper accepts):
+ *   1. the greedy warm start: every pair on its fastest candidate; while the
+ *      most loaded forward start (the earliest pair among equal loads) is over
+ *      the cap, move the live pair whose next candidate adds the least time
+ *      per memory unit freed (lowest pair on ties); stop when none can move;
+ *   2. pairs in index order each go back to the fastest candidate that keeps
+ *      every forward start it is live at within the cap, until nothing moves;
+ *   3. a depth-first branch and bound, pairs by forward position, candidates
+ *      fastest first, a node cut when 1.05 x (its placed time + the unplaced
+ *      pairs' fastest times) reaches the incumbent; it ends proven (the
+ *      incumbent is within 5 % of the optimum) or after bb_nodes placements
+ *      examined; ranks of more than 512 pairs skip it.
+ * Outputs, device [n_cand][P]: out_time (int64, the rank's total pair time),
+ * out_peak (memory at the most loaded forward start), out_status (1 within
+ * the cap and proven within 5 %, 3 within the cap but not proven, 0 the cap
+ * cannot be met, 2 the rank's section is not a permutation: time and peak -1);
+ * out_choice (device [n_cand][n_pairs] uint8, or null): the chosen candidate
+ * of every pair, pairs numbered rank by rank and within a rank in slot order
+ * (candidates by time ascending; undefined for status 2).  Enqueued on
+ * stream; DIP_E_STATE before dip_sim_configure_memopt, DIP_E_INVAL for null
+ * or misaligned outputs, DIP_E_UNSUPPORTED when a rank's state does not fit
+ * in LDS. */
 int dip_sim_memopt(dip_sim *h, const int16_t *orders, int64_t n_cand, int64_t *out_time,
-                   int32_t *out_peak, uint8_t *out_status, void *stream);
+                   int32_t *out_peak, uint8_t *out_status, uint8_t *out_choice, void *stream);
+
+/* dip_sim_evaluate of schedules re-timed with a memory selection (Sec. 5.3,
+ * then Sec. 5.1's iteration time): pair p of schedule i runs candidate
+ * choice[i][p] (dip_sim_memopt's out_choice layout) -- its backward costs
+ * its op_cost plus the candidate's time less the pair's fastest time (the
+ * recomputation runs inside the backward), and its activation is the
+ * candidate's memory -- with the costs and latencies of the last
+ * dip_sim_evaluate call.  Outputs and flags as dip_sim_evaluate's (the peak
+ * and the cap flag from the chosen memories); a choice beyond a pair's
+ * candidates makes its schedule invalid (DIP_FLAG_INVALID, outputs -1).
+ * DIP_E_STATE before dip_sim_configure_memopt or before any costs,
+ * DIP_E_RANGE when a re-timed backward could exceed 2^31 - 1 microseconds,
+ * DIP_E_INVAL for null or misaligned pointers. */
+int dip_sim_evaluate_selected(dip_sim *h, const int16_t *orders, const uint8_t *choice,
+                              int64_t n_cand, int32_t *out_makespan, int32_t *out_bubble,
+                              int32_t *out_peakmem, uint8_t *out_flags, void *stream);
 
 /* Operator-level cost tables (Sec. 6.1), independent of any handle.  An item
  * (a pipeline stage, a data edge, ...) is a run of operator rows; each row

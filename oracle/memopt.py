@@ -16,25 +16,47 @@ Offline candidates (Sec. 5.3, "Offline Candidate Generation"), per stage pair:
   most the edge; equal points once; listed by time ascending (memory then
   strictly descends).
 
-Per-rank selection (Sec. 5.3, "ILP Formulation"): each stage pair i on a rank
-takes one candidate; total latency is minimised subject to the memory at
-every forward start staying within the rank's cap.  A pair is live at pair
-k's forward start when its forward comes no later and its backward no
-earlier in the rank's order (on one rank the order gives the timestamps'
-order, [s_i <= s_k <= t_i]).  The paper warm-starts an ILP solver with a
-greedy solution and accepts a small gap; this build computes the greedy
-solution:
-  every pair on its fastest candidate; then while the most loaded checkpoint
-  (lowest index among equal loads) exceeds the cap, among its live pairs that
-  can move to their next (leaner, slower) candidate take the one with the
-  least added time per freed memory unit (compared as dt_a * dm_b < dt_b *
-  dm_a; lowest pair index on ties) and move it; stop when no live pair can
-  move (infeasible).
-``exact`` solves the same problem by enumeration, for small cases.
+Per-rank selection (Sec. 5.3, "ILP Formulation" and "Optimizations"): each
+stage pair i on a rank takes one candidate; total latency is minimised
+subject to the memory at every forward start staying within the rank's cap.
+A pair is live at pair k's forward start when its forward comes no later and
+its backward no earlier in the rank's order (on one rank the order gives the
+timestamps' order, [s_i <= s_k <= t_i]).  The paper warm-starts an ILP
+solver with a greedy solution and stops it once the solution is within 5 %
+of optimal.  This build's solver, ``select``:
+  1. the greedy warm start: every pair on its fastest candidate; then while
+     the most loaded checkpoint (lowest index among equal loads) exceeds the
+     cap, among its live pairs that can move to their next (leaner, slower)
+     candidate take the one with the least added time per freed memory unit
+     (compared as dt_a * dm_b < dt_b * dm_a; lowest pair index on ties) and
+     move it; no live pair can move: the cap cannot be met (every live pair
+     of that checkpoint is on its leanest candidate);
+  2. an improvement pass: pairs in index order each go back to the fastest
+     candidate that keeps every checkpoint it is live at within the cap;
+     passes repeat until one changes nothing;
+  3. a depth-first branch and bound from that incumbent, pairs in the order
+     of their forward starts (a pair's checkpoint then involves only pairs
+     already placed), candidates fastest first; a placement is dropped when
+     its checkpoint exceeds the cap, and a node is cut (with the slower
+     candidates after it) when its placed time plus every unplaced pair's
+     fastest time, times 1.05, reaches the incumbent.  A leaf below the
+     incumbent replaces it.  When the search ends every cut subtree was
+     worth at least incumbent / 1.05, so the incumbent is within 5 % of the
+     optimum (status 1).  The search stops early after BB_NODES placements
+     examined, or is skipped for ranks of more than BB_MAX_PAIRS pairs; the
+     incumbent is then returned unproven (status 3).
+``exact`` solves the same problem by enumeration and ``exact_bb`` by the same
+search without the 5 % allowance or a node limit, for small cases.
 """
 from __future__ import annotations
 
 import itertools
+
+import numpy as np
+
+BB_NODES = 512          # placements the branch and bound may examine per rank
+BB_MAX_PAIRS = 512      # larger ranks keep the improved warm start
+GAP_NUM, GAP_DEN = 105, 100   # a cut needs (placed + fastest rest) * 1.05 >= incumbent
 
 
 def pareto(layers):
@@ -113,6 +135,108 @@ def greedy_select(cands, live, cap):
     return cur, total, feasible, max(load) if n else 0
 
 
+def tighten(cands, live, cap, cur):
+    """Step 2: each pair in index order moves back to the fastest candidate
+    that keeps every checkpoint it is live at within the cap; repeated until a
+    pass changes nothing."""
+    n = len(cands)
+    cur = list(cur)
+    at = [[k for k in range(n) if i in live[k]] for i in range(n)]
+    load = [sum(cands[i][cur[i]][1] for i in live[k]) for k in range(n)]
+    changed = True
+    while changed:
+        changed = False
+        for i in range(n):
+            # (a pair whose backward comes before its forward is live nowhere)
+            top = max((load[k] for k in at[i]), default=None)
+            for j in range(cur[i]):
+                add = cands[i][j][1] - cands[i][cur[i]][1]
+                if top is None or top + add <= cap:
+                    for k in at[i]:
+                        load[k] += add
+                    cur[i] = j
+                    changed = True
+                    break
+    return cur
+
+
+def branch_and_bound(cands, pf, pb, cap, cur, nodes=BB_NODES, gap=(GAP_NUM, GAP_DEN)):
+    """Step 3 from incumbent ``cur`` (a feasible choice): returns (choice,
+    proven, placements examined).  ``nodes`` None: no limit."""
+    n = len(cands)
+    num, den = gap
+    inc = sum(cands[i][cur[i]][0] for i in range(n))
+    best = list(cur)
+    order = sorted(range(n), key=lambda i: pf[i])
+    rest = [0] * (n + 1)             # fastest time of the pairs at depth >= d
+    for d in range(n - 1, -1, -1):
+        rest[d] = rest[d + 1] + cands[order[d]][0][0]
+    ch = [-1] * n
+    placed = [0] * (n + 1)           # time of the pairs above depth d
+    seen = 0
+    d = 0
+    while d >= 0:
+        i = order[d]
+        ch[d] += 1
+        if ch[d] >= len(cands[i]):
+            ch[d] = -1
+            d -= 1
+            continue
+        seen += 1
+        if nodes is not None and seen > nodes:
+            return best, False, seen - 1
+        t, m = cands[i][ch[d]]
+        load = (m if pb[i] >= pf[i] else 0) + sum(cands[order[e]][ch[e]][1] for e in range(d)
+                                                  if pb[order[e]] >= pf[i])
+        if cap >= 0 and load > cap:
+            continue                  # a leaner candidate may fit
+        f = placed[d] + t
+        if num * (f + rest[d + 1]) >= den * inc:
+            ch[d] = len(cands[i])     # this and the slower candidates are cut
+            continue
+        if d == n - 1:
+            inc = f
+            for e in range(n):
+                best[order[e]] = ch[e]
+            continue
+        placed[d + 1] = f
+        d += 1
+    return best, True, seen
+
+
+def select(cands, live, pf, pb, cap, nodes=BB_NODES):
+    """The solver of a rank: (choice, total time, status, peak); status 1
+    within the cap and proven within 5 % of optimal, 3 within the cap but
+    not proven, 0 the cap cannot be met (choice where the warm start gave
+    up)."""
+    n = len(cands)
+    cur, total, ok, peak = greedy_select(cands, live, cap)
+    if not ok:
+        return cur, total, 0, peak
+    proven = True
+    if cap >= 0 and n:
+        cur = tighten(cands, live, cap, cur)
+        if n <= BB_MAX_PAIRS:
+            cur, proven, _ = branch_and_bound(cands, pf, pb, cap, cur, nodes)
+        else:
+            proven = False
+    total = sum(cands[i][cur[i]][0] for i in range(n))
+    peak = max((sum(cands[i][cur[i]][1] for i in live[k]) for k in range(n)), default=0)
+    return cur, total, 1 if proven else 3, peak
+
+
+def exact_bb(cands, live, pf, pb, cap):
+    """The optimum by the same search with no allowance and no limit, from the
+    improved warm start; None when the cap cannot be met."""
+    cur, _, ok, _ = greedy_select(cands, live, cap)
+    if not ok:
+        return None
+    if cap >= 0 and cands:
+        cur = tighten(cands, live, cap, cur)
+        cur, _, _ = branch_and_bound(cands, pf, pb, cap, cur, None, (1, 1))
+    return sum(cands[i][cur[i]][0] for i in range(len(cands)))
+
+
 def exact(cands, live, cap):
     """Least total time over every choice meeting the cap; None if none does."""
     best = None
@@ -140,8 +264,22 @@ def rank_problem(prob, table, cands, order, r):
     return slots, [cands[s] for s in slots], live_sets(pf, pb)
 
 
-def optimise(prob, table, cands, orders, caps=None):
-    """Per candidate schedule and rank: (total time, feasible, peak)."""
+def rank_positions(prob, table, order, r):
+    """Positions of rank r's pairs' forwards and backwards in its order (pairs
+    in slot order, as rank_problem lists them)."""
+    base = int(prob.rank_off[r])
+    nr = int(prob.rank_off[r + 1]) - base
+    pos = [0] * nr
+    for p in range(nr):
+        pos[int(order[base + p])] = p
+    slots = [s for s in range(len(table.slot_rank)) if table.slot_rank[s] == r]
+    return ([pos[int(table.slot_f[s]) - base] for s in slots],
+            [pos[int(table.slot_b[s]) - base] for s in slots])
+
+
+def optimise(prob, table, cands, orders, caps=None, nodes=BB_NODES):
+    """Per candidate schedule and rank: (total time, status, peak, choice by
+    pair in slot order) of ``select``."""
     P = prob.n_ranks
     caps = prob.mem_cap if caps is None else caps
     out = []
@@ -149,7 +287,46 @@ def optimise(prob, table, cands, orders, caps=None):
         per = []
         for r in range(P):
             _, c, live = rank_problem(prob, table, cands, row, r)
-            _, total, ok, peak = greedy_select(c, live, int(caps[r]))
-            per.append((total, ok, peak))
+            pf, pb = rank_positions(prob, table, row, r)
+            cur, total, status, peak = select(c, live, pf, pb, int(caps[r]), nodes)
+            per.append((total, status, peak, cur))
         out.append(per)
     return out
+
+
+def retimed_costs(prob, table, cands, per):
+    """Op costs of one schedule after the selection (``per``: optimise's
+    entries of its ranks): a pair's chosen time is its forward's cost plus its
+    backward's, the recomputation landing in the backward; forwards keep
+    their cost."""
+    cost = prob.op_cost.astype(np.int64).copy()
+    for r, (_, status, _, cur) in enumerate(per):
+        slots = [s for s in range(len(table.slot_rank)) if table.slot_rank[s] == r]
+        for i, s in enumerate(slots):
+            f, b = int(table.slot_f[s]), int(table.slot_b[s])
+            cost[b] = cands[s][cur[i]][0] - cost[f]
+    return cost
+
+
+def selected_problem(prob, table, cands, per):
+    """The problem as one schedule runs it after the selection: re-timed op
+    costs and each pair's activation the chosen candidate's memory."""
+    import dataclasses
+    act = prob.slot_act.astype(np.int64).copy()
+    for r, (_, _, _, cur) in enumerate(per):
+        slots = [s for s in range(len(table.slot_rank)) if table.slot_rank[s] == r]
+        for i, s in enumerate(slots):
+            act[s] = cands[s][cur[i]][1]
+    cost = retimed_costs(prob, table, cands, per)
+    return dataclasses.replace(prob, op_cost=cost.astype(prob.op_cost.dtype),
+                               slot_act=act.astype(prob.slot_act.dtype))
+
+
+def choice_row(table, per):
+    """A schedule's choices in the library's pair numbering (rank by rank,
+    slot order within a rank)."""
+    out = []
+    for r, (_, _, _, cur) in enumerate(per):
+        out.extend(cur)
+    return out
+

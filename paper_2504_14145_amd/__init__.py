@@ -32,7 +32,8 @@ EXPORTS = ("dip_sim_abi_version", "dip_sim_check_topology", "dip_sim_check_costs
            "dip_sim_last_retries", "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_set_greedy_inbox", "dip_sim_greedy",
            "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_sim_rollouts_batch",
            "dip_cost_tables",
-           "dip_sim_configure_memopt", "dip_sim_memopt", "dip_sim_destroy", "dip_sim_strerror")
+           "dip_sim_configure_memopt", "dip_sim_memopt", "dip_sim_evaluate_selected",
+           "dip_sim_destroy", "dip_sim_strerror")
 
 
 class DipSimError(RuntimeError):
@@ -105,8 +106,9 @@ def load():
         lib.dip_sim_greedy.argtypes = [vp, ctypes.POINTER(Costs), vp, i64, vp, vp, vp, vp, vp, vp]
         lib.dip_sim_configure_rollouts.argtypes = [vp, i32, vp]
         lib.dip_cost_tables.argtypes = [ctypes.POINTER(OpTable), i64, vp, vp, vp]
-        lib.dip_sim_configure_memopt.argtypes = [vp, vp, vp, vp, i32, i32]
-        lib.dip_sim_memopt.argtypes = [vp, vp, i64, vp, vp, vp, vp]
+        lib.dip_sim_configure_memopt.argtypes = [vp, vp, vp, vp, i32, i32, i32]
+        lib.dip_sim_memopt.argtypes = [vp, vp, i64, vp, vp, vp, vp, vp]
+        lib.dip_sim_evaluate_selected.argtypes = [vp, vp, vp, i64, vp, vp, vp, vp, vp]
         lib.dip_sim_rollouts.argtypes = [vp, vp, i32, i64, ctypes.c_uint64, ctypes.c_uint64,
                                          vp, vp, vp, vp, vp]
         lib.dip_sim_rollouts_batch.argtypes = [vp, i32, vp, vp, i64, ctypes.c_uint64,
@@ -124,7 +126,7 @@ def load():
                      "dip_sim_argmin", "dip_sim_configure_greedy", "dip_sim_set_greedy_inbox", "dip_sim_greedy",
                      "dip_sim_configure_rollouts", "dip_sim_rollouts", "dip_sim_rollouts_batch",
            "dip_cost_tables",
-                     "dip_sim_configure_memopt", "dip_sim_memopt"):
+                     "dip_sim_configure_memopt", "dip_sim_memopt", "dip_sim_evaluate_selected"):
             getattr(lib, name).restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -346,21 +348,34 @@ def cost_tables(table: DeviceOpTable, coef, out, stream=None) -> None:
     _check(rc, "dip_cost_tables")
 
 
-def configure_memopt(h, slot_layers, layer_time, layer_mem, n_candidates: int) -> int:
+def configure_memopt(h, slot_layers, layer_time, layer_mem, n_candidates: int,
+                     bb_nodes: int = 0) -> int:
     """Host arrays: slot_layers int32 [n_slots+1], layer_time / layer_mem int64
-    [layers][n_strategies]."""
+    [layers][n_strategies]; bb_nodes 0: the library's default."""
     sl = np.ascontiguousarray(slot_layers, np.int32)
     lt = np.ascontiguousarray(layer_time, np.int64)
     lm = np.ascontiguousarray(layer_mem, np.int64)
     ns = lt.shape[1] if lt.ndim == 2 else 1
     return load().dip_sim_configure_memopt(h, sl.ctypes.data, lt.ctypes.data, lm.ctypes.data,
-                                           int(ns), int(n_candidates))
+                                           int(ns), int(n_candidates), int(bb_nodes))
 
 
-def memopt(h, orders, n_cand, out_time, out_peak, out_status, stream=None) -> None:
+def memopt(h, orders, n_cand, out_time, out_peak, out_status, out_choice=None,
+           stream=None) -> None:
     rc = load().dip_sim_memopt(h, orders.data_ptr(), int(n_cand), out_time.data_ptr(),
-                               out_peak.data_ptr(), out_status.data_ptr(), _stream_ptr(stream))
+                               out_peak.data_ptr(), out_status.data_ptr(),
+                               out_choice.data_ptr() if out_choice is not None else None,
+                               _stream_ptr(stream))
     _check(rc, "dip_sim_memopt")
+
+
+def evaluate_selected(h, orders, choice, n_cand, out_makespan, out_bubble, out_peakmem,
+                      out_flags, stream=None) -> None:
+    rc = load().dip_sim_evaluate_selected(h, orders.data_ptr(), choice.data_ptr(), int(n_cand),
+                                          out_makespan.data_ptr(), out_bubble.data_ptr(),
+                                          out_peakmem.data_ptr(), out_flags.data_ptr(),
+                                          _stream_ptr(stream))
+    _check(rc, "dip_sim_evaluate_selected")
 
 
 def destroy(h) -> None:

@@ -240,7 +240,10 @@ struct dip_sim {
   int64_t rl_cap = 0;
   // per-layer memory optimisation (dip_sim_configure_memopt / dip_sim_memopt)
   bool mo_ok = false;
-  int32_t mo_max_pairs = 0;
+  int32_t mo_max_pairs = 0, mo_n_pairs = 0, mo_bb_nodes = 512;
+  int64_t mo_max_extra = 0;            // largest slowest-less-fastest time of a pair
+  std::vector<int32_t> mo_pair_b;      // the backward op of every pair (pair order)
+  std::vector<int64_t> mo_pair_extra;  // its slowest time less its fastest
   int32_t *d_mo_pair_off = nullptr, *d_mo_lid_pair = nullptr;
   int64_t *d_mo_time = nullptr;
   int32_t *d_mo_mem = nullptr, *d_mo_dm = nullptr;
@@ -2004,9 +2007,10 @@ int dip_sim_rollouts(dip_sim *h, const int32_t *prefix, int32_t depth, int64_t n
 }
 
 int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64_t *layer_time,
-                             const int64_t *layer_mem, int32_t n_strategies, int32_t n_candidates) {
+                             const int64_t *layer_mem, int32_t n_strategies, int32_t n_candidates,
+                             int32_t bb_nodes) {
   if (!h || !slot_layers || n_strategies < 1 || n_candidates < 2 ||
-      n_candidates > kMemoptMaxCands)
+      n_candidates > kMemoptMaxCands || bb_nodes < 0)
     return DIP_E_INVAL;
   const int32_t P = h->P, N = h->N, ns = h->n_slots;
   // every slot: one forward and one backward on one rank
@@ -2060,11 +2064,12 @@ int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64
     for (const Pt &p : pick)
       if (uniq.empty() || uniq.back().t != p.t || uniq.back().m != p.m) uniq.push_back(p);
     for (const Pt &p : uniq)
-      if (p.m > INT32_MAX) return DIP_E_RANGE;
+      if (p.m > INT32_MAX || p.t > (int64_t(1) << 40)) return DIP_E_RANGE;
     cand[q] = uniq;
   }
   // pairs per rank in slot order; each op's pair index and kind
-  std::vector<int32_t> pair_off(P + 1, 0), lid_pair(N, 0), slot_pair(ns, 0);
+  std::vector<int32_t> pair_off(P + 1, 0), lid_pair(N, 0), slot_pair(ns, 0), pair_b;
+  std::vector<int64_t> pair_extra;
   std::vector<int32_t> mem, mdm;
   std::vector<int64_t> tim;
   std::vector<uint32_t> mkey;
@@ -2078,10 +2083,14 @@ int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64
     int32_t i = 0;
     const size_t first = tim.size();
     moves.clear();
+    int64_t fastest_mem = 0;
     for (int32_t q = 0; q < ns; ++q) {
       if (h->rank_of[f_of[q]] != r) continue;
       slot_pair[q] = i;
       const int32_t nc = int32_t(cand[q].size());
+      fastest_mem += cand[q][0].m;
+      pair_b.push_back(b_of[q]);
+      pair_extra.push_back(cand[q][nc - 1].t - cand[q][0].t);
       for (int32_t j = 0; j < kMemoptMaxCands; ++j) {
         const bool in = j < nc;
         tim.push_back(in ? cand[q][j].t : 0);
@@ -2095,6 +2104,7 @@ int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64
       ++i;
     }
     if (i >= (1 << kMemoptPairBits)) return DIP_E_UNSUPPORTED;
+    if (fastest_mem > INT32_MAX) return DIP_E_RANGE;
     // exact ratio order of the rank's moves: dt_a / dm_a < dt_b / dm_b (dm > 0)
     auto less = [](const Move &x, const Move &y) {
       return __int128(x.dt) * y.dm < __int128(y.dt) * x.dm;
@@ -2136,12 +2146,18 @@ int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64
         (e = hipMemcpy(h->d_mo_dm, mdm.data(), mdm.size() * 4, hipMemcpyHostToDevice)))))
     return fail(e);
   h->mo_max_pairs = max_pairs;
+  h->mo_n_pairs = pair_off[P];
+  h->mo_bb_nodes = bb_nodes > 0 ? bb_nodes : 512;
+  h->mo_pair_b = pair_b;
+  h->mo_pair_extra = pair_extra;
+  h->mo_max_extra = 0;
+  for (int64_t x : pair_extra) h->mo_max_extra = std::max(h->mo_max_extra, x);
   h->mo_ok = true;
   return DIP_OK;
 }
 
 int dip_sim_memopt(dip_sim *h, const int16_t *orders, int64_t n_cand, int64_t *out_time,
-                   int32_t *out_peak, uint8_t *out_status, void *stream) {
+                   int32_t *out_peak, uint8_t *out_status, uint8_t *out_choice, void *stream) {
   if (!h || n_cand < 0) return DIP_E_INVAL;
   if (!h->mo_ok) return DIP_E_STATE;
   if (n_cand == 0) return DIP_OK;
@@ -2156,6 +2172,9 @@ int dip_sim_memopt(dip_sim *h, const int16_t *orders, int64_t n_cand, int64_t *o
   a.out_time = out_time;
   a.out_peak = out_peak;
   a.out_status = out_status;
+  a.out_choice = out_choice;
+  a.n_pairs = h->mo_n_pairs;
+  a.bb_nodes = h->mo_bb_nodes;
   a.rank_off = h->d_rank_off;
   a.pair_off = h->d_mo_pair_off;
   a.lid_pair = h->d_mo_lid_pair;
@@ -2183,6 +2202,62 @@ int dip_sim_memopt(dip_sim *h, const int16_t *orders, int64_t n_cand, int64_t *o
   if (int64_t(tpb) * a.bytes_per_thread > 65536) return DIP_E_UNSUPPORTED;
   if (n_cand * h->P / tpb + 1 > INT32_MAX) return DIP_E_INVAL;
   DIP_HIP(launch_memopt(tpb, static_cast<hipStream_t>(stream), a));
+  return DIP_OK;
+}
+
+int dip_sim_evaluate_selected(dip_sim *h, const int16_t *orders, const uint8_t *choice,
+                              int64_t n_cand, int32_t *out_makespan, int32_t *out_bubble,
+                              int32_t *out_peakmem, uint8_t *out_flags, void *stream) {
+  if (!h || n_cand < 0) return DIP_E_INVAL;
+  if (!h->mo_ok || !h->costs_set) return DIP_E_STATE;
+  if (n_cand == 0) return DIP_OK;
+  if (!orders || !choice || !out_makespan || !out_bubble || !out_peakmem || !out_flags)
+    return DIP_E_INVAL;
+  if ((reinterpret_cast<uintptr_t>(orders) & 15) ||
+      ((reinterpret_cast<uintptr_t>(out_makespan) | reinterpret_cast<uintptr_t>(out_bubble) |
+        reinterpret_cast<uintptr_t>(out_peakmem)) & 3))
+    return DIP_E_INVAL;
+  // a re-timed backward stays within int32
+  for (size_t p = 0; p < h->mo_pair_b.size(); ++p)
+    if (int64_t(h->last_cost[size_t(h->mo_pair_b[p])]) + h->mo_pair_extra[p] > INT32_MAX)
+      return DIP_E_RANGE;
+  GeneralArgs a{};
+  a.orders = orders;
+  a.n_cand = n_cand;
+  a.stride = h->stride;
+  a.n_groups = (n_cand + h->G - 1) / h->G;
+  a.out_ms = out_makespan;
+  a.out_bub = out_bubble;
+  a.out_peak = out_peakmem;
+  a.out_flags = out_flags;
+  a.rec = h->d_rec;
+  a.edge = h->d_edge;
+  a.rank_off = h->d_rank_off;
+  a.busy = h->d_busy;
+  a.cap = h->d_cap;
+  a.gends = static_cast<int32_t *>(h->d_scratch_gen);
+  a.P = h->P;
+  a.pwl = h->pwl;
+  a.G = h->G;
+  a.N = h->N;
+  a.E = h->E;
+  a.wpb = h->gen_wpb;
+  a.choice = choice;
+  a.n_pairs = h->mo_n_pairs;
+  a.lid_pair = h->d_mo_lid_pair;
+  a.pair_off = h->d_mo_pair_off;
+  a.cand_time = h->d_mo_time;
+  a.cand_mem = h->d_mo_mem;
+  a.cand_key = h->d_mo_key;
+  const GenBytes b = general_bytes(h, h->gen_variant);
+  a.tab_bytes = uint32_t(b.tab);
+  a.ord_bytes = uint32_t(b.ord);
+  a.end_bytes = uint32_t(b.end);
+  const int64_t want = (a.n_groups + h->gen_wpb - 1) / h->gen_wpb;
+  const int blocks = int(std::min<int64_t>(want, h->gen_max_blocks));
+  (void)hipGetLastError();
+  DIP_HIP(launch_general(h->gen_variant, blocks, h->gen_wpb, size_t(h->gen_lds),
+                         static_cast<hipStream_t>(stream), a));
   return DIP_OK;
 }
 

@@ -38,6 +38,17 @@ struct GeneralArgs {
   uint32_t tab_bytes;      // LDS bytes holding rec + edge (variant 1)
   uint32_t ord_bytes;      // LDS bytes of order rows per wave (variants 1, 2)
   uint32_t end_bytes;      // LDS bytes of end tables per wave (variants 1-3)
+  // re-timing with a memory selection (choice != null): the backward of pair
+  // p costs its op cost + cand_time[p][c] - cand_time[p][0] and the pair's
+  // activation is cand_mem[p][c], c = choice[cand][p]
+  const uint8_t *choice;   // [n_cand][n_pairs]
+  int32_t n_pairs;
+  const int32_t *lid_pair; // [N] pair index on its rank | kind << 31
+  const int32_t *pair_off; // [P+1]
+  const int64_t *cand_time;   // [pairs][kMemoptMaxCands]
+  const int32_t *cand_mem;    // [pairs][kMemoptMaxCands]
+  const uint32_t *cand_key;   // [pairs][kMemoptMaxCands] move keys: candidate c exists when
+                              // c == 0 or key[c - 1] marks a move
 };
 
 const void *general_kernel_ptr(int variant);
@@ -359,7 +370,9 @@ struct MemoptArgs {
   int64_t stride;
   int64_t *out_time;          // [n][P]
   int32_t *out_peak;          // [n][P]
-  uint8_t *out_status;        // [n][P] 1 within the cap, 0 not reachable, 2 order not a permutation
+  uint8_t *out_status;        // [n][P] 1 within the cap (5 % gap proven), 3 within the cap
+                              // (not proven), 0 not reachable, 2 order not a permutation
+  uint8_t *out_choice;        // [n][n_pairs] chosen candidate of every pair, or null
   const int32_t *rank_off;    // [P+1] ops
   const int32_t *pair_off;    // [P+1] pairs of each rank (slot order)
   const int32_t *lid_pair;    // [N] pair index on its rank | kind << 31 (by global op)
@@ -369,12 +382,14 @@ struct MemoptArgs {
   const int32_t *move_dm;     // [pairs][kMemoptMaxCands] memory it frees; 0 past the last
   const int32_t *cap;         // [P]
   int32_t P, max_pairs;
+  int32_t n_pairs;            // pairs of all ranks
+  int32_t bb_nodes;           // placements the branch and bound may examine
   int32_t bytes_per_thread;   // LDS per thread: 9 bytes per pair
 };
 hipError_t launch_memopt(int threads_per_block, hipStream_t s, const MemoptArgs &a);
 // a wave per (schedule, rank), waves_per_block schedules of one rank per block,
 // up to 64 * ppl pairs per rank (ppl 1, 2, 4, 8); LDS per block:
-// (68 + 4 * waves_per_block) bytes per pair
+// (68 + 7 * waves_per_block) bytes per pair
 hipError_t launch_memopt_wave(int ppl, int waves_per_block, hipStream_t s, const MemoptArgs &a);
 size_t memopt_wave_lds(int32_t max_pairs, int waves_per_block);
 

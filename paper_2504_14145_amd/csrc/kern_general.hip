@@ -22,6 +22,11 @@
 //   2: op records/edges read through the caches, rows and end times in LDS;
 //   3: only end times in LDS (rows read straight from HBM);
 //   4: end times in device scratch (one region per resident wave).
+//
+// With a memory selection (Sec. 5.3) an op's cost and activation come from
+// its stage pair's chosen candidate instead: the backward runs the
+// candidate's extra time (its recomputation), and the pair holds the
+// candidate's memory from its forward to its backward.
 #include "dip_sim.h"
 #include "internal.h"
 
@@ -83,6 +88,32 @@ __device__ __forceinline__ void round_fence() {
   }
 }
 
+// Cost and memory change of op g in candidate cand: its record's, or under a
+// memory selection those of its pair's chosen candidate (the backward adds
+// the candidate's time over the pair's fastest).  false for a choice beyond
+// the pair's candidates.
+__device__ __forceinline__ bool op_cost_mem(const SimArgs &a, const int4 &rc, int g, int64_t cand,
+                                            int pair_base, int &cost, int &dmem) {
+  cost = rc.x;
+  dmem = rc.y;
+  if (!a.choice) return true;
+  const uint32_t w = uint32_t(a.lid_pair[g]);
+  const int p = pair_base + int(w & 0x7fffffffu);
+  const int c = a.choice[cand * a.n_pairs + p];
+  if (c >= kMemoptMaxCands ||
+      (c > 0 && a.cand_key[int64_t(p) * kMemoptMaxCands + c - 1] == kMemoptNoMove))
+    return false;
+  const int32_t m = a.cand_mem[int64_t(p) * kMemoptMaxCands + c];
+  if (w >> 31) {
+    cost += int(a.cand_time[int64_t(p) * kMemoptMaxCands + c] -
+                a.cand_time[int64_t(p) * kMemoptMaxCands]);
+    dmem = -m;
+  } else {
+    dmem = m;
+  }
+  return true;
+}
+
 __device__ __forceinline__ uint64_t group_bits(uint64_t ballot, int grp, int pwl) {
   if (pwl == 6) return ballot;
   const int pw = 1 << pwl;
@@ -113,12 +144,13 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
   int32_t *gbase = nullptr;
   if constexpr (V == 4) gbase = a.gends + (wslot * a.G + grp) * int64_t(a.N);
 
-  int rb = 0, nr = 0, busy_r = 0, cap_r = -1;
+  int rb = 0, nr = 0, busy_r = 0, cap_r = -1, pair_base = 0;
   if (lane_on) {
     rb = a.rank_off[r];
     nr = a.rank_off[r + 1] - rb;
     busy_r = a.busy[r];
     cap_r = a.cap[r];
+    if (a.choice) pair_base = a.pair_off[r];
   }
 
   const int64_t total_waves = int64_t(gridDim.x) * a.wpb;
@@ -159,6 +191,7 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
     round_fence<V>();
 
     int ptr = 0, tfree = 0, mem = 0, peak = 0;
+    int busy_run = 0;   // the rank's fired op time (its busy time under a selection)
     bool bad = false;
     int st = live ? (nr > 0 ? kRun : kDone) : kOff;
 
@@ -172,8 +205,11 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
         } else {
           const int g = rb + o;
           const int4 rc = load_rec<V>(a, g);
+          int cost = 0, dmem = 0;
           if (load_end<V>(a, end_off, gbase, g) != -1) {
             bad = true;  // the id already fired: not a permutation
+          } else if (!op_cost_mem(a, rc, g, cand, pair_base, cost, dmem)) {
+            bad = true;  // a choice beyond the pair's candidates
           } else {
             int t = tfree;
             bool ready = true;
@@ -184,10 +220,11 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
               t = max(t, pe + ed.y);
             }
             if (ready) {
-              const int en = t + rc.x;
+              const int en = t + cost;
               store_end<V>(a, end_off, gbase, g, en);
               tfree = en;
-              mem += rc.y;
+              busy_run += cost;
+              mem += dmem;
               peak = max(peak, mem);
               fired = true;
               if (++ptr == nr) st = kDone;
@@ -215,7 +252,9 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
         const int g = rb + o;
         if (load_end<V>(a, end_off, gbase, g) != -1) { bad = true; break; }
         store_end<V>(a, end_off, gbase, g, -2);
-        mem += load_rec<V>(a, g).y;
+        int cost = 0, dmem = 0;
+        if (!op_cost_mem(a, load_rec<V>(a, g), g, cand, pair_base, cost, dmem)) { bad = true; break; }
+        mem += dmem;
         peak = max(peak, mem);
       }
     }
@@ -233,7 +272,7 @@ __global__ __launch_bounds__(256) void sim_kernel(SimArgs a) {
         a.out_bub[o] = -1;
         a.out_peak[o] = -1;
       } else {
-        a.out_bub[o] = gb_stall ? -1 : T - busy_r;
+        a.out_bub[o] = gb_stall ? -1 : T - (a.choice ? busy_run : busy_r);
         a.out_peak[o] = peak;
       }
       if (r == 0) {

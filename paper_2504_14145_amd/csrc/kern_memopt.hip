@@ -4,13 +4,25 @@
 // For every (candidate schedule, rank), each stage pair of the rank takes one
 // of its memory candidates (time ascending, memory strictly descending) so
 // that the live memory at every forward start stays within the rank's cap,
-// with the least total time the greedy warm start of Sec. 5.3's ILP finds:
-// all pairs on their fastest candidate; while the most loaded checkpoint
-// (lowest index among equal loads) is over the cap, move the live pair with
-// the least added time per freed memory unit (dt_a * dm_b < dt_b * dm_a,
-// lowest pair index on ties) to its next candidate; give up when no live
-// pair can move.  Pair i is live at pair k's forward start when its forward
-// comes no later and its backward no earlier in the rank's order.
+// with the least total time (Sec. 5.3's ILP, solved to within 5 %):
+//   1. the greedy warm start: all pairs on their fastest candidate; while the
+//      most loaded checkpoint (lowest index among equal loads) is over the
+//      cap, move the live pair with the least added time per freed memory
+//      unit (dt_a * dm_b < dt_b * dm_a, lowest pair index on ties) to its
+//      next candidate; give up when no live pair can move;
+//   2. an improvement pass: pairs in index order each go back to the fastest
+//      candidate that keeps every checkpoint it is live at within the cap,
+//      until a pass changes nothing;
+//   3. a depth-first branch and bound from there, pairs in the order of their
+//      forward starts, candidates fastest first: a placement whose own
+//      checkpoint exceeds the cap is dropped, a node whose placed time plus
+//      the unplaced pairs' fastest times, times 1.05, reaches the incumbent
+//      is cut with its slower siblings, and a complete placement below the
+//      incumbent replaces it.  A finished search proves the incumbent within
+//      5 % of the optimum (status 1); after bb_nodes placements examined, or
+//      on ranks of more than 512 pairs (no search), status 3.
+// Pair i is live at pair k's forward start when its forward comes no later
+// and its backward no earlier in the rank's order.
 //
 // The comparison of moves depends on the candidates only, not on the
 // schedule, so the host ranks every move of a rank once (exact 128-bit cross
@@ -20,10 +32,14 @@
 //                       j, j + 64, ... in registers; the most loaded
 //                       checkpoint and the best move are one DPP wave
 //                       reduction each; a block holds schedules of one rank
-//                       and shares that rank's move tables in LDS.
+//                       and shares that rank's move tables in LDS.  In the
+//                       search, lane j also holds the stack entries of
+//                       depths j, j + 64, ... (candidate, placed time,
+//                       fastest time of the rest), and a checkpoint's load
+//                       is one wave sum over the placed pairs.
 //   memopt_kernel       a thread per (schedule, rank), for ranks of more
-//                       than 512 pairs; its state sits in LDS,
-//                       element-major across the block.
+//                       than 512 pairs (steps 1 and 2); its state sits in
+//                       LDS, element-major across the block.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -55,6 +71,23 @@ __device__ __forceinline__ uint32_t wave_reduce63(uint32_t v) {
   v = op(v, uint32_t(__builtin_amdgcn_update_dpp(kId, int(v), 0x142, 0xa, 0xf, false)));  // row_bcast:15
   v = op(v, uint32_t(__builtin_amdgcn_update_dpp(kId, int(v), 0x143, 0xc, 0xf, false)));  // row_bcast:31
   return uint32_t(__builtin_amdgcn_readlane(int(v), 63));
+}
+
+// sum of one value over the 64 lanes of a wave (wrapping), the same in every lane
+__device__ __forceinline__ int32_t wave_sum(int32_t v) {
+  v += int32_t(dpp_row<0xb1>(uint32_t(v)));    // quad_perm [1,0,3,2]
+  v += int32_t(dpp_row<0x4e>(uint32_t(v)));    // quad_perm [2,3,0,1]
+  v += int32_t(dpp_row<0x141>(uint32_t(v)));   // row_half_mirror
+  v += int32_t(dpp_row<0x140>(uint32_t(v)));   // row_mirror
+  return __builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16) +
+         __builtin_amdgcn_readlane(v, 32) + __builtin_amdgcn_readlane(v, 48);
+}
+
+__device__ __forceinline__ int64_t wave_sum64(int64_t v) {
+#pragma unroll
+  for (int s = 1; s < 64; s <<= 1)
+    v += (int64_t(__shfl_xor(int(v >> 32), s)) << 32) | uint32_t(__shfl_xor(int(uint32_t(v)), s));
+  return v;
 }
 
 __device__ __forceinline__ void write_out(const MemoptArgs &a, int64_t o, int64_t t, int32_t pk,
@@ -146,13 +179,39 @@ __global__ __launch_bounds__(256) void memopt_kernel(MemoptArgs a) {
         if (pf(bi) <= pf(k) && pf(k) <= pb(bi)) load(k) -= dm;
     }
   }
+  uint8_t status = ok ? 1 : 0;
+  if (ok && cap >= 0 && np > 0) {
+    // step 2; no search on ranks this large
+    for (bool changed = true; changed;) {
+      changed = false;
+      for (int32_t i = 0; i < np; ++i) {
+        int32_t top = INT32_MIN;
+        for (int32_t k = 0; k < np; ++k)
+          if (pf(i) <= pf(k) && pf(k) <= pb(i)) top = max(top, load(k));
+        const int32_t ci = cur(i);
+        const int32_t mc = cm[i * kMemoptMaxCands + ci];
+        for (int32_t j = 0; j < ci; ++j) {
+          const int32_t add = cm[i * kMemoptMaxCands + j] - mc;
+          if (int64_t(top) + add <= int64_t(cap)) {
+            for (int32_t k = 0; k < np; ++k)
+              if (pf(i) <= pf(k) && pf(k) <= pb(i)) load(k) += add;
+            cur(i) = uint8_t(j);
+            changed = true;
+            break;
+          }
+        }
+      }
+    }
+    status = 3;
+  }
   int64_t total = 0;
   int32_t peak = 0;
   for (int32_t i = 0; i < np; ++i) {
     total += ct[i * kMemoptMaxCands + cur(i)];
     peak = max(peak, load(i));
+    if (a.out_choice) a.out_choice[c * a.n_pairs + pbase + i] = cur(i);
   }
-  write_out(a, o, total, peak, ok ? 1 : 0);
+  write_out(a, o, total, peak, status);
 }
 #undef load
 #undef pf
@@ -176,9 +235,12 @@ __global__ __launch_bounds__(256) void memopt_wave_kernel(MemoptArgs a) {
   uint32_t *tkey = reinterpret_cast<uint32_t *>(sh);
   int32_t *tdm = reinterpret_cast<int32_t *>(sh + 32 * mp);
   int32_t *tm0 = reinterpret_cast<int32_t *>(sh + 64 * mp);
-  // this wave's positions of each pair's forward and backward
-  uint16_t *pfa = reinterpret_cast<uint16_t *>(sh + 68 * mp) + int64_t(wv) * 2 * mp;
+  // this wave's positions of each pair's forward and backward, its pairs in
+  // the order of their forwards, and the final choice of each pair
+  uint16_t *pfa = reinterpret_cast<uint16_t *>(sh + 68 * mp) + int64_t(wv) * 3 * mp;
   uint16_t *pba = pfa + mp;
+  uint16_t *orda = pba + mp;
+  uint8_t *sela = sh + 68 * mp + 6 * mp * nw + int64_t(wv) * mp;
   {
     const uint32_t *gk = a.move_key + int64_t(pbase) * kMemoptMaxCands;
     const int32_t *gd = a.move_dm + int64_t(pbase) * kMemoptMaxCands;
@@ -293,6 +355,175 @@ __global__ __launch_bounds__(256) void memopt_wave_kernel(MemoptArgs a) {
     }
   }
   const int64_t *ct = a.cand_time + int64_t(pbase) * kMemoptMaxCands;
+  const int32_t *cmem = a.cand_mem + int64_t(pbase) * kMemoptMaxCands;
+  // the register of slot q of every lane as one value, and its update in one lane
+  auto pick = [](const auto (&v)[PPL], int qd) {
+    auto x = v[0];
+#pragma unroll
+    for (int q = 1; q < PPL; ++q)
+      if (q == qd) x = v[q];
+    return x;
+  };
+  auto own = [&](int q) { return lane + 64 * q < np; };
+  uint8_t status = ok ? 1 : 0;
+  if (ok && cap >= 0 && np > 0) {
+    // ---- step 2: back to faster candidates where every checkpoint allows
+    for (bool changed = true; changed;) {
+      changed = false;
+      for (int32_t i = 0; i < np; ++i) {
+        const uint32_t spf = pfa[i], spb = pba[i];
+        uint32_t mx = 0;
+#pragma unroll
+        for (int q = 0; q < PPL; ++q)
+          if (own(q) && spf <= pf[q] && pf[q] <= spb) mx = max(mx, uint32_t(load[q]) ^ 0x80000000u);
+        const int64_t top = int32_t(wave_reduce63<true>(mx) ^ 0x80000000u);
+        const int qi = i >> 6, li = i & 63;
+        const int32_t ci = __builtin_amdgcn_readlane(pick(cur, qi), li);
+        const int32_t mc = cmem[i * kMemoptMaxCands + ci];
+        int32_t nj = ci;
+        for (int32_t j = 0; j < ci; ++j)
+          if (top + (cmem[i * kMemoptMaxCands + j] - mc) <= int64_t(cap)) {
+            nj = j;
+            break;
+          }
+        if (nj < ci) {
+          const int32_t add = cmem[i * kMemoptMaxCands + nj] - mc;
+#pragma unroll
+          for (int q = 0; q < PPL; ++q) {
+            if (own(q) && spf <= pf[q] && pf[q] <= spb) load[q] += add;
+            if (q == qi && lane == li) cur[q] = nj;
+          }
+          changed = true;
+        }
+      }
+    }
+
+    // ---- step 3: branch and bound, pairs by forward position
+    // depth of each own pair: the pairs whose forward comes earlier
+#pragma unroll
+    for (int q = 0; q < PPL; ++q)
+      if (own(q)) {
+        int32_t dep = 0;
+        for (int32_t j = 0; j < np; ++j) dep += pfa[j] < pf[q] ? 1 : 0;
+        orda[dep] = uint16_t(lane + 64 * q);
+      }
+    lds_sync_wave();
+    // stack entries of depths lane + 64 q: pair, candidate, placed time
+    // above the depth, fastest time of the pairs from the depth on
+    int32_t dpair[PPL], dch[PPL];
+    int64_t dplaced[PPL], drest[PPL];
+    // own pairs: candidate and memory of the current placement, best choice
+    int32_t pcur[PPL], pmem[PPL], best[PPL];
+#pragma unroll
+    for (int q = 0; q < PPL; ++q) {
+      dpair[q] = own(q) ? orda[lane + 64 * q] : 0;
+      dch[q] = -1;
+      dplaced[q] = 0;
+      drest[q] = 0;
+      pcur[q] = 0;
+      pmem[q] = 0;
+      best[q] = cur[q];
+    }
+    {
+      int64_t rest = 0;
+      for (int32_t d = np - 1; d >= 0; --d) {
+        rest += ct[int32_t(orda[d]) * kMemoptMaxCands];
+#pragma unroll
+        for (int q = 0; q < PPL; ++q)
+          if (q == (d >> 6) && lane == (d & 63)) drest[q] = rest;
+      }
+    }
+    int64_t inc = 0;
+#pragma unroll
+    for (int q = 0; q < PPL; ++q)
+      if (own(q)) inc += ct[(lane + 64 * q) * kMemoptMaxCands + cur[q]];
+    inc = wave_sum64(inc);
+    bool proven = true;
+    uint32_t seen = 0;
+    int32_t d = 0;
+    while (d >= 0) {
+      const int qd = d >> 6, ld = d & 63;
+      const int32_t i = __builtin_amdgcn_readlane(pick(dpair, qd), ld);
+      const int32_t c = __builtin_amdgcn_readlane(pick(dch, qd), ld) + 1;
+      // candidate c of pair i exists when the move into it does
+      const bool has = c < kMemoptMaxCands && (c == 0 || tkey[i * kMemoptMaxCands + c - 1] != kMemoptNoMove);
+      if (!has) {
+#pragma unroll
+        for (int q = 0; q < PPL; ++q)
+          if (q == qd && lane == ld) dch[q] = -1;
+        --d;
+        continue;
+      }
+#pragma unroll
+      for (int q = 0; q < PPL; ++q)
+        if (q == qd && lane == ld) dch[q] = c;
+      if (++seen > uint32_t(a.bb_nodes)) {
+        proven = false;
+        break;
+      }
+      const int64_t t = ct[i * kMemoptMaxCands + c];
+      const int32_t m = cmem[i * kMemoptMaxCands + c];
+      // its checkpoint: the placed pairs (forward earlier) still live there
+      const uint32_t spf = pfa[i];
+      int32_t part = 0;
+#pragma unroll
+      for (int q = 0; q < PPL; ++q)
+        if (own(q) && pf[q] < spf && pb[q] >= spf) part += pmem[q];
+      // (a pair whose backward comes before its forward is live nowhere)
+      const int64_t own_m = pba[i] >= spf ? int64_t(m) : 0;
+      if (own_m + wave_sum(part) > int64_t(cap)) continue;   // a leaner one may fit
+      const int64_t f =
+          int64_t(uint32_t(__builtin_amdgcn_readlane(int(uint32_t(pick(dplaced, qd))), ld))) |
+          (int64_t(__builtin_amdgcn_readlane(int(pick(dplaced, qd) >> 32), ld)) << 32);
+      const int64_t f_t = f + t;
+      int64_t rest = 0;
+      if (d + 1 < np) {
+        const int q1 = (d + 1) >> 6, l1 = (d + 1) & 63;
+        rest = int64_t(uint32_t(__builtin_amdgcn_readlane(int(uint32_t(pick(drest, q1))), l1))) |
+               (int64_t(__builtin_amdgcn_readlane(int(pick(drest, q1) >> 32), l1)) << 32);
+      }
+      if (__int128(105) * (f_t + rest) >= __int128(100) * inc) {   // cut, with the slower ones
+#pragma unroll
+        for (int q = 0; q < PPL; ++q)
+          if (q == qd && lane == ld) dch[q] = kMemoptMaxCands;
+        continue;
+      }
+      const int qi = i >> 6, li = i & 63;
+#pragma unroll
+      for (int q = 0; q < PPL; ++q)
+        if (q == qi && lane == li) {
+          pcur[q] = c;
+          pmem[q] = m;
+        }
+      if (d == np - 1) {   // every pair placed, below the incumbent
+        inc = f_t;
+#pragma unroll
+        for (int q = 0; q < PPL; ++q) best[q] = pcur[q];
+        continue;
+      }
+      const int q1 = (d + 1) >> 6, l1 = (d + 1) & 63;
+#pragma unroll
+      for (int q = 0; q < PPL; ++q)
+        if (q == q1 && lane == l1) dplaced[q] = f_t;
+      ++d;
+    }
+    status = proven ? 1 : 3;
+    // the final choice and its checkpoint loads
+#pragma unroll
+    for (int q = 0; q < PPL; ++q) {
+      cur[q] = best[q];
+      if (own(q)) sela[lane + 64 * q] = uint8_t(cur[q]);
+    }
+    lds_sync_wave();
+#pragma unroll
+    for (int q = 0; q < PPL; ++q) {
+      int32_t s = 0;
+      if (own(q))
+        for (int32_t j = 0; j < np; ++j)
+          if (pfa[j] <= pf[q] && pf[q] <= pba[j]) s += cmem[j * kMemoptMaxCands + sela[j]];
+      load[q] = s;
+    }
+  }
   int64_t total = 0;
   uint32_t pk = 0x80000000u;                        // image of load 0
 #pragma unroll
@@ -301,6 +532,7 @@ __global__ __launch_bounds__(256) void memopt_wave_kernel(MemoptArgs a) {
     if (i < np) {
       total += ct[i * kMemoptMaxCands + cur[q]];
       pk = max(pk, uint32_t(load[q]) ^ 0x80000000u);
+      if (a.out_choice) a.out_choice[c * a.n_pairs + pbase + i] = uint8_t(cur[q]);
     }
   }
   pk = wave_reduce63<true>(pk);
@@ -308,13 +540,13 @@ __global__ __launch_bounds__(256) void memopt_wave_kernel(MemoptArgs a) {
   for (int s = 1; s < 64; s <<= 1)
     total += (int64_t(__shfl_xor(int(total >> 32), s)) << 32) |
              uint32_t(__shfl_xor(int(uint32_t(total)), s));
-  if (lane == 0) write_out(a, o, total, int32_t(pk ^ 0x80000000u), ok ? 1 : 0);
+  if (lane == 0) write_out(a, o, total, int32_t(pk ^ 0x80000000u), status);
 }
 
 }  // namespace
 
 size_t memopt_wave_lds(int32_t max_pairs, int waves_per_block) {
-  return size_t(max_pairs) * (68 + 4 * size_t(waves_per_block));
+  return size_t(max_pairs) * (68 + 7 * size_t(waves_per_block));
 }
 
 hipError_t launch_memopt_wave(int ppl, int waves_per_block, hipStream_t s, const MemoptArgs &a) {

@@ -27,7 +27,7 @@ def test_library_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(dip.EXPORTS)
-    assert lib.dip_sim_abi_version() == 6
+    assert lib.dip_sim_abi_version() == 7
 
 
 def test_strerror_strings():

@@ -74,8 +74,7 @@ def test_memopt_full_batch_sampled():
     want = MO.optimise(prob, tab, MO.pair_candidates(tab, S), rows[idx])
     np.testing.assert_array_equal(t.cpu().numpy()[idx], [[x[0] for x in per] for per in want])
     np.testing.assert_array_equal(p.cpu().numpy()[idx], [[x[2] for x in per] for per in want])
-    np.testing.assert_array_equal(s.cpu().numpy()[idx], [[1 if x[1] else 0 for x in per]
-                                                         for per in want])
+    np.testing.assert_array_equal(s.cpu().numpy()[idx], [[x[1] for x in per] for per in want])
     sim.close()
 
 
