@@ -300,7 +300,13 @@ int dip_sim_configure_rollouts(dip_sim *h, int32_t n_classes, const int32_t *gro
  *               from mix(mix(seed + (draw+1)*G) + (i+1)*G), G =
  *               0x9E3779B97F4A7C15, mix = SplitMix64's output function.
  *   out_prio    device int32 [n_rollouts][n_groups]: the rollouts' priorities.
- *   out_makespan, out_flags  device [n_rollouts], as dip_sim_greedy's.
+ *   out_makespan, out_flags  device [n_rollouts], as dip_sim_greedy's; once
+ *               dip_sim_configure_memopt has run on the handle, a rollout is
+ *               scored as Sec. 5.1 says, by its iteration time after the
+ *               per-layer memory optimisation: its interleaved schedule goes
+ *               through dip_sim_memopt and is re-timed with the selection
+ *               (dip_sim_evaluate_selected), whose makespan and flags these
+ *               are (DIP_FLAG_CAP where a rank's cap cannot be met).
  *   inout_best_key  device uint64.
  * Costs are those of the last call that passed them (DIP_E_STATE if none since
  * the grouping).  Enqueued on stream; the prefix is copied before return. */

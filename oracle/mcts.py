@@ -8,10 +8,15 @@ Python, one node object per tree node, following the paper's loop:
   segments after its search-space reduction: the pieces of one module in one
   microbatch share a class).  The class at position i (0-based) gets priority
   n - i; a group's priority is its class's; the dual-queue interleaving of
-  Sec. 5.2 (``oracle.greedy``) turns the priorities into a schedule and its
-  makespan is the score (lower is better).  A rollout whose schedule exceeds a
-  memory cap scores +inf: the paper's per-layer memory optimisation
-  (Sec. 5.3), which could repair it, is not part of this path.
+  Sec. 5.2 (``oracle.greedy``) turns the priorities into a schedule, and the
+  score (lower is better) is the iteration time: with ``memory`` given (a
+  strategy table and its pair candidates), the schedule's per-layer memory
+  optimisation (Sec. 5.3, ``oracle.memopt.optimise``) picks each stage pair's
+  candidate and the schedule re-timed with that selection
+  (``oracle.memopt.selected_problem``) is simulated; its makespan is the
+  score, +inf when a rank's cap cannot be met (the re-timed run is then over
+  the cap).  Without ``memory`` the score is the interleaved schedule's
+  makespan, +inf over a cap.
 * Tree: a node at depth d fixes the class at position d - 1; it keeps s, the
   best score seen in its subtree, and N, its visit count.
 * Selection: from the root, while the node has no untried child, step to the
@@ -154,8 +159,26 @@ def mark_done(v, n_classes):
             break
 
 
+def score_rollouts(prob, op_group, n_groups, prio, threads=8, memory=None):
+    """Scores of priority rows: the iteration time after the interleaving
+    (and the memory optimisation when ``memory`` = (table, candidates)), +inf
+    for a flagged schedule."""
+    orders, res = _greedy(prob, op_group, n_groups, prio, threads=threads)
+    if memory is None:
+        return [float(m) if f == 0 else INF for m, f in zip(res.makespan, res.flags)]
+    from . import evaluate
+    from . import memopt as _mo
+    table, cands = memory
+    per_row = _mo.optimise(prob, table, cands, orders)
+    out = []
+    for row, per in zip(orders, per_row):
+        r = evaluate(_mo.selected_problem(prob, table, cands, per), row[None, :])
+        out.append(float(r.makespan[0]) if r.flags[0] == 0 else INF)
+    return out
+
+
 def search(prob, op_group, n_groups, group_class, iterations, rollouts, seed,
-           alpha=1.0, beta=0.1, threads=8, policy="ucb", workers=1):
+           alpha=1.0, beta=0.1, threads=8, policy="ucb", workers=1, memory=None):
     """Run the search for ``iterations`` rounds of ``workers`` leaves; returns
     (trajectory, best, root) where trajectory[k] = (prefix of leaf k, best score
     of its rollouts, index of the best rollout) and best = (score, sequence,
@@ -211,8 +234,7 @@ def search(prob, op_group, n_groups, group_class, iterations, rollouts, seed,
             rest = [c for c in range(n) if c not in set(prefix)]
             seqs = [prefix + shuffled(rest, seed, kk, i) for i in range(rollouts)]
             prio = np.stack([priorities_of(q, group_class, n) for q in seqs])
-            _, res = _greedy(prob, op_group, n_groups, prio, threads=threads)
-            scores = [float(m) if f == 0 else INF for m, f in zip(res.makespan, res.flags)]
+            scores = score_rollouts(prob, op_group, n_groups, prio, threads, memory)
             b = min(range(rollouts), key=lambda i: (scores[i], i))
             if scores[b] == INF:
                 b = -1                       # no feasible rollout

@@ -238,6 +238,13 @@ struct dip_sim {
   bool rl_seq_pending = false;
   int32_t *d_rl_bub = nullptr, *d_rl_peak = nullptr;  // [cap][P] greedy outputs
   int64_t rl_cap = 0;
+  // rollouts scored after the memory selection: the orders, the selection's
+  // outputs and choices
+  int16_t *d_rl_orders = nullptr;
+  int64_t *d_rl_mo_time = nullptr;
+  int32_t *d_rl_mo_peak = nullptr;
+  uint8_t *d_rl_mo_status = nullptr, *d_rl_choice = nullptr;
+  int64_t rl_mo_cap = 0;
   // per-layer memory optimisation (dip_sim_configure_memopt / dip_sim_memopt)
   bool mo_ok = false;
   int32_t mo_max_pairs = 0, mo_n_pairs = 0, mo_bb_nodes = 512;
@@ -1024,6 +1031,19 @@ bool greedy_layout(const dip_sim *h, int K, int pwl, dip_sim::GrLaunch *L, bool 
   return true;
 }
 
+void release_rollout_memopt(dip_sim *h) {
+  if (h->d_rl_orders) (void)hipFree(h->d_rl_orders);
+  if (h->d_rl_mo_time) (void)hipFree(h->d_rl_mo_time);
+  if (h->d_rl_mo_peak) (void)hipFree(h->d_rl_mo_peak);
+  if (h->d_rl_mo_status) (void)hipFree(h->d_rl_mo_status);
+  if (h->d_rl_choice) (void)hipFree(h->d_rl_choice);
+  h->d_rl_orders = nullptr;
+  h->d_rl_mo_time = nullptr;
+  h->d_rl_mo_peak = nullptr;
+  h->d_rl_mo_status = h->d_rl_choice = nullptr;
+  h->rl_mo_cap = 0;
+}
+
 void release_rollouts(dip_sim *h) {
   if (h->d_rl_class) (void)hipFree(h->d_rl_class);
   if (h->d_rl_seq) (void)hipFree(h->d_rl_seq);
@@ -1031,6 +1051,7 @@ void release_rollouts(dip_sim *h) {
   if (h->rl_seq_ev) (void)hipEventDestroy(h->rl_seq_ev);
   if (h->d_rl_bub) (void)hipFree(h->d_rl_bub);
   if (h->d_rl_peak) (void)hipFree(h->d_rl_peak);
+  release_rollout_memopt(h);
   h->d_rl_class = h->d_rl_seq = h->h_rl_seq = nullptr;
   h->rl_leaf_cap = 0;
   h->rl_seq_ev = nullptr;
@@ -1987,9 +2008,35 @@ int dip_sim_rollouts_batch(dip_sim *h, int32_t n_leaves, const int32_t *depths,
   a.n_classes = n;
   a.G = h->gr_G;
   DIP_HIP(launch_rollout_prio(stream, a));
-  int rc = dip_sim_greedy(h, nullptr, out_prio, rows, nullptr, out_makespan, h->d_rl_bub,
-                          h->d_rl_peak, out_flags, stream_);
-  if (rc != DIP_OK) return rc;
+  int rc;
+  if (!h->mo_ok) {
+    rc = dip_sim_greedy(h, nullptr, out_prio, rows, nullptr, out_makespan, h->d_rl_bub,
+                        h->d_rl_peak, out_flags, stream_);
+    if (rc != DIP_OK) return rc;
+  } else {
+    // Sec. 5.1's score: the interleaved schedule after the per-layer memory
+    // optimisation, re-timed with its selection (a rank whose cap cannot be
+    // met keeps a selection over the cap, which the re-timed run flags)
+    if (h->rl_mo_cap < rows) {
+      DIP_HIP(hipDeviceSynchronize());
+      release_rollout_memopt(h);
+      DIP_HIP(hipMalloc(&h->d_rl_orders, size_t(rows) * size_t(h->stride) * 2));
+      DIP_HIP(hipMalloc(&h->d_rl_mo_time, size_t(rows) * h->P * 8));
+      DIP_HIP(hipMalloc(&h->d_rl_mo_peak, size_t(rows) * h->P * 4));
+      DIP_HIP(hipMalloc(&h->d_rl_mo_status, size_t(rows) * h->P));
+      DIP_HIP(hipMalloc(&h->d_rl_choice, size_t(rows) * std::max(h->mo_n_pairs, 1)));
+      h->rl_mo_cap = rows;
+    }
+    rc = dip_sim_greedy(h, nullptr, out_prio, rows, h->d_rl_orders, out_makespan, h->d_rl_bub,
+                        h->d_rl_peak, out_flags, stream_);
+    if (rc != DIP_OK) return rc;
+    rc = dip_sim_memopt(h, h->d_rl_orders, rows, h->d_rl_mo_time, h->d_rl_mo_peak,
+                        h->d_rl_mo_status, h->d_rl_choice, stream_);
+    if (rc != DIP_OK) return rc;
+    rc = dip_sim_evaluate_selected(h, h->d_rl_orders, h->d_rl_choice, rows, out_makespan,
+                                   h->d_rl_bub, h->d_rl_peak, out_flags, stream_);
+    if (rc != DIP_OK) return rc;
+  }
   // the best unflagged rollout of each leaf, indexed within the leaf
   const int64_t want = (per_leaf + 255) / 256;
   const int blocks = int(std::max<int64_t>(1, std::min<int64_t>(want, int64_t(h->n_cu) * 8 / n_leaves)));

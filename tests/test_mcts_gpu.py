@@ -191,3 +191,85 @@ def test_parallel_search_matches_oracle(case, workers, policy):
     if case == "tiny":
         assert srch.done[0] and len(traj) == 64
     sim.close()
+
+
+def _sim_memory(prob, S):
+    """A handle with the greedy, the rollouts' classes and the memory
+    selection configured: rollouts are then scored after the selection."""
+    from workloads.strategies import strategy_table
+    import oracle.memopt as MO
+    sim, g, G, cls = _sim(prob)
+    tab = strategy_table(prob)
+    assert dip.configure_memopt(sim.h, tab.slot_layers, tab.time, tab.mem, S) == dip.OK
+    return sim, g, G, cls, (tab, MO.pair_candidates(tab, S))
+
+
+def _capped_tiny(cap):
+    inst = W.pipeline_instance(2, 3, np.array([[3, 7, 4], [5, 2, 6]]), comm=1, act=8, mem_cap=cap)
+    return W.compile_instance(inst)
+
+
+def _capped_vlm(frac):
+    """The 8-rank VLM workload with caps below what its interleavings reach."""
+    prob = W.make_problem(2)
+    g, G, cls = W.priority_groups(prob)
+    n = int(cls.max()) + 1
+    prio = np.stack([OM.priorities_of(list(np.random.default_rng(i).permutation(n)), cls, n)
+                     for i in range(16)])
+    _, res = O.greedy(prob, g, G, prio, threads=16)
+    prob.mem_cap[:] = int(np.median(res.peak) * frac)
+    return prob
+
+
+@pytest.mark.parametrize("case,R", [("tiny", 60), ("c2", 48)])
+def test_rollouts_scored_after_memory_selection(case, R):
+    """Sec. 5.1's score: every rollout interleaved, memory-optimised and
+    re-timed; makespans, flags and the best key against the oracle."""
+    need_gpu()
+    prob = _capped_tiny(4) if case == "tiny" else _capped_vlm(0.3)
+    sim, g, G, cls, mem = _sim_memory(prob, 4 if case == "tiny" else 6)
+    n = int(cls.max()) + 1
+    assert dip.configure_rollouts(sim.h, n, cls) == dip.OK
+    prefix = [int(c) for c in np.random.default_rng(5).permutation(n)[:n // 3]]
+    prio = torch.empty((R, G), dtype=torch.int32, device=DEV)
+    ms = torch.empty(R, dtype=torch.int32, device=DEV)
+    fl = torch.empty(R, dtype=torch.uint8, device=DEV)
+    key = torch.full((1,), -1, dtype=torch.int64, device=DEV)
+    print(f"{case}: caps {prob.mem_cap.tolist()}, {R} rollouts", flush=True)
+    dip.rollouts(sim.h, prefix, R, 777, 3, prio, ms, fl, key)
+    torch.cuda.synchronize()
+    rest = [c for c in range(n) if c not in set(prefix)]
+    want_prio = np.stack([OM.priorities_of(prefix + OM.shuffled(rest, 777, 3, i), cls, n)
+                          for i in range(R)])
+    np.testing.assert_array_equal(prio.cpu().numpy(), want_prio)
+    scores = OM.score_rollouts(prob, g, G, want_prio, threads=16, memory=mem)
+    got_ms, got_fl = ms.cpu().numpy(), fl.cpu().numpy()
+    for i in range(R):
+        assert (got_fl[i] == 0) == (scores[i] < OM.INF), i
+        if scores[i] < OM.INF:
+            assert got_ms[i] == scores[i], i
+    plain = OM.score_rollouts(prob, g, G, want_prio, threads=16)
+    finite = [i for i in range(R) if scores[i] < OM.INF]
+    assert finite and any(plain[i] == OM.INF for i in finite)   # the selection repaired some
+    b = min(finite, key=lambda i: (scores[i], i))
+    assert dip.decode_key(int(key.item())) == (b, int(scores[b]))
+    sim.close()
+
+
+@pytest.mark.parametrize("case", ["tiny", "c2"])
+def test_memory_aware_search_matches_oracle(case):
+    need_gpu()
+    prob = _capped_tiny(4) if case == "tiny" else _capped_vlm(0.3)
+    iters, R = {"tiny": (120, 3), "c2": (4, 16)}[case]
+    sim, g, G, cls, mem = _sim_memory(prob, 4 if case == "tiny" else 6)
+    print(f"{case}: {iters} iterations x {R} rollouts, memory-aware", flush=True)
+    srch = Search(sim, cls, R, seed=17)
+    traj, best = srch.run(iters)
+    want_traj, want_best, root = OM.search(prob, g, G, cls, iters, R, seed=17, threads=16,
+                                           memory=mem)
+    assert traj == want_traj
+    assert best[0] == want_best[0] and best[2:] == want_best[2:]
+    if want_best[1] is not None:
+        assert best[1] == list(want_best[1])
+    assert want_best[0] < OM.INF
+    sim.close()

@@ -197,3 +197,57 @@ def test_parallel_workers_invariants():
     t1, b1, _ = M.search(prob, g, G, cls, iterations=12, rollouts=4, seed=8, workers=1)
     t2, b2, _ = M.search(prob, g, G, cls, iterations=12, rollouts=4, seed=8)
     assert t1 == t2 and b1[0] == b2[0]
+
+
+def _capped_tiny(cap):
+    inst = W.pipeline_instance(2, 3, np.array([[3, 7, 4], [5, 2, 6]]), comm=1, act=8, mem_cap=cap)
+    prob = W.compile_instance(inst)
+    g, G, cls = W.priority_groups(prob)
+    return prob, g, G, cls
+
+
+def test_memory_aware_scores():
+    """Sec. 5.1's rollout score with the memory optimisation: equal to the
+    makespan when nothing is capped; under a binding cap finite where the
+    selection meets it, never below the same orders' makespan without
+    recomputation, and +inf exactly where some rank's cap is out of reach."""
+    from workloads.strategies import strategy_table
+    import oracle.memopt as MO
+    prob, g, G, cls = _capped_tiny(-1)
+    tab = strategy_table(prob)
+    mem = (tab, MO.pair_candidates(tab, 4))
+    n = int(cls.max()) + 1
+    seqs = list(itertools.permutations(range(n)))
+    prio = np.stack([M.priorities_of(q, cls, n) for q in seqs])
+    free = M.score_rollouts(prob, g, G, prio)
+    assert M.score_rollouts(prob, g, G, prio, memory=mem) == free
+    for cap in (20, 12, 8, 4, 1):
+        pc, _, _, _ = _capped_tiny(cap)
+        plain = M.score_rollouts(pc, g, G, prio)
+        aware = M.score_rollouts(pc, g, G, prio, memory=mem)
+        orders, _ = O.greedy(pc, g, G, prio)       # (the interleaving sees the cap)
+        base = O.evaluate(pc, orders).makespan       # the same orders, nothing recomputed
+        per = MO.optimise(pc, tab, mem[1], orders)
+        for k in range(len(seqs)):
+            reach = all(x[1] in (1, 3) for x in per[k])
+            assert (aware[k] < M.INF) == reach, (cap, k)
+            if reach:
+                assert aware[k] >= base[k]
+            if plain[k] < M.INF:              # within the cap as interleaved: kept as is
+                assert aware[k] == plain[k]
+        if cap == 4:   # below what the interleaving alone can meet: recomputation repairs it
+            assert all(p == M.INF and a < M.INF for p, a in zip(plain, aware))
+
+
+def test_exhaustive_memory_aware_search_finds_the_brute_force_optimum():
+    from workloads.strategies import strategy_table
+    import oracle.memopt as MO
+    prob, g, G, cls = _capped_tiny(4)
+    tab = strategy_table(prob)
+    mem = (tab, MO.pair_candidates(tab, 4))
+    n = int(cls.max()) + 1
+    seqs = list(itertools.permutations(range(n)))
+    prio = np.stack([M.priorities_of(q, cls, n) for q in seqs])
+    brute = min(M.score_rollouts(prob, g, G, prio, memory=mem))
+    traj, best, root = M.search(prob, g, G, cls, iterations=2000, rollouts=3, seed=1, memory=mem)
+    assert root.done and best[0] == brute < M.INF
