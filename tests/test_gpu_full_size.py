@@ -156,15 +156,16 @@ def test_full_stream_large_16x4_argmin():
     cs = ChunkStream(sim, chunk)
     all_ms = np.empty(cfg.n_cand, np.int32)
     all_fl = np.empty(cfg.n_cand, np.uint8)
-    hosts = []
+    # two pinned host buffers, refilled once the copy out of them has ended
+    hosts = [torch.empty((chunk, prob.stride), dtype=torch.int16, pin_memory=True)
+             for _ in range(2)]
     for k in range(cfg.n_cand // chunk):
         lo = k * chunk
         rows = gen.generate(lo, chunk)
-        host = torch.from_numpy(rows).pin_memory()
-        cs.submit(host, lo)
-        hosts.append(host)
-        if len(hosts) > 2:
-            hosts.pop(0)
+        if k >= 2:
+            cs.copied[k % 2].synchronize()
+        hosts[k % 2].numpy()[:] = rows
+        cs.submit(hosts[k % 2], lo)
         for a in range(0, chunk, ORACLE_CHUNK):
             want = O.evaluate(prob, rows[a:a + ORACLE_CHUNK], threads=THREADS)
             all_ms[lo + a:lo + a + ORACLE_CHUNK] = want.makespan
