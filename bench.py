@@ -336,6 +336,7 @@ def main():
         step()
         per_kernel.append(dip.last_profile(sim.h))
     dip.profile(sim.h, False)
+    retries = dip.last_retries(sim.h) if info["variant"] >= 8 else (0, 0)
     nk = min(len(p) for p in per_kernel)
     kern_avg_ms = [sum(p[i] for p in per_kernel) / len(per_kernel) for i in range(nk)]
     names = {8: ["check", "simulate", "retry"],
@@ -343,7 +344,8 @@ def main():
                                                                  ["simulate"])[:nk]
     dom = names.index("simulate")
     dom_s = kern_avg_ms[dom] / 1e3
-    log(f"[bench] per-kernel avg ms: " + ", ".join(f"{n} {t:.4f}" for n, t in zip(names, kern_avg_ms)))
+    log(f"[bench] per-kernel avg ms: " + ", ".join(f"{n} {t:.4f}" for n, t in zip(names, kern_avg_ms))
+        + f"; retries {retries}")
 
     calib_copies(args, dev)
 
@@ -446,6 +448,9 @@ def main():
         "evaluate_us": kern_avg_s * 1e6,
         "kernel_us": {n: t * 1e3 for n, t in zip(names, kern_avg_ms)},
         "kernel_variant": info["variant"],
+        # candidates whose pools filled in the first simulation pass, and
+        # those the second pass (16 slots) handed to the general kernel
+        "retries": {"first_pass": retries[0], "second_pass": retries[1]},
         "pool_slots": slots,
         "best": {"index": best[0], "makespan_us": best[1]},
         "roofline": {"bound": "hbm", "kernel": "simulate", "achieved": achieved_gbs,

@@ -256,10 +256,38 @@ __global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
       };
       // positions lo .. hi-1 of a unit of 8 (lo, hi uniform)
       auto unit = [&](const uint4 v, int lo, int hi) {
+        if constexpr (ORDER) {   // an op's predecessor may sit earlier in the same unit
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          const uint32_t w = q < 2 ? v.x : q < 4 ? v.y : q < 6 ? v.z : v.w;
-          if (q >= lo && q < hi) take((q & 1) ? (w >> 16) : (w & 0xffffu));
+          for (int q = 0; q < 8; ++q) {
+            const uint32_t w = q < 2 ? v.x : q < 4 ? v.y : q < 6 ? v.z : v.w;
+            if (q >= lo && q < hi) take((q & 1) ? (w >> 16) : (w & 0xffffu));
+          }
+        } else {
+          // the unit's deltas are read first, all eight in flight at once,
+          // then its bits are set, then the running sum takes the deltas in
+          // order (the bitmap and the deltas are different words, so the
+          // reads need not wait for the ORs)
+          uint32_t c[8];
+          int32_t dl[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            const uint32_t w = q < 2 ? v.x : q < 4 ? v.y : q < 6 ? v.z : v.w;
+            c[q] = min((q & 1) ? (w >> 16) : (w & 0xffffu), lim);
+            dl[q] = q >= lo && q < hi ? mdl[c[q]] : 0;
+          }
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            if (q >= lo && q < hi) {
+              uint32_t wd;
+              asm("v_lshrrev_b32 %0, 5, %1" : "=v"(wd) : "v"(c[q]));
+              __hip_atomic_fetch_or(bm + wd * kWave, 1u << (c[q] & 31u), __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_WORKGROUP);
+            }
+#pragma unroll
+          for (int q = 0; q < 8; ++q) {
+            run += dl[q];
+            if (q >= lo && q < hi) peak = max(peak, run);
+          }
         }
       };
       if (nr > 0) {
