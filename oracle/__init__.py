@@ -18,7 +18,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRCS = [os.path.join(_HERE, "dip_oracle.c"), os.path.join(_HERE, "dip_greedy.c")]
-_LIB = os.path.join(_HERE, "libdip_oracle.so")
+# DIPSIM_ORACLE_LIB names another build of the same sources (the sanitizer test loads
+# one built with -fsanitize=address,undefined); it is then used as it is
+_LIB = os.environ.get("DIPSIM_ORACLE_LIB") or os.path.join(_HERE, "libdip_oracle.so")
 
 FLAG_DEADLOCK = 1
 FLAG_CAP = 2
@@ -26,6 +28,8 @@ FLAG_INVALID = 4
 
 
 def build(force: bool = True) -> str:
+    if os.environ.get("DIPSIM_ORACLE_LIB"):
+        return _LIB
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-Wall", "-Wextra", "-shared",

@@ -8,8 +8,10 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 SOURCES = [os.path.join(CSRC, f) for f in
-           ("host.hip", "kern_general.hip", "kern_check.hip", "kern_pool.hip", "kern_sim.hip", "kern_greedy.hip", "kern_rollout.hip",
-            "kern_costmodel.hip", "kern_memopt.hip", "kern_argmin.hip")]
+           ("host.hip", "host_plan.hip", "host_tables.hip", "host_next.hip", "host_check.cpp",
+            "kern_general.hip", "kern_check.hip", "kern_pool.hip", "kern_sim.hip",
+            "kern_greedy.hip", "kern_rollout.hip", "kern_costmodel.hip", "kern_memopt.hip",
+            "kern_argmin.hip")]
 LIB = os.path.join(HERE, "libdip_sim.so")
 INCLUDE = os.path.join(ROOT, "include")
 

@@ -17,7 +17,9 @@ from .instance import KIND_B, KIND_F, Problem
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "gen.c")
-_LIB = os.path.join(_HERE, "libdipgen.so")
+# DIPSIM_GEN_LIB names another build of the same sources (the sanitizer test loads
+# one built with -fsanitize=address,undefined); it is then used as it is
+_LIB = os.environ.get("DIPSIM_GEN_LIB") or os.path.join(_HERE, "libdipgen.so")
 
 MODE_1F1B = 0
 MODE_LIST = 1
@@ -26,6 +28,8 @@ PURPOSE_POOL = 3
 
 
 def build(force: bool = True) -> str:
+    if os.environ.get("DIPSIM_GEN_LIB"):
+        return _LIB
     if force or not os.path.exists(_LIB):
         tmp = _LIB + ".tmp"
         subprocess.check_call(["gcc", "-O2", "-std=c11", "-Wall", "-shared", "-fPIC",
