@@ -17,21 +17,26 @@ if torch.cuda.is_available():
 DEV = "cuda:0"
 
 
+@pytest.mark.parametrize("variant", [8, 9])
 @pytest.mark.parametrize("cid,n", [(2, 65536), (1, 4096)])
-def test_tiled_batch_past_the_slots(cid, n):
+def test_tiled_batch_past_the_slots(cid, n, variant):
+    """The pool kernel (variant 8) and the compact-record simulation kernel
+    (variant 9, the default here) alike."""
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     cfg = W.get(cid)
     prob = W.make_problem(cfg)
     rows = W.generator_for(prob, cfg).generate(0, n)
     sim = dip.Sim(prob)
-    info = sim.info
-    assert info["variant"] == 8
-    slots = info["max_blocks"] * info["waves_per_block"] * info["groups_per_wave"]
-    reps = int(np.ceil(2.5 * slots / n)) + 1          # well past twice the slots
+    assert sim.configure(variant, 0) == dip.OK
     orders = torch.from_numpy(rows).to(DEV)
-    print(f"config {cid}: {n} x {reps} candidates, {slots} slots", flush=True)
-    ms, bub, pk, fl = sim.evaluate(orders)
+    ms, bub, pk, fl = sim.evaluate(orders)       # (variant 9's shape follows the costs)
+    info = sim.info
+    assert info["variant"] == variant
+    slots = info["max_blocks"] * info["waves_per_block"] * info["groups_per_wave"]
+    assert slots > 0
+    reps = int(np.ceil(2.5 * slots / n)) + 1          # well past twice the slots
+    print(f"config {cid} variant {variant}: {n} x {reps} candidates, {slots} slots", flush=True)
     big = orders.repeat(reps, 1)
     bms, bbub, bpk, bfl = sim.evaluate(big)
     torch.cuda.synchronize()
