@@ -126,7 +126,8 @@ typedef struct {
   int32_t max_blocks;        /* resident blocks the grid is capped at            */
   int64_t scratch_bytes;     /* device scratch owned by the handle               */
   int32_t pool_slots;        /* variant 8: end-time slots per rank pool, else 0  */
-  int32_t check_kernel;      /* variant 8: 1 wave per candidate, 2 tiles, else 0 */
+  int32_t check_kernel;      /* variants 8, 9: 1 wave per candidate, 2 tiles,
+                                else 0                                         */
   int32_t greedy_inbox;      /* dip_sim_greedy: stages a rank's inbox holds (0:
                                 not configured); grows when many overflow     */
   int32_t greedy_lds_bytes;  /* dip_sim_greedy: LDS per block of its launch    */
@@ -173,15 +174,17 @@ int dip_sim_configure(dip_sim *h, int32_t variant, int32_t waves_per_block);
  * DIP_E_UNSUPPORTED if the topology does not fit variant 8. */
 int dip_sim_configure_pool(dip_sim *h, int32_t slots_per_rank);
 
-/* Variant 8: the kernel of the order-only part of the verdict (permutation
- * check, per-rank peak memory, cap flag; Sec. 5.3's memory liveness).
- * 0 = automatic (tiles when they fit), 1 = one wavefront per candidate with
- * an op-id bitmap of N bits in LDS, 2 = tiles of 64 candidates, one lane per
- * candidate, the ranks split between the waves of a block, each wave holding
- * one rank's memory deltas and 64 bitmaps of (ops of the rank + 1) bits in
- * LDS.  Results are the same either way.  DIP_E_UNSUPPORTED if the topology
- * does not fit variant 8 or the kernel asked for does not fit the device's
- * LDS; DIP_E_INVAL for another mode. */
+/* Variants 8 and 9: the kernel of the order-only part of the verdict
+ * (permutation check, per-rank peak memory, cap flag; Sec. 5.3's memory
+ * liveness).  0 = automatic (tiles when they fit), 1 = one wavefront per
+ * candidate with an op-id bitmap of N bits in LDS, 2 = tiles of 64
+ * candidates, one lane per candidate, the ranks split between the waves of a
+ * block, each wave holding one rank's memory deltas and 64 bitmaps of (ops of
+ * the rank + 1) bits in LDS; after it, for the ranks whose ops wait on an op
+ * of their own rank, one wavefront per rank section tests that order from a
+ * table of the section's positions.  Results are the same either way.
+ * DIP_E_UNSUPPORTED if the topology does not fit variant 8 or the kernel
+ * asked for does not fit the device's LDS; DIP_E_INVAL for another mode. */
 int dip_sim_configure_check(dip_sim *h, int32_t mode);
 
 int dip_sim_get_info(const dip_sim *h, dip_sim_info *info);

@@ -35,6 +35,15 @@ __device__ __forceinline__ uint64_t any_lane_of_group(uint64_t m) {
 // Waits for this wave's outstanding LDS (and scalar-load) operations.
 __device__ __forceinline__ void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
 
+// Keeps this wave's LDS accesses on either side of this point in program
+// order (the LDS serves one wave's instructions in issue order), without the
+// wait for outstanding global loads that a workgroup-scope fence brings.
+__device__ __forceinline__ void wave_lds_order() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Orders the LDS accesses of the lanes of one wave around this point.
 __device__ __forceinline__ void wave_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");

@@ -119,13 +119,13 @@ void release(dip_sim *h) {
   if (h->d_edge) (void)hipFree(h->d_edge);
   if (h->d_md) (void)hipFree(h->d_md);
   if (h->d_selfp) (void)hipFree(h->d_selfp);
+  if (h->d_oc_ranks) (void)hipFree(h->d_oc_ranks);
   if (h->d_sim_tab) (void)hipFree(h->d_sim_tab);
   if (h->d_sim_lane) (void)hipFree(h->d_sim_lane);
   if (h->d_rank_off) (void)hipFree(h->d_rank_off);
   if (h->d_busy) (void)hipFree(h->d_busy);
   if (h->d_cap) (void)hipFree(h->d_cap);
   if (h->tc.d_plan) (void)hipFree(h->tc.d_plan);
-  if (h->to.d_plan) (void)hipFree(h->to.d_plan);
   if (h->d_scratch_gen) (void)hipFree(h->d_scratch_gen);
   if (h->d_scratch_fb) (void)hipFree(h->d_scratch_fb);
   if (h->d_pool_rec) (void)hipFree(h->d_pool_rec);
@@ -317,9 +317,9 @@ int dip_sim_configure_check(dip_sim *h, int32_t mode) {
   if (!h || mode < 0 || mode > 2) return DIP_E_INVAL;
   if (!h->pool_ok || (mode == 1 && !h->wc_ok) || (mode == 2 && !h->tc_ok)) return DIP_E_UNSUPPORTED;
   h->check_mode = mode;
-  // the simulation kernel's tables drop own-rank edges only behind the tile
-  // check: rebuild them from the last costs when that changes
-  if (h->sim_ok && h->costs_set && h->sim_drop_self != (h->to_ok && use_tile_check(h))) {
+  // the simulation kernel's tables drop own-rank edges only behind a check
+  // that tests their order: rebuild them from the last costs when that changes
+  if (h->sim_ok && h->costs_set && h->sim_drop_self != order_checked(h)) {
     const dip_costs c{h->last_cost.data(), h->last_comm.data(), h->last_act.data()};
     int rc = upload_costs(h, &c, nullptr);
     if (rc != DIP_OK) return rc;
@@ -346,7 +346,7 @@ int dip_sim_get_info(const dip_sim *h, dip_sim_info *info) {
   info->max_blocks = sim ? (h->sim_costs_ok ? h->sim_max_blocks : 0) : h->max_blocks;
   info->scratch_bytes = h->scratch_gen_bytes + h->scratch_fb_bytes + h->retry_cap * 8;
   info->pool_slots = v >= 8 ? h->pool_slots : 0;
-  info->check_kernel = v >= 8 ? (use_tile_check(h) ? 2 : 1) : 0;
+  info->check_kernel = v >= 8 ? check_kind(h) : 0;
   info->greedy_inbox = h->gr_ok ? h->gr_K : 0;
   info->greedy_lds_bytes = h->gr_ok ? int32_t(h->gr_main.lds) : 0;
   info->greedy_retry_ring_bytes = h->gr_ok ? h->gr_ring_bytes : 0;
@@ -400,10 +400,10 @@ int evaluate_impl(dip_sim *h, const dip_costs *costs, const int16_t *orders, int
     uint32_t *const counts = sx->counts;
     h->last_counts = counts;
     DIP_HIP(mark(0));
-    int rc = use_tile_check(h) ? run_tile_check(h, orders, n_cand, out_makespan, out_bubble,
-                                                out_peakmem, out_flags, stream, counts)
-                               : run_wave_check(h, orders, n_cand, out_makespan, out_bubble,
-                                                out_peakmem, out_flags, stream, counts);
+    int rc = check_kind(h) == 2 ? run_tile_check(h, orders, n_cand, out_makespan, out_bubble,
+                                                 out_peakmem, out_flags, stream, counts)
+                                : run_wave_check(h, orders, n_cand, out_makespan, out_bubble,
+                                                 out_peakmem, out_flags, stream, counts);
     if (rc != DIP_OK) return rc;
     DIP_HIP(mark(1));
     const uint32_t round_limit = uint32_t(h->N) + uint32_t(h->E) + 16u;

@@ -79,23 +79,23 @@ int ensure_scratch(dip_sim *h, int64_t need) {
 }
 
 // The pool kernel's fallback: the general kernel with end tables in device
-// Tile check plan over a set of ranks: they are split between the waves of a
-// block, longest section first onto the least loaded wave.  The number of
-// waves per block is the one (up to 16, and not above the ranks or what keeps
-// every wave near the longest section) that keeps the most waves resident per
-// CU.  false when a rank's section does not fit.
-bool plan_tiles(dip_sim *h, const std::vector<int32_t> &rks, bool order, dip_sim::TilePlan *T) {
+// Tile check plan: the ranks are split between the waves of a block,
+// longest section first onto the least loaded wave.  The number of waves per
+// block is the one (up to kTileMaxWaves, and not above the ranks or what
+// keeps every wave near the longest section) that keeps the most waves
+// resident per CU.  false when a rank's section does not fit.
+bool plan_tiles(dip_sim *h, dip_sim::TilePlan *T) {
   int32_t max_nr = 0;
   int64_t n_sum = 0;
-  for (int32_t r : rks) {
+  for (int r = 0; r < h->P; ++r) {
     max_nr = std::max(max_nr, h->n_ops[r]);
     n_sum += h->n_ops[r];
   }
-  if (rks.empty() || int64_t(h->stride) * 2 * kWave > int64_t(INT32_MAX)) return false;
-  const void *kern = tile_check_kernel_ptr(order);
+  if (int64_t(h->stride) * 2 * kWave > int64_t(INT32_MAX)) return false;
+  const void *kern = tile_check_kernel_ptr();
   const int64_t region = tile_region_bytes(max_nr);
   const int nw_max = int(std::min<int64_t>(
-      {16, int64_t(rks.size()), (n_sum + std::max(max_nr, 1) - 1) / std::max(max_nr, 1)}));
+      {int64_t(kTileMaxWaves), int64_t(h->P), (n_sum + std::max(max_nr, 1) - 1) / std::max(max_nr, 1)}));
   int nw = 0, nb = 0, best_waves = 0;
   for (int w = 1; w <= std::max(nw_max, 1); ++w) {
     const int64_t lds = kTileFlagBytes + int64_t(w) * region;
@@ -117,7 +117,8 @@ bool plan_tiles(dip_sim *h, const std::vector<int32_t> &rks, bool order, dip_sim
     }
   }
   if (nw == 0) return false;
-  std::vector<int32_t> sorted(rks), load(nw, 0), wave_of(h->P, -1);
+  std::vector<int32_t> sorted(size_t(h->P)), load(nw, 0), wave_of(h->P, -1);
+  for (int r = 0; r < h->P; ++r) sorted[r] = r;
   std::stable_sort(sorted.begin(), sorted.end(),
                    [&](int32_t x, int32_t y) { return h->n_ops[x] > h->n_ops[y]; });
   for (int32_t r : sorted) {
@@ -125,7 +126,7 @@ bool plan_tiles(dip_sim *h, const std::vector<int32_t> &rks, bool order, dip_sim
     wave_of[r] = w;
     load[w] += h->n_ops[r];
   }
-  std::vector<int32_t> plan(size_t(nw) + 1 + rks.size());
+  std::vector<int32_t> plan(size_t(nw) + 1 + size_t(h->P));
   int k = 0;
   for (int w = 0; w < nw; ++w) {
     plan[w] = k;
@@ -139,7 +140,7 @@ bool plan_tiles(dip_sim *h, const std::vector<int32_t> &rks, bool order, dip_sim
     (void)hipGetLastError();
     return false;
   }
-  if (!T->d_plan && hipMalloc(&T->d_plan, size_t(h->P + 17) * 4) != hipSuccess) {
+  if (!T->d_plan && hipMalloc(&T->d_plan, size_t(h->P + kTileMaxWaves + 1) * 4) != hipSuccess) {
     (void)hipGetLastError();
     return false;
   }
@@ -154,17 +155,71 @@ bool plan_tiles(dip_sim *h, const std::vector<int32_t> &rks, bool order, dip_sim
   return true;
 }
 
-// The main tile check over every rank, and the order pass over the ranks
-// with own-rank predecessors (when there are any).
-int plan_tile_check(dip_sim *h) {
-  std::vector<int32_t> all(h->P), own;
-  for (int r = 0; r < h->P; ++r) {
-    all[r] = r;
-    if ((h->self_ranks >> r) & 1u) own.push_back(r);
+// The order kernel over the ranks with own-rank predecessors: the waves per
+// block are the count (4, 8 or 16) that keeps the most waves resident per
+// CU, the larger on ties (fewer table copies).  false when nothing fits.
+bool plan_order_check(dip_sim *h, const std::vector<int32_t> &rks) {
+  int32_t max_nr = 0;
+  int64_t n_sum = 0;
+  for (int32_t r : rks) {
+    max_nr = std::max(max_nr, h->n_ops[r]);
+    n_sum += h->n_ops[r];
   }
-  h->tc_ok = plan_tiles(h, all, false, &h->tc);
-  // (without the order pass the simulation kernel keeps those edges)
-  h->to_ok = h->tc_ok && h->self_ok && !own.empty() && plan_tiles(h, own, true, &h->to);
+  const int32_t tab = order_table_bytes(max_nr);
+  const void *kern = order_check_kernel_ptr();
+  int best = 0;
+  for (int w : {4, 8, 16}) {
+    const int64_t lds = int64_t(tab) * (w + 1);
+    if (lds > h->lds_block_max) break;
+    if (lds > 65536 &&
+        hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, int(lds)) != hipSuccess) {
+      (void)hipGetLastError();
+      break;
+    }
+    int b = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&b, kern, w * kWave, size_t(lds)) != hipSuccess) {
+      (void)hipGetLastError();
+      break;
+    }
+    if (b > 0 && b * w >= best) {
+      best = b * w;
+      h->oc_wpb = w;
+      h->oc_blocks_per_cu = b;
+      h->oc_lds = lds;
+    }
+  }
+  if (best == 0) return false;
+  if (h->oc_lds > 65536 && hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize,
+                                               int(h->oc_lds)) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  if (!h->d_oc_ranks && hipMalloc(&h->d_oc_ranks, size_t(h->P) * 4) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  if (hipMemcpy(h->d_oc_ranks, rks.data(), rks.size() * 4, hipMemcpyHostToDevice) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  // candidates per wave and block: about 64 KB of a mean section's ids, so
+  // that the table copy at a block's start stays a few percent of its work
+  const int64_t mean_bytes = std::max<int64_t>(2 * n_sum / int64_t(rks.size()), 1);
+  h->oc_per_wave = int(std::min<int64_t>(64, std::max<int64_t>(2, 65536 / mean_bytes)));
+  h->oc_tab_bytes = tab;
+  h->oc_n_ranks = int32_t(rks.size());
+  return true;
+}
+
+// The tile check over every rank, and the order kernel over the ranks with
+// own-rank predecessors (when there are any and each op has at most one).
+int plan_tile_check(dip_sim *h) {
+  std::vector<int32_t> own;
+  for (int r = 0; r < h->P; ++r)
+    if ((h->self_ranks >> r) & 1u) own.push_back(r);
+  h->tc_ok = plan_tiles(h, &h->tc);
+  // (without the order kernel the simulation kernel keeps those edges)
+  h->to_ok = h->tc_ok && h->self_ok && !own.empty() && plan_order_check(h, own);
   return DIP_OK;
 }
 
@@ -222,9 +277,12 @@ int ensure_fallback(dip_sim *h) {
   return (h->wc_ok || h->tc_ok) ? DIP_OK : DIP_E_UNSUPPORTED;
 }
 
-bool use_tile_check(const dip_sim *h) {
-  return h->check_mode == 2 || (h->check_mode == 0 && h->tc_ok) || !h->wc_ok;
+int check_kind(const dip_sim *h) {
+  if (h->check_mode != 0) return h->check_mode;
+  return h->tc_ok ? 2 : 1;
 }
+
+bool order_checked(const dip_sim *h) { return check_kind(h) == 2 && h->to_ok; }
 
 int run_tile_check(dip_sim *h, const int16_t *orders, int64_t n_cand, int32_t *out_ms,
                    int32_t *out_bub, int32_t *out_peak, uint8_t *out_flags, hipStream_t stream,
@@ -240,19 +298,44 @@ int run_tile_check(dip_sim *h, const int16_t *orders, int64_t n_cand, int32_t *o
   c.md = h->d_md;
   c.rank_off = h->d_rank_off;
   c.cap = h->d_cap;
-  c.selfp = h->d_selfp;
   c.P = h->P;
   c.retry_count = counts;
   const int64_t tiles = (n_cand + kWave - 1) / kWave;
-  for (int pass = 0; pass < (h->to_ok ? 2 : 1); ++pass) {
-    const dip_sim::TilePlan &T = pass ? h->to : h->tc;
-    c.plan = T.d_plan;
-    c.nw = T.nw;
-    c.md_bytes = tile_md_bytes(T.max_nr);
-    c.region_bytes = tile_region_bytes(T.max_nr);
-    const int blocks = int(std::min<int64_t>(tiles, int64_t(T.blocks_per_cu) * h->n_cu));
-    DIP_HIP(launch_tile_check(std::max(blocks, 1), T.nw, size_t(T.lds), stream, c, pass == 1));
-  }
+  const dip_sim::TilePlan &T = h->tc;
+  c.plan = T.d_plan;
+  c.nw = T.nw;
+  c.md_bytes = tile_md_bytes(T.max_nr);
+  c.region_bytes = tile_region_bytes(T.max_nr);
+  const int blocks = int(std::min<int64_t>(tiles, int64_t(T.blocks_per_cu) * h->n_cu));
+  DIP_HIP(launch_tile_check(std::max(blocks, 1), T.nw, size_t(T.lds), stream, c));
+  if (!h->to_ok) return DIP_OK;
+  OrderCheckArgs o{};
+  o.orders = orders;
+  o.n_cand = n_cand;
+  o.stride = h->stride;
+  o.out_ms = out_ms;
+  o.out_bub = out_bub;
+  o.out_flags = out_flags;
+  o.selfp = h->d_selfp;
+  o.rank_off = h->d_rank_off;
+  o.ranks = h->d_oc_ranks;
+  o.P = h->P;
+  o.n_ranks = h->oc_n_ranks;
+  o.wpb = h->oc_wpb;
+  o.tab_bytes = h->oc_tab_bytes;
+  o.wave_bytes = h->oc_tab_bytes;
+  // fewer candidates per wave for batches too small to give every resident
+  // block slot four chunks of each rank
+  const int64_t resident = int64_t(h->oc_blocks_per_cu) * h->n_cu;
+  const int64_t want_chunks = std::max<int64_t>(1, 4 * resident / o.n_ranks);
+  const int64_t per_wave =
+      (n_cand + int64_t(o.wpb) * want_chunks - 1) / (int64_t(o.wpb) * want_chunks);
+  o.per_wave = int32_t(std::max<int64_t>(1, std::min<int64_t>(h->oc_per_wave, per_wave)));
+  const int64_t per_block = int64_t(o.per_wave) * o.wpb;
+  o.n_chunks = (n_cand + per_block - 1) / per_block;
+  const int64_t blocks_o = order_blocks(o.n_chunks, o.n_ranks);
+  if (blocks_o > int64_t(INT32_MAX)) return DIP_E_INVAL;
+  DIP_HIP(launch_order_check(blocks_o, o.wpb, size_t(h->oc_lds), stream, o));
   return DIP_OK;
 }
 

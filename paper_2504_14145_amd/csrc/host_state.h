@@ -128,8 +128,16 @@ struct dip_sim {
   };
   bool tc_ok = false;                  // the main pass (every rank)
   TilePlan tc;
-  bool to_ok = false;                  // the order pass (ranks with own-rank predecessors)
-  TilePlan to;
+  // order kernel after the tile check (ranks with own-rank predecessors):
+  // one wave per section, a block per rank and chunk of candidates
+  bool to_ok = false;
+  int oc_wpb = 4;                      // waves per block
+  int oc_per_wave = 1;                 // candidates per wave and block (for large batches)
+  int oc_blocks_per_cu = 1;
+  int64_t oc_lds = 0;
+  int32_t oc_tab_bytes = 0;
+  int32_t oc_n_ranks = 0;
+  int32_t *d_oc_ranks = nullptr;       // [oc_n_ranks]
   void *d_scratch_fb = nullptr;        // general kernel (list mode) end tables
   int fb_variant = 4;                  // retry kernel: 3 (end times in LDS) when they fit, else 4
   int64_t fb_lds = 0;
@@ -258,7 +266,11 @@ int ensure_scratch(dip_sim *h, int64_t need);
 bool plan_tiles(dip_sim *h, const std::vector<int32_t> &rks, bool order, dip_sim::TilePlan *T);
 int plan_tile_check(dip_sim *h);
 int ensure_fallback(dip_sim *h);
-bool use_tile_check(const dip_sim *h);
+// the check kernel evaluate runs: 1 wave per candidate, 2 tiles
+int check_kind(const dip_sim *h);
+// evaluate's check tests the order of own-rank edges (the simulation
+// kernel's tables may then drop those of zero latency)
+bool order_checked(const dip_sim *h);
 int run_tile_check(dip_sim *h, const int16_t *orders, int64_t n_cand, int32_t *out_ms,
                    int32_t *out_bub, int32_t *out_peak, uint8_t *out_flags, hipStream_t stream,
                    uint32_t *counts);

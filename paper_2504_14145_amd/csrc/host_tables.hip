@@ -87,10 +87,10 @@ int upload_sim_tables(dip_sim *h, const dip_costs *c, const int32_t *busy, const
     if (uint32_t(c->edge_comm[e]) > kSimCommMax) return DIP_OK;
   const int32_t P = h->P;
   // an edge between two ops of one rank with zero latency holds by the order
-  // alone once the tile check has verified that the predecessor comes first
+  // alone once the check kernel has verified that the predecessor comes first
   // (it flags the candidate deadlocked otherwise): dropped, its producer then
   // publishes no end time for it
-  h->sim_drop_self = h->to_ok && use_tile_check(h);
+  h->sim_drop_self = order_checked(h);
   auto dropped = [&](int32_t g, int32_t k) {
     return h->sim_drop_self && h->rank_of[h->pred_op[k]] == h->rank_of[g] && c->edge_comm[k] == 0;
   };

@@ -97,8 +97,6 @@ struct TileCheckArgs {
   const int32_t *rank_off;  // [P+1]
   const int32_t *cap;       // [P]
   const int32_t *plan;      // [nw+1] offsets into the rank list, then the list [P]
-  const int32_t *selfp;     // [N] local id + 1 of the op's predecessor on its own rank
-                            // (0: none): what the order pass reads in place of md
   int32_t P, nw;
   int32_t md_bytes;         // bytes of a wave's delta area (16-aligned)
   int32_t region_bytes;     // bytes per wave: delta area + bitmap of 64 lanes
@@ -111,18 +109,48 @@ struct TileCheckArgs {
 // regions (deltas and bits of ids 0 .. max_nr, the last one the overflow
 // entry; then the staging of 8 units of the 64 rows)
 constexpr int kTileFlagBytes = 256;
+// waves per tile-check block at most (12: LDS holds at most three waves per
+// SIMD on the workloads that need many, and 168 registers per lane keep the
+// staged units and the two units in flight out of scratch)
+constexpr int kTileMaxWaves = 12;
 constexpr int kTileStageBytes = 64 * 8 * 16;
 __host__ __device__ inline int32_t tile_md_bytes(int32_t max_nr) { return ((max_nr + 1) * 4 + 15) & ~15; }
 __host__ __device__ inline int32_t tile_region_bytes(int32_t max_nr) {
   return tile_md_bytes(max_nr) + ((max_nr + 32) / 32) * 64 * 4 + kTileStageBytes;
 }
-// order: the pass over the ranks that run ops with an own-rank predecessor
-// (plan lists only those), after the main pass: a candidate in which such an
-// op comes before its predecessor deadlocks (flag added, makespan and bubbles
-// -1); nothing else is written
-const void *tile_check_kernel_ptr(bool order = false);
-hipError_t launch_tile_check(int blocks, int nw, size_t lds, hipStream_t s, const TileCheckArgs &a,
-                             bool order = false);
+const void *tile_check_kernel_ptr();
+hipError_t launch_tile_check(int blocks, int nw, size_t lds, hipStream_t s, const TileCheckArgs &a);
+
+// Own-rank order of the ranks whose ops wait on an op of their own rank: one
+// wave per (candidate, rank) section, a block per rank and chunk of
+// candidates, with the rank's own-rank predecessors in LDS and a table of the
+// section's positions per wave.  Runs after the tile check: skips candidates
+// flagged invalid; adds the deadlock flag and -1 makespan and bubbles.
+struct OrderCheckArgs {
+  const int16_t *orders;
+  int64_t n_cand;
+  int64_t stride;
+  int32_t *out_ms;
+  int32_t *out_bub;
+  uint8_t *out_flags;
+  const int32_t *selfp;     // [N] local id + 1 of the op's own-rank predecessor (0: none)
+  const int32_t *rank_off;  // [P+1]
+  const int32_t *ranks;     // [n_ranks] the ranks checked
+  int64_t n_chunks;         // chunks of wpb * per_wave candidates
+  int32_t P, n_ranks, wpb, per_wave;
+  int32_t tab_bytes;        // LDS: predecessors [max_nr + 1] uint16 (16-aligned)
+  int32_t wave_bytes;       // per wave: positions [max_nr + 1] uint16 (16-aligned)
+};
+__host__ __device__ inline int32_t order_table_bytes(int32_t max_nr) { return int32_t(align16(int64_t(max_nr + 1) * 2)); }
+// blocks of a launch over n_chunks chunks of n_ranks ranks: chunk j's blocks
+// are 8 apart, so they share j % 8 and with it the XCD the dispatcher sends
+// them to
+__host__ __device__ inline int64_t order_blocks(int64_t n_chunks, int32_t n_ranks) {
+  return 8 * int64_t(n_ranks) * ((n_chunks + 7) / 8);
+}
+const void *order_check_kernel_ptr();
+hipError_t launch_order_check(int64_t blocks, int wpb, size_t lds, hipStream_t s,
+                              const OrderCheckArgs &a);
 
 // ---------------------------------------------------------------- pool
 // Timing simulation with per-rank slot pools holding the end times still to

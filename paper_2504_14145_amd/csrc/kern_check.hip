@@ -1,5 +1,6 @@
 // kern_check.hip -- the order-only part of a candidate's verdict, run before
-// the timing simulation of the pool kernel:
+// the timing simulation (one wave per candidate, or tiles of 64 candidates
+// with lane = candidate followed by the order kernel):
 //
 //   * every rank section must be a permutation of that rank's op ids
 //     (an id out of range or repeated makes the candidate invalid, and every
@@ -20,6 +21,8 @@
 // that scan minus its value just before the rank's first lane, plus what the
 // rank had accumulated in earlier steps.  The rank's peak is then a masked
 // DPP max over its lanes.
+#include <type_traits>
+
 #include "dip_sim.h"
 #include "dev_util.h"
 #include "internal.h"
@@ -168,31 +171,23 @@ __global__ __launch_bounds__(256) void check_kernel(CheckArgs a) {
 //   * The running memory is the sum of the deltas of the ops taken so far,
 //     read from the wave's copy of the rank's deltas in LDS; the peak is its
 //     maximum, starting from 0 (Sec. 5.3).
-//   * (ORDER pass, over the ranks that need it) An op whose predecessor runs
-//     on its own rank must come after it in the rank's order: the
-//     predecessor's bit is tested before the op's own bit is set.  If it
-//     comes first, the two wait for each other (the data edge one way, the
-//     order the other): the candidate deadlocks, and its makespan and bubbles
-//     are -1 here already.  This pass reads the predecessors where the main
-//     pass reads the memory deltas.
 // The verdict of a candidate needs all of its ranks: each wave ORs its
 // findings into the candidates' flag words in LDS, and after a block barrier
-// the outputs of an invalid candidate are overwritten with -1 (makespan and
-// bubbles only, for one deadlocked on its own order).
+// the outputs of an invalid candidate are overwritten with -1.  (The order of
+// ops that wait on an op of their own rank is the order kernel's, below.)
 
-template <bool ORDER>
-__global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
+__global__ __launch_bounds__(kTileMaxWaves * kWave) void tile_check_kernel(TileCheckArgs a) {
   const int lane = threadIdx.x & (kWave - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   uint32_t *flg = reinterpret_cast<uint32_t *>(c_lds);
   unsigned char *region = c_lds + kTileFlagBytes + wave * a.region_bytes;
-  int32_t *mdl = reinterpret_cast<int32_t *>(region);   // deltas, or predecessors (ORDER)
+  int32_t *mdl = reinterpret_cast<int32_t *>(region);   // the rank's deltas
   uint32_t *bm = reinterpret_cast<uint32_t *>(region + a.md_bytes) + lane;   // word w at bm[64 w]
   // staging of 8 units of the 64 rows (8 KB), unit k of row l at slot
   // k ^ (l & 7) of the row's 8, so the reads of one unit by 8 lanes hit 8
   // distinct bank groups
   unsigned char *stg = region + a.region_bytes - kTileStageBytes;
-  if (!ORDER && a.retry_count && blockIdx.x == 0 && threadIdx.x < 4) a.retry_count[threadIdx.x] = 0u;
+  if (a.retry_count && blockIdx.x == 0 && threadIdx.x < 4) a.retry_count[threadIdx.x] = 0u;
 
   const int kb = a.plan[wave], ke = a.plan[wave + 1];
   const int32_t *ranks = a.plan + a.nw + 1;
@@ -219,7 +214,7 @@ __global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
       const int rb = a.rank_off[r], re = a.rank_off[r + 1];
       const int nr = re - rb;
       const int n_words = (nr + 32) >> 5;   // bits 0 .. nr
-      const int32_t *src = ORDER ? a.selfp : a.md;
+      const int32_t *src = a.md;
       // the rank's deltas into the wave's region (entry nr, the overflow
       // entry, is 0), the lanes' bitmaps cleared
       wave_sync();
@@ -236,68 +231,43 @@ __global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
 
       const uint32_t lim = uint32_t(nr);
       int run = 0, peak = 0;
-      bool late = false;   // an op before its own-rank predecessor
-      auto take = [&](uint32_t id) {
-        const uint32_t c = min(id, lim);
-        if constexpr (ORDER) {
-          const uint32_t sp = uint32_t(mdl[c]);
-          if (sp != 0u) late = late || !((bm[((sp - 1u) >> 5) * kWave] >> ((sp - 1u) & 31u)) & 1u);
-        }
-        // word index c >> 5, kept as one shift (the byte offset is then one
-        // shift-add instead of a shift, a mask and an add)
-        uint32_t w;
-        asm("v_lshrrev_b32 %0, 5, %1" : "=v"(w) : "v"(c));
-        __hip_atomic_fetch_or(bm + w * kWave, 1u << (c & 31u), __ATOMIC_RELAXED,
-                              __HIP_MEMORY_SCOPE_WORKGROUP);
-        if constexpr (!ORDER) {
-          run += mdl[c];
-          peak = max(peak, run);
+      // A unit of 8 ids is taken in two halves: its ids and deltas (eight
+      // LDS reads in flight at once), then its bits and running sum.  The
+      // deltas of the next unit are read before the current one's bits and
+      // sums, so the reads overlap that work (the bitmap and the deltas are
+      // different words: the reads need not wait for the ORs).
+      struct Fetched {
+        uint32_t c[8];
+        int32_t dl[8];
+      };
+      auto fetch = [&](const uint4 v, int lo, int hi, Fetched &f) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const uint32_t w = q < 2 ? v.x : q < 4 ? v.y : q < 6 ? v.z : v.w;
+          f.c[q] = min((q & 1) ? (w >> 16) : (w & 0xffffu), lim);
+          f.dl[q] = q >= lo && q < hi ? mdl[f.c[q]] : 0;
         }
       };
-      // positions lo .. hi-1 of a unit of 8 (lo, hi uniform)
-      auto unit = [&](const uint4 v, int lo, int hi) {
-        if constexpr (ORDER) {   // an op's predecessor may sit earlier in the same unit
+      auto apply = [&](const Fetched &f, int lo, int hi) {
 #pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            const uint32_t w = q < 2 ? v.x : q < 4 ? v.y : q < 6 ? v.z : v.w;
-            if (q >= lo && q < hi) take((q & 1) ? (w >> 16) : (w & 0xffffu));
-          }
-        } else {
-          // the unit's deltas are read first, all eight in flight at once,
-          // then its bits are set, then the running sum takes the deltas in
-          // order (the bitmap and the deltas are different words, so the
-          // reads need not wait for the ORs)
-          uint32_t c[8];
-          int32_t dl[8];
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            const uint32_t w = q < 2 ? v.x : q < 4 ? v.y : q < 6 ? v.z : v.w;
-            c[q] = min((q & 1) ? (w >> 16) : (w & 0xffffu), lim);
-            dl[q] = q >= lo && q < hi ? mdl[c[q]] : 0;
+        for (int q = 0; q < 8; ++q)
+          if (q >= lo && q < hi) {
+            uint32_t wd;
+            asm("v_lshrrev_b32 %0, 5, %1" : "=v"(wd) : "v"(f.c[q]));
+            __hip_atomic_fetch_or(bm + wd * kWave, 1u << (f.c[q] & 31u), __ATOMIC_RELAXED,
+                                  __HIP_MEMORY_SCOPE_WORKGROUP);
           }
 #pragma unroll
-          for (int q = 0; q < 8; ++q)
-            if (q >= lo && q < hi) {
-              uint32_t wd;
-              asm("v_lshrrev_b32 %0, 5, %1" : "=v"(wd) : "v"(c[q]));
-              __hip_atomic_fetch_or(bm + wd * kWave, 1u << (c[q] & 31u), __ATOMIC_RELAXED,
-                                    __HIP_MEMORY_SCOPE_WORKGROUP);
-            }
-#pragma unroll
-          for (int q = 0; q < 8; ++q) {
-            run += dl[q];
-            if (q >= lo && q < hi) peak = max(peak, run);
-          }
+        for (int q = 0; q < 8; ++q) {
+          run += f.dl[q];
+          if (q >= lo && q < hi) peak = max(peak, run);
         }
       };
       if (nr > 0) {
         const int u0 = rb >> 3, u1 = (re - 1) >> 3;   // first and last unit of 8 ids
-        auto step = [&](int u, const uint4 v) {
-          const int lo = max(rb - 8 * u, 0), hi = min(re - 8 * u, 8);
-          if (lo == 0 && hi == 8)
-            unit(v, 0, 8);
-          else
-            unit(v, lo, hi);
+        auto bounds = [&](int u, int &lo, int &hi) {
+          lo = max(rb - 8 * u, 0);
+          hi = min(re - 8 * u, 8);
         };
         // Rows are read 8 units (128 bytes) at a time, cooperatively: load i
         // brings rows 8i .. 8i+7, lane l reading unit (l & 7) of row
@@ -318,57 +288,189 @@ __global__ __launch_bounds__(1024) void tile_check_kernel(TileCheckArgs a) {
         uint4 nb[8];
         load_chunk(u0, nb);
         for (int cu = u0; cu <= u1; cu += 8) {
-          wave_sync();   // the previous chunk's reads are done
+          // the staging area is written and read by this wave only: program
+          // order of its LDS accesses is all it needs (no wait for the
+          // global loads in flight)
+          wave_lds_order();   // the previous chunk's reads are done
 #pragma unroll
           for (int i = 0; i < 8; ++i) *reinterpret_cast<uint4 *>(stg + 1024u * i + put) = nb[i];
-          wave_sync();
+          wave_lds_order();
           uint4 b[8];
 #pragma unroll
           for (int q = 0; q < 8; ++q)
             b[q] = *reinterpret_cast<const uint4 *>(stg + uint32_t((lane * 8 + (q ^ (lane & 7))) * 16));
           if (cu + 8 <= u1) load_chunk(cu + 8, nb);   // the next chunk, while this one runs
+          {
+            // (a chunk of eight units all inside the section takes the
+            // variant without position bounds)
+            auto run_chunk = [&](auto inner) {
+              constexpr bool kInner = decltype(inner)::value;
+              auto lim_of = [&](int u, int &lo, int &hi) {
+                if constexpr (kInner) {
+                  lo = 0;
+                  hi = 8;
+                } else {
+                  bounds(u, lo, hi);
+                }
+              };
+              Fetched fa, fb;
+              int lo, hi;
+              lim_of(cu, lo, hi);
+              fetch(b[0], lo, hi, fa);
 #pragma unroll
-          for (int q = 0; q < 8; ++q)
-            if (cu + q <= u1) step(cu + q, b[q]);
+              for (int q = 0; q < 8; ++q) {
+                if (!kInner && cu + q > u1) break;
+                Fetched &cur = (q & 1) ? fb : fa;
+                Fetched &nxt = (q & 1) ? fa : fb;
+                if (q + 1 < 8 && (kInner || cu + q + 1 <= u1)) {
+                  int l2, h2;
+                  lim_of(cu + q + 1, l2, h2);
+                  fetch(b[q + 1], l2, h2, nxt);
+                }
+                lim_of(cu + q, lo, hi);
+                apply(cur, lo, hi);
+              }
+            };
+            if (8 * cu >= rb && 8 * (cu + 8) <= re)
+              run_chunk(std::integral_constant<bool, true>{});
+            else
+              run_chunk(std::integral_constant<bool, false>{});
+          }
         }
       }
       uint32_t bits = 0;
       for (int w = 0; w < n_words; ++w) bits += uint32_t(__builtin_popcount(bm[w * kWave]));
       const bool ovf = (bm[(nr >> 5) * kWave] >> (nr & 31)) & 1u;
       const bool bad = ovf || bits != lim;
-      if constexpr (ORDER) {
-        fl |= late ? 4u : 0u;
-      } else {
-        const int cap_r = a.cap[r];
-        const bool over = cap_r >= 0 && peak > cap_r;
-        if (live) a.out_peak[cand * a.P + r] = peak;
-        fl |= (bad ? 1u : 0u) | (over ? 2u : 0u);
-      }
+      const int cap_r = a.cap[r];
+      const bool over = cap_r >= 0 && peak > cap_r;
+      if (live) a.out_peak[cand * a.P + r] = peak;
+      fl |= (bad ? 1u : 0u) | (over ? 2u : 0u);
     }
     if (fl) __hip_atomic_fetch_or(flg + lane, fl, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     __syncthreads();
     const uint32_t f = flg[lane];
-    if constexpr (ORDER) {
-      if (wave == 0 && live && (f & 4u)) {
-        const uint8_t old = a.out_flags[cand];
-        if (!(old & DIP_FLAG_INVALID)) {
-          a.out_flags[cand] = uint8_t(old | DIP_FLAG_DEADLOCK);
-          a.out_ms[cand] = -1;
-          for (int q = 0; q < a.P; ++q) a.out_bub[cand * a.P + q] = -1;
-        }
-      }
-    } else {
-      if (live && (f & 1u))
-        for (int k = kb; k < ke; ++k) a.out_peak[cand * a.P + ranks[k]] = -1;
-      if (wave == 0 && live) {
-        a.out_flags[cand] = (f & 1u) ? uint8_t(DIP_FLAG_INVALID) : uint8_t((f & 2u) ? DIP_FLAG_CAP : 0u);
-        if (f & 1u) {
-          a.out_ms[cand] = -1;
-          for (int q = 0; q < a.P; ++q) a.out_bub[cand * a.P + q] = -1;
-        }
+    if (live && (f & 1u))
+      for (int k = kb; k < ke; ++k) a.out_peak[cand * a.P + ranks[k]] = -1;
+    if (wave == 0 && live) {
+      a.out_flags[cand] = (f & 1u) ? uint8_t(DIP_FLAG_INVALID) : uint8_t((f & 2u) ? DIP_FLAG_CAP : 0u);
+      if (f & 1u) {
+        a.out_ms[cand] = -1;
+        for (int q = 0; q < a.P; ++q) a.out_bub[cand * a.P + q] = -1;
       }
     }
     __syncthreads();   // the flag words are cleared for the next tile
+  }
+}
+
+// -------------------------------------------------------------- order check
+// An op whose predecessor runs on its own rank must come after it in the
+// rank's order; if it comes first, the two wait for each other (the data edge
+// one way, the order the other) and the candidate deadlocks: its makespan and
+// bubbles are -1 and the deadlock flag is added.  One wave per (candidate,
+// rank) section of the ranks that have such ops, a block per rank and chunk of
+// candidates.  The main check has verified that a section is a permutation
+// (candidates it found invalid are skipped), so the wave can write each id's
+// position into a table, its inverse permutation, and then compare, for every
+// op with an own-rank predecessor, the two positions: no test depends on the
+// order in which the lanes take the ids.
+
+__device__ __forceinline__ uint32_t id_of(const uint4 &v, int q) {
+  const uint32_t w = q < 2 ? v.x : q < 4 ? v.y : q < 6 ? v.z : v.w;
+  return (q & 1) ? (w >> 16) : (w & 0xffffu);
+}
+
+// steps of 64 units of a section held in registers between the two passes
+// (longer sections read the rest again)
+constexpr int kOrderRegSteps = 4;
+
+__global__ __launch_bounds__(1024) void order_check_kernel(OrderCheckArgs a) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const uint32_t k = blockIdx.x >> 3;
+  const int r = a.ranks[k % uint32_t(a.n_ranks)];
+  const int64_t chunk = int64_t(k / uint32_t(a.n_ranks)) * 8 + (blockIdx.x & 7);
+  if (chunk >= a.n_chunks) return;
+  const int rb = a.rank_off[r], re = a.rank_off[r + 1];
+  const int nr = re - rb;
+  // the rank's predecessors (local id + 1, 0: none), entry nr 0; the wave's
+  // positions table
+  uint16_t *spl = reinterpret_cast<uint16_t *>(c_lds);
+  uint16_t *pos = reinterpret_cast<uint16_t *>(c_lds + a.tab_bytes + wave * a.wave_bytes);
+  {
+    const int nt = a.wpb * kWave;
+    for (int i = threadIdx.x; i <= nr; i += 4 * nt) {
+      int32_t sp[4];
+#pragma unroll
+      for (int t = 0; t < 4; ++t) sp[t] = i + t * nt < nr ? a.selfp[rb + i + t * nt] : 0;
+#pragma unroll
+      for (int t = 0; t < 4; ++t)
+        if (i + t * nt <= nr) spl[i + t * nt] = uint16_t(sp[t]);
+    }
+  }
+  __syncthreads();
+  if (nr == 0) return;
+
+  const int u0 = rb >> 3;
+  const int u_last = (re - 1) >> 3;
+  const int nu = u_last - u0 + 1;   // units of 8 ids touching the section
+  const int ns = (nu + kWave - 1) / kWave;
+  const int64_t c0 = chunk * int64_t(a.wpb) * a.per_wave + wave;
+  for (int i = 0; i < a.per_wave; ++i) {
+    const int64_t cand = c0 + int64_t(i) * a.wpb;
+    if (cand >= a.n_cand) break;
+    if (__builtin_amdgcn_readfirstlane(a.out_flags[cand]) & DIP_FLAG_INVALID) continue;
+    const uint4 *row = reinterpret_cast<const uint4 *>(a.orders + cand * a.stride);
+    auto unit_of = [&](int s) { return u0 + s * kWave + lane; };
+    auto load = [&](int s) { return row[min(unit_of(s), u_last)]; };
+    uint4 v[kOrderRegSteps];
+#pragma unroll
+    for (int s = 0; s < kOrderRegSteps; ++s)
+      if (s < ns) v[s] = load(s);
+    // positions (positions outside the section and ids out of range, which
+    // a valid section has none of, go to entry nr)
+    auto place = [&](const uint4 &w, int s) {
+      const int u = unit_of(s);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int p = 8 * u + q - rb;
+        const bool in = p >= 0 && p < nr;
+        pos[in ? min(id_of(w, q), uint32_t(nr)) : uint32_t(nr)] = uint16_t(p);
+      }
+    };
+#pragma unroll
+    for (int s = 0; s < kOrderRegSteps; ++s)
+      if (s < ns) place(v[s], s);
+    for (int s = kOrderRegSteps; s < ns; ++s) place(load(s), s);
+    wave_lds_order();
+    // (the units pass an empty asm statement, so that the second pass
+    // decodes them again instead of keeping the first pass's 64 indices)
+#pragma unroll
+    for (int s = 0; s < kOrderRegSteps; ++s)
+      asm volatile("" : "+v"(v[s].x), "+v"(v[s].y), "+v"(v[s].z), "+v"(v[s].w));
+    bool late = false;
+    auto test = [&](const uint4 &w, int s) {
+      const int u = unit_of(s);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const int p = 8 * u + q - rb;
+        const bool in = p >= 0 && p < nr;
+        const uint32_t sp = spl[in ? min(id_of(w, q), uint32_t(nr)) : uint32_t(nr)];
+        if (sp != 0u) late = late || int(pos[sp - 1u]) > p;
+      }
+    };
+#pragma unroll
+    for (int s = 0; s < kOrderRegSteps; ++s)
+      if (s < ns) test(v[s], s);
+    for (int s = kOrderRegSteps; s < ns; ++s) test(load(s), s);
+    if (__builtin_amdgcn_ballot_w64(late) != 0ull) {
+      if (lane == 0) {
+        a.out_flags[cand] = uint8_t(a.out_flags[cand] | DIP_FLAG_DEADLOCK);
+        a.out_ms[cand] = -1;
+      }
+      for (int q = lane; q < a.P; q += kWave) a.out_bub[cand * a.P + q] = -1;
+    }
+    wave_lds_order();   // this section's positions are read before the next one's are written
   }
 }
 
@@ -381,17 +483,18 @@ hipError_t launch_check(int, int blocks, int wpb, size_t lds, hipStream_t s, con
   return hipGetLastError();
 }
 
-const void *tile_check_kernel_ptr(bool order) {
-  return order ? reinterpret_cast<const void *>(tile_check_kernel<true>)
-               : reinterpret_cast<const void *>(tile_check_kernel<false>);
+const void *tile_check_kernel_ptr() { return reinterpret_cast<const void *>(tile_check_kernel); }
+
+hipError_t launch_tile_check(int blocks, int nw, size_t lds, hipStream_t s, const TileCheckArgs &a) {
+  tile_check_kernel<<<dim3(blocks), dim3(nw * kWave), lds, s>>>(a);
+  return hipGetLastError();
 }
 
-hipError_t launch_tile_check(int blocks, int nw, size_t lds, hipStream_t s, const TileCheckArgs &a,
-                             bool order) {
-  if (order)
-    tile_check_kernel<true><<<dim3(blocks), dim3(nw * kWave), lds, s>>>(a);
-  else
-    tile_check_kernel<false><<<dim3(blocks), dim3(nw * kWave), lds, s>>>(a);
+const void *order_check_kernel_ptr() { return reinterpret_cast<const void *>(order_check_kernel); }
+
+hipError_t launch_order_check(int64_t blocks, int wpb, size_t lds, hipStream_t s,
+                              const OrderCheckArgs &a) {
+  order_check_kernel<<<dim3(uint32_t(blocks)), dim3(wpb * kWave), lds, s>>>(a);
   return hipGetLastError();
 }
 

@@ -42,6 +42,27 @@ def assert_same(got, want, idx=None):
 SMALL = {1: 1024, 2: 4099, 3: 515, 4: 259, 5: 67}
 
 
+def own_rank_swap(prob, row, r, rng):
+    """Swap, in rank r's section of row, an op that has a predecessor on its
+    own rank with that predecessor's position, if the predecessor comes first
+    (the op then comes first: the two wait for each other)."""
+    b, e = int(prob.rank_off[r]), int(prob.rank_off[r + 1])
+    sec = row[b:e]
+    where = {int(x): q for q, x in enumerate(sec)}
+    swaps = []
+    for q, lid in enumerate(sec):
+        if not 0 <= int(lid) < e - b:
+            continue
+        g = b + int(lid)
+        for k in range(prob.pred_ptr[g], prob.pred_ptr[g + 1]):
+            p = int(prob.pred_op[k])
+            if b <= p < e and where.get(p - b, e) < q:
+                swaps.append((q, where[p - b]))
+    if swaps:
+        q, pq = swaps[int(rng.integers(len(swaps)))]
+        sec[q], sec[pq] = sec[pq], sec[q]
+
+
 @pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
 def test_parity_small_all_variants(cid):
     """Every config at an oracle-friendly size with a ragged tail, under every
@@ -125,8 +146,9 @@ def test_pool_fallback_when_pools_fill():
 
 @pytest.mark.parametrize("cid", [1, 2, 3, 4, 5])
 def test_check_kernels_caps_and_invalid_ids(cid):
-    """Both kernels of the order-only verdict (one wave per candidate; tiles of
-    64 candidates with the ranks split between the waves of a block) against
+    """Both kernels of the order-only verdict (one wave per candidate; tiles
+    of 64 candidates with the ranks split between the waves of a block, then
+    the own-rank order kernel) against
     the oracle, with per-rank caps at the median peak (so some candidates are
     capped and some are not) and ids out of range (n_r itself, the overflow
     bit of the tile kernel), negative or repeated, planted on random ranks and
@@ -140,7 +162,8 @@ def test_check_kernels_caps_and_invalid_ids(cid):
     prob = dataclasses.replace(prob, mem_cap=cap)
     rng = np.random.default_rng(cid)
     P, ro = prob.n_ranks, prob.rank_off
-    for i in rng.choice(n, size=max(3, n // 16), replace=False):
+    planted = rng.choice(n, size=max(3, n // 16), replace=False)
+    for i in planted:
         r = int(rng.integers(P)) if i % 2 else P - 1
         b, e = int(ro[r]), int(ro[r + 1])
         p = int(rng.integers(b, e))
@@ -150,6 +173,12 @@ def test_check_kernels_caps_and_invalid_ids(cid):
             rows[i, p] = -1 - int(rng.integers(100))
         else:
             rows[i, p] = rows[i, b if p != b else e - 1]
+    # ops moved before their own-rank predecessor on the last rank (the loss
+    # turnaround), on rows that hold no planted id
+    planted = set(int(i) for i in planted)
+    for i in range(n):
+        if i % 4 == 3 and i not in planted:
+            own_rank_swap(prob, rows[i], P - 1, rng)
     want = O.evaluate(prob, rows, threads=16)
     assert (want.flags & O.FLAG_INVALID).any() and (want.flags & O.FLAG_CAP).any()
     sim = dip.Sim(prob)
