@@ -145,32 +145,30 @@ int dip_sim_check_costs(const dip_topology *topo, const dip_costs *costs);
 int dip_sim_create(const dip_topology *topo, dip_sim **out);
 
 /* Force a kernel variant (0 = automatic choice) and waves per block
- * (0 = automatic; 1, 2 or 4, and 8 for the pool kernel when its tables fit in
- * LDS).  DIP_E_UNSUPPORTED if the variant does not fit the device
- * or the topology.  General kernels (any dependence DAG): 1 tables, orders
- * and end times in LDS; 2 tables in global memory, orders and end times in
- * LDS; 3 end times in LDS only; 4 nothing in LDS (end times in device
- * scratch).  Pipeline kernels (every op with several predecessors has them
- * all on one rank, and every op feeds at most one such op): 5 end times and
- * orders in LDS, op records read through the caches; 6 end times in device
- * scratch; 7 end times, orders and op records in LDS.  Variants 5 and 7 also
- * need every edge latency below 2^16, and all pipeline kernels need the sum
- * of all costs below 2^30, at evaluate time; when the costs do not allow the
- * configured pipeline kernel, evaluate runs the automatically chosen general
- * kernel instead (dip_sim_get_info reports the one that runs).
- * Variant 8 (the automatic choice when the topology allows it: at most 15
- * consumers per op and E < 2^24): a check
- * kernel (permutation, peak memory, cap) followed by the pool kernel, which
- * hands end times between ranks through per-rank pools of a few slots, and by
- * the variant-4 kernel for the candidates whose pools filled up (results are
- * the same either way). */
+ * (0 = automatic; 1, 2, 4 or 8, and 16 for variant 9).  DIP_E_UNSUPPORTED if
+ * the variant does not fit the device or the topology.
+ * General kernels (any dependence DAG): 1 tables, orders and end times in
+ * LDS; 2 tables in global memory, orders and end times in LDS; 3 end times
+ * in LDS only; 4 nothing in LDS (end times in device scratch).
+ * Variant 8 (at most 15 consumers per op, fewer than 2^16 extra edges): a
+ * check kernel (permutation, peak memory, cap) followed by the pool kernel,
+ * which hands end times between ranks through per-rank pools of a few
+ * slots, and by a general kernel for the candidates whose pools filled up.
+ * Variant 9 (the automatic choice where it fits: variant 8's topology limits,
+ * a power-of-two rank count and at most 8,192 ops per rank): the same check,
+ * then the simulation kernel with compact op records and the pools in LDS,
+ * a second pass of it with 16 slots per pool over the candidates whose pools
+ * filled, and a general kernel for those that filled again.  Costs that do
+ * not fit its records (a cost of 2^20 or more, a latency of 2^11 or more)
+ * run variant 8 for that call.  Otherwise a general kernel is chosen.
+ * Results are the same whichever kernel runs. */
 int dip_sim_configure(dip_sim *h, int32_t variant, int32_t waves_per_block);
 
-/* Variant 8: end-time slots per rank pool, 4, 8 or 16 (0 = automatic: 8,
- * doubled for later calls when a call sent more than 1/256 of its candidates
- * to the retry kernel).  Fewer slots keep more candidates resident; a
- * candidate whose pools fill up is re-simulated by the general kernel, so
- * results never depend on it.
+/* Variants 8 and 9: end-time slots per rank pool, 4, 8 or 16 (0 = automatic:
+ * 8), set at create time and by this call only, never by earlier calls.
+ * Fewer slots keep more candidates resident; a candidate whose pools fill up
+ * is re-simulated (variant 9: with 16 slots first, then by the general
+ * kernel; variant 8: by the general kernel), so results never depend on it.
  * DIP_E_UNSUPPORTED if the topology does not fit variant 8. */
 int dip_sim_configure_pool(dip_sim *h, int32_t slots_per_rank);
 

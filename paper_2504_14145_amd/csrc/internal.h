@@ -233,8 +233,9 @@ hipError_t launch_pool(int pwl, int slots, bool tab, int blocks, int wpb, size_t
 //
 // Record (8 bytes) of an op, relative to the op itself so that ops of
 // identically placed model chunks share records:
-//   w0 = cost (bits 0-19) | consumers (20-23) | several predecessors (24) |
-//        has predecessors (25)
+//   w0 = cost (bits 0-19) | consumers (20-23) | several predecessors (30) |
+//        has predecessors (31) (the top bits, so that each test is one
+//        compare: w0 < 0 as a signed word, and w0 >= both flags)
 //   w1 = the edge word of its only predecessor, or, with several, the index
 //        of its first edge word in the extra-edge table (the rest follow, the
 //        last one marked)
@@ -244,8 +245,8 @@ constexpr uint32_t kSimCostBits = 20;
 constexpr uint32_t kSimCostMax = (1u << kSimCostBits) - 1;
 constexpr uint32_t kSimCommMax = 2047;
 constexpr int32_t kSimDeltaMax = 8191;          // |pred local id - own local id|
-constexpr uint32_t kSimMulti = 1u << 24;
-constexpr uint32_t kSimHasPred = 1u << 25;
+constexpr uint32_t kSimMulti = 1u << 30;
+constexpr uint32_t kSimHasPred = 1u << 31;
 constexpr uint32_t kSimLast = 1u << 31;
 // ops per record page (paged tables: a rank's records come in pages of 16
 // consecutive local ids, equal pages stored once); the page map holds each

@@ -55,9 +55,6 @@ extern __shared__ __align__(16) unsigned char s_lds[];
 __device__ __forceinline__ uint32_t lds32(uint32_t a) {
   return *reinterpret_cast<const uint32_t *>(s_lds + a);
 }
-__device__ __forceinline__ uint32_t lds16(uint32_t a) {
-  return *reinterpret_cast<const uint16_t *>(s_lds + a);
-}
 __device__ __forceinline__ uint2 lds64(uint32_t a) {
   return *reinterpret_cast<const uint2 *>(s_lds + a);
 }
@@ -78,6 +75,23 @@ __device__ __forceinline__ void lds_add(uint32_t a, uint32_t v) {
 }
 __device__ __forceinline__ void lds_sub(uint32_t a, uint32_t v) {
   (void)__hip_atomic_fetch_sub(lds_word(a), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WAVEFRONT);
+}
+// LDS addresses as the hardware takes them (the dynamic array's own address
+// added), for values computed outside the helpers above
+typedef __attribute__((address_space(3))) unsigned char lds_byte_t;
+__device__ __forceinline__ uint32_t lds_abs(uint32_t a) {
+  return a + uint32_t(reinterpret_cast<uintptr_t>((lds_byte_t *)s_lds));
+}
+__device__ __forceinline__ uint32_t lds16_at(uint32_t abs_addr) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) uint16_t *>(uintptr_t(abs_addr));
+}
+// (x << s) + base in one instruction: written out, because the compiler
+// turns (i & m) << s into (i << s) & (m << s) and then needs a separate add
+template <int SH>
+__device__ __forceinline__ uint32_t shl_add(uint32_t x, uint32_t base) {
+  uint32_t d;
+  asm("v_lshl_add_u32 %0, %1, %2, %3" : "=v"(d) : "v"(x), "i"(SH), "v"(base));
+  return d;
 }
 __device__ __forceinline__ bool lane_in(uint64_t m) { return __builtin_amdgcn_inverse_ballot_w64(m); }
 __device__ __forceinline__ uint64_t ballot(bool b) { return __builtin_amdgcn_ballot_w64(b); }
@@ -160,19 +174,22 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
   // absolute row positions: past this lane's section, its last block
   const uint32_t a_end = uint32_t(rb + nr);
   const uint32_t blk_last = uint32_t(rb + max(nr - 1, 0)) / uint32_t(kSimBlockIds);
-  const uint32_t pmap_lane = a.off_pmap + 2u * uint32_t(recb);
+  const uint32_t pmap_lane = lds_abs(a.off_pmap + 2u * uint32_t(recb));
 
   // the record of local id `id` of this lane's rank
   auto rec_of = [&](uint32_t id) -> uint2 {
     uint32_t first;   // record index of the page's first op, or of the rank's
     if constexpr (PAGED) {
-      first = lds16(pmap_lane + (__builtin_amdgcn_ubfe(id, 4u, 12u) << 1)) + (id & 15u);
+      // (the page map holds multiples of 16: or-ing the offset in the page
+      // adds it)
+      first = lds16_at(shl_add<1>(id >> 4, pmap_lane)) | (id & 15u);
     } else {
       first = uint32_t(recb) + id;
     }
     return lds64(first << 3);
   };
-  auto ring_at = [&](uint32_t pos) { return my_ring + ((pos & 15u) << 1); };
+  const uint32_t my_ring_abs = lds_abs(my_ring);
+  auto ring_id = [&](uint32_t pos) { return lds16_at(shl_add<1>(pos & 15u, my_ring_abs)); };
 
   // candidates: positions k < n of the batch, or of the list in list mode
   const int64_t n_todo = a.list ? int64_t(*a.list_count) : a.n_cand;
@@ -202,7 +219,7 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     cur0 = c.x;
     ce = c.y;
     xi = c.y + 1u;
-    if (c.x & kSimMulti) ce = lds32(a.off_extra + 4u * c.y);
+    if (c.x >= (kSimHasPred | kSimMulti)) ce = lds32(a.off_extra + 4u * c.y);   // several predecessors
   };
 
   auto next_k = [&]() -> int64_t {
@@ -242,7 +259,7 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     for (uint32_t b = b0; b <= bn; ++b) store_block(my_ring + (b & 1u) * 16u, load_block(row, b));
     lb = bn + 1u;
     apos1 = uint32_t(rb) + 1u;
-    const uint32_t id0 = lds16(ring_at(uint32_t(rb)));
+    const uint32_t id0 = ring_id(uint32_t(rb));
     set_current(id0, rec_of(id0));
   };
 
@@ -250,7 +267,7 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
   {
     const bool live = has && on && nr > 0;
     m_live = ballot(live);
-    m_npend = m_live & ballot((cur0 & kSimHasPred) == 0);
+    m_npend = m_live & ballot(int32_t(cur0) >= 0);
   }
   uint64_t g_has = any_in_group<PWL>(ballot(has));
 
@@ -291,7 +308,7 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     uint32_t cnt[kC];
 #pragma unroll
     for (int i = 0; i < kC; ++i) cnt[i] = lds32(my_pool + 4u * i);
-    const uint32_t idn = lds16(ring_at(apos1));
+    const uint32_t idn = ring_id(apos1);
     // the next op's record, read ahead (used by the lanes that advance)
     const uint2 nrec = rec_of(idn);
 
@@ -364,14 +381,16 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
       ++apos1;
     }
     m_npend = ((m_npend & ~m_fire) | (m_found & m_last & ~m_fire) |
-               (m_adv & ballot((cur0 & kSimHasPred) == 0))) & ~m_fin;
+               (m_adv & ballot(int32_t(cur0) >= 0))) & ~m_fin;
     m_live &= ~m_fin;
 
     // ---- order blocks: every 4 rounds, a lane in the later of its two
     // blocks loads the one after it
     if (phase == 0u) {
-      const uint32_t cur_blk = (apos1 - 1u) / uint32_t(kSimBlockIds);
-      const bool load = lane_in(m_live) && lb <= blk_last && lb <= cur_blk + 1u;
+      // (the current op is at apos1 - 1 >= 0: its block plus one is
+      // (apos1 + 7) / 8)
+      const uint32_t next_blk = (apos1 + uint32_t(kSimBlockIds) - 1u) / uint32_t(kSimBlockIds);
+      const bool load = lane_in(m_live) && lb <= min(next_blk, blk_last);
       m_blk = ballot(load);
       if (load) blk = load_block(row, lb);
     }
@@ -417,7 +436,7 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
     // the restarted groups' lanes: live and edge state from their new records
     const bool live_new = has && on && nr > 0;
     m_live = (m_live & ~m_ev) | (m_ev & ballot(live_new));
-    m_npend = (m_npend & ~m_ev) | (m_ev & m_live & ballot((cur0 & kSimHasPred) == 0));
+    m_npend = (m_npend & ~m_ev) | (m_ev & m_live & ballot(int32_t(cur0) >= 0));
     m_blk &= ~m_ev;
     g_has = any_in_group<PWL>(ballot(has));
   }
