@@ -340,7 +340,7 @@ def main():
     nk = min(len(p) for p in per_kernel)
     kern_avg_ms = [sum(p[i] for p in per_kernel) / len(per_kernel) for i in range(nk)]
     names = {8: ["check", "simulate", "retry"],
-             9: ["check", "simulate", "simulate_16", "retry"]}.get(info["variant"],
+             9: ["check", "simulate", "simulate_16", "simulate_32", "retry"]}.get(info["variant"],
                                                                  ["simulate"])[:nk]
     dom = names.index("simulate")
     dom_s = kern_avg_ms[dom] / 1e3

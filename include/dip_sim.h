@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define DIP_SIM_ABI_VERSION 7
+#define DIP_SIM_ABI_VERSION 8
 
 enum {
   DIP_OK = 0,
@@ -158,16 +158,17 @@ int dip_sim_create(const dip_topology *topo, dip_sim **out);
  * a power-of-two rank count and at most 8,192 ops per rank): the same check,
  * then the simulation kernel with compact op records and the pools in LDS,
  * a second pass of it with 16 slots per pool over the candidates whose pools
- * filled, and a general kernel for those that filled again.  Costs that do
- * not fit its records (a cost of 2^20 or more, a latency of 2^11 or more)
- * run variant 8 for that call.  Otherwise a general kernel is chosen.
+ * filled, a third with 32 slots, and a general kernel for those that filled
+ * again.  Costs that do not fit its records (a cost of 2^20 or more, a
+ * latency of 2^11 or more) run variant 8 for that call.  Otherwise a general
+ * kernel is chosen.
  * Results are the same whichever kernel runs. */
 int dip_sim_configure(dip_sim *h, int32_t variant, int32_t waves_per_block);
 
 /* Variants 8 and 9: end-time slots per rank pool, 4, 8 or 16 (0 = automatic:
  * 8), set at create time and by this call only, never by earlier calls.
  * Fewer slots keep more candidates resident; a candidate whose pools fill up
- * is re-simulated (variant 9: with 16 slots first, then by the general
+ * is re-simulated (variant 9: with 16 and then 32 slots, then by the general
  * kernel; variant 8: by the general kernel), so results never depend on it.
  * DIP_E_UNSUPPORTED if the topology does not fit variant 8. */
 int dip_sim_configure_pool(dip_sim *h, int32_t slots_per_rank);
@@ -431,18 +432,21 @@ int dip_cost_tables(const dip_op_table *t, int64_t n_configs, const double *coef
  * later evaluate records HIP events on its stream around each kernel it
  * launches; dip_sim_last_profile then waits for the last of them and writes
  * the kernel times in milliseconds, in launch order, to out_ms[0 .. *n_out-1]
- * (n_out <= 4: variant 8 launches the check, pool and retry kernels;
- * variant 9 the check kernel, the simulation kernel, its second pass with
- * 16-slot pools over the candidates whose pools filled, and the retry
- * kernel; variants 1-4 one kernel; dip_sim_greedy records its two launches
- * the same way).  *n_out = 0 if the last evaluate recorded nothing. */
+ * (out_ms must hold DIP_SIM_PROFILE_MAX floats; n_out <= 5: variant 8 launches the check, pool and retry kernels;
+ * variant 9 the check kernel, the simulation kernel, its passes with 16-
+ * and 32-slot pools over the candidates whose pools filled (a pass that
+ * does not run reports about 0), and the retry kernel; variants 1-4 one
+ * kernel; dip_sim_greedy records its two launches the same way).  *n_out = 0
+ * if the last evaluate recorded nothing. */
+#define DIP_SIM_PROFILE_MAX 8
 int dip_sim_profile(dip_sim *h, int32_t enable);
 int dip_sim_last_profile(dip_sim *h, float *out_ms, int32_t *n_out);
 
 /* Diagnostics of the last evaluate (variants 8 and 9): *out_first = the
  * candidates whose pools filled in the first simulation pass; *out_second =
- * those left to the general kernel (variant 9: the ones its second pass, with
- * 16-slot pools, could not finish either).  Waits for that call's stream. */
+ * those left to the general kernel (variant 9: the ones its passes with 16-
+ * and 32-slot pools could not finish either).  Waits for that call's
+ * stream. */
 int dip_sim_last_retries(dip_sim *h, int64_t *out_first, int64_t *out_second);
 
 /* Release the handle's device memory.  Waits for the device first. */

@@ -22,6 +22,7 @@ OK = 0
 E_INVAL, E_TOPO, E_RANGE, E_UNSUPPORTED, E_NOMEM, E_HIP, E_STATE, E_CAPACITY = (
     -1, -2, -3, -4, -5, -6, -7, -8)
 STATIC_MAX_CAND = 1 << 22
+PROFILE_MAX = 8   # DIP_SIM_PROFILE_MAX: entries dip_sim_last_profile may write
 FLAG_DEADLOCK, FLAG_CAP, FLAG_INVALID = 1, 2, 4
 NO_KEY = (1 << 64) - 1
 
@@ -213,7 +214,7 @@ def profile(h, enable: bool = True) -> int:
 
 def last_profile(h) -> list:
     """Kernel times (ms) of the last evaluate, in launch order."""
-    buf = (ctypes.c_float * 4)()
+    buf = (ctypes.c_float * PROFILE_MAX)()
     n = ctypes.c_int32(0)
     _check(load().dip_sim_last_profile(h, buf, ctypes.byref(n)), "dip_sim_last_profile")
     return [float(buf[i]) for i in range(n.value)]

@@ -360,7 +360,7 @@ namespace {
 // Device memory an evaluate call works in beyond its inputs and outputs: the
 // retry counters and the two retry lists (variants 8 and 9).
 struct CallScratch {
-  uint32_t *counts;   // [4] zeroed by the check kernel
+  uint32_t *counts;   // [kRetryCounters] zeroed by the check kernel
   int64_t *list_a;    // [n_cand] first pass retries
   int64_t *list_b;    // [n_cand] second pass retries (variant 9)
 };
@@ -421,7 +421,7 @@ int evaluate_impl(dip_sim *h, const dip_costs *costs, const int16_t *orders, int
     const int64_t *retry_list = sx->list_a;
     const uint32_t *retry_count = counts;
     h->last_stream = stream;
-    h->last_pass2 = false;
+    h->last_general = 0;
     if (h->variant == 9 && h->sim_costs_ok) {
       SimArgs a{};
       a.orders = orders;
@@ -448,23 +448,34 @@ int evaluate_impl(dip_sim *h, const dip_costs *costs, const int16_t *orders, int
       DIP_HIP(launch_sim(h->pwl, h->pool_slots, h->sim_paged, blocks, h->sim_wpb,
                          size_t(h->sim_lds), stream, a));
       DIP_HIP(mark(2));
-      if (h->sim2_ok) {
-        // the candidates whose pools filled, again with 16 slots per pool
-        // (deadlocked orders fill small pools too; larger ones tell them
-        // from merely crowded ones); its own retries go to the general kernel
-        a.list = sx->list_a;
-        a.list_count = counts;
-        a.retry = sx->list_b;
-        a.retry_count = counts + 2;
-        a.wpb = h->sim2_wpb;
-        a.static_end = INT64_MAX;
-        DIP_HIP(launch_sim(h->pwl, 16, h->sim_paged, h->sim2_max_blocks, h->sim2_wpb,
-                           size_t(h->sim2_lds), stream, a));
-        retry_list = sx->list_b;
-        retry_count = counts + 2;
-        h->last_pass2 = true;
-      }
+      // The candidates whose pools filled, again with 16 and then 32 slots
+      // per pool (deadlocked orders fill small pools too; larger ones tell
+      // them from merely crowded ones), each pass in list mode over the
+      // previous one's retries, the two lists taking turns; what the last
+      // pass leaves goes to the general kernel.  (A pass that does not run
+      // still records its event: the profile keeps one entry per pass.)
+      auto pass = [&](bool run, int slots, int wpb, int max_blocks, int64_t lds, int next) -> int {
+        if (run) {
+          int64_t *out = retry_list == sx->list_a ? sx->list_b : sx->list_a;
+          a.list = retry_list;
+          a.list_count = retry_count;
+          a.retry = out;
+          a.retry_count = counts + next;
+          a.wpb = wpb;
+          a.static_end = INT64_MAX;
+          DIP_HIP(launch_sim(h->pwl, slots, h->sim_paged, max_blocks, wpb, size_t(lds), stream, a));
+          retry_list = out;
+          retry_count = counts + next;
+          h->last_general = next;
+        }
+        return DIP_OK;
+      };
+      if ((rc = pass(h->sim2_ok, 16, h->sim2_wpb, h->sim2_max_blocks, h->sim2_lds, 2)) != DIP_OK)
+        return rc;
       DIP_HIP(mark(3));
+      if ((rc = pass(h->sim3_ok, 32, h->sim3_wpb, h->sim3_max_blocks, h->sim3_lds, 4)) != DIP_OK)
+        return rc;
+      DIP_HIP(mark(4));
     } else {
       PoolArgs a{};
       a.orders = orders;
@@ -629,10 +640,10 @@ int dip_sim_last_retries(dip_sim *h, int64_t *out_first, int64_t *out_second) {
   *out_first = *out_second = 0;
   if (h->variant < 8 || !h->last_counts) return DIP_OK;
   DIP_HIP(hipStreamSynchronize(h->last_stream));
-  uint32_t cnt[4] = {0, 0, 0, 0};
+  uint32_t cnt[kRetryCounters] = {};
   DIP_HIP(hipMemcpy(cnt, h->last_counts, sizeof(cnt), hipMemcpyDeviceToHost));
   *out_first = cnt[0];
-  *out_second = h->last_pass2 ? cnt[2] : cnt[0];
+  *out_second = cnt[h->last_general];
   return DIP_OK;
 }
 

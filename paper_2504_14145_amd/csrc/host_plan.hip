@@ -366,7 +366,7 @@ int run_wave_check(dip_sim *h, const int16_t *orders, int64_t n_cand, int32_t *o
 }
 
 int ensure_retry(dip_sim *h, int64_t n) {
-  if (!h->d_retry_count) DIP_HIP(hipMalloc(&h->d_retry_count, 16));
+  if (!h->d_retry_count) DIP_HIP(hipMalloc(&h->d_retry_count, kRetryCounters * 4));
   if (n <= h->retry_cap) return DIP_OK;
   if (h->d_retry) {
     DIP_HIP(hipDeviceSynchronize());
@@ -466,10 +466,13 @@ bool sim_shape(dip_sim *h, int slots, int forced_wpb, int *wpb, int *max_blocks,
   return true;
 }
 
-// Both passes' shapes; sim_costs_ok false when the first does not fit.
+// The passes' shapes (the configured pools, then 16 and 32 slots for the
+// candidates whose pools filled); sim_costs_ok false when the first does not
+// fit.
 int sim_plan(dip_sim *h) {
   h->sim_costs_ok = false;
   h->sim2_ok = false;
+  h->sim3_ok = false;
   h->sim_state_base = int64_t(h->sim_tab_vec) * 16;
   if (!sim_shape(h, h->pool_slots, h->forced_variant == 9 ? h->forced_wpb : 0, &h->sim_wpb,
                  &h->sim_max_blocks, &h->sim_lds))
@@ -477,6 +480,7 @@ int sim_plan(dip_sim *h) {
   h->sim_costs_ok = true;
   if (h->pool_slots < 16)
     h->sim2_ok = sim_shape(h, 16, 0, &h->sim2_wpb, &h->sim2_max_blocks, &h->sim2_lds);
+  h->sim3_ok = sim_shape(h, 32, 0, &h->sim3_wpb, &h->sim3_max_blocks, &h->sim3_lds);
   return DIP_OK;
 }
 

@@ -106,10 +106,14 @@ struct dip_sim {
   int sim2_wpb = 1, sim2_max_blocks = 1;
   int64_t sim2_lds = 0;
   int64_t *d_retry2 = nullptr;         // candidates the second pass could not hold
+  // third pass over what the earlier ones could not hold, with 32-slot pools
+  bool sim3_ok = false;
+  int sim3_wpb = 1, sim3_max_blocks = 1;
+  int64_t sim3_lds = 0;
   hipStream_t last_stream = nullptr;   // stream of the last evaluate (diagnostics)
   uint32_t *last_counts = nullptr;     // its retry counters
   void *d_static = nullptr;            // this device's address of the static scratch array
-  bool last_pass2 = false;             // it ran the second simulation pass
+  int last_general = 0;                // counter (index) of the list its general kernel took
   int4 *d_pool_rec = nullptr;          // pool records [N][2]
   int2 *d_pool_edge = nullptr;         // pool edges [E]
   int64_t *d_retry = nullptr;          // candidates re-run by the general kernel
@@ -156,7 +160,7 @@ struct dip_sim {
   hipEvent_t stage_done = nullptr;
   // optional per-kernel timing of evaluate: events before each kernel and after the last
   bool profile = false;
-  hipEvent_t prof_ev[5] = {nullptr, nullptr, nullptr, nullptr, nullptr};
+  hipEvent_t prof_ev[6] = {nullptr, nullptr, nullptr, nullptr, nullptr, nullptr};
   int prof_n = 0;                      // events recorded by the last evaluate
   bool stage_pending = false;
   bool costs_set = false;

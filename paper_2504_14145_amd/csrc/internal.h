@@ -55,6 +55,11 @@ const void *general_kernel_ptr(int variant);
 hipError_t launch_general(int variant, int blocks, int wpb, size_t lds, hipStream_t s,
                           const GeneralArgs &a);
 
+// Counters of one evaluate call, zeroed by its check kernel: per simulation
+// pass (8, 16 and 32 slots) the count of its retry list and its on-demand
+// candidate counter
+constexpr int kRetryCounters = 8;
+
 // ---------------------------------------------------------------- check
 // Order-only verdict of each candidate: permutation check, per-rank peak
 // memory, cap flag (one wavefront per candidate; an op-id bitmap in LDS).
@@ -70,9 +75,9 @@ struct CheckArgs {
   const int32_t *rank_off;  // [P+1]
   const int32_t *cap;       // [P]
   int32_t P, N, wpb;
-  uint32_t *retry_count;    // [4] zeroed by the kernel when not null (retry
-                            // counts and the on-demand candidate counter of
-                            // the simulation passes)
+  uint32_t *retry_count;    // [kRetryCounters] zeroed by the kernel when not
+                            // null (retry counts and on-demand candidate
+                            // counters of the simulation passes)
 };
 
 // bytes of one candidate's op-id bitmap
@@ -100,9 +105,9 @@ struct TileCheckArgs {
   int32_t P, nw;
   int32_t md_bytes;         // bytes of a wave's delta area (16-aligned)
   int32_t region_bytes;     // bytes per wave: delta area + bitmap of 64 lanes
-  uint32_t *retry_count;    // [4] zeroed by the kernel when not null (retry
-                            // counts and the on-demand candidate counter of
-                            // the simulation passes)
+  uint32_t *retry_count;    // [kRetryCounters] zeroed by the kernel when not
+                            // null (retry counts and on-demand candidate
+                            // counters of the simulation passes)
 };
 
 // LDS of a tile-check block: the 64 candidates' flag words, then the waves'

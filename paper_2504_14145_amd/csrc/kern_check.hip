@@ -65,7 +65,7 @@ __global__ __launch_bounds__(256) void check_kernel(CheckArgs a) {
   const int wave = threadIdx.x / kWave;
   const int wpw = int(check_lds_per_group(a.N) / 4);
   uint32_t *bm = reinterpret_cast<uint32_t *>(c_lds) + wave * wpw;
-  if (a.retry_count && blockIdx.x == 0 && threadIdx.x < 4) a.retry_count[threadIdx.x] = 0u;
+  if (a.retry_count && blockIdx.x == 0 && threadIdx.x < kRetryCounters) a.retry_count[threadIdx.x] = 0u;
 
   const int cap_l = lane < a.P ? a.cap[lane] : -1;
   // section offsets in a register, lane k holding rank_off[k] (read with
@@ -187,7 +187,7 @@ __global__ __launch_bounds__(kTileMaxWaves * kWave) void tile_check_kernel(TileC
   // k ^ (l & 7) of the row's 8, so the reads of one unit by 8 lanes hit 8
   // distinct bank groups
   unsigned char *stg = region + a.region_bytes - kTileStageBytes;
-  if (a.retry_count && blockIdx.x == 0 && threadIdx.x < 4) a.retry_count[threadIdx.x] = 0u;
+  if (a.retry_count && blockIdx.x == 0 && threadIdx.x < kRetryCounters) a.retry_count[threadIdx.x] = 0u;
 
   const int kb = a.plan[wave], ke = a.plan[wave + 1];
   const int32_t *ranks = a.plan + a.nw + 1;

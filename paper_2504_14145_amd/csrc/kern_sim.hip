@@ -144,7 +144,7 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
   constexpr uint32_t kEndAt = 4u * uint32_t(kC);      // end times after a pool's counts
   constexpr uint32_t kRing = uint32_t(sim_ring_offset(PW, S));
   constexpr uint32_t kGroup = uint32_t(sim_group_bytes(PW, S));
-  static_assert(S == 4 || S == 8 || S == 16, "pool size");
+  static_assert(S == 4 || S == 8 || S == 16 || S == 32, "pool size");
 
   // the tables into LDS, once per block
   for (int i = threadIdx.x; i < a.tab_vec; i += blockDim.x)
@@ -473,6 +473,7 @@ const void *ptr_p(int pwl, int slots) {
   switch (slots) {
     case 4: return ptr_s<4, PAGED>(pwl);
     case 16: return ptr_s<16, PAGED>(pwl);
+    case 32: return ptr_s<32, PAGED>(pwl);
     default: return ptr_s<8, PAGED>(pwl);
   }
 }
@@ -483,6 +484,7 @@ void launch_p(int pwl, int slots, dim3 grid, dim3 block, size_t lds, hipStream_t
   switch (slots) {
     case 4: launch_s<4, PAGED>(pwl, grid, block, lds, s, a); break;
     case 16: launch_s<16, PAGED>(pwl, grid, block, lds, s, a); break;
+    case 32: launch_s<32, PAGED>(pwl, grid, block, lds, s, a); break;
     default: launch_s<8, PAGED>(pwl, grid, block, lds, s, a); break;
   }
 }

@@ -27,7 +27,13 @@ def test_library_exports_every_declared_symbol():
     for n in names:
         assert hasattr(lib, n), n
     assert set(names) == set(dip.EXPORTS)
-    assert lib.dip_sim_abi_version() == 7
+    assert lib.dip_sim_abi_version() == 8
+
+
+def test_binding_constants_match_header():
+    text = open(HEADER).read()
+    assert int(re.search(r"#define DIP_SIM_PROFILE_MAX (\d+)", text).group(1)) == dip.PROFILE_MAX
+    assert int(re.search(r"#define DIP_SIM_ABI_VERSION (\d+)", text).group(1)) == 8
 
 
 def test_strerror_strings():

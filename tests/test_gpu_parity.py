@@ -225,6 +225,34 @@ def test_check_kernels_empty_rank():
     sim.close()
 
 
+def test_retry_passes_16_and_32_slots():
+    """Candidates whose pools fill go through the passes with 16 and then 32
+    slots per pool before the general kernel; with 4 and 8 slots in the first
+    pass on the 32-rank diffusion workload (a third of its orders deadlock,
+    and deadlocked orders fill small pools), every output still equals the
+    oracle's and the passes leave next to nothing to the general kernel."""
+    need_gpu()
+    prob = W.make_problem(4)
+    n = 3000
+    rows = W.generator_for(prob, 4).generate(11, n)
+    want = O.evaluate(prob, rows, threads=16)
+    sim = dip.Sim(prob)
+    dip.profile(sim.h, True)
+    for slots in (4, 8):
+        assert sim.configure_pool(slots) == dip.OK
+        got = run_gpu(sim, rows)
+        first, left = dip.last_retries(sim.h)
+        times = dip.last_profile(sim.h)
+        print(f"slots {slots}: first-pass retries {first}, left to the general kernel {left}, "
+              f"kernel ms {[round(t, 3) for t in times]}", flush=True)
+        assert_same(got, want)
+        assert first > 0 and left <= first // 20
+        if sim.info["variant"] == 9:
+            assert len(times) == 5
+    dip.profile(sim.h, False)
+    sim.close()
+
+
 def test_parity_full_bench_workload():
     """The 8-stage VLM workload at its full 65,536 candidates, in the launch
     configuration the benchmark times, compared on every candidate, plus the
