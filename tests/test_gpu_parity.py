@@ -225,6 +225,83 @@ def test_check_kernels_empty_rank():
     sim.close()
 
 
+def with_microbatch_order(base, comm):
+    """The pipeline instance `base` (one unit per lane and microbatch, v = 1)
+    with an extra edge F(u, r) -> F(u + 1, r) on every rank r (latency
+    `comm`): every rank then has ops that wait on an op of their own rank."""
+    P, ro = base.n_ranks, np.asarray(base.rank_off)
+    preds = [list(base.pred_op[base.pred_ptr[g]:base.pred_ptr[g + 1]]) for g in range(int(ro[-1]))]
+    comms = [list(base.edge_comm[base.pred_ptr[g]:base.pred_ptr[g + 1]]) for g in range(int(ro[-1]))]
+    for r in range(P):
+        for lid in range(2, int(base.n_ops[r]), 2):   # F(u) at 2u, B(u) at 2u + 1
+            preds[ro[r] + lid].append(int(ro[r]) + lid - 2)
+            comms[ro[r] + lid].append(comm)
+    ptr = np.zeros(len(preds) + 1, base.pred_ptr.dtype)
+    ptr[1:] = np.cumsum([len(x) for x in preds])
+    return dataclasses.replace(base, pred_ptr=ptr,
+                               pred_op=np.array([q for x in preds for q in x], base.pred_op.dtype),
+                               edge_comm=np.array([c for x in comms for c in x], base.edge_comm.dtype))
+
+
+@pytest.mark.parametrize("comm", [0, 2])
+def test_own_rank_order_on_every_rank(comm):
+    """Every rank has ops that wait on an op of their own rank (the extra
+    microbatch-order edges, plus the loss turnaround on the last rank), so the
+    order kernel runs on all four ranks at once: orders that keep each F(u)
+    before F(u + 1) and orders that swap them, against the oracle, under both
+    check kernels and every variant that fits (with latency 0 the simulation
+    kernel drops these edges and relies on the order check; with latency 2 it
+    keeps them)."""
+    need_gpu()
+    rng = np.random.default_rng(40 + comm)
+    M = 12
+    base = W.compile_instance(W.pipeline_instance(4, M, rng.integers(5, 40, size=(4, M)), comm=3))
+    prob = with_microbatch_order(base, comm)
+    ro = np.asarray(prob.rank_off)
+    n = 700
+    rows = np.zeros((n, prob.stride), np.int16)
+    def one_f_one_b(d):
+        # d forwards first, then each backward followed by the next forward
+        ids = [2 * u for u in range(d)]
+        for k in range(M):
+            ids.append(2 * k + 1)
+            if k + d < M:
+                ids.append(2 * (k + d))
+        return np.array(ids, np.int16)
+    for i in range(n):
+        # warm-up depths that do not grow along the pipeline are deadlock free;
+        # on some rows one rank's depth exceeds its predecessor's (a cycle
+        # across ranks the simulation finds)
+        d = np.sort(rng.integers(1, M + 1, size=prob.n_ranks))[::-1].copy()
+        if i % 5 == 1:
+            r = int(rng.integers(1, prob.n_ranks))
+            d[r] = min(M, d[r - 1] + 1)
+        for r in range(prob.n_ranks):
+            rows[i, ro[r]:ro[r + 1]] = one_f_one_b(int(d[r]))
+        if i % 3 == 0:   # F(u + 1) moved before F(u) on one rank: an own-rank order violation
+            r = int(rng.integers(prob.n_ranks))
+            sec = rows[i, ro[r]:ro[r + 1]]
+            pairs = [q for q in range(len(sec) - 1) if sec[q] % 2 == 0 and sec[q + 1] == sec[q] + 2]
+            if pairs:
+                q = pairs[int(rng.integers(len(pairs)))]
+                sec[q], sec[q + 1] = sec[q + 1], sec[q]
+    want = O.evaluate(prob, rows, threads=16)
+    dead = np.mean(want.flags & O.FLAG_DEADLOCK > 0)
+    print(f"comm {comm}: deadlocked {dead:.2f}", flush=True)
+    assert 0.1 < dead < 0.9
+    sim = dip.Sim(prob)
+    tried = 0
+    for variant in (0, 3, 8, 9):
+        for mode in (1, 2):
+            if sim.configure(variant, 0) != dip.OK or sim.configure_check(mode) != dip.OK:
+                continue
+            print(f"variant {variant} check {mode}: {sim.info['variant']}", flush=True)
+            assert_same(run_gpu(sim, rows), want)
+            tried += 1
+    assert tried >= 4
+    sim.close()
+
+
 def test_retry_passes_16_and_32_slots():
     """Candidates whose pools fill go through the passes with 16 and then 32
     slots per pool before the general kernel; with 4 and 8 slots in the first
