@@ -213,6 +213,8 @@ def main():
     ap.add_argument("--variant", type=int, default=0)
     ap.add_argument("--wpb", type=int, default=0)
     ap.add_argument("--slots", type=int, default=0, help="pool slots per rank (pool kernel)")
+    ap.add_argument("--inbox", type=int, default=0,
+                    help="greedy: fix the first launch's inbox entries per kind (0: adaptive)")
     ap.add_argument("--cpu-seconds", type=float, default=6.0,
                     help="wall-time bound of each CPU oracle baseline leg (all cores, one core)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -495,6 +497,8 @@ def run_greedy(args, cfg):
     rc = sim.configure_greedy(G, op_group)
     if rc != dip.OK:
         raise SystemExit(f"greedy unsupported on {cfg.name}: {dip.strerror(rc)}")
+    if args.inbox and dip.set_greedy_inbox(sim.h, args.inbox) != dip.OK:
+        raise SystemExit(f"inbox size {args.inbox} not accepted")
     out = sim.outputs(n_cand)
     orders = torch.empty((n_cand, prob.stride), dtype=torch.int16, device=dev)
     key = torch.empty(1, dtype=torch.int64, device=dev)
@@ -507,9 +511,11 @@ def run_greedy(args, cfg):
 
     dip.greedy(sim.h, sim.costs, prio, n_cand, orders, *out, stream=stream)   # uploads costs
     torch.cuda.synchronize()
-    for _ in range(max(args.warmup, 2)):     # the inbox size settles within two calls
+    # the inbox size adapts to the overflow counts of earlier calls, each read
+    # once its call has finished: warm-up calls wait for the previous one
+    for _ in range(max(args.warmup, 6)):
         step()
-    torch.cuda.synchronize()
+        torch.cuda.synchronize()
     t_start = time.perf_counter()
     for _ in range(args.steps):
         step()

@@ -128,8 +128,9 @@ typedef struct {
   int32_t pool_slots;        /* variant 8: end-time slots per rank pool, else 0  */
   int32_t check_kernel;      /* variants 8, 9: 1 wave per candidate, 2 tiles,
                                 else 0                                         */
-  int32_t greedy_inbox;      /* dip_sim_greedy: stages a rank's inbox holds (0:
-                                not configured); grows when many overflow     */
+  int32_t greedy_inbox;      /* dip_sim_greedy: stages a rank's inbox holds in
+                                its first launch (0: not configured; -1: that
+                                launch is skipped); grows when many overflow  */
   int32_t greedy_lds_bytes;  /* dip_sim_greedy: LDS per block of its launch    */
   int64_t greedy_retry_ring_bytes; /* dip_sim_greedy: device memory holding the
                                 second launch's inboxes where LDS cannot, else 0 */
@@ -249,7 +250,10 @@ int dip_sim_configure_greedy(dip_sim *h, int32_t n_groups, const int32_t *op_gro
  * first launch (a candidate that overflows one is simulated again by the
  * second launch, whose inboxes hold a whole rank): k a power of two from 1 to
  * 256 fixes it; k = 0 restores the default, 8 to start with and doubled by
- * a later call when more than 1/64 of a call's candidates overflowed.
+ * a later call when more than 1/64 of a call's candidates overflowed, and,
+ * once more than half of a call's candidates overflow the largest inboxes
+ * that fit in LDS, later calls skip the first launch and give every
+ * candidate to the second.
  * Results do not depend on k.  DIP_E_STATE before dip_sim_configure_greedy,
  * DIP_E_INVAL for another k, DIP_E_UNSUPPORTED if the inboxes do not fit in
  * LDS.  Reset by dip_sim_configure_greedy. */

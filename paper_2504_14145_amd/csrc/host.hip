@@ -347,7 +347,7 @@ int dip_sim_get_info(const dip_sim *h, dip_sim_info *info) {
   info->scratch_bytes = h->scratch_gen_bytes + h->scratch_fb_bytes + h->retry_cap * 8;
   info->pool_slots = v >= 8 ? h->pool_slots : 0;
   info->check_kernel = v >= 8 ? check_kind(h) : 0;
-  info->greedy_inbox = h->gr_ok ? h->gr_K : 0;
+  info->greedy_inbox = h->gr_ok ? (h->gr_direct ? -1 : h->gr_K) : 0;
   info->greedy_lds_bytes = h->gr_ok ? int32_t(h->gr_main.lds) : 0;
   info->greedy_retry_ring_bytes = h->gr_ok ? h->gr_ring_bytes : 0;
   return DIP_OK;

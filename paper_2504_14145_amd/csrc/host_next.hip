@@ -139,6 +139,7 @@ int dip_sim_configure_greedy(dip_sim *h, int32_t n_groups, const int32_t *op_gro
   const int pwl = std::max(2, h->pwl);
   h->gr_K = 8;
   h->gr_K_fixed = false;
+  h->gr_direct = false;
   if (!greedy_layout(h, h->gr_K, pwl, &h->gr_main)) return DIP_E_UNSUPPORTED;
   // a stage joins its rank's inbox of its kind once, so a ring of a power
   // of two entries no fewer than the rank's stages of that kind never fills
@@ -219,12 +220,20 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
   }
   if (!h->d_gr_retry_count) DIP_HIP(hipMalloc(&h->d_gr_retry_count, 16));
   if (h->gr_seen_pending && hipEventQuery(h->gr_seen_ev) == hipSuccess) {
+    // an earlier call's overflow count: more than 1/64 of its candidates
+    // doubles the first launch's inboxes while they fit LDS; more than half of
+    // them at the largest inbox that fits makes later calls skip the first
+    // launch (it would run them all only for the second to run them again)
     h->gr_seen_pending = false;
     dip_sim::GrLaunch bigger;
-    if (!h->gr_K_fixed && h->gr_K < 256 && int64_t(*h->h_gr_seen) * 64 > h->gr_seen_n &&
-        greedy_layout(h, 2 * h->gr_K, h->gr_main.pwl, &bigger)) {
-      h->gr_K *= 2;
-      h->gr_main = bigger;
+    const int64_t seen = int64_t(*h->h_gr_seen);
+    if (!h->gr_K_fixed && seen * 64 > h->gr_seen_n) {
+      if (h->gr_K < 256 && greedy_layout(h, 2 * h->gr_K, h->gr_main.pwl, &bigger)) {
+        h->gr_K *= 2;
+        h->gr_main = bigger;
+      } else if (seen * 2 > h->gr_seen_n) {
+        h->gr_direct = true;
+      }
     }
   }
   (void)hipGetLastError();
@@ -235,7 +244,7 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
     return hipEventRecord(h->prof_ev[i], stream);
   };
   (void)hipGetLastError();
-  DIP_HIP(hipMemsetAsync(h->d_gr_retry_count, 0, 4, stream));
+  DIP_HIP(launch_zero_words(h->d_gr_retry_count, 1, stream));
   GreedyArgs a{};
   a.prio = prio;
   a.n_cand = n_cand;
@@ -278,16 +287,20 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
   const int64_t blocks = (n_cand + per_block - 1) / per_block;
   if (blocks > INT32_MAX) return DIP_E_INVAL;
   DIP_HIP(mark(0));
-  DIP_HIP(launch_greedy(h->gr_main.pwl, h->gr_nw, false, int(blocks), h->gr_main.wpb,
-                        size_t(h->gr_main.lds), stream, a));
+  if (!h->gr_direct)
+    DIP_HIP(launch_greedy(h->gr_main.pwl, h->gr_nw, false, int(blocks), h->gr_main.wpb,
+                          size_t(h->gr_main.lds), stream, a));
   DIP_HIP(mark(1));
-  // candidates whose inboxes overflowed, with inboxes as large as a rank
+  // candidates whose inboxes overflowed (or, skipping the first launch, all
+  // of them), with inboxes as large as a rank
   set_layout(h->gr_retry);
-  a.list = h->d_gr_retry;
-  a.list_count = h->d_gr_retry_count;
+  a.list = h->gr_direct ? nullptr : h->d_gr_retry;
+  a.list_count = h->gr_direct ? nullptr : h->d_gr_retry_count;
   a.retry = nullptr;
   a.retry_count = nullptr;
-  int64_t rb = std::min<int64_t>(int64_t(h->n_cu) * h->gr_retry.blocks_per_cu, blocks);
+  const int64_t per_block_r = int64_t(h->gr_retry.wpb) * (kWave >> h->gr_retry.pwl);
+  int64_t rb = std::min<int64_t>(int64_t(h->n_cu) * h->gr_retry.blocks_per_cu,
+                                 h->gr_direct ? (n_cand + per_block_r - 1) / per_block_r : blocks);
   if (h->gr_retry.gring) {
     rb = std::min<int64_t>(rb, h->gr_retry.max_blocks);   // one ring region per resident slot
     a.gring = h->d_gr_ring;
@@ -295,7 +308,7 @@ int dip_sim_greedy(dip_sim *h, const dip_costs *costs, const int32_t *prio, int6
   DIP_HIP(launch_greedy(h->gr_retry.pwl, h->gr_nw, h->gr_retry.gring, int(rb), h->gr_retry.wpb,
                         size_t(h->gr_retry.lds), stream, a));
   DIP_HIP(mark(2));
-  if (!h->gr_K_fixed && h->gr_K < 256 && !h->gr_seen_pending) {
+  if (!h->gr_K_fixed && !h->gr_direct && !h->gr_seen_pending) {
     if (!h->h_gr_seen) {
       DIP_HIP(hipHostMalloc(reinterpret_cast<void **>(&h->h_gr_seen), 16, hipHostMallocDefault));
       DIP_HIP(hipEventCreateWithFlags(&h->gr_seen_ev, hipEventDisableTiming));
@@ -317,6 +330,7 @@ int dip_sim_set_greedy_inbox(dip_sim *h, int32_t k) {
   h->gr_K = kk;
   h->gr_main = L;
   h->gr_K_fixed = k != 0;
+  h->gr_direct = false;
   return DIP_OK;
 }
 

@@ -199,6 +199,7 @@ struct dip_sim {
   // of its candidates needed the second launch
   int gr_K = 16;
   bool gr_K_fixed = false;             // dip_sim_set_greedy_inbox fixed it
+  bool gr_direct = false;              // later calls run only the whole-rank-inbox launch
   uint32_t *h_gr_seen = nullptr;       // pinned
   hipEvent_t gr_seen_ev = nullptr;
   bool gr_seen_pending = false;

@@ -369,6 +369,9 @@ struct GreedyArgs {
 constexpr uint32_t kGreedyNoStage = 0xffffu;
 // nw: bitmap words per kind (1, 2, 4, 8, 16, 32); gring: inboxes in device
 // memory (GreedyArgs::gring) rather than LDS
+// Zeroes n (<= 64) words: a kernel instead of a memset node, so that code a
+// caller captures into a HIP graph holds no memset.
+hipError_t launch_zero_words(uint32_t *p, int n, hipStream_t s);
 const void *greedy_kernel_ptr(int pwl, int nw, bool gring);
 hipError_t launch_greedy(int pwl, int nw, bool gring, int blocks, int wpb, size_t lds, hipStream_t s,
                          const GreedyArgs &a);

@@ -480,6 +480,15 @@ const void *ptr_pwl(int nw, bool gring) {
 
 }  // namespace
 
+__global__ void zero_words_kernel(uint32_t *p, int n) {
+  if (int(threadIdx.x) < n) p[threadIdx.x] = 0u;
+}
+
+hipError_t launch_zero_words(uint32_t *p, int n, hipStream_t s) {
+  zero_words_kernel<<<1, 64, 0, s>>>(p, n);
+  return hipGetLastError();
+}
+
 const void *greedy_kernel_ptr(int pwl, int nw, bool gring) {
   switch (pwl) {
     case 2: return ptr_pwl<2>(nw, gring);

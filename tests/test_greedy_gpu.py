@@ -127,6 +127,27 @@ def test_greedy_inbox_overflow_goes_through_retry():
     sim.close()
 
 
+def test_greedy_skips_first_launch_when_most_overflow():
+    """On the large 16 x 64-lane workload most candidates overflow even the
+    largest inboxes that fit in LDS: after a few calls the inboxes stop
+    growing and later calls give every candidate to the second launch
+    (greedy_inbox -1), with results equal to the oracle's on every call."""
+    need_gpu()
+    prob = W.make_problem(5)
+    g, G, cls = W.priority_groups(prob)
+    prio = W.rollout_priorities(cls, SMALL[5], seed=13)
+    sim = dip.Sim(prob)
+    assert sim.configure_greedy(G, g) == dip.OK
+    seen = []
+    for call in range(8):
+        check_against_oracle(prob, (g, G), prio, sim=sim, tag=f"large call {call}")
+        seen.append(sim.info["greedy_inbox"])
+    print(f"inbox after each call: {seen}", flush=True)
+    assert seen[-1] == -1
+    assert sim.set_greedy_inbox(0) == dip.OK and sim.info["greedy_inbox"] == 8
+    sim.close()
+
+
 @pytest.mark.parametrize("cid", [2, 3, 4, 5])
 def test_greedy_second_launch_for_every_candidate(cid):
     """Inboxes of one stage in the first launch: nearly every candidate
