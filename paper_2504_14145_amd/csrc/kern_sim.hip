@@ -193,7 +193,12 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
 
   // candidates: positions k < n of the batch, or of the list in list mode
   const int64_t n_todo = a.list ? int64_t(*a.list_count) : a.n_cand;
-  int64_t k = (int64_t(blockIdx.x) * a.wpb + wave) * G + grp;
+  // slot of this group: block-major for a batch (a block's groups take
+  // neighbouring candidates); in list mode, which carries few candidates,
+  // block-minor, so that they spread over the CUs instead of sharing the
+  // first few (either way a permutation of 0 .. n_slots - 1)
+  int64_t k = a.list ? (int64_t(grp) * a.wpb + wave) * gridDim.x + blockIdx.x
+                     : (int64_t(blockIdx.x) * a.wpb + wave) * G + grp;
   auto cand_at = [&](int64_t i) { return a.list ? a.list[i] : i; };
 
   // per-lane state
