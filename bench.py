@@ -213,6 +213,8 @@ def main():
     ap.add_argument("--variant", type=int, default=0)
     ap.add_argument("--wpb", type=int, default=0)
     ap.add_argument("--slots", type=int, default=0, help="pool slots per rank (pool kernel)")
+    ap.add_argument("--check", type=int, default=0,
+                    help="check kernel (dip_sim_configure_check mode; 0: automatic)")
     ap.add_argument("--inbox", type=int, default=0,
                     help="greedy: fix the first launch's inbox entries per kind (0: adaptive)")
     ap.add_argument("--cpu-seconds", type=float, default=6.0,
@@ -284,6 +286,10 @@ def main():
     torch.cuda.set_device(dev)
     orders = torch.from_numpy(rows).to(dev)
     sim = dip.Sim(prob)
+    if args.check:
+        rc = sim.configure_check(args.check)
+        if rc != dip.OK:
+            raise SystemExit(f"check kernel {args.check} unsupported: {dip.strerror(rc)}")
     if args.slots:
         rc = sim.configure_pool(args.slots)
         if rc != dip.OK:
