@@ -202,6 +202,51 @@ def cpu_oracle_baseline(prob, rows, seconds: float) -> dict:
             "cpu_model": cpu_model(), "host_cpus_visible": visible}
 
 
+# the candidates the oracle is timed on per workload: all of the three
+# smaller ones, fixed prefixes of the two larger
+ORACLE_PREFIX = {1: 1024, 2: 65536, 3: 262144, 4: 65536, 5: 16384}
+
+
+def run_oracle_timing(args):
+    """The CPU oracle alone (no GPU work): every workload's prefix on one
+    thread, then candidate-parallel on this process's share of the host's
+    cores, and what a full parity sweep of the workload takes at that rate."""
+    import numpy as np   # noqa: F401  (the generator's arrays)
+    import oracle
+    import workloads as W
+
+    visible = len(os.sched_getaffinity(0))
+    share = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    cores = max(1, min(visible, share) if share > 0 else visible)
+    per = {}
+    for cid in sorted(ORACLE_PREFIX):
+        cfg = W.get(cid)
+        prob = W.make_problem(cfg)
+        n = min(ORACLE_PREFIX[cid], args.n_cand or ORACLE_PREFIX[cid])
+        rows = W.generator_for(prob, cfg).generate(0, n)
+        t0 = time.perf_counter()
+        one = oracle.evaluate(prob, rows, threads=1)
+        t_one = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        par = oracle.evaluate(prob, rows, threads=cores)
+        t_all = time.perf_counter() - t0
+        assert (one.makespan == par.makespan).all() and (one.flags == par.flags).all()
+        ops = n * prob.n_total
+        per[cfg.name] = {
+            "candidates": n, "ops_per_candidate": int(prob.n_total),
+            "one_core": {"seconds": t_one, "candidates_per_s": n / t_one, "ops_per_s": ops / t_one},
+            "all_cores": {"threads": cores, "seconds": t_all, "candidates_per_s": n / t_all,
+                          "ops_per_s": ops / t_all},
+            "full_sweep_s_at_all_cores": cfg.n_cand / (n / t_all),
+        }
+        log(f"[bench] oracle on {cfg.name}: {n} candidates, one core {n / t_one:.4g}/s "
+            f"({ops / t_one:.3g} ops/s), {cores} threads {n / t_all:.4g}/s; a full sweep of "
+            f"{cfg.n_cand} candidates would take {cfg.n_cand / (n / t_all):.0f} s")
+    print(json.dumps({"metric": "oracle candidates simulated/sec", "unit": "candidates/s",
+                      "kind": "oracle", "cpu_model": cpu_model(), "host_cpus_visible": visible,
+                      "threads": cores, "workloads": per, "data": "synthetic"}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -228,7 +273,8 @@ def main():
                          "separately, host-link inclusive (the default for workloads larger "
                          "than one chunk)")
     ap.add_argument("--no-stream", action="store_true", help="skip that stream")
-    ap.add_argument("--path", choices=("simulate", "greedy", "mcts", "search", "cost", "memopt"),
+    ap.add_argument("--path", choices=("simulate", "greedy", "mcts", "search", "cost", "memopt",
+                                        "oracle"),
                     default="simulate",
                     help="simulate given orders (default), build them with the greedy, "
                          "search priorities with MCTS over GPU-batched greedy rollouts, or "
@@ -276,6 +322,8 @@ def main():
         return run_cost(args, cfg)
     if args.path == "memopt":
         return run_memopt(args, cfg)
+    if args.path == "oracle":
+        return run_oracle_timing(args)
     n_cand = args.n_cand or (cfg.chunk or cfg.n_cand)
     t0 = time.time()
     prob = W.make_problem(cfg)
