@@ -39,10 +39,12 @@
 // Verdicts: a group is done when all of its lanes ran their whole order.  A
 // round in which no lane of a group fired an op or read an item leaves its
 // state unchanged for good: if no lane was held by back-pressure the orders
-// deadlock; otherwise the bounded pools may be what stalls it, and the
-// candidate goes to a retry list that a later pass re-simulates.  The
-// permutation check and the memory scan ran before, in the check kernel,
-// whose flags this kernel reads (invalid candidates are skipped) and extends.
+// deadlock; so they do if the lanes that wait for items wait on one another
+// in a cycle (pools of any size would not free them); otherwise the bounded
+// pools may be what stalls it, and the candidate goes to a retry list that a
+// later pass re-simulates.  The permutation check and the memory scan ran
+// before, in the check kernel, whose flags this kernel reads (invalid
+// candidates are skipped) and extends.
 #include "dip_sim.h"
 #include "dev_util.h"
 #include "internal.h"
@@ -414,10 +416,30 @@ __global__ __launch_bounds__(1024) void sim_kernel(SimArgs a) {
 
     // ---- some groups finished their candidate
     const uint64_t g_held = any_in_group<PWL>(m_held);
+    // A stalled group with held lanes still deadlocks whatever the pool size
+    // when the lanes that wait for an item wait on one another in a cycle:
+    // a waiting lane's predecessor op has not run (its item would be in the
+    // pool), so it waits on the predecessor's rank, and when that rank waits
+    // too, on that rank's predecessor rank, and so on; a chain of PW steps
+    // that meets no held or finished lane has closed a cycle of waiting
+    // lanes, none of which can ever move.  Pointer doubling over the group's
+    // lanes follows every chain PW steps.
+    uint64_t g_cyc = 0;
+    if (const uint64_t g_sh = g_stall & g_held) {
+      const bool waiting = lane_in(m_live & ~m_npend & ~m_held);
+      int x = waiting ? gbit + int((ce + rr) & uint32_t(PW - 1)) : -1;
+#pragma unroll
+      for (int s = 0; s < PWL; ++s) {
+        const int y = __shfl(x, x < 0 ? lane : x, kWave);
+        x = x < 0 ? -1 : y;
+      }
+      g_cyc = g_sh & any_in_group<PWL>(ballot(x >= 0));
+    }
     const uint64_t m_ev = any_lane_of_group<PWL>(ev);
     if (lane_in(m_ev)) {
       const bool stalled = (g_stall >> gbit) & 1;
-      const bool retry = (stalled && ((g_held >> gbit) & 1)) || ((g_over >> gbit) & 1);
+      const bool retry = (stalled && ((g_held >> gbit) & 1) && !((g_cyc >> gbit) & 1)) ||
+                         ((g_over >> gbit) & 1);
       uint32_t T = on ? tfree : 0u;
 #pragma unroll
       for (int off = 1; off < PW; off <<= 1) T = max(T, uint32_t(__shfl_xor(int(T), off, kWave)));
