@@ -245,6 +245,26 @@ def run_oracle_timing(args):
         log(f"[bench] oracle on {cfg.name}: {n} candidates, one core {n / t_one:.4g}/s "
             f"({ops / t_one:.3g} ops/s), {cores} threads {n / t_all:.4g}/s; a full sweep of "
             f"{cfg.n_cand} candidates would take {cfg.n_cand / (n / t_all):.0f} s")
+        if args.oracle_full and cid in args.oracle_full:
+            # the whole workload, candidate-parallel, in chunks the generator
+            # writes between timed oracle calls
+            chunk = 65536
+            t_sweep = t_gen = 0.0
+            for c0 in range(0, cfg.n_cand, chunk):
+                m = min(chunk, cfg.n_cand - c0)
+                t0 = time.perf_counter()
+                rows = W.generator_for(prob, cfg).generate(c0, m)
+                t_gen += time.perf_counter() - t0
+                t0 = time.perf_counter()
+                oracle.evaluate(prob, rows, threads=cores)
+                t_sweep += time.perf_counter() - t0
+                if (c0 // chunk) % 8 == 7:
+                    log(f"[bench]   full sweep of {cfg.name}: {c0 + m} candidates, "
+                        f"{t_sweep:.1f} s of oracle time")
+            per[cfg.name]["full_sweep"] = {"candidates": cfg.n_cand, "threads": cores,
+                                           "oracle_s": t_sweep, "generator_s": t_gen}
+            log(f"[bench] full sweep of {cfg.name}: {cfg.n_cand} candidates in {t_sweep:.1f} s "
+                f"on {cores} threads (+ {t_gen:.1f} s generating them)")
     print(json.dumps({"metric": "oracle candidates simulated/sec", "unit": "candidates/s",
                       "kind": "oracle", "cpu_model": cpu_model(), "host_cpus_visible": visible,
                       "threads": cores, "workloads": per, "data": "synthetic"}), flush=True)
@@ -258,6 +278,9 @@ def main():
     ap.add_argument("--config", type=int, default=0,
                     help="workload id 1-5 (default: 5 for the simulation, 2 for the other paths)")
     ap.add_argument("--n-cand", type=int, default=0, help="override candidates per batch")
+    ap.add_argument("--oracle-full", type=lambda x: [int(c) for c in x.split(",")], default=[],
+                    help="with --path oracle: workloads (e.g. 1,2,3,4,5) whose every candidate "
+                         "the oracle also simulates, candidate-parallel, with the wall time")
     ap.add_argument("--variant", type=int, default=0)
     ap.add_argument("--wpb", type=int, default=0)
     ap.add_argument("--slots", type=int, default=0, help="pool slots per rank (pool kernel)")
