@@ -44,7 +44,15 @@ of optimal.  This build's solver, ``select``:
      worth at least incumbent / 1.05, so the incumbent is within 5 % of the
      optimum (status 1).  The search stops early after BB_NODES placements
      examined, or is skipped for ranks of more than BB_MAX_PAIRS pairs; the
-     incumbent is then returned unproven (status 3).
+     incumbent is then returned unproven (status 3);
+  4. when the search stopped early, a certificate from the Lagrangian
+     relaxation of the checkpoint constraints (the dual side of the ILP's
+     LP bound): for multipliers l_k >= 0, every selection within the cap
+     takes at least  sum_i min_j (t_ij + m_ij * sum_{k: i live at k} l_k)
+     - cap * sum_k l_k.  ``lagrangian_proof`` runs LAGR_ITERS subgradient
+     steps in exact integer arithmetic (multipliers in units of 2^-F time
+     per memory unit) and proves the incumbent within 5 % (status 1) once
+     1.05 times that bound reaches it.
 ``exact`` solves the same problem by enumeration and ``exact_bb`` by the same
 search without the 5 % allowance or a node limit, for small cases.
 """
@@ -57,6 +65,9 @@ import numpy as np
 BB_NODES = 512          # placements the branch and bound may examine per rank
 BB_MAX_PAIRS = 512      # larger ranks keep the improved warm start
 GAP_NUM, GAP_DEN = 105, 100   # a cut needs (placed + fastest rest) * 1.05 >= incumbent
+LAGR_ITERS = 200        # subgradient steps of the certificate
+LAGR_F = 20             # fraction bits of the multipliers (at most)
+LAGR_LIMIT = 1 << 60    # magnitude every intermediate value stays below
 
 
 def pareto(layers):
@@ -204,6 +215,72 @@ def branch_and_bound(cands, pf, pb, cap, cur, nodes=BB_NODES, gap=(GAP_NUM, GAP_
     return best, True, seen
 
 
+def _trunc_div(a, b):
+    """a / b rounded toward zero (b > 0), as C integer division does."""
+    q = abs(a) // b
+    return q if a >= 0 else -q
+
+
+def lagrangian_values(cands, live, cap, iters=LAGR_ITERS):
+    """The Lagrangian bound of every subgradient step, as (value, F): the
+    bound is value / 2^F.  Multipliers l_k >= 0, one per checkpoint
+    k (pair k's forward start), in units of 2^-F; pair i's price is the sum of
+    l_k over the checkpoints it is live at; each step every pair takes its
+    cheapest candidate under t * 2^F + m * price (the first on ties), the
+    bound is the sum of those values less cap * sum_k l_k, and every
+    multiplier moves by g_k * step / max_k |g_k| (rounded toward zero, kept
+    within [0, lmax]), g_k being the memory those candidates put on
+    checkpoint k less the cap; step = s0 * 16 / (16 + t) at step t.  F, lmax
+    and s0 depend on the rank's candidates and cap only, and keep every
+    intermediate value below 2^60 (2^61 for the bound).  Nothing when the
+    rank has no pairs or no cap, or its sizes leave no such F."""
+    n = len(cands)
+    if n == 0 or cap < 0:
+        return
+    tmax = max(x[0] for c in cands for x in c)
+    mmax = max(x[1] for c in cands for x in c)
+    F = LAGR_F
+    while F > 0 and n * max(tmax, 1) << F > LAGR_LIMIT:
+        F -= 1
+    lmax = LAGR_LIMIT // (n * n * max(1, mmax, cap))
+    if n * max(tmax, 1) << F > LAGR_LIMIT or lmax == 0:
+        return
+    s0 = 0
+    for c in cands:
+        for j in range(1, len(c)):
+            s0 = max(s0, ((c[j][0] - c[0][0]) << F) // (c[0][1] - c[j][1]))
+    s0 = min(lmax, max(1, s0 // 2))
+    cover = [[k for k in range(n) if i in live[k]] for i in range(n)]
+    lam = [0] * n
+    for t in range(iters):
+        val = -cap * sum(lam)
+        mem = [0] * n
+        for i in range(n):
+            price = sum(lam[k] for k in cover[i])
+            best = None
+            for tt, mm in cands[i]:
+                v = (tt << F) + mm * price
+                if best is None or v < best:
+                    best, mem[i] = v, mm
+            val += best
+        yield val, F
+        g = [sum(mem[i] for i in live[k]) - cap for k in range(n)]
+        gmax = max(abs(x) for x in g)
+        if gmax == 0:
+            return
+        step = s0 * 16 // (16 + t)
+        lam = [min(lmax, max(0, lam[k] + _trunc_div(g[k] * step, gmax))) for k in range(n)]
+
+
+def lagrangian_proof(cands, live, cap, inc, iters=LAGR_ITERS, gap=(GAP_NUM, GAP_DEN)):
+    """Step 4: True when, at some step, the Lagrangian bound times the gap
+    reaches the incumbent's total time ``inc`` (the steps stop there)."""
+    if not cands or cap < 0:
+        return True
+    num, den = gap
+    return any(num * val >= den * (inc << F) for val, F in lagrangian_values(cands, live, cap, iters))
+
+
 def select(cands, live, pf, pb, cap, nodes=BB_NODES):
     """The solver of a rank: (choice, total time, status, peak); status 1
     within the cap and proven within 5 % of optimal, 3 within the cap but
@@ -218,6 +295,9 @@ def select(cands, live, pf, pb, cap, nodes=BB_NODES):
         cur = tighten(cands, live, cap, cur)
         if n <= BB_MAX_PAIRS:
             cur, proven, _ = branch_and_bound(cands, pf, pb, cap, cur, nodes)
+            if not proven:
+                proven = lagrangian_proof(cands, live, cap,
+                                          sum(cands[i][cur[i]][0] for i in range(n)))
         else:
             proven = False
     total = sum(cands[i][cur[i]][0] for i in range(n))

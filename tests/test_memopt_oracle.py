@@ -150,11 +150,61 @@ def _milp_optimum(cands, live, cap):
     return None if res.status != 0 else int(round(res.fun))
 
 
+def test_lagrangian_bound_is_sound_and_certifies():
+    """Step 4's bound never exceeds the optimum exhaustive search finds (so a
+    certificate is never wrong), and with the branch and bound cut short
+    (one placement) every selection the certificate proves is within 5 % of
+    the optimum.  (On these tiny random cases the relaxation is often more
+    than 5 % below the optimum, so it proves only some.)"""
+    rng = np.random.default_rng(11)
+    proved = tried = 0
+    for _ in range(600):
+        cands, pf, pb, cap = _random_case(rng)
+        live = MO.live_sets(pf, pb)
+        best = MO.exact(cands, live, cap)
+        if best is None:
+            continue
+        for val, F in MO.lagrangian_values(cands, live, cap):
+            assert val <= best << F, (val, F, best)
+        cur, _, ok, _ = MO.greedy_select(cands, live, cap)
+        cur = MO.tighten(cands, live, cap, cur)
+        cur, proven, _ = MO.branch_and_bound(cands, pf, pb, cap, cur, 1)
+        if proven:
+            continue
+        total = sum(cands[i][cur[i]][0] for i in range(len(cands)))
+        tried += 1
+        if MO.lagrangian_proof(cands, live, cap, total):
+            proved += 1
+            assert 100 * total <= 105 * best
+    print(f"certificate: {proved} of {tried} selections the cut-short search left unproven")
+    assert tried > 100 and proved > 0
+
+
+def test_lagrangian_step_by_hand():
+    """Two pairs live at both checkpoints, cap 10: pair 0 takes (t, m) = (1, 8)
+    or (3, 2), pair 1 (1, 8) or (2, 4).  Within the cap: (3, 2) + (1, 8),
+    time 4 (the optimum), and (3, 2) + (2, 4), time 5.  With both pairs live
+    at both checkpoints the relaxation depends on the sum p of the two
+    multipliers only:  L(p) = min(1 + 8p, 3 + 2p) + min(1 + 8p, 2 + 4p) - 10p,
+    at most 11/3 (at p = 1/3).  Its first step (no multipliers) is 2; the
+    steps climb towards 11/3 and never pass it; 1.05 * 11/3 < 4, so the
+    certificate proves an incumbent of 3 but never the optimum 4."""
+    cands = [[(1, 8), (3, 2)], [(1, 8), (2, 4)]]
+    live = [[0, 1], [0, 1]]
+    vals = [v / (1 << F) for v, F in MO.lagrangian_values(cands, live, 10)]
+    assert vals[0] == 2
+    assert 3.5 <= max(vals) <= 11 / 3
+    assert MO.exact(cands, live, 10) == 4
+    assert MO.lagrangian_proof(cands, live, 10, 3)
+    assert not MO.lagrangian_proof(cands, live, 10, 4)
+
+
 @pytest.mark.parametrize("frac,S", [(0.6, 6), (0.3, 6), (0.15, 4)])
 def test_selection_on_workload_ranks_against_milp(frac, S):
     """The 8-rank VLM workload's ranks (32 and 68 stage pairs) under caps
     that bind: the solver never beats and stays within 5 % of the optimum
-    an independent MILP solver finds."""
+    an independent MILP solver finds, and proves it under the two looser
+    caps."""
     pytest.importorskip("scipy")
     prob = W.make_problem(2)
     tab = strategy_table(prob)
@@ -171,7 +221,11 @@ def test_selection_on_workload_ranks_against_milp(frac, S):
             if opt is None:
                 assert status == 0
                 continue
-            assert status in (1, 3) and peak <= cap
+            # proven within 5 % (by the search or the certificate), except
+            # under the tightest cap with 4 candidates, where the relaxation
+            # falls 5.5-7.5 % below the optimum on some ranks: there the
+            # selection is within 5 % but stays unproven (status 3)
+            assert (status == 1 if frac > 0.2 else status in (1, 3)) and peak <= cap
             assert total >= opt and 100 * total <= 105 * opt, (r, total, opt)
             n += 1
     assert n > 0
