@@ -20,7 +20,11 @@
 //      is cut with its slower siblings, and a complete placement below the
 //      incumbent replaces it.  A finished search proves the incumbent within
 //      5 % of the optimum (status 1); after bb_nodes placements examined, or
-//      on ranks of more than 512 pairs (no search), status 3.
+//      on ranks of more than 512 pairs (no search), status 3;
+//   4. when the search stopped early, a certificate from the Lagrangian
+//      relaxation of the checkpoint constraints (the dual side of the ILP's
+//      LP bound), by exact integer subgradient steps: status 1 once 1.05
+//      times the bound reaches the incumbent.
 // Pair i is live at pair k's forward start when its forward comes no later
 // and its backward no earlier in the rank's order.
 //
@@ -50,6 +54,12 @@
 namespace dipsim {
 
 namespace {
+
+// the Lagrangian certificate: subgradient steps, fraction bits of the
+// multipliers (at most), and the magnitude every value stays below
+constexpr int kMemoptLagrIters = 200;
+constexpr int kMemoptLagrF = 20;
+constexpr int64_t kMemoptLagrLimit = int64_t(1) << 60;
 
 __device__ __forceinline__ void lds_sync_wave() {
   lds_wait();
@@ -506,6 +516,123 @@ __global__ __launch_bounds__(256) void memopt_wave_kernel(MemoptArgs a) {
       for (int q = 0; q < PPL; ++q)
         if (q == q1 && lane == l1) dplaced[q] = f_t;
       ++d;
+    }
+    if (!proven) {
+      // ---- step 4: the Lagrangian certificate.  Multipliers l_k >= 0 (units
+      // of 2^-F time per memory unit), one per checkpoint k (pair k's
+      // forward start), lane k & 63 holding checkpoint k's in slot k >> 6.
+      // Each step: a pair's price is the sum of the multipliers of the
+      // checkpoints it is live at; it takes its cheapest candidate under
+      // t * 2^F + m * price (the first on ties); the bound (times 2^F) is
+      // the sum of those values less cap * sum_k l_k, and proves the
+      // incumbent once 1.05 times it reaches the incumbent; otherwise each
+      // multiplier moves by g_k * step / max |g| (rounded toward zero, kept
+      // in [0, lmax]), g_k being the memory of the taken candidates live at
+      // checkpoint k less the cap, step = s0 * 16 / (16 + t).  F, lmax and
+      // s0 come from the rank's candidates and cap and keep every value
+      // below 2^61.  Integer arithmetic, the same steps on any device.
+      auto has = [&](int32_t i, int32_t j) {
+        return j < kMemoptMaxCands && (j == 0 || tkey[i * kMemoptMaxCands + j - 1] != kMemoptNoMove);
+      };
+      auto wave_max64 = [](int64_t v) {
+#pragma unroll
+        for (int s = 1; s < 64; s <<= 1)
+          v = max(v, (int64_t(__shfl_xor(int(v >> 32), s)) << 32) |
+                         uint32_t(__shfl_xor(int(uint32_t(v)), s)));
+        return v;
+      };
+      int64_t tmx = 0, mmx = 0, s0 = 0;
+#pragma unroll
+      for (int q = 0; q < PPL; ++q)
+        if (own(q)) {
+          const int32_t i = lane + 64 * q;
+          for (int32_t j = 0; has(i, j); ++j) {
+            tmx = max(tmx, ct[i * kMemoptMaxCands + j]);
+            mmx = max(mmx, int64_t(cmem[i * kMemoptMaxCands + j]));
+          }
+        }
+      tmx = wave_max64(tmx);
+      mmx = wave_max64(mmx);
+      const __int128 span = __int128(np) * max(tmx, int64_t(1));
+      int F = kMemoptLagrF;
+      while (F > 0 && (span << F) > __int128(kMemoptLagrLimit)) --F;
+      const int64_t lmax =
+          kMemoptLagrLimit / (int64_t(np) * np * max(max(int64_t(1), mmx), int64_t(cap)));
+      if ((span << F) <= __int128(kMemoptLagrLimit) && lmax > 0) {
+#pragma unroll
+        for (int q = 0; q < PPL; ++q)
+          if (own(q)) {
+            const int32_t i = lane + 64 * q;
+            const int64_t t0 = ct[i * kMemoptMaxCands];
+            const int64_t m0 = cmem[i * kMemoptMaxCands];
+            for (int32_t j = 1; has(i, j); ++j)
+              s0 = max(s0, ((ct[i * kMemoptMaxCands + j] - t0) << F) /
+                               (m0 - cmem[i * kMemoptMaxCands + j]));
+          }
+        s0 = min(lmax, max(int64_t(1), wave_max64(s0) / 2));
+        int64_t lam[PPL];
+        int32_t took[PPL];   // memory of each own pair's candidate this step
+#pragma unroll
+        for (int q = 0; q < PPL; ++q) {
+          lam[q] = 0;
+          took[q] = 0;
+        }
+        for (int t = 0; t < kMemoptLagrIters; ++t) {
+          int64_t part = 0, lsum = 0;
+#pragma unroll
+          for (int q = 0; q < PPL; ++q) {
+            if (64 * q >= np) continue;   // (no pair of the rank in this slot)
+            int64_t price = 0;
+            for (int32_t k = 0; k < np; ++k) {   // checkpoints, uniform
+              const int qk = k >> 6, lk = k & 63;
+              const int64_t lv =
+                  int64_t(uint32_t(__builtin_amdgcn_readlane(int(uint32_t(pick(lam, qk))), lk))) |
+                  (int64_t(__builtin_amdgcn_readlane(int(pick(lam, qk) >> 32), lk)) << 32);
+              const uint32_t pk = pfa[k];
+              if (pf[q] <= pk && pk <= pb[q]) price += lv;
+            }
+            if (own(q)) {
+              const int32_t i = lane + 64 * q;
+              int64_t bv = 0;
+              for (int32_t j = 0; has(i, j); ++j) {
+                const int64_t v = (ct[i * kMemoptMaxCands + j] << F) +
+                                  int64_t(cmem[i * kMemoptMaxCands + j]) * price;
+                if (j == 0 || v < bv) {
+                  bv = v;
+                  took[q] = cmem[i * kMemoptMaxCands + j];
+                }
+              }
+              part += bv;
+              lsum += lam[q];
+            }
+          }
+          const int64_t val = wave_sum64(part) - int64_t(cap) * wave_sum64(lsum);
+          if (__int128(105) * val >= __int128(100) * (__int128(inc) << F)) {
+            proven = true;
+            break;
+          }
+          int64_t g[PPL], gabs = 0;
+#pragma unroll
+          for (int q = 0; q < PPL; ++q) {
+            g[q] = 0;
+            if (64 * q >= np) continue;
+            int64_t s = 0;
+            for (int32_t j = 0; j < np; ++j) {   // pairs, uniform
+              const int qj = j >> 6, lj = j & 63;
+              const int32_t mj = __builtin_amdgcn_readlane(pick(took, qj), lj);
+              if (pfa[j] <= pf[q] && pf[q] <= pba[j]) s += mj;
+            }
+            g[q] = s - int64_t(cap);
+            if (own(q)) gabs = max(gabs, g[q] < 0 ? -g[q] : g[q]);
+          }
+          gabs = wave_max64(gabs);
+          if (gabs == 0) break;
+          const int64_t step = s0 * 16 / (16 + t);
+#pragma unroll
+          for (int q = 0; q < PPL; ++q)
+            if (own(q)) lam[q] = min(lmax, max(int64_t(0), lam[q] + g[q] * step / gabs));
+        }
+      }
     }
     status = proven ? 1 : 3;
     // the final choice and its checkpoint loads
