@@ -375,7 +375,13 @@ int dip_sim_configure_memopt(dip_sim *h, const int32_t *slot_layers, const int64
  *      fastest first, a node cut when 1.05 x (its placed time + the unplaced
  *      pairs' fastest times) reaches the incumbent; it ends proven (the
  *      incumbent is within 5 % of the optimum) or after bb_nodes placements
- *      examined; ranks of more than 512 pairs skip it.
+ *      examined; ranks of more than 512 pairs skip it;
+ *   4. when the search stopped early, a certificate: 200 steps of integer
+ *      subgradient ascent on the Lagrangian relaxation of the forward-start
+ *      constraints (for multipliers l_k >= 0 every selection within the cap
+ *      takes at least sum_i min_j (t_ij + m_ij * sum_{k: i live at k} l_k)
+ *      - cap * sum_k l_k); the incumbent is proven once 1.05 x that bound
+ *      reaches it.
  * Outputs, device [n_cand][P]: out_time (int64, the rank's total pair time),
  * out_peak (memory at the most loaded forward start), out_status (1 within
  * the cap and proven within 5 %, 3 within the cap but not proven, 0 the cap
