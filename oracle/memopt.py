@@ -68,6 +68,7 @@ GAP_NUM, GAP_DEN = 105, 100   # a cut needs (placed + fastest rest) * 1.05 >= in
 LAGR_ITERS = 200        # subgradient steps of the certificate
 LAGR_F = 20             # fraction bits of the multipliers (at most)
 LAGR_LIMIT = 1 << 60    # magnitude every intermediate value stays below
+LAGR_HALVE = 24         # steps between halvings of the step size
 
 
 def pareto(layers):
@@ -215,41 +216,42 @@ def branch_and_bound(cands, pf, pb, cap, cur, nodes=BB_NODES, gap=(GAP_NUM, GAP_
     return best, True, seen
 
 
-def _trunc_div(a, b):
-    """a / b rounded toward zero (b > 0), as C integer division does."""
-    q = abs(a) // b
-    return q if a >= 0 else -q
+def _bits(x):
+    """Bits of a non-negative integer (0 for 0)."""
+    return int(x).bit_length()
 
 
 def lagrangian_values(cands, live, cap, iters=LAGR_ITERS):
     """The Lagrangian bound of every subgradient step, as (value, F): the
-    bound is value / 2^F.  Multipliers l_k >= 0, one per checkpoint
-    k (pair k's forward start), in units of 2^-F; pair i's price is the sum of
-    l_k over the checkpoints it is live at; each step every pair takes its
+    bound is value / 2^F.  Multipliers l_k >= 0, one per checkpoint k (pair
+    k's forward start), in units of 2^-F; pair i's price is the sum of l_k
+    over the checkpoints it is live at; each step every pair takes its
     cheapest candidate under t * 2^F + m * price (the first on ties), the
     bound is the sum of those values less cap * sum_k l_k, and every
-    multiplier moves by g_k * step / max_k |g_k| (rounded toward zero, kept
-    within [0, lmax]), g_k being the memory those candidates put on
-    checkpoint k less the cap; step = s0 * 16 / (16 + t) at step t.  F, lmax
-    and s0 depend on the rank's candidates and cap only, and keep every
-    intermediate value below 2^60 (2^61 for the bound).  Nothing when the
-    rank has no pairs or no cap, or its sizes leave no such F."""
+    multiplier moves by g_k * step / 2^b, b the bits of max_k |g_k| (the
+    magnitude shifted down, the sign kept; kept within [0, lmax]), g_k being
+    the memory those candidates put on checkpoint k less the cap;
+    step = s0 / 2^(t / LAGR_HALVE) at step t (rounded down).  The constants depend on the rank's
+    candidates and cap only: F = min(LAGR_F, 60 - bits(n * tmax));
+    lmax = 2^60 / 2^bits(n^2 * max(1, mmax, cap)); s0 = half the largest
+    (dt << F) / 2^(bits(dm) - 1) over the candidates' moves from the fastest,
+    at least 1 and at most lmax -- every intermediate value stays below 2^60
+    (2^61 for the bound).  Nothing when the rank has no pairs or no cap, or
+    its sizes leave no such F."""
     n = len(cands)
     if n == 0 or cap < 0:
         return
     tmax = max(x[0] for c in cands for x in c)
     mmax = max(x[1] for c in cands for x in c)
-    F = LAGR_F
-    while F > 0 and n * max(tmax, 1) << F > LAGR_LIMIT:
-        F -= 1
-    lmax = LAGR_LIMIT // (n * n * max(1, mmax, cap))
-    if n * max(tmax, 1) << F > LAGR_LIMIT or lmax == 0:
+    F = min(LAGR_F, 60 - _bits(n * max(tmax, 1)))
+    lmax = LAGR_LIMIT >> _bits(n * n * max(1, mmax, cap))
+    if F < 0 or lmax == 0:
         return
     s0 = 0
     for c in cands:
         for j in range(1, len(c)):
-            s0 = max(s0, ((c[j][0] - c[0][0]) << F) // (c[0][1] - c[j][1]))
-    s0 = min(lmax, max(1, s0 // 2))
+            s0 = max(s0, ((c[j][0] - c[0][0]) << F) >> (_bits(c[0][1] - c[j][1]) - 1))
+    s0 = min(lmax, max(1, s0 >> 1))
     cover = [[k for k in range(n) if i in live[k]] for i in range(n)]
     lam = [0] * n
     for t in range(iters):
@@ -265,11 +267,12 @@ def lagrangian_values(cands, live, cap, iters=LAGR_ITERS):
             val += best
         yield val, F
         g = [sum(mem[i] for i in live[k]) - cap for k in range(n)]
-        gmax = max(abs(x) for x in g)
-        if gmax == 0:
+        sh = _bits(max(abs(x) for x in g))
+        if sh == 0:
             return
-        step = s0 * 16 // (16 + t)
-        lam = [min(lmax, max(0, lam[k] + _trunc_div(g[k] * step, gmax))) for k in range(n)]
+        step = s0 >> (t // LAGR_HALVE)
+        lam = [min(lmax, max(0, lam[k] + (1 if g[k] >= 0 else -1) * ((abs(g[k]) * step) >> sh)))
+               for k in range(n)]
 
 
 def lagrangian_proof(cands, live, cap, inc, iters=LAGR_ITERS, gap=(GAP_NUM, GAP_DEN)):

@@ -682,13 +682,15 @@ int dip_sim_memopt(dip_sim *h, const int16_t *orders, int64_t n_cand, int64_t *o
   a.max_pairs = std::max(h->mo_max_pairs, 1);
   (void)hipGetLastError();
   if (a.max_pairs <= 512) {
-    // a wave per (schedule, rank), pairs in registers
-    constexpr int kWaves = 4;
+    // a wave per (schedule, rank), pairs in registers; four waves per block
+    // where their LDS fits, else two, else one
+    int waves = 4;
+    while (waves > 1 && memopt_wave_lds(a.max_pairs, waves) > 65536) waves /= 2;
     int ppl = 1;
     while (64 * ppl < a.max_pairs) ppl *= 2;
-    if ((n_cand + kWaves - 1) / kWaves > INT32_MAX || h->P > 65535) return DIP_E_INVAL;
-    if (memopt_wave_lds(a.max_pairs, kWaves) > 65536) return DIP_E_UNSUPPORTED;
-    DIP_HIP(launch_memopt_wave(ppl, kWaves, static_cast<hipStream_t>(stream), a));
+    if ((n_cand + waves - 1) / waves > INT32_MAX || h->P > 65535) return DIP_E_INVAL;
+    if (memopt_wave_lds(a.max_pairs, waves) > 65536) return DIP_E_UNSUPPORTED;
+    DIP_HIP(launch_memopt_wave(ppl, waves, static_cast<hipStream_t>(stream), a));
     return DIP_OK;
   }
   a.bytes_per_thread = int32_t(int64_t(a.max_pairs) * 9);

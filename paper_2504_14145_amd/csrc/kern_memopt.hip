@@ -59,7 +59,11 @@ namespace {
 // multipliers (at most), and the magnitude every value stays below
 constexpr int kMemoptLagrIters = 200;
 constexpr int kMemoptLagrF = 20;
-constexpr int64_t kMemoptLagrLimit = int64_t(1) << 60;
+constexpr int kMemoptLagrLimitBits = 60;
+constexpr int kMemoptLagrHalve = 24;   // steps between halvings of the step size
+
+// bits of a non-negative value (0 for 0)
+__device__ __forceinline__ int bits64(int64_t x) { return x ? 64 - __clzll(x) : 0; }
 
 __device__ __forceinline__ void lds_sync_wave() {
   lds_wait();
@@ -251,6 +255,10 @@ __global__ __launch_bounds__(256) void memopt_wave_kernel(MemoptArgs a) {
   uint16_t *pba = pfa + mp;
   uint16_t *orda = pba + mp;
   uint8_t *sela = sh + 68 * mp + 6 * mp * nw + int64_t(wv) * mp;
+  // the certificate's arrays over the checkpoints in forward order: prefix
+  // sums of the multipliers, memory differences, multipliers
+  int64_t *lps = reinterpret_cast<int64_t *>(sh + ((68 + 7 * nw) * mp + 7) / 8 * 8) +
+                 int64_t(wv) * 3 * (mp + 1);
   {
     const uint32_t *gk = a.move_key + int64_t(pbase) * kMemoptMaxCands;
     const int32_t *gd = a.move_dm + int64_t(pbase) * kMemoptMaxCands;
@@ -517,123 +525,6 @@ __global__ __launch_bounds__(256) void memopt_wave_kernel(MemoptArgs a) {
         if (q == q1 && lane == l1) dplaced[q] = f_t;
       ++d;
     }
-    if (!proven) {
-      // ---- step 4: the Lagrangian certificate.  Multipliers l_k >= 0 (units
-      // of 2^-F time per memory unit), one per checkpoint k (pair k's
-      // forward start), lane k & 63 holding checkpoint k's in slot k >> 6.
-      // Each step: a pair's price is the sum of the multipliers of the
-      // checkpoints it is live at; it takes its cheapest candidate under
-      // t * 2^F + m * price (the first on ties); the bound (times 2^F) is
-      // the sum of those values less cap * sum_k l_k, and proves the
-      // incumbent once 1.05 times it reaches the incumbent; otherwise each
-      // multiplier moves by g_k * step / max |g| (rounded toward zero, kept
-      // in [0, lmax]), g_k being the memory of the taken candidates live at
-      // checkpoint k less the cap, step = s0 * 16 / (16 + t).  F, lmax and
-      // s0 come from the rank's candidates and cap and keep every value
-      // below 2^61.  Integer arithmetic, the same steps on any device.
-      auto has = [&](int32_t i, int32_t j) {
-        return j < kMemoptMaxCands && (j == 0 || tkey[i * kMemoptMaxCands + j - 1] != kMemoptNoMove);
-      };
-      auto wave_max64 = [](int64_t v) {
-#pragma unroll
-        for (int s = 1; s < 64; s <<= 1)
-          v = max(v, (int64_t(__shfl_xor(int(v >> 32), s)) << 32) |
-                         uint32_t(__shfl_xor(int(uint32_t(v)), s)));
-        return v;
-      };
-      int64_t tmx = 0, mmx = 0, s0 = 0;
-#pragma unroll
-      for (int q = 0; q < PPL; ++q)
-        if (own(q)) {
-          const int32_t i = lane + 64 * q;
-          for (int32_t j = 0; has(i, j); ++j) {
-            tmx = max(tmx, ct[i * kMemoptMaxCands + j]);
-            mmx = max(mmx, int64_t(cmem[i * kMemoptMaxCands + j]));
-          }
-        }
-      tmx = wave_max64(tmx);
-      mmx = wave_max64(mmx);
-      const __int128 span = __int128(np) * max(tmx, int64_t(1));
-      int F = kMemoptLagrF;
-      while (F > 0 && (span << F) > __int128(kMemoptLagrLimit)) --F;
-      const int64_t lmax =
-          kMemoptLagrLimit / (int64_t(np) * np * max(max(int64_t(1), mmx), int64_t(cap)));
-      if ((span << F) <= __int128(kMemoptLagrLimit) && lmax > 0) {
-#pragma unroll
-        for (int q = 0; q < PPL; ++q)
-          if (own(q)) {
-            const int32_t i = lane + 64 * q;
-            const int64_t t0 = ct[i * kMemoptMaxCands];
-            const int64_t m0 = cmem[i * kMemoptMaxCands];
-            for (int32_t j = 1; has(i, j); ++j)
-              s0 = max(s0, ((ct[i * kMemoptMaxCands + j] - t0) << F) /
-                               (m0 - cmem[i * kMemoptMaxCands + j]));
-          }
-        s0 = min(lmax, max(int64_t(1), wave_max64(s0) / 2));
-        int64_t lam[PPL];
-        int32_t took[PPL];   // memory of each own pair's candidate this step
-#pragma unroll
-        for (int q = 0; q < PPL; ++q) {
-          lam[q] = 0;
-          took[q] = 0;
-        }
-        for (int t = 0; t < kMemoptLagrIters; ++t) {
-          int64_t part = 0, lsum = 0;
-#pragma unroll
-          for (int q = 0; q < PPL; ++q) {
-            if (64 * q >= np) continue;   // (no pair of the rank in this slot)
-            int64_t price = 0;
-            for (int32_t k = 0; k < np; ++k) {   // checkpoints, uniform
-              const int qk = k >> 6, lk = k & 63;
-              const int64_t lv =
-                  int64_t(uint32_t(__builtin_amdgcn_readlane(int(uint32_t(pick(lam, qk))), lk))) |
-                  (int64_t(__builtin_amdgcn_readlane(int(pick(lam, qk) >> 32), lk)) << 32);
-              const uint32_t pk = pfa[k];
-              if (pf[q] <= pk && pk <= pb[q]) price += lv;
-            }
-            if (own(q)) {
-              const int32_t i = lane + 64 * q;
-              int64_t bv = 0;
-              for (int32_t j = 0; has(i, j); ++j) {
-                const int64_t v = (ct[i * kMemoptMaxCands + j] << F) +
-                                  int64_t(cmem[i * kMemoptMaxCands + j]) * price;
-                if (j == 0 || v < bv) {
-                  bv = v;
-                  took[q] = cmem[i * kMemoptMaxCands + j];
-                }
-              }
-              part += bv;
-              lsum += lam[q];
-            }
-          }
-          const int64_t val = wave_sum64(part) - int64_t(cap) * wave_sum64(lsum);
-          if (__int128(105) * val >= __int128(100) * (__int128(inc) << F)) {
-            proven = true;
-            break;
-          }
-          int64_t g[PPL], gabs = 0;
-#pragma unroll
-          for (int q = 0; q < PPL; ++q) {
-            g[q] = 0;
-            if (64 * q >= np) continue;
-            int64_t s = 0;
-            for (int32_t j = 0; j < np; ++j) {   // pairs, uniform
-              const int qj = j >> 6, lj = j & 63;
-              const int32_t mj = __builtin_amdgcn_readlane(pick(took, qj), lj);
-              if (pfa[j] <= pf[q] && pf[q] <= pba[j]) s += mj;
-            }
-            g[q] = s - int64_t(cap);
-            if (own(q)) gabs = max(gabs, g[q] < 0 ? -g[q] : g[q]);
-          }
-          gabs = wave_max64(gabs);
-          if (gabs == 0) break;
-          const int64_t step = s0 * 16 / (16 + t);
-#pragma unroll
-          for (int q = 0; q < PPL; ++q)
-            if (own(q)) lam[q] = min(lmax, max(int64_t(0), lam[q] + g[q] * step / gabs));
-        }
-      }
-    }
     status = proven ? 1 : 3;
     // the final choice and its checkpoint loads
 #pragma unroll
@@ -649,6 +540,168 @@ __global__ __launch_bounds__(256) void memopt_wave_kernel(MemoptArgs a) {
         for (int32_t j = 0; j < np; ++j)
           if (pfa[j] <= pf[q] && pf[q] <= pba[j]) s += cmem[j * kMemoptMaxCands + sela[j]];
       load[q] = s;
+    }
+    if (!proven) {
+      // ---- step 4 (after the final choice, whose loads are set): the
+      // Lagrangian certificate.  Multipliers l_k >= 0 (units
+      // of 2^-F time per memory unit), one per checkpoint k (pair k's
+      // forward start).  Each step: a pair's price is the sum of the
+      // multipliers of the checkpoints it is live at; it takes its cheapest
+      // candidate under t * 2^F + m * price (the first on ties); the bound
+      // (times 2^F) is the sum of those values less cap * sum_k l_k, and
+      // proves the incumbent once 1.05 times it reaches the incumbent;
+      // otherwise each multiplier moves by g_k * step / 2^b, b the bits of
+      // max |g| (the magnitude shifted down, the sign kept; kept in [0,
+      // lmax]), g_k being the memory of the taken candidates live at
+      // checkpoint k less the cap, step = s0 / 2^(t / 24).  F = min(20, 60 -
+      // bits(np * tmax)), lmax = 2^60 / 2^bits(np^2 * max(1, mmax, cap)) and
+      // s0 = half the largest (dt << F) / 2^(bits(dm) - 1) over the moves
+      // from each pair's fastest candidate (at least 1, at most lmax) keep
+      // every value below 2^61, with no division.  A pair is live exactly at the
+      // checkpoints whose forward order lies in [its own, the number of
+      // forwards not after its backward), so both sums are differences of
+      // prefix sums over the checkpoints in forward order, kept in the
+      // wave's LDS.  Integer arithmetic: the same values as any other order
+      // of summation.
+      auto has = [&](int32_t i, int32_t j) {
+        return j < kMemoptMaxCands && (j == 0 || tkey[i * kMemoptMaxCands + j - 1] != kMemoptNoMove);
+      };
+      auto shfl64 = [](int64_t v, int src) {
+        return (int64_t(__shfl(int(v >> 32), src)) << 32) | uint32_t(__shfl(int(uint32_t(v)), src));
+      };
+      auto wave_max64 = [](int64_t v) {
+#pragma unroll
+        for (int s = 1; s < 64; s <<= 1)
+          v = max(v, (int64_t(__shfl_xor(int(v >> 32), s)) << 32) |
+                         uint32_t(__shfl_xor(int(uint32_t(v)), s)));
+        return v;
+      };
+      // inclusive prefix sum over the 64 lanes
+      auto wave_scan64 = [&](int64_t v) {
+#pragma unroll
+        for (int s = 1; s < 64; s <<= 1) {
+          const int64_t y = shfl64(v, lane >= s ? lane - s : lane);
+          if (lane >= s) v += y;
+        }
+        return v;
+      };
+      int64_t tmx = 0, mmx = 0, s0 = 0;
+#pragma unroll
+      for (int q = 0; q < PPL; ++q)
+        if (own(q)) {
+          const int32_t i = lane + 64 * q;
+          for (int32_t j = 0; has(i, j); ++j) {
+            tmx = max(tmx, ct[i * kMemoptMaxCands + j]);
+            mmx = max(mmx, int64_t(cmem[i * kMemoptMaxCands + j]));
+          }
+        }
+      tmx = wave_max64(tmx);
+      mmx = wave_max64(mmx);
+      const int F = min(kMemoptLagrF, kMemoptLagrLimitBits - bits64(int64_t(np) * max(tmx, int64_t(1))));
+      const int lb = bits64(int64_t(np) * np * max(max(int64_t(1), mmx), int64_t(cap)));
+      const int64_t lmax = lb <= kMemoptLagrLimitBits ? int64_t(1) << (kMemoptLagrLimitBits - lb) : 0;
+      if (F >= 0 && lmax > 0) {
+#pragma unroll
+        for (int q = 0; q < PPL; ++q)
+          if (own(q)) {
+            const int32_t i = lane + 64 * q;
+            const int64_t t0 = ct[i * kMemoptMaxCands];
+            const int64_t m0 = cmem[i * kMemoptMaxCands];
+            for (int32_t j = 1; has(i, j); ++j)
+              s0 = max(s0, ((ct[i * kMemoptMaxCands + j] - t0) << F) >>
+                               (bits64(m0 - cmem[i * kMemoptMaxCands + j]) - 1));
+          }
+        s0 = min(lmax, max(int64_t(1), wave_max64(s0) >> 1));
+        // own pairs: the forward-order range [lo, hi) of the checkpoints
+        // they are live at
+        int32_t lo[PPL], hi[PPL];
+#pragma unroll
+        for (int q = 0; q < PPL; ++q) {
+          int32_t x = 0, y = 0;
+          if (own(q))
+            for (int32_t j = 0; j < np; ++j) {
+              x += pfa[j] < pf[q] ? 1 : 0;
+              y += pfa[j] <= pb[q] ? 1 : 0;
+            }
+          lo[q] = x;
+          hi[q] = y;
+        }
+        int64_t *ps = lps;                   // [np + 1] prefix sums of the multipliers
+        int64_t *dif = lps + (mp + 1);       // [np + 1] memory differences, then g
+        int64_t *lam = lps + 2 * (mp + 1);   // [np] multipliers, by forward order
+        for (int32_t d = lane; d < np; d += 64) lam[d] = 0;
+        lds_sync_wave();
+        for (int t = 0; t < kMemoptLagrIters; ++t) {
+          // prefix sums of the multipliers; the difference array cleared
+          int64_t carry = 0;
+#pragma unroll
+          for (int q = 0; q < PPL; ++q) {
+            if (64 * q >= np) continue;
+            const int32_t d = lane + 64 * q;
+            const int64_t v = wave_scan64(d < np ? lam[d] : 0) + carry;
+            if (d < np) ps[d + 1] = v;
+            if (d <= np) dif[d] = 0;
+            carry = shfl64(v, 63);
+          }
+          if (lane == 0) ps[0] = 0;
+          if (np % 64 == 0 && lane == 0) dif[np] = 0;
+          lds_sync_wave();
+          int64_t part = 0;
+#pragma unroll
+          for (int q = 0; q < PPL; ++q)
+            if (own(q)) {
+              const int32_t i = lane + 64 * q;
+              const int64_t price = hi[q] > lo[q] ? ps[hi[q]] - ps[lo[q]] : 0;
+              int64_t bv = 0;
+              int32_t bm = 0;
+              for (int32_t j = 0; has(i, j); ++j) {
+                const int64_t v = (ct[i * kMemoptMaxCands + j] << F) +
+                                  int64_t(cmem[i * kMemoptMaxCands + j]) * price;
+                if (j == 0 || v < bv) {
+                  bv = v;
+                  bm = cmem[i * kMemoptMaxCands + j];
+                }
+              }
+              part += bv;
+              if (hi[q] > lo[q]) {
+                atomicAdd(reinterpret_cast<unsigned long long *>(dif + lo[q]),
+                          static_cast<unsigned long long>(int64_t(bm)));
+                atomicAdd(reinterpret_cast<unsigned long long *>(dif + hi[q]),
+                          static_cast<unsigned long long>(-int64_t(bm)));
+              }
+            }
+          const int64_t val = wave_sum64(part) - int64_t(cap) * carry;
+          if (__int128(105) * val >= __int128(100) * (__int128(inc) << F)) {
+            status = 1;
+            break;
+          }
+          lds_sync_wave();
+          // g at every depth: the running sum of the differences less the
+          // cap, written over the differences
+          int64_t gabs = 0, run = 0;
+#pragma unroll
+          for (int q = 0; q < PPL; ++q) {
+            if (64 * q >= np) continue;
+            const int32_t d = lane + 64 * q;
+            const int64_t v = wave_scan64(d < np ? dif[d] : 0) + run;
+            run = shfl64(v, 63);
+            const int64_t g = v - int64_t(cap);
+            if (d < np) {
+              dif[d] = g;
+              gabs = max(gabs, g < 0 ? -g : g);
+            }
+          }
+          const int sh = bits64(wave_max64(gabs));
+          if (sh == 0) break;
+          const int64_t step = s0 >> (t / kMemoptLagrHalve);
+          for (int32_t d = lane; d < np; d += 64) {
+            const int64_t g = dif[d];
+            const int64_t mv = ((g < 0 ? -g : g) * step) >> sh;
+            lam[d] = min(lmax, max(int64_t(0), lam[d] + (g < 0 ? -mv : mv)));
+          }
+          lds_sync_wave();   // (the next step rewrites the arrays)
+        }
+      }
     }
   }
   int64_t total = 0;
@@ -673,7 +726,10 @@ __global__ __launch_bounds__(256) void memopt_wave_kernel(MemoptArgs a) {
 }  // namespace
 
 size_t memopt_wave_lds(int32_t max_pairs, int waves_per_block) {
-  return size_t(max_pairs) * (68 + 7 * size_t(waves_per_block));
+  // the rank's tables and the waves' positions and choices, then (8-byte
+  // aligned) each wave's two certificate arrays of max_pairs + 1 words
+  const size_t head = size_t(max_pairs) * (68 + 7 * size_t(waves_per_block));
+  return (head + 7) / 8 * 8 + size_t(waves_per_block) * 24 * (size_t(max_pairs) + 1);
 }
 
 hipError_t launch_memopt_wave(int ppl, int waves_per_block, hipStream_t s, const MemoptArgs &a) {
