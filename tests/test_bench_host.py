@@ -66,3 +66,22 @@ def test_cpu_baseline_legs_and_fields():
     assert cpu["ops_per_s"] == cpu["value"] * prob.n_total or abs(
         cpu["ops_per_s"] / (cpu["value"] * prob.n_total) - 1) < 1e-9
     assert isinstance(cpu["cpu_model"], str) and cpu["cpu_model"]
+
+
+def test_oracle_timing_path():
+    """--path oracle (no GPU work): one line with every workload's one-core
+    and all-core oracle rates, the full sweep of the requested workloads, and
+    the host description."""
+    p = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--path", "oracle",
+                        "--n-cand", "32", "--oracle-full", "1"],
+                       capture_output=True, text=True, timeout=600)
+    assert p.returncode == 0, p.stderr[-2000:]
+    rec = json.loads(p.stdout.strip().splitlines()[-1])
+    assert rec["kind"] == "oracle" and rec["threads"] >= 1 and rec["cpu_model"]
+    assert set(rec["workloads"]) == {"tiny", "vlm_s8", "vlm_interleaved_16x2", "diffusion_s32",
+                                     "large_16x4"}
+    for name, w in rec["workloads"].items():
+        assert w["candidates"] == 32
+        assert w["one_core"]["candidates_per_s"] > 0 and w["all_cores"]["candidates_per_s"] > 0
+        assert ("full_sweep" in w) == (name == "tiny")
+    assert rec["workloads"]["tiny"]["full_sweep"]["candidates"] == 1024
