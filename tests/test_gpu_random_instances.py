@@ -105,3 +105,32 @@ def test_random_instances_match_oracle(seed):
         np.testing.assert_array_equal(got[1], want.bubble)
         np.testing.assert_array_equal(got[2], want.peak)
     sim.close()
+
+
+@pytest.mark.parametrize("seed", range(20))
+def test_random_instances_greedy_matches_oracle(seed):
+    """The dual-queue interleaving on the same random instances (caps that
+    bind the forward queue), random rollout priorities: the emitted orders
+    and their scores equal the oracle's."""
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    rng = np.random.default_rng(1000 + seed)
+    prob = random_instance(rng)
+    base = topo_orders(prob, rng, 16)
+    peak = O.evaluate(prob, base).peak
+    prob.mem_cap[:] = int(rng.integers(peak.min(), peak.max() + 1))
+    g, G, cls = W.priority_groups(prob)
+    prio = W.rollout_priorities(cls, 96, seed=seed)
+    want_o, want = O.greedy(prob, g, G, prio, stride=prob.stride, threads=16)
+    print(f"seed {seed}: P {prob.n_ranks}, {prob.n_total} ops, {G} groups", flush=True)
+    sim = dip.Sim(prob)
+    assert sim.configure_greedy(G, g) == dip.OK
+    ords, (ms, bub, pk, fl) = sim.greedy(torch.from_numpy(np.ascontiguousarray(prio, np.int32)).to(DEV))
+    torch.cuda.synchronize()
+    N = prob.n_total
+    np.testing.assert_array_equal(ords.cpu().numpy()[:, :N], want_o[:, :N])
+    np.testing.assert_array_equal(fl.cpu().numpy(), want.flags)
+    np.testing.assert_array_equal(ms.cpu().numpy(), want.makespan)
+    np.testing.assert_array_equal(bub.cpu().numpy(), want.bubble)
+    np.testing.assert_array_equal(pk.cpu().numpy(), want.peak)
+    sim.close()
