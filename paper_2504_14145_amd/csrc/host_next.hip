@@ -26,7 +26,10 @@ bool greedy_layout(const dip_sim *h, int K, int pwl, dip_sim::GrLaunch *L, bool 
   L->off_gpos = int32_t(head);
   L->off_ord = int32_t(head + align16(2 * G));
   L->off_grk = int32_t(head + 2 * align16(2 * G));
-  L->cand_bytes = int32_t(head + 3 * align16(2 * G));
+  // (wide E sets, 32 words, sit in LDS after the tables: each lane
+  // of the candidate two sets of gr_nw words)
+  const int64_t ebits = h->gr_nw >= 32 ? lanes * 16 * int64_t(h->gr_nw) : 0;
+  L->cand_bytes = int32_t(head + 3 * align16(2 * G) + ebits);
   L->lds = h->gr_meta_bytes + int64_t(kWave >> pwl) * L->cand_bytes;
   if (L->lds > h->lds_block_max) return false;
   int bpc = 0;

@@ -90,6 +90,63 @@ __device__ __forceinline__ void set_kind(Bits<NW> &f, Bits<NW> &b, uint32_t kind
   }
 }
 
+// The two E sets of one rank (forward, backward).  Up to 16 words a set they
+// live in registers; 32-word sets (every set or clear would touch every word
+// through selects) live in the lane's own LDS words, with a register mask of
+// the words that are not zero, so that a set, a clear and the first
+// position each take one or two LDS accesses.
+template <int NW, bool IN_LDS = (NW >= 32)>
+struct EPair {
+  Bits<NW> f, b;
+  __device__ __forceinline__ void init(uint64_t *) {
+    f.zero();
+    b.zero();
+  }
+  __device__ __forceinline__ void set(uint32_t kind, uint32_t p) { set_kind(f, b, kind, p); }
+  // clears position p of a kind; the kind's new first position
+  __device__ __forceinline__ uint32_t clear_first(uint32_t kind, uint32_t p) {
+    if (kind) {
+      b.clear(p);
+      return first_in(b);
+    }
+    f.clear(p);
+    return first_in(f);
+  }
+  __device__ __forceinline__ uint32_t first(uint32_t kind) const { return first_in(kind ? b : f); }
+};
+
+template <int NW>
+struct EPair<NW, true> {
+  static_assert(NW <= 32, "one summary bit per word");
+  uint64_t *w;        // [2][NW] this lane's words: forward, then backward
+  uint32_t nz[2];     // words that are not zero, per kind
+  __device__ __forceinline__ void init(uint64_t *words) {
+    w = words;
+#pragma unroll
+    for (int i = 0; i < 2 * NW; ++i) w[i] = 0;
+    nz[0] = nz[1] = 0;
+  }
+  __device__ __forceinline__ void set(uint32_t kind, uint32_t p) {
+    const uint32_t k = p >> 6;
+    __hip_atomic_fetch_or(w + kind * NW + k, uint64_t(1) << (p & 63u), __ATOMIC_RELAXED,
+                          __HIP_MEMORY_SCOPE_WAVEFRONT);
+    nz[kind] |= 1u << k;
+  }
+  __device__ __forceinline__ uint32_t first(uint32_t kind) const {
+    if (nz[kind] == 0) return kNoPos;
+    const uint32_t k = uint32_t(__builtin_ctz(nz[kind]));
+    return k * 64u + uint32_t(__builtin_ctzll(w[kind * NW + k]));
+  }
+  __device__ __forceinline__ uint32_t clear_first(uint32_t kind, uint32_t p) {
+    const uint32_t k = p >> 6;
+    const uint64_t bit = uint64_t(1) << (p & 63u);
+    const uint64_t old = __hip_atomic_fetch_and(w + kind * NW + k, ~bit, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_WAVEFRONT);
+    if ((old & ~bit) == 0) nz[kind] &= ~(1u << k);
+    return first(kind);
+  }
+};
+
 template <int CTRL>
 __device__ __forceinline__ uint32_t dpp(uint32_t v) {
   return uint32_t(__builtin_amdgcn_update_dpp(0, int(v), CTRL, 0xf, 0xf, false));
@@ -174,6 +231,8 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
   uint16_t *gpos = reinterpret_cast<uint16_t *>(cb + a.off_gpos);
   uint16_t *ord = reinterpret_cast<uint16_t *>(cb + a.off_ord);
   uint16_t *grk = reinterpret_cast<uint16_t *>(cb + a.off_grk);
+  // wide E sets: each lane's 2 NW words at the end of its candidate's region
+  uint64_t *ebits = reinterpret_cast<uint64_t *>(cb + a.cand_bytes) - int64_t(PW - r) * 2 * NW;
 
   const int64_t n_slots = int64_t(gridDim.x) * a.wpb * GW;
   for (int64_t slot = (int64_t(blockIdx.x) * a.wpb + wave) * GW + grp;; slot += n_slots) {
@@ -238,19 +297,18 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
     // E: queued stages with t_start < t_last (and the stages without
     // predecessors while t_last is still 0, their t_start); a stage with
     // t_start >= t_last waits in its kind's inbox
-    Bits<NW> eF, eB;
-    eF.zero();
-    eB.zero();
+    EPair<NW> e;
+    e.init(ebits);
     if (real) {
       const int32_t *src_list = a.src + P + 1;
       for (int s = a.src[r]; s < a.src[r + 1]; ++s) {
         const int g = src_list[s];
-        set_kind(eF, eB, g < GF ? 0u : 1u, gpos[g]);
+        e.set(g < GF ? 0u : 1u, gpos[g]);
       }
     }
     // first (best) position in each E, kept up to date: an entry moving in
-    // can only lower it; the commit that takes it scans again
-    uint32_t eF1 = first_in(eF), eB1 = first_in(eB);
+    // can only lower it; the commit that takes it looks again
+    uint32_t eF1 = e.first(0u), eB1 = e.first(1u);
     wave_sync();
 
     uint32_t t_last = 0, last_kind = 0, n_emit = 0;
@@ -273,7 +331,7 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
         frF = ringF[hF & mask];
         if (uint32_t(frF >> 17) >= t_last) break;
         const uint32_t p = uint32_t(frF >> 1) & 0xffffu;
-        set_kind(eF, eB, 0u, p);
+        e.set(0u, p);
         eF1 = min(eF1, p);
         frF = ~uint64_t(0);
       }
@@ -281,7 +339,7 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
         frB = ringB[hB & mask];
         if (uint32_t(frB >> 17) >= t_last) break;
         const uint32_t p = uint32_t(frB >> 1) & 0xffffu;
-        set_kind(eF, eB, 1u, p);
+        e.set(1u, p);
         eB1 = min(eB1, p);
         frB = ~uint64_t(0);
       }
@@ -359,13 +417,10 @@ __global__ __launch_bounds__(256) void greedy_kernel(GreedyArgs a) {
         if (forced) fetch(c);
         const uint32_t end = c.tau + uint32_t(q0.x);
         if (c.slot == 0) {
-          if (c.kind) {
-            eB.clear(c.pos);
-            eB1 = first_in(eB);
-          } else {
-            eF.clear(c.pos);
-            eF1 = first_in(eF);
-          }
+          if (c.kind)
+            eB1 = e.clear_first(1u, c.pos);
+          else
+            eF1 = e.clear_first(0u, c.pos);
         } else {
           // the kind's inbox front: one step on
           const uint32_t hw = hcw[2 * r + c.kind];
