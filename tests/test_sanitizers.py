@@ -5,7 +5,7 @@ simulator and greedy oracles (oracle/*.c), the candidate generator
 (paper_2504_14145_amd/csrc/host_check.cpp).  A child Python process loads the
 sanitized builds (the sanitizer runtime preloaded) and runs the oracles on
 every workload, the generator, and the validation on valid and malformed
-instances and costs; any sanitizer report fails the test."""
+instances and costs (hand-made cases and 400 seeded random corruptions); any sanitizer report fails the test."""
 import os
 import shutil
 import subprocess
@@ -74,6 +74,55 @@ CHILD = textwrap.dedent(r'''
     bad_costs = dip.HostCosts(cost, prob.edge_comm.copy(), prob.slot_act.copy())
     codes.append(lib.dip_sim_check_costs(ctypes.byref(t.c), ctypes.byref(bad_costs.c)))
     assert all(x < 0 for x in codes), codes
+
+    # seeded random corruptions of values (array sizes stay as the
+    # instance's, which is the caller's part of the contract): every call
+    # returns 0 or an error code, with no sanitizer report
+    rng = np.random.default_rng(7)
+    N, E = prob.n_total, prob.n_edges
+    for trial in range(400):
+        kw = {}
+        which = trial % 8
+        if which == 0 and N > 2:
+            pp = prob.pred_ptr.copy()
+            pp[rng.integers(1, N)] = rng.integers(-5, E + 50)
+            kw["pred_ptr"] = pp
+        elif which == 1:
+            po = prob.pred_op.copy()
+            po[rng.integers(E)] = rng.integers(-(2**31), 2**31 - 1)
+            kw["pred_op"] = po
+        elif which == 2:
+            ok = prob.op_kind.copy()
+            ok[rng.integers(N)] = rng.integers(0, 256)
+            kw["op_kind"] = ok
+        elif which == 3:
+            sl = prob.op_slot.copy()
+            sl[rng.integers(N)] = rng.integers(-(2**31), 2**31 - 1)
+            kw["op_slot"] = sl
+        elif which == 4:
+            kw["n_slots"] = int(rng.integers(-3, prob.n_slots + 1))
+        elif which == 5:
+            kw["cand_stride"] = int(rng.integers(-8, 2 * prob.stride))
+        elif which == 6:
+            no = prob.n_ops.copy()
+            r = rng.integers(prob.n_ranks)
+            d = int(rng.integers(-3, 4))
+            no[r] += d
+            no[(r + 1) % prob.n_ranks] -= d          # the same total
+            kw["n_ops"] = no
+        else:
+            mc = prob.mem_cap.copy()
+            mc[rng.integers(prob.n_ranks)] = rng.integers(-(2**31), 2**31 - 1)
+            kw["mem_cap"] = mc
+        tt = topo(**kw)
+        rc = lib.dip_sim_check_topology(ctypes.byref(tt.c))
+        assert rc <= 0, (trial, rc)
+        if rc == 0:
+            arrays = [prob.op_cost.copy(), prob.edge_comm.copy(), prob.slot_act.copy()]
+            a = arrays[trial % 3]
+            a[rng.integers(len(a))] = rng.integers(-(2**31), 2**31 - 1)
+            cc = dip.HostCosts(*arrays)
+            assert lib.dip_sim_check_costs(ctypes.byref(tt.c), ctypes.byref(cc.c)) <= 0
 
     # the memory selection's search on small ranks
     tab = strategy_table(prob)
